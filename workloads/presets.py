@@ -1,0 +1,173 @@
+"""Model presets and seeded initial conditions for the paper's benchmark shapes.
+
+The paper evaluates on Vogels-Abbott ("Vogels"), Brunel and Brunel with STDP
+("Brunel+") (Sec. IV) and studies the synapse pass on them (Sec. IV-C). The
+model definitions themselves are deferred to another paper, so the values
+here are readings: sizes, probabilities, delays and weights follow the
+benchmark descriptions this implementation is measured on, and every value
+the paper leaves open is a documented choice. All presets use dt = 0.1 ms and
+fp32 state, matching the single-precision Euler simulators the paper compares
+(Sec. IV-A).
+
+Presets hold *physical* parameters only. Each side of the comparison (the HIP
+library and the CPU oracle) derives its own constants from them.
+"""
+
+from dataclasses import dataclass, replace, field
+import math
+
+import numpy as np
+
+from .rng import rng_u32, STREAM_INIT_V
+
+LIF_DELTA = 0
+LIF_CUBA = 1
+BERNOULLI_SOURCE = 2
+
+PLASTIC_NONE = 0
+PLASTIC_EXC_EXC = 1
+PLASTIC_ALL = 2
+
+GRAPH_BERNOULLI = 0
+GRAPH_FIXED_FANOUT = 1
+
+SEED = 20210708
+
+
+@dataclass(frozen=True)
+class Preset:
+    name: str
+    n: int
+    n_exc: int
+    model: int
+    graph_kind: int
+    p_or_fanout: float
+    w_exc: float
+    w_inh: float
+    delay: int = 1
+    dt: float = 0.1            # ms
+    tau_m: float = 20.0        # ms
+    v_th: float = -50.0        # mV
+    v_reset: float = -60.0     # mV
+    v_inf: float = -49.0       # mV, resting/asymptotic potential (includes bias)
+    tau_ref: float = 5.0       # ms
+    tau_e: float = 5.0         # ms (CUBA only)
+    tau_i: float = 10.0        # ms (CUBA only)
+    v0_lo: float = -60.0       # initial V ~ U[v0_lo, v0_hi)
+    v0_hi: float = -50.0
+    poisson_mu: float = 0.0    # external Poisson events per neuron per step
+    j_ext: float = 0.0         # mV per external event
+    p_fire: float = 0.0        # Bernoulli source firing probability per step
+    plastic: int = PLASTIC_NONE
+    tau_plus: float = 20.0     # ms
+    tau_minus: float = 20.0    # ms
+    lam: float = 0.1
+    alpha: float = 0.11
+    mu: float = 0.4
+    w0: float = 0.0            # power-law reference weight
+    slice_width: int = 1024
+    spike_chunks: int = 1
+    steps: int = 1000
+    seed: int = SEED
+
+    def scaled(self, **kw):
+        return replace(self, **kw)
+
+
+def _w0_fixed_point(w_init, alpha, mu):
+    # Reference weight at which one potentiation and one depression of equal
+    # trace value cancel for w = w_init (w0^(1-mu) w^mu = alpha w).
+    return w_init * alpha ** (1.0 / (1.0 - mu))
+
+
+PRESETS = {
+    # 1,000 LIF neurons (800/200), p=0.02, 1-step delay, +0.27/-4.5 mV,
+    # bias through V_inf = -49 mV (isolated period 529 steps).
+    "tiny": Preset(
+        name="tiny", n=1000, n_exc=800, model=LIF_DELTA,
+        graph_kind=GRAPH_BERNOULLI, p_or_fanout=0.02, w_exc=0.27, w_inh=-4.5,
+        delay=1, slice_width=256, steps=10_000),
+    # 4,000-neuron CUBA balanced network (3,200/800), p=0.02, tau_e=5/tau_i=10.
+    "vogels": Preset(
+        name="vogels", n=4000, n_exc=3200, model=LIF_CUBA,
+        graph_kind=GRAPH_BERNOULLI, p_or_fanout=0.02, w_exc=1.62, w_inh=-9.0,
+        delay=1, slice_width=1024, steps=100_000),
+    # 62,500 LIF neurons (50,000/12,500), p=0.1, D=15 steps, J=0.1/-0.5 mV,
+    # Poisson drive at twice the threshold rate (mu = 2 events per step).
+    "brunel": Preset(
+        name="brunel", n=62_500, n_exc=50_000, model=LIF_DELTA,
+        graph_kind=GRAPH_BERNOULLI, p_or_fanout=0.1, w_exc=0.1, w_inh=-0.5,
+        delay=15, v_th=20.0, v_reset=10.0, v_inf=0.0, tau_ref=2.0,
+        v0_lo=0.0, v0_hi=20.0, poisson_mu=2.0, j_ext=0.1,
+        slice_width=4096, steps=10_000),
+    # Brunel scaled to 25,000 neurons (20,000/5,000) with power-law STDP on
+    # exc->exc synapses.
+    "brunel_plus": Preset(
+        name="brunel_plus", n=25_000, n_exc=20_000, model=LIF_DELTA,
+        graph_kind=GRAPH_BERNOULLI, p_or_fanout=0.1, w_exc=0.1, w_inh=-0.5,
+        delay=15, v_th=20.0, v_reset=10.0, v_inf=0.0, tau_ref=2.0,
+        v0_lo=0.0, v0_hi=20.0, poisson_mu=2.0, j_ext=0.1,
+        plastic=PLASTIC_EXC_EXC, w0=_w0_fixed_point(0.1, 0.11, 0.4),
+        slice_width=4096, steps=100_000),
+    # 250,000 Bernoulli(0.005) sources, fan-out 1,000 uniform-random targets
+    # (with replacement), STDP on all synapses, D=1.
+    "stress": Preset(
+        name="stress", n=250_000, n_exc=250_000, model=BERNOULLI_SOURCE,
+        graph_kind=GRAPH_FIXED_FANOUT, p_or_fanout=1000, w_exc=0.1, w_inh=0.1,
+        delay=1, p_fire=0.005, plastic=PLASTIC_ALL,
+        w0=_w0_fixed_point(0.1, 0.11, 0.4),
+        slice_width=4096, spike_chunks=1, steps=1000),
+}
+
+
+def preset(name, **overrides):
+    p = PRESETS[name]
+    return replace(p, **overrides) if overrides else p
+
+
+def initial_state(p: Preset):
+    """Seeded initial neuron state (fp32 V, zero everything else).
+
+    V_i = v0_lo + (v0_hi - v0_lo) * u_i with u_i = (u32 >> 8) * 2^-24 drawn
+    from stream 2 at (0, i); evaluated in double, rounded once to fp32.
+    """
+    n = p.n
+    u = (rng_u32(p.seed, STREAM_INIT_V, 0, np.arange(n, dtype=np.uint64))
+         >> np.uint32(8)).astype(np.float64) * (2.0 ** -24)
+    if p.model == BERNOULLI_SOURCE:
+        v = np.zeros(n, dtype=np.float32)
+    else:
+        v = (p.v0_lo + (p.v0_hi - p.v0_lo) * u).astype(np.float32)
+    return {
+        "v": v,
+        "refractory": np.zeros(n, dtype=np.int32),
+        "i_exc": np.zeros(n, dtype=np.float32),
+        "i_inh": np.zeros(n, dtype=np.float32),
+        "hist": np.zeros(n, dtype=np.uint64),
+    }
+
+
+MAX_POISSON = 32
+
+
+def poisson_cdf_table(mu):
+    """uint32 inverse-CDF table for Poisson(mu) external events.
+
+    T[k] = min(2^32 - 1, floor(F(k) * 2^32)) with F the Poisson CDF, for
+    k = 0 .. L-1, where L is the first length at which T saturates (at most
+    32). A draw u (uint32) yields k = #{k' : T[k'] <= u}. Returns an empty
+    table for mu == 0.
+    """
+    if mu <= 0.0:
+        return np.zeros(0, dtype=np.uint32)
+    table = []
+    pmf = math.exp(-mu)
+    cdf = 0.0
+    for k in range(MAX_POISSON):
+        cdf += pmf
+        v = min((1 << 32) - 1, int(math.floor(cdf * 4294967296.0)))
+        table.append(v)
+        if v == (1 << 32) - 1:
+            break
+        pmf *= mu / (k + 1)
+    return np.asarray(table, dtype=np.uint32)
