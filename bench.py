@@ -1,0 +1,266 @@
+"""Benchmark of the synapse pass on one MI355X.
+
+Workload (default): the stress network - 250,000 Bernoulli(0.005) sources,
+fan-out 1,000 uniform-random targets with replacement (250M synapses, int32
+targets + fp32 weights), power-law STDP on every synapse, delay 1 step.
+
+One step = neuron update + spike-list compaction, lazy + event-driven STDP,
+and slice (LDS) delivery. Timed region: K steps issued by one snn_step call,
+bracketed by device synchronisation. A second pass of K steps records HIP
+events around each kernel group on the library's stream to get per-kernel
+durations; the roofline figure of the dominant kernel (STDP) is its
+algorithmic bytes per launch over that duration.
+
+Prints one JSON line. `--gpus N` with N > 1 exits: this build runs on one GPU.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "synaptic events/sec (delivery+STDP) on 1 MI355X; % of HBM roofline"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=100)
+    ap.add_argument("--config", default="stress")
+    ap.add_argument("--mode", choices=["lds", "global"], default="lds")
+    ap.add_argument("--slice-width", type=int, default=None)
+    ap.add_argument("--chunks", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-instrumented", action="store_true",
+                    help="skip the per-kernel event pass (used under rocprofv3)")
+    return ap.parse_args()
+
+
+def kernel_source_digest():
+    h = hashlib.sha256()
+    for f in ("snn_kernels.hip", "snn_api.hip", "snn_internal.h"):
+        with open(os.path.join(ROOT, "paper_2107_04092_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel, workload_key):
+    """HBM bytes per launch from committed rocprofv3 counter summaries, if they
+    were taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        d = json.load(open(path))
+        ent = d[workload_key][kernel]
+        if ent.get("source_digest") != kernel_source_digest():
+            return None
+        return float(ent["bytes_per_launch"])
+    except (KeyError, ValueError, TypeError):
+        return None
+
+
+def stdp_bytes(st, n, launches):
+    """Algorithmic bytes of the STDP kernel: per synapse-update 8 B (target +
+    weight read), per changed weight 4 B (store), per row 40 B (list entry,
+    row pointer, plastic end, source history, t_last and pre trace read and
+    written), per launch 12 B per neuron (target history + post trace)."""
+    return (8 * st["stdp_synapse_updates"] + 4 * st["stdp_weights_written"] +
+            40 * st["stdp_rows"] + 12 * n * launches)
+
+
+def delivery_bytes(st, n, n_slices, chunks, nacc, launches, mode):
+    """Algorithmic bytes of delivery: 8 B per event (target + weight). LDS
+    mode adds per (transmitted spike, slice) 20 B (list entry, row pointer,
+    pivot pair) and per launch the slice write-back: nacc * n * 4 B of fp32
+    inputs with one chunk, else C * nacc * n * 8 B of fixed-point partial
+    sums. The global mode adds per spike 20 B, per event the 8 B atomic
+    update, and per launch the clear of nacc * n * 8 B."""
+    ev, tx = st["delivered_events"], st["spikes"]
+    if mode == "lds":
+        wb = 4 * nacc * n if chunks == 1 else 8 * chunks * nacc * n
+        return 8 * ev + 20 * tx * n_slices + wb * launches
+    return 16 * ev + 20 * tx + 8 * nacc * n * launches
+
+
+def cpu_baseline(p, seconds):
+    """The oracle as it stands on this host's cores: naive dense STDP over all
+    synapses every step plus row-wise delivery, a prefix of the same workload."""
+    from oracle import oracle
+    import workloads as wl
+    o = oracle.Oracle(p, wl.poisson_cdf_table(p.poisson_mu))
+    t0 = time.time()
+    o.build_random()
+    o.set_neurons(**wl.initial_state(p))
+    build_s = time.time() - t0
+    rp = None
+    events = 0
+    steps = 0
+    t0 = time.time()
+    while True:
+        o.step()
+        steps += 1
+        _, lst = o.spikes()
+        if rp is None:
+            rp = o.graph()[0]
+        events += int((rp[lst + 1] - rp[lst]).sum())
+        el = time.time() - t0
+        if el >= seconds or steps >= 200:
+            break
+    return {"value": events / el, "unit": "synaptic events/s", "cores": oracle.threads(),
+            "kind": "oracle",
+            "sample": "%s workload at full size (n=%d, %d synapses), first %d steps after a "
+                      "%.1f s build; dense per-synapse STDP every step + row-wise delivery; "
+                      "%.3f s/step" % (p.name, p.n, o.n_edges, steps, build_s, el / steps)}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build runs the synapse pass on one GPU only; "
+              "--gpus %d is not supported (sharding is described in DESIGN.md)" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import workloads as wl
+    from paper_2107_04092_amd import snn
+
+    p = wl.preset(args.config)
+    width = args.slice_width or p.slice_width
+    chunks = args.chunks or p.spike_chunks
+    mode = snn.SNN_DELIVER_LDS_SLICE if args.mode == "lds" else snn.SNN_DELIVER_GLOBAL_ATOMIC
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    stream = torch.cuda.current_stream(dev)
+
+    cfg = snn.config_from_preset(p, wl.poisson_cdf_table(p.poisson_mu),
+                                 slice_width=width,
+                                 spike_chunks=chunks)
+    t0 = time.time()
+    net = snn.Network(cfg, stream=stream, device=dev)
+    e = net.build_random(p.graph_kind, p.p_or_fanout, p.w_exc, p.w_inh)
+    st0 = wl.initial_state(p)
+    net.set_state(0, v=torch.from_numpy(st0["v"]))
+    torch.cuda.synchronize()
+    setup_s = time.time() - t0
+
+    # warm-up (untimed)
+    net.step(args.warmup, mode)
+    torch.cuda.synchronize()
+    net.reset_stats()
+
+    # timed region: exactly K steps
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    t_wall = time.perf_counter()
+    net.step(args.steps, mode)
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    ms_total = start.elapsed_time(end)
+    st = net.stats()
+    ms_per_step = ms_total / args.steps
+    events_per_s = st["delivered_events"] / (ms_total * 1e-3)
+    stdp_per_s = st["stdp_synapse_updates"] / (ms_total * 1e-3)
+
+    n_slices = (p.n + width - 1) // width
+    nacc = 2 if p.model == snn.SNN_LIF_CUBA else 1
+    b_stdp = stdp_bytes(st, p.n, args.steps) / args.steps
+    b_dlv = delivery_bytes(st, p.n, n_slices, chunks, nacc, args.steps, args.mode) / args.steps
+
+    kernels = None
+    roofline = None
+    combined = None
+    if not args.no_instrumented:
+        # instrumented pass: events around each kernel group on the library stream
+        net.reset_stats()
+        K = args.steps
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+        torch.cuda.synchronize()
+        for q in range(K):
+            ev[q][0].record(stream)
+            net.update_neurons()
+            ev[q][1].record(stream)
+            net.update_plasticity()
+            ev[q][2].record(stream)
+            net.deliver_spikes(mode)
+            ev[q][3].record(stream)
+            net.advance()
+        torch.cuda.synchronize()
+        t_neu = sum(ev[q][0].elapsed_time(ev[q][1]) for q in range(K)) / K
+        t_stdp = sum(ev[q][1].elapsed_time(ev[q][2]) for q in range(K)) / K
+        t_dlv = sum(ev[q][2].elapsed_time(ev[q][3]) for q in range(K)) / K
+        st2 = net.stats()
+        b_stdp2 = stdp_bytes(st2, p.n, K) / K
+        b_dlv2 = delivery_bytes(st2, p.n, n_slices, chunks, nacc, K, args.mode) / K
+        kernels = {
+            "neuron_update+compact_us": round(t_neu * 1e3, 3),
+            "stdp_us": round(t_stdp * 1e3, 3),
+            "delivery_us": round(t_dlv * 1e3, 3),
+            "stdp_bytes_per_launch": int(b_stdp2),
+            "delivery_bytes_per_launch": int(b_dlv2),
+            "delivery_GBs": round(b_dlv2 / (t_dlv * 1e-3) / 1e9, 1),
+        }
+        ach = b_stdp2 / (t_stdp * 1e-3) / 1e9
+        traffic = load_traffic("k_stdp", p.name)
+        roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
+                    "traffic": traffic, "kernel": "k_stdp"}
+        comb = (b_stdp2 + b_dlv2) / ((t_stdp + t_dlv) * 1e-3) / 1e9
+        combined = {"achieved_GBs": round(comb, 1), "frac": round(comb / HBM_PEAK_GBS, 4),
+                    "us_per_step": round((t_stdp + t_dlv) * 1e3, 3)}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(p, args.cpu_seconds)
+
+    out = {
+        "metric": METRIC,
+        "value": events_per_s,
+        "unit": "synaptic events/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "%s: n=%d, %s %s, %d synapses, delay %d, plasticity %s, "
+                        "delivery %s, slice width %d, chunks %d"
+                        % (p.name, p.n,
+                           "fan-out" if p.graph_kind == 1 else "p",
+                           p.p_or_fanout, e, p.delay,
+                           ["none", "exc-exc", "all"][p.plastic], args.mode, width, chunks),
+            "n": p.n, "synapses": e, "slice_width": width, "spike_chunks": chunks,
+            "delivery": args.mode, "seed": p.seed,
+        },
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "stdp_synapse_updates_per_s": stdp_per_s,
+        "delivery_plus_stdp": combined,
+        "kernels": kernels,
+        "stats": {k: int(v) for k, v in st.items()},
+        "bytes_per_step": {"stdp": int(b_stdp), "delivery": int(b_dlv)},
+        "setup_s": round(setup_s, 3),
+        "host_wall_s": round(wall, 4),
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,282 @@
+/*
+ * snn.h - C ABI of libsnn.so, the MI355X (gfx950) synapse pass of a
+ * clock-based spiking-neural-network simulator.
+ *
+ * Method: Bautembach, Oikonomidis & Argyros, "Even Faster SNN Simulation with
+ * Lazy+Event-driven Plasticity and Shared Atomics". One simulation step is
+ * the three-part loop of Sec. I:
+ *   (1) update neurons and note which fire,
+ *   (2) update synapses, recovering pre- and post-synaptic spikes,
+ *   (3) deliver spikes to the neurons' neighbours.
+ * Every part runs in hand-written HIP kernels:
+ *   - (1) emits a 64-bit firing mask word per 64 neurons (one wave64 ballot),
+ *     an ascending spike list, and shifts each neuron's 64-bit firing
+ *     history (least significant bit = most recent step, Fig. 2);
+ *   - a ring of the last D spike lists implements the network-wide delay;
+ *   - (2) is lazy + event-driven STDP (Sec. III-A, Fig. 2(b,c)): only rows
+ *     that transmit this step are brought up to date, replaying the missed
+ *     steps by walking the set bits of each target's history word; rows idle
+ *     for 64 steps are forced so no post-synaptic spike leaves the window;
+ *   - (3) is slice delivery (Sec. III-B, Fig. 3(b)): the target domain is cut
+ *     into slices of W neurons and one workgroup accumulates one slice in
+ *     LDS with LDS atomics; a global-atomic row-wise variant (Fig. 3(a)) is
+ *     kept for comparison. Both accumulate exact 64-bit fixed-point sums
+ *     (32 fractional bits), so delivered inputs do not depend on the order of
+ *     the atomic updates; each input is rounded once to fp32;
+ *   - the graph is a CSR grouped by source with sorted rows plus per-row
+ *     slice pivots (Fig. 1), built on the device.
+ *
+ * Conventions for every call:
+ *   - Ownership. The caller owns all device memory and the HIP stream. The
+ *     library never allocates device memory: it works inside the workspace
+ *     and graph buffers the caller binds, which stay borrowed until
+ *     snn_destroy. The library owns only the host-side snn_ctx.
+ *   - Pointers. "device" pointers must be addresses in device memory of the
+ *     device that was current at snn_create; "host" pointers are ordinary
+ *     process memory. Nothing is retained beyond the call unless stated.
+ *   - Streams. All device work is enqueued on the stream given to
+ *     snn_create, in call order. Calls that return values computed on the
+ *     device synchronise that stream and say so.
+ *   - Errors. Every call returns an snn_status and never throws or aborts.
+ *     Arguments are checked before any launch; on failure nothing is
+ *     enqueued and snn_last_error(ctx) describes the problem. Asynchronous
+ *     kernel faults surface as SNN_EDEVICE at the next synchronising call.
+ *   - Threads. A context is bound to one stream and is not thread-safe.
+ */
+#ifndef SNN_H
+#define SNN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum snn_status {
+    SNN_OK = 0,
+    SNN_EINVAL = 1,  /* bad argument or configuration */
+    SNN_ENOMEM = 2,  /* a caller-provided buffer is too small */
+    SNN_EDEVICE = 3, /* a HIP call or kernel failed */
+    SNN_ESTATE = 4   /* call out of order (e.g. step before the graph exists) */
+} snn_status;
+
+/* Neuron dynamics of part (1). All use dt-step Euler integration in fp32. */
+enum snn_neuron_model {
+    SNN_LIF_DELTA = 0,       /* V += (V_inf - V) dt/tau_m + A + J_ext k_Poisson */
+    SNN_LIF_CUBA = 1,        /* exponential exc/inh currents, tau_e / tau_i */
+    SNN_BERNOULLI_SOURCE = 2 /* fires with probability p_fire per step */
+};
+
+/* Which synapses are plastic (part (2)). */
+enum snn_plasticity {
+    SNN_PLASTIC_NONE = 0,
+    SNN_PLASTIC_EXC_EXC = 1, /* source and target both below n_exc */
+    SNN_PLASTIC_ALL = 2
+};
+
+/* Delivery algorithm for part (3). */
+enum snn_delivery {
+    SNN_DELIVER_LDS_SLICE = 0,    /* Fig. 3(b): per-slice LDS accumulation */
+    SNN_DELIVER_GLOBAL_ATOMIC = 1 /* Fig. 3(a): row-wise global atomics */
+};
+
+/* Random graph families for snn_graph_count_random. */
+enum snn_graph_kind {
+    SNN_GRAPH_BERNOULLI = 0,   /* each ordered pair j != k with probability p */
+    SNN_GRAPH_FIXED_FANOUT = 1 /* F uniform targets per source, with replacement */
+};
+
+#define SNN_MAX_POISSON 32
+#define SNN_MAX_DELAY 64
+
+/* Network configuration: physical parameters only; the library derives its
+ * own fp32 constants (dt/tau_m, exp(-dt/tau), ...) from them. */
+typedef struct snn_config {
+    int32_t n;            /* neurons, 1 .. 2^24-1 */
+    int32_t n_exc;        /* excitatory neurons are 0 .. n_exc-1 (0 <= n_exc <= n) */
+    int32_t delay_steps;  /* D, 1 .. 64: a spike emitted at step t reaches the
+                             neuron update of step t+D */
+    int32_t slice_width;  /* W for LDS delivery: multiple of 64, and the
+                             W * 8 B fixed-point accumulator (x2 for CUBA)
+                             must fit in the device's LDS (160 KiB) */
+    int32_t spike_chunks; /* C in 1..64: workgroups that share one slice, each
+                             taking 1/C of the spike list (partial sums are
+                             added by the next neuron update) */
+    int32_t neuron_model; /* enum snn_neuron_model */
+    int32_t plastic;      /* enum snn_plasticity */
+    int32_t poisson_len;  /* entries used in poisson_cdf (0 = no external drive) */
+    double dt_ms, tau_m_ms, v_th, v_reset, v_inf, tau_ref_ms, tau_e_ms, tau_i_ms;
+    double j_ext;         /* mV per external Poisson event */
+    double p_fire;        /* Bernoulli source firing probability per step */
+    double tau_plus_ms, tau_minus_ms;     /* STDP trace time constants */
+    double lambda, alpha, mu, w0;         /* power-law STDP: dw+ = lambda w0^(1-mu)
+                                             w^mu x_pre, dw- = -lambda alpha w x_post */
+    uint64_t seed;        /* counter-based random streams (graph, drive, sources) */
+    /* External drive: k ~ Poisson drawn by inversion, k = #{q : cdf[q] <= u}
+     * for the 32-bit draw u of stream 3 at (step, neuron). */
+    uint32_t poisson_cdf[SNN_MAX_POISSON];
+} snn_config;
+
+typedef struct snn_ctx snn_ctx;
+
+/* Device views of the simulation state, all inside the bound workspace. Each
+ * array has n entries unless stated. Returned by snn_get_state (pointers
+ * into the workspace, valid until snn_destroy); passed to snn_set_state
+ * (caller device buffers to copy from; NULL fields are left unchanged). */
+typedef struct snn_state_view {
+    int64_t t;              /* index of the next step to run */
+    float *v;               /* membrane potential (mV) */
+    int32_t *refractory;    /* remaining refractory steps */
+    float *i_exc, *i_inh;   /* CUBA currents (mV) */
+    uint64_t *hist;         /* firing history, bit i = spike at step t-1-i */
+    float *trace_post;      /* post-synaptic trace as of the last neuron update */
+    int32_t *t_last;        /* step each plastic row was last brought up to date */
+    float *trace_pre;       /* pre-synaptic row trace at t_last */
+    float *input_exc;       /* fp32 input A(t) the next neuron update uses */
+    float *input_inh;       /* (CUBA inhibitory input; NULL otherwise) */
+    uint64_t *spike_mask;   /* last neuron update: ceil(n/64) words, bits >= n zero */
+    int32_t *spike_list;    /* last neuron update: ascending indices */
+    int32_t *spike_count;   /* device int32 */
+    int32_t *tx_list;       /* spikes transmitted by the last delivery step */
+    int32_t *tx_count;      /* device int32 */
+    int32_t *stdp_rows;     /* rows brought up to date by the last STDP step */
+    int32_t *stdp_row_count;/* device int32 */
+    int32_t *ring_lists;    /* delay ring: D x n spike lists, slot = step mod D */
+    int32_t *ring_counts;   /* delay ring: D counts */
+} snn_state_view;
+
+/* Device views of the graph (inside the bound graph buffer / workspace). */
+typedef struct snn_graph_view {
+    int64_t n_edges;
+    int32_t n_slices;      /* S = ceil(n / W) */
+    int64_t *row_ptr;      /* n+1 entries: row k is col[row_ptr[k] .. row_ptr[k+1]) */
+    int32_t *col;          /* targets, ascending within each row */
+    float *w;              /* weights, 1:1 with col */
+    int32_t *pivots;       /* n x (S+1), row-relative: entries pivots[k][s] ..
+                              pivots[k][s+1]-1 of row k target [sW, (s+1)W) */
+    int32_t *plastic_end;  /* n: row-relative end of the plastic prefix */
+} snn_graph_view;
+
+typedef struct snn_stats {
+    int64_t steps;                 /* completed steps */
+    int64_t spikes;                /* spikes emitted */
+    int64_t delivered_events;      /* (transmitted spike, outgoing synapse) pairs */
+    int64_t stdp_rows;             /* rows brought up to date (incl. forced, flush) */
+    int64_t stdp_forced_rows;      /* rows forced by the 64-step history window */
+    int64_t stdp_synapse_updates;  /* plastic synapses advanced */
+    int64_t stdp_weights_written;  /* weights that changed and were stored */
+    int64_t device_errors;         /* conditions flagged by kernels: 4 = a plastic row
+                                      fell more than 64 steps behind (its update was
+                                      skipped), so its weights are no longer exact */
+} snn_stats;
+
+/* Human-readable name of a status code (static string). */
+const char *snn_status_string(snn_status s);
+
+/* Creates a context for cfg on the current HIP device and stream hip_stream
+ * (a hipStream_t; NULL = the null stream). Validates cfg (SNN_EINVAL with a
+ * message in *out's error if *out could be created, else only the status).
+ * Derived constants are computed here on the host. */
+snn_status snn_create(const snn_config *cfg, void *hip_stream, snn_ctx **out);
+
+/* Releases the host context. Does not touch caller device memory. NULL is
+ * accepted. Work already enqueued is not waited for. */
+void snn_destroy(snn_ctx *ctx);
+
+/* Last error message of ctx (empty string if none; never NULL). */
+const char *snn_last_error(const snn_ctx *ctx);
+
+/* Bytes of device workspace for neuron state, spike lists, the delay ring,
+ * row pointers and statistics. Depends only on the configuration. */
+snn_status snn_workspace_size(const snn_ctx *ctx, size_t *bytes);
+
+/* Binds a device buffer of at least snn_workspace_size bytes (256-byte
+ * aligned) and initialises the state: V, currents, histories, traces and
+ * inputs 0, t_last = -1, t = 0, statistics 0. SNN_ENOMEM if too small. */
+snn_status snn_bind_workspace(snn_ctx *ctx, void *device_ptr, size_t bytes);
+
+/* First half of the random graph builder (Fig. 1 data structures, built on
+ * the device as in Sec. IV-B): draws the edge count of every row and scans
+ * them into row_ptr. kind SNN_GRAPH_BERNOULLI: pair (k, j), j != k, exists
+ * when the stream-0 draw at (k, j) is below floor(p 2^32). kind
+ * SNN_GRAPH_FIXED_FANOUT: row k has F = p_or_fanout targets
+ * (u32 * n) >> 32 from stream 1 at (k, draw). Synchronises the stream and
+ * returns the total in *n_edges. Needs a bound workspace. */
+snn_status snn_graph_count_random(snn_ctx *ctx, int32_t kind, double p_or_fanout,
+                                  int64_t *n_edges);
+
+/* Bytes of the graph buffer for n_edges edges: targets, weights and the
+ * n x (S+1) pivot table. */
+snn_status snn_graph_size(const snn_ctx *ctx, int64_t n_edges, size_t *bytes);
+
+/* Binds a device graph buffer of at least snn_graph_size(n_edges) bytes. */
+snn_status snn_bind_graph(snn_ctx *ctx, void *device_ptr, size_t bytes, int64_t n_edges);
+
+/* Second half of the random builder (after snn_graph_count_random and
+ * snn_bind_graph with the same edge count): fills sorted rows, weights by
+ * source type (w_exc for sources below n_exc, else w_inh), slice pivots and
+ * plastic prefixes. Synchronises the stream to check for errors. */
+snn_status snn_build_graph_random(snn_ctx *ctx, float w_exc, float w_inh);
+
+/* Builds the graph from an edge list in device memory (src, dst, w each with
+ * the n_edges entries given to snn_bind_graph): groups edges by source,
+ * sorts each row by (target, weight), then computes pivots and plastic
+ * prefixes. Rows longer than 16384 edges are rejected (SNN_EINVAL), as are
+ * indices outside [0, n). Synchronises the stream. */
+snn_status snn_build_graph_edges(snn_ctx *ctx, const int32_t *src, const int32_t *dst,
+                                 const float *w);
+
+/* Part (1) of step t (Sec. I): integrates every neuron with its input A(t),
+ * writes the firing mask, the spike list into ring slot t mod D, shifts the
+ * histories, updates the post-synaptic trace, and lists the plastic rows to
+ * update at t (rows transmitting at t, and rows idle for 64 steps). */
+snn_status snn_update_neurons(snn_ctx *ctx);
+
+/* Part (2) of step t (Sec. III-A, Fig. 2(c)): brings the listed plastic rows
+ * up to step t (lazy), visiting only set history bits (event-driven); rows
+ * transmitting at t see their pre-synaptic spike at t. */
+snn_status snn_update_plasticity(snn_ctx *ctx);
+
+/* Part (3) of step t: delivers the spikes emitted at t-D+1 (ring slot
+ * (t-D+1) mod D) with the weights as they stand after part (2), producing
+ * A(t+1). mode is an enum snn_delivery value. */
+snn_status snn_deliver_spikes(snn_ctx *ctx, int32_t mode);
+
+/* Ends step t (t <- t+1). */
+snn_status snn_advance(snn_ctx *ctx);
+
+/* n_steps full steps: parts (1), (2), (3) with delivery mode, then advance.
+ * Enqueues only; never synchronises. */
+snn_status snn_step(snn_ctx *ctx, int32_t n_steps, int32_t mode);
+
+/* Brings every plastic row up to the last completed step t-1 (no pre-
+ * synaptic spike), so that all weights equal those of per-step updates. */
+snn_status snn_flush_plasticity(snn_ctx *ctx);
+
+/* Fills *out with device pointers into the workspace and the step index.
+ * Delivery accumulates inputs exactly in 64-bit fixed point (32 fractional
+ * bits) over C partial sums; this call first converts them into the fp32
+ * input the next neuron update would use, so input_exc/input_inh are
+ * readable (and writable) fp32 arrays. */
+snn_status snn_get_state(snn_ctx *ctx, snn_state_view *out);
+
+/* Copies every non-NULL array of *in (caller device buffers) into the state
+ * and sets t = in->t. Used for teacher forcing and checkpoint restore. The
+ * output-only fields (spike mask/list/count, tx, stdp rows) are ignored. */
+snn_status snn_set_state(snn_ctx *ctx, const snn_state_view *in);
+
+/* Device pointers of the graph arrays. */
+snn_status snn_get_graph(const snn_ctx *ctx, snn_graph_view *out);
+
+/* Synchronises the stream and returns accumulated counters. */
+snn_status snn_get_stats(snn_ctx *ctx, snn_stats *out);
+
+/* Zeroes the counters (enqueued on the stream). */
+snn_status snn_reset_stats(snn_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SNN_H */

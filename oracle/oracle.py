@@ -91,6 +91,7 @@ def _load():
         "oracle_set_time": (None, [P, i64]),
         "oracle_num_edges": (i64, [P]),
         "oracle_spike_count": (i32, [P]),
+        "oracle_spikes_total": (i64, [P]),
         "oracle_set_neurons": (None, [P, P, P, P, P, P]),
         "oracle_get_neurons": (None, [P, P, P, P, P, P]),
         "oracle_set_input": (None, [P, P, P]),
@@ -275,6 +276,10 @@ class Oracle:
         lst = np.zeros(cnt, np.int32)
         self._lib.oracle_get_spikes(self._h, _ptr(mask), _ptr(lst))
         return mask, lst
+
+    @property
+    def spikes_total(self):
+        return int(self._lib.oracle_spikes_total(self._h))
 
     def step(self, n=1):
         if n == 1:

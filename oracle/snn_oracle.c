@@ -79,6 +79,7 @@ typedef struct oracle {
     uint64_t *mask;
     int32_t *list;
     int32_t count;
+    int64_t spikes_total; /* spikes emitted since creation */
     int64_t t;
 } oracle;
 
@@ -417,6 +418,7 @@ void oracle_step(oracle *o)
             o->mask[i >> 6] |= 1ULL << (i & 63);
             o->list[o->count++] = i;
         }
+    o->spikes_total += o->count;
 
     /* (2) synapses: every plastic synapse, every step (Fig. 2(a)):
      * pre = source history bit (delay-1), post = target history bit 0 */
@@ -465,6 +467,7 @@ int64_t oracle_time(const oracle *o) { return o->t; }
 void oracle_set_time(oracle *o, int64_t t) { o->t = t; }
 int64_t oracle_num_edges(const oracle *o) { return o->n_edges; }
 int32_t oracle_spike_count(const oracle *o) { return o->count; }
+int64_t oracle_spikes_total(const oracle *o) { return o->spikes_total; }
 
 void oracle_set_neurons(oracle *o, const float *v, const int32_t *r, const float *ie,
                         const float *ii, const uint64_t *hist)

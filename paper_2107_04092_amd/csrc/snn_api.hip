@@ -1,0 +1,871 @@
+// Host runtime behind the C ABI of include/snn.h: configuration checks,
+// derived constants, the workspace plan over caller memory, launch
+// sequencing of one step, graph-building phases and statistics.
+#include "snn_internal.h"
+#include "snn.h"
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+using namespace snn;
+
+struct snn_ctx {
+    snn_config cfg;
+    hipStream_t stream = nullptr;
+    int device = 0;
+    std::string err;
+
+    // derived configuration
+    int32_t n = 0, nw = 0, nblk = 0, nacc = 1, n_slices = 0, chunks = 1, delay = 1;
+    int32_t n_plastic_rows = 0, ref_steps = 0, dlv_blocks = 0, stdp_blocks = 0;
+    float k_m = 0, v_th = 0, v_reset = 0, v_inf = 0, d_e = 0, d_i = 0, j_ext = 0;
+    float d_minus = 0, c_pot = 0, c_dep = 0, mu = 0;
+    float dpow[65] = {};
+    uint32_t fire_thr = 0;
+
+    // workspace plan
+    size_t ws_need = 0;
+    uint8_t *ws = nullptr;
+    float *v = nullptr, *ie = nullptr, *ii = nullptr, *ypost = nullptr, *xpre = nullptr;
+    long long *apart = nullptr;  // fixed-point partial inputs [C][nacc][n]
+    float *ain = nullptr;        // fp32 input [nacc][n] (teacher forcing / views)
+    int32_t *ref = nullptr, *t_last = nullptr, *pend = nullptr;
+    uint64_t *hist = nullptr, *mask = nullptr, *rmask = nullptr;
+    int32_t *blk_spk = nullptr, *blk_row = nullptr, *ring = nullptr, *ring_cnt = nullptr;
+    int32_t *rows = nullptr, *row_cnt = nullptr, *err_flag = nullptr, *maxlen = nullptr;
+    int64_t *row_ptr = nullptr, *scratch = nullptr, *bsum = nullptr;
+    int64_t *gstats = nullptr, *stdp_stats = nullptr, *dlv_stats = nullptr;
+    int32_t dlv_slots = 0;
+
+    // graph
+    uint8_t *g = nullptr;
+    size_t g_bytes = 0;
+    int64_t n_edges = -1, counted_edges = -1;
+    int32_t *col = nullptr, *piv = nullptr;
+    float *w = nullptr;
+    int graph_state = 0;  // 0 none, 1 counted, 2 buffer bound, 3 built
+    int32_t counted_kind = -1;
+    double counted_p = 0.0;
+
+    // time
+    int64_t t = 0, steps_done = 0, last_neuron_t = -1, last_deliver_t = -1;
+    int32_t n_parts = 1;       // partial sums written by the last delivery
+    int32_t input_forced = 1;  // next neuron update reads `ain` instead of partials
+};
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+
+snn_status fail(snn_ctx *c, snn_status st, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    if (c) c->err = buf;
+    return st;
+}
+
+snn_status check_hip(snn_ctx *c, hipError_t e, const char *what)
+{
+    if (e == hipSuccess) return SNN_OK;
+    return fail(c, SNN_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool finite_all(std::initializer_list<double> xs)
+{
+    for (double x : xs)
+        if (!std::isfinite(x)) return false;
+    return true;
+}
+
+snn_status validate(snn_ctx *c, const snn_config &k)
+{
+    if (k.n < 1 || k.n >= (1 << 24)) return fail(c, SNN_EINVAL, "n must be in [1, 2^24)");
+    if (k.n_exc < 0 || k.n_exc > k.n) return fail(c, SNN_EINVAL, "n_exc must be in [0, n]");
+    if (k.delay_steps < 1 || k.delay_steps > SNN_MAX_DELAY)
+        return fail(c, SNN_EINVAL, "delay_steps must be in [1, 64]");
+    if (k.neuron_model < 0 || k.neuron_model > 2)
+        return fail(c, SNN_EINVAL, "unknown neuron_model %d", k.neuron_model);
+    if (k.plastic < 0 || k.plastic > 2) return fail(c, SNN_EINVAL, "unknown plastic %d", k.plastic);
+    const int nacc = k.neuron_model == SNN_LIF_CUBA ? 2 : 1;
+    if (k.slice_width < kWave || k.slice_width % kWave != 0)
+        return fail(c, SNN_EINVAL, "slice_width must be a positive multiple of 64");
+    if ((int64_t)k.slice_width * 8 * nacc > kLdsBytes)
+        return fail(c, SNN_EINVAL, "slice_width * 8 B * %d accumulators exceeds 160 KiB of LDS",
+                    nacc);
+    if (k.spike_chunks < 1 || k.spike_chunks > 64)
+        return fail(c, SNN_EINVAL, "spike_chunks must be in [1, 64]");
+    const int64_t slices = (k.n + k.slice_width - 1) / k.slice_width;
+    if (slices * k.spike_chunks > (1 << 20))
+        return fail(c, SNN_EINVAL, "slices * spike_chunks must not exceed 2^20");
+    if (k.poisson_len < 0 || k.poisson_len > SNN_MAX_POISSON)
+        return fail(c, SNN_EINVAL, "poisson_len must be in [0, 32]");
+    for (int q = 1; q < k.poisson_len; ++q)
+        if (k.poisson_cdf[q] < k.poisson_cdf[q - 1])
+            return fail(c, SNN_EINVAL, "poisson_cdf must be non-decreasing");
+    if (!finite_all({k.dt_ms, k.tau_m_ms, k.v_th, k.v_reset, k.v_inf, k.tau_ref_ms, k.tau_e_ms,
+                     k.tau_i_ms, k.j_ext, k.p_fire, k.tau_plus_ms, k.tau_minus_ms, k.lambda,
+                     k.alpha, k.mu, k.w0}))
+        return fail(c, SNN_EINVAL, "configuration contains a NaN or infinity");
+    if (!(k.dt_ms > 0)) return fail(c, SNN_EINVAL, "dt_ms must be > 0");
+    if (k.neuron_model != SNN_BERNOULLI_SOURCE) {
+        if (!(k.tau_m_ms > 0)) return fail(c, SNN_EINVAL, "tau_m_ms must be > 0");
+        if (!(k.tau_ref_ms >= 0)) return fail(c, SNN_EINVAL, "tau_ref_ms must be >= 0");
+    } else if (!(k.p_fire >= 0 && k.p_fire <= 1)) {
+        return fail(c, SNN_EINVAL, "p_fire must be in [0, 1]");
+    }
+    if (k.neuron_model == SNN_LIF_CUBA && !(k.tau_e_ms > 0 && k.tau_i_ms > 0))
+        return fail(c, SNN_EINVAL, "tau_e_ms and tau_i_ms must be > 0");
+    if (k.plastic != SNN_PLASTIC_NONE) {
+        if (!(k.tau_plus_ms > 0 && k.tau_minus_ms > 0))
+            return fail(c, SNN_EINVAL, "STDP time constants must be > 0");
+        if (!(k.mu >= 0 && k.mu < 1)) return fail(c, SNN_EINVAL, "mu must be in [0, 1)");
+        if (!(k.w0 > 0)) return fail(c, SNN_EINVAL, "w0 must be > 0");
+        if (!(k.lambda >= 0 && k.alpha >= 0))
+            return fail(c, SNN_EINVAL, "lambda and alpha must be >= 0");
+    }
+    return SNN_OK;
+}
+
+// Constants derived here on the host from the physical parameters (double,
+// rounded once to fp32).
+void derive(snn_ctx *c)
+{
+    const snn_config &k = c->cfg;
+    c->n = k.n;
+    c->nw = (k.n + 63) / 64;
+    c->nblk = (k.n + kBlock - 1) / kBlock;
+    c->nacc = k.neuron_model == SNN_LIF_CUBA ? 2 : 1;
+    c->n_slices = (k.n + k.slice_width - 1) / k.slice_width;
+    c->chunks = k.spike_chunks;
+    c->delay = k.delay_steps;
+    c->n_plastic_rows = k.plastic == SNN_PLASTIC_ALL ? k.n
+                      : k.plastic == SNN_PLASTIC_EXC_EXC ? k.n_exc : 0;
+    c->k_m = k.neuron_model == SNN_BERNOULLI_SOURCE ? 0.f : (float)(k.dt_ms / k.tau_m_ms);
+    c->v_th = (float)k.v_th;
+    c->v_reset = (float)k.v_reset;
+    c->v_inf = (float)k.v_inf;
+    c->d_e = k.neuron_model == SNN_LIF_CUBA ? (float)std::exp(-k.dt_ms / k.tau_e_ms) : 0.f;
+    c->d_i = k.neuron_model == SNN_LIF_CUBA ? (float)std::exp(-k.dt_ms / k.tau_i_ms) : 0.f;
+    c->j_ext = (float)k.j_ext;
+    c->ref_steps = k.neuron_model == SNN_BERNOULLI_SOURCE
+                       ? 0 : (int32_t)std::lround(k.tau_ref_ms / k.dt_ms);
+    const double thr = std::floor(k.p_fire * 4294967296.0);
+    c->fire_thr = thr <= 0 ? 0u : thr >= 4294967295.0 ? 0xFFFFFFFFu : (uint32_t)thr;
+    if (k.plastic != SNN_PLASTIC_NONE) {
+        const double dp = std::exp(-k.dt_ms / k.tau_plus_ms);
+        for (int q = 0; q <= 64; ++q) c->dpow[q] = (float)std::pow(dp, (double)q);
+        c->d_minus = (float)std::exp(-k.dt_ms / k.tau_minus_ms);
+        c->c_pot = (float)(k.lambda * std::pow(k.w0, 1.0 - k.mu));
+        c->c_dep = (float)(k.lambda * k.alpha);
+        c->mu = (float)k.mu;
+    }
+    const int64_t work = (int64_t)c->n_slices * c->chunks;
+    c->dlv_blocks = (int32_t)((work + 7) / 8 * 8);
+    const int64_t sb = (c->n_plastic_rows + 3) / 4;
+    c->stdp_blocks = (int32_t)(sb < 1 ? 1 : sb > kStdpMaxBlocks ? kStdpMaxBlocks : sb);
+    c->dlv_slots = c->dlv_blocks > kGlobalMaxBlocks ? c->dlv_blocks : kGlobalMaxBlocks;
+}
+
+// Workspace plan: a bump allocator over the caller's buffer.
+struct Plan {
+    size_t off = 0;
+    uint8_t *base = nullptr;
+    template <typename T> T *take(int64_t count)
+    {
+        T *p = base ? (T *)(base + off) : nullptr;
+        off = align_up(off + (size_t)count * sizeof(T));
+        return p;
+    }
+};
+
+void plan_workspace(snn_ctx *c, uint8_t *base)
+{
+    Plan p;
+    p.base = base;
+    const int64_t n = c->n;
+    c->v = p.take<float>(n);
+    c->ref = p.take<int32_t>(n);
+    c->ie = p.take<float>(n);
+    c->ii = p.take<float>(n);
+    c->hist = p.take<uint64_t>(n);
+    c->ypost = p.take<float>(n);
+    c->t_last = p.take<int32_t>(n);
+    c->xpre = p.take<float>(n);
+    c->apart = p.take<long long>((int64_t)c->chunks * c->nacc * n);
+    c->ain = p.take<float>((int64_t)c->nacc * n);
+    c->mask = p.take<uint64_t>(c->nw);
+    c->rmask = p.take<uint64_t>(c->nw);
+    c->blk_spk = p.take<int32_t>(c->nblk);
+    c->blk_row = p.take<int32_t>(c->nblk);
+    c->ring = p.take<int32_t>((int64_t)c->delay * n);
+    c->ring_cnt = p.take<int32_t>(c->delay);
+    c->rows = p.take<int32_t>(n);
+    c->row_cnt = p.take<int32_t>(1);
+    c->err_flag = p.take<int32_t>(1);
+    c->maxlen = p.take<int32_t>(1);
+    c->row_ptr = p.take<int64_t>(n + 1);
+    c->pend = p.take<int32_t>(n);
+    c->scratch = p.take<int64_t>(n + 1);
+    c->bsum = p.take<int64_t>((n + 1 + 1023) / 1024 + 1);
+    c->gstats = p.take<int64_t>(kGFields);
+    c->stdp_stats = p.take<int64_t>((int64_t)kStdpMaxBlocks * kStFields);
+    c->dlv_stats = p.take<int64_t>(c->dlv_slots);
+    c->ws_need = p.off;
+}
+
+snn_status require_ws(snn_ctx *c)
+{
+    if (!c->ws) return fail(c, SNN_ESTATE, "no workspace bound");
+    return SNN_OK;
+}
+
+snn_status require_graph(snn_ctx *c)
+{
+    if (!c->ws) return fail(c, SNN_ESTATE, "no workspace bound");
+    if (c->graph_state != 3) return fail(c, SNN_ESTATE, "graph not built");
+    return SNN_OK;
+}
+
+GraphArgs graph_args(snn_ctx *c)
+{
+    GraphArgs a{};
+    a.row_ptr = c->row_ptr;
+    a.col = c->col;
+    a.w = c->w;
+    a.piv = c->piv;
+    a.pend = c->pend;
+    a.err = c->err_flag;
+    a.maxlen = c->maxlen;
+    a.seed = c->cfg.seed;
+    a.n = c->n;
+    a.n_exc = c->cfg.n_exc;
+    a.width = c->cfg.slice_width;
+    a.n_slices = c->n_slices;
+    a.plastic = c->cfg.plastic;
+    return a;
+}
+
+int ring_slot(const snn_ctx *c, int64_t step)
+{
+    const int64_t d = c->delay;
+    return (int)(((step % d) + d) % d);
+}
+
+snn_status zero_stats(snn_ctx *c)
+{
+    hipError_t e = launch_fill_i64(c->stream, c->gstats, kGFields, 0);
+    if (e == hipSuccess)
+        e = launch_fill_i64(c->stream, c->stdp_stats, (int64_t)kStdpMaxBlocks * kStFields, 0);
+    if (e == hipSuccess) e = launch_fill_i64(c->stream, c->dlv_stats, c->dlv_slots, 0);
+    c->steps_done = 0;
+    return check_hip(c, e, "reset statistics");
+}
+
+// Finish a graph build: pivots, plastic prefixes, error check, group size.
+snn_status finish_graph(snn_ctx *c)
+{
+    GraphArgs a = graph_args(c);
+    snn_status st = check_hip(c, launch_pivots(c->stream, a), "pivot kernel");
+    if (st) return st;
+    int32_t err = 0;
+    st = check_hip(c, hipMemcpyAsync(&err, c->err_flag, sizeof err, hipMemcpyDeviceToHost,
+                                     c->stream), "read error flag");
+    if (st) return st;
+    st = check_hip(c, hipStreamSynchronize(c->stream), "graph build");
+    if (st) return st;
+    if (err & kErrIndex) return fail(c, SNN_EINVAL, "edge index outside [0, n)");
+    if (err & kErrRowTooLong)
+        return fail(c, SNN_EINVAL, "a row has more than %d edges", kMaxSortRow);
+    c->graph_state = 3;
+    return SNN_OK;
+}
+
+// Turns pending fixed-point partial inputs into the fp32 input the next
+// neuron update would compute, so it can be viewed or overwritten.
+snn_status materialize_input(snn_ctx *c)
+{
+    if (c->input_forced) return SNN_OK;
+    snn_status st = check_hip(c, launch_materialize_input(c->stream, c->apart,
+                                                         (int64_t)c->nacc * c->n, c->n_parts,
+                                                         c->ain, (int64_t)c->nacc * c->n),
+                              "materialise input");
+    if (st) return st;
+    c->input_forced = 1;
+    return SNN_OK;
+}
+
+snn_status launch_step_neurons(snn_ctx *c)
+{
+    NeuronArgs a{};
+    a.v = c->v;
+    a.ref = c->ref;
+    a.ie = c->ie;
+    a.ii = c->ii;
+    a.hist = c->hist;
+    a.ypost = c->ypost;
+    a.t_last = c->t_last;
+    a.apart = c->apart;
+    a.ain = c->ain;
+    a.part_stride = (int64_t)c->nacc * c->n;
+    a.input_forced = c->input_forced;
+    a.mask = c->mask;
+    a.rmask = c->rmask;
+    a.blk_spk = c->blk_spk;
+    a.blk_row = c->blk_row;
+    a.t = c->t;
+    a.n = c->n;
+    a.n_exc = c->cfg.n_exc;
+    a.model = c->cfg.neuron_model;
+    a.n_plastic_rows = c->n_plastic_rows;
+    a.dm1 = c->delay - 1;
+    a.ref_steps = c->ref_steps;
+    a.poisson_len = c->cfg.neuron_model == SNN_LIF_DELTA ? c->cfg.poisson_len : 0;
+    a.n_parts = c->n_parts;
+    a.k_m = c->k_m;
+    a.v_th = c->v_th;
+    a.v_reset = c->v_reset;
+    a.v_inf = c->v_inf;
+    a.d_e = c->d_e;
+    a.d_i = c->d_i;
+    a.j_ext = c->j_ext;
+    a.d_minus = c->d_minus;
+    a.fire_thr = c->fire_thr;
+    a.seed = c->cfg.seed;
+    for (int q = 0; q < kMaxPoisson; ++q) a.poisson[q] = c->cfg.poisson_cdf[q];
+    snn_status st = check_hip(c, launch_neuron(c->stream, a), "neuron kernel");
+    if (st) return st;
+    c->input_forced = 0;  // the input has been consumed; the next comes from delivery
+    CompactArgs b{};
+    b.mask = c->mask;
+    b.rmask = c->rmask;
+    b.blk_spk = c->blk_spk;
+    b.blk_row = c->blk_row;
+    b.spk_list = c->ring + (int64_t)ring_slot(c, c->t) * c->n;
+    b.spk_cnt = c->ring_cnt + ring_slot(c, c->t);
+    b.row_list = c->rows;
+    b.row_cnt = c->row_cnt;
+    b.gstats = c->gstats;
+    b.n = c->n;
+    b.nw = c->nw;
+    st = check_hip(c, launch_compact(c->stream, b), "compaction kernel");
+    if (st) return st;
+    c->last_neuron_t = c->t;
+    return SNN_OK;
+}
+
+StdpArgs stdp_args(snn_ctx *c)
+{
+    StdpArgs a{};
+    a.row_ptr = c->row_ptr;
+    a.pend = c->pend;
+    a.col = c->col;
+    a.w = c->w;
+    a.hist = c->hist;
+    a.ypost = c->ypost;
+    a.t_last = c->t_last;
+    a.xpre = c->xpre;
+    a.rows = c->rows;
+    a.row_cnt = c->row_cnt;
+    a.n_rows_all = c->n_plastic_rows;
+    a.dm1 = c->delay - 1;
+    a.t = c->t;
+    a.c_pot = c->c_pot;
+    a.c_dep = c->c_dep;
+    a.mu = c->mu;
+    a.stats = c->stdp_stats;
+    a.err = c->err_flag;
+    for (int q = 0; q <= 64; ++q) a.dpow[q] = c->dpow[q];
+    return a;
+}
+
+snn_status launch_step_plasticity(snn_ctx *c)
+{
+    if (c->n_plastic_rows == 0) return SNN_OK;
+    StdpArgs a = stdp_args(c);
+    return check_hip(c, launch_stdp(c->stream, a, c->stdp_blocks), "STDP kernel");
+}
+
+snn_status launch_step_delivery(snn_ctx *c, int32_t mode)
+{
+    DeliverArgs a{};
+    a.row_ptr = c->row_ptr;
+    a.col = c->col;
+    a.w = c->w;
+    a.piv = c->piv;
+    const int slot = ring_slot(c, c->t - (c->delay - 1));
+    a.list = c->ring + (int64_t)slot * c->n;
+    a.cnt = c->ring_cnt + slot;
+    a.apart = c->apart;
+    a.ain = c->ain;
+    a.part_stride = (int64_t)c->nacc * c->n;
+    a.n = c->n;
+    a.n_exc = c->cfg.n_exc;
+    a.width = c->cfg.slice_width;
+    a.n_slices = c->n_slices;
+    a.chunks = c->chunks;
+    a.nacc = c->nacc;
+    a.n_work = c->n_slices * c->chunks;
+    a.stats = c->dlv_stats;
+    snn_status st;
+    if (mode == SNN_DELIVER_LDS_SLICE) {
+        const size_t lds = (size_t)c->cfg.slice_width * c->nacc * sizeof(long long);
+        st = check_hip(c, launch_deliver_lds(c->stream, a, c->dlv_blocks, lds),
+                       "LDS delivery kernel");
+        if (st) return st;
+        c->n_parts = c->chunks;
+        c->last_deliver_t = c->t;
+        // with one chunk each workgroup owns its slice and stores the fp32 input
+        c->input_forced = c->chunks == 1 ? 1 : 0;
+        return SNN_OK;
+    } else {
+        st = check_hip(c, launch_fill_ll(c->stream, c->apart, a.part_stride, 0),
+                       "clear input");
+        if (st) return st;
+        st = check_hip(c, launch_deliver_global(c->stream, a, kGlobalMaxBlocks),
+                       "global delivery kernel");
+        if (st) return st;
+        c->n_parts = 1;
+    }
+    c->input_forced = 0;
+    c->last_deliver_t = c->t;
+    return SNN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *snn_status_string(snn_status s)
+{
+    switch (s) {
+    case SNN_OK: return "ok";
+    case SNN_EINVAL: return "invalid argument";
+    case SNN_ENOMEM: return "buffer too small";
+    case SNN_EDEVICE: return "device error";
+    case SNN_ESTATE: return "call out of order";
+    }
+    return "unknown status";
+}
+
+snn_status snn_create(const snn_config *cfg, void *hip_stream, snn_ctx **out)
+{
+    if (!out) return SNN_EINVAL;
+    *out = nullptr;
+    if (!cfg) return SNN_EINVAL;
+    snn_ctx *c = new (std::nothrow) snn_ctx();
+    if (!c) return SNN_ENOMEM;
+    c->cfg = *cfg;
+    c->stream = (hipStream_t)hip_stream;
+    *out = c;
+    snn_status st = validate(c, *cfg);
+    if (st) return st;
+    if (hipGetDevice(&c->device) != hipSuccess)
+        return fail(c, SNN_EDEVICE, "no HIP device");
+    int lds_max = 0;
+    if (hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, c->device) !=
+        hipSuccess)
+        return fail(c, SNN_EDEVICE, "cannot query the LDS size");
+    const int stat = deliver_lds_static_bytes();
+    if (stat < 0) return fail(c, SNN_EDEVICE, "cannot query the delivery kernel");
+    const int64_t need = (int64_t)cfg->slice_width * 8 * (cfg->neuron_model == SNN_LIF_CUBA ? 2 : 1);
+    if (need + stat > lds_max)
+        return fail(c, SNN_EINVAL,
+                    "slice accumulator needs %lld B of LDS besides %d B of staging; the "
+                    "device allows %d in total", (long long)need, stat, lds_max);
+    derive(c);
+    plan_workspace(c, nullptr);
+    return SNN_OK;
+}
+
+void snn_destroy(snn_ctx *ctx) { delete ctx; }
+
+const char *snn_last_error(const snn_ctx *ctx) { return ctx ? ctx->err.c_str() : "null context"; }
+
+snn_status snn_workspace_size(const snn_ctx *ctx, size_t *bytes)
+{
+    if (!ctx || !bytes) return SNN_EINVAL;
+    *bytes = ctx->ws_need;
+    return SNN_OK;
+}
+
+snn_status snn_bind_workspace(snn_ctx *c, void *device_ptr, size_t bytes)
+{
+    if (!c) return SNN_EINVAL;
+    if (!device_ptr) return fail(c, SNN_EINVAL, "workspace pointer is NULL");
+    if ((uintptr_t)device_ptr % kAlign) return fail(c, SNN_EINVAL, "workspace not 256-byte aligned");
+    if (bytes < c->ws_need)
+        return fail(c, SNN_ENOMEM, "workspace has %zu bytes, needs %zu", bytes, c->ws_need);
+    c->ws = (uint8_t *)device_ptr;
+    plan_workspace(c, c->ws);
+    hipError_t e = launch_init_state(c->stream, c->v, c->ref, c->ie, c->ii, c->hist, c->ypost,
+                                     c->t_last, c->xpre, c->n);
+    if (e == hipSuccess)
+        e = launch_fill_ll(c->stream, c->apart, (int64_t)c->chunks * c->nacc * c->n, 0);
+    if (e == hipSuccess) e = launch_fill_f32(c->stream, c->ain, (int64_t)c->nacc * c->n, 0.f);
+    if (e == hipSuccess) e = launch_fill_i32(c->stream, c->ring_cnt, c->delay, 0);
+    if (e == hipSuccess) e = launch_fill_i32(c->stream, c->row_cnt, 1, 0);
+    if (e == hipSuccess) e = launch_fill_i32(c->stream, c->err_flag, 1, 0);
+    if (e == hipSuccess) e = launch_fill_i32(c->stream, c->pend, c->n, 0);
+    snn_status st = check_hip(c, e, "workspace initialisation");
+    if (st) return st;
+    c->t = 0;
+    c->n_parts = 1;
+    c->input_forced = 1;
+    c->last_neuron_t = c->last_deliver_t = -1;
+    c->graph_state = 0;
+    return zero_stats(c);
+}
+
+snn_status snn_graph_count_random(snn_ctx *c, int32_t kind, double p_or_fanout,
+                                  int64_t *n_edges)
+{
+    if (!c || !n_edges) return SNN_EINVAL;
+    snn_status st = require_ws(c);
+    if (st) return st;
+    GraphArgs a = graph_args(c);
+    a.col = nullptr;
+    hipError_t e;
+    if (kind == SNN_GRAPH_BERNOULLI) {
+        if (!(p_or_fanout >= 0 && p_or_fanout <= 1))
+            return fail(c, SNN_EINVAL, "connection probability must be in [0, 1]");
+        const double thr = std::floor(p_or_fanout * 4294967296.0);
+        a.thr = thr >= 4294967295.0 ? 0xFFFFFFFFu : (uint32_t)thr;
+        e = launch_graph_count_bernoulli(c->stream, a);
+        if (e == hipSuccess) e = launch_scan_i64(c->stream, c->row_ptr + 1, c->n, c->bsum);
+    } else if (kind == SNN_GRAPH_FIXED_FANOUT) {
+        if (!(p_or_fanout >= 0 && p_or_fanout < (1 << 24)) ||
+            p_or_fanout != std::floor(p_or_fanout))
+            return fail(c, SNN_EINVAL, "fan-out must be an integer in [0, 2^24)");
+        a.fanout = (int32_t)p_or_fanout;
+        e = launch_graph_fill_fanout(c->stream, a);
+    } else {
+        return fail(c, SNN_EINVAL, "unknown graph kind %d", kind);
+    }
+    st = check_hip(c, e, "graph count");
+    if (st) return st;
+    int64_t total = 0;
+    st = check_hip(c, hipMemcpyAsync(&total, c->row_ptr + c->n, sizeof total,
+                                     hipMemcpyDeviceToHost, c->stream), "read edge count");
+    if (st) return st;
+    st = check_hip(c, hipStreamSynchronize(c->stream), "graph count");
+    if (st) return st;
+    c->counted_edges = total;
+    c->counted_kind = kind;
+    c->counted_p = p_or_fanout;
+    c->graph_state = 1;
+    *n_edges = total;
+    return SNN_OK;
+}
+
+snn_status snn_graph_size(const snn_ctx *c, int64_t n_edges, size_t *bytes)
+{
+    if (!c || !bytes || n_edges < 0) return SNN_EINVAL;
+    *bytes = align_up((size_t)n_edges * 4) * 2 +
+             align_up((size_t)c->n * (size_t)(c->n_slices + 1) * 4);
+    return SNN_OK;
+}
+
+snn_status snn_bind_graph(snn_ctx *c, void *device_ptr, size_t bytes, int64_t n_edges)
+{
+    if (!c) return SNN_EINVAL;
+    snn_status st = require_ws(c);
+    if (st) return st;
+    if (!device_ptr) return fail(c, SNN_EINVAL, "graph pointer is NULL");
+    if ((uintptr_t)device_ptr % kAlign) return fail(c, SNN_EINVAL, "graph buffer not 256-byte aligned");
+    if (n_edges < 0) return fail(c, SNN_EINVAL, "n_edges must be >= 0");
+    if (c->graph_state == 1 && n_edges != c->counted_edges)
+        return fail(c, SNN_EINVAL, "n_edges %lld differs from the counted %lld",
+                    (long long)n_edges, (long long)c->counted_edges);
+    size_t need = 0;
+    snn_graph_size(c, n_edges, &need);
+    if (bytes < need) return fail(c, SNN_ENOMEM, "graph buffer has %zu bytes, needs %zu", bytes, need);
+    c->g = (uint8_t *)device_ptr;
+    c->g_bytes = bytes;
+    c->n_edges = n_edges;
+    c->col = (int32_t *)c->g;
+    c->w = (float *)(c->g + align_up((size_t)n_edges * 4));
+    c->piv = (int32_t *)(c->g + 2 * align_up((size_t)n_edges * 4));
+    if (c->graph_state != 1) c->counted_kind = -1;
+    c->graph_state = 2;
+    return SNN_OK;
+}
+
+snn_status snn_build_graph_random(snn_ctx *c, float w_exc, float w_inh)
+{
+    if (!c) return SNN_EINVAL;
+    snn_status st = require_ws(c);
+    if (st) return st;
+    if (c->graph_state != 2 || c->counted_kind < 0)
+        return fail(c, SNN_ESTATE, "call snn_graph_count_random and snn_bind_graph first");
+    if (!std::isfinite(w_exc) || !std::isfinite(w_inh))
+        return fail(c, SNN_EINVAL, "weights must be finite");
+    GraphArgs a = graph_args(c);
+    a.w_exc = w_exc;
+    a.w_inh = w_inh;
+    hipError_t e = launch_fill_i32(c->stream, c->err_flag, 1, 0);
+    if (c->counted_kind == SNN_GRAPH_BERNOULLI) {
+        const double thr = std::floor(c->counted_p * 4294967296.0);
+        a.thr = thr >= 4294967295.0 ? 0xFFFFFFFFu : (uint32_t)thr;
+        if (e == hipSuccess) e = launch_graph_fill_bernoulli(c->stream, a);
+    } else {
+        a.fanout = (int32_t)c->counted_p;
+        if (e == hipSuccess) e = launch_graph_fill_fanout(c->stream, a);
+        if (e == hipSuccess && a.fanout > 1) {
+            int p2 = 2;
+            while (p2 < a.fanout) p2 <<= 1;
+            if (a.fanout > kMaxSortRow) return fail(c, SNN_EINVAL, "fan-out above %d", kMaxSortRow);
+            e = launch_row_sort(c->stream, a, p2);
+        }
+    }
+    st = check_hip(c, e, "graph fill");
+    if (st) return st;
+    return finish_graph(c);
+}
+
+snn_status snn_build_graph_edges(snn_ctx *c, const int32_t *src, const int32_t *dst,
+                                 const float *w)
+{
+    if (!c) return SNN_EINVAL;
+    snn_status st = require_ws(c);
+    if (st) return st;
+    if (c->graph_state < 2) return fail(c, SNN_ESTATE, "call snn_bind_graph first");
+    const int64_t e = c->n_edges;
+    if (e > 0 && (!src || !dst || !w)) return fail(c, SNN_EINVAL, "edge arrays are NULL");
+    GraphArgs a = graph_args(c);
+    hipError_t he = launch_fill_i32(c->stream, c->err_flag, 1, 0);
+    if (he == hipSuccess) he = launch_fill_i32(c->stream, c->maxlen, 1, 0);
+    if (he == hipSuccess) he = launch_fill_i64(c->stream, c->row_ptr, (int64_t)c->n + 1, 0);
+    if (he == hipSuccess) he = launch_edges_count(c->stream, a, src, dst, e);
+    if (he == hipSuccess) he = launch_scan_i64(c->stream, c->row_ptr + 1, c->n, c->bsum);
+    if (he == hipSuccess)
+        he = launch_copy_bytes(c->stream, c->scratch, c->row_ptr, (int64_t)c->n * 8);
+    if (he == hipSuccess) he = launch_edges_scatter(c->stream, a, src, dst, w, e, c->scratch);
+    if (he == hipSuccess) he = launch_row_maxlen(c->stream, a);
+    st = check_hip(c, he, "edge grouping");
+    if (st) return st;
+    int32_t maxlen = 0, err = 0;
+    st = check_hip(c, hipMemcpyAsync(&maxlen, c->maxlen, 4, hipMemcpyDeviceToHost, c->stream),
+                   "read row length");
+    if (!st)
+        st = check_hip(c, hipMemcpyAsync(&err, c->err_flag, 4, hipMemcpyDeviceToHost, c->stream),
+                       "read error flag");
+    if (!st) st = check_hip(c, hipStreamSynchronize(c->stream), "edge grouping");
+    if (st) return st;
+    if (err & kErrIndex) return fail(c, SNN_EINVAL, "edge index outside [0, n)");
+    if (maxlen > kMaxSortRow) return fail(c, SNN_EINVAL, "a row has more than %d edges", kMaxSortRow);
+    if (maxlen > 1) {
+        int p2 = 2;
+        while (p2 < maxlen) p2 <<= 1;
+        st = check_hip(c, launch_row_sort(c->stream, a, p2), "row sort");
+        if (st) return st;
+    }
+    return finish_graph(c);
+}
+
+snn_status snn_update_neurons(snn_ctx *c)
+{
+    if (!c) return SNN_EINVAL;
+    snn_status st = require_graph(c);
+    if (st) return st;
+    return launch_step_neurons(c);
+}
+
+snn_status snn_update_plasticity(snn_ctx *c)
+{
+    if (!c) return SNN_EINVAL;
+    snn_status st = require_graph(c);
+    if (st) return st;
+    if (c->last_neuron_t != c->t)
+        return fail(c, SNN_ESTATE, "update neurons of step %lld first", (long long)c->t);
+    return launch_step_plasticity(c);
+}
+
+snn_status snn_deliver_spikes(snn_ctx *c, int32_t mode)
+{
+    if (!c) return SNN_EINVAL;
+    snn_status st = require_graph(c);
+    if (st) return st;
+    if (mode != SNN_DELIVER_LDS_SLICE && mode != SNN_DELIVER_GLOBAL_ATOMIC)
+        return fail(c, SNN_EINVAL, "unknown delivery mode %d", mode);
+    if (c->last_neuron_t != c->t)
+        return fail(c, SNN_ESTATE, "update neurons of step %lld first", (long long)c->t);
+    return launch_step_delivery(c, mode);
+}
+
+snn_status snn_advance(snn_ctx *c)
+{
+    if (!c) return SNN_EINVAL;
+    snn_status st = require_graph(c);
+    if (st) return st;
+    if (c->last_neuron_t != c->t)
+        return fail(c, SNN_ESTATE, "step %lld has not run", (long long)c->t);
+    c->t += 1;
+    c->steps_done += 1;
+    return SNN_OK;
+}
+
+snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
+{
+    if (!c) return SNN_EINVAL;
+    snn_status st = require_graph(c);
+    if (st) return st;
+    if (n_steps < 0) return fail(c, SNN_EINVAL, "n_steps must be >= 0");
+    if (mode != SNN_DELIVER_LDS_SLICE && mode != SNN_DELIVER_GLOBAL_ATOMIC)
+        return fail(c, SNN_EINVAL, "unknown delivery mode %d", mode);
+    for (int32_t q = 0; q < n_steps; ++q) {
+        if ((st = launch_step_neurons(c))) return st;
+        if ((st = launch_step_plasticity(c))) return st;
+        if ((st = launch_step_delivery(c, mode))) return st;
+        c->t += 1;
+        c->steps_done += 1;
+    }
+    return SNN_OK;
+}
+
+snn_status snn_flush_plasticity(snn_ctx *c)
+{
+    if (!c) return SNN_EINVAL;
+    snn_status st = require_graph(c);
+    if (st) return st;
+    if (c->n_plastic_rows == 0 || c->t == 0) return SNN_OK;
+    StdpArgs a = stdp_args(c);
+    a.rows = nullptr;
+    a.t = c->t - 1;
+    return check_hip(c, launch_stdp(c->stream, a, c->stdp_blocks), "STDP flush");
+}
+
+snn_status snn_get_state(snn_ctx *c, snn_state_view *out)
+{
+    if (!c || !out) return SNN_EINVAL;
+    snn_status st = require_ws(c);
+    if (st) return st;
+    st = materialize_input(c);
+    if (st) return st;
+    std::memset(out, 0, sizeof *out);
+    out->t = c->t;
+    out->v = c->v;
+    out->refractory = c->ref;
+    out->i_exc = c->ie;
+    out->i_inh = c->ii;
+    out->hist = c->hist;
+    out->trace_post = c->ypost;
+    out->t_last = c->t_last;
+    out->trace_pre = c->xpre;
+    out->input_exc = c->ain;
+    out->input_inh = c->nacc == 2 ? c->ain + c->n : nullptr;
+    out->spike_mask = c->mask;
+    const int sl = ring_slot(c, c->last_neuron_t < 0 ? 0 : c->last_neuron_t);
+    out->spike_list = c->ring + (int64_t)sl * c->n;
+    out->spike_count = c->ring_cnt + sl;
+    const int tl = ring_slot(c, c->last_deliver_t < 0 ? 0 : c->last_deliver_t - (c->delay - 1));
+    out->tx_list = c->ring + (int64_t)tl * c->n;
+    out->tx_count = c->ring_cnt + tl;
+    out->stdp_rows = c->rows;
+    out->stdp_row_count = c->row_cnt;
+    out->ring_lists = c->ring;
+    out->ring_counts = c->ring_cnt;
+    return SNN_OK;
+}
+
+snn_status snn_set_state(snn_ctx *c, const snn_state_view *in)
+{
+    if (!c || !in) return SNN_EINVAL;
+    snn_status st = require_ws(c);
+    if (st) return st;
+    if (in->t < 0) return fail(c, SNN_EINVAL, "t must be >= 0");
+    const int64_t n = c->n;
+    if (in->input_exc || in->input_inh) {
+        st = materialize_input(c);  // a field not given keeps its current value
+        if (st) return st;
+    }
+    struct Item { void *dst; const void *src; int64_t bytes; };
+    const Item items[] = {
+        {c->v, in->v, n * 4},           {c->ref, in->refractory, n * 4},
+        {c->ie, in->i_exc, n * 4},      {c->ii, in->i_inh, n * 4},
+        {c->hist, in->hist, n * 8},     {c->ypost, in->trace_post, n * 4},
+        {c->t_last, in->t_last, n * 4}, {c->xpre, in->trace_pre, n * 4},
+        {c->ain, in->input_exc, n * 4},
+        {c->nacc == 2 ? c->ain + n : nullptr, in->input_inh, n * 4},
+        {c->ring, in->ring_lists, (int64_t)c->delay * n * 4},
+        {c->ring_cnt, in->ring_counts, (int64_t)c->delay * 4},
+    };
+    for (const Item &it : items) {
+        if (!it.src || !it.dst) continue;
+        st = check_hip(c, launch_copy_bytes(c->stream, it.dst, it.src, it.bytes), "state copy");
+        if (st) return st;
+    }
+    c->t = in->t;
+    c->last_neuron_t = c->last_deliver_t = -1;
+    return SNN_OK;
+}
+
+snn_status snn_get_graph(const snn_ctx *c, snn_graph_view *out)
+{
+    if (!c || !out) return SNN_EINVAL;
+    std::memset(out, 0, sizeof *out);
+    if (!c->ws || c->graph_state < 2) return SNN_ESTATE;
+    out->n_edges = c->n_edges;
+    out->n_slices = c->n_slices;
+    out->row_ptr = c->row_ptr;
+    out->col = c->col;
+    out->w = c->w;
+    out->pivots = c->piv;
+    out->plastic_end = c->pend;
+    return SNN_OK;
+}
+
+snn_status snn_get_stats(snn_ctx *c, snn_stats *out)
+{
+    if (!c || !out) return SNN_EINVAL;
+    snn_status st = require_ws(c);
+    if (st) return st;
+    std::vector<int64_t> g(kGFields), sd((size_t)kStdpMaxBlocks * kStFields),
+        dv((size_t)c->dlv_slots);
+    int32_t err = 0;
+    hipError_t e = hipMemcpyAsync(g.data(), c->gstats, g.size() * 8, hipMemcpyDeviceToHost,
+                                  c->stream);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(&err, c->err_flag, sizeof err, hipMemcpyDeviceToHost, c->stream);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(sd.data(), c->stdp_stats, sd.size() * 8, hipMemcpyDeviceToHost,
+                           c->stream);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(dv.data(), c->dlv_stats, dv.size() * 8, hipMemcpyDeviceToHost,
+                           c->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+    st = check_hip(c, e, "read statistics");
+    if (st) return st;
+    std::memset(out, 0, sizeof *out);
+    out->steps = c->steps_done;
+    out->spikes = g[kGSpikes];
+    out->device_errors = err;
+    for (int b = 0; b < kStdpMaxBlocks; ++b) {
+        out->stdp_rows += sd[(size_t)b * kStFields + kStRows];
+        out->stdp_forced_rows += sd[(size_t)b * kStFields + kStForced];
+        out->stdp_synapse_updates += sd[(size_t)b * kStFields + kStSyn];
+        out->stdp_weights_written += sd[(size_t)b * kStFields + kStWritten];
+    }
+    for (int64_t v : dv) out->delivered_events += v;
+    return SNN_OK;
+}
+
+snn_status snn_reset_stats(snn_ctx *c)
+{
+    if (!c) return SNN_EINVAL;
+    snn_status st = require_ws(c);
+    if (st) return st;
+    return zero_stats(c);
+}
+
+}  // extern "C"

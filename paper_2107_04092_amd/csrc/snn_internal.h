@@ -1,0 +1,143 @@
+// Internal interface between the host runtime (snn_api.hip) and the gfx950
+// kernels (snn_kernels.hip). Not part of the public C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace snn {
+
+constexpr int kBlock = 256;          // threads per workgroup of the element kernels
+constexpr int kWave = 64;            // CDNA wavefront width
+constexpr int kMaxPoisson = 32;
+constexpr int kMaxSortRow = 16384;   // longest row the LDS row sort accepts
+constexpr int kStdpMaxBlocks = 2048; // persistent STDP grid (8 waves of 64 per CU slot)
+constexpr int kStdpUnroll = 16;      // synapses per lane issued together in STDP
+constexpr int kGlobalMaxBlocks = 2048;
+constexpr int kLdsBytes = 160 * 1024;
+
+// Delivered inputs are accumulated exactly as 64-bit fixed-point integers with
+// 32 fractional bits (sums of |x| < 2^31 mV, resolution 2^-32 mV); integer
+// atomics make the sum independent of the order of the atomic updates.
+constexpr float kFixScale = 4294967296.0f;        // 2^32
+constexpr float kFixUnit = 2.3283064365386963e-10f; // 2^-32
+
+// Per-block statistics slots of the STDP kernel.
+enum StdpStat { kStRows = 0, kStForced = 1, kStSyn = 2, kStWritten = 3, kStFields = 4 };
+
+// Global counters.
+enum GlobalStat { kGSpikes = 0, kGFields = 8 };
+
+// Error bits raised by kernels (device int32, ORed).
+enum DevError { kErrIndex = 1, kErrRowTooLong = 2, kErrWindow = 4 };
+
+struct NeuronArgs {
+    float *v;
+    int32_t *ref;
+    float *ie, *ii;
+    uint64_t *hist;
+    float *ypost;
+    const int32_t *t_last;
+    const long long *apart; // fixed-point partial inputs [n_parts][nacc][n]
+    const float *ain;       // fp32 input [nacc][n], used when input_forced
+    int64_t part_stride;    // nacc * n
+    int32_t input_forced;
+    uint64_t *mask, *rmask; // spike mask, plastic-row trigger mask
+    int32_t *blk_spk, *blk_row;
+    int64_t t;
+    int32_t n, n_exc, model, n_plastic_rows, dm1, ref_steps, poisson_len, n_parts;
+    float k_m, v_th, v_reset, v_inf, d_e, d_i, j_ext, d_minus;
+    uint32_t fire_thr;
+    uint64_t seed;
+    uint32_t poisson[kMaxPoisson];
+};
+
+struct CompactArgs {
+    const uint64_t *mask, *rmask;
+    const int32_t *blk_spk, *blk_row;
+    int32_t *spk_list, *spk_cnt;
+    int32_t *row_list, *row_cnt;
+    int64_t *gstats;
+    int32_t n, nw;
+};
+
+struct StdpArgs {
+    const int64_t *row_ptr;
+    const int32_t *pend;
+    const int32_t *col;
+    float *w;
+    const uint64_t *hist;
+    const float *ypost;
+    int32_t *t_last;
+    float *xpre;
+    const int32_t *rows;     // list mode: rows to update; nullptr in flush mode
+    const int32_t *row_cnt;
+    int32_t n_rows_all;      // flush mode: rows 0 .. n_rows_all-1
+    int32_t dm1;
+    int64_t t;               // list mode: step t; flush mode: last completed step
+    float c_pot, c_dep, mu;
+    int64_t *stats;          // [gridDim.x][kStFields]
+    int32_t *err;            // kErrWindow when a row fell more than 64 steps behind
+    float dpow[65];          // d_plus^i, i = 0..64
+};
+
+struct DeliverArgs {
+    const int64_t *row_ptr;
+    const int32_t *col;
+    const float *w;
+    const int32_t *piv;      // [n][S+1]
+    const int32_t *list;
+    const int32_t *cnt;
+    long long *apart;        // fixed-point partial inputs [C][nacc][n]
+    float *ain;              // fp32 input [nacc][n], written directly when C == 1
+    int64_t part_stride;
+    int32_t n, n_exc, width, n_slices, chunks, nacc, n_work;
+    int64_t *stats;          // [gridDim.x]
+};
+
+struct GraphArgs {
+    int64_t *row_ptr;        // n+1
+    int32_t *col;
+    float *w;
+    int32_t *piv;
+    int32_t *pend;
+    int32_t *err;
+    int32_t *maxlen;
+    uint64_t seed;
+    int32_t n, n_exc, width, n_slices, plastic, fanout;
+    uint32_t thr;
+    float w_exc, w_inh;
+};
+
+// ---- launchers (snn_kernels.hip); all enqueue on `s` and return the launch
+// status of the last kernel they started.
+hipError_t launch_init_state(hipStream_t s, float *v, int32_t *ref, float *ie, float *ii,
+                             uint64_t *hist, float *ypost, int32_t *t_last, float *xpre,
+                             int32_t n);
+hipError_t launch_fill_f32(hipStream_t s, float *p, int64_t count, float value);
+hipError_t launch_fill_i64(hipStream_t s, int64_t *p, int64_t count, int64_t value);
+hipError_t launch_fill_i32(hipStream_t s, int32_t *p, int64_t count, int32_t value);
+hipError_t launch_fill_ll(hipStream_t s, long long *p, int64_t count, long long value);
+hipError_t launch_copy_bytes(hipStream_t s, void *dst, const void *src, int64_t bytes);
+hipError_t launch_neuron(hipStream_t s, const NeuronArgs &a);
+hipError_t launch_compact(hipStream_t s, const CompactArgs &a);
+hipError_t launch_stdp(hipStream_t s, const StdpArgs &a, int blocks);
+hipError_t launch_deliver_lds(hipStream_t s, const DeliverArgs &a, int blocks, size_t lds);
+hipError_t launch_deliver_global(hipStream_t s, const DeliverArgs &a, int blocks);
+int deliver_lds_static_bytes();  // static LDS of the slice kernel (-1 on error)
+hipError_t launch_materialize_input(hipStream_t s, const long long *apart, int64_t part_stride,
+                                    int32_t n_parts, float *ain, int64_t count);
+hipError_t launch_scan_i64(hipStream_t s, int64_t *data, int64_t count, int64_t *bsum);
+hipError_t launch_graph_count_bernoulli(hipStream_t s, const GraphArgs &a);
+hipError_t launch_graph_fill_bernoulli(hipStream_t s, const GraphArgs &a);
+hipError_t launch_graph_fill_fanout(hipStream_t s, const GraphArgs &a);
+hipError_t launch_edges_count(hipStream_t s, const GraphArgs &a, const int32_t *src,
+                              const int32_t *dst, int64_t e);
+hipError_t launch_edges_scatter(hipStream_t s, const GraphArgs &a, const int32_t *src,
+                                const int32_t *dst, const float *w, int64_t e,
+                                int64_t *cursor);
+hipError_t launch_row_maxlen(hipStream_t s, const GraphArgs &a);
+hipError_t launch_row_sort(hipStream_t s, const GraphArgs &a, int pow2len);
+hipError_t launch_pivots(hipStream_t s, const GraphArgs &a);
+
+}  // namespace snn

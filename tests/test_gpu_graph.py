@@ -1,0 +1,127 @@
+"""GPU sliced-CSR builder (Fig. 1 data structures) against the oracle's
+generators and the pivot definition: bit-exact."""
+
+import json
+import os
+
+import numpy as np
+import pytest
+
+import workloads as wl
+from workloads.presets import PLASTIC_EXC_EXC, PLASTIC_ALL, PLASTIC_NONE, LIF_DELTA, \
+    GRAPH_BERNOULLI
+from paper_2107_04092_amd import snn
+
+from gpu_common import gpu_net, oracle_net, to_np, log
+
+pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _check_graph(net, o, p, rows_to_check=None):
+    g = net.graph()
+    rp_o, col_o, w_o = o.graph()
+    rp = to_np(g["row_ptr"])
+    assert np.array_equal(rp, rp_o), "row_ptr"
+    col = to_np(g["col"])
+    assert np.array_equal(col, col_o), "targets"
+    assert np.array_equal(to_np(g["w"]).astype(np.float64), w_o), "weights"
+    piv = to_np(g["pivots"])
+    pend = to_np(g["plastic_end"])
+    from oracle import oracle
+    rows = range(p.n) if rows_to_check is None else rows_to_check
+    for k in rows:
+        row = col[rp[k]:rp[k + 1]]
+        assert np.array_equal(piv[k], oracle.pivots(row, p.n, net.cfg.slice_width)), k
+        if p.plastic == PLASTIC_ALL:
+            assert pend[k] == len(row)
+        elif p.plastic == PLASTIC_EXC_EXC:
+            assert pend[k] == (int((row < p.n_exc).sum()) if k < p.n_exc else 0)
+        else:
+            assert pend[k] == 0
+
+
+@pytest.mark.parametrize("name,kw,width", [
+    ("tiny", {}, 256),
+    ("tiny", dict(n=1000 + 37), 320),
+    ("brunel_plus", dict(n=3000, n_exc=2400), 1024),
+    ("stress", dict(n=20_000, p_or_fanout=300), 4096),
+    ("stress", dict(n=777, p_or_fanout=3000, plastic=PLASTIC_NONE), 64),
+])
+def test_random_graph_matches_oracle(name, kw, width):
+    p = wl.preset(name, slice_width=width, **kw)
+    log("graph %s %s W=%d" % (name, kw, width))
+    net = gpu_net(p)
+    o = oracle_net(p)
+    assert net.n_edges == o.n_edges
+    _check_graph(net, o, p)
+
+
+def test_fig1_graph_from_edges():
+    g = json.load(open(os.path.join(GOLDEN, "fig1_pivots.json")))
+    src, dst = [], []
+    for k, row in enumerate(g["rows"]):
+        src += [k] * len(row)
+        dst += row
+    # shuffled edge order: the builder must group and sort
+    rs = np.random.default_rng(5)
+    perm = rs.permutation(len(src))
+    src = np.array(src)[perm]
+    dst = np.array(dst)[perm]
+    w = (src + 1).astype(np.float32)
+    p = wl.Preset(name="fig1", n=9, n_exc=9, model=LIF_DELTA, graph_kind=GRAPH_BERNOULLI,
+                  p_or_fanout=0, w_exc=0, w_inh=0, slice_width=64)
+    net = gpu_net(p, build=False, slice_width=64)
+    net.build_edges(src, dst, w)
+    gr = net.graph()
+    rp = to_np(gr["row_ptr"])
+    col = to_np(gr["col"])
+    for k, row in enumerate(g["rows"]):
+        assert col[rp[k]:rp[k + 1]].tolist() == row
+    # Fig. 1 uses slices of 3 neurons, below the library's minimum width of 64;
+    # mapping index i to i*64//3 (n = 192) keeps every entry in the same slice
+    # when slices are 64 wide, so the figure's pivots must come out unchanged.
+    src2 = np.repeat(np.arange(3), [len(r) for r in g["rows"]])
+    dst2 = np.concatenate([np.array(r) * 64 // 3 for r in g["rows"]])
+    p2 = p.scaled(n=192, n_exc=192)
+    net2 = gpu_net(p2, build=False, slice_width=64)
+    net2.build_edges(src2, dst2, np.ones(len(src2), np.float32))
+    piv = to_np(net2.graph()["pivots"])
+    for k, want in enumerate(g["pivots"]):
+        assert piv[k].tolist() == want, (k, piv[k], want)
+
+
+def test_edge_builder_sorts_duplicates_and_weights():
+    rs = np.random.default_rng(7)
+    n, e = 500, 20_000
+    src = rs.integers(0, n, e)
+    dst = rs.integers(0, 40, e)  # many duplicate pairs
+    w = rs.standard_normal(e).astype(np.float32)
+    p = wl.preset("tiny", n=n, n_exc=400, slice_width=128)
+    net = gpu_net(p, build=False, slice_width=128)
+    net.build_edges(src, dst, w)
+    o = oracle_net(p, build=False)
+    o.build_edges(src, dst, w)
+    _check_graph(net, o, p)
+
+
+def test_edge_builder_rejects_bad_input():
+    p = wl.preset("tiny", n=100, n_exc=80, slice_width=64)
+    net = gpu_net(p, build=False, slice_width=64)
+    with pytest.raises(snn.SnnError, match="outside"):
+        net.build_edges([0, 1, 100], [1, 2, 3], [1, 1, 1])
+    net = gpu_net(p, build=False, slice_width=64)
+    with pytest.raises(snn.SnnError, match="more than"):
+        net.build_edges(np.zeros(16385, np.int32), np.arange(16385) % 100,
+                        np.ones(16385, np.float32))
+
+
+def test_steps_before_graph_are_rejected():
+    p = wl.preset("tiny", slice_width=256)
+    net = gpu_net(p, build=False)
+    with pytest.raises(snn.SnnError) as e:
+        net.step(1)
+    assert e.value.status == snn.SNN_ESTATE
+    with pytest.raises(snn.SnnError) as e:
+        snn.snn_build_graph_random(net.ctx, 0.1, 0.1)
+    assert e.value.status == snn.SNN_ESTATE

@@ -1,0 +1,159 @@
+"""Teacher-forced parity of the HIP step against the CPU oracle.
+
+Each step the GPU receives the oracle's neuron state and pending input; the
+synaptic state (weights, row ages and traces, post traces, delay ring) evolves
+on the GPU from identical spikes. Spike masks, spike lists, histories,
+potentials and refractory counters must match bit for bit; delivered inputs
+and the weights of the rows STDP just made current must match within
+|g - o| <= 1e-5 |o| + 1e-7; after a final flush every plastic weight must.
+"""
+
+import numpy as np
+import pytest
+
+import workloads as wl
+from workloads.presets import PLASTIC_ALL, PLASTIC_NONE, BERNOULLI_SOURCE, LIF_DELTA, \
+    GRAPH_BERNOULLI
+from paper_2107_04092_amd import snn
+
+from gpu_common import (teacher_forced_run, compare_all_plastic_weights, gpu_net, oracle_net,
+                        compare_step, force_from_oracle, to_np, log, assert_close)
+
+pytestmark = pytest.mark.gpu
+LDS, GLOBAL = snn.SNN_DELIVER_LDS_SLICE, snn.SNN_DELIVER_GLOBAL_ATOMIC
+
+CASES = [
+    # name, preset overrides, steps, slice width, chunks
+    ("tiny", dict(), 300, 256, 1),
+    ("tiny", dict(n=1037, n_exc=830), 300, 320, 3),
+    ("vogels", dict(), 300, 1024, 2),
+    ("brunel", dict(n=5000, n_exc=4000), 200, 1024, 1),
+    ("brunel_plus", dict(n=2500, n_exc=2000), 300, 512, 2),
+    ("stress", dict(n=6000, p_or_fanout=200, p_fire=0.02), 200, 1024, 4),
+    ("stress", dict(n=3000, p_or_fanout=150, p_fire=0.03, delay=3), 160, 640, 1),
+]
+
+
+@pytest.mark.parametrize("mode", [LDS, GLOBAL], ids=["lds", "global"])
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "%s-%s" % (c[0], c[1].get("n", "")))
+def test_teacher_forced_parity(case, mode):
+    name, kw, steps, width, chunks = case
+    p = wl.preset(name, **kw)
+    log("parity %s %s mode=%d W=%d C=%d steps=%d" % (name, kw, mode, width, chunks, steps))
+    net, o, cnt = teacher_forced_run(p, steps, mode, slice_width=width, spike_chunks=chunks)
+    assert cnt["spikes"] > 0
+    if p.plastic != PLASTIC_NONE:
+        assert cnt["rows"] > 0 and cnt["weights"] > 0
+        net.flush_plasticity()
+        compare_all_plastic_weights(net, o)
+        st = net.stats()
+        assert st["stdp_forced_rows"] > 0  # rows idle for 64 steps were forced
+    st = net.stats()
+    assert st["steps"] == steps
+    assert st["spikes"] == cnt["spikes"]
+
+
+@pytest.mark.parametrize("width,chunks,fanout", [(64, 1, 300), (2048, 2, 300),
+                                                 (16384, 1, 3000), (1024, 64, 300)])
+def test_slice_shapes(width, chunks, fanout):
+    """Segments from 1 to ~600 entries, one to many chunks, more spikes per
+    workgroup than one staging batch holds."""
+    p = wl.preset("stress", n=4000, p_or_fanout=fanout, p_fire=0.3 if chunks == 1 else 0.02)
+    log("slice shape W=%d C=%d F=%d" % (width, chunks, fanout))
+    net, o, _ = teacher_forced_run(p, 70, LDS, slice_width=width, spike_chunks=chunks)
+    net.flush_plasticity()
+    compare_all_plastic_weights(net, o)
+
+
+def test_three_part_calls_equal_step():
+    """update_neurons / update_plasticity / deliver_spikes / advance == step."""
+    p = wl.preset("stress", n=2000, p_or_fanout=100, p_fire=0.03)
+    a = gpu_net(p, slice_width=512)
+    b = gpu_net(p, slice_width=512)
+    for t in range(100):
+        a.step(1, LDS)
+        b.update_neurons()
+        b.update_plasticity()
+        b.deliver_spikes(LDS)
+        b.advance()
+    a.flush_plasticity()
+    b.flush_plasticity()
+    sa, sb = a.state(), b.state()
+    for key in ("hist", "input_exc", "t_last", "trace_pre", "trace_post"):
+        assert np.array_equal(to_np(sa[key]), to_np(sb[key])), key
+    assert np.array_equal(to_np(a.graph()["w"]), to_np(b.graph()["w"]))
+
+
+def test_out_of_order_calls_rejected():
+    p = wl.preset("stress", n=500, p_or_fanout=10, p_fire=0.03)
+    net = gpu_net(p, slice_width=128)
+    with pytest.raises(snn.SnnError) as e:
+        net.update_plasticity()
+    assert e.value.status == snn.SNN_ESTATE
+    with pytest.raises(snn.SnnError):
+        net.deliver_spikes(7)
+
+
+def test_silent_network():
+    """No spikes at all: empty lists, zero input, rows only forced."""
+    p = wl.preset("stress", n=1500, p_or_fanout=50, p_fire=0.0)
+    net, o, cnt = teacher_forced_run(p, 140, LDS, slice_width=512, spike_chunks=2)
+    assert cnt["spikes"] == 0
+    st = net.stats()
+    assert st["delivered_events"] == 0
+    assert st["stdp_forced_rows"] == 2 * 1500  # every row forced at t=63 and t=127
+    assert st["stdp_weights_written"] == 0
+    assert not to_np(net.state()["input_exc"]).any()
+
+
+@pytest.mark.parametrize("mode", [LDS, GLOBAL], ids=["lds", "global"])
+def test_all_spikes_hit_one_target(mode):
+    """Maximum atomic contention: 3000 sources, all edges into neuron 5."""
+    n = 3000
+    src = np.arange(n)
+    dst = np.full(n, 5)
+    w = np.full(n, 0.25, np.float32)  # sums of quarters are exact in fp32
+    p = wl.Preset(name="contention", n=n, n_exc=n, model=BERNOULLI_SOURCE,
+                  graph_kind=GRAPH_BERNOULLI, p_or_fanout=0, w_exc=0, w_inh=0,
+                  p_fire=0.5, slice_width=1024)
+    net = gpu_net(p, build=False, slice_width=1024, spike_chunks=3)
+    net.build_edges(src, dst, w)
+    o = oracle_net(p, build=False)
+    o.build_edges(src, dst, w)
+    for t in range(20):
+        o.step()
+        net.step(1, mode)
+        compare_step(net, o, "contention", t, check_rows=False)
+        a = to_np(net.state()["input_exc"])
+        assert a[5] == o.input()[0][5] and a[5] > 100
+
+
+def test_weights_span_sign_and_cancel():
+    """Brunel weights +0.1/-0.5 summed into one input: cancellation cases."""
+    p = wl.preset("brunel", n=3000, n_exc=2400, delay=1)
+    net, o, cnt = teacher_forced_run(p, 150, LDS, slice_width=64, spike_chunks=1)
+    assert cnt["spikes"] > 100
+
+
+def test_checkpoint_restore_resumes_identically():
+    """get_state -> copy -> set_state into a fresh network continues identically
+    (spikes are Bernoulli draws, so no teacher forcing is needed)."""
+    import torch
+    p = wl.preset("stress", n=2500, p_or_fanout=100, p_fire=0.03, delay=4)
+    a = gpu_net(p, slice_width=512)
+    a.step(90, LDS)
+    s = a.state()
+    snap = {k: v.clone() for k, v in s.items() if isinstance(v, torch.Tensor)}
+    w_snap = a.graph()["w"].clone()
+    a.step(50, LDS)
+    b = gpu_net(p, slice_width=512)
+    b.graph()["w"].copy_(w_snap)
+    keys = ("v", "refractory", "i_exc", "i_inh", "hist", "trace_post", "t_last", "trace_pre",
+            "input_exc", "ring_lists", "ring_counts")
+    b.set_state(int(s["t"]), **{k: snap[k] for k in keys})
+    b.step(50, LDS)
+    sa, sb = a.state(), b.state()
+    for k in ("hist", "t_last", "trace_pre", "trace_post"):
+        assert np.array_equal(to_np(sa[k]), to_np(sb[k])), k
+    assert_close(to_np(sb["input_exc"]), to_np(sa["input_exc"]), "input after restore")
+    assert_close(to_np(b.graph()["w"]), to_np(a.graph()["w"]), "weights after restore")

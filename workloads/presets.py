@@ -122,6 +122,8 @@ PRESETS = {
 
 def preset(name, **overrides):
     p = PRESETS[name]
+    if "n" in overrides and "n_exc" not in overrides and p.n_exc == p.n:
+        overrides["n_exc"] = overrides["n"]   # all-excitatory presets stay so
     return replace(p, **overrides) if overrides else p
 
 
