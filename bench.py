@@ -38,6 +38,9 @@ def parse():
     ap.add_argument("--mode", choices=["lds", "global"], default="lds")
     ap.add_argument("--slice-width", type=int, default=None)
     ap.add_argument("--chunks", type=int, default=None)
+    ap.add_argument("--stdp-layout", choices=["rows", "slice"], default="rows")
+    ap.add_argument("--stdp-mult", type=int, default=0)
+    ap.add_argument("--stdp-chunks", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-instrumented", action="store_true",
@@ -47,7 +50,8 @@ def parse():
 
 def kernel_source_digest():
     h = hashlib.sha256()
-    for f in ("snn_kernels.hip", "snn_api.hip", "snn_internal.h"):
+    for f in ("k_neuron.hip", "k_synapse.hip", "k_graph.hip", "snn_device.h", "snn_api.hip",
+              "snn_internal.h"):
         with open(os.path.join(ROOT, "paper_2107_04092_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -144,8 +148,9 @@ def main():
     stream = torch.cuda.current_stream(dev)
 
     cfg = snn.config_from_preset(p, wl.poisson_cdf_table(p.poisson_mu),
-                                 slice_width=width,
-                                 spike_chunks=chunks)
+                                 slice_width=width, spike_chunks=chunks,
+                                 stdp_slice_mult=args.stdp_mult, stdp_chunks=args.stdp_chunks,
+                                 stdp_layout=0 if args.stdp_layout == "rows" else 1)
     t0 = time.time()
     net = snn.Network(cfg, stream=stream, device=dev)
     e = net.build_random(p.graph_kind, p.p_or_fanout, p.w_exc, p.w_inh)
@@ -247,7 +252,8 @@ def main():
                            p.p_or_fanout, e, p.delay,
                            ["none", "exc-exc", "all"][p.plastic], args.mode, width, chunks),
             "n": p.n, "synapses": e, "slice_width": width, "spike_chunks": chunks,
-            "delivery": args.mode, "seed": p.seed,
+            "delivery": args.mode, "stdp_layout": args.stdp_layout,
+            "stdp_slice_mult": args.stdp_mult, "stdp_chunks": args.stdp_chunks, "seed": p.seed,
         },
         "roofline": roofline,
         "cpu_baseline": cpu,

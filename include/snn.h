@@ -103,6 +103,17 @@ typedef struct snn_config {
     int32_t spike_chunks; /* C in 1..64: workgroups that share one slice, each
                              taking 1/C of the spike list (partial sums are
                              added by the next neuron update) */
+    int32_t stdp_slice_mult; /* STDP target groups span stdp_slice_mult * W
+                             neurons (0 = about 4096); their history words and
+                             post traces (12 B each) are staged in LDS */
+    int32_t stdp_chunks;  /* workgroups sharing one STDP target group, each
+                             taking 1/stdp_chunks of the rows (0 = auto) */
+    int32_t stdp_layout;  /* forced rows (idle for 64 steps): 0 = row-wise, a
+                             wave per row, histories gathered from L2 only for
+                             targets that spiked within 64 steps (a recency
+                             bitmap in LDS), run in the same launch as
+                             delivery by snn_step; 1 = slice-organised, the
+                             target group's histories staged in LDS */
     int32_t neuron_model; /* enum snn_neuron_model */
     int32_t plastic;      /* enum snn_plasticity */
     int32_t poisson_len;  /* entries used in poisson_cdf (0 = no external drive) */
@@ -140,17 +151,23 @@ typedef struct snn_state_view {
     int32_t *spike_count;   /* device int32 */
     int32_t *tx_list;       /* spikes transmitted by the last delivery step */
     int32_t *tx_count;      /* device int32 */
-    int32_t *stdp_rows;     /* rows brought up to date by the last STDP step */
+    int32_t *stdp_rows;     /* plastic rows forced by the 64-step window at the
+                               last neuron update (brought up to date by
+                               snn_update_plasticity); transmitting plastic
+                               rows are brought up to date by delivery */
     int32_t *stdp_row_count;/* device int32 */
     int32_t *ring_lists;    /* delay ring: D x n spike lists, slot = step mod D */
     int32_t *ring_counts;   /* delay ring: D counts */
 } snn_state_view;
 
-/* Device views of the graph (inside the bound graph buffer / workspace). */
+/* Device views of the graph (inside the bound graph buffer / workspace).
+ * Each synapse is stored as a (target, weight) pair, so the target of edge e
+ * is col[e * edge_stride] and its weight w[e * edge_stride]. */
 typedef struct snn_graph_view {
     int64_t n_edges;
     int32_t n_slices;      /* S = ceil(n / W) */
-    int64_t *row_ptr;      /* n+1 entries: row k is col[row_ptr[k] .. row_ptr[k+1]) */
+    int32_t edge_stride;   /* distance between consecutive edges, in 4-byte words (2) */
+    int64_t *row_ptr;      /* n+1 entries: row k is edges row_ptr[k] .. row_ptr[k+1]-1 */
     int32_t *col;          /* targets, ascending within each row */
     float *w;              /* weights, 1:1 with col */
     int32_t *pivots;       /* n x (S+1), row-relative: entries pivots[k][s] ..
@@ -206,8 +223,8 @@ snn_status snn_bind_workspace(snn_ctx *ctx, void *device_ptr, size_t bytes);
 snn_status snn_graph_count_random(snn_ctx *ctx, int32_t kind, double p_or_fanout,
                                   int64_t *n_edges);
 
-/* Bytes of the graph buffer for n_edges edges: targets, weights and the
- * n x (S+1) pivot table. */
+/* Bytes of the graph buffer for n_edges edges: (target, weight) pairs and
+ * the n x (S+1) pivot table. */
 snn_status snn_graph_size(const snn_ctx *ctx, int64_t n_edges, size_t *bytes);
 
 /* Binds a device graph buffer of at least snn_graph_size(n_edges) bytes. */
@@ -229,18 +246,21 @@ snn_status snn_build_graph_edges(snn_ctx *ctx, const int32_t *src, const int32_t
 
 /* Part (1) of step t (Sec. I): integrates every neuron with its input A(t),
  * writes the firing mask, the spike list into ring slot t mod D, shifts the
- * histories, updates the post-synaptic trace, and lists the plastic rows to
- * update at t (rows transmitting at t, and rows idle for 64 steps). */
+ * histories, updates the post-synaptic trace, lists the plastic rows idle
+ * for 64 steps (forced), and snapshots the plastic rows to update at t. */
 snn_status snn_update_neurons(snn_ctx *ctx);
 
-/* Part (2) of step t (Sec. III-A, Fig. 2(c)): brings the listed plastic rows
- * up to step t (lazy), visiting only set history bits (event-driven); rows
- * transmitting at t see their pre-synaptic spike at t. */
+/* Part (2) of step t (Sec. III-A, Fig. 2(c)) for the forced rows: brings
+ * them up to step t (lazy), visiting only set history bits (event-driven).
+ * Rows transmitting at t are brought up to date by snn_deliver_spikes,
+ * immediately before their weights are delivered. */
 snn_status snn_update_plasticity(snn_ctx *ctx);
 
 /* Part (3) of step t: delivers the spikes emitted at t-D+1 (ring slot
- * (t-D+1) mod D) with the weights as they stand after part (2), producing
- * A(t+1). mode is an enum snn_delivery value. */
+ * (t-D+1) mod D), producing A(t+1). Each transmitting plastic row is first
+ * brought up to step t, with its pre-synaptic spike at t (the remainder of
+ * part (2)); with SNN_DELIVER_LDS_SLICE inside the slice kernel, so the row
+ * is read once. mode is an enum snn_delivery value. */
 snn_status snn_deliver_spikes(snn_ctx *ctx, int32_t mode);
 
 /* Ends step t (t <- t+1). */

@@ -22,7 +22,11 @@ struct snn_ctx {
 
     // derived configuration
     int32_t n = 0, nw = 0, nblk = 0, nacc = 1, n_slices = 0, chunks = 1, delay = 1;
-    int32_t n_plastic_rows = 0, ref_steps = 0, dlv_blocks = 0, stdp_blocks = 0;
+    int32_t n_plastic_rows = 0, ref_steps = 0, dlv_blocks = 0;
+    int32_t stdp_mult = 1, stdp_width = 0, stdp_groups = 0, stdp_chunks = 1, stdp_grid = 0;
+    int32_t info_blocks = 1, syn_slots = 1;
+    bool fused = false;       // snn_step runs delivery + forced-row STDP as one launch
+    size_t fused_lds = 0;
     float k_m = 0, v_th = 0, v_reset = 0, v_inf = 0, d_e = 0, d_i = 0, j_ext = 0;
     float d_minus = 0, c_pot = 0, c_dep = 0, mu = 0;
     float dpow[65] = {};
@@ -35,19 +39,22 @@ struct snn_ctx {
     long long *apart = nullptr;  // fixed-point partial inputs [C][nacc][n]
     float *ain = nullptr;        // fp32 input [nacc][n] (teacher forcing / views)
     int32_t *ref = nullptr, *t_last = nullptr, *pend = nullptr;
-    uint64_t *hist = nullptr, *mask = nullptr, *rmask = nullptr;
-    int32_t *blk_spk = nullptr, *blk_row = nullptr, *ring = nullptr, *ring_cnt = nullptr;
+    uint64_t *hist = nullptr, *mask = nullptr, *txmask = nullptr, *fmask = nullptr;
+    uint64_t *recent = nullptr;
+    int32_t *blk_spk = nullptr, *blk_tx = nullptr, *blk_f = nullptr;
+    int32_t *ring = nullptr, *ring_cnt = nullptr;
     int32_t *rows = nullptr, *row_cnt = nullptr, *err_flag = nullptr, *maxlen = nullptr;
     int64_t *row_ptr = nullptr, *scratch = nullptr, *bsum = nullptr;
-    int64_t *gstats = nullptr, *stdp_stats = nullptr, *dlv_stats = nullptr;
+    int64_t *gstats = nullptr, *info_stats = nullptr, *syn_stats = nullptr, *dlv_stats = nullptr;
+    RowInfo *info = nullptr, *txinfo = nullptr;
     int32_t dlv_slots = 0;
 
     // graph
     uint8_t *g = nullptr;
     size_t g_bytes = 0;
     int64_t n_edges = -1, counted_edges = -1;
-    int32_t *col = nullptr, *piv = nullptr;
-    float *w = nullptr;
+    Edge *edges = nullptr;
+    int32_t *piv = nullptr;
     int graph_state = 0;  // 0 none, 1 counted, 2 buffer bound, 3 built
     int32_t counted_kind = -1;
     double counted_p = 0.0;
@@ -105,6 +112,12 @@ snn_status validate(snn_ctx *c, const snn_config &k)
                     nacc);
     if (k.spike_chunks < 1 || k.spike_chunks > 64)
         return fail(c, SNN_EINVAL, "spike_chunks must be in [1, 64]");
+    if (k.stdp_slice_mult < 0 || k.stdp_slice_mult > 4096)
+        return fail(c, SNN_EINVAL, "stdp_slice_mult must be in [0, 4096]");
+    if (k.stdp_chunks < 0 || k.stdp_chunks > 1024)
+        return fail(c, SNN_EINVAL, "stdp_chunks must be in [0, 1024]");
+    if (k.stdp_layout < 0 || k.stdp_layout > 1)
+        return fail(c, SNN_EINVAL, "stdp_layout must be 0 or 1");
     const int64_t slices = (k.n + k.slice_width - 1) / k.slice_width;
     if (slices * k.spike_chunks > (1 << 20))
         return fail(c, SNN_EINVAL, "slices * spike_chunks must not exceed 2^20");
@@ -172,9 +185,8 @@ void derive(snn_ctx *c)
     }
     const int64_t work = (int64_t)c->n_slices * c->chunks;
     c->dlv_blocks = (int32_t)((work + 7) / 8 * 8);
-    const int64_t sb = (c->n_plastic_rows + 3) / 4;
-    c->stdp_blocks = (int32_t)(sb < 1 ? 1 : sb > kStdpMaxBlocks ? kStdpMaxBlocks : sb);
     c->dlv_slots = c->dlv_blocks > kGlobalMaxBlocks ? c->dlv_blocks : kGlobalMaxBlocks;
+    c->info_blocks = c->nblk;  // statistics slots of the compaction / flush snapshots
 }
 
 // Workspace plan: a bump allocator over the caller's buffer.
@@ -205,9 +217,12 @@ void plan_workspace(snn_ctx *c, uint8_t *base)
     c->apart = p.take<long long>((int64_t)c->chunks * c->nacc * n);
     c->ain = p.take<float>((int64_t)c->nacc * n);
     c->mask = p.take<uint64_t>(c->nw);
-    c->rmask = p.take<uint64_t>(c->nw);
+    c->txmask = p.take<uint64_t>(c->nw);
+    c->fmask = p.take<uint64_t>(c->nw);
+    c->recent = p.take<uint64_t>(c->nw);
     c->blk_spk = p.take<int32_t>(c->nblk);
-    c->blk_row = p.take<int32_t>(c->nblk);
+    c->blk_tx = p.take<int32_t>(c->nblk);
+    c->blk_f = p.take<int32_t>(c->nblk);
     c->ring = p.take<int32_t>((int64_t)c->delay * n);
     c->ring_cnt = p.take<int32_t>(c->delay);
     c->rows = p.take<int32_t>(n);
@@ -219,8 +234,11 @@ void plan_workspace(snn_ctx *c, uint8_t *base)
     c->scratch = p.take<int64_t>(n + 1);
     c->bsum = p.take<int64_t>((n + 1 + 1023) / 1024 + 1);
     c->gstats = p.take<int64_t>(kGFields);
-    c->stdp_stats = p.take<int64_t>((int64_t)kStdpMaxBlocks * kStFields);
-    c->dlv_stats = p.take<int64_t>(c->dlv_slots);
+    c->info = p.take<RowInfo>(c->n_plastic_rows > 0 ? c->n_plastic_rows : 1);
+    c->txinfo = p.take<RowInfo>(n);  // transmitted rows: start, and plasticity snapshot
+    c->info_stats = p.take<int64_t>((int64_t)c->info_blocks * kStFields);
+    c->syn_stats = p.take<int64_t>(c->syn_slots);
+    c->dlv_stats = p.take<int64_t>(2 * (int64_t)c->dlv_slots);
     c->ws_need = p.off;
 }
 
@@ -241,8 +259,7 @@ GraphArgs graph_args(snn_ctx *c)
 {
     GraphArgs a{};
     a.row_ptr = c->row_ptr;
-    a.col = c->col;
-    a.w = c->w;
+    a.edges = c->edges;
     a.piv = c->piv;
     a.pend = c->pend;
     a.err = c->err_flag;
@@ -266,8 +283,9 @@ snn_status zero_stats(snn_ctx *c)
 {
     hipError_t e = launch_fill_i64(c->stream, c->gstats, kGFields, 0);
     if (e == hipSuccess)
-        e = launch_fill_i64(c->stream, c->stdp_stats, (int64_t)kStdpMaxBlocks * kStFields, 0);
-    if (e == hipSuccess) e = launch_fill_i64(c->stream, c->dlv_stats, c->dlv_slots, 0);
+        e = launch_fill_i64(c->stream, c->info_stats, (int64_t)c->info_blocks * kStFields, 0);
+    if (e == hipSuccess) e = launch_fill_i64(c->stream, c->syn_stats, c->syn_slots, 0);
+    if (e == hipSuccess) e = launch_fill_i64(c->stream, c->dlv_stats, 2 * (int64_t)c->dlv_slots, 0);
     c->steps_done = 0;
     return check_hip(c, e, "reset statistics");
 }
@@ -320,9 +338,12 @@ snn_status launch_step_neurons(snn_ctx *c)
     a.part_stride = (int64_t)c->nacc * c->n;
     a.input_forced = c->input_forced;
     a.mask = c->mask;
-    a.rmask = c->rmask;
+    a.txmask = c->txmask;
+    a.fmask = c->fmask;
+    a.recent = c->recent;
     a.blk_spk = c->blk_spk;
-    a.blk_row = c->blk_row;
+    a.blk_tx = c->blk_tx;
+    a.blk_f = c->blk_f;
     a.t = c->t;
     a.n = c->n;
     a.n_exc = c->cfg.n_exc;
@@ -348,9 +369,11 @@ snn_status launch_step_neurons(snn_ctx *c)
     c->input_forced = 0;  // the input has been consumed; the next comes from delivery
     CompactArgs b{};
     b.mask = c->mask;
-    b.rmask = c->rmask;
+    b.txmask = c->txmask;
+    b.fmask = c->fmask;
     b.blk_spk = c->blk_spk;
-    b.blk_row = c->blk_row;
+    b.blk_tx = c->blk_tx;
+    b.blk_f = c->blk_f;
     b.spk_list = c->ring + (int64_t)ring_slot(c, c->t) * c->n;
     b.spk_cnt = c->ring_cnt + ring_slot(c, c->t);
     b.row_list = c->rows;
@@ -358,50 +381,111 @@ snn_status launch_step_neurons(snn_ctx *c)
     b.gstats = c->gstats;
     b.n = c->n;
     b.nw = c->nw;
+    b.n_plastic_rows = c->n_plastic_rows;
+    b.info = c->info;
+    b.txinfo = c->txinfo;
+    b.row_ptr = c->row_ptr;
+    b.pend = c->pend;
+    b.hist = c->hist;
+    b.t_last = c->t_last;
+    b.xpre = c->xpre;
+    b.err = c->err_flag;
+    b.info_stats = c->n_plastic_rows > 0 ? c->info_stats : nullptr;
+    b.t = c->t;
+    b.dm1 = c->delay - 1;
+    for (int q = 0; q <= 64; ++q) b.dpow[q] = c->dpow[q];
     st = check_hip(c, launch_compact(c->stream, b), "compaction kernel");
     if (st) return st;
     c->last_neuron_t = c->t;
     return SNN_OK;
 }
 
-StdpArgs stdp_args(snn_ctx *c)
+size_t dlv_lds_bytes(const snn_ctx *c)
+{
+    size_t b = (size_t)c->cfg.slice_width * c->nacc * sizeof(long long);
+    if (c->n_plastic_rows > 0)
+        b += (size_t)c->cfg.slice_width * (sizeof(uint64_t) + sizeof(float));
+    return b;
+}
+
+// Arguments of the synapse pass over the forced rows (flush: all rows).
+StdpArgs stdp_args(snn_ctx *c, bool flush)
 {
     StdpArgs a{};
-    a.row_ptr = c->row_ptr;
-    a.pend = c->pend;
-    a.col = c->col;
-    a.w = c->w;
-    a.hist = c->hist;
-    a.ypost = c->ypost;
+    a.info = c->info;
+    a.row_cnt = flush ? nullptr : c->row_cnt;
+    a.n_rows_all = c->n_plastic_rows;
     a.t_last = c->t_last;
     a.xpre = c->xpre;
-    a.rows = c->rows;
-    a.row_cnt = c->row_cnt;
-    a.n_rows_all = c->n_plastic_rows;
-    a.dm1 = c->delay - 1;
-    a.t = c->t;
+    a.t = flush ? c->t - 1 : c->t;
+    a.edges = c->edges;
+    a.piv = c->piv;
+    a.hist = c->hist;
+    a.ypost = c->ypost;
+    a.n = c->n;
+    a.n_slices = c->n_slices;
+    a.mult = c->stdp_mult;
+    a.width = c->stdp_width;
+    a.n_groups = c->stdp_groups;
+    a.chunks = c->stdp_chunks;
+    a.n_work = c->stdp_groups * c->stdp_chunks;
+    a.target_limit = c->cfg.plastic == SNN_PLASTIC_EXC_EXC ? c->cfg.n_exc : c->n;
     a.c_pot = c->c_pot;
     a.c_dep = c->c_dep;
     a.mu = c->mu;
-    a.stats = c->stdp_stats;
-    a.err = c->err_flag;
+    a.stats = c->syn_stats;
+    // the recency bitmap is rebuilt by every neuron update; a flush follows one
+    a.recent = c->nw <= kRecentMaxWords && c->last_neuron_t >= 0 ? c->recent : nullptr;
+    a.nw = c->nw;
     for (int q = 0; q <= 64; ++q) a.dpow[q] = c->dpow[q];
     return a;
+}
+
+// The plasticity part for rows forced by the 64-step history window (their
+// snapshots were taken by the compaction kernel); rows transmitting at t are
+// brought up to date by the delivery part. A flush (every plastic row up to
+// step t-1, no pre-synaptic spike) takes its snapshots first. The synapse
+// pass commits t_last and the pre traces.
+snn_status launch_plasticity(snn_ctx *c, bool flush)
+{
+    if (flush) {
+        RowInfoArgs r{};
+        r.rows = nullptr;
+        r.row_cnt = nullptr;
+        r.n_rows_all = c->n_plastic_rows;
+        r.dm1 = c->delay - 1;
+        r.t = c->t - 1;
+        r.row_ptr = c->row_ptr;
+        r.pend = c->pend;
+        r.hist = c->hist;
+        r.t_last = c->t_last;
+        r.xpre = c->xpre;
+        r.info = c->info;
+        r.err = c->err_flag;
+        r.stats = c->info_stats;
+        for (int q = 0; q <= 64; ++q) r.dpow[q] = c->dpow[q];
+        snn_status st = check_hip(c, launch_row_info(c->stream, r, c->n_plastic_rows),
+                                  "STDP row snapshot kernel");
+        if (st) return st;
+    }
+    StdpArgs a = stdp_args(c, flush);
+    if (c->cfg.stdp_layout == 0)
+        return check_hip(c, launch_stdp_rows(c->stream, a, kStdpRowsBlocks), "STDP kernel");
+    const size_t lds = (size_t)c->stdp_width * (sizeof(uint64_t) + sizeof(float));
+    return check_hip(c, launch_stdp(c->stream, a, c->stdp_grid, lds), "STDP kernel");
 }
 
 snn_status launch_step_plasticity(snn_ctx *c)
 {
     if (c->n_plastic_rows == 0) return SNN_OK;
-    StdpArgs a = stdp_args(c);
-    return check_hip(c, launch_stdp(c->stream, a, c->stdp_blocks), "STDP kernel");
+    return launch_plasticity(c, false);
 }
 
-snn_status launch_step_delivery(snn_ctx *c, int32_t mode)
+DeliverArgs deliver_args(snn_ctx *c)
 {
     DeliverArgs a{};
     a.row_ptr = c->row_ptr;
-    a.col = c->col;
-    a.w = c->w;
+    a.edges = c->edges;
     a.piv = c->piv;
     const int slot = ring_slot(c, c->t - (c->delay - 1));
     a.list = c->ring + (int64_t)slot * c->n;
@@ -417,10 +501,27 @@ snn_status launch_step_delivery(snn_ctx *c, int32_t mode)
     a.nacc = c->nacc;
     a.n_work = c->n_slices * c->chunks;
     a.stats = c->dlv_stats;
+    a.plastic = c->n_plastic_rows > 0;
+    a.txinfo = c->txinfo;
+    a.hist = c->hist;
+    a.ypost = c->ypost;
+    a.t_last = c->t_last;
+    a.xpre = c->xpre;
+    a.t = c->t;
+    a.c_pot = c->c_pot;
+    a.c_dep = c->c_dep;
+    a.mu = c->mu;
+    for (int q = 0; q <= 64; ++q) a.dpow[q] = c->dpow[q];
+    return a;
+}
+
+snn_status launch_step_delivery(snn_ctx *c, int32_t mode)
+{
+    DeliverArgs a = deliver_args(c);
     snn_status st;
     if (mode == SNN_DELIVER_LDS_SLICE) {
-        const size_t lds = (size_t)c->cfg.slice_width * c->nacc * sizeof(long long);
-        st = check_hip(c, launch_deliver_lds(c->stream, a, c->dlv_blocks, lds),
+        // the transmitting rows' plasticity is fused into slice delivery
+        st = check_hip(c, launch_deliver_lds(c->stream, a, c->dlv_blocks, dlv_lds_bytes(c)),
                        "LDS delivery kernel");
         if (st) return st;
         c->n_parts = c->chunks;
@@ -428,17 +529,40 @@ snn_status launch_step_delivery(snn_ctx *c, int32_t mode)
         // with one chunk each workgroup owns its slice and stores the fp32 input
         c->input_forced = c->chunks == 1 ? 1 : 0;
         return SNN_OK;
-    } else {
-        st = check_hip(c, launch_fill_ll(c->stream, c->apart, a.part_stride, 0),
-                       "clear input");
-        if (st) return st;
-        st = check_hip(c, launch_deliver_global(c->stream, a, kGlobalMaxBlocks),
-                       "global delivery kernel");
-        if (st) return st;
-        c->n_parts = 1;
     }
+    if (a.plastic) {
+        // bring the transmitting rows up to date first (row-wise, L2 gathers)
+        StdpArgs r = stdp_args(c, false);
+        r.info = c->txinfo;
+        r.row_cnt = a.cnt;
+        st = check_hip(c, launch_stdp_rows(c->stream, r, kStdpRowsBlocks),
+                       "STDP of transmitting rows");
+        if (st) return st;
+    }
+    st = check_hip(c, launch_fill_ll(c->stream, c->apart, a.part_stride, 0), "clear input");
+    if (st) return st;
+    st = check_hip(c, launch_deliver_global(c->stream, a, kGlobalMaxBlocks),
+                   "global delivery kernel");
+    if (st) return st;
+    c->n_parts = 1;
     c->input_forced = 0;
     c->last_deliver_t = c->t;
+    return SNN_OK;
+}
+
+// Parts (2) and (3) of a step in one launch (slice delivery with the
+// transmitting rows' plasticity, plus the forced rows row-wise).
+snn_status launch_step_synapse_pass(snn_ctx *c)
+{
+    DeliverArgs a = deliver_args(c);
+    StdpArgs f = stdp_args(c, false);
+    snn_status st = check_hip(c, launch_synapse_pass(c->stream, a, f, c->dlv_blocks,
+                                                     kFusedStdpBlocks, c->fused_lds),
+                              "synapse pass kernel");
+    if (st) return st;
+    c->n_parts = c->chunks;
+    c->last_deliver_t = c->t;
+    c->input_forced = c->chunks == 1 ? 1 : 0;
     return SNN_OK;
 }
 
@@ -477,13 +601,54 @@ snn_status snn_create(const snn_config *cfg, void *hip_stream, snn_ctx **out)
         hipSuccess)
         return fail(c, SNN_EDEVICE, "cannot query the LDS size");
     const int stat = deliver_lds_static_bytes();
-    if (stat < 0) return fail(c, SNN_EDEVICE, "cannot query the delivery kernel");
-    const int64_t need = (int64_t)cfg->slice_width * 8 * (cfg->neuron_model == SNN_LIF_CUBA ? 2 : 1);
+    const int stat_stdp = stdp_static_bytes();
+    if (stat < 0 || stat_stdp < 0) return fail(c, SNN_EDEVICE, "cannot query the kernels");
+    int64_t need = (int64_t)cfg->slice_width * 8 * (cfg->neuron_model == SNN_LIF_CUBA ? 2 : 1);
+    if (cfg->plastic != SNN_PLASTIC_NONE) need += (int64_t)cfg->slice_width * 12;
     if (need + stat > lds_max)
         return fail(c, SNN_EINVAL,
-                    "slice accumulator needs %lld B of LDS besides %d B of staging; the "
-                    "device allows %d in total", (long long)need, stat, lds_max);
+                    "slice delivery needs %lld B of LDS (accumulator%s) besides %d B of "
+                    "staging; the device allows %d", (long long)need,
+                    cfg->plastic != SNN_PLASTIC_NONE ? ", histories and post traces" : "", stat,
+                    lds_max);
     derive(c);
+    if (c->n_plastic_rows > 0) {
+        // STDP target groups: mult * W neurons, staged at 12 B each in LDS
+        const int64_t per = sizeof(uint64_t) + sizeof(float);
+        int mult = cfg->stdp_slice_mult;
+        if (mult == 0) {
+            mult = 4096 / cfg->slice_width;
+            if (mult < 1) mult = 1;
+            if (mult > c->n_slices) mult = c->n_slices;
+            while (mult > 1 && (int64_t)mult * cfg->slice_width * per + stat_stdp > lds_max) --mult;
+        }
+        if ((int64_t)mult * cfg->slice_width * per + stat_stdp > lds_max)
+            return fail(c, SNN_EINVAL,
+                        "STDP staging of %d x %d neurons needs %lld B of LDS; the device "
+                        "allows %d", mult, cfg->slice_width,
+                        (long long)(mult * cfg->slice_width * per + stat_stdp), lds_max);
+        c->stdp_mult = mult;
+        c->stdp_width = mult * cfg->slice_width;
+        c->stdp_groups = (c->n_slices + mult - 1) / mult;
+        int chunks = cfg->stdp_chunks;
+        if (chunks == 0) {
+            chunks = (512 + c->stdp_groups - 1) / c->stdp_groups;
+            if (chunks > 256) chunks = 256;
+        }
+        c->stdp_chunks = chunks;
+        const int64_t work = (int64_t)c->stdp_groups * chunks;
+        if (work > (1 << 20)) return fail(c, SNN_EINVAL, "too many STDP work items");
+        c->stdp_grid = (int32_t)((work + 7) / 8 * 8);
+        c->syn_slots = c->stdp_grid > kStdpRowsBlocks ? c->stdp_grid : kStdpRowsBlocks;
+        if (c->syn_slots < kFusedStdpBlocks) c->syn_slots = kFusedStdpBlocks;
+        // one launch for delivery and the forced rows when both fit in LDS
+        const int stat_f = synapse_pass_static_bytes();
+        size_t dyn = (size_t)cfg->slice_width * c->nacc * 8 + (size_t)cfg->slice_width * 12;
+        const size_t bm = c->nw <= kRecentMaxWords ? (size_t)c->nw * 8 : 0;
+        if (bm > dyn) dyn = bm;
+        c->fused = cfg->stdp_layout == 0 && stat_f >= 0 && (int64_t)dyn + stat_f <= lds_max;
+        c->fused_lds = dyn;
+    }
     plan_workspace(c, nullptr);
     return SNN_OK;
 }
@@ -534,7 +699,7 @@ snn_status snn_graph_count_random(snn_ctx *c, int32_t kind, double p_or_fanout,
     snn_status st = require_ws(c);
     if (st) return st;
     GraphArgs a = graph_args(c);
-    a.col = nullptr;
+    a.edges = nullptr;
     hipError_t e;
     if (kind == SNN_GRAPH_BERNOULLI) {
         if (!(p_or_fanout >= 0 && p_or_fanout <= 1))
@@ -571,7 +736,7 @@ snn_status snn_graph_count_random(snn_ctx *c, int32_t kind, double p_or_fanout,
 snn_status snn_graph_size(const snn_ctx *c, int64_t n_edges, size_t *bytes)
 {
     if (!c || !bytes || n_edges < 0) return SNN_EINVAL;
-    *bytes = align_up((size_t)n_edges * 4) * 2 +
+    *bytes = align_up((size_t)n_edges * sizeof(Edge)) +
              align_up((size_t)c->n * (size_t)(c->n_slices + 1) * 4);
     return SNN_OK;
 }
@@ -593,9 +758,8 @@ snn_status snn_bind_graph(snn_ctx *c, void *device_ptr, size_t bytes, int64_t n_
     c->g = (uint8_t *)device_ptr;
     c->g_bytes = bytes;
     c->n_edges = n_edges;
-    c->col = (int32_t *)c->g;
-    c->w = (float *)(c->g + align_up((size_t)n_edges * 4));
-    c->piv = (int32_t *)(c->g + 2 * align_up((size_t)n_edges * 4));
+    c->edges = (Edge *)c->g;
+    c->piv = (int32_t *)(c->g + align_up((size_t)n_edges * sizeof(Edge)));
     if (c->graph_state != 1) c->counted_kind = -1;
     c->graph_state = 2;
     return SNN_OK;
@@ -723,10 +887,15 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
     if (n_steps < 0) return fail(c, SNN_EINVAL, "n_steps must be >= 0");
     if (mode != SNN_DELIVER_LDS_SLICE && mode != SNN_DELIVER_GLOBAL_ATOMIC)
         return fail(c, SNN_EINVAL, "unknown delivery mode %d", mode);
+    const bool fused = mode == SNN_DELIVER_LDS_SLICE && c->fused && c->n_plastic_rows > 0;
     for (int32_t q = 0; q < n_steps; ++q) {
         if ((st = launch_step_neurons(c))) return st;
-        if ((st = launch_step_plasticity(c))) return st;
-        if ((st = launch_step_delivery(c, mode))) return st;
+        if (fused) {
+            if ((st = launch_step_synapse_pass(c))) return st;
+        } else {
+            if ((st = launch_step_plasticity(c))) return st;
+            if ((st = launch_step_delivery(c, mode))) return st;
+        }
         c->t += 1;
         c->steps_done += 1;
     }
@@ -739,10 +908,7 @@ snn_status snn_flush_plasticity(snn_ctx *c)
     snn_status st = require_graph(c);
     if (st) return st;
     if (c->n_plastic_rows == 0 || c->t == 0) return SNN_OK;
-    StdpArgs a = stdp_args(c);
-    a.rows = nullptr;
-    a.t = c->t - 1;
-    return check_hip(c, launch_stdp(c->stream, a, c->stdp_blocks), "STDP flush");
+    return launch_plasticity(c, true);
 }
 
 snn_status snn_get_state(snn_ctx *c, snn_state_view *out)
@@ -818,8 +984,9 @@ snn_status snn_get_graph(const snn_ctx *c, snn_graph_view *out)
     out->n_edges = c->n_edges;
     out->n_slices = c->n_slices;
     out->row_ptr = c->row_ptr;
-    out->col = c->col;
-    out->w = c->w;
+    out->col = &c->edges->col;
+    out->w = &c->edges->w;
+    out->edge_stride = (int32_t)(sizeof(Edge) / sizeof(int32_t));
     out->pivots = c->piv;
     out->plastic_end = c->pend;
     return SNN_OK;
@@ -830,15 +997,18 @@ snn_status snn_get_stats(snn_ctx *c, snn_stats *out)
     if (!c || !out) return SNN_EINVAL;
     snn_status st = require_ws(c);
     if (st) return st;
-    std::vector<int64_t> g(kGFields), sd((size_t)kStdpMaxBlocks * kStFields),
-        dv((size_t)c->dlv_slots);
+    std::vector<int64_t> g(kGFields), si((size_t)c->info_blocks * kStFields),
+        sy((size_t)c->syn_slots), dv(2 * (size_t)c->dlv_slots);
     int32_t err = 0;
     hipError_t e = hipMemcpyAsync(g.data(), c->gstats, g.size() * 8, hipMemcpyDeviceToHost,
                                   c->stream);
     if (e == hipSuccess)
         e = hipMemcpyAsync(&err, c->err_flag, sizeof err, hipMemcpyDeviceToHost, c->stream);
     if (e == hipSuccess)
-        e = hipMemcpyAsync(sd.data(), c->stdp_stats, sd.size() * 8, hipMemcpyDeviceToHost,
+        e = hipMemcpyAsync(si.data(), c->info_stats, si.size() * 8, hipMemcpyDeviceToHost,
+                           c->stream);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(sy.data(), c->syn_stats, sy.size() * 8, hipMemcpyDeviceToHost,
                            c->stream);
     if (e == hipSuccess)
         e = hipMemcpyAsync(dv.data(), c->dlv_stats, dv.size() * 8, hipMemcpyDeviceToHost,
@@ -850,13 +1020,16 @@ snn_status snn_get_stats(snn_ctx *c, snn_stats *out)
     out->steps = c->steps_done;
     out->spikes = g[kGSpikes];
     out->device_errors = err;
-    for (int b = 0; b < kStdpMaxBlocks; ++b) {
-        out->stdp_rows += sd[(size_t)b * kStFields + kStRows];
-        out->stdp_forced_rows += sd[(size_t)b * kStFields + kStForced];
-        out->stdp_synapse_updates += sd[(size_t)b * kStFields + kStSyn];
-        out->stdp_weights_written += sd[(size_t)b * kStFields + kStWritten];
+    for (int b = 0; b < c->info_blocks; ++b) {
+        out->stdp_rows += si[(size_t)b * kStFields + kStRows];
+        out->stdp_forced_rows += si[(size_t)b * kStFields + kStForced];
+        out->stdp_synapse_updates += si[(size_t)b * kStFields + kStSyn];
     }
-    for (int64_t v : dv) out->delivered_events += v;
+    for (int64_t v : sy) out->stdp_weights_written += v;
+    for (int b = 0; b < c->dlv_slots; ++b) {
+        out->delivered_events += dv[2 * (size_t)b];
+        out->stdp_weights_written += dv[2 * (size_t)b + 1];
+    }
     return SNN_OK;
 }
 

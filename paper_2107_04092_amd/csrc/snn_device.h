@@ -1,0 +1,228 @@
+// Device helpers shared by the gfx950 kernels of the synapse pass: the
+// counter-based generator, wave/workgroup reductions and scans, the segment
+// map of flattened row segments, fixed-point accumulation, row snapshots and
+// the per-synapse STDP update.
+#pragma once
+
+#include "snn_internal.h"
+
+#include <mutex>
+
+namespace snn {
+namespace {
+
+// ---------------------------------------------------------------------------
+// helpers
+
+// SplitMix64 output function (Steele, Lea & Flood 2014) of seed XOR key, with
+// key = stream << 58 | a << 24 | b: a counter-based draw per (stream, a, b).
+__device__ __forceinline__ uint32_t rng32(uint64_t seed, uint32_t stream, uint64_t a,
+                                          uint64_t b)
+{
+    uint64_t z = (seed ^ (((uint64_t)stream << 58) | (a << 24) | b)) + 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    z ^= z >> 31;
+    return (uint32_t)(z >> 32);
+}
+
+__device__ __forceinline__ uint64_t ballot64(bool p) { return __builtin_amdgcn_ballot_w64(p); }
+
+// w^mu for w >= 0 and 0 <= mu < 1, as 2^(mu log2 w) on the hardware
+// transcendental unit (v_log_f32 / v_exp_f32, about 1 ulp each): relative
+// error around 1e-7, against a few hundred instructions for a libm powf.
+__device__ __forceinline__ float pow_mu(float w, float mu)
+{
+    if (mu == 0.f) return 1.f;
+    if (!(w > 0.f)) return 0.f;
+    return __builtin_amdgcn_exp2f(mu * __builtin_amdgcn_logf(w));
+}
+
+// fp32 -> fixed point (x * 2^32 is exact in fp32; only |x| < 2^-9 loses bits)
+__device__ __forceinline__ long long to_fix(float x) { return __float2ll_rn(x * kFixScale); }
+// fixed point -> fp32, one correctly rounded conversion (the scaling is exact)
+__device__ __forceinline__ float from_fix(long long s) { return __ll2float_rn(s) * kFixUnit; }
+
+__device__ __forceinline__ int wave_sum_i32(int v)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+    return v;
+}
+
+__device__ __forceinline__ long long wave_sum_i64(long long v)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+    return v;
+}
+
+// Sum over a kBlock-thread workgroup; every thread gets the total.
+__device__ __forceinline__ long long block_sum_i64(long long v, long long *sh)
+{
+    v = wave_sum_i64(v);
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    __syncthreads();
+    if (lane == 0) sh[wave] = v;
+    __syncthreads();
+    long long t = 0;
+#pragma unroll
+    for (int q = 0; q < kBlock / kWave; ++q) t += sh[q];
+    return t;
+}
+
+// Sum / inclusive scan over a NT-thread workgroup (sh: NT/64 entries).
+template <int NT>
+__device__ __forceinline__ long long block_sum_i64_n(long long v, long long *sh)
+{
+    v = wave_sum_i64(v);
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    __syncthreads();
+    if (lane == 0) sh[wave] = v;
+    __syncthreads();
+    long long t = 0;
+#pragma unroll
+    for (int q = 0; q < NT / kWave; ++q) t += sh[q];
+    return t;
+}
+
+template <int NT>
+__device__ __forceinline__ long long block_incl_scan_i64_n(long long v, long long *sh)
+{
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const long long u = __shfl_up(v, off, kWave);
+        if (lane >= off) v += u;
+    }
+    __syncthreads();
+    if (lane == kWave - 1) sh[wave] = v;
+    __syncthreads();
+    for (int q = 0; q < wave; ++q) v += sh[q];
+    return v;
+}
+
+// Segment map of a window of flattened elements. On entry mark[x] holds the
+// index of the (non-empty) segment that starts at x, or -1; on exit every
+// entry holds the index of the segment containing x (an inclusive max-scan,
+// valid because segment indices grow with their start offsets). NT threads,
+// 4 consecutive entries each; len <= 4 NT. Ends with a barrier.
+template <int NT>
+__device__ __forceinline__ void fill_segment_map(int *mark, int len, int *sh)
+{
+    const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+    int v[4], m = -1;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int x = 4 * tid + q;
+        const int u = x < len ? mark[x] : -1;
+        m = max(m, u);
+        v[q] = m;
+    }
+    int inc = m;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int u = __shfl_up(inc, off, kWave);
+        if (lane >= off) inc = max(inc, u);
+    }
+    if (lane == kWave - 1) sh[wave] = inc;
+    __syncthreads();
+    int excl = __shfl_up(inc, 1, kWave);
+    if (lane == 0) excl = -1;
+    for (int q = 0; q < wave; ++q) excl = max(excl, sh[q]);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int x = 4 * tid + q;
+        if (x < len) mark[x] = max(excl, v[q]);
+    }
+    __syncthreads();
+}
+
+
+// Snapshot of plastic row k for an update at step t (see RowInfo). Returns
+// 1 if the row has something to bring up to date.
+__device__ __forceinline__ int make_row_info(RowInfo &ri, int k, int64_t t, bool pre_allowed,
+                                             int dm1, const int64_t *row_ptr,
+                                             const int32_t *pend, const uint64_t *hist,
+                                             const int32_t *t_last, const float *xpre,
+                                             const float *dpow, int32_t *err)
+{
+    int age = (int)(t - (int64_t)t_last[k]);
+    ri.k = k;
+    ri.rs = row_ptr[k];
+    ri.pad = 0;
+    ri.xp0 = xpre[k];
+    if (age <= 0) {  // flush: already current
+        ri.len = 0;
+        ri.age_pre = 0;
+        ri.xp_now = ri.xp0;
+        return 0;
+    }
+    if (age > 64) {
+        // the plasticity part was skipped for this row: posts older than the
+        // history word are lost; flag it and stay inside the table
+        atomicOr(err, kErrWindow);
+        age = 64;
+    }
+    const int pre = pre_allowed ? (int)((hist[k] >> dm1) & 1ull) : 0;
+    ri.len = pend[k];
+    ri.age_pre = age | (pre << 8);
+    ri.xp_now = __fadd_rn(__fmul_rn(ri.xp0, dpow[age]), (float)pre);
+    return 1;
+}
+
+// One synapse k->j brought from t_last to t (age = t - t_last, window bits
+// h = hist[j] & (2^age - 1), pre = transmitting at t). Returns the new weight.
+__device__ __forceinline__ float stdp_synapse(float w, uint64_t h, int age, int pre, float xp0,
+                                              float xp_now, float y, const float *dpow,
+                                              float c_pot, float c_dep, float mu)
+{
+    uint64_t older = h & ~1ull;
+    while (older) {  // posts before t, oldest first
+        const int bit = 63 - __clzll((long long)older);
+        older ^= 1ull << bit;
+        w = w + c_pot * pow_mu(w, mu) * __fmul_rn(xp0, dpow[age - bit]);
+    }
+    if (pre) {  // pre at t sees the posts strictly before t
+        w = w - c_dep * w * y;
+        w = fmaxf(w, 0.f);
+    }
+    if (h & 1ull) w = w + c_pot * pow_mu(w, mu) * xp_now;  // post at t
+    return w;
+}
+
+inline int blocks_for(int64_t count, int per = kBlock, int64_t cap = 1 << 20)
+{
+    int64_t b = (count + per - 1) / per;
+    if (b < 1) b = 1;
+    if (b > cap) b = cap;
+    return (int)b;
+}
+
+// Raises a kernel's dynamic-LDS limit to `bytes` (once per size increase).
+inline hipError_t allow_dynamic_lds(const void *kernel, int bytes, std::mutex &mu, int &granted)
+{
+    std::lock_guard<std::mutex> lock(mu);
+    if (bytes <= granted) return hipSuccess;
+    const hipError_t e =
+        hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();  // do not leave the error for the next launch
+        return e;
+    }
+    granted = bytes;
+    return hipSuccess;
+}
+
+inline int static_lds_bytes(const void *kernel)
+{
+    hipFuncAttributes attr{};
+    if (hipFuncGetAttributes(&attr, kernel) != hipSuccess) {
+        (void)hipGetLastError();
+        return -1;
+    }
+    return (int)attr.sharedSizeBytes;
+}
+
+}  // namespace
+}  // namespace snn

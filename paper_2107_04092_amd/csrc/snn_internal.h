@@ -11,8 +11,10 @@ constexpr int kBlock = 256;          // threads per workgroup of the element ker
 constexpr int kWave = 64;            // CDNA wavefront width
 constexpr int kMaxPoisson = 32;
 constexpr int kMaxSortRow = 16384;   // longest row the LDS row sort accepts
-constexpr int kStdpMaxBlocks = 2048; // persistent STDP grid (8 waves of 64 per CU slot)
-constexpr int kStdpUnroll = 16;      // synapses per lane issued together in STDP
+constexpr int kStdpBlock = 512;      // threads of the slice STDP kernel
+constexpr int kStdpBatch = 512;      // rows whose segments are staged at once
+constexpr int kStdpUnroll = 4;       // elements per thread with loads in flight
+constexpr int kStdpWindow = kStdpBlock * kStdpUnroll;  // elements per segment map
 constexpr int kGlobalMaxBlocks = 2048;
 constexpr int kLdsBytes = 160 * 1024;
 
@@ -42,8 +44,11 @@ struct NeuronArgs {
     const float *ain;       // fp32 input [nacc][n], used when input_forced
     int64_t part_stride;    // nacc * n
     int32_t input_forced;
-    uint64_t *mask, *rmask; // spike mask, plastic-row trigger mask
-    int32_t *blk_spk, *blk_row;
+    uint64_t *mask;         // spikes emitted at t
+    uint64_t *txmask;       // spikes transmitted at t (emitted at t-D+1)
+    uint64_t *fmask;        // plastic rows forced at t (idle for 64 steps, not transmitting)
+    uint64_t *recent;       // neurons with a spike in the last 64 steps (hist != 0)
+    int32_t *blk_spk, *blk_tx, *blk_f;
     int64_t t;
     int32_t n, n_exc, model, n_plastic_rows, dm1, ref_steps, poisson_len, n_parts;
     float k_m, v_th, v_reset, v_inf, d_e, d_i, j_ext, d_minus;
@@ -52,39 +57,92 @@ struct NeuronArgs {
     uint32_t poisson[kMaxPoisson];
 };
 
-struct CompactArgs {
-    const uint64_t *mask, *rmask;
-    const int32_t *blk_spk, *blk_row;
-    int32_t *spk_list, *spk_cnt;
-    int32_t *row_list, *row_cnt;
-    int64_t *gstats;
-    int32_t n, nw;
+struct RowInfo;
+
+// One synapse of the sliced CSR: target and weight side by side, so a run of
+// a row's synapses is one contiguous stretch of memory (one request per
+// cache line for both) and one 8-byte load per synapse.
+struct Edge {
+    int32_t col;
+    float w;
 };
 
-struct StdpArgs {
+struct CompactArgs {
+    const uint64_t *mask, *txmask, *fmask;
+    const int32_t *blk_spk, *blk_tx, *blk_f;
+    int32_t *spk_list, *spk_cnt;   // ascending spikes of step t (delay-ring slot)
+    int32_t *row_list, *row_cnt;   // forced plastic rows
+    int64_t *gstats;
+    int32_t n, nw, n_plastic_rows;
+    // snapshots of the plastic rows to update at step t (see RowInfo): forced
+    // rows in list order, transmitting rows at their position in the
+    // transmitted list (which is the delay-ring list of step t-D+1)
+    RowInfo *info;
+    RowInfo *txinfo;
     const int64_t *row_ptr;
     const int32_t *pend;
-    const int32_t *col;
-    float *w;
     const uint64_t *hist;
-    const float *ypost;
-    int32_t *t_last;
-    float *xpre;
+    const int32_t *t_last;
+    const float *xpre;
+    int32_t *err;
+    int64_t *info_stats;     // [gridDim.x][kStFields]
+    int64_t t;
+    int32_t dm1;
+    float dpow[65];
+};
+
+// Snapshot of one row to bring up to date, taken before the synapse pass;
+// the pass reads only snapshots, so the workgroup that commits t_last and
+// xpre never races with another that still needs the old values.
+struct RowInfo {
+    long long rs;    // first edge of the row
+    int32_t k;       // row (source neuron)
+    int32_t len;     // plastic prefix length; 0 = nothing to do
+    int32_t age_pre; // age (1..64) | pre << 8
+    float xp0;       // pre trace at the previous update
+    float xp_now;    // pre trace after this update
+    int32_t pad;
+};
+
+struct RowInfoArgs {
     const int32_t *rows;     // list mode: rows to update; nullptr in flush mode
     const int32_t *row_cnt;
     int32_t n_rows_all;      // flush mode: rows 0 .. n_rows_all-1
     int32_t dm1;
     int64_t t;               // list mode: step t; flush mode: last completed step
-    float c_pot, c_dep, mu;
-    int64_t *stats;          // [gridDim.x][kStFields]
+    const int64_t *row_ptr;
+    const int32_t *pend;
+    const uint64_t *hist;
+    const int32_t *t_last;
+    const float *xpre;
+    RowInfo *info;
     int32_t *err;            // kErrWindow when a row fell more than 64 steps behind
+    int64_t *stats;          // [gridDim.x][kStFields]
     float dpow[65];          // d_plus^i, i = 0..64
+};
+
+struct StdpArgs {
+    const RowInfo *info;
+    const int32_t *row_cnt;  // list mode row count (nullptr: flush, n_rows_all)
+    int32_t n_rows_all;
+    int32_t *t_last;         // committed here: t_last = t, xpre = xp_now
+    float *xpre;
+    int64_t t;
+    Edge *edges;
+    const int32_t *piv;      // [n][S+1] delivery pivots, used at multiples of `mult`
+    const uint64_t *hist;
+    const float *ypost;
+    int32_t n, n_slices, mult, width, n_groups, chunks, n_work, target_limit;
+    float c_pot, c_dep, mu;
+    int64_t *stats;          // [gridDim.x] weights written
+    const uint64_t *recent;  // 1 bit per neuron: spiked in the last 64 steps (or nullptr)
+    int32_t nw;              // words of `recent`
+    float dpow[65];
 };
 
 struct DeliverArgs {
     const int64_t *row_ptr;
-    const int32_t *col;
-    const float *w;
+    Edge *edges;
     const int32_t *piv;      // [n][S+1]
     const int32_t *list;
     const int32_t *cnt;
@@ -92,13 +150,22 @@ struct DeliverArgs {
     float *ain;              // fp32 input [nacc][n], written directly when C == 1
     int64_t part_stride;
     int32_t n, n_exc, width, n_slices, chunks, nacc, n_work;
-    int64_t *stats;          // [gridDim.x]
+    int64_t *stats;          // [gridDim.x][2]: events delivered, weights written
+    // plasticity of the transmitting rows, fused into slice delivery
+    int32_t plastic;         // 0: no plastic rows
+    const RowInfo *txinfo;   // aligned with `list`
+    const uint64_t *hist;
+    const float *ypost;
+    int32_t *t_last;
+    float *xpre;
+    int64_t t;
+    float c_pot, c_dep, mu;
+    float dpow[65];
 };
 
 struct GraphArgs {
     int64_t *row_ptr;        // n+1
-    int32_t *col;
-    float *w;
+    Edge *edges;
     int32_t *piv;
     int32_t *pend;
     int32_t *err;
@@ -121,9 +188,21 @@ hipError_t launch_fill_ll(hipStream_t s, long long *p, int64_t count, long long 
 hipError_t launch_copy_bytes(hipStream_t s, void *dst, const void *src, int64_t bytes);
 hipError_t launch_neuron(hipStream_t s, const NeuronArgs &a);
 hipError_t launch_compact(hipStream_t s, const CompactArgs &a);
-hipError_t launch_stdp(hipStream_t s, const StdpArgs &a, int blocks);
+hipError_t launch_row_info(hipStream_t s, const RowInfoArgs &a, int64_t max_rows);
+hipError_t launch_stdp(hipStream_t s, const StdpArgs &a, int blocks, size_t lds);
+hipError_t launch_stdp_rows(hipStream_t s, const StdpArgs &a, int blocks);
+constexpr int kStdpRowsBlock = 1024;   // threads of the row-wise STDP kernel
+constexpr int kStdpRowsUnroll = 8;     // synapses per lane with loads in flight
+constexpr int kStdpRowsBlocks = 256;   // its persistent grid (one workgroup per CU)
+constexpr int kFusedStdpBlocks = 512;  // 512-thread workgroups of the forced-row part of the
+                                       // one-launch synapse pass
+constexpr int kRecentMaxWords = 8192;  // LDS-staged spike-recency bitmap: up to 512k neurons
+int stdp_static_bytes();  // static LDS of the slice STDP kernel (-1 on error)
 hipError_t launch_deliver_lds(hipStream_t s, const DeliverArgs &a, int blocks, size_t lds);
 hipError_t launch_deliver_global(hipStream_t s, const DeliverArgs &a, int blocks);
+hipError_t launch_synapse_pass(hipStream_t s, const DeliverArgs &d, const StdpArgs &f, int nd,
+                               int ns, size_t lds);
+int synapse_pass_static_bytes();  // static LDS of the one-launch synapse pass
 int deliver_lds_static_bytes();  // static LDS of the slice kernel (-1 on error)
 hipError_t launch_materialize_input(hipStream_t s, const long long *apart, int64_t part_stride,
                                     int32_t n_parts, float *ain, int64_t count);

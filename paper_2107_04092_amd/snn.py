@@ -32,7 +32,8 @@ _P = ctypes.c_void_p
 class snn_config(ctypes.Structure):
     _fields_ = [
         ("n", _i32), ("n_exc", _i32), ("delay_steps", _i32), ("slice_width", _i32),
-        ("spike_chunks", _i32), ("neuron_model", _i32),
+        ("spike_chunks", _i32), ("stdp_slice_mult", _i32), ("stdp_chunks", _i32),
+        ("stdp_layout", _i32), ("neuron_model", _i32),
         ("plastic", _i32), ("poisson_len", _i32),
         ("dt_ms", _f64), ("tau_m_ms", _f64), ("v_th", _f64), ("v_reset", _f64),
         ("v_inf", _f64), ("tau_ref_ms", _f64), ("tau_e_ms", _f64), ("tau_i_ms", _f64),
@@ -50,8 +51,8 @@ class snn_state_view(ctypes.Structure):
 
 
 class snn_graph_view(ctypes.Structure):
-    _fields_ = [("n_edges", _i64), ("n_slices", _i32), ("row_ptr", _P), ("col", _P),
-                ("w", _P), ("pivots", _P), ("plastic_end", _P)]
+    _fields_ = [("n_edges", _i64), ("n_slices", _i32), ("edge_stride", _i32), ("row_ptr", _P),
+                ("col", _P), ("w", _P), ("pivots", _P), ("plastic_end", _P)]
 
 
 class snn_stats(ctypes.Structure):
@@ -221,12 +222,15 @@ def snn_reset_stats(ctx):
 
 # ---- configuration marshalling ---------------------------------------------
 
-def config_from_preset(p, poisson_table=(), slice_width=None, spike_chunks=None):
+def config_from_preset(p, poisson_table=(), slice_width=None, spike_chunks=None,
+                       stdp_slice_mult=0, stdp_chunks=0, stdp_layout=0):
     """snn_config from a preset-like object with the physical parameters."""
     c = snn_config()
     c.n, c.n_exc, c.delay_steps = p.n, p.n_exc, p.delay
     c.slice_width = p.slice_width if slice_width is None else slice_width
     c.spike_chunks = p.spike_chunks if spike_chunks is None else spike_chunks
+    c.stdp_slice_mult, c.stdp_chunks = stdp_slice_mult, stdp_chunks
+    c.stdp_layout = stdp_layout
     c.neuron_model, c.plastic = p.model, p.plastic
     c.dt_ms, c.tau_m_ms, c.v_th, c.v_reset, c.v_inf = p.dt, p.tau_m, p.v_th, p.v_reset, p.v_inf
     c.tau_ref_ms, c.tau_e_ms, c.tau_i_ms = p.tau_ref, p.tau_e, p.tau_i
@@ -389,11 +393,13 @@ class Network:
         torch = self._torch
         v = snn_get_graph(self.ctx)
         n, s, e = self.n, v.n_slices, v.n_edges
+        st = v.edge_stride
+        edges = self._view(self.g, v.col, e * st, torch.int32)  # (target, weight) pairs
         return {
             "n_edges": e, "n_slices": s,
             "row_ptr": self._view(self.ws, v.row_ptr, n + 1, torch.int64),
-            "col": self._view(self.g, v.col, e, torch.int32),
-            "w": self._view(self.g, v.w, e, torch.float32),
+            "col": edges[0::st],
+            "w": edges.view(torch.float32)[1::st],
             "pivots": self._view(self.g, v.pivots, n * (s + 1), torch.int32).view(n, s + 1),
             "plastic_end": self._view(self.ws, v.plastic_end, n, torch.int32),
         }

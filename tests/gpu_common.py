@@ -24,10 +24,11 @@ def torch_mod():
     return torch
 
 
-def gpu_net(p, slice_width=None, spike_chunks=None, build=True):
+def gpu_net(p, slice_width=None, spike_chunks=None, build=True, **cfg_kw):
     torch = torch_mod()
     tab = wl.poisson_cdf_table(p.poisson_mu)
-    cfg = snn.config_from_preset(p, tab, slice_width=slice_width, spike_chunks=spike_chunks)
+    cfg = snn.config_from_preset(p, tab, slice_width=slice_width, spike_chunks=spike_chunks,
+                                 **cfg_kw)
     net = snn.Network(cfg)
     if build:
         net.build_random(p.graph_kind, p.p_or_fanout, p.w_exc, p.w_inh)
@@ -113,8 +114,13 @@ def compare_step(net, o, mode_name, t, check_rows=True):
         assert np.array_equal(to_np(s["i_inh"]).view(np.uint32), ost["i_inh"].view(np.uint32))
     rows = None
     if check_rows and net.cfg.plastic != snn.SNN_PLASTIC_NONE:
-        nr = int(to_np(s["stdp_row_count"])[0])
-        rows = np.sort(to_np(s["stdp_rows"])[:nr])
+        # rows made current at this step: those forced by the 64-step window
+        # and the plastic rows that transmitted
+        nf = int(to_np(s["stdp_row_count"])[0])
+        nt = int(to_np(s["tx_count"])[0])
+        n_plastic = net.n if net.cfg.plastic == snn.SNN_PLASTIC_ALL else net.cfg.n_exc
+        tx = to_np(s["tx_list"])[:nt]
+        rows = np.unique(np.concatenate([to_np(s["stdp_rows"])[:nf], tx[tx < n_plastic]]))
     return rows
 
 
@@ -136,9 +142,10 @@ def compare_rows(net, o, rows, what, graph_cache):
     return len(idx)
 
 
-def teacher_forced_run(p, steps, mode, slice_width=None, spike_chunks=None, check_every=1):
+def teacher_forced_run(p, steps, mode, slice_width=None, spike_chunks=None, check_every=1,
+                       **cfg_kw):
     """Runs `steps` teacher-forced steps; returns (net, oracle, counters)."""
-    net = gpu_net(p, slice_width, spike_chunks)
+    net = gpu_net(p, slice_width, spike_chunks, **cfg_kw)
     o = oracle_net(p)
     cache = {}
     n_rows = n_w = n_spk = 0

@@ -34,13 +34,16 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("mode", [LDS, GLOBAL], ids=["lds", "global"])
+@pytest.mark.parametrize("mode,layout", [(LDS, 0), (GLOBAL, 1)],
+                         ids=["lds-rows-fused", "global-slicestdp"])
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "%s-%s" % (c[0], c[1].get("n", "")))
-def test_teacher_forced_parity(case, mode):
+def test_teacher_forced_parity(case, mode, layout):
     name, kw, steps, width, chunks = case
     p = wl.preset(name, **kw)
-    log("parity %s %s mode=%d W=%d C=%d steps=%d" % (name, kw, mode, width, chunks, steps))
-    net, o, cnt = teacher_forced_run(p, steps, mode, slice_width=width, spike_chunks=chunks)
+    log("parity %s %s mode=%d layout=%d W=%d C=%d steps=%d" % (name, kw, mode, layout, width,
+                                                                chunks, steps))
+    net, o, cnt = teacher_forced_run(p, steps, mode, slice_width=width, spike_chunks=chunks,
+                                     stdp_layout=layout)
     assert cnt["spikes"] > 0
     if p.plastic != PLASTIC_NONE:
         assert cnt["rows"] > 0 and cnt["weights"] > 0
@@ -53,14 +56,18 @@ def test_teacher_forced_parity(case, mode):
     assert st["spikes"] == cnt["spikes"]
 
 
-@pytest.mark.parametrize("width,chunks,fanout", [(64, 1, 300), (2048, 2, 300),
-                                                 (16384, 1, 3000), (1024, 64, 300)])
-def test_slice_shapes(width, chunks, fanout):
-    """Segments from 1 to ~600 entries, one to many chunks, more spikes per
-    workgroup than one staging batch holds."""
+@pytest.mark.parametrize("width,chunks,fanout,mult,schunks", [
+    (64, 1, 300, 1, 1), (2048, 2, 300, 0, 0), (4096, 1, 3000, 1, 1), (1024, 64, 300, 3, 7),
+    (640, 1, 300, 4, 300)])
+def test_slice_shapes(width, chunks, fanout, mult, schunks):
+    """Delivery segments from 1 to ~600 entries, one to many chunks, more
+    spikes (and rows) per workgroup than one staging batch holds; STDP target
+    groups of 1..8 slices shared by 1..300 workgroups."""
     p = wl.preset("stress", n=4000, p_or_fanout=fanout, p_fire=0.3 if chunks == 1 else 0.02)
-    log("slice shape W=%d C=%d F=%d" % (width, chunks, fanout))
-    net, o, _ = teacher_forced_run(p, 70, LDS, slice_width=width, spike_chunks=chunks)
+    log("slice shape W=%d C=%d F=%d mult=%d stdp_chunks=%d" % (width, chunks, fanout, mult,
+                                                                 schunks))
+    net, o, _ = teacher_forced_run(p, 70, LDS, slice_width=width, spike_chunks=chunks,
+                                   stdp_slice_mult=mult, stdp_chunks=schunks)
     net.flush_plasticity()
     compare_all_plastic_weights(net, o)
 
@@ -101,7 +108,9 @@ def test_silent_network():
     assert cnt["spikes"] == 0
     st = net.stats()
     assert st["delivered_events"] == 0
-    assert st["stdp_forced_rows"] == 2 * 1500  # every row forced at t=63 and t=127
+    # row k starts 1 + (k mod 64) steps old: forced at 63 - (k mod 64) + 64 i
+    want = sum(len(range(63 - (k % 64), 140, 64)) for k in range(1500))
+    assert st["stdp_forced_rows"] == want
     assert st["stdp_weights_written"] == 0
     assert not to_np(net.state()["input_exc"]).any()
 
