@@ -45,6 +45,10 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-instrumented", action="store_true",
                     help="skip the per-kernel event pass (used under rocprofv3)")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="after the timed region, run one device-to-device copy of this many "
+                         "MiB: the reference kernel that scales rocprofv3 FETCH_SIZE/WRITE_SIZE "
+                         "readings to bytes")
     return ap.parse_args()
 
 
@@ -219,13 +223,23 @@ def main():
             "delivery_GBs": round(b_dlv2 / (t_dlv * 1e-3) / 1e9, 1),
         }
         ach = b_stdp2 / (t_stdp * 1e-3) / 1e9
-        traffic = load_traffic("k_stdp", p.name)
+        kname = "k_stdp_rows" if args.stdp_layout == "rows" else "k_stdp"
+        traffic = load_traffic(kname, p.name)
         roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
-                    "traffic": traffic, "kernel": "k_stdp"}
+                    "traffic": traffic, "kernel": kname}
         comb = (b_stdp2 + b_dlv2) / ((t_stdp + t_dlv) * 1e-3) / 1e9
         combined = {"achieved_GBs": round(comb, 1), "frac": round(comb / HBM_PEAK_GBS, 4),
                     "us_per_step": round((t_stdp + t_dlv) * 1e3, 3)}
+
+    if args.copy_probe_mib > 0:
+        nbytes = args.copy_probe_mib << 20
+        src = torch.empty(nbytes, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -111,8 +111,7 @@ typedef struct snn_config {
     int32_t stdp_layout;  /* forced rows (idle for 64 steps): 0 = row-wise, a
                              wave per row, histories gathered from L2 only for
                              targets that spiked within 64 steps (a recency
-                             bitmap in LDS), run in the same launch as
-                             delivery by snn_step; 1 = slice-organised, the
+                             bitmap in LDS); 1 = slice-organised, the
                              target group's histories staged in LDS */
     int32_t neuron_model; /* enum snn_neuron_model */
     int32_t plastic;      /* enum snn_plasticity */

@@ -194,7 +194,7 @@ __global__ __launch_bounds__(kBlock) void k_compact(CompactArgs a)
         s_pc[2][wave] = __popcll(fm);
     }
     __syncthreads();
-    int o0 = (int)p0, o1 = (int)p1, o2 = (int)p2, t0 = 0, t1 = 0, t2 = 0;
+    int o0 = (int)p0, o1 = (int)p1, o2 = (int)p2, t0 = 0, t2 = 0;
 #pragma unroll
     for (int q = 0; q < kBlock / kWave; ++q) {
         if (q < wave) {
@@ -203,7 +203,6 @@ __global__ __launch_bounds__(kBlock) void k_compact(CompactArgs a)
             o2 += s_pc[2][q];
         }
         t0 += s_pc[0][q];
-        t1 += s_pc[1][q];
         t2 += s_pc[2][q];
     }
     const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));

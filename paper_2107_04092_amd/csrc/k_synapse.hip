@@ -453,30 +453,6 @@ __global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
     deliver_lds_body(a, blockIdx.x, gridDim.x, dyn_acc);
 }
 
-// The synapse pass of one step in one launch: slice delivery (with the
-// transmitting rows' plasticity) and the row-wise plasticity of the forced
-// rows touch disjoint rows, so their workgroups run side by side and their
-// memory latencies overlap. Groups of 8 consecutive workgroups alternate
-// between the two kinds (8 = one per XCD, keeping each kind's XCD mapping).
-__global__ __launch_bounds__(kDlvBlock) void k_synapse_pass(DeliverArgs d, StdpArgs f, int nd,
-                                                            int ns)
-{
-    extern __shared__ long long dyn_lds[];
-    const int ch = blockIdx.x / 8, lane8 = blockIdx.x % 8;
-    const int cd = nd / 8, cs = ns / 8, both = cd < cs ? cd : cs;
-    bool deliver;
-    int idx;
-    if (ch < 2 * both) {
-        deliver = (ch & 1) == 0;
-        idx = ch >> 1;
-    } else {
-        deliver = cd > cs;
-        idx = both + (ch - 2 * both);
-    }
-    if (deliver) deliver_lds_body(d, idx * 8 + lane8, nd, dyn_lds);
-    else stdp_rows_body<kDlvBlock, kStdpRowsUnroll>(f, idx * 8 + lane8, ns, (uint64_t *)dyn_lds);
-}
-
 // Row-wise delivery with global atomics (Fig. 3(a)): a wave per transmitted
 // spike, lanes over its row, hardware 64-bit integer atomics on the same
 // fixed-point accumulator in HBM/L2. A lane loads U entries before issuing
@@ -554,17 +530,6 @@ hipError_t launch_deliver_lds(hipStream_t s, const DeliverArgs &a, int blocks, s
     return hipGetLastError();
 }
 
-hipError_t launch_synapse_pass(hipStream_t s, const DeliverArgs &d, const StdpArgs &f, int nd,
-                               int ns, size_t lds)
-{
-    static std::mutex mu;
-    static int granted = 64 * 1024;
-    const hipError_t e = allow_dynamic_lds((const void *)k_synapse_pass, (int)lds, mu, granted);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_synapse_pass, dim3(nd + ns), dim3(kDlvBlock), lds, s, d, f, nd, ns);
-    return hipGetLastError();
-}
-
 hipError_t launch_deliver_global(hipStream_t s, const DeliverArgs &a, int blocks)
 {
     hipLaunchKernelGGL(k_deliver_global, dim3(blocks), dim3(kBlock), 0, s, a);
@@ -573,6 +538,5 @@ hipError_t launch_deliver_global(hipStream_t s, const DeliverArgs &a, int blocks
 
 int deliver_lds_static_bytes() { return static_lds_bytes((const void *)k_deliver_lds); }
 int stdp_static_bytes() { return static_lds_bytes((const void *)k_stdp); }
-int synapse_pass_static_bytes() { return static_lds_bytes((const void *)k_synapse_pass); }
 
 }  // namespace snn

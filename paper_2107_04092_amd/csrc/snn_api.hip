@@ -25,8 +25,6 @@ struct snn_ctx {
     int32_t n_plastic_rows = 0, ref_steps = 0, dlv_blocks = 0;
     int32_t stdp_mult = 1, stdp_width = 0, stdp_groups = 0, stdp_chunks = 1, stdp_grid = 0;
     int32_t info_blocks = 1, syn_slots = 1;
-    bool fused = false;       // snn_step runs delivery + forced-row STDP as one launch
-    size_t fused_lds = 0;
     float k_m = 0, v_th = 0, v_reset = 0, v_inf = 0, d_e = 0, d_i = 0, j_ext = 0;
     float d_minus = 0, c_pot = 0, c_dep = 0, mu = 0;
     float dpow[65] = {};
@@ -550,22 +548,6 @@ snn_status launch_step_delivery(snn_ctx *c, int32_t mode)
     return SNN_OK;
 }
 
-// Parts (2) and (3) of a step in one launch (slice delivery with the
-// transmitting rows' plasticity, plus the forced rows row-wise).
-snn_status launch_step_synapse_pass(snn_ctx *c)
-{
-    DeliverArgs a = deliver_args(c);
-    StdpArgs f = stdp_args(c, false);
-    snn_status st = check_hip(c, launch_synapse_pass(c->stream, a, f, c->dlv_blocks,
-                                                     kFusedStdpBlocks, c->fused_lds),
-                              "synapse pass kernel");
-    if (st) return st;
-    c->n_parts = c->chunks;
-    c->last_deliver_t = c->t;
-    c->input_forced = c->chunks == 1 ? 1 : 0;
-    return SNN_OK;
-}
-
 }  // namespace
 
 extern "C" {
@@ -640,14 +622,6 @@ snn_status snn_create(const snn_config *cfg, void *hip_stream, snn_ctx **out)
         if (work > (1 << 20)) return fail(c, SNN_EINVAL, "too many STDP work items");
         c->stdp_grid = (int32_t)((work + 7) / 8 * 8);
         c->syn_slots = c->stdp_grid > kStdpRowsBlocks ? c->stdp_grid : kStdpRowsBlocks;
-        if (c->syn_slots < kFusedStdpBlocks) c->syn_slots = kFusedStdpBlocks;
-        // one launch for delivery and the forced rows when both fit in LDS
-        const int stat_f = synapse_pass_static_bytes();
-        size_t dyn = (size_t)cfg->slice_width * c->nacc * 8 + (size_t)cfg->slice_width * 12;
-        const size_t bm = c->nw <= kRecentMaxWords ? (size_t)c->nw * 8 : 0;
-        if (bm > dyn) dyn = bm;
-        c->fused = cfg->stdp_layout == 0 && stat_f >= 0 && (int64_t)dyn + stat_f <= lds_max;
-        c->fused_lds = dyn;
     }
     plan_workspace(c, nullptr);
     return SNN_OK;
@@ -887,15 +861,10 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
     if (n_steps < 0) return fail(c, SNN_EINVAL, "n_steps must be >= 0");
     if (mode != SNN_DELIVER_LDS_SLICE && mode != SNN_DELIVER_GLOBAL_ATOMIC)
         return fail(c, SNN_EINVAL, "unknown delivery mode %d", mode);
-    const bool fused = mode == SNN_DELIVER_LDS_SLICE && c->fused && c->n_plastic_rows > 0;
     for (int32_t q = 0; q < n_steps; ++q) {
         if ((st = launch_step_neurons(c))) return st;
-        if (fused) {
-            if ((st = launch_step_synapse_pass(c))) return st;
-        } else {
-            if ((st = launch_step_plasticity(c))) return st;
-            if ((st = launch_step_delivery(c, mode))) return st;
-        }
+        if ((st = launch_step_plasticity(c))) return st;
+        if ((st = launch_step_delivery(c, mode))) return st;
         c->t += 1;
         c->steps_done += 1;
     }

@@ -194,15 +194,10 @@ hipError_t launch_stdp_rows(hipStream_t s, const StdpArgs &a, int blocks);
 constexpr int kStdpRowsBlock = 1024;   // threads of the row-wise STDP kernel
 constexpr int kStdpRowsUnroll = 8;     // synapses per lane with loads in flight
 constexpr int kStdpRowsBlocks = 256;   // its persistent grid (one workgroup per CU)
-constexpr int kFusedStdpBlocks = 512;  // 512-thread workgroups of the forced-row part of the
-                                       // one-launch synapse pass
 constexpr int kRecentMaxWords = 8192;  // LDS-staged spike-recency bitmap: up to 512k neurons
 int stdp_static_bytes();  // static LDS of the slice STDP kernel (-1 on error)
 hipError_t launch_deliver_lds(hipStream_t s, const DeliverArgs &a, int blocks, size_t lds);
 hipError_t launch_deliver_global(hipStream_t s, const DeliverArgs &a, int blocks);
-hipError_t launch_synapse_pass(hipStream_t s, const DeliverArgs &d, const StdpArgs &f, int nd,
-                               int ns, size_t lds);
-int synapse_pass_static_bytes();  // static LDS of the one-launch synapse pass
 int deliver_lds_static_bytes();  // static LDS of the slice kernel (-1 on error)
 hipError_t launch_materialize_input(hipStream_t s, const long long *apart, int64_t part_stride,
                                     int32_t n_parts, float *ain, int64_t count);
