@@ -78,25 +78,30 @@ def load_traffic(kernel, workload_key):
 
 
 def stdp_bytes(st, n, launches):
-    """Algorithmic bytes of the STDP kernel: per synapse-update 8 B (target +
-    weight read), per changed weight 4 B (store), per row 40 B (list entry,
-    row pointer, plastic end, source history, t_last and pre trace read and
-    written), per launch 12 B per neuron (target history + post trace)."""
-    return (8 * st["stdp_synapse_updates"] + 4 * st["stdp_weights_written"] +
-            40 * st["stdp_rows"] + 12 * n * launches)
+    """Algorithmic bytes of the forced-row STDP kernel (snn_update_plasticity):
+    per synapse update 8 B (target + weight read), per changed weight 4 B
+    (store), per row 40 B (list entry, row pointer, plastic end, source
+    history, t_last and pre trace read and written), per launch 8 B per neuron
+    (the target histories)."""
+    return (8 * st["stdp_forced_synapse_updates"] + 4 * st["stdp_forced_weights_written"] +
+            40 * st["stdp_forced_rows"] + 8 * n * launches)
 
 
 def delivery_bytes(st, n, n_slices, chunks, nacc, launches, mode):
-    """Algorithmic bytes of delivery: 8 B per event (target + weight). LDS
-    mode adds per (transmitted spike, slice) 20 B (list entry, row pointer,
-    pivot pair) and per launch the slice write-back: nacc * n * 4 B of fp32
-    inputs with one chunk, else C * nacc * n * 8 B of fixed-point partial
-    sums. The global mode adds per spike 20 B, per event the 8 B atomic
-    update, and per launch the clear of nacc * n * 8 B."""
+    """Algorithmic bytes of delivery with the transmitting rows' STDP: 8 B per
+    event (target + weight) and 4 B per weight STDP changed there. LDS mode
+    adds per (transmitted spike, slice) 20 B (row snapshot or list entry,
+    pivot pair), per launch 12 B per neuron for the targets' histories and
+    post traces (plastic networks) and the slice write-back: nacc * n * 4 B of
+    fp32 inputs with one chunk, else C * nacc * n * 8 B of fixed-point
+    partial sums. The global mode adds per spike 20 B, per event the 8 B
+    atomic update, and per launch the clear of nacc * n * 8 B."""
     ev, tx = st["delivered_events"], st["spikes"]
+    wtx = st["stdp_weights_written"] - st["stdp_forced_weights_written"]
+    plastic = 12 * n if st["stdp_rows"] > 0 else 0
     if mode == "lds":
         wb = 4 * nacc * n if chunks == 1 else 8 * chunks * nacc * n
-        return 8 * ev + 20 * tx * n_slices + wb * launches
+        return 8 * ev + 4 * wtx + 20 * tx * n_slices + (wb + plastic) * launches
     return 16 * ev + 20 * tx + 8 * nacc * n * launches
 
 

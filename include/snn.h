@@ -160,12 +160,10 @@ typedef struct snn_state_view {
 } snn_state_view;
 
 /* Device views of the graph (inside the bound graph buffer / workspace).
- * Each synapse is stored as a (target, weight) pair, so the target of edge e
- * is col[e * edge_stride] and its weight w[e * edge_stride]. */
+ * Targets and weights are separate arrays indexed by edge. */
 typedef struct snn_graph_view {
     int64_t n_edges;
     int32_t n_slices;      /* S = ceil(n / W) */
-    int32_t edge_stride;   /* distance between consecutive edges, in 4-byte words (2) */
     int64_t *row_ptr;      /* n+1 entries: row k is edges row_ptr[k] .. row_ptr[k+1]-1 */
     int32_t *col;          /* targets, ascending within each row */
     float *w;              /* weights, 1:1 with col */
@@ -182,6 +180,12 @@ typedef struct snn_stats {
     int64_t stdp_forced_rows;      /* rows forced by the 64-step history window */
     int64_t stdp_synapse_updates;  /* plastic synapses advanced */
     int64_t stdp_weights_written;  /* weights that changed and were stored */
+    int64_t stdp_forced_synapse_updates;  /* of stdp_synapse_updates: in forced rows
+                                             (snn_update_plasticity) */
+    int64_t stdp_forced_weights_written;  /* of stdp_weights_written: by
+                                             snn_update_plasticity and flushes
+                                             (with global-atomic delivery also
+                                             the transmitting rows) */
     int64_t device_errors;         /* conditions flagged by kernels: 4 = a plastic row
                                       fell more than 64 steps behind (its update was
                                       skipped), so its weights are no longer exact */
@@ -222,8 +226,8 @@ snn_status snn_bind_workspace(snn_ctx *ctx, void *device_ptr, size_t bytes);
 snn_status snn_graph_count_random(snn_ctx *ctx, int32_t kind, double p_or_fanout,
                                   int64_t *n_edges);
 
-/* Bytes of the graph buffer for n_edges edges: (target, weight) pairs and
- * the n x (S+1) pivot table. */
+/* Bytes of the graph buffer for n_edges edges: int32 targets, fp32 weights
+ * and the n x (S+1) pivot table. */
 snn_status snn_graph_size(const snn_ctx *ctx, int64_t n_edges, size_t *bytes);
 
 /* Binds a device graph buffer of at least snn_graph_size(n_edges) bytes. */

@@ -115,7 +115,8 @@ __global__ __launch_bounds__(kBlock) void k_fill_bernoulli(GraphArgs a)
         }
         if (f) {
             const int64_t pos = base + off + pre + __popcll(m & below);
-            a.edges[pos] = Edge{j, wk};
+            a.col[pos] = j;
+            a.w[pos] = wk;
         }
         off += tot;
         __syncthreads();
@@ -136,8 +137,8 @@ __global__ __launch_bounds__(kBlock) void k_fill_fanout(GraphArgs a)
     for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < total; e += stride) {
         const int64_t k = e / a.fanout, b = e - k * a.fanout;
         const uint32_t u = rng32(a.seed, 1, (uint64_t)k, (uint64_t)b);
-        a.edges[e] = Edge{(int32_t)(((uint64_t)u * (uint64_t)a.n) >> 32),
-                          k < a.n_exc ? a.w_exc : a.w_inh};
+        a.col[e] = (int32_t)(((uint64_t)u * (uint64_t)a.n) >> 32);
+        a.w[e] = k < a.n_exc ? a.w_exc : a.w_inh;
     }
 }
 
@@ -165,7 +166,8 @@ __global__ __launch_bounds__(kBlock) void k_edges_scatter(GraphArgs a, const int
         const int32_t s = src[i], d = dst[i];
         if (s < 0 || s >= a.n || d < 0 || d >= a.n) continue;
         const int64_t pos = (int64_t)atomicAdd((unsigned long long *)(cursor + s), 1ull);
-        a.edges[pos] = Edge{d, w[i]};
+        a.col[pos] = d;
+        a.w[pos] = w[i];
     }
 }
 
@@ -204,8 +206,8 @@ __global__ __launch_bounds__(kSortBlock) void k_row_sort(GraphArgs a)
     int p2 = 2;
     while (p2 < len) p2 <<= 1;
     for (int x = tid; x < p2; x += kSortBlock)
-        keys[x] = x < len ? (((unsigned long long)(uint32_t)a.edges[rs + x].col << 32) |
-                             f2ord(a.edges[rs + x].w))
+        keys[x] = x < len ? (((unsigned long long)(uint32_t)a.col[rs + x] << 32) |
+                             f2ord(a.w[rs + x]))
                           : ~0ull;
     __syncthreads();
     for (int size = 2; size <= p2; size <<= 1) {
@@ -225,17 +227,18 @@ __global__ __launch_bounds__(kSortBlock) void k_row_sort(GraphArgs a)
     }
     for (int x = tid; x < len; x += kSortBlock) {
         const unsigned long long key = keys[x];
-        a.edges[rs + x] = Edge{(int32_t)(key >> 32), ord2f((uint32_t)key)};
+        a.col[rs + x] = (int32_t)(key >> 32);
+        a.w[rs + x] = ord2f((uint32_t)key);
     }
 }
 
 // First index in the row [p, p+len) (sorted by target) whose target is >= v.
-__device__ __forceinline__ int lower_bound_col(const Edge *p, int len, int64_t v)
+__device__ __forceinline__ int lower_bound_col(const int32_t *p, int len, int64_t v)
 {
     int lo = 0, hi = len;
     while (lo < hi) {
         const int mid = (lo + hi) >> 1;
-        if ((int64_t)p[mid].col < v) lo = mid + 1;
+        if ((int64_t)p[mid] < v) lo = mid + 1;
         else hi = mid;
     }
     return lo;
@@ -251,7 +254,7 @@ __global__ __launch_bounds__(kBlock) void k_pivots(GraphArgs a)
     if (k >= a.n) return;  // wave-uniform
     const int64_t rs = a.row_ptr[k];
     const int len = (int)(a.row_ptr[k + 1] - rs);
-    const Edge *row = a.edges + rs;
+    const int32_t *row = a.col + rs;
     int32_t *out = a.piv + k * (int64_t)(a.n_slices + 1);
     for (int s = lane; s <= a.n_slices; s += kWave)
         out[s] = s == a.n_slices ? len : lower_bound_col(row, len, (int64_t)s * a.width);
@@ -291,7 +294,7 @@ hipError_t launch_graph_fill_fanout(hipStream_t s, const GraphArgs &a)
 {
     hipLaunchKernelGGL(k_rowptr_fanout, dim3(blocks_for((int64_t)a.n + 1)), dim3(kBlock), 0, s,
                        a);
-    if (a.edges != nullptr) {
+    if (a.col != nullptr) {
         hipLaunchKernelGGL(k_fill_fanout, dim3(blocks_for((int64_t)a.n * a.fanout, kBlock,
                                                           1 << 16)),
                            dim3(kBlock), 0, s, a);

@@ -208,7 +208,7 @@ __global__ __launch_bounds__(kBlock) void k_compact(CompactArgs a)
     const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
     const int i = (int)(word * kWave) + lane;
     if ((m >> lane) & 1ull) a.spk_list[o0 + __popcll(m & below)] = i;
-    long long st_rows = 0, st_forced = 0, st_syn = 0;
+    long long st_rows = 0, st_forced = 0, st_syn = 0, st_fsyn = 0;
     if ((txm >> lane) & 1ull) {
         RowInfo ri;
         if (i < a.n_plastic_rows &&
@@ -235,6 +235,7 @@ __global__ __launch_bounds__(kBlock) void k_compact(CompactArgs a)
             st_rows += 1;
             st_forced = 1;
             st_syn += ri.len;
+            st_fsyn = ri.len;
         }
         a.info[r] = ri;
     }
@@ -247,11 +248,13 @@ __global__ __launch_bounds__(kBlock) void k_compact(CompactArgs a)
         st_rows = block_sum_i64(st_rows, sh);
         st_forced = block_sum_i64(st_forced, sh);
         st_syn = block_sum_i64(st_syn, sh);
+        st_fsyn = block_sum_i64(st_fsyn, sh);
         if (tid == 0) {
             int64_t *slot = a.info_stats + (int64_t)b * kStFields;
             slot[kStRows] += st_rows;
             slot[kStForced] += st_forced;
             slot[kStSyn] += st_syn;
+            slot[kStForcedSyn] += st_fsyn;
         }
     }
 }

@@ -1,7 +1,7 @@
 // gfx950 kernels of the synapse pass: row snapshots for a flush, lazy +
 // event-driven STDP (slice-organised and row-wise layouts), slice delivery
-// with LDS accumulation and the transmitting rows' plasticity fused in, the
-// global-atomic delivery variant, and the one-launch synapse pass of a step.
+// with LDS accumulation and the transmitting rows' plasticity fused in, and
+// the global-atomic delivery variant.
 #include "snn_device.h"
 
 namespace snn {
@@ -106,7 +106,8 @@ __global__ __launch_bounds__(kStdpBlock) void k_stdp(StdpArgs a)
     const int pv_lo = g * a.mult;
     const int pv_hi = min((g + 1) * a.mult, a.n_slices);
     const int piv_stride = a.n_slices + 1;
-    Edge *__restrict__ edges = a.edges;
+    const int32_t *__restrict__ col = a.col;
+    float *__restrict__ wgt = a.w;
     const float c_pot = a.c_pot, c_dep = a.c_dep, mu = a.mu;
     long long written = 0;
     for (int b0 = lo; b0 < hi; b0 += kStdpBatch) {
@@ -145,19 +146,20 @@ __global__ __launch_bounds__(kStdpBlock) void k_stdp(StdpArgs a)
             int jl[kStdpUnroll], slot[kStdpUnroll];
             long long gi[kStdpUnroll];
             float wv[kStdpUnroll];
+            int cv[kStdpUnroll];
 #pragma unroll
             for (int u = 0; u < kStdpUnroll; ++u) {
-                const int x = u * kStdpBlock + tid;
-                jl[u] = -1;
-                if (x < we) {
-                    const int l = s_map[x];
-                    slot[u] = l;
-                    gi[u] = s_start[l] + (e0 + x - s_off[l]);
-                    const Edge ed = edges[gi[u]];
-                    jl[u] = ed.col - j0;
-                    wv[u] = ed.w;
-                }
+                const int x = u * kStdpBlock + tid;  // < kStdpWindow
+                const int lm = s_map[x];
+                const int l = x < we ? lm : 0;
+                slot[u] = l;
+                gi[u] = x < we ? s_start[l] + (e0 + x - s_off[l]) : 0;  // edge 0 exists
+                cv[u] = col[gi[u]];
+                wv[u] = wgt[gi[u]];
             }
+#pragma unroll
+            for (int u = 0; u < kStdpUnroll; ++u)
+                jl[u] = u * kStdpBlock + tid < we ? cv[u] - j0 : -1;
 #pragma unroll
             for (int u = 0; u < kStdpUnroll; ++u) {
                 if (jl[u] < 0) continue;
@@ -166,7 +168,7 @@ __global__ __launch_bounds__(kStdpBlock) void k_stdp(StdpArgs a)
                 const int pre = ap >> 8;
                 const uint64_t h = s_hist[jl[u]] & s_win[l];
                 if (!h && !pre) continue;  // nothing happened to this synapse
-                edges[gi[u]].w = stdp_synapse(wv[u], h, ap & 0xff, pre, s_xp0[l], s_xpn[l],
+                wgt[gi[u]] = stdp_synapse(wv[u], h, ap & 0xff, pre, s_xp0[l], s_xpn[l],
                                           pre ? s_y[jl[u]] : 0.f, s_dpow, c_pot, c_dep, mu);
                 ++written;
             }
@@ -178,80 +180,180 @@ __global__ __launch_bounds__(kStdpBlock) void k_stdp(StdpArgs a)
     if (tid == 0) a.stats[blockIdx.x] += written;
 }
 
-// Row-wise layout: a wave per row to update, lanes over its plastic
-// synapses in the row's own order, U synapses per lane with their edge loads
-// and their history (and post-trace) gathers in flight together. Histories
-// and traces come from L2 instead of LDS. With the spike-recency bitmap
-// staged in LDS, a synapse of a row without a pre spike whose target has not
-// fired within 64 steps is skipped without touching its history word in L2:
-// most of them, at low rates. NT threads per workgroup; workgroup `bid` of
-// `nblocks`.
+// Row-wise layout: waves walk the rows to update (row list entries gw,
+// gw + nwv, ...) in parts of up to U*64 plastic synapses, lanes over a
+// part's synapses in the row's own order. Histories and post traces come from
+// L2 instead of LDS. With the spike-recency bitmap staged in LDS, a synapse
+// of a row without a pre spike whose target has not fired within 64 steps is
+// skipped without touching its history word in L2: most of them, at low
+// rates. Part boundaries are aligned to 64-byte lines of the weight array,
+// and a line that holds a changed weight is stored whole (its unchanged
+// weights included), so the L2 never writes a partial line back to HBM.
+//
+// Two parts are in flight per wave: the targets and weights of the next part
+// are loaded while the current one gathers its histories, is updated and
+// stored, so HBM streaming, L2 gathers and ALU work of one wave overlap
+// instead of every wave of the grid waiting on the same kind of access at
+// the same time. The next row's snapshot is fetched one part ahead.
+
+template <int U>
+struct RowPart {
+    RowInfo ri;  // snapshot of the part's row (len 0: no part)
+    int i;       // index in the row list (>= nrows: no part)
+    int base;    // element index of lane 0 (multiple of 16 from the line start)
+    int j[U];    // targets (-1: no synapse)
+    float w[U];  // weights
+};
+
+__device__ __forceinline__ RowInfo row_info_at(const StdpArgs &a, int i, int nrows)
+{
+    RowInfo ri{};
+    if (i < nrows) ri = a.info[i];
+    return ri;
+}
+
+// Issues the loads of part p. Every lane loads from an address inside the
+// row (clamped) and selects afterwards: a load whose result is used under a
+// lane condition makes the compiler wait for it inside that condition, which
+// would serialise the U loads of a lane.
+template <int U>
+__device__ __forceinline__ void rows_issue(RowPart<U> &p, const int32_t *col, const float *wgt,
+                                           int lane)
+{
+    const int len = p.ri.age_pre != 0 ? p.ri.len : 0;
+    if (len == 0) {  // wave-uniform
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            p.j[u] = -1;
+            p.w[u] = 0.f;
+        }
+        return;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int q = p.base + u * kWave + lane;
+        const int qc = min(max(q, 0), len - 1);
+        p.j[u] = col[p.ri.rs + qc];
+        p.w[u] = wgt[p.ri.rs + qc];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int q = p.base + u * kWave + lane;
+        if (q < 0 || q >= len) p.j[u] = -1;
+    }
+}
+
+// The part after `cur` into `nxt`; la / la_i: snapshot of the next row.
+template <int U>
+__device__ __forceinline__ void rows_next(const RowPart<U> &cur, RowPart<U> &nxt, RowInfo &la,
+                                          int &la_i, const StdpArgs &a, int nrows, int nwv)
+{
+    if (cur.ri.age_pre != 0 && cur.base + U * kWave < cur.ri.len) {
+        nxt.ri = cur.ri;
+        nxt.i = cur.i;
+        nxt.base = cur.base + U * kWave;
+    } else {
+        nxt.ri = la;
+        nxt.i = la_i;
+        nxt.base = -(int)(la.rs & 15);
+        la_i += nwv;
+        la = row_info_at(a, la_i, nrows);
+    }
+}
 
 template <int NT, int U>
 __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int nblocks,
                                                uint64_t *s_recent)
 {
     __shared__ float s_dpow[65];
-    __shared__ long long sh[NT / kWave];
     const int tid = threadIdx.x;
     for (int q = tid; q < 65; q += NT) s_dpow[q] = a.dpow[q];
     const bool filt = a.recent != nullptr;
     if (filt)
         for (int q = tid; q < a.nw; q += NT) s_recent[q] = a.recent[q];
-    __syncthreads();
-    Edge *__restrict__ edges = a.edges;
+    const int32_t *__restrict__ col = a.col;
+    float *__restrict__ wgt = a.w;
     const uint64_t *__restrict__ hist = a.hist;
     const float *__restrict__ ypost = a.ypost;
     const float c_pot = a.c_pot, c_dep = a.c_dep, mu = a.mu;
     const int lane = tid % kWave;
+    const int line0 = lane & ~15;  // first lane of this lane's 16-weight line
     const int gw = (bid * NT + tid) / kWave;
     const int nwv = nblocks * (NT / kWave);
     const int nrows = a.row_cnt ? *a.row_cnt : a.n_rows_all;
     long long written = 0;
-    for (int r = gw; r < nrows; r += nwv) {
-        const RowInfo ri = a.info[r];
-        if (ri.age_pre == 0) continue;  // wave-uniform
-        if (lane == 0) {
+
+    RowPart<U> A, B;
+    int la_i = gw;
+    RowInfo la = row_info_at(a, la_i, nrows);
+    A.ri = la;
+    A.i = la_i;
+    A.base = -(int)(la.rs & 15);
+    la_i += nwv;
+    la = row_info_at(a, la_i, nrows);
+    rows_issue(A, col, wgt, lane);  // first loads overlap the bitmap staging
+    __syncthreads();
+
+    // gathers of `p`, then the next part's loads, then p's update and stores
+    auto step = [&](RowPart<U> &p, RowPart<U> &nx) {
+        const RowInfo ri = p.ri;
+        const int age = ri.age_pre & 0xff, pre = ri.age_pre >> 8;
+        const uint64_t win = age >= 64 ? ~0ull : ((1ull << age) - 1ull);
+        // all loads unconditional (safe index 0), selected afterwards
+        bool live[U];
+        if (filt && !pre) {
+            uint64_t rw[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) rw[u] = s_recent[max(p.j[u], 0) >> 6];
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                live[u] = p.j[u] >= 0 && ((rw[u] >> (p.j[u] & 63)) & 1ull);
+        } else {
+#pragma unroll
+            for (int u = 0; u < U; ++u) live[u] = p.j[u] >= 0;
+        }
+        uint64_t h[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) h[u] = hist[live[u] ? p.j[u] : 0];
+        float y[U];
+        if (pre) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) y[u] = ypost[live[u] ? p.j[u] : 0];
+        } else {
+#pragma unroll
+            for (int u = 0; u < U; ++u) y[u] = 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) h[u] = live[u] ? (h[u] & win) : 0ull;
+        rows_next(p, nx, la, la_i, a, nrows, nwv);
+        rows_issue(nx, col, wgt, lane);
+        if (ri.age_pre != 0 && p.base == -(int)(ri.rs & 15) && lane == 0) {  // first part
             a.t_last[ri.k] = (int32_t)a.t;
             a.xpre[ri.k] = ri.xp_now;
         }
-        const int len = ri.len;
-        const int age = ri.age_pre & 0xff, pre = ri.age_pre >> 8;
-        const uint64_t win = age >= 64 ? ~0ull : ((1ull << age) - 1ull);
-        const long long rs = ri.rs;
-        for (int base = 0; base < len; base += kWave * U) {
-            int j[U];
-            float w[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int q = base + u * kWave + lane;
-                Edge ed{-1, 0.f};
-                if (q < len) ed = edges[rs + q];
-                j[u] = ed.col;
-                w[u] = ed.w;
-            }
-            if (filt && !pre) {
-#pragma unroll
-                for (int u = 0; u < U; ++u)
-                    if (j[u] >= 0 && !((s_recent[j[u] >> 6] >> (j[u] & 63)) & 1ull)) j[u] = -1;
-            }
-            uint64_t h[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u) h[u] = j[u] >= 0 ? (hist[j[u]] & win) : 0ull;
-            float y[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u) y[u] = (pre && j[u] >= 0) ? ypost[j[u]] : 0.f;
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                if (j[u] < 0 || (!h[u] && !pre)) continue;
-                edges[rs + base + u * kWave + lane].w = stdp_synapse(
-                    w[u], h[u], age, pre, ri.xp0, ri.xp_now, y[u], s_dpow, c_pot, c_dep, mu);
+        for (int u = 0; u < U; ++u) {
+            const bool chg = live[u] && (h[u] || pre);
+            float w = p.w[u];
+            if (chg) {
+                w = stdp_synapse(w, h[u], age, pre, ri.xp0, ri.xp_now, y[u], s_dpow, c_pot, c_dep,
+                                 mu);
                 ++written;
             }
+            const uint64_t m = ballot64(chg);
+            if (((m >> line0) & 0xffffull) && p.j[u] >= 0)
+                wgt[ri.rs + p.base + u * kWave + lane] = w;
         }
+    };
+    while (A.i < nrows) {
+        step(A, B);
+        if (B.i >= nrows) break;
+        step(B, A);
     }
-    written = block_sum_i64_n<NT>(written, sh);
-    if (tid == 0) a.stats[bid] += written;
+    // one atomic per wave: no workgroup barrier waits for the weight stores
+    written = wave_sum_i64(written);
+    if (lane == 0 && written)
+        atomicAdd((unsigned long long *)(a.stats + bid), (unsigned long long)written);
 }
 
 __global__ __launch_bounds__(kStdpRowsBlock) void k_stdp_rows(StdpArgs a)
@@ -264,24 +366,20 @@ __global__ __launch_bounds__(kStdpRowsBlock) void k_stdp_rows(StdpArgs a)
 // (3) delivery.
 //
 // Slice delivery (Sec. III-B, Fig. 3(b)): work item q = (slice s, chunk c)
-// owns targets [sW, (s+1)W) for the c-th 1/C of the transmitted spikes. The
-// slice accumulator lives in LDS as exact 64-bit fixed point. For a batch of
-// spikes the workgroup first gathers each spike's in-slice segment
-// (row start + piv[k][s], length piv[k][s+1] - piv[k][s]) into LDS and
-// prefix-sums the lengths; then every thread takes flattened elements of the
-// concatenated segments, so lanes stay busy whatever the segment lengths and
-// consecutive lanes read consecutive entries of a segment. Each element adds
-// its weight into acc[target - sW] with an LDS 64-bit integer atomic. With
-// C = 1 the workgroup owns the slice and stores the fp32 input directly;
-// with C > 1 it stores fixed-point partial sum c. Workgroup b runs on XCD
-// b mod 8, so work items are dealt out so that each XCD gets a contiguous
-// range of slices (neighbouring segments of one row share cache lines).
-
-constexpr int kDlvBlock = 512;
-constexpr int kDlvBatch = 512;   // spikes whose segments are staged at once
-constexpr int kDlvUnroll = 4;
-constexpr int kDlvWindow = kDlvBlock * kDlvUnroll;
-
+// owns targets [sW, (s+1)W) for the transmitted spikes at list positions
+// c, c + C, c + 2C, ... The slice accumulator lives in LDS as exact 64-bit
+// fixed point. For a batch of spikes the workgroup first gathers each
+// spike's in-slice segment (row start + piv[k][s], length piv[k][s+1] -
+// piv[k][s]) into LDS and prefix-sums the lengths; then every thread takes
+// flattened elements of the concatenated segments, so lanes stay busy
+// whatever the segment lengths and consecutive lanes read consecutive
+// entries of a segment (coalesced loads). Each element adds its weight into
+// acc[target - sW] with an LDS 64-bit integer atomic. With C = 1 the
+// workgroup owns the slice and stores the fp32 input directly; with C > 1 it
+// stores fixed-point partial sum c. Workgroup b runs on XCD b mod 8, so work
+// items are dealt out so that each XCD gets a contiguous range of slices
+// (neighbouring segments of one row share cache lines).
+//
 // With plastic rows, each transmitting row is brought up to date here,
 // immediately before its weights are delivered (Sec. III-A: a synapse need
 // only be current to transmit; Sec. I: steps (2) and (3) walk the same
@@ -289,13 +387,21 @@ constexpr int kDlvWindow = kDlvBlock * kDlvUnroll;
 // the accumulator, and every plastic element of a segment is updated, stored
 // and then delivered, so the row's targets and weights are read once. The
 // workgroups of slice 0 commit t_last and the pre traces of their spikes.
-// Workgroup `bid` of `nb` (a multiple of 8); `acc` is the dynamic LDS.
-__device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, int nb,
-                                                 long long *acc)
+//
+// The spike count is read in parallel with the first batch's snapshots (the
+// snapshot buffer holds n entries, so reading past the count stays inside
+// it; entries past the count are discarded), and the workgroup's statistics
+// are reduced before its final stores, so no barrier waits for them.
+
+constexpr int kDlvBlock = 512;
+constexpr int kDlvBatch = 512;   // spikes whose segments are staged at once
+constexpr int kDlvUnroll = 8;    // flattened elements per thread per window
+constexpr int kDlvWindow = kDlvBlock * kDlvUnroll;
+
+__global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
 {
-    // acc: nacc * W accumulators [, W histories, W post traces]
+    extern __shared__ long long acc[];  // nacc * W accumulators [, W histories, W traces]
     __shared__ long long s_start[kDlvBatch];
-    __shared__ uint64_t s_win[kDlvBatch];
     __shared__ int s_off[kDlvBatch + 1];
     __shared__ int s_half[kDlvBatch];
     __shared__ int s_plen[kDlvBatch];
@@ -307,15 +413,15 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
     __shared__ long long sh[kDlvBlock / kWave];
     __shared__ int shi[kDlvBlock / kWave];
     const int tid = threadIdx.x;
-    const int q = (bid & 7) * (nb >> 3) + (bid >> 3);
+    const int nb = gridDim.x;  // multiple of 8
+    const int q = (blockIdx.x & 7) * (nb >> 3) + (blockIdx.x >> 3);
     if (q >= a.n_work) return;  // whole workgroup, before any barrier
     const int s = q / a.chunks, c = q - s * a.chunks;
+    const int C = a.chunks;
     const int base = s * a.width;
     const int span = a.nacc * a.width;
+    const int cnt = *a.cnt;  // used only once the first batch's loads are out
     for (int x = tid; x < span; x += kDlvBlock) acc[x] = 0;
-    const int cnt = *a.cnt;
-    const int lo = (int)((int64_t)cnt * c / a.chunks);
-    const int hi = (int)((int64_t)cnt * (c + 1) / a.chunks);
     uint64_t *s_hist = (uint64_t *)(acc + span);
     float *s_y = (float *)(s_hist + a.width);
     if (a.plastic) {
@@ -325,45 +431,51 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
             s_y[x] = a.ypost[base + x];
         }
         for (int x = tid; x < 65; x += kDlvBlock) s_dpow[x] = a.dpow[x];
-        if (s == 0) {
-            for (int x = lo + tid; x < hi; x += kDlvBlock) {
-                const RowInfo ri = a.txinfo[x];
-                if (ri.age_pre != 0) {
-                    a.t_last[ri.k] = (int32_t)a.t;
-                    a.xpre[ri.k] = ri.xp_now;
-                }
-            }
-        }
     }
     const int piv_stride = a.n_slices + 1;
-    Edge *__restrict__ edges = a.edges;
+    const int32_t *__restrict__ col = a.col;
+    float *__restrict__ wgt = a.w;
     const float c_pot = a.c_pot, c_dep = a.c_dep, mu = a.mu;
     long long ev = 0, written = 0;
-    for (int b0 = lo; b0 < hi; b0 += kDlvBatch) {
-        const int nbt = min(kDlvBatch, hi - b0);
+    for (int b0 = 0;; b0 += kDlvBatch) {
         // stage segment starts and lengths (one spike per thread)
+        const int r = c + C * (b0 + tid);
         int len = 0;
-        if (tid < nbt) {
-            const RowInfo ri = a.txinfo[b0 + tid];
-            const int k = ri.k;
+        if (r < a.n) {
+            int k, plen_row = 0, ap = 0;
+            int64_t rs;
+            float xp0 = 0.f, xpn = 0.f;
+            if (a.plastic) {
+                const RowInfo ri = a.txinfo[r];
+                k = ri.k;
+                rs = ri.rs;
+                ap = ri.age_pre;
+                plen_row = ri.len;
+                xp0 = ri.xp0;
+                xpn = ri.xp_now;
+            } else {
+                k = a.list[r];
+                rs = 0;
+            }
+            k = min(max(k, 0), a.n - 1);  // entries past the count are stale
             const int32_t *pv = a.piv + (int64_t)k * piv_stride + s;
             const int p0 = pv[0], p1 = pv[1];
-            s_start[tid] = ri.rs + p0;
-            s_half[tid] = (a.nacc == 2 && k >= a.n_exc) ? a.width : 0;
-            len = p1 - p0;
-            int plen = 0;
-            if (a.plastic) {
-                if (ri.age_pre != 0) {
-                    plen = min(max(ri.len - p0, 0), len);
-                    const int age = ri.age_pre & 0xff;
-                    s_age[tid] = age;
-                    s_win[tid] = age >= 64 ? ~0ull : ((1ull << age) - 1ull);
-                    s_xp0[tid] = ri.xp0;
-                    s_xpn[tid] = ri.xp_now;
+            if (!a.plastic) rs = a.row_ptr[k];
+            if (r < cnt) {
+                len = p1 - p0;
+                s_start[tid] = rs + p0;
+                s_half[tid] = (a.nacc == 2 && k >= a.n_exc) ? a.width : 0;
+                s_plen[tid] = ap != 0 ? min(max(plen_row - p0, 0), len) : 0;
+                s_age[tid] = ap & 0xff;
+                s_xp0[tid] = xp0;
+                s_xpn[tid] = xpn;
+                if (a.plastic && s == 0 && ap != 0) {
+                    a.t_last[k] = (int32_t)a.t;
+                    a.xpre[k] = xpn;
                 }
             }
-            s_plen[tid] = plen;
         }
+        const int nbt = min(kDlvBatch, max(0, (cnt - c + C - 1) / C - b0));
         const long long incl = block_incl_scan_i64_n<kDlvBlock>(len, sh);
         if (tid < nbt) s_off[tid] = (int)(incl - len);
         if (tid == kDlvBlock - 1) s_off[nbt] = (int)incl;  // = total (threads >= nbt add 0)
@@ -379,24 +491,30 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
                 if (a0 < a1) s_map[a0 - e0] = tid;
             }
             __syncthreads();
-            fill_segment_map<kDlvBlock>(s_map, we, shi);
+            fill_segment_map<kDlvBlock, kDlvUnroll>(s_map, we, shi);
             int tgt[kDlvUnroll], slot[kDlvUnroll], off[kDlvUnroll];
             long long gi[kDlvUnroll];
             float wv[kDlvUnroll];
+            // loads from safe addresses for every element slot, selected after
+            // all of them are in flight (a load used under a lane condition
+            // would be waited for inside it)
+            int cv[kDlvUnroll];
 #pragma unroll
             for (int u = 0; u < kDlvUnroll; ++u) {
-                const int x = u * kDlvBlock + tid;
-                tgt[u] = -1;
-                wv[u] = 0.f;
-                if (x < we) {
-                    const int l = s_map[x];
-                    slot[u] = l;
-                    off[u] = e0 + x - s_off[l];
-                    gi[u] = s_start[l] + off[u];
-                    const Edge ed = edges[gi[u]];
-                    tgt[u] = ed.col - base;
-                    wv[u] = ed.w;
-                }
+                const int x = u * kDlvBlock + tid;  // < kDlvWindow
+                const int lm = s_map[x];
+                const int l = x < we ? lm : 0;
+                slot[u] = l;
+                off[u] = e0 + x - s_off[l];
+                gi[u] = x < we ? s_start[l] + off[u] : 0;  // edge 0 exists when total > 0
+                cv[u] = col[gi[u]];
+                wv[u] = wgt[gi[u]];
+            }
+#pragma unroll
+            for (int u = 0; u < kDlvUnroll; ++u) {
+                const bool in = u * kDlvBlock + tid < we;
+                tgt[u] = in ? cv[u] - base : -1;
+                if (!in) wv[u] = 0.f;
             }
             if (a.plastic) {
 #pragma unroll
@@ -404,10 +522,11 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
                     if (tgt[u] < 0) continue;
                     const int l = slot[u];
                     if (off[u] >= s_plen[l]) continue;  // not plastic
-                    const uint64_t h = s_hist[tgt[u]] & s_win[l];
-                    wv[u] = stdp_synapse(wv[u], h, s_age[l], 1, s_xp0[l], s_xpn[l], s_y[tgt[u]],
-                                         s_dpow, c_pot, c_dep, mu);
-                    edges[gi[u]].w = wv[u];
+                    const int age = s_age[l];
+                    const uint64_t win = age >= 64 ? ~0ull : ((1ull << age) - 1ull);
+                    wv[u] = stdp_synapse(wv[u], s_hist[tgt[u]] & win, age, 1, s_xp0[l],
+                                         s_xpn[l], s_y[tgt[u]], s_dpow, c_pot, c_dep, mu);
+                    wgt[gi[u]] = wv[u];
                     ++written;
                 }
             }
@@ -416,11 +535,17 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
                 if (tgt[u] >= 0)
                     atomicAdd((unsigned long long *)(acc + tgt[u] + s_half[slot[u]]),
                               (unsigned long long)to_fix(wv[u]));
-            __syncthreads();  // map rewritten by the next window
+            if (e0 + kDlvWindow < total) __syncthreads();  // map rewritten by the next window
         }
+        if (c + C * (b0 + kDlvBatch) >= cnt) break;
         __syncthreads();  // staging arrays are rewritten by the next batch
     }
-    __syncthreads();
+    ev = block_sum_i64_n<kDlvBlock>(ev, sh);  // ends with the accumulation barrier
+    written = block_sum_i64_n<kDlvBlock>(written, sh);
+    if (tid == 0) {
+        a.stats[2 * (int64_t)blockIdx.x] += ev;
+        a.stats[2 * (int64_t)blockIdx.x + 1] += written;
+    }
     if (a.chunks == 1) {
         for (int x = tid; x < a.width; x += kDlvBlock) {
             const int j = base + x;
@@ -439,18 +564,6 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
             }
         }
     }
-    ev = block_sum_i64_n<kDlvBlock>(ev, sh);
-    written = block_sum_i64_n<kDlvBlock>(written, sh);
-    if (tid == 0) {
-        a.stats[2 * (int64_t)bid] += ev;
-        a.stats[2 * (int64_t)bid + 1] += written;
-    }
-}
-
-__global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
-{
-    extern __shared__ long long dyn_acc[];
-    deliver_lds_body(a, blockIdx.x, gridDim.x, dyn_acc);
 }
 
 // Row-wise delivery with global atomics (Fig. 3(a)): a wave per transmitted
@@ -466,7 +579,8 @@ __global__ __launch_bounds__(kBlock) void k_deliver_global(DeliverArgs a)
     const int gw = (blockIdx.x * kBlock + tid) / kWave;
     const int nwv = gridDim.x * (kBlock / kWave);
     const int cnt = *a.cnt;
-    const Edge *__restrict__ edges = a.edges;
+    const int32_t *__restrict__ col = a.col;
+    const float *__restrict__ wgt = a.w;
     long long ev = 0;
     for (int x = gw; x < cnt; x += nwv) {
         const int k = a.list[x];
@@ -478,10 +592,13 @@ __global__ __launch_bounds__(kBlock) void k_deliver_global(DeliverArgs a)
 #pragma unroll
             for (int u = 0; u < kGlobalUnroll; ++u) {
                 const int64_t e = e0 + u * kWave + lane;
-                Edge ed{-1, 0.f};
-                if (e < re) ed = edges[e];
-                tgt[u] = ed.col;
-                wv[u] = ed.w;
+                const int64_t ec = e < re ? e : rs;  // safe address, selected below
+                tgt[u] = col[ec];
+                wv[u] = wgt[ec];
+            }
+#pragma unroll
+            for (int u = 0; u < kGlobalUnroll; ++u) {
+                if (e0 + u * kWave + lane >= re) tgt[u] = -1;
             }
 #pragma unroll
             for (int u = 0; u < kGlobalUnroll; ++u)

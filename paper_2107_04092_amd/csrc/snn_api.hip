@@ -51,7 +51,8 @@ struct snn_ctx {
     uint8_t *g = nullptr;
     size_t g_bytes = 0;
     int64_t n_edges = -1, counted_edges = -1;
-    Edge *edges = nullptr;
+    int32_t *col = nullptr;
+    float *w = nullptr;
     int32_t *piv = nullptr;
     int graph_state = 0;  // 0 none, 1 counted, 2 buffer bound, 3 built
     int32_t counted_kind = -1;
@@ -257,7 +258,8 @@ GraphArgs graph_args(snn_ctx *c)
 {
     GraphArgs a{};
     a.row_ptr = c->row_ptr;
-    a.edges = c->edges;
+    a.col = c->col;
+    a.w = c->w;
     a.piv = c->piv;
     a.pend = c->pend;
     a.err = c->err_flag;
@@ -416,7 +418,8 @@ StdpArgs stdp_args(snn_ctx *c, bool flush)
     a.t_last = c->t_last;
     a.xpre = c->xpre;
     a.t = flush ? c->t - 1 : c->t;
-    a.edges = c->edges;
+    a.col = c->col;
+    a.w = c->w;
     a.piv = c->piv;
     a.hist = c->hist;
     a.ypost = c->ypost;
@@ -444,7 +447,7 @@ StdpArgs stdp_args(snn_ctx *c, bool flush)
 // brought up to date by the delivery part. A flush (every plastic row up to
 // step t-1, no pre-synaptic spike) takes its snapshots first. The synapse
 // pass commits t_last and the pre traces.
-snn_status launch_plasticity(snn_ctx *c, bool flush)
+snn_status launch_plasticity(snn_ctx *c, bool flush, hipStream_t s)
 {
     if (flush) {
         RowInfoArgs r{};
@@ -462,28 +465,30 @@ snn_status launch_plasticity(snn_ctx *c, bool flush)
         r.err = c->err_flag;
         r.stats = c->info_stats;
         for (int q = 0; q <= 64; ++q) r.dpow[q] = c->dpow[q];
-        snn_status st = check_hip(c, launch_row_info(c->stream, r, c->n_plastic_rows),
+        snn_status st = check_hip(c, launch_row_info(s, r, c->n_plastic_rows),
                                   "STDP row snapshot kernel");
         if (st) return st;
     }
     StdpArgs a = stdp_args(c, flush);
     if (c->cfg.stdp_layout == 0)
-        return check_hip(c, launch_stdp_rows(c->stream, a, kStdpRowsBlocks), "STDP kernel");
+        return check_hip(c, launch_stdp_rows(s, a, kStdpRowsBlocks), "STDP kernel");
     const size_t lds = (size_t)c->stdp_width * (sizeof(uint64_t) + sizeof(float));
-    return check_hip(c, launch_stdp(c->stream, a, c->stdp_grid, lds), "STDP kernel");
+    return check_hip(c, launch_stdp(s, a, c->stdp_grid, lds), "STDP kernel");
 }
 
 snn_status launch_step_plasticity(snn_ctx *c)
 {
     if (c->n_plastic_rows == 0) return SNN_OK;
-    return launch_plasticity(c, false);
+    return launch_plasticity(c, false, c->stream);
 }
+
 
 DeliverArgs deliver_args(snn_ctx *c)
 {
     DeliverArgs a{};
     a.row_ptr = c->row_ptr;
-    a.edges = c->edges;
+    a.col = c->col;
+    a.w = c->w;
     a.piv = c->piv;
     const int slot = ring_slot(c, c->t - (c->delay - 1));
     a.list = c->ring + (int64_t)slot * c->n;
@@ -520,7 +525,7 @@ snn_status launch_step_delivery(snn_ctx *c, int32_t mode)
     if (mode == SNN_DELIVER_LDS_SLICE) {
         // the transmitting rows' plasticity is fused into slice delivery
         st = check_hip(c, launch_deliver_lds(c->stream, a, c->dlv_blocks, dlv_lds_bytes(c)),
-                       "LDS delivery kernel");
+                       "slice delivery kernel");
         if (st) return st;
         c->n_parts = c->chunks;
         c->last_deliver_t = c->t;
@@ -547,6 +552,7 @@ snn_status launch_step_delivery(snn_ctx *c, int32_t mode)
     c->last_deliver_t = c->t;
     return SNN_OK;
 }
+
 
 }  // namespace
 
@@ -673,7 +679,8 @@ snn_status snn_graph_count_random(snn_ctx *c, int32_t kind, double p_or_fanout,
     snn_status st = require_ws(c);
     if (st) return st;
     GraphArgs a = graph_args(c);
-    a.edges = nullptr;
+    a.col = nullptr;
+    a.w = nullptr;
     hipError_t e;
     if (kind == SNN_GRAPH_BERNOULLI) {
         if (!(p_or_fanout >= 0 && p_or_fanout <= 1))
@@ -710,7 +717,7 @@ snn_status snn_graph_count_random(snn_ctx *c, int32_t kind, double p_or_fanout,
 snn_status snn_graph_size(const snn_ctx *c, int64_t n_edges, size_t *bytes)
 {
     if (!c || !bytes || n_edges < 0) return SNN_EINVAL;
-    *bytes = align_up((size_t)n_edges * sizeof(Edge)) +
+    *bytes = 2 * align_up((size_t)n_edges * sizeof(int32_t)) +
              align_up((size_t)c->n * (size_t)(c->n_slices + 1) * 4);
     return SNN_OK;
 }
@@ -732,8 +739,10 @@ snn_status snn_bind_graph(snn_ctx *c, void *device_ptr, size_t bytes, int64_t n_
     c->g = (uint8_t *)device_ptr;
     c->g_bytes = bytes;
     c->n_edges = n_edges;
-    c->edges = (Edge *)c->g;
-    c->piv = (int32_t *)(c->g + align_up((size_t)n_edges * sizeof(Edge)));
+    const size_t arr = align_up((size_t)n_edges * sizeof(int32_t));
+    c->col = (int32_t *)c->g;
+    c->w = (float *)(c->g + arr);
+    c->piv = (int32_t *)(c->g + 2 * arr);
     if (c->graph_state != 1) c->counted_kind = -1;
     c->graph_state = 2;
     return SNN_OK;
@@ -877,7 +886,7 @@ snn_status snn_flush_plasticity(snn_ctx *c)
     snn_status st = require_graph(c);
     if (st) return st;
     if (c->n_plastic_rows == 0 || c->t == 0) return SNN_OK;
-    return launch_plasticity(c, true);
+    return launch_plasticity(c, true, c->stream);
 }
 
 snn_status snn_get_state(snn_ctx *c, snn_state_view *out)
@@ -953,9 +962,8 @@ snn_status snn_get_graph(const snn_ctx *c, snn_graph_view *out)
     out->n_edges = c->n_edges;
     out->n_slices = c->n_slices;
     out->row_ptr = c->row_ptr;
-    out->col = &c->edges->col;
-    out->w = &c->edges->w;
-    out->edge_stride = (int32_t)(sizeof(Edge) / sizeof(int32_t));
+    out->col = c->col;
+    out->w = c->w;
     out->pivots = c->piv;
     out->plastic_end = c->pend;
     return SNN_OK;
@@ -993,8 +1001,10 @@ snn_status snn_get_stats(snn_ctx *c, snn_stats *out)
         out->stdp_rows += si[(size_t)b * kStFields + kStRows];
         out->stdp_forced_rows += si[(size_t)b * kStFields + kStForced];
         out->stdp_synapse_updates += si[(size_t)b * kStFields + kStSyn];
+        out->stdp_forced_synapse_updates += si[(size_t)b * kStFields + kStForcedSyn];
     }
-    for (int64_t v : sy) out->stdp_weights_written += v;
+    for (int64_t v : sy) out->stdp_forced_weights_written += v;
+    out->stdp_weights_written = out->stdp_forced_weights_written;
     for (int b = 0; b < c->dlv_slots; ++b) {
         out->delivered_events += dv[2 * (size_t)b];
         out->stdp_weights_written += dv[2 * (size_t)b + 1];

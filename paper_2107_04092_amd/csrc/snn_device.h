@@ -106,15 +106,15 @@ __device__ __forceinline__ long long block_incl_scan_i64_n(long long v, long lon
 // index of the (non-empty) segment that starts at x, or -1; on exit every
 // entry holds the index of the segment containing x (an inclusive max-scan,
 // valid because segment indices grow with their start offsets). NT threads,
-// 4 consecutive entries each; len <= 4 NT. Ends with a barrier.
-template <int NT>
+// E consecutive entries each; len <= E NT. Ends with a barrier.
+template <int NT, int E = 4>
 __device__ __forceinline__ void fill_segment_map(int *mark, int len, int *sh)
 {
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
-    int v[4], m = -1;
+    int v[E], m = -1;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const int x = 4 * tid + q;
+    for (int q = 0; q < E; ++q) {
+        const int x = E * tid + q;
         const int u = x < len ? mark[x] : -1;
         m = max(m, u);
         v[q] = m;
@@ -131,8 +131,8 @@ __device__ __forceinline__ void fill_segment_map(int *mark, int len, int *sh)
     if (lane == 0) excl = -1;
     for (int q = 0; q < wave; ++q) excl = max(excl, sh[q]);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const int x = 4 * tid + q;
+    for (int q = 0; q < E; ++q) {
+        const int x = E * tid + q;
         if (x < len) mark[x] = max(excl, v[q]);
     }
     __syncthreads();

@@ -25,7 +25,7 @@ constexpr float kFixScale = 4294967296.0f;        // 2^32
 constexpr float kFixUnit = 2.3283064365386963e-10f; // 2^-32
 
 // Per-block statistics slots of the STDP kernel.
-enum StdpStat { kStRows = 0, kStForced = 1, kStSyn = 2, kStWritten = 3, kStFields = 4 };
+enum StdpStat { kStRows = 0, kStForced = 1, kStSyn = 2, kStForcedSyn = 3, kStFields = 4 };
 
 // Global counters.
 enum GlobalStat { kGSpikes = 0, kGFields = 8 };
@@ -58,14 +58,6 @@ struct NeuronArgs {
 };
 
 struct RowInfo;
-
-// One synapse of the sliced CSR: target and weight side by side, so a run of
-// a row's synapses is one contiguous stretch of memory (one request per
-// cache line for both) and one 8-byte load per synapse.
-struct Edge {
-    int32_t col;
-    float w;
-};
 
 struct CompactArgs {
     const uint64_t *mask, *txmask, *fmask;
@@ -128,7 +120,8 @@ struct StdpArgs {
     int32_t *t_last;         // committed here: t_last = t, xpre = xp_now
     float *xpre;
     int64_t t;
-    Edge *edges;
+    const int32_t *col;      // synapse targets (sorted per row)
+    float *w;                // synapse weights
     const int32_t *piv;      // [n][S+1] delivery pivots, used at multiples of `mult`
     const uint64_t *hist;
     const float *ypost;
@@ -142,7 +135,8 @@ struct StdpArgs {
 
 struct DeliverArgs {
     const int64_t *row_ptr;
-    Edge *edges;
+    const int32_t *col;
+    float *w;
     const int32_t *piv;      // [n][S+1]
     const int32_t *list;
     const int32_t *cnt;
@@ -165,7 +159,8 @@ struct DeliverArgs {
 
 struct GraphArgs {
     int64_t *row_ptr;        // n+1
-    Edge *edges;
+    int32_t *col;
+    float *w;
     int32_t *piv;
     int32_t *pend;
     int32_t *err;
@@ -176,7 +171,7 @@ struct GraphArgs {
     float w_exc, w_inh;
 };
 
-// ---- launchers (snn_kernels.hip); all enqueue on `s` and return the launch
+// ---- launchers (k_*.hip); all enqueue on `s` and return the launch
 // status of the last kernel they started.
 hipError_t launch_init_state(hipStream_t s, float *v, int32_t *ref, float *ie, float *ii,
                              uint64_t *hist, float *ypost, int32_t *t_last, float *xpre,
@@ -192,7 +187,7 @@ hipError_t launch_row_info(hipStream_t s, const RowInfoArgs &a, int64_t max_rows
 hipError_t launch_stdp(hipStream_t s, const StdpArgs &a, int blocks, size_t lds);
 hipError_t launch_stdp_rows(hipStream_t s, const StdpArgs &a, int blocks);
 constexpr int kStdpRowsBlock = 1024;   // threads of the row-wise STDP kernel
-constexpr int kStdpRowsUnroll = 8;     // synapses per lane with loads in flight
+constexpr int kStdpRowsUnroll = 8;     // synapses per lane and row part
 constexpr int kStdpRowsBlocks = 256;   // its persistent grid (one workgroup per CU)
 constexpr int kRecentMaxWords = 8192;  // LDS-staged spike-recency bitmap: up to 512k neurons
 int stdp_static_bytes();  // static LDS of the slice STDP kernel (-1 on error)

@@ -51,14 +51,15 @@ class snn_state_view(ctypes.Structure):
 
 
 class snn_graph_view(ctypes.Structure):
-    _fields_ = [("n_edges", _i64), ("n_slices", _i32), ("edge_stride", _i32), ("row_ptr", _P),
+    _fields_ = [("n_edges", _i64), ("n_slices", _i32), ("row_ptr", _P),
                 ("col", _P), ("w", _P), ("pivots", _P), ("plastic_end", _P)]
 
 
 class snn_stats(ctypes.Structure):
     _fields_ = [(name, _i64) for name in (
         "steps", "spikes", "delivered_events", "stdp_rows", "stdp_forced_rows",
-        "stdp_synapse_updates", "stdp_weights_written", "device_errors")]
+        "stdp_synapse_updates", "stdp_weights_written", "stdp_forced_synapse_updates",
+        "stdp_forced_weights_written", "device_errors")]
 
 
 _SIGNATURES = {
@@ -393,13 +394,11 @@ class Network:
         torch = self._torch
         v = snn_get_graph(self.ctx)
         n, s, e = self.n, v.n_slices, v.n_edges
-        st = v.edge_stride
-        edges = self._view(self.g, v.col, e * st, torch.int32)  # (target, weight) pairs
         return {
             "n_edges": e, "n_slices": s,
             "row_ptr": self._view(self.ws, v.row_ptr, n + 1, torch.int64),
-            "col": edges[0::st],
-            "w": edges.view(torch.float32)[1::st],
+            "col": self._view(self.g, v.col, e, torch.int32),
+            "w": self._view(self.g, v.w, e, torch.float32),
             "pivots": self._view(self.g, v.pivots, n * (s + 1), torch.int32).view(n, s + 1),
             "plastic_end": self._view(self.ws, v.plastic_end, n, torch.int32),
         }

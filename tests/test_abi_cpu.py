@@ -68,6 +68,7 @@ def test_struct_layouts_match_header(tmp_path):
     ("spike_chunks", 0, "spike_chunks"),
     ("neuron_model", 7, "neuron_model"),
     ("plastic", 9, "plastic"),
+    ("stdp_layout", 2, "stdp_layout"),
     ("poisson_len", 33, "poisson_len"),
     ("dt_ms", float("nan"), "NaN"),
     ("tau_m_ms", 0.0, "tau_m_ms"),

@@ -34,14 +34,14 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("mode,layout", [(LDS, 0), (GLOBAL, 1)],
-                         ids=["lds-rows-fused", "global-slicestdp"])
+@pytest.mark.parametrize("mode,layout", [(LDS, 0), (LDS, 1), (GLOBAL, 0)],
+                         ids=["lds-rowstdp", "lds-slicestdp", "global-rowstdp"])
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "%s-%s" % (c[0], c[1].get("n", "")))
 def test_teacher_forced_parity(case, mode, layout):
     name, kw, steps, width, chunks = case
     p = wl.preset(name, **kw)
-    log("parity %s %s mode=%d layout=%d W=%d C=%d steps=%d" % (name, kw, mode, layout, width,
-                                                                chunks, steps))
+    log("parity %s %s mode=%d layout=%d W=%d C=%d steps=%d" % (
+        name, kw, mode, layout, width, chunks, steps))
     net, o, cnt = teacher_forced_run(p, steps, mode, slice_width=width, spike_chunks=chunks,
                                      stdp_layout=layout)
     assert cnt["spikes"] > 0
@@ -58,7 +58,7 @@ def test_teacher_forced_parity(case, mode, layout):
 
 @pytest.mark.parametrize("width,chunks,fanout,mult,schunks", [
     (64, 1, 300, 1, 1), (2048, 2, 300, 0, 0), (4096, 1, 3000, 1, 1), (1024, 64, 300, 3, 7),
-    (640, 1, 300, 4, 300)])
+    (640, 1, 300, 4, 300), (1024, 3, 400, 0, 0)])
 def test_slice_shapes(width, chunks, fanout, mult, schunks):
     """Delivery segments from 1 to ~600 entries, one to many chunks, more
     spikes (and rows) per workgroup than one staging batch holds; STDP target
@@ -66,8 +66,9 @@ def test_slice_shapes(width, chunks, fanout, mult, schunks):
     p = wl.preset("stress", n=4000, p_or_fanout=fanout, p_fire=0.3 if chunks == 1 else 0.02)
     log("slice shape W=%d C=%d F=%d mult=%d stdp_chunks=%d" % (width, chunks, fanout, mult,
                                                                  schunks))
+    layout = 1 if mult else 0
     net, o, _ = teacher_forced_run(p, 70, LDS, slice_width=width, spike_chunks=chunks,
-                                   stdp_slice_mult=mult, stdp_chunks=schunks)
+                                   stdp_slice_mult=mult, stdp_chunks=schunks, stdp_layout=layout)
     net.flush_plasticity()
     compare_all_plastic_weights(net, o)
 
