@@ -39,6 +39,8 @@ def parse():
     ap.add_argument("--slice-width", type=int, default=None)
     ap.add_argument("--chunks", type=int, default=None)
     ap.add_argument("--stdp-layout", choices=["rows", "slice"], default="rows")
+    ap.add_argument("--stdp-filter", choices=["auto", "codes", "bitmap", "none"],
+                    default="auto")
     ap.add_argument("--stdp-mult", type=int, default=0)
     ap.add_argument("--stdp-chunks", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -159,7 +161,9 @@ def main():
     cfg = snn.config_from_preset(p, wl.poisson_cdf_table(p.poisson_mu),
                                  slice_width=width, spike_chunks=chunks,
                                  stdp_slice_mult=args.stdp_mult, stdp_chunks=args.stdp_chunks,
-                                 stdp_layout=0 if args.stdp_layout == "rows" else 1)
+                                 stdp_layout=0 if args.stdp_layout == "rows" else 1,
+                                 stdp_filter=["auto", "codes", "bitmap", "none"].index(
+                                     args.stdp_filter))
     t0 = time.time()
     net = snn.Network(cfg, stream=stream, device=dev)
     e = net.build_random(p.graph_kind, p.p_or_fanout, p.w_exc, p.w_inh)
@@ -272,6 +276,7 @@ def main():
                            ["none", "exc-exc", "all"][p.plastic], args.mode, width, chunks),
             "n": p.n, "synapses": e, "slice_width": width, "spike_chunks": chunks,
             "delivery": args.mode, "stdp_layout": args.stdp_layout,
+            "stdp_filter": args.stdp_filter,
             "stdp_slice_mult": args.stdp_mult, "stdp_chunks": args.stdp_chunks, "seed": p.seed,
         },
         "roofline": roofline,

@@ -108,11 +108,17 @@ typedef struct snn_config {
                              post traces (12 B each) are staged in LDS */
     int32_t stdp_chunks;  /* workgroups sharing one STDP target group, each
                              taking 1/stdp_chunks of the rows (0 = auto) */
-    int32_t stdp_layout;  /* forced rows (idle for 64 steps): 0 = row-wise, a
-                             wave per row, histories gathered from L2 only for
-                             targets that spiked within 64 steps (a recency
-                             bitmap in LDS); 1 = slice-organised, the
+    int32_t stdp_layout;  /* forced rows (idle for 64 steps): 0 = row-wise,
+                             waves over each row's synapses, histories
+                             looked up as below; 1 = slice-organised, the
                              target group's histories staged in LDS */
+    int32_t stdp_filter;  /* row-wise layout, per-neuron summary staged in LDS:
+                             0 = automatic (codes if n + 16 <= 147456, else
+                             the bitmap if n <= 2^20, else none), 1 = history
+                             codes (which single step of the window held a
+                             spike; more than one: gather), 2 = spike-recency
+                             bitmap (gather for targets that fired in the
+                             window), 3 = none (gather for every synapse) */
     int32_t neuron_model; /* enum snn_neuron_model */
     int32_t plastic;      /* enum snn_plasticity */
     int32_t poisson_len;  /* entries used in poisson_cdf (0 = no external drive) */

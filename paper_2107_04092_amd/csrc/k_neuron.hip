@@ -122,6 +122,10 @@ __global__ __launch_bounds__(kBlock) void k_neuron(NeuronArgs a)
         }
         h = (h << 1) | (uint64_t)s;
         a.hist[i] = h;
+        // history code for the row-wise STDP of this step: the position + 1 of
+        // the only spike of the last 64 steps (bit i = step t-i), 0 for none
+        const int np = __popcll(h);
+        a.code[i] = np == 0 ? (uint8_t)0 : np == 1 ? (uint8_t)__ffsll((long long)h) : kCodeMulti;
         tx = (int)((h >> a.dm1) & 1ull);
         if (i < a.n_plastic_rows) forced = !tx && (a.t - (int64_t)a.t_last[i] >= 64);
     }

@@ -180,36 +180,42 @@ __global__ __launch_bounds__(kStdpBlock) void k_stdp(StdpArgs a)
     if (tid == 0) a.stats[blockIdx.x] += written;
 }
 
-// Row-wise layout: waves walk the rows to update (row list entries gw,
-// gw + nwv, ...) in parts of up to U*64 plastic synapses, lanes over a
-// part's synapses in the row's own order. Histories and post traces come from
-// L2 instead of LDS. With the spike-recency bitmap staged in LDS, a synapse
-// of a row without a pre spike whose target has not fired within 64 steps is
-// skipped without touching its history word in L2: most of them, at low
-// rates. Part boundaries are aligned to 64-byte lines of the weight array,
-// and a line that holds a changed weight is stored whole (its unchanged
-// weights included), so the L2 never writes a partial line back to HBM.
+// Row-wise layout: waves walk the rows to update in parts of up to U*64
+// plastic synapses, lanes over a part's synapses in the row's own order.
+// Histories and post traces come from L2 unless a per-neuron summary staged
+// in LDS answers:
+//   - history codes (k_neuron), when the codes of all neurons fit in LDS: a
+//     synapse whose target did not fire within the window is skipped, one
+//     whose target fired once takes its window bit from the code, and only
+//     targets with two or more spikes have their history word gathered;
+//   - else the spike-recency bitmap (1 bit per neuron: fired within the
+//     window), which skips the synapses of silent targets.
+// Rows with a pre spike (transmitting rows, in the global-atomic delivery
+// mode) need every target's post trace and gather histories and traces.
 //
-// Two parts are in flight per wave: the targets and weights of the next part
-// are loaded while the current one gathers its histories, is updated and
-// stored, so HBM streaming, L2 gathers and ALU work of one wave overlap
-// instead of every wave of the grid waiting on the same kind of access at
-// the same time. The next row's snapshot is fetched one part ahead.
+// Parts start at 64-byte lines of the weight array, and a line that holds a
+// changed weight is stored whole (its unchanged weights included), so the
+// L2 writes no partial line back to HBM. Two parts are in flight per wave:
+// the targets and weights of the next part are loaded while the current one
+// is looked up, updated and stored; the next row's snapshot is fetched one
+// part ahead.
 
 template <int U>
 struct RowPart {
-    RowInfo ri;  // snapshot of the part's row (len 0: no part)
+    RowInfo ri;  // snapshot of the part's row (age_pre 0: nothing to do)
     int i;       // index in the row list (>= nrows: no part)
-    int base;    // element index of lane 0 (multiple of 16 from the line start)
+    int base;    // element index of lane 0 (line-aligned, may be negative)
     int j[U];    // targets (-1: no synapse)
     float w[U];  // weights
 };
 
-__device__ __forceinline__ RowInfo row_info_at(const StdpArgs &a, int i, int nrows)
+template <int U>
+__device__ __forceinline__ void row_part_at(RowPart<U> &p, const StdpArgs &a, int i, int nrows)
 {
-    RowInfo ri{};
-    if (i < nrows) ri = a.info[i];
-    return ri;
+    p.i = i;
+    p.ri = RowInfo{};
+    if (i < nrows) p.ri = a.info[i];
+    p.base = -(int)(p.ri.rs & 15);
 }
 
 // Issues the loads of part p. Every lane loads from an address inside the
@@ -243,34 +249,12 @@ __device__ __forceinline__ void rows_issue(RowPart<U> &p, const int32_t *col, co
     }
 }
 
-// The part after `cur` into `nxt`; la / la_i: snapshot of the next row.
-template <int U>
-__device__ __forceinline__ void rows_next(const RowPart<U> &cur, RowPart<U> &nxt, RowInfo &la,
-                                          int &la_i, const StdpArgs &a, int nrows, int nwv)
-{
-    if (cur.ri.age_pre != 0 && cur.base + U * kWave < cur.ri.len) {
-        nxt.ri = cur.ri;
-        nxt.i = cur.i;
-        nxt.base = cur.base + U * kWave;
-    } else {
-        nxt.ri = la;
-        nxt.i = la_i;
-        nxt.base = -(int)(la.rs & 15);
-        la_i += nwv;
-        la = row_info_at(a, la_i, nrows);
-    }
-}
-
 template <int NT, int U>
 __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int nblocks,
-                                               uint64_t *s_recent)
+                                               unsigned char *s_sum)
 {
     __shared__ float s_dpow[65];
     const int tid = threadIdx.x;
-    for (int q = tid; q < 65; q += NT) s_dpow[q] = a.dpow[q];
-    const bool filt = a.recent != nullptr;
-    if (filt)
-        for (int q = tid; q < a.nw; q += NT) s_recent[q] = a.recent[q];
     const int32_t *__restrict__ col = a.col;
     float *__restrict__ wgt = a.w;
     const uint64_t *__restrict__ hist = a.hist;
@@ -284,48 +268,83 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
     long long written = 0;
 
     RowPart<U> A, B;
-    int la_i = gw;
-    RowInfo la = row_info_at(a, la_i, nrows);
-    A.ri = la;
-    A.i = la_i;
-    A.base = -(int)(la.rs & 15);
-    la_i += nwv;
-    la = row_info_at(a, la_i, nrows);
-    rows_issue(A, col, wgt, lane);  // first loads overlap the bitmap staging
+    row_part_at(A, a, gw, nrows);
+    rows_issue(A, col, wgt, lane);  // the first loads overlap the staging
+    RowInfo la = RowInfo{};         // lookahead: snapshot of the next row
+    int la_i = gw + nwv;
+    if (la_i < nrows) la = a.info[la_i];
+    for (int q = tid; q < 65; q += NT) s_dpow[q] = a.dpow[q];
+    const uint8_t *s_code = s_sum;
+    const uint64_t *s_recent = (const uint64_t *)s_sum;
+    if (a.code) {
+        const uint4 *src = (const uint4 *)a.code;
+        for (int q = tid; q < (a.n + 15) / 16; q += NT) ((uint4 *)s_sum)[q] = src[q];
+    } else if (a.recent) {
+        for (int q = tid; q < a.nw; q += NT) ((uint64_t *)s_sum)[q] = a.recent[q];
+    }
     __syncthreads();
 
-    // gathers of `p`, then the next part's loads, then p's update and stores
+    // look-ups of `p`, then the next part's loads, then p's update and stores
     auto step = [&](RowPart<U> &p, RowPart<U> &nx) {
         const RowInfo ri = p.ri;
         const int age = ri.age_pre & 0xff, pre = ri.age_pre >> 8;
         const uint64_t win = age >= 64 ? ~0ull : ((1ull << age) - 1ull);
-        // all loads unconditional (safe index 0), selected afterwards
         bool live[U];
-        if (filt && !pre) {
-            uint64_t rw[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u) rw[u] = s_recent[max(p.j[u], 0) >> 6];
-#pragma unroll
-            for (int u = 0; u < U; ++u)
-                live[u] = p.j[u] >= 0 && ((rw[u] >> (p.j[u] & 63)) & 1ull);
-        } else {
-#pragma unroll
-            for (int u = 0; u < U; ++u) live[u] = p.j[u] >= 0;
-        }
         uint64_t h[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) h[u] = hist[live[u] ? p.j[u] : 0];
         float y[U];
-        if (pre) {
+        if (!pre && a.code) {
+            int cd[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) y[u] = ypost[live[u] ? p.j[u] : 0];
+            for (int u = 0; u < U; ++u) cd[u] = s_code[max(p.j[u], 0)];
+            uint64_t hv[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                live[u] = p.j[u] >= 0 && cd[u] != 0;
+                hv[u] = hist[(live[u] && cd[u] == kCodeMulti) ? p.j[u] : 0];
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const uint64_t one = 1ull << ((cd[u] - 1) & 63);
+                h[u] = !live[u] ? 0ull : (cd[u] == kCodeMulti ? hv[u] : one) & win;
+                y[u] = 0.f;
+            }
         } else {
+            if (!pre && a.recent) {
+                uint64_t rw[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) y[u] = 0.f;
+                for (int u = 0; u < U; ++u) rw[u] = s_recent[max(p.j[u], 0) >> 6];
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    live[u] = p.j[u] >= 0 && ((rw[u] >> (p.j[u] & 63)) & 1ull);
+            } else {
+#pragma unroll
+                for (int u = 0; u < U; ++u) live[u] = p.j[u] >= 0;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) h[u] = hist[live[u] ? p.j[u] : 0];
+            if (pre) {
+#pragma unroll
+                for (int u = 0; u < U; ++u) y[u] = ypost[live[u] ? p.j[u] : 0];
+            } else {
+#pragma unroll
+                for (int u = 0; u < U; ++u) y[u] = 0.f;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) h[u] = live[u] ? (h[u] & win) : 0ull;
         }
-#pragma unroll
-        for (int u = 0; u < U; ++u) h[u] = live[u] ? (h[u] & win) : 0ull;
-        rows_next(p, nx, la, la_i, a, nrows, nwv);
+        // next part: the rest of this row, else the lookahead row
+        if (ri.age_pre != 0 && p.base + U * kWave < ri.len) {
+            nx.ri = ri;
+            nx.i = p.i;
+            nx.base = p.base + U * kWave;
+        } else {
+            nx.ri = la;
+            nx.i = la_i;
+            nx.base = -(int)(la.rs & 15);
+            la_i += nwv;
+            la = RowInfo{};
+            if (la_i < nrows) la = a.info[la_i];
+        }
         rows_issue(nx, col, wgt, lane);
         if (ri.age_pre != 0 && p.base == -(int)(ri.rs & 15) && lane == 0) {  // first part
             a.t_last[ri.k] = (int32_t)a.t;
@@ -358,8 +377,9 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
 
 __global__ __launch_bounds__(kStdpRowsBlock) void k_stdp_rows(StdpArgs a)
 {
-    extern __shared__ uint64_t dyn_recent[];
-    stdp_rows_body<kStdpRowsBlock, kStdpRowsUnroll>(a, blockIdx.x, gridDim.x, dyn_recent);
+    extern __shared__ uint4 dyn_sum[];
+    stdp_rows_body<kStdpRowsBlock, kStdpRowsUnroll>(a, blockIdx.x, gridDim.x,
+                                                    (unsigned char *)dyn_sum);
 }
 
 // ---------------------------------------------------------------------------
@@ -632,7 +652,13 @@ hipError_t launch_stdp(hipStream_t s, const StdpArgs &a, int blocks, size_t lds)
 
 hipError_t launch_stdp_rows(hipStream_t s, const StdpArgs &a, int blocks)
 {
-    const size_t lds = a.recent ? (size_t)a.nw * sizeof(uint64_t) : 0;
+    static std::mutex mu;
+    static int granted = 64 * 1024;
+    const size_t lds = a.code     ? (((size_t)a.n + 15) / 16) * 16
+                       : a.recent ? (size_t)a.nw * sizeof(uint64_t)
+                                  : 0;
+    const hipError_t e = allow_dynamic_lds((const void *)k_stdp_rows, (int)lds, mu, granted);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_stdp_rows, dim3(blocks), dim3(kStdpRowsBlock), lds, s, a);
     return hipGetLastError();
 }

@@ -38,6 +38,7 @@ struct snn_ctx {
     float *ain = nullptr;        // fp32 input [nacc][n] (teacher forcing / views)
     int32_t *ref = nullptr, *t_last = nullptr, *pend = nullptr;
     uint64_t *hist = nullptr, *mask = nullptr, *txmask = nullptr, *fmask = nullptr;
+    uint8_t *code = nullptr;  // per-neuron history codes (k_neuron), n + 16 bytes
     uint64_t *recent = nullptr;
     int32_t *blk_spk = nullptr, *blk_tx = nullptr, *blk_f = nullptr;
     int32_t *ring = nullptr, *ring_cnt = nullptr;
@@ -117,6 +118,12 @@ snn_status validate(snn_ctx *c, const snn_config &k)
         return fail(c, SNN_EINVAL, "stdp_chunks must be in [0, 1024]");
     if (k.stdp_layout < 0 || k.stdp_layout > 1)
         return fail(c, SNN_EINVAL, "stdp_layout must be 0 or 1");
+    if (k.stdp_filter < 0 || k.stdp_filter > 3)
+        return fail(c, SNN_EINVAL, "stdp_filter must be in [0, 3]");
+    if (k.stdp_filter == 1 && (int64_t)k.n + 16 > kCodeMax)
+        return fail(c, SNN_EINVAL, "stdp_filter 1 needs n + 16 <= %d", kCodeMax);
+    if (k.stdp_filter == 2 && (k.n + 63) / 64 > kRecentMaxWords)
+        return fail(c, SNN_EINVAL, "stdp_filter 2 needs n <= %d", kRecentMaxWords * 64);
     const int64_t slices = (k.n + k.slice_width - 1) / k.slice_width;
     if (slices * k.spike_chunks > (1 << 20))
         return fail(c, SNN_EINVAL, "slices * spike_chunks must not exceed 2^20");
@@ -218,6 +225,7 @@ void plan_workspace(snn_ctx *c, uint8_t *base)
     c->mask = p.take<uint64_t>(c->nw);
     c->txmask = p.take<uint64_t>(c->nw);
     c->fmask = p.take<uint64_t>(c->nw);
+    c->code = p.take<uint8_t>((int64_t)c->n + 16);
     c->recent = p.take<uint64_t>(c->nw);
     c->blk_spk = p.take<int32_t>(c->nblk);
     c->blk_tx = p.take<int32_t>(c->nblk);
@@ -340,6 +348,7 @@ snn_status launch_step_neurons(snn_ctx *c)
     a.mask = c->mask;
     a.txmask = c->txmask;
     a.fmask = c->fmask;
+    a.code = c->code;
     a.recent = c->recent;
     a.blk_spk = c->blk_spk;
     a.blk_tx = c->blk_tx;
@@ -435,8 +444,12 @@ StdpArgs stdp_args(snn_ctx *c, bool flush)
     a.c_dep = c->c_dep;
     a.mu = c->mu;
     a.stats = c->syn_stats;
-    // the recency bitmap is rebuilt by every neuron update; a flush follows one
-    a.recent = c->nw <= kRecentMaxWords && c->last_neuron_t >= 0 ? c->recent : nullptr;
+    // codes and bitmap are rebuilt by every neuron update (not by set_state)
+    const bool fresh = c->last_neuron_t >= 0;
+    const int f = c->cfg.stdp_filter;
+    const bool fits_code = (int64_t)c->n + 16 <= kCodeMax, fits_map = c->nw <= kRecentMaxWords;
+    a.code = fresh && (f == 1 || (f == 0 && fits_code)) ? c->code : nullptr;
+    a.recent = fresh && (f == 2 || (f == 0 && !fits_code && fits_map)) ? c->recent : nullptr;
     a.nw = c->nw;
     for (int q = 0; q <= 64; ++q) a.dpow[q] = c->dpow[q];
     return a;

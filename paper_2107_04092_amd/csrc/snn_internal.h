@@ -47,6 +47,8 @@ struct NeuronArgs {
     uint64_t *mask;         // spikes emitted at t
     uint64_t *txmask;       // spikes transmitted at t (emitted at t-D+1)
     uint64_t *fmask;        // plastic rows forced at t (idle for 64 steps, not transmitting)
+    uint8_t *code;          // per neuron: 0 no spike in the last 64 steps, 1 + i one spike
+                            // at step t-i, kCodeMulti more than one (see k_neuron)
     uint64_t *recent;       // neurons with a spike in the last 64 steps (hist != 0)
     int32_t *blk_spk, *blk_tx, *blk_f;
     int64_t t;
@@ -128,7 +130,10 @@ struct StdpArgs {
     int32_t n, n_slices, mult, width, n_groups, chunks, n_work, target_limit;
     float c_pot, c_dep, mu;
     int64_t *stats;          // [gridDim.x] weights written
-    const uint64_t *recent;  // 1 bit per neuron: spiked in the last 64 steps (or nullptr)
+    // row-wise layout: per-neuron history codes or the spike-recency bitmap
+    // staged in LDS (at most one of them; both nullptr: gather everything)
+    const uint8_t *code;
+    const uint64_t *recent;
     int32_t nw;              // words of `recent`
     float dpow[65];
 };
@@ -189,7 +194,9 @@ hipError_t launch_stdp_rows(hipStream_t s, const StdpArgs &a, int blocks);
 constexpr int kStdpRowsBlock = 1024;   // threads of the row-wise STDP kernel
 constexpr int kStdpRowsUnroll = 8;     // synapses per lane and row part
 constexpr int kStdpRowsBlocks = 256;   // its persistent grid (one workgroup per CU)
-constexpr int kRecentMaxWords = 8192;  // LDS-staged spike-recency bitmap: up to 512k neurons
+constexpr int kCodeMax = 147456;       // LDS bytes of history codes one row-STDP workgroup stages
+constexpr int kRecentMaxWords = 16384; // LDS-staged spike-recency bitmap: up to 1M neurons
+constexpr uint8_t kCodeMulti = 255;    // history code: two or more spikes in the window
 int stdp_static_bytes();  // static LDS of the slice STDP kernel (-1 on error)
 hipError_t launch_deliver_lds(hipStream_t s, const DeliverArgs &a, int blocks, size_t lds);
 hipError_t launch_deliver_global(hipStream_t s, const DeliverArgs &a, int blocks);

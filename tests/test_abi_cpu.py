@@ -69,6 +69,7 @@ def test_struct_layouts_match_header(tmp_path):
     ("neuron_model", 7, "neuron_model"),
     ("plastic", 9, "plastic"),
     ("stdp_layout", 2, "stdp_layout"),
+    ("stdp_filter", 4, "stdp_filter"),
     ("poisson_len", 33, "poisson_len"),
     ("dt_ms", float("nan"), "NaN"),
     ("tau_m_ms", 0.0, "tau_m_ms"),

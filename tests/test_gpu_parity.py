@@ -34,16 +34,18 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("mode,layout", [(LDS, 0), (LDS, 1), (GLOBAL, 0)],
-                         ids=["lds-rowstdp", "lds-slicestdp", "global-rowstdp"])
+@pytest.mark.parametrize("mode,layout,filt", [(LDS, 0, 1), (LDS, 0, 2), (LDS, 1, 0),
+                                              (GLOBAL, 0, 3)],
+                         ids=["lds-rowstdp-codes", "lds-rowstdp-bitmap", "lds-slicestdp",
+                              "global-rowstdp-gather"])
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "%s-%s" % (c[0], c[1].get("n", "")))
-def test_teacher_forced_parity(case, mode, layout):
+def test_teacher_forced_parity(case, mode, layout, filt):
     name, kw, steps, width, chunks = case
     p = wl.preset(name, **kw)
-    log("parity %s %s mode=%d layout=%d W=%d C=%d steps=%d" % (
-        name, kw, mode, layout, width, chunks, steps))
+    log("parity %s %s mode=%d layout=%d filter=%d W=%d C=%d steps=%d" % (
+        name, kw, mode, layout, filt, width, chunks, steps))
     net, o, cnt = teacher_forced_run(p, steps, mode, slice_width=width, spike_chunks=chunks,
-                                     stdp_layout=layout)
+                                     stdp_layout=layout, stdp_filter=filt)
     assert cnt["spikes"] > 0
     if p.plastic != PLASTIC_NONE:
         assert cnt["rows"] > 0 and cnt["weights"] > 0
