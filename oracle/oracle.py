@@ -94,6 +94,8 @@ def _load():
         "oracle_spikes_total": (i64, [P]),
         "oracle_set_neurons": (None, [P, P, P, P, P, P]),
         "oracle_get_neurons": (None, [P, P, P, P, P, P]),
+        "oracle_set_history_old": (None, [P, P]),
+        "oracle_get_history_old": (None, [P, P]),
         "oracle_set_input": (None, [P, P, P]),
         "oracle_get_input": (None, [P, P, P]),
         "oracle_get_spikes": (None, [P, P, P]),
@@ -239,14 +241,18 @@ class Oracle:
     def t(self, v):
         self._lib.oracle_set_time(self._h, int(v))
 
-    def set_neurons(self, v=None, refractory=None, i_exc=None, i_inh=None, hist=None):
+    def set_neurons(self, v=None, refractory=None, i_exc=None, i_inh=None, hist=None,
+                    hist_old=None):
         conv = lambda a, dt: None if a is None else np.ascontiguousarray(a, dtype=dt)
         arrs = [conv(v, np.float32), conv(refractory, np.int32), conv(i_exc, np.float32),
                 conv(i_inh, np.float32), conv(hist, np.uint64)]
-        for a in arrs:
+        old = conv(hist_old, np.uint64)
+        for a in arrs + [old]:
             if a is not None and a.shape != (self.n,):
                 raise ValueError("neuron array shape mismatch")
         self._lib.oracle_set_neurons(self._h, *[_ptr(a) for a in arrs])
+        if old is not None:
+            self._lib.oracle_set_history_old(self._h, _ptr(old))
 
     def neurons(self):
         n = self.n
@@ -256,6 +262,8 @@ class Oracle:
         self._lib.oracle_get_neurons(self._h, _ptr(out["v"]), _ptr(out["refractory"]),
                                      _ptr(out["i_exc"]), _ptr(out["i_inh"]),
                                      _ptr(out["hist"]))
+        out["hist_old"] = np.zeros(n, np.uint64)
+        self._lib.oracle_get_history_old(self._h, _ptr(out["hist_old"]))
         return out
 
     def set_input(self, a_exc=None, a_inh=None):

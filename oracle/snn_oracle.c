@@ -74,6 +74,7 @@ typedef struct oracle {
     float *v, *ie, *ii;
     int32_t *r;
     uint64_t *hist;
+    uint64_t *hist_old; /* the 64 steps before those of hist: bit b = step t-64-b */
     float *a_e, *a_i; /* input consumed by the next neuron update */
     /* outputs of the last step */
     uint64_t *mask;
@@ -149,12 +150,13 @@ oracle *oracle_new(const oracle_cfg *cfg)
     o->ii = (float *)calloc(n, sizeof(float));
     o->r = (int32_t *)calloc(n, sizeof(int32_t));
     o->hist = (uint64_t *)calloc(n, sizeof(uint64_t));
+    o->hist_old = (uint64_t *)calloc(n, sizeof(uint64_t));
     o->a_e = (float *)calloc(n, sizeof(float));
     o->a_i = (float *)calloc(n, sizeof(float));
     o->mask = (uint64_t *)calloc(nw ? nw : 1, sizeof(uint64_t));
     o->list = (int32_t *)calloc(n ? n : 1, sizeof(int32_t));
     o->row_ptr = (int64_t *)calloc(n + 1, sizeof(int64_t));
-    if (!o->v || !o->ie || !o->ii || !o->r || !o->hist || !o->a_e || !o->a_i ||
+    if (!o->v || !o->ie || !o->ii || !o->r || !o->hist || !o->hist_old || !o->a_e || !o->a_i ||
         !o->mask || !o->list || !o->row_ptr) {
         free(o);
         return NULL;
@@ -165,7 +167,7 @@ oracle *oracle_new(const oracle_cfg *cfg)
 void oracle_free(oracle *o)
 {
     if (!o) return;
-    free(o->v); free(o->ie); free(o->ii); free(o->r); free(o->hist);
+    free(o->v); free(o->ie); free(o->ii); free(o->r); free(o->hist); free(o->hist_old);
     free(o->a_e); free(o->a_i); free(o->mask); free(o->list);
     free(o->row_ptr); free(o->col); free(o->w); free(o->x_pre); free(o->x_post);
     free(o);
@@ -408,6 +410,7 @@ void oracle_step(oracle *o)
 #pragma omp parallel for schedule(static)
     for (int32_t i = 0; i < n; ++i) {
         int s = neuron_update(o, i, t);
+        o->hist_old[i] = (o->hist_old[i] << 1) | (o->hist[i] >> 63);
         o->hist[i] = (o->hist[i] << 1) | (uint64_t)s;
     }
     int64_t nw = (n + 63) / 64;
@@ -489,6 +492,18 @@ void oracle_get_neurons(const oracle *o, float *v, int32_t *r, float *ie, float 
     if (ie) memcpy(ie, o->ie, n * sizeof(float));
     if (ii) memcpy(ii, o->ii, n * sizeof(float));
     if (hist) memcpy(hist, o->hist, n * sizeof(uint64_t));
+}
+
+/* The spike history of the 64 steps before those of the history word (for
+ * comparing and forcing a simulator that keeps 128 steps of history). */
+void oracle_set_history_old(oracle *o, const uint64_t *h)
+{
+    if (h) memcpy(o->hist_old, h, (size_t)o->c.n * sizeof(uint64_t));
+}
+
+void oracle_get_history_old(const oracle *o, uint64_t *h)
+{
+    if (h) memcpy(h, o->hist_old, (size_t)o->c.n * sizeof(uint64_t));
 }
 
 void oracle_set_input(oracle *o, const float *a_e, const float *a_i)

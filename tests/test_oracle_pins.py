@@ -192,6 +192,26 @@ def test_mask_list_history_invariants(orc):
     assert seen > 0
 
 
+def test_128_step_history_equals_spike_lists(orc):
+    """The history word and the older word together hold exactly the spikes
+    of the last 128 steps (bit b of the pair = step t-b), rebuilt here from
+    the recorded spike lists."""
+    p = wl.preset("stress", n=700, p_or_fanout=20, p_fire=0.05, plastic=0)
+    o = orc.Oracle(p)
+    o.build_random()
+    lists = []
+    for _ in range(300):
+        o.step()
+        lists.append(o.spikes()[1].copy())
+    st = o.neurons()
+    for b in range(128):
+        fired = np.zeros(p.n, bool)
+        fired[lists[-1 - b]] = True
+        word = st["hist"] if b < 64 else st["hist_old"]
+        bit = (word >> np.uint64(b % 64)) & np.uint64(1)
+        assert np.array_equal(bit.astype(bool), fired), b
+
+
 def test_poisson_drive_table_and_samples(orc):
     from scipy.stats import poisson
     mu = 2.0
