@@ -41,6 +41,7 @@ def parse():
     ap.add_argument("--stdp-layout", choices=["rows", "slice"], default="rows")
     ap.add_argument("--stdp-filter", choices=["auto", "codes", "bitmap", "none"],
                     default="auto")
+    ap.add_argument("--history-bits", type=int, choices=[64, 128], default=64)
     ap.add_argument("--stdp-mult", type=int, default=0)
     ap.add_argument("--stdp-chunks", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -163,7 +164,8 @@ def main():
                                  stdp_slice_mult=args.stdp_mult, stdp_chunks=args.stdp_chunks,
                                  stdp_layout=0 if args.stdp_layout == "rows" else 1,
                                  stdp_filter=["auto", "codes", "bitmap", "none"].index(
-                                     args.stdp_filter))
+                                     args.stdp_filter),
+                                 history_bits=args.history_bits)
     t0 = time.time()
     net = snn.Network(cfg, stream=stream, device=dev)
     e = net.build_random(p.graph_kind, p.p_or_fanout, p.w_exc, p.w_inh)
@@ -276,7 +278,7 @@ def main():
                            ["none", "exc-exc", "all"][p.plastic], args.mode, width, chunks),
             "n": p.n, "synapses": e, "slice_width": width, "spike_chunks": chunks,
             "delivery": args.mode, "stdp_layout": args.stdp_layout,
-            "stdp_filter": args.stdp_filter,
+            "stdp_filter": args.stdp_filter, "history_bits": args.history_bits,
             "stdp_slice_mult": args.stdp_mult, "stdp_chunks": args.stdp_chunks, "seed": p.seed,
         },
         "roofline": roofline,

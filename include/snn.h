@@ -10,13 +10,15 @@
  *   (3) deliver spikes to the neurons' neighbours.
  * Every part runs in hand-written HIP kernels:
  *   - (1) emits a 64-bit firing mask word per 64 neurons (one wave64 ballot),
- *     an ascending spike list, and shifts each neuron's 64-bit firing
- *     history (least significant bit = most recent step, Fig. 2);
+ *     an ascending spike list, and shifts each neuron's firing history of
+ *     one or two 64-bit words (least significant bit = most recent step,
+ *     Fig. 2);
  *   - a ring of the last D spike lists implements the network-wide delay;
  *   - (2) is lazy + event-driven STDP (Sec. III-A, Fig. 2(b,c)): only rows
  *     that transmit this step are brought up to date, replaying the missed
- *     steps by walking the set bits of each target's history word; rows idle
- *     for 64 steps are forced so no post-synaptic spike leaves the window;
+ *     steps by walking the set bits of each target's history; rows idle for
+ *     as many steps as the history holds are forced so no post-synaptic
+ *     spike leaves the window;
  *   - (3) is slice delivery (Sec. III-B, Fig. 3(b)): the target domain is cut
  *     into slices of W neurons and one workgroup accumulates one slice in
  *     LDS with LDS atomics; a global-atomic row-wise variant (Fig. 3(a)) is
@@ -119,6 +121,10 @@ typedef struct snn_config {
                              spike; more than one: gather), 2 = spike-recency
                              bitmap (gather for targets that fired in the
                              window), 3 = none (gather for every synapse) */
+    int32_t history_bits; /* spike history per neuron: 64 (or 0) or 128 steps.
+                             Rows idle for that many steps are forced, so 128
+                             halves the forced updates of silent rows; the
+                             weights are the same either way */
     int32_t neuron_model; /* enum snn_neuron_model */
     int32_t plastic;      /* enum snn_plasticity */
     int32_t poisson_len;  /* entries used in poisson_cdf (0 = no external drive) */
@@ -145,7 +151,9 @@ typedef struct snn_state_view {
     float *v;               /* membrane potential (mV) */
     int32_t *refractory;    /* remaining refractory steps */
     float *i_exc, *i_inh;   /* CUBA currents (mV) */
-    uint64_t *hist;         /* firing history, bit i = spike at step t-1-i */
+    uint64_t *hist;         /* firing history, history_bits/64 words per neuron
+                               (neuron-major): word 0 bit i = spike at step
+                               t-1-i, word 1 bit i = spike at step t-65-i */
     float *trace_post;      /* post-synaptic trace as of the last neuron update */
     int32_t *t_last;        /* step each plastic row was last brought up to date */
     float *trace_pre;       /* pre-synaptic row trace at t_last */
@@ -183,7 +191,7 @@ typedef struct snn_stats {
     int64_t spikes;                /* spikes emitted */
     int64_t delivered_events;      /* (transmitted spike, outgoing synapse) pairs */
     int64_t stdp_rows;             /* rows brought up to date (incl. forced, flush) */
-    int64_t stdp_forced_rows;      /* rows forced by the 64-step history window */
+    int64_t stdp_forced_rows;      /* rows forced by the history window */
     int64_t stdp_synapse_updates;  /* plastic synapses advanced */
     int64_t stdp_weights_written;  /* weights that changed and were stored */
     int64_t stdp_forced_synapse_updates;  /* of stdp_synapse_updates: in forced rows

@@ -15,7 +15,8 @@ namespace {
 
 __global__ __launch_bounds__(kBlock) void k_init_state(float *v, int32_t *ref, float *ie,
                                                        float *ii, uint64_t *hist, float *ypost,
-                                                       int32_t *t_last, float *xpre, int32_t n)
+                                                       int32_t *t_last, float *xpre, int32_t n,
+                                                       int32_t hw)
 {
     const int i = blockIdx.x * kBlock + threadIdx.x;
     if (i >= n) return;
@@ -23,12 +24,12 @@ __global__ __launch_bounds__(kBlock) void k_init_state(float *v, int32_t *ref, f
     ref[i] = 0;
     ie[i] = 0.f;
     ii[i] = 0.f;
-    hist[i] = 0ull;
+    for (int q = 0; q < hw; ++q) hist[(int64_t)i * hw + q] = 0ull;
     ypost[i] = 0.f;
-    // Rows start staggered over 64 phases. No spike precedes step 0 and the
-    // pre trace starts at 0, so any t_last <= -1 gives the same weights;
+    // Rows start staggered over 64 hw phases. No spike precedes step 0 and
+    // the pre trace starts at 0, so any t_last <= -1 gives the same weights;
     // staggering spreads the forced updates of idle rows evenly over steps.
-    t_last[i] = -1 - (i & 63);
+    t_last[i] = -1 - (i & (64 * hw - 1));
     xpre[i] = 0.f;
 }
 
@@ -48,6 +49,7 @@ __global__ __launch_bounds__(kBlock) void k_neuron(NeuronArgs a)
     const int tid = threadIdx.x;
     const int i = blockIdx.x * kBlock + tid;
     int s = 0, tx = 0, forced = 0;
+    bool fired_recently = false;
     if (i < a.n) {
         if (a.model == 2) {
             s = rng32(a.seed, 4, (uint64_t)a.t, (uint64_t)i) < a.fire_thr;
@@ -114,23 +116,27 @@ __global__ __launch_bounds__(kBlock) void k_neuron(NeuronArgs a)
             a.v[i] = v;
             a.ref[i] = r;
         }
-        uint64_t h = a.hist[i];
+        uint64_t *hp = a.hist + (int64_t)i * a.hw;
+        uint64_t h = hp[0];
+        uint64_t h1 = a.hw == 2 ? hp[1] : 0ull;
         if (a.n_plastic_rows > 0) {
             // post trace seen by a pre spike at step t: posts strictly before t
             const float y = __fmul_rn(__fadd_rn(a.ypost[i], (float)(h & 1ull)), a.d_minus);
             a.ypost[i] = y;
         }
+        h1 = a.hw == 2 ? (h1 << 1) | (h >> 63) : 0ull;
         h = (h << 1) | (uint64_t)s;
-        a.hist[i] = h;
+        hp[0] = h;
+        if (a.hw == 2) hp[1] = h1;
         // history code for the row-wise STDP of this step: the position + 1 of
-        // the only spike of the last 64 steps (bit i = step t-i), 0 for none
-        const int np = __popcll(h);
-        a.code[i] = np == 0 ? (uint8_t)0 : np == 1 ? (uint8_t)__ffsll((long long)h) : kCodeMulti;
+        // the only spike of the last 64 hw steps (bit b = step t-b), 0 for none
+        const int np = __popcll(h) + __popcll(h1);
+        const int pos = h ? __ffsll((long long)h) : 64 + __ffsll((long long)h1);
+        a.code[i] = np == 0 ? (uint8_t)0 : np == 1 ? (uint8_t)pos : kCodeMulti;
+        fired_recently = np != 0;
         tx = (int)((h >> a.dm1) & 1ull);
-        if (i < a.n_plastic_rows) forced = !tx && (a.t - (int64_t)a.t_last[i] >= 64);
+        if (i < a.n_plastic_rows) forced = !tx && (a.t - (int64_t)a.t_last[i] >= 64 * a.hw);
     }
-    bool fired_recently = false;
-    if (i < a.n) fired_recently = a.hist[i] != 0ull;
     const uint64_t m = ballot64(s), txm = ballot64(tx), fm = ballot64(forced);
     const uint64_t rcm = ballot64(fired_recently);
     const int wave = tid / kWave, lane = tid % kWave;
@@ -172,9 +178,9 @@ __global__ __launch_bounds__(kBlock) void k_compact(CompactArgs a)
 {
     __shared__ long long sh[kBlock / kWave];
     __shared__ int s_pc[3][kBlock / kWave];
-    __shared__ float s_dpow[65];
+    __shared__ float s_dpow[kMaxAge + 1];
     const int tid = threadIdx.x, b = blockIdx.x;
-    for (int q = tid; q < 65; q += kBlock) s_dpow[q] = a.dpow[q];
+    for (int q = tid; q <= kMaxAge; q += kBlock) s_dpow[q] = a.dpow[q];
     long long p0 = 0, p1 = 0, p2 = 0;
     for (int q = tid; q < b; q += kBlock) {
         p0 += a.blk_spk[q];
@@ -216,7 +222,7 @@ __global__ __launch_bounds__(kBlock) void k_compact(CompactArgs a)
     if ((txm >> lane) & 1ull) {
         RowInfo ri;
         if (i < a.n_plastic_rows &&
-            make_row_info(ri, i, a.t, true, a.dm1, a.row_ptr, a.pend, a.hist, a.t_last, a.xpre,
+            make_row_info(ri, i, a.t, true, a.dm1, a.hw, a.row_ptr, a.pend, a.hist, a.t_last, a.xpre,
                           s_dpow, a.err)) {
             st_rows = 1;
             st_syn = ri.len;
@@ -234,7 +240,7 @@ __global__ __launch_bounds__(kBlock) void k_compact(CompactArgs a)
         const int r = o2 + __popcll(fm & below);
         a.row_list[r] = i;
         RowInfo ri;
-        if (make_row_info(ri, i, a.t, true, a.dm1, a.row_ptr, a.pend, a.hist, a.t_last, a.xpre,
+        if (make_row_info(ri, i, a.t, true, a.dm1, a.hw, a.row_ptr, a.pend, a.hist, a.t_last, a.xpre,
                           s_dpow, a.err)) {
             st_rows += 1;
             st_forced = 1;
@@ -279,10 +285,10 @@ __global__ __launch_bounds__(kBlock) void k_materialize_input(const long long *a
 
 hipError_t launch_init_state(hipStream_t s, float *v, int32_t *ref, float *ie, float *ii,
                              uint64_t *hist, float *ypost, int32_t *t_last, float *xpre,
-                             int32_t n)
+                             int32_t n, int32_t hw)
 {
     hipLaunchKernelGGL(k_init_state, dim3(blocks_for(n)), dim3(kBlock), 0, s, v, ref, ie, ii,
-                       hist, ypost, t_last, xpre, n);
+                       hist, ypost, t_last, xpre, n, hw);
     return hipGetLastError();
 }
 

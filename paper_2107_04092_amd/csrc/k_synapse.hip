@@ -23,16 +23,16 @@ namespace {
 
 __global__ __launch_bounds__(kBlock) void k_row_info(RowInfoArgs a)
 {
-    __shared__ float s_dpow[65];
+    __shared__ float s_dpow[kMaxAge + 1];
     __shared__ long long sh[kBlock / kWave];
     const int tid = threadIdx.x;
-    for (int q = tid; q < 65; q += kBlock) s_dpow[q] = a.dpow[q];
+    for (int q = tid; q <= kMaxAge; q += kBlock) s_dpow[q] = a.dpow[q];
     __syncthreads();
     const int r = blockIdx.x * kBlock + tid;
     long long st_rows = 0, st_syn = 0;
     if (r < a.n_rows_all) {
         RowInfo ri;
-        if (make_row_info(ri, r, a.t, false, a.dm1, a.row_ptr, a.pend, a.hist, a.t_last, a.xpre,
+        if (make_row_info(ri, r, a.t, false, a.dm1, a.hw, a.row_ptr, a.pend, a.hist, a.t_last, a.xpre,
                           s_dpow, a.err)) {
             st_rows = 1;
             st_syn = ri.len;
@@ -65,15 +65,14 @@ __global__ __launch_bounds__(kBlock) void k_row_info(RowInfoArgs a)
 
 __global__ __launch_bounds__(kStdpBlock) void k_stdp(StdpArgs a)
 {
-    extern __shared__ unsigned char stage[];  // W_s history words, then W_s post traces
+    extern __shared__ unsigned char stage[];  // W_s x hw history words, then W_s post traces
     __shared__ long long s_start[kStdpBatch];
-    __shared__ uint64_t s_win[kStdpBatch];
     __shared__ int s_off[kStdpBatch + 1];
     __shared__ int s_ap[kStdpBatch];
     __shared__ float s_xp0[kStdpBatch];
     __shared__ float s_xpn[kStdpBatch];
     __shared__ int s_map[kStdpWindow];
-    __shared__ float s_dpow[65];
+    __shared__ float s_dpow[kMaxAge + 1];
     __shared__ long long sh[kStdpBlock / kWave];
     __shared__ int shi[kStdpBlock / kWave];
     const int tid = threadIdx.x;
@@ -95,14 +94,15 @@ __global__ __launch_bounds__(kStdpBlock) void k_stdp(StdpArgs a)
     }
     const int j0 = g * a.width;
     if (j0 >= a.target_limit) return;  // no plastic synapse targets this group (g > 0)
+    const int hw = a.hw;
     uint64_t *s_hist = (uint64_t *)stage;
-    float *s_y = (float *)(stage + (size_t)a.width * sizeof(uint64_t));
+    float *s_y = (float *)(stage + (size_t)a.width * hw * sizeof(uint64_t));
     const int jn = min(a.width, a.n - j0);
     for (int x = tid; x < jn; x += kStdpBlock) {
-        s_hist[x] = a.hist[j0 + x];
+        for (int q = 0; q < hw; ++q) s_hist[x * hw + q] = a.hist[(int64_t)(j0 + x) * hw + q];
         s_y[x] = a.ypost[j0 + x];
     }
-    for (int x = tid; x < 65; x += kStdpBlock) s_dpow[x] = a.dpow[x];
+    for (int x = tid; x <= kMaxAge; x += kStdpBlock) s_dpow[x] = a.dpow[x];
     const int pv_lo = g * a.mult;
     const int pv_hi = min((g + 1) * a.mult, a.n_slices);
     const int piv_stride = a.n_slices + 1;
@@ -120,9 +120,7 @@ __global__ __launch_bounds__(kStdpBlock) void k_stdp(StdpArgs a)
                 const int p0 = pv[pv_lo];
                 const int p1 = min(pv[pv_hi], ri.len);
                 len = max(0, p1 - p0);
-                const int age = ri.age_pre & 0xff;
                 s_start[tid] = ri.rs + p0;
-                s_win[tid] = age >= 64 ? ~0ull : ((1ull << age) - 1ull);
                 s_ap[tid] = ri.age_pre;
                 s_xp0[tid] = ri.xp0;
                 s_xpn[tid] = ri.xp_now;
@@ -166,9 +164,12 @@ __global__ __launch_bounds__(kStdpBlock) void k_stdp(StdpArgs a)
                 const int l = slot[u];
                 const int ap = s_ap[l];
                 const int pre = ap >> 8;
-                const uint64_t h = s_hist[jl[u]] & s_win[l];
-                if (!h && !pre) continue;  // nothing happened to this synapse
-                wgt[gi[u]] = stdp_synapse(wv[u], h, ap & 0xff, pre, s_xp0[l], s_xpn[l],
+                uint64_t m0, m1;
+                window_masks(ap & 0xff, m0, m1);
+                const uint64_t h0 = s_hist[jl[u] * hw] & m0;
+                const uint64_t h1 = hw == 2 ? s_hist[jl[u] * hw + 1] & m1 : 0ull;
+                if (!h0 && !h1 && !pre) continue;  // nothing happened to this synapse
+                wgt[gi[u]] = stdp_synapse(wv[u], h0, h1, ap & 0xff, pre, s_xp0[l], s_xpn[l],
                                           pre ? s_y[jl[u]] : 0.f, s_dpow, c_pot, c_dep, mu);
                 ++written;
             }
@@ -208,6 +209,21 @@ struct RowPart {
     int j[U];    // targets (-1: no synapse)
     float w[U];  // weights
 };
+
+// History words 0 and 1 of neuron j (one 16-byte load with two words).
+template <int HW>
+__device__ __forceinline__ void gather_hist(const uint64_t *hist, int j, uint64_t &h0,
+                                            uint64_t &h1)
+{
+    if (HW == 2) {
+        const ulonglong2 v = ((const ulonglong2 *)hist)[j];
+        h0 = v.x;
+        h1 = v.y;
+    } else {
+        h0 = hist[j];
+        h1 = 0ull;
+    }
+}
 
 template <int U>
 __device__ __forceinline__ void row_part_at(RowPart<U> &p, const StdpArgs &a, int i, int nrows)
@@ -249,11 +265,11 @@ __device__ __forceinline__ void rows_issue(RowPart<U> &p, const int32_t *col, co
     }
 }
 
-template <int NT, int U>
+template <int NT, int U, int HW>
 __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int nblocks,
                                                unsigned char *s_sum)
 {
-    __shared__ float s_dpow[65];
+    __shared__ float s_dpow[kMaxAge + 1];
     const int tid = threadIdx.x;
     const int32_t *__restrict__ col = a.col;
     float *__restrict__ wgt = a.w;
@@ -273,7 +289,7 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
     RowInfo la = RowInfo{};         // lookahead: snapshot of the next row
     int la_i = gw + nwv;
     if (la_i < nrows) la = a.info[la_i];
-    for (int q = tid; q < 65; q += NT) s_dpow[q] = a.dpow[q];
+    for (int q = tid; q <= kMaxAge; q += NT) s_dpow[q] = a.dpow[q];
     const uint8_t *s_code = s_sum;
     const uint64_t *s_recent = (const uint64_t *)s_sum;
     if (a.code) {
@@ -288,24 +304,28 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
     auto step = [&](RowPart<U> &p, RowPart<U> &nx) {
         const RowInfo ri = p.ri;
         const int age = ri.age_pre & 0xff, pre = ri.age_pre >> 8;
-        const uint64_t win = age >= 64 ? ~0ull : ((1ull << age) - 1ull);
+        uint64_t m0, m1;
+        window_masks(age, m0, m1);
+        if (HW == 1) m1 = 0ull;  // lets the compiler drop the second word
         bool live[U];
-        uint64_t h[U];
+        uint64_t h[U], g[U];  // window bits of the target's history words 0 and 1
         float y[U];
         if (!pre && a.code) {
             int cd[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) cd[u] = s_code[max(p.j[u], 0)];
-            uint64_t hv[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 live[u] = p.j[u] >= 0 && cd[u] != 0;
-                hv[u] = hist[(live[u] && cd[u] == kCodeMulti) ? p.j[u] : 0];
+                gather_hist<HW>(hist, (live[u] && cd[u] == kCodeMulti) ? p.j[u] : 0, h[u], g[u]);
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const uint64_t one = 1ull << ((cd[u] - 1) & 63);
-                h[u] = !live[u] ? 0ull : (cd[u] == kCodeMulti ? hv[u] : one) & win;
+                const int pos = (cd[u] - 1) & 127;  // single spike: pos steps ago
+                const uint64_t one = 1ull << (pos & 63);
+                const bool multi = cd[u] == kCodeMulti;
+                h[u] = !live[u] ? 0ull : (multi ? h[u] : (pos < 64 ? one : 0ull)) & m0;
+                g[u] = !live[u] ? 0ull : (multi ? g[u] : (pos >= 64 ? one : 0ull)) & m1;
                 y[u] = 0.f;
             }
         } else {
@@ -321,7 +341,7 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
                 for (int u = 0; u < U; ++u) live[u] = p.j[u] >= 0;
             }
 #pragma unroll
-            for (int u = 0; u < U; ++u) h[u] = hist[live[u] ? p.j[u] : 0];
+            for (int u = 0; u < U; ++u) gather_hist<HW>(hist, live[u] ? p.j[u] : 0, h[u], g[u]);
             if (pre) {
 #pragma unroll
                 for (int u = 0; u < U; ++u) y[u] = ypost[live[u] ? p.j[u] : 0];
@@ -330,7 +350,10 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
                 for (int u = 0; u < U; ++u) y[u] = 0.f;
             }
 #pragma unroll
-            for (int u = 0; u < U; ++u) h[u] = live[u] ? (h[u] & win) : 0ull;
+            for (int u = 0; u < U; ++u) {
+                h[u] = live[u] ? (h[u] & m0) : 0ull;
+                g[u] = live[u] ? (g[u] & m1) : 0ull;
+            }
         }
         // next part: the rest of this row, else the lookahead row
         if (ri.age_pre != 0 && p.base + U * kWave < ri.len) {
@@ -352,11 +375,11 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const bool chg = live[u] && (h[u] || pre);
+            const bool chg = live[u] && (h[u] || g[u] || pre);
             float w = p.w[u];
             if (chg) {
-                w = stdp_synapse(w, h[u], age, pre, ri.xp0, ri.xp_now, y[u], s_dpow, c_pot, c_dep,
-                                 mu);
+                w = stdp_synapse(w, h[u], g[u], age, pre, ri.xp0, ri.xp_now, y[u], s_dpow, c_pot,
+                                 c_dep, mu);
                 ++written;
             }
             const uint64_t m = ballot64(chg);
@@ -375,11 +398,14 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
         atomicAdd((unsigned long long *)(a.stats + bid), (unsigned long long)written);
 }
 
+// One instance per history length: the 128-step one keeps a second word per
+// synapse in registers and takes fewer synapses per lane and part.
+template <int HW>
 __global__ __launch_bounds__(kStdpRowsBlock) void k_stdp_rows(StdpArgs a)
 {
     extern __shared__ uint4 dyn_sum[];
-    stdp_rows_body<kStdpRowsBlock, kStdpRowsUnroll>(a, blockIdx.x, gridDim.x,
-                                                    (unsigned char *)dyn_sum);
+    stdp_rows_body<kStdpRowsBlock, HW == 1 ? kStdpRowsUnroll : kStdpRowsUnroll2, HW>(
+        a, blockIdx.x, gridDim.x, (unsigned char *)dyn_sum);
 }
 
 // ---------------------------------------------------------------------------
@@ -429,7 +455,7 @@ __global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
     __shared__ float s_xp0[kDlvBatch];
     __shared__ float s_xpn[kDlvBatch];
     __shared__ int s_map[kDlvWindow];
-    __shared__ float s_dpow[65];
+    __shared__ float s_dpow[kMaxAge + 1];
     __shared__ long long sh[kDlvBlock / kWave];
     __shared__ int shi[kDlvBlock / kWave];
     const int tid = threadIdx.x;
@@ -442,15 +468,17 @@ __global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
     const int span = a.nacc * a.width;
     const int cnt = *a.cnt;  // used only once the first batch's loads are out
     for (int x = tid; x < span; x += kDlvBlock) acc[x] = 0;
+    const int hw = a.hw;
     uint64_t *s_hist = (uint64_t *)(acc + span);
-    float *s_y = (float *)(s_hist + a.width);
+    float *s_y = (float *)(s_hist + (size_t)a.width * hw);
     if (a.plastic) {
         const int jn = min(a.width, a.n - base);
         for (int x = tid; x < jn; x += kDlvBlock) {
-            s_hist[x] = a.hist[base + x];
+            for (int q = 0; q < hw; ++q)
+                s_hist[x * hw + q] = a.hist[(int64_t)(base + x) * hw + q];
             s_y[x] = a.ypost[base + x];
         }
-        for (int x = tid; x < 65; x += kDlvBlock) s_dpow[x] = a.dpow[x];
+        for (int x = tid; x <= kMaxAge; x += kDlvBlock) s_dpow[x] = a.dpow[x];
     }
     const int piv_stride = a.n_slices + 1;
     const int32_t *__restrict__ col = a.col;
@@ -543,8 +571,10 @@ __global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
                     const int l = slot[u];
                     if (off[u] >= s_plen[l]) continue;  // not plastic
                     const int age = s_age[l];
-                    const uint64_t win = age >= 64 ? ~0ull : ((1ull << age) - 1ull);
-                    wv[u] = stdp_synapse(wv[u], s_hist[tgt[u]] & win, age, 1, s_xp0[l],
+                    uint64_t m0, m1;
+                    window_masks(age, m0, m1);
+                    const uint64_t h1 = hw == 2 ? s_hist[tgt[u] * 2 + 1] & m1 : 0ull;
+                    wv[u] = stdp_synapse(wv[u], s_hist[tgt[u] * hw] & m0, h1, age, 1, s_xp0[l],
                                          s_xpn[l], s_y[tgt[u]], s_dpow, c_pot, c_dep, mu);
                     wgt[gi[u]] = wv[u];
                     ++written;
@@ -653,13 +683,17 @@ hipError_t launch_stdp(hipStream_t s, const StdpArgs &a, int blocks, size_t lds)
 hipError_t launch_stdp_rows(hipStream_t s, const StdpArgs &a, int blocks)
 {
     static std::mutex mu;
-    static int granted = 64 * 1024;
+    static int granted[2] = {64 * 1024, 64 * 1024};
     const size_t lds = a.code     ? (((size_t)a.n + 15) / 16) * 16
                        : a.recent ? (size_t)a.nw * sizeof(uint64_t)
                                   : 0;
-    const hipError_t e = allow_dynamic_lds((const void *)k_stdp_rows, (int)lds, mu, granted);
+    const void *kern = a.hw == 2 ? (const void *)k_stdp_rows<2> : (const void *)k_stdp_rows<1>;
+    const hipError_t e = allow_dynamic_lds(kern, (int)lds, mu, granted[a.hw == 2]);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_stdp_rows, dim3(blocks), dim3(kStdpRowsBlock), lds, s, a);
+    if (a.hw == 2)
+        hipLaunchKernelGGL(k_stdp_rows<2>, dim3(blocks), dim3(kStdpRowsBlock), lds, s, a);
+    else
+        hipLaunchKernelGGL(k_stdp_rows<1>, dim3(blocks), dim3(kStdpRowsBlock), lds, s, a);
     return hipGetLastError();
 }
 

@@ -25,9 +25,10 @@ struct snn_ctx {
     int32_t n_plastic_rows = 0, ref_steps = 0, dlv_blocks = 0;
     int32_t stdp_mult = 1, stdp_width = 0, stdp_groups = 0, stdp_chunks = 1, stdp_grid = 0;
     int32_t info_blocks = 1, syn_slots = 1;
+    int32_t hw = 1;  // 64-bit history words per neuron
     float k_m = 0, v_th = 0, v_reset = 0, v_inf = 0, d_e = 0, d_i = 0, j_ext = 0;
     float d_minus = 0, c_pot = 0, c_dep = 0, mu = 0;
-    float dpow[65] = {};
+    float dpow[kMaxAge + 1] = {};
     uint32_t fire_thr = 0;
 
     // workspace plan
@@ -118,6 +119,8 @@ snn_status validate(snn_ctx *c, const snn_config &k)
         return fail(c, SNN_EINVAL, "stdp_chunks must be in [0, 1024]");
     if (k.stdp_layout < 0 || k.stdp_layout > 1)
         return fail(c, SNN_EINVAL, "stdp_layout must be 0 or 1");
+    if (k.history_bits != 0 && k.history_bits != 64 && k.history_bits != 128)
+        return fail(c, SNN_EINVAL, "history_bits must be 64 or 128 (0: 64)");
     if (k.stdp_filter < 0 || k.stdp_filter > 3)
         return fail(c, SNN_EINVAL, "stdp_filter must be in [0, 3]");
     if (k.stdp_filter == 1 && (int64_t)k.n + 16 > kCodeMax)
@@ -165,6 +168,7 @@ void derive(snn_ctx *c)
     c->nw = (k.n + 63) / 64;
     c->nblk = (k.n + kBlock - 1) / kBlock;
     c->nacc = k.neuron_model == SNN_LIF_CUBA ? 2 : 1;
+    c->hw = k.history_bits == 128 ? 2 : 1;
     c->n_slices = (k.n + k.slice_width - 1) / k.slice_width;
     c->chunks = k.spike_chunks;
     c->delay = k.delay_steps;
@@ -183,7 +187,8 @@ void derive(snn_ctx *c)
     c->fire_thr = thr <= 0 ? 0u : thr >= 4294967295.0 ? 0xFFFFFFFFu : (uint32_t)thr;
     if (k.plastic != SNN_PLASTIC_NONE) {
         const double dp = std::exp(-k.dt_ms / k.tau_plus_ms);
-        for (int q = 0; q <= 64; ++q) c->dpow[q] = (float)std::pow(dp, (double)q);
+        static_assert(sizeof(c->dpow) == sizeof(float) * (kMaxAge + 1), "decay table size");
+        for (int q = 0; q <= kMaxAge; ++q) c->dpow[q] = (float)std::pow(dp, (double)q);
         c->d_minus = (float)std::exp(-k.dt_ms / k.tau_minus_ms);
         c->c_pot = (float)(k.lambda * std::pow(k.w0, 1.0 - k.mu));
         c->c_dep = (float)(k.lambda * k.alpha);
@@ -216,7 +221,7 @@ void plan_workspace(snn_ctx *c, uint8_t *base)
     c->ref = p.take<int32_t>(n);
     c->ie = p.take<float>(n);
     c->ii = p.take<float>(n);
-    c->hist = p.take<uint64_t>(n);
+    c->hist = p.take<uint64_t>(n * c->hw);
     c->ypost = p.take<float>(n);
     c->t_last = p.take<int32_t>(n);
     c->xpre = p.take<float>(n);
@@ -339,6 +344,7 @@ snn_status launch_step_neurons(snn_ctx *c)
     a.ie = c->ie;
     a.ii = c->ii;
     a.hist = c->hist;
+    a.hw = c->hw;
     a.ypost = c->ypost;
     a.t_last = c->t_last;
     a.apart = c->apart;
@@ -396,13 +402,14 @@ snn_status launch_step_neurons(snn_ctx *c)
     b.row_ptr = c->row_ptr;
     b.pend = c->pend;
     b.hist = c->hist;
+    b.hw = c->hw;
     b.t_last = c->t_last;
     b.xpre = c->xpre;
     b.err = c->err_flag;
     b.info_stats = c->n_plastic_rows > 0 ? c->info_stats : nullptr;
     b.t = c->t;
     b.dm1 = c->delay - 1;
-    for (int q = 0; q <= 64; ++q) b.dpow[q] = c->dpow[q];
+    for (int q = 0; q <= kMaxAge; ++q) b.dpow[q] = c->dpow[q];
     st = check_hip(c, launch_compact(c->stream, b), "compaction kernel");
     if (st) return st;
     c->last_neuron_t = c->t;
@@ -413,7 +420,7 @@ size_t dlv_lds_bytes(const snn_ctx *c)
 {
     size_t b = (size_t)c->cfg.slice_width * c->nacc * sizeof(long long);
     if (c->n_plastic_rows > 0)
-        b += (size_t)c->cfg.slice_width * (sizeof(uint64_t) + sizeof(float));
+        b += (size_t)c->cfg.slice_width * (c->hw * sizeof(uint64_t) + sizeof(float));
     return b;
 }
 
@@ -431,6 +438,7 @@ StdpArgs stdp_args(snn_ctx *c, bool flush)
     a.w = c->w;
     a.piv = c->piv;
     a.hist = c->hist;
+    a.hw = c->hw;
     a.ypost = c->ypost;
     a.n = c->n;
     a.n_slices = c->n_slices;
@@ -451,7 +459,7 @@ StdpArgs stdp_args(snn_ctx *c, bool flush)
     a.code = fresh && (f == 1 || (f == 0 && fits_code)) ? c->code : nullptr;
     a.recent = fresh && (f == 2 || (f == 0 && !fits_code && fits_map)) ? c->recent : nullptr;
     a.nw = c->nw;
-    for (int q = 0; q <= 64; ++q) a.dpow[q] = c->dpow[q];
+    for (int q = 0; q <= kMaxAge; ++q) a.dpow[q] = c->dpow[q];
     return a;
 }
 
@@ -472,12 +480,13 @@ snn_status launch_plasticity(snn_ctx *c, bool flush, hipStream_t s)
         r.row_ptr = c->row_ptr;
         r.pend = c->pend;
         r.hist = c->hist;
+        r.hw = c->hw;
         r.t_last = c->t_last;
         r.xpre = c->xpre;
         r.info = c->info;
         r.err = c->err_flag;
         r.stats = c->info_stats;
-        for (int q = 0; q <= 64; ++q) r.dpow[q] = c->dpow[q];
+        for (int q = 0; q <= kMaxAge; ++q) r.dpow[q] = c->dpow[q];
         snn_status st = check_hip(c, launch_row_info(s, r, c->n_plastic_rows),
                                   "STDP row snapshot kernel");
         if (st) return st;
@@ -485,7 +494,7 @@ snn_status launch_plasticity(snn_ctx *c, bool flush, hipStream_t s)
     StdpArgs a = stdp_args(c, flush);
     if (c->cfg.stdp_layout == 0)
         return check_hip(c, launch_stdp_rows(s, a, kStdpRowsBlocks), "STDP kernel");
-    const size_t lds = (size_t)c->stdp_width * (sizeof(uint64_t) + sizeof(float));
+    const size_t lds = (size_t)c->stdp_width * (c->hw * sizeof(uint64_t) + sizeof(float));
     return check_hip(c, launch_stdp(s, a, c->stdp_grid, lds), "STDP kernel");
 }
 
@@ -520,6 +529,7 @@ DeliverArgs deliver_args(snn_ctx *c)
     a.plastic = c->n_plastic_rows > 0;
     a.txinfo = c->txinfo;
     a.hist = c->hist;
+    a.hw = c->hw;
     a.ypost = c->ypost;
     a.t_last = c->t_last;
     a.xpre = c->xpre;
@@ -527,7 +537,7 @@ DeliverArgs deliver_args(snn_ctx *c)
     a.c_pot = c->c_pot;
     a.c_dep = c->c_dep;
     a.mu = c->mu;
-    for (int q = 0; q <= 64; ++q) a.dpow[q] = c->dpow[q];
+    for (int q = 0; q <= kMaxAge; ++q) a.dpow[q] = c->dpow[q];
     return a;
 }
 
@@ -605,7 +615,8 @@ snn_status snn_create(const snn_config *cfg, void *hip_stream, snn_ctx **out)
     const int stat_stdp = stdp_static_bytes();
     if (stat < 0 || stat_stdp < 0) return fail(c, SNN_EDEVICE, "cannot query the kernels");
     int64_t need = (int64_t)cfg->slice_width * 8 * (cfg->neuron_model == SNN_LIF_CUBA ? 2 : 1);
-    if (cfg->plastic != SNN_PLASTIC_NONE) need += (int64_t)cfg->slice_width * 12;
+    const int hw = cfg->history_bits == 128 ? 2 : 1;
+    if (cfg->plastic != SNN_PLASTIC_NONE) need += (int64_t)cfg->slice_width * (8 * hw + 4);
     if (need + stat > lds_max)
         return fail(c, SNN_EINVAL,
                     "slice delivery needs %lld B of LDS (accumulator%s) besides %d B of "
@@ -615,7 +626,7 @@ snn_status snn_create(const snn_config *cfg, void *hip_stream, snn_ctx **out)
     derive(c);
     if (c->n_plastic_rows > 0) {
         // STDP target groups: mult * W neurons, staged at 12 B each in LDS
-        const int64_t per = sizeof(uint64_t) + sizeof(float);
+        const int64_t per = hw * sizeof(uint64_t) + sizeof(float);
         int mult = cfg->stdp_slice_mult;
         if (mult == 0) {
             mult = 4096 / cfg->slice_width;
@@ -667,7 +678,7 @@ snn_status snn_bind_workspace(snn_ctx *c, void *device_ptr, size_t bytes)
     c->ws = (uint8_t *)device_ptr;
     plan_workspace(c, c->ws);
     hipError_t e = launch_init_state(c->stream, c->v, c->ref, c->ie, c->ii, c->hist, c->ypost,
-                                     c->t_last, c->xpre, c->n);
+                                     c->t_last, c->xpre, c->n, c->hw);
     if (e == hipSuccess)
         e = launch_fill_ll(c->stream, c->apart, (int64_t)c->chunks * c->nacc * c->n, 0);
     if (e == hipSuccess) e = launch_fill_f32(c->stream, c->ain, (int64_t)c->nacc * c->n, 0.f);
@@ -950,7 +961,7 @@ snn_status snn_set_state(snn_ctx *c, const snn_state_view *in)
     const Item items[] = {
         {c->v, in->v, n * 4},           {c->ref, in->refractory, n * 4},
         {c->ie, in->i_exc, n * 4},      {c->ii, in->i_inh, n * 4},
-        {c->hist, in->hist, n * 8},     {c->ypost, in->trace_post, n * 4},
+        {c->hist, in->hist, n * 8 * c->hw},     {c->ypost, in->trace_post, n * 4},
         {c->t_last, in->t_last, n * 4}, {c->xpre, in->trace_pre, n * 4},
         {c->ain, in->input_exc, n * 4},
         {c->nacc == 2 ? c->ain + n : nullptr, in->input_inh, n * 4},

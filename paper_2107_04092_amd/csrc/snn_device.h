@@ -142,7 +142,7 @@ __device__ __forceinline__ void fill_segment_map(int *mark, int len, int *sh)
 // Snapshot of plastic row k for an update at step t (see RowInfo). Returns
 // 1 if the row has something to bring up to date.
 __device__ __forceinline__ int make_row_info(RowInfo &ri, int k, int64_t t, bool pre_allowed,
-                                             int dm1, const int64_t *row_ptr,
+                                             int dm1, int hw, const int64_t *row_ptr,
                                              const int32_t *pend, const uint64_t *hist,
                                              const int32_t *t_last, const float *xpre,
                                              const float *dpow, int32_t *err)
@@ -158,26 +158,41 @@ __device__ __forceinline__ int make_row_info(RowInfo &ri, int k, int64_t t, bool
         ri.xp_now = ri.xp0;
         return 0;
     }
-    if (age > 64) {
+    if (age > 64 * hw) {
         // the plasticity part was skipped for this row: posts older than the
-        // history word are lost; flag it and stay inside the table
+        // history are lost; flag it and stay inside the table
         atomicOr(err, kErrWindow);
-        age = 64;
+        age = 64 * hw;
     }
-    const int pre = pre_allowed ? (int)((hist[k] >> dm1) & 1ull) : 0;
+    const int pre = pre_allowed ? (int)((hist[(int64_t)k * hw] >> dm1) & 1ull) : 0;
     ri.len = pend[k];
     ri.age_pre = age | (pre << 8);
     ri.xp_now = __fadd_rn(__fmul_rn(ri.xp0, dpow[age]), (float)pre);
     return 1;
 }
 
-// One synapse k->j brought from t_last to t (age = t - t_last, window bits
-// h = hist[j] & (2^age - 1), pre = transmitting at t). Returns the new weight.
-__device__ __forceinline__ float stdp_synapse(float w, uint64_t h, int age, int pre, float xp0,
-                                              float xp_now, float y, const float *dpow,
-                                              float c_pot, float c_dep, float mu)
+// Masks of the window of a row of age `age` (bits age-1 .. 0 of the
+// history, word 0 = the last 64 steps, word 1 = the 64 before).
+__device__ __forceinline__ void window_masks(int age, uint64_t &m0, uint64_t &m1)
 {
-    uint64_t older = h & ~1ull;
+    m0 = age >= 64 ? ~0ull : ((1ull << age) - 1ull);
+    m1 = age >= 128 ? ~0ull : age > 64 ? ((1ull << (age - 64)) - 1ull) : 0ull;
+}
+
+// One synapse k->j brought from t_last to t (age = t - t_last; h0, h1 the
+// window bits of the target's history words 0 and 1; pre = transmitting at
+// t). Returns the new weight.
+__device__ __forceinline__ float stdp_synapse(float w, uint64_t h0, uint64_t h1, int age,
+                                              int pre, float xp0, float xp_now, float y,
+                                              const float *dpow, float c_pot, float c_dep,
+                                              float mu)
+{
+    while (h1) {  // posts 64 .. 127 steps ago, oldest first
+        const int bit = 63 - __clzll((long long)h1);
+        h1 ^= 1ull << bit;
+        w = w + c_pot * pow_mu(w, mu) * __fmul_rn(xp0, dpow[age - 64 - bit]);
+    }
+    uint64_t older = h0 & ~1ull;
     while (older) {  // posts before t, oldest first
         const int bit = 63 - __clzll((long long)older);
         older ^= 1ull << bit;
@@ -187,7 +202,7 @@ __device__ __forceinline__ float stdp_synapse(float w, uint64_t h, int age, int 
         w = w - c_dep * w * y;
         w = fmaxf(w, 0.f);
     }
-    if (h & 1ull) w = w + c_pot * pow_mu(w, mu) * xp_now;  // post at t
+    if (h0 & 1ull) w = w + c_pot * pow_mu(w, mu) * xp_now;  // post at t
     return w;
 }
 

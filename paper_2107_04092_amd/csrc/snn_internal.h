@@ -17,6 +17,11 @@ constexpr int kStdpUnroll = 4;       // elements per thread with loads in flight
 constexpr int kStdpWindow = kStdpBlock * kStdpUnroll;  // elements per segment map
 constexpr int kGlobalMaxBlocks = 2048;
 constexpr int kLdsBytes = 160 * 1024;
+// Spike histories: hw 64-bit words per neuron (1 or 2), neuron-major; word 0
+// bit b = step t-b, word 1 bit b = step t-64-b. A plastic row is forced once
+// its last update is 64 hw steps old, so every window fits the history.
+constexpr int kMaxHistWords = 2;
+constexpr int kMaxAge = 64 * kMaxHistWords;
 
 // Delivered inputs are accumulated exactly as 64-bit fixed-point integers with
 // 32 fractional bits (sums of |x| < 2^31 mV, resolution 2^-32 mV); integer
@@ -52,7 +57,7 @@ struct NeuronArgs {
     uint64_t *recent;       // neurons with a spike in the last 64 steps (hist != 0)
     int32_t *blk_spk, *blk_tx, *blk_f;
     int64_t t;
-    int32_t n, n_exc, model, n_plastic_rows, dm1, ref_steps, poisson_len, n_parts;
+    int32_t n, n_exc, model, n_plastic_rows, dm1, ref_steps, poisson_len, n_parts, hw;
     float k_m, v_th, v_reset, v_inf, d_e, d_i, j_ext, d_minus;
     uint32_t fire_thr;
     uint64_t seed;
@@ -67,7 +72,7 @@ struct CompactArgs {
     int32_t *spk_list, *spk_cnt;   // ascending spikes of step t (delay-ring slot)
     int32_t *row_list, *row_cnt;   // forced plastic rows
     int64_t *gstats;
-    int32_t n, nw, n_plastic_rows;
+    int32_t n, nw, n_plastic_rows, hw;
     // snapshots of the plastic rows to update at step t (see RowInfo): forced
     // rows in list order, transmitting rows at their position in the
     // transmitted list (which is the delay-ring list of step t-D+1)
@@ -82,7 +87,7 @@ struct CompactArgs {
     int64_t *info_stats;     // [gridDim.x][kStFields]
     int64_t t;
     int32_t dm1;
-    float dpow[65];
+    float dpow[kMaxAge + 1];
 };
 
 // Snapshot of one row to bring up to date, taken before the synapse pass;
@@ -92,7 +97,7 @@ struct RowInfo {
     long long rs;    // first edge of the row
     int32_t k;       // row (source neuron)
     int32_t len;     // plastic prefix length; 0 = nothing to do
-    int32_t age_pre; // age (1..64) | pre << 8
+    int32_t age_pre; // age (1 .. 64 hw) | pre << 8
     float xp0;       // pre trace at the previous update
     float xp_now;    // pre trace after this update
     int32_t pad;
@@ -102,7 +107,7 @@ struct RowInfoArgs {
     const int32_t *rows;     // list mode: rows to update; nullptr in flush mode
     const int32_t *row_cnt;
     int32_t n_rows_all;      // flush mode: rows 0 .. n_rows_all-1
-    int32_t dm1;
+    int32_t dm1, hw;
     int64_t t;               // list mode: step t; flush mode: last completed step
     const int64_t *row_ptr;
     const int32_t *pend;
@@ -110,9 +115,9 @@ struct RowInfoArgs {
     const int32_t *t_last;
     const float *xpre;
     RowInfo *info;
-    int32_t *err;            // kErrWindow when a row fell more than 64 steps behind
+    int32_t *err;            // kErrWindow when a row fell more than 64 hw steps behind
     int64_t *stats;          // [gridDim.x][kStFields]
-    float dpow[65];          // d_plus^i, i = 0..64
+    float dpow[kMaxAge + 1]; // d_plus^i, i = 0..kMaxAge
 };
 
 struct StdpArgs {
@@ -127,7 +132,7 @@ struct StdpArgs {
     const int32_t *piv;      // [n][S+1] delivery pivots, used at multiples of `mult`
     const uint64_t *hist;
     const float *ypost;
-    int32_t n, n_slices, mult, width, n_groups, chunks, n_work, target_limit;
+    int32_t n, n_slices, mult, width, n_groups, chunks, n_work, target_limit, hw;
     float c_pot, c_dep, mu;
     int64_t *stats;          // [gridDim.x] weights written
     // row-wise layout: per-neuron history codes or the spike-recency bitmap
@@ -135,7 +140,7 @@ struct StdpArgs {
     const uint8_t *code;
     const uint64_t *recent;
     int32_t nw;              // words of `recent`
-    float dpow[65];
+    float dpow[kMaxAge + 1];
 };
 
 struct DeliverArgs {
@@ -148,7 +153,7 @@ struct DeliverArgs {
     long long *apart;        // fixed-point partial inputs [C][nacc][n]
     float *ain;              // fp32 input [nacc][n], written directly when C == 1
     int64_t part_stride;
-    int32_t n, n_exc, width, n_slices, chunks, nacc, n_work;
+    int32_t n, n_exc, width, n_slices, chunks, nacc, n_work, hw;
     int64_t *stats;          // [gridDim.x][2]: events delivered, weights written
     // plasticity of the transmitting rows, fused into slice delivery
     int32_t plastic;         // 0: no plastic rows
@@ -159,7 +164,7 @@ struct DeliverArgs {
     float *xpre;
     int64_t t;
     float c_pot, c_dep, mu;
-    float dpow[65];
+    float dpow[kMaxAge + 1];
 };
 
 struct GraphArgs {
@@ -180,7 +185,7 @@ struct GraphArgs {
 // status of the last kernel they started.
 hipError_t launch_init_state(hipStream_t s, float *v, int32_t *ref, float *ie, float *ii,
                              uint64_t *hist, float *ypost, int32_t *t_last, float *xpre,
-                             int32_t n);
+                             int32_t n, int32_t hw);
 hipError_t launch_fill_f32(hipStream_t s, float *p, int64_t count, float value);
 hipError_t launch_fill_i64(hipStream_t s, int64_t *p, int64_t count, int64_t value);
 hipError_t launch_fill_i32(hipStream_t s, int32_t *p, int64_t count, int32_t value);
@@ -192,7 +197,8 @@ hipError_t launch_row_info(hipStream_t s, const RowInfoArgs &a, int64_t max_rows
 hipError_t launch_stdp(hipStream_t s, const StdpArgs &a, int blocks, size_t lds);
 hipError_t launch_stdp_rows(hipStream_t s, const StdpArgs &a, int blocks);
 constexpr int kStdpRowsBlock = 1024;   // threads of the row-wise STDP kernel
-constexpr int kStdpRowsUnroll = 8;     // synapses per lane and row part
+constexpr int kStdpRowsUnroll = 8;     // synapses per lane and row part (64-step histories)
+constexpr int kStdpRowsUnroll2 = 4;    // the same with 128-step histories
 constexpr int kStdpRowsBlocks = 256;   // its persistent grid (one workgroup per CU)
 constexpr int kCodeMax = 147456;       // LDS bytes of history codes one row-STDP workgroup stages
 constexpr int kRecentMaxWords = 16384; // LDS-staged spike-recency bitmap: up to 1M neurons

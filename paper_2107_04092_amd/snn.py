@@ -33,7 +33,8 @@ class snn_config(ctypes.Structure):
     _fields_ = [
         ("n", _i32), ("n_exc", _i32), ("delay_steps", _i32), ("slice_width", _i32),
         ("spike_chunks", _i32), ("stdp_slice_mult", _i32), ("stdp_chunks", _i32),
-        ("stdp_layout", _i32), ("stdp_filter", _i32), ("neuron_model", _i32),
+        ("stdp_layout", _i32), ("stdp_filter", _i32), ("history_bits", _i32),
+        ("neuron_model", _i32),
         ("plastic", _i32), ("poisson_len", _i32),
         ("dt_ms", _f64), ("tau_m_ms", _f64), ("v_th", _f64), ("v_reset", _f64),
         ("v_inf", _f64), ("tau_ref_ms", _f64), ("tau_e_ms", _f64), ("tau_i_ms", _f64),
@@ -224,7 +225,8 @@ def snn_reset_stats(ctx):
 # ---- configuration marshalling ---------------------------------------------
 
 def config_from_preset(p, poisson_table=(), slice_width=None, spike_chunks=None,
-                       stdp_slice_mult=0, stdp_chunks=0, stdp_layout=0, stdp_filter=0):
+                       stdp_slice_mult=0, stdp_chunks=0, stdp_layout=0, stdp_filter=0,
+                       history_bits=64):
     """snn_config from a preset-like object with the physical parameters."""
     c = snn_config()
     c.n, c.n_exc, c.delay_steps = p.n, p.n_exc, p.delay
@@ -233,6 +235,7 @@ def config_from_preset(p, poisson_table=(), slice_width=None, spike_chunks=None,
     c.stdp_slice_mult, c.stdp_chunks = stdp_slice_mult, stdp_chunks
     c.stdp_layout = stdp_layout
     c.stdp_filter = stdp_filter
+    c.history_bits = history_bits
     c.neuron_model, c.plastic = p.model, p.plastic
     c.dt_ms, c.tau_m_ms, c.v_th, c.v_reset, c.v_inf = p.dt, p.tau_m, p.v_th, p.v_reset, p.v_inf
     c.tau_ref_ms, c.tau_e_ms, c.tau_i_ms = p.tau_ref, p.tau_e, p.tau_i
@@ -262,6 +265,7 @@ class Network:
         self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
         self.cfg = cfg
         self.n = cfg.n
+        self.history_words = 2 if cfg.history_bits == 128 else 1
         self.ctx = snn_create(cfg, self.stream.cuda_stream)
         nbytes = snn_workspace_size(self.ctx)
         with torch.cuda.stream(self.stream):
@@ -359,7 +363,8 @@ class Network:
         out = {"t": v.t}
         for name, dt, cnt in (("v", torch.float32, n), ("refractory", torch.int32, n),
                               ("i_exc", torch.float32, n), ("i_inh", torch.float32, n),
-                              ("hist", torch.int64, n), ("trace_post", torch.float32, n),
+                              ("hist", torch.int64, n * self.history_words),
+                              ("trace_post", torch.float32, n),
                               ("t_last", torch.int32, n), ("trace_pre", torch.float32, n),
                               ("input_exc", torch.float32, n), ("input_inh", torch.float32, n),
                               ("spike_mask", torch.int64, nw), ("spike_list", torch.int32, n),

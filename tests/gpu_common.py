@@ -70,13 +70,21 @@ def assert_close(g, o, what, rtol=RTOL, atol=ATOL, terms=None):
                                                 g[i], o[i], diag))
 
 
+def oracle_hist(st, words):
+    """The oracle's spike history in the GPU layout (words per neuron, neuron-major)."""
+    if words == 1:
+        return st["hist"]
+    return np.stack([st["hist"], st["hist_old"]], axis=1).reshape(-1)
+
+
 def force_from_oracle(net, o, t):
     """Teacher forcing: hand the oracle's neuron state and pending input to the GPU."""
     torch = torch_mod()
     st = o.neurons()
     a_e, a_i = o.input()
+    h = np.ascontiguousarray(oracle_hist(st, net.history_words))
     kw = dict(v=torch.from_numpy(st["v"]), refractory=torch.from_numpy(st["refractory"]),
-              hist=torch.from_numpy(st["hist"].view(np.int64)),
+              hist=torch.from_numpy(h.view(np.int64)),
               input_exc=torch.from_numpy(a_e))
     if net.cfg.neuron_model == snn.SNN_LIF_CUBA:
         kw.update(i_exc=torch.from_numpy(st["i_exc"]), i_inh=torch.from_numpy(st["i_inh"]),
@@ -103,7 +111,7 @@ def compare_step(net, o, mode_name, t, check_rows=True):
     cnt = int(to_np(s["spike_count"])[0])
     assert cnt == len(lst), ("spike count", t, cnt, len(lst))
     assert np.array_equal(to_np(s["spike_list"])[:cnt], lst), ("spike list", t)
-    assert np.array_equal(hist_np(s["hist"]), ost["hist"]), ("history", t)
+    assert np.array_equal(hist_np(s["hist"]), oracle_hist(ost, net.history_words)), ("history", t)
     assert np.array_equal(to_np(s["v"]).view(np.uint32), ost["v"].view(np.uint32)), ("V", t)
     assert np.array_equal(to_np(s["refractory"]), ost["refractory"]), ("refractory", t)
     a_e, a_i = o.input()
@@ -114,7 +122,7 @@ def compare_step(net, o, mode_name, t, check_rows=True):
         assert np.array_equal(to_np(s["i_inh"]).view(np.uint32), ost["i_inh"].view(np.uint32))
     rows = None
     if check_rows and net.cfg.plastic != snn.SNN_PLASTIC_NONE:
-        # rows made current at this step: those forced by the 64-step window
+        # rows made current at this step: those forced by the history window
         # and the plastic rows that transmitted
         nf = int(to_np(s["stdp_row_count"])[0])
         nt = int(to_np(s["tx_count"])[0])

@@ -18,12 +18,13 @@ from gpu_common import gpu_net, oracle_net, to_np, hist_np, assert_close, log
 pytestmark = pytest.mark.gpu
 
 
-def test_stress_full_size_sampled_parity():
+@pytest.mark.parametrize("hbits", [64, 128])
+def test_stress_full_size_sampled_parity(hbits):
     from oracle import oracle
     p = wl.preset("stress")
-    log("full-size stress: build n=%d fanout=%d W=%d C=%d" % (
-        p.n, p.p_or_fanout, p.slice_width, p.spike_chunks))
-    net = gpu_net(p)
+    log("full-size stress: build n=%d fanout=%d W=%d C=%d history=%d" % (
+        p.n, p.p_or_fanout, p.slice_width, p.spike_chunks, hbits))
+    net = gpu_net(p, history_bits=hbits)
     o = oracle_net(p, build=False)
     F = int(p.p_or_fanout)
     w_init = float(np.float32(p.w_exc))

@@ -34,34 +34,36 @@ CASES = [
 ]
 
 
+@pytest.mark.parametrize("hbits", [64, 128], ids=["h64", "h128"])
 @pytest.mark.parametrize("mode,layout,filt", [(LDS, 0, 1), (LDS, 0, 2), (LDS, 1, 0),
                                               (GLOBAL, 0, 3)],
                          ids=["lds-rowstdp-codes", "lds-rowstdp-bitmap", "lds-slicestdp",
                               "global-rowstdp-gather"])
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "%s-%s" % (c[0], c[1].get("n", "")))
-def test_teacher_forced_parity(case, mode, layout, filt):
+def test_teacher_forced_parity(case, mode, layout, filt, hbits):
     name, kw, steps, width, chunks = case
     p = wl.preset(name, **kw)
-    log("parity %s %s mode=%d layout=%d filter=%d W=%d C=%d steps=%d" % (
-        name, kw, mode, layout, filt, width, chunks, steps))
+    log("parity %s %s mode=%d layout=%d filter=%d history=%d W=%d C=%d steps=%d" % (
+        name, kw, mode, layout, filt, hbits, width, chunks, steps))
     net, o, cnt = teacher_forced_run(p, steps, mode, slice_width=width, spike_chunks=chunks,
-                                     stdp_layout=layout, stdp_filter=filt)
+                                     stdp_layout=layout, stdp_filter=filt, history_bits=hbits)
     assert cnt["spikes"] > 0
     if p.plastic != PLASTIC_NONE:
         assert cnt["rows"] > 0 and cnt["weights"] > 0
         net.flush_plasticity()
         compare_all_plastic_weights(net, o)
         st = net.stats()
-        assert st["stdp_forced_rows"] > 0  # rows idle for 64 steps were forced
+        assert st["stdp_forced_rows"] > 0  # rows idle for the whole history were forced
     st = net.stats()
     assert st["steps"] == steps
     assert st["spikes"] == cnt["spikes"]
 
 
-@pytest.mark.parametrize("width,chunks,fanout,mult,schunks", [
-    (64, 1, 300, 1, 1), (2048, 2, 300, 0, 0), (4096, 1, 3000, 1, 1), (1024, 64, 300, 3, 7),
-    (640, 1, 300, 4, 300), (1024, 3, 400, 0, 0)])
-def test_slice_shapes(width, chunks, fanout, mult, schunks):
+@pytest.mark.parametrize("width,chunks,fanout,mult,schunks,hbits", [
+    (64, 1, 300, 1, 1, 64), (2048, 2, 300, 0, 0, 64), (4096, 1, 3000, 1, 1, 64),
+    (1024, 64, 300, 3, 7, 64), (640, 1, 300, 4, 300, 128), (1024, 3, 400, 0, 0, 128),
+    (2048, 1, 300, 2, 5, 128)])
+def test_slice_shapes(width, chunks, fanout, mult, schunks, hbits):
     """Delivery segments from 1 to ~600 entries, one to many chunks, more
     spikes (and rows) per workgroup than one staging batch holds; STDP target
     groups of 1..8 slices shared by 1..300 workgroups."""
@@ -70,7 +72,8 @@ def test_slice_shapes(width, chunks, fanout, mult, schunks):
                                                                  schunks))
     layout = 1 if mult else 0
     net, o, _ = teacher_forced_run(p, 70, LDS, slice_width=width, spike_chunks=chunks,
-                                   stdp_slice_mult=mult, stdp_chunks=schunks, stdp_layout=layout)
+                                   stdp_slice_mult=mult, stdp_chunks=schunks, stdp_layout=layout,
+                                   history_bits=hbits)
     net.flush_plasticity()
     compare_all_plastic_weights(net, o)
 
@@ -104,15 +107,18 @@ def test_out_of_order_calls_rejected():
         net.deliver_spikes(7)
 
 
-def test_silent_network():
+@pytest.mark.parametrize("hbits", [64, 128])
+def test_silent_network(hbits):
     """No spikes at all: empty lists, zero input, rows only forced."""
     p = wl.preset("stress", n=1500, p_or_fanout=50, p_fire=0.0)
-    net, o, cnt = teacher_forced_run(p, 140, LDS, slice_width=512, spike_chunks=2)
+    net, o, cnt = teacher_forced_run(p, 300, LDS, slice_width=512, spike_chunks=2,
+                                     history_bits=hbits)
     assert cnt["spikes"] == 0
     st = net.stats()
     assert st["delivered_events"] == 0
-    # row k starts 1 + (k mod 64) steps old: forced at 63 - (k mod 64) + 64 i
-    want = sum(len(range(63 - (k % 64), 140, 64)) for k in range(1500))
+    # row k starts 1 + (k mod H) steps old: forced at H-1 - (k mod H) + H i
+    H = hbits
+    want = sum(len(range(H - 1 - (k % H), 300, H)) for k in range(1500))
     assert st["stdp_forced_rows"] == want
     assert st["stdp_weights_written"] == 0
     assert not to_np(net.state()["input_exc"]).any()
