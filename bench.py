@@ -42,6 +42,9 @@ def parse():
     ap.add_argument("--stdp-filter", choices=["auto", "codes", "bitmap", "none"],
                     default="auto")
     ap.add_argument("--history-bits", type=int, choices=[64, 128], default=64)
+    ap.add_argument("--plasticity", choices=["lazy-event", "lazy", "naive"],
+                    default="lazy-event",
+                    help="plasticity algorithm (Fig. 2(c), (b), (a))")
     ap.add_argument("--stdp-mult", type=int, default=0)
     ap.add_argument("--stdp-chunks", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -165,7 +168,9 @@ def main():
                                  stdp_layout=0 if args.stdp_layout == "rows" else 1,
                                  stdp_filter=["auto", "codes", "bitmap", "none"].index(
                                      args.stdp_filter),
-                                 history_bits=args.history_bits)
+                                 history_bits=args.history_bits,
+                                 plasticity_algorithm=["lazy-event", "lazy", "naive"].index(
+                                     args.plasticity))
     t0 = time.time()
     net = snn.Network(cfg, stream=stream, device=dev)
     e = net.build_random(p.graph_kind, p.p_or_fanout, p.w_exc, p.w_inh)
@@ -279,6 +284,7 @@ def main():
             "n": p.n, "synapses": e, "slice_width": width, "spike_chunks": chunks,
             "delivery": args.mode, "stdp_layout": args.stdp_layout,
             "stdp_filter": args.stdp_filter, "history_bits": args.history_bits,
+            "plasticity": args.plasticity,
             "stdp_slice_mult": args.stdp_mult, "stdp_chunks": args.stdp_chunks, "seed": p.seed,
         },
         "roofline": roofline,

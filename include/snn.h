@@ -125,6 +125,15 @@ typedef struct snn_config {
                              Rows idle for that many steps are forced, so 128
                              halves the forced updates of silent rows; the
                              weights are the same either way */
+    int32_t plasticity_algorithm; /* 0 = lazy + event-driven (Fig. 2(c)); 1 =
+                             lazy only (Fig. 2(b)): rows are still updated
+                             only when they transmit or are forced, but each
+                             synapse steps through every step of the window;
+                             2 = naive (Fig. 2(a)): every plastic synapse
+                             every step with its own pre and post traces,
+                             which the graph buffer then holds (8 B more per
+                             synapse). All three reach the same weights up to
+                             rounding; they differ in work */
     int32_t neuron_model; /* enum snn_neuron_model */
     int32_t plastic;      /* enum snn_plasticity */
     int32_t poisson_len;  /* entries used in poisson_cdf (0 = no external drive) */

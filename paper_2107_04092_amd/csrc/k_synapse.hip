@@ -168,9 +168,13 @@ __global__ __launch_bounds__(kStdpBlock) void k_stdp(StdpArgs a)
                 window_masks(ap & 0xff, m0, m1);
                 const uint64_t h0 = s_hist[jl[u] * hw] & m0;
                 const uint64_t h1 = hw == 2 ? s_hist[jl[u] * hw + 1] & m1 : 0ull;
-                if (!h0 && !h1 && !pre) continue;  // nothing happened to this synapse
-                wgt[gi[u]] = stdp_synapse(wv[u], h0, h1, ap & 0xff, pre, s_xp0[l], s_xpn[l],
-                                          pre ? s_y[jl[u]] : 0.f, s_dpow, c_pot, c_dep, mu);
+                if (a.event && !h0 && !h1 && !pre) continue;  // nothing happened to it
+                const float y = pre ? s_y[jl[u]] : 0.f;
+                wgt[gi[u]] = a.event ? stdp_synapse(wv[u], h0, h1, ap & 0xff, pre, s_xp0[l],
+                                                    s_xpn[l], y, s_dpow, c_pot, c_dep, mu)
+                                     : stdp_synapse_steps(wv[u], h0, h1, ap & 0xff, pre, s_xp0[l],
+                                                          s_xpn[l], y, s_dpow[1], c_pot, c_dep,
+                                                          mu);
                 ++written;
             }
             __syncthreads();  // map rewritten by the next window
@@ -375,11 +379,13 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const bool chg = live[u] && (h[u] || g[u] || pre);
+            const bool chg = live[u] && (h[u] || g[u] || pre || !a.event);
             float w = p.w[u];
             if (chg) {
-                w = stdp_synapse(w, h[u], g[u], age, pre, ri.xp0, ri.xp_now, y[u], s_dpow, c_pot,
-                                 c_dep, mu);
+                w = a.event ? stdp_synapse(w, h[u], g[u], age, pre, ri.xp0, ri.xp_now, y[u],
+                                           s_dpow, c_pot, c_dep, mu)
+                            : stdp_synapse_steps(w, h[u], g[u], age, pre, ri.xp0, ri.xp_now,
+                                                 y[u], s_dpow[1], c_pot, c_dep, mu);
                 ++written;
             }
             const uint64_t m = ballot64(chg);
@@ -406,6 +412,74 @@ __global__ __launch_bounds__(kStdpRowsBlock) void k_stdp_rows(StdpArgs a)
     extern __shared__ uint4 dyn_sum[];
     stdp_rows_body<kStdpRowsBlock, HW == 1 ? kStdpRowsUnroll : kStdpRowsUnroll2, HW>(
         a, blockIdx.x, gridDim.x, (unsigned char *)dyn_sum);
+}
+
+// Naive plasticity (Fig. 2(a)), the baseline the lazy forms are measured
+// against: every plastic synapse every step, each with its own pre and post
+// trace. Per step and synapse k->j both traces decay; a pre spike (k
+// transmits at t) depresses with the post trace and bumps the pre trace; a
+// post spike (j fires at t) potentiates with the pre trace and bumps the
+// post trace. A wave per row, U synapses per lane; the fire mask of step t
+// is staged in LDS for the post spikes.
+constexpr int kNaiveBlock = 1024;
+constexpr int kNaiveUnroll = 4;
+
+__global__ __launch_bounds__(kNaiveBlock) void k_stdp_naive(NaiveArgs a)
+{
+    extern __shared__ uint64_t s_fire[];
+    const int tid = threadIdx.x, lane = tid % kWave;
+    for (int q = tid; q < a.nw; q += kNaiveBlock) s_fire[q] = a.mask[q];
+    __syncthreads();
+    const int gw = (blockIdx.x * kNaiveBlock + tid) / kWave;
+    const int nwv = gridDim.x * (kNaiveBlock / kWave);
+    const float dp = a.d_plus, dm = a.d_minus, c_pot = a.c_pot, c_dep = a.c_dep, mu = a.mu;
+    long long written = 0, updates = 0;
+    for (int k = gw; k < a.n_rows; k += nwv) {
+        const int pre = (int)((a.txmask[k >> 6] >> (k & 63)) & 1ull);  // wave-uniform
+        const int64_t rs = a.row_ptr[k];
+        const int len = a.pend[k];
+        updates += len;
+        for (int b = 0; b < len; b += kWave * kNaiveUnroll) {
+            int j[kNaiveUnroll];
+            float w[kNaiveUnroll], xp[kNaiveUnroll], xq[kNaiveUnroll];
+#pragma unroll
+            for (int u = 0; u < kNaiveUnroll; ++u) {  // clamped loads, selected below
+                const int e = min(b + u * kWave + lane, len - 1);
+                j[u] = a.col[rs + e];
+                w[u] = a.w[rs + e];
+                xp[u] = a.sx_pre[rs + e];
+                xq[u] = a.sx_post[rs + e];
+            }
+#pragma unroll
+            for (int u = 0; u < kNaiveUnroll; ++u) {
+                const int e = b + u * kWave + lane;
+                if (e >= len) continue;
+                const int post = (int)((s_fire[j[u] >> 6] >> (j[u] & 63)) & 1ull);
+                float x = xp[u] * dp, y = xq[u] * dm, ww = w[u];
+                if (pre) {
+                    ww = ww - c_dep * ww * y;
+                    ww = fmaxf(ww, 0.f);
+                    x = x + 1.f;
+                }
+                if (post) {
+                    ww = ww + c_pot * pow_mu(ww, mu) * x;
+                    y = y + 1.f;
+                }
+                if (pre || post) {
+                    a.w[rs + e] = ww;
+                    ++written;
+                }
+                a.sx_pre[rs + e] = x;
+                a.sx_post[rs + e] = y;
+            }
+        }
+    }
+    written = wave_sum_i64(written);
+    if (lane == 0) {
+        if (written)
+            atomicAdd((unsigned long long *)(a.stats + blockIdx.x), (unsigned long long)written);
+        if (updates) atomicAdd((unsigned long long *)a.syn_count, (unsigned long long)updates);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -574,8 +648,12 @@ __global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
                     uint64_t m0, m1;
                     window_masks(age, m0, m1);
                     const uint64_t h1 = hw == 2 ? s_hist[tgt[u] * 2 + 1] & m1 : 0ull;
-                    wv[u] = stdp_synapse(wv[u], s_hist[tgt[u] * hw] & m0, h1, age, 1, s_xp0[l],
-                                         s_xpn[l], s_y[tgt[u]], s_dpow, c_pot, c_dep, mu);
+                    const uint64_t h0 = s_hist[tgt[u] * hw] & m0;
+                    wv[u] = a.event ? stdp_synapse(wv[u], h0, h1, age, 1, s_xp0[l], s_xpn[l],
+                                                   s_y[tgt[u]], s_dpow, c_pot, c_dep, mu)
+                                    : stdp_synapse_steps(wv[u], h0, h1, age, 1, s_xp0[l],
+                                                         s_xpn[l], s_y[tgt[u]], s_dpow[1], c_pot,
+                                                         c_dep, mu);
                     wgt[gi[u]] = wv[u];
                     ++written;
                 }
@@ -694,6 +772,17 @@ hipError_t launch_stdp_rows(hipStream_t s, const StdpArgs &a, int blocks)
         hipLaunchKernelGGL(k_stdp_rows<2>, dim3(blocks), dim3(kStdpRowsBlock), lds, s, a);
     else
         hipLaunchKernelGGL(k_stdp_rows<1>, dim3(blocks), dim3(kStdpRowsBlock), lds, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_stdp_naive(hipStream_t s, const NaiveArgs &a, int blocks)
+{
+    static std::mutex mu;
+    static int granted = 64 * 1024;
+    const size_t lds = (size_t)a.nw * sizeof(uint64_t);
+    const hipError_t e = allow_dynamic_lds((const void *)k_stdp_naive, (int)lds, mu, granted);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_stdp_naive, dim3(blocks), dim3(kNaiveBlock), lds, s, a);
     return hipGetLastError();
 }
 

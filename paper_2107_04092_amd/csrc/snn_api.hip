@@ -26,6 +26,8 @@ struct snn_ctx {
     int32_t stdp_mult = 1, stdp_width = 0, stdp_groups = 0, stdp_chunks = 1, stdp_grid = 0;
     int32_t info_blocks = 1, syn_slots = 1;
     int32_t hw = 1;  // 64-bit history words per neuron
+    int32_t algo = 0;  // plasticity_algorithm: 0 lazy + event, 1 lazy, 2 naive
+    float *sx_pre = nullptr, *sx_post = nullptr;  // per-synapse traces (naive)
     float k_m = 0, v_th = 0, v_reset = 0, v_inf = 0, d_e = 0, d_i = 0, j_ext = 0;
     float d_minus = 0, c_pot = 0, c_dep = 0, mu = 0;
     float dpow[kMaxAge + 1] = {};
@@ -121,6 +123,8 @@ snn_status validate(snn_ctx *c, const snn_config &k)
         return fail(c, SNN_EINVAL, "stdp_layout must be 0 or 1");
     if (k.history_bits != 0 && k.history_bits != 64 && k.history_bits != 128)
         return fail(c, SNN_EINVAL, "history_bits must be 64 or 128 (0: 64)");
+    if (k.plasticity_algorithm < 0 || k.plasticity_algorithm > 2)
+        return fail(c, SNN_EINVAL, "plasticity_algorithm must be 0, 1 or 2");
     if (k.stdp_filter < 0 || k.stdp_filter > 3)
         return fail(c, SNN_EINVAL, "stdp_filter must be in [0, 3]");
     if (k.stdp_filter == 1 && (int64_t)k.n + 16 > kCodeMax)
@@ -169,6 +173,7 @@ void derive(snn_ctx *c)
     c->nblk = (k.n + kBlock - 1) / kBlock;
     c->nacc = k.neuron_model == SNN_LIF_CUBA ? 2 : 1;
     c->hw = k.history_bits == 128 ? 2 : 1;
+    c->algo = k.plasticity_algorithm;
     c->n_slices = (k.n + k.slice_width - 1) / k.slice_width;
     c->chunks = k.spike_chunks;
     c->delay = k.delay_steps;
@@ -309,6 +314,12 @@ snn_status finish_graph(snn_ctx *c)
     GraphArgs a = graph_args(c);
     snn_status st = check_hip(c, launch_pivots(c->stream, a), "pivot kernel");
     if (st) return st;
+    if (c->algo == 2) {  // per-synapse traces start at 0
+        st = check_hip(c, launch_fill_f32(c->stream, c->sx_pre, c->n_edges, 0.f), "traces");
+        if (!st) st = check_hip(c, launch_fill_f32(c->stream, c->sx_post, c->n_edges, 0.f),
+                                "traces");
+        if (st) return st;
+    }
     int32_t err = 0;
     st = check_hip(c, hipMemcpyAsync(&err, c->err_flag, sizeof err, hipMemcpyDeviceToHost,
                                      c->stream), "read error flag");
@@ -363,7 +374,7 @@ snn_status launch_step_neurons(snn_ctx *c)
     a.n = c->n;
     a.n_exc = c->cfg.n_exc;
     a.model = c->cfg.neuron_model;
-    a.n_plastic_rows = c->n_plastic_rows;
+    a.n_plastic_rows = c->algo == 2 ? 0 : c->n_plastic_rows;  // naive: no lazy rows
     a.dm1 = c->delay - 1;
     a.ref_steps = c->ref_steps;
     a.poisson_len = c->cfg.neuron_model == SNN_LIF_DELTA ? c->cfg.poisson_len : 0;
@@ -396,7 +407,7 @@ snn_status launch_step_neurons(snn_ctx *c)
     b.gstats = c->gstats;
     b.n = c->n;
     b.nw = c->nw;
-    b.n_plastic_rows = c->n_plastic_rows;
+    b.n_plastic_rows = c->algo == 2 ? 0 : c->n_plastic_rows;
     b.info = c->info;
     b.txinfo = c->txinfo;
     b.row_ptr = c->row_ptr;
@@ -406,7 +417,7 @@ snn_status launch_step_neurons(snn_ctx *c)
     b.t_last = c->t_last;
     b.xpre = c->xpre;
     b.err = c->err_flag;
-    b.info_stats = c->n_plastic_rows > 0 ? c->info_stats : nullptr;
+    b.info_stats = c->n_plastic_rows > 0 && c->algo != 2 ? c->info_stats : nullptr;
     b.t = c->t;
     b.dm1 = c->delay - 1;
     for (int q = 0; q <= kMaxAge; ++q) b.dpow[q] = c->dpow[q];
@@ -419,7 +430,7 @@ snn_status launch_step_neurons(snn_ctx *c)
 size_t dlv_lds_bytes(const snn_ctx *c)
 {
     size_t b = (size_t)c->cfg.slice_width * c->nacc * sizeof(long long);
-    if (c->n_plastic_rows > 0)
+    if (c->n_plastic_rows > 0 && c->algo != 2)
         b += (size_t)c->cfg.slice_width * (c->hw * sizeof(uint64_t) + sizeof(float));
     return b;
 }
@@ -456,8 +467,11 @@ StdpArgs stdp_args(snn_ctx *c, bool flush)
     const bool fresh = c->last_neuron_t >= 0;
     const int f = c->cfg.stdp_filter;
     const bool fits_code = (int64_t)c->n + 16 <= kCodeMax, fits_map = c->nw <= kRecentMaxWords;
-    a.code = fresh && (f == 1 || (f == 0 && fits_code)) ? c->code : nullptr;
-    a.recent = fresh && (f == 2 || (f == 0 && !fits_code && fits_map)) ? c->recent : nullptr;
+    // lazy but not event-driven: every synapse of a row walks every step
+    const bool filt = fresh && c->algo == 0;
+    a.code = filt && (f == 1 || (f == 0 && fits_code)) ? c->code : nullptr;
+    a.recent = filt && (f == 2 || (f == 0 && !fits_code && fits_map)) ? c->recent : nullptr;
+    a.event = c->algo == 0;
     a.nw = c->nw;
     for (int q = 0; q <= kMaxAge; ++q) a.dpow[q] = c->dpow[q];
     return a;
@@ -501,6 +515,27 @@ snn_status launch_plasticity(snn_ctx *c, bool flush, hipStream_t s)
 snn_status launch_step_plasticity(snn_ctx *c)
 {
     if (c->n_plastic_rows == 0) return SNN_OK;
+    if (c->algo == 2) {  // naive: every plastic synapse of every row
+        NaiveArgs a{};
+        a.row_ptr = c->row_ptr;
+        a.pend = c->pend;
+        a.col = c->col;
+        a.w = c->w;
+        a.sx_pre = c->sx_pre;
+        a.sx_post = c->sx_post;
+        a.mask = c->mask;
+        a.txmask = c->txmask;
+        a.n_rows = c->n_plastic_rows;
+        a.nw = c->nw;
+        a.d_plus = c->dpow[1];
+        a.d_minus = c->d_minus;
+        a.c_pot = c->c_pot;
+        a.c_dep = c->c_dep;
+        a.mu = c->mu;
+        a.stats = c->syn_stats;
+        a.syn_count = c->gstats + kGNaiveSyn;
+        return check_hip(c, launch_stdp_naive(c->stream, a, kStdpRowsBlocks), "naive STDP");
+    }
     return launch_plasticity(c, false, c->stream);
 }
 
@@ -526,7 +561,8 @@ DeliverArgs deliver_args(snn_ctx *c)
     a.nacc = c->nacc;
     a.n_work = c->n_slices * c->chunks;
     a.stats = c->dlv_stats;
-    a.plastic = c->n_plastic_rows > 0;
+    a.plastic = c->n_plastic_rows > 0 && c->algo != 2;
+    a.event = c->algo == 0;
     a.txinfo = c->txinfo;
     a.hist = c->hist;
     a.hw = c->hw;
@@ -741,7 +777,7 @@ snn_status snn_graph_count_random(snn_ctx *c, int32_t kind, double p_or_fanout,
 snn_status snn_graph_size(const snn_ctx *c, int64_t n_edges, size_t *bytes)
 {
     if (!c || !bytes || n_edges < 0) return SNN_EINVAL;
-    *bytes = 2 * align_up((size_t)n_edges * sizeof(int32_t)) +
+    *bytes = (c->algo == 2 ? 4 : 2) * align_up((size_t)n_edges * sizeof(int32_t)) +
              align_up((size_t)c->n * (size_t)(c->n_slices + 1) * 4);
     return SNN_OK;
 }
@@ -767,6 +803,9 @@ snn_status snn_bind_graph(snn_ctx *c, void *device_ptr, size_t bytes, int64_t n_
     c->col = (int32_t *)c->g;
     c->w = (float *)(c->g + arr);
     c->piv = (int32_t *)(c->g + 2 * arr);
+    const size_t pivb = align_up((size_t)c->n * (size_t)(c->n_slices + 1) * 4);
+    c->sx_pre = c->algo == 2 ? (float *)(c->g + 2 * arr + pivb) : nullptr;
+    c->sx_post = c->algo == 2 ? (float *)(c->g + 3 * arr + pivb) : nullptr;
     if (c->graph_state != 1) c->counted_kind = -1;
     c->graph_state = 2;
     return SNN_OK;
@@ -909,7 +948,7 @@ snn_status snn_flush_plasticity(snn_ctx *c)
     if (!c) return SNN_EINVAL;
     snn_status st = require_graph(c);
     if (st) return st;
-    if (c->n_plastic_rows == 0 || c->t == 0) return SNN_OK;
+    if (c->n_plastic_rows == 0 || c->t == 0 || c->algo == 2) return SNN_OK;  // naive: current
     return launch_plasticity(c, true, c->stream);
 }
 
@@ -1020,6 +1059,7 @@ snn_status snn_get_stats(snn_ctx *c, snn_stats *out)
     std::memset(out, 0, sizeof *out);
     out->steps = c->steps_done;
     out->spikes = g[kGSpikes];
+    out->stdp_synapse_updates = g[kGNaiveSyn];  // naive plasticity (0 otherwise)
     out->device_errors = err;
     for (int b = 0; b < c->info_blocks; ++b) {
         out->stdp_rows += si[(size_t)b * kStFields + kStRows];

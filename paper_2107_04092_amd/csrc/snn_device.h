@@ -206,6 +206,29 @@ __device__ __forceinline__ float stdp_synapse(float w, uint64_t h0, uint64_t h1,
     return w;
 }
 
+// The same update stepping through every step of the window (lazy but not
+// event-driven, Fig. 2(b)): the pre trace decays one step at a time and every
+// history bit is tested. Differs from stdp_synapse only in the rounding of
+// the decayed pre trace.
+__device__ __forceinline__ float stdp_synapse_steps(float w, uint64_t h0, uint64_t h1, int age,
+                                                    int pre, float xp0, float xp_now, float y,
+                                                    float d_plus, float c_pot, float c_dep,
+                                                    float mu)
+{
+    float xp = xp0;
+    for (int s = age - 1; s >= 1; --s) {  // steps t-s before t, oldest first
+        xp = xp * d_plus;
+        const uint64_t bit = s < 64 ? (h0 >> s) & 1ull : (h1 >> (s - 64)) & 1ull;
+        if (bit) w = w + c_pot * pow_mu(w, mu) * xp;
+    }
+    if (pre) {
+        w = w - c_dep * w * y;
+        w = fmaxf(w, 0.f);
+    }
+    if (h0 & 1ull) w = w + c_pot * pow_mu(w, mu) * xp_now;
+    return w;
+}
+
 inline int blocks_for(int64_t count, int per = kBlock, int64_t cap = 1 << 20)
 {
     int64_t b = (count + per - 1) / per;

@@ -33,7 +33,7 @@ constexpr float kFixUnit = 2.3283064365386963e-10f; // 2^-32
 enum StdpStat { kStRows = 0, kStForced = 1, kStSyn = 2, kStForcedSyn = 3, kStFields = 4 };
 
 // Global counters.
-enum GlobalStat { kGSpikes = 0, kGFields = 8 };
+enum GlobalStat { kGSpikes = 0, kGNaiveSyn = 1, kGFields = 8 };
 
 // Error bits raised by kernels (device int32, ORed).
 enum DevError { kErrIndex = 1, kErrRowTooLong = 2, kErrWindow = 4 };
@@ -133,6 +133,7 @@ struct StdpArgs {
     const uint64_t *hist;
     const float *ypost;
     int32_t n, n_slices, mult, width, n_groups, chunks, n_work, target_limit, hw;
+    int32_t event;           // 1: replay only the set history bits; 0: every step (lazy only)
     float c_pot, c_dep, mu;
     int64_t *stats;          // [gridDim.x] weights written
     // row-wise layout: per-neuron history codes or the spike-recency bitmap
@@ -157,6 +158,7 @@ struct DeliverArgs {
     int64_t *stats;          // [gridDim.x][2]: events delivered, weights written
     // plasticity of the transmitting rows, fused into slice delivery
     int32_t plastic;         // 0: no plastic rows
+    int32_t event;           // as in StdpArgs
     const RowInfo *txinfo;   // aligned with `list`
     const uint64_t *hist;
     const float *ypost;
@@ -165,6 +167,21 @@ struct DeliverArgs {
     int64_t t;
     float c_pot, c_dep, mu;
     float dpow[kMaxAge + 1];
+};
+
+// Naive plasticity (every plastic synapse every step, per-synapse traces).
+struct NaiveArgs {
+    const int64_t *row_ptr;
+    const int32_t *pend;     // plastic prefix length per row
+    const int32_t *col;
+    float *w;
+    float *sx_pre, *sx_post; // per-synapse pre and post traces
+    const uint64_t *mask;    // spikes of step t (post)
+    const uint64_t *txmask;  // spikes transmitted at t (pre)
+    int32_t n_rows, nw;
+    float d_plus, d_minus, c_pot, c_dep, mu;
+    int64_t *stats;          // [gridDim.x] weights written
+    int64_t *syn_count;      // synapse updates (one counter)
 };
 
 struct GraphArgs {
@@ -196,6 +213,7 @@ hipError_t launch_compact(hipStream_t s, const CompactArgs &a);
 hipError_t launch_row_info(hipStream_t s, const RowInfoArgs &a, int64_t max_rows);
 hipError_t launch_stdp(hipStream_t s, const StdpArgs &a, int blocks, size_t lds);
 hipError_t launch_stdp_rows(hipStream_t s, const StdpArgs &a, int blocks);
+hipError_t launch_stdp_naive(hipStream_t s, const NaiveArgs &a, int blocks);
 constexpr int kStdpRowsBlock = 1024;   // threads of the row-wise STDP kernel
 constexpr int kStdpRowsUnroll = 8;     // synapses per lane and row part (64-step histories)
 constexpr int kStdpRowsUnroll2 = 4;    // the same with 128-step histories

@@ -70,6 +70,8 @@ def test_struct_layouts_match_header(tmp_path):
     ("plastic", 9, "plastic"),
     ("stdp_layout", 2, "stdp_layout"),
     ("stdp_filter", 4, "stdp_filter"),
+    ("plasticity_algorithm", 3, "plasticity_algorithm"),
+    ("history_bits", 96, "history_bits"),
     ("poisson_len", 33, "poisson_len"),
     ("dt_ms", float("nan"), "NaN"),
     ("tau_m_ms", 0.0, "tau_m_ms"),
