@@ -296,6 +296,20 @@ snn_status snn_advance(snn_ctx *ctx);
  * Enqueues only; never synchronises. */
 snn_status snn_step(snn_ctx *ctx, int32_t n_steps, int32_t mode);
 
+/* Kernel timing for profiling. After this call the next max_steps steps run
+ * by snn_step record, per step, the device time of its kernels in four parts:
+ * [0] neuron update, [1] compaction, [2] plasticity, [3] delivery (for the
+ * global-atomic mode from the start of the transmitting rows' plasticity to
+ * the end of delivery). Each launch places its own events around the kernel
+ * (no extra stream work). 0 stops recording and frees the events. Calls the
+ * stream's synchronisation first. */
+snn_status snn_record_kernel_times(snn_ctx *ctx, int32_t max_steps);
+
+/* Mean device time per recorded step of each part in milliseconds (0 for a
+ * part that launched nothing) and the number of steps recorded.
+ * Synchronises the stream. */
+snn_status snn_get_kernel_times(snn_ctx *ctx, double *mean_ms, int32_t *steps);
+
 /* Brings every plastic row up to the last completed step t-1 (no pre-
  * synaptic spike), so that all weights equal those of per-step updates. */
 snn_status snn_flush_plasticity(snn_ctx *ctx);

@@ -330,15 +330,17 @@ hipError_t launch_copy_bytes(hipStream_t s, void *dst, const void *src, int64_t 
     return hipMemcpyAsync(dst, src, (size_t)bytes, hipMemcpyDeviceToDevice, s);
 }
 
-hipError_t launch_neuron(hipStream_t s, const NeuronArgs &a)
+hipError_t launch_neuron(hipStream_t s, const NeuronArgs &a, KernelEvents ev)
 {
-    hipLaunchKernelGGL(k_neuron, dim3(blocks_for(a.n)), dim3(kBlock), 0, s, a);
+    hipExtLaunchKernelGGL(k_neuron, dim3(blocks_for(a.n)), dim3(kBlock), 0, s,
+                          ev.start, ev.stop, 0, a);
     return hipGetLastError();
 }
 
-hipError_t launch_compact(hipStream_t s, const CompactArgs &a)
+hipError_t launch_compact(hipStream_t s, const CompactArgs &a, KernelEvents ev)
 {
-    hipLaunchKernelGGL(k_compact, dim3(blocks_for(a.n)), dim3(kBlock), 0, s, a);
+    hipExtLaunchKernelGGL(k_compact, dim3(blocks_for(a.n)), dim3(kBlock), 0, s,
+                          ev.start, ev.stop, 0, a);
     return hipGetLastError();
 }
 

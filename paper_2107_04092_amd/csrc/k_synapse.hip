@@ -517,6 +517,7 @@ constexpr int kDlvBlock = 512;
 constexpr int kDlvBatch = 512;   // spikes whose segments are staged at once
 constexpr int kDlvUnroll = 8;    // flattened elements per thread per window
 constexpr int kDlvWindow = kDlvBlock * kDlvUnroll;
+static_assert(kDlvBatch == kDlvBlock, "one staged spike per thread");
 
 __global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
 {
@@ -748,17 +749,18 @@ hipError_t launch_row_info(hipStream_t s, const RowInfoArgs &a, int64_t max_rows
     return hipGetLastError();
 }
 
-hipError_t launch_stdp(hipStream_t s, const StdpArgs &a, int blocks, size_t lds)
+hipError_t launch_stdp(hipStream_t s, const StdpArgs &a, int blocks, size_t lds, KernelEvents ev)
 {
     static std::mutex mu;
     static int granted = 64 * 1024;
     const hipError_t e = allow_dynamic_lds((const void *)k_stdp, (int)lds, mu, granted);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_stdp, dim3(blocks), dim3(kStdpBlock), lds, s, a);
+    hipExtLaunchKernelGGL(k_stdp, dim3(blocks), dim3(kStdpBlock), lds, s,
+                          ev.start, ev.stop, 0, a);
     return hipGetLastError();
 }
 
-hipError_t launch_stdp_rows(hipStream_t s, const StdpArgs &a, int blocks)
+hipError_t launch_stdp_rows(hipStream_t s, const StdpArgs &a, int blocks, KernelEvents ev)
 {
     static std::mutex mu;
     static int granted[2] = {64 * 1024, 64 * 1024};
@@ -769,36 +771,41 @@ hipError_t launch_stdp_rows(hipStream_t s, const StdpArgs &a, int blocks)
     const hipError_t e = allow_dynamic_lds(kern, (int)lds, mu, granted[a.hw == 2]);
     if (e != hipSuccess) return e;
     if (a.hw == 2)
-        hipLaunchKernelGGL(k_stdp_rows<2>, dim3(blocks), dim3(kStdpRowsBlock), lds, s, a);
+        hipExtLaunchKernelGGL(k_stdp_rows<2>, dim3(blocks), dim3(kStdpRowsBlock), lds, s,
+                              ev.start, ev.stop, 0, a);
     else
-        hipLaunchKernelGGL(k_stdp_rows<1>, dim3(blocks), dim3(kStdpRowsBlock), lds, s, a);
+        hipExtLaunchKernelGGL(k_stdp_rows<1>, dim3(blocks), dim3(kStdpRowsBlock), lds, s,
+                              ev.start, ev.stop, 0, a);
     return hipGetLastError();
 }
 
-hipError_t launch_stdp_naive(hipStream_t s, const NaiveArgs &a, int blocks)
+hipError_t launch_stdp_naive(hipStream_t s, const NaiveArgs &a, int blocks, KernelEvents ev)
 {
     static std::mutex mu;
     static int granted = 64 * 1024;
     const size_t lds = (size_t)a.nw * sizeof(uint64_t);
     const hipError_t e = allow_dynamic_lds((const void *)k_stdp_naive, (int)lds, mu, granted);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_stdp_naive, dim3(blocks), dim3(kNaiveBlock), lds, s, a);
+    hipExtLaunchKernelGGL(k_stdp_naive, dim3(blocks), dim3(kNaiveBlock), lds, s,
+                          ev.start, ev.stop, 0, a);
     return hipGetLastError();
 }
 
-hipError_t launch_deliver_lds(hipStream_t s, const DeliverArgs &a, int blocks, size_t lds)
+hipError_t launch_deliver_lds(hipStream_t s, const DeliverArgs &a, int blocks, size_t lds, KernelEvents ev)
 {
     static std::mutex mu;
     static int granted = 64 * 1024;
     const hipError_t e = allow_dynamic_lds((const void *)k_deliver_lds, (int)lds, mu, granted);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_deliver_lds, dim3(blocks), dim3(kDlvBlock), lds, s, a);
+    hipExtLaunchKernelGGL(k_deliver_lds, dim3(blocks), dim3(kDlvBlock), lds, s,
+                          ev.start, ev.stop, 0, a);
     return hipGetLastError();
 }
 
-hipError_t launch_deliver_global(hipStream_t s, const DeliverArgs &a, int blocks)
+hipError_t launch_deliver_global(hipStream_t s, const DeliverArgs &a, int blocks, KernelEvents ev)
 {
-    hipLaunchKernelGGL(k_deliver_global, dim3(blocks), dim3(kBlock), 0, s, a);
+    hipExtLaunchKernelGGL(k_deliver_global, dim3(blocks), dim3(kBlock), 0, s,
+                          ev.start, ev.stop, 0, a);
     return hipGetLastError();
 }
 

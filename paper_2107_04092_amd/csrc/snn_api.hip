@@ -28,6 +28,16 @@ struct snn_ctx {
     int32_t hw = 1;  // 64-bit history words per neuron
     int32_t algo = 0;  // plasticity_algorithm: 0 lazy + event, 1 lazy, 2 naive
     float *sx_pre = nullptr, *sx_post = nullptr;  // per-synapse traces (naive)
+    // kernel timing: events [step][part][start, stop] for the first t_cap
+    // steps run by snn_step after snn_record_kernel_times; t_rec marks parts
+    // that launched a kernel
+    std::vector<hipEvent_t> tev;
+    std::vector<uint8_t> t_rec;
+    int32_t t_cap = 0, t_used = 0;
+    ~snn_ctx()
+    {
+        for (hipEvent_t e : tev) (void)hipEventDestroy(e);
+    }
     float k_m = 0, v_th = 0, v_reset = 0, v_inf = 0, d_e = 0, d_i = 0, j_ext = 0;
     float d_minus = 0, c_pot = 0, c_dep = 0, mu = 0;
     float dpow[kMaxAge + 1] = {};
@@ -347,6 +357,20 @@ snn_status materialize_input(snn_ctx *c)
     return SNN_OK;
 }
 
+// Events of part `part` (0 neurons, 1 compaction, 2 plasticity, 3 delivery)
+// of the current step when timing is on; marks the part as timed.
+KernelEvents part_events(snn_ctx *c, int part)
+{
+    KernelEvents ev;
+    if (c->t_used < c->t_cap) {
+        const size_t q = (size_t)c->t_used * 4 + part;
+        ev.start = c->tev[2 * q];
+        ev.stop = c->tev[2 * q + 1];
+        c->t_rec[q] = 1;
+    }
+    return ev;
+}
+
 snn_status launch_step_neurons(snn_ctx *c)
 {
     NeuronArgs a{};
@@ -390,7 +414,7 @@ snn_status launch_step_neurons(snn_ctx *c)
     a.fire_thr = c->fire_thr;
     a.seed = c->cfg.seed;
     for (int q = 0; q < kMaxPoisson; ++q) a.poisson[q] = c->cfg.poisson_cdf[q];
-    snn_status st = check_hip(c, launch_neuron(c->stream, a), "neuron kernel");
+    snn_status st = check_hip(c, launch_neuron(c->stream, a, part_events(c, 0)), "neuron kernel");
     if (st) return st;
     c->input_forced = 0;  // the input has been consumed; the next comes from delivery
     CompactArgs b{};
@@ -421,7 +445,7 @@ snn_status launch_step_neurons(snn_ctx *c)
     b.t = c->t;
     b.dm1 = c->delay - 1;
     for (int q = 0; q <= kMaxAge; ++q) b.dpow[q] = c->dpow[q];
-    st = check_hip(c, launch_compact(c->stream, b), "compaction kernel");
+    st = check_hip(c, launch_compact(c->stream, b, part_events(c, 1)), "compaction kernel");
     if (st) return st;
     c->last_neuron_t = c->t;
     return SNN_OK;
@@ -482,7 +506,7 @@ StdpArgs stdp_args(snn_ctx *c, bool flush)
 // brought up to date by the delivery part. A flush (every plastic row up to
 // step t-1, no pre-synaptic spike) takes its snapshots first. The synapse
 // pass commits t_last and the pre traces.
-snn_status launch_plasticity(snn_ctx *c, bool flush, hipStream_t s)
+snn_status launch_plasticity(snn_ctx *c, bool flush, hipStream_t s, KernelEvents ev = {})
 {
     if (flush) {
         RowInfoArgs r{};
@@ -507,9 +531,9 @@ snn_status launch_plasticity(snn_ctx *c, bool flush, hipStream_t s)
     }
     StdpArgs a = stdp_args(c, flush);
     if (c->cfg.stdp_layout == 0)
-        return check_hip(c, launch_stdp_rows(s, a, kStdpRowsBlocks), "STDP kernel");
+        return check_hip(c, launch_stdp_rows(s, a, kStdpRowsBlocks, ev), "STDP kernel");
     const size_t lds = (size_t)c->stdp_width * (c->hw * sizeof(uint64_t) + sizeof(float));
-    return check_hip(c, launch_stdp(s, a, c->stdp_grid, lds), "STDP kernel");
+    return check_hip(c, launch_stdp(s, a, c->stdp_grid, lds, ev), "STDP kernel");
 }
 
 snn_status launch_step_plasticity(snn_ctx *c)
@@ -534,9 +558,10 @@ snn_status launch_step_plasticity(snn_ctx *c)
         a.mu = c->mu;
         a.stats = c->syn_stats;
         a.syn_count = c->gstats + kGNaiveSyn;
-        return check_hip(c, launch_stdp_naive(c->stream, a, kStdpRowsBlocks), "naive STDP");
+        return check_hip(c, launch_stdp_naive(c->stream, a, kStdpRowsBlocks, part_events(c, 2)),
+                         "naive STDP");
     }
-    return launch_plasticity(c, false, c->stream);
+    return launch_plasticity(c, false, c->stream, part_events(c, 2));
 }
 
 
@@ -583,7 +608,8 @@ snn_status launch_step_delivery(snn_ctx *c, int32_t mode)
     snn_status st;
     if (mode == SNN_DELIVER_LDS_SLICE) {
         // the transmitting rows' plasticity is fused into slice delivery
-        st = check_hip(c, launch_deliver_lds(c->stream, a, c->dlv_blocks, dlv_lds_bytes(c)),
+        st = check_hip(c, launch_deliver_lds(c->stream, a, c->dlv_blocks, dlv_lds_bytes(c),
+                                             part_events(c, 3)),
                        "slice delivery kernel");
         if (st) return st;
         c->n_parts = c->chunks;
@@ -592,18 +618,21 @@ snn_status launch_step_delivery(snn_ctx *c, int32_t mode)
         c->input_forced = c->chunks == 1 ? 1 : 0;
         return SNN_OK;
     }
+    const KernelEvents ev = part_events(c, 3);
+    KernelEvents last{ev.start, ev.stop};
     if (a.plastic) {
         // bring the transmitting rows up to date first (row-wise, L2 gathers)
         StdpArgs r = stdp_args(c, false);
         r.info = c->txinfo;
         r.row_cnt = a.cnt;
-        st = check_hip(c, launch_stdp_rows(c->stream, r, kStdpRowsBlocks),
+        st = check_hip(c, launch_stdp_rows(c->stream, r, kStdpRowsBlocks, {ev.start, nullptr}),
                        "STDP of transmitting rows");
         if (st) return st;
+        last.start = nullptr;
     }
     st = check_hip(c, launch_fill_ll(c->stream, c->apart, a.part_stride, 0), "clear input");
     if (st) return st;
-    st = check_hip(c, launch_deliver_global(c->stream, a, kGlobalMaxBlocks),
+    st = check_hip(c, launch_deliver_global(c->stream, a, kGlobalMaxBlocks, last),
                    "global delivery kernel");
     if (st) return st;
     c->n_parts = 1;
@@ -937,9 +966,60 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
         if ((st = launch_step_neurons(c))) return st;
         if ((st = launch_step_plasticity(c))) return st;
         if ((st = launch_step_delivery(c, mode))) return st;
+        if (c->t_used < c->t_cap) c->t_used += 1;
         c->t += 1;
         c->steps_done += 1;
     }
+    return SNN_OK;
+}
+
+snn_status snn_record_kernel_times(snn_ctx *c, int32_t max_steps)
+{
+    if (!c) return SNN_EINVAL;
+    if (max_steps < 0 || max_steps > (1 << 20))
+        return fail(c, SNN_EINVAL, "max_steps must be in [0, 2^20]");
+    snn_status st = check_hip(c, hipStreamSynchronize(c->stream), "kernel timing");
+    if (st) return st;
+    for (hipEvent_t e : c->tev) (void)hipEventDestroy(e);
+    c->tev.assign((size_t)max_steps * 8, nullptr);
+    c->t_rec.assign((size_t)max_steps * 4, 0);
+    c->t_cap = c->t_used = 0;
+    for (hipEvent_t &e : c->tev) {
+        if (hipEventCreate(&e) != hipSuccess) {
+            (void)hipGetLastError();
+            e = nullptr;
+            for (hipEvent_t x : c->tev)
+                if (x) (void)hipEventDestroy(x);
+            c->tev.clear();
+            c->t_rec.clear();
+            return fail(c, SNN_EDEVICE, "cannot create timing events");
+        }
+    }
+    c->t_cap = max_steps;
+    return SNN_OK;
+}
+
+snn_status snn_get_kernel_times(snn_ctx *c, double *mean_ms, int32_t *steps)
+{
+    if (!c || !mean_ms || !steps) return SNN_EINVAL;
+    snn_status st = check_hip(c, hipStreamSynchronize(c->stream), "kernel timing");
+    if (st) return st;
+    for (int part = 0; part < 4; ++part) {
+        double sum = 0;
+        int cnt = 0;
+        for (int q = 0; q < c->t_used; ++q) {
+            const size_t k = (size_t)q * 4 + part;
+            if (!c->t_rec[k]) continue;
+            float ms = 0;
+            st = check_hip(c, hipEventElapsedTime(&ms, c->tev[2 * k], c->tev[2 * k + 1]),
+                           "kernel timing");
+            if (st) return st;
+            sum += ms;
+            ++cnt;
+        }
+        mean_ms[part] = cnt ? sum / cnt : 0.0;
+    }
+    *steps = c->t_used;
     return SNN_OK;
 }
 

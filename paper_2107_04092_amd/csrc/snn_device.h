@@ -6,6 +6,8 @@
 
 #include "snn_internal.h"
 
+#include <hip/hip_ext.h>
+
 #include <mutex>
 
 namespace snn {

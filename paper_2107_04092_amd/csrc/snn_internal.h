@@ -198,6 +198,12 @@ struct GraphArgs {
     float w_exc, w_inh;
 };
 
+// Optional events placed by a launch itself around the kernel
+// (hipExtLaunchKernelGGL): its device time without marker or dispatch gaps.
+struct KernelEvents {
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+
 // ---- launchers (k_*.hip); all enqueue on `s` and return the launch
 // status of the last kernel they started.
 hipError_t launch_init_state(hipStream_t s, float *v, int32_t *ref, float *ie, float *ii,
@@ -208,12 +214,12 @@ hipError_t launch_fill_i64(hipStream_t s, int64_t *p, int64_t count, int64_t val
 hipError_t launch_fill_i32(hipStream_t s, int32_t *p, int64_t count, int32_t value);
 hipError_t launch_fill_ll(hipStream_t s, long long *p, int64_t count, long long value);
 hipError_t launch_copy_bytes(hipStream_t s, void *dst, const void *src, int64_t bytes);
-hipError_t launch_neuron(hipStream_t s, const NeuronArgs &a);
-hipError_t launch_compact(hipStream_t s, const CompactArgs &a);
+hipError_t launch_neuron(hipStream_t s, const NeuronArgs &a, KernelEvents ev = {});
+hipError_t launch_compact(hipStream_t s, const CompactArgs &a, KernelEvents ev = {});
 hipError_t launch_row_info(hipStream_t s, const RowInfoArgs &a, int64_t max_rows);
-hipError_t launch_stdp(hipStream_t s, const StdpArgs &a, int blocks, size_t lds);
-hipError_t launch_stdp_rows(hipStream_t s, const StdpArgs &a, int blocks);
-hipError_t launch_stdp_naive(hipStream_t s, const NaiveArgs &a, int blocks);
+hipError_t launch_stdp(hipStream_t s, const StdpArgs &a, int blocks, size_t lds, KernelEvents ev = {});
+hipError_t launch_stdp_rows(hipStream_t s, const StdpArgs &a, int blocks, KernelEvents ev = {});
+hipError_t launch_stdp_naive(hipStream_t s, const NaiveArgs &a, int blocks, KernelEvents ev = {});
 constexpr int kStdpRowsBlock = 1024;   // threads of the row-wise STDP kernel
 constexpr int kStdpRowsUnroll = 8;     // synapses per lane and row part (64-step histories)
 constexpr int kStdpRowsUnroll2 = 4;    // the same with 128-step histories
@@ -222,8 +228,8 @@ constexpr int kCodeMax = 147456;       // LDS bytes of history codes one row-STD
 constexpr int kRecentMaxWords = 16384; // LDS-staged spike-recency bitmap: up to 1M neurons
 constexpr uint8_t kCodeMulti = 255;    // history code: two or more spikes in the window
 int stdp_static_bytes();  // static LDS of the slice STDP kernel (-1 on error)
-hipError_t launch_deliver_lds(hipStream_t s, const DeliverArgs &a, int blocks, size_t lds);
-hipError_t launch_deliver_global(hipStream_t s, const DeliverArgs &a, int blocks);
+hipError_t launch_deliver_lds(hipStream_t s, const DeliverArgs &a, int blocks, size_t lds, KernelEvents ev = {});
+hipError_t launch_deliver_global(hipStream_t s, const DeliverArgs &a, int blocks, KernelEvents ev = {});
 int deliver_lds_static_bytes();  // static LDS of the slice kernel (-1 on error)
 hipError_t launch_materialize_input(hipStream_t s, const long long *apart, int64_t part_stride,
                                     int32_t n_parts, float *ain, int64_t count);

@@ -68,6 +68,9 @@ _SIGNATURES = {
     "snn_status_string": (ctypes.c_char_p, [_i32]),
     "snn_create": (_i32, [ctypes.POINTER(snn_config), _P, ctypes.POINTER(_P)]),
     "snn_destroy": (None, [_P]),
+    "snn_record_kernel_times": (_i32, [_P, _i32]),
+    "snn_get_kernel_times": (_i32, [_P, ctypes.POINTER(ctypes.c_double),
+                                    ctypes.POINTER(_i32)]),
     "snn_last_error": (ctypes.c_char_p, [_P]),
     "snn_workspace_size": (_i32, [_P, ctypes.POINTER(ctypes.c_size_t)]),
     "snn_bind_workspace": (_i32, [_P, _P, ctypes.c_size_t]),
@@ -223,6 +226,21 @@ def snn_reset_stats(ctx):
     _check(ctx, load().snn_reset_stats(ctx))
 
 
+def snn_record_kernel_times(ctx, max_steps):
+    _check(ctx, load().snn_record_kernel_times(ctx, int(max_steps)))
+
+
+KERNEL_PARTS = ("neuron", "compaction", "plasticity", "delivery")
+
+
+def snn_get_kernel_times(ctx):
+    """Mean device milliseconds per step of each part, and the steps recorded."""
+    ms = (ctypes.c_double * 4)()
+    steps = _i32()
+    _check(ctx, load().snn_get_kernel_times(ctx, ms, ctypes.byref(steps)))
+    return dict(zip(KERNEL_PARTS, list(ms))), steps.value
+
+
 # ---- configuration marshalling ---------------------------------------------
 
 def config_from_preset(p, poisson_table=(), slice_width=None, spike_chunks=None,
@@ -341,6 +359,12 @@ class Network:
 
     def reset_stats(self):
         snn_reset_stats(self.ctx)
+
+    def record_kernel_times(self, max_steps):
+        snn_record_kernel_times(self.ctx, max_steps)
+
+    def kernel_times(self):
+        return snn_get_kernel_times(self.ctx)
 
     def synchronize(self):
         self.stream.synchronize()
