@@ -4,7 +4,7 @@ Workload (default): the stress network - 250,000 Bernoulli(0.005) sources,
 fan-out 1,000 uniform-random targets with replacement (250M synapses, int32
 targets + fp32 weights), power-law STDP on every synapse, delay 1 step.
 
-One step = neuron update + spike-list compaction, lazy + event-driven STDP
+One step = neuron update (with the spike and row lists), lazy + event-driven STDP
 of the forced rows, and slice (LDS) delivery with the transmitting rows'
 STDP. Timed region: K steps issued by one snn_step call, bracketed by device
 synchronisation. Then K more steps run with the library's kernel timing:
@@ -14,7 +14,7 @@ between kernels, so the timed region runs without them). The roofline
 figure of the dominant kernel (forced-row STDP) is its algorithmic bytes
 per launch over its device time.
 
-Prints one JSON line. `--gpus N` with N > 1 exits: this build runs on one GPU.
+Prints one JSON line. `--gpus N` with N > 1 exits: the benchmark runs on one GPU.
 """
 
 import argparse
@@ -149,9 +149,8 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py: this build runs the synapse pass on one GPU only; "
-              "--gpus %d is not supported (sharding is described in DESIGN.md)" % args.gpus,
-              file=sys.stderr)
+        print("bench.py: the synapse pass is benchmarked on one GPU only; "
+              "--gpus %d is not supported" % args.gpus, file=sys.stderr)
         sys.exit(2)
     import torch
     import workloads as wl
@@ -225,12 +224,10 @@ def main():
         b_stdp = stdp_bytes(st2, p.n, args.steps) / args.steps
         b_dlv = delivery_bytes(st2, p.n, n_slices, chunks, nacc, args.steps,
                                args.mode) / args.steps
-        t_neu, t_cmp, t_stdp, t_dlv = (kt["neuron"], kt["compaction"], kt["plasticity"],
-                                       kt["delivery"])
+        t_neu, t_stdp, t_dlv = kt["neuron"], kt["plasticity"], kt["delivery"]
         kernels = {
             "steps_timed": nrec,
             "neuron_us": round(t_neu * 1e3, 3),
-            "compaction_us": round(t_cmp * 1e3, 3),
             "plasticity_us": round(t_stdp * 1e3, 3),
             "delivery_us": round(t_dlv * 1e3, 3),
             "plasticity_bytes_per_launch": int(b_stdp),

@@ -10,7 +10,8 @@
  *   (3) deliver spikes to the neurons' neighbours.
  * Every part runs in hand-written HIP kernels:
  *   - (1) emits a 64-bit firing mask word per 64 neurons (one wave64 ballot),
- *     an ascending spike list, and shifts each neuron's firing history of
+ *     a spike list (each workgroup appends its spikes at a reserved offset;
+ *     snn_get_state puts the lists in ascending order), and shifts each neuron's firing history of
  *     one or two 64-bit words (least significant bit = most recent step,
  *     Fig. 2);
  *   - a ring of the last D spike lists implements the network-wide delay;
@@ -211,7 +212,10 @@ typedef struct snn_stats {
                                              the transmitting rows) */
     int64_t device_errors;         /* conditions flagged by kernels: 4 = a plastic row
                                       fell more than 64 steps behind (its update was
-                                      skipped), so its weights are no longer exact */
+                                      skipped), so its weights are no longer exact;
+                                      8 = a transmitting neuron had no entry in the
+                                      delay ring (a state set whose ring lists
+                                      disagree with the histories) */
 } snn_stats;
 
 /* Human-readable name of a status code (static string). */
@@ -297,16 +301,17 @@ snn_status snn_advance(snn_ctx *ctx);
 snn_status snn_step(snn_ctx *ctx, int32_t n_steps, int32_t mode);
 
 /* Kernel timing for profiling. After this call the next max_steps steps run
- * by snn_step record, per step, the device time of its kernels in four parts:
- * [0] neuron update, [1] compaction, [2] plasticity, [3] delivery (for the
- * global-atomic mode from the start of the transmitting rows' plasticity to
- * the end of delivery). Each launch places its own events around the kernel
+ * by snn_step record, per step, the device time of its kernels in three
+ * parts: [0] neuron update with its spike / row lists, [1] plasticity,
+ * [2] delivery (for the global-atomic mode from the start of the
+ * transmitting rows' plasticity to the end of delivery). Each launch places its own events around the kernel
  * (no extra stream work). 0 stops recording and frees the events. Calls the
  * stream's synchronisation first. */
 snn_status snn_record_kernel_times(snn_ctx *ctx, int32_t max_steps);
 
-/* Mean device time per recorded step of each part in milliseconds (0 for a
- * part that launched nothing) and the number of steps recorded.
+/* Mean device time per recorded step of each part in milliseconds
+ * (mean_ms: 3 doubles, host; 0 for a part that launched nothing) and the
+ * number of steps recorded.
  * Synchronises the stream. */
 snn_status snn_get_kernel_times(snn_ctx *ctx, double *mean_ms, int32_t *steps);
 
@@ -318,7 +323,9 @@ snn_status snn_flush_plasticity(snn_ctx *ctx);
  * Delivery accumulates inputs exactly in 64-bit fixed point (32 fractional
  * bits) over C partial sums; this call first converts them into the fp32
  * input the next neuron update would use, so input_exc/input_inh are
- * readable (and writable) fp32 arrays. */
+ * readable (and writable) fp32 arrays. It also sorts the D delay-ring
+ * lists and the forced-row list into ascending order (a step writes them
+ * in workgroup completion order; no part of a step depends on it). */
 snn_status snn_get_state(snn_ctx *ctx, snn_state_view *out);
 
 /* Copies every non-NULL array of *in (caller device buffers) into the state

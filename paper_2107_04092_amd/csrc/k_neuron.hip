@@ -1,6 +1,6 @@
 // gfx950 kernels of the neuron part of a step: state initialisation and
-// fills, the neuron update (firing masks, histories, post traces) and the
-// compaction of spike / transmitted / forced lists with row snapshots.
+// fills, and the neuron update (firing masks, histories, post traces) that
+// also builds the spike / transmitted / forced lists with row snapshots.
 //
 // Built with -ffp-contract=off: the neuron update must reproduce a fixed
 // fp32 operation order, so no multiply-add is ever fused.
@@ -42,12 +42,36 @@ __global__ __launch_bounds__(kBlock) void k_fill(T *p, int64_t count, T value)
 }
 
 // ---------------------------------------------------------------------------
-// (1) neuron update. One thread per neuron, one wave64 per mask word.
+// (1) neuron update, one thread per neuron and one wave64 per mask word, and
+// the lists of the step: spikes (into the delay ring), forced plastic rows
+// and the snapshots of the rows to bring up to date (see CompactArgs).
+//
+// List offsets: each workgroup reserves its stretch of the spike list and of
+// the forced-row list with ONE 64-bit atomic on a packed word (spikes in bits
+// 0-23, forced rows in bits 24-47, a workgroup ticket in bits 48-63; counts
+// stay below n < 2^24). Same-address device-scope atomics serialise, so a
+// workgroup is large (fewer reservations). The workgroup whose ticket comes
+// last holds every other contribution in the returned value: it publishes
+// the counts and clears the word for the next step. Transmitting rows need
+// no reservation: a row transmitting at t spiked at t-D+1, when its position
+// in that step's spike list was recorded (spk_pos); its snapshot goes to the
+// same position, so snapshots line up with the delay-ring list delivery reads.
 
-__global__ __launch_bounds__(kBlock) void k_neuron(NeuronArgs a)
+static_assert((1 << 24) / kNeuronBlock <= 65536, "workgroup ticket must fit in 16 bits");
+
+__global__ __launch_bounds__(kNeuronBlock) void k_neuron(NeuronArgs a, CompactArgs lst)
 {
+    constexpr int NWV = kNeuronBlock / kWave;
+    __shared__ float s_dpow[kMaxAge + 1];
+    __shared__ int s_cnt[2][NWV];
+    __shared__ unsigned long long s_st[4];
+    __shared__ unsigned long long s_base;
     const int tid = threadIdx.x;
-    const int i = blockIdx.x * kBlock + tid;
+    const bool plastic = lst.n_plastic_rows > 0;
+    if (plastic)
+        for (int q = tid; q <= kMaxAge; q += kNeuronBlock) s_dpow[q] = lst.dpow[q];
+    if (tid < 4) s_st[tid] = 0ull;
+    const int i = blockIdx.x * kNeuronBlock + tid;
     int s = 0, tx = 0, forced = 0;
     bool fired_recently = false;
     if (i < a.n) {
@@ -140,133 +164,164 @@ __global__ __launch_bounds__(kBlock) void k_neuron(NeuronArgs a)
     const uint64_t m = ballot64(s), txm = ballot64(tx), fm = ballot64(forced);
     const uint64_t rcm = ballot64(fired_recently);
     const int wave = tid / kWave, lane = tid % kWave;
-    const int64_t word = (int64_t)blockIdx.x * (kBlock / kWave) + wave;
-    __shared__ int s_cnt[3][kBlock / kWave];
+    const int64_t word = (int64_t)blockIdx.x * NWV + wave;
     if (lane == 0) {
         if (word * kWave < a.n) {
             a.mask[word] = m;
             a.txmask[word] = txm;
-            a.fmask[word] = fm;
             a.recent[word] = rcm;
         }
         s_cnt[0][wave] = __popcll(m);
-        s_cnt[1][wave] = __popcll(txm);
-        s_cnt[2][wave] = __popcll(fm);
+        s_cnt[1][wave] = __popcll(fm);
     }
-    __syncthreads();
-    if (tid == 0) {
-        int c0 = 0, c1 = 0, c2 = 0;
-#pragma unroll
-        for (int q = 0; q < kBlock / kWave; ++q) {
-            c0 += s_cnt[0][q];
-            c1 += s_cnt[1][q];
-            c2 += s_cnt[2][q];
+    // position of a transmitting row in the spike list of step t-D+1
+    int txpos = -1;
+    if (tx && plastic && lst.dm1 > 0) txpos = lst.tx_pos[i];
+    __syncthreads();  // publishes s_cnt, s_dpow, s_st
+    // snapshots of this thread's row (taken before any kernel commits
+    // t_last / x_pre); their loads overlap the reservation below
+    RowInfo ri{};
+    int ri_ok = 0;
+    if (tx && plastic) {
+        if (i < lst.n_plastic_rows)
+            ri_ok = make_row_info(ri, i, lst.t, true, lst.dm1, lst.hw, lst.row_ptr, lst.pend,
+                                  lst.hist, lst.t_last, lst.xpre, s_dpow, lst.err);
+        if (!ri_ok) {  // nothing to bring up to date: the row is only delivered
+            ri = RowInfo{};
+            ri.k = i;
+            ri.rs = lst.row_ptr[i];
         }
-        a.blk_spk[blockIdx.x] = c0;
-        a.blk_tx[blockIdx.x] = c1;
-        a.blk_f[blockIdx.x] = c2;
+    } else if (forced) {
+        ri_ok = make_row_info(ri, i, lst.t, true, lst.dm1, lst.hw, lst.row_ptr, lst.pend,
+                              lst.hist, lst.t_last, lst.xpre, s_dpow, lst.err);
+    }
+    if (tid == 0) {
+        int spk = 0, fr = 0;
+#pragma unroll
+        for (int q = 0; q < NWV; ++q) {
+            spk += s_cnt[0][q];
+            fr += s_cnt[1][q];
+        }
+        const unsigned long long mine =
+            (unsigned long long)spk | ((unsigned long long)fr << 24) | (1ull << 48);
+        const unsigned long long old = atomicAdd(lst.acc, mine);
+        s_base = old;
+        if ((int)(old >> 48) == (int)gridDim.x - 1) {
+            const int n_spk = (int)(old & 0xffffffull) + spk;
+            const int n_forced = (int)((old >> 24) & 0xffffffull) + fr;
+            (void)atomicExch(lst.acc, 0ull);
+            *lst.spk_cnt = n_spk;
+            *lst.row_cnt = n_forced;
+            lst.gstats[kGSpikes] += n_spk;
+        }
+    }
+    if (lst.info_stats) {
+        const bool f = forced && ri_ok;
+        const long long v0 = wave_sum_i64(ri_ok ? 1 : 0), v1 = wave_sum_i64(f ? 1 : 0);
+        const long long v2 = wave_sum_i64(ri_ok ? ri.len : 0), v3 = wave_sum_i64(f ? ri.len : 0);
+        if (lane == 0) {
+            if (v0) atomicAdd(s_st + 0, (unsigned long long)v0);
+            if (v1) atomicAdd(s_st + 1, (unsigned long long)v1);
+            if (v2) atomicAdd(s_st + 2, (unsigned long long)v2);
+            if (v3) atomicAdd(s_st + 3, (unsigned long long)v3);
+        }
+    }
+    __syncthreads();  // publishes s_base, s_st
+    const unsigned long long base = s_base;
+    int o0 = (int)(base & 0xffffffull), o2 = (int)((base >> 24) & 0xffffffull);
+#pragma unroll
+    for (int q = 0; q < NWV; ++q) {
+        if (q < wave) {
+            o0 += s_cnt[0][q];
+            o2 += s_cnt[1][q];
+        }
+    }
+    const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+    // (the bounds checks only catch an accumulator left non-zero by a failed
+    // step; with a cleared one every offset is in range)
+    if (s) {
+        const int pos = o0 + __popcll(m & below);
+        if (pos < a.n) {
+            lst.spk_list[pos] = i;
+            if (plastic && lst.dm1 > 0) lst.spk_pos[i] = pos;
+            if (lst.dm1 == 0) txpos = pos;  // D = 1: transmitted as it fires
+        } else {
+            atomicOr(lst.err, kErrRing);
+        }
+    }
+    if (tx && plastic) {
+        if (txpos >= 0 && txpos < a.n)
+            lst.txinfo[txpos] = ri;
+        else
+            atomicOr(lst.err, kErrRing);
+    }
+    if (forced) {
+        const int r = o2 + __popcll(fm & below);
+        if (r < lst.n_plastic_rows) {
+            lst.row_list[r] = i;
+            lst.info[r] = ri;
+        } else {
+            atomicOr(lst.err, kErrRing);
+        }
+    }
+    if (lst.info_stats && tid == 0) {
+        int64_t *slot = lst.info_stats + (int64_t)blockIdx.x * kStFields;
+        slot[kStRows] += (int64_t)s_st[0];
+        slot[kStForced] += (int64_t)s_st[1];
+        slot[kStSyn] += (int64_t)s_st[2];
+        slot[kStForcedSyn] += (int64_t)s_st[3];
     }
 }
 
-// Ascending lists from the masks: each workgroup adds the counts of the
-// workgroups before it, then ranks its bits. Spikes go to the delay-ring
-// slot of step t; forced plastic rows to the forced list with their
-// snapshots; each transmitting plastic row gets its snapshot at its position
-// in the transmitted list (the ring list of step t-D+1, which holds the same
-// neurons in the same ascending order).
-__global__ __launch_bounds__(kBlock) void k_compact(CompactArgs a)
+// Sorts a list of distinct neuron indices (capacity n entries, values in
+// [0, n)) into ascending order (one workgroup; not on the step's path):
+// scatter into a bitmap of nw = ceil(n/64) words, then read it back in order.
+// Entries past min(*cnt, n) are not read; out-of-range values are dropped.
+// With pos, records each index's new position.
+constexpr int kSortListBlock = 1024;
+__global__ __launch_bounds__(kSortListBlock) void k_sort_list(int32_t *list, const int32_t *cnt,
+                                                              uint64_t *bitmap, int32_t *pos,
+                                                              int32_t n, int32_t nw)
 {
-    __shared__ long long sh[kBlock / kWave];
-    __shared__ int s_pc[3][kBlock / kWave];
-    __shared__ float s_dpow[kMaxAge + 1];
-    const int tid = threadIdx.x, b = blockIdx.x;
-    for (int q = tid; q <= kMaxAge; q += kBlock) s_dpow[q] = a.dpow[q];
-    long long p0 = 0, p1 = 0, p2 = 0;
-    for (int q = tid; q < b; q += kBlock) {
-        p0 += a.blk_spk[q];
-        p1 += a.blk_tx[q];
-        p2 += a.blk_f[q];
-    }
-    // pack two prefix sums into one reduction (each < 2^31)
-    const long long packed = block_sum_i64((p0 << 32) | p1, sh);
-    p0 = packed >> 32;
-    p1 = packed & 0xffffffffll;
-    p2 = block_sum_i64(p2, sh);
-    const int wave = tid / kWave, lane = tid % kWave;
-    const int64_t word = (int64_t)b * (kBlock / kWave) + wave;
-    const bool inb = word < a.nw;
-    const uint64_t m = inb ? a.mask[word] : 0ull;
-    const uint64_t txm = inb ? a.txmask[word] : 0ull;
-    const uint64_t fm = inb ? a.fmask[word] : 0ull;
-    if (lane == 0) {
-        s_pc[0][wave] = __popcll(m);
-        s_pc[1][wave] = __popcll(txm);
-        s_pc[2][wave] = __popcll(fm);
+    __shared__ long long sh[kSortListBlock / kWave];
+    const int tid = threadIdx.x;
+    const int len = min(max(*cnt, 0), n);
+    for (int q = tid; q < nw; q += kSortListBlock) bitmap[q] = 0ull;
+    __syncthreads();
+    for (int q = tid; q < len; q += kSortListBlock) {
+        const int k = list[q];
+        if (k >= 0 && k < n)
+            atomicOr((unsigned long long *)(bitmap + (k >> 6)), 1ull << (k & 63));
     }
     __syncthreads();
-    int o0 = (int)p0, o1 = (int)p1, o2 = (int)p2, t0 = 0, t2 = 0;
-#pragma unroll
-    for (int q = 0; q < kBlock / kWave; ++q) {
-        if (q < wave) {
-            o0 += s_pc[0][q];
-            o1 += s_pc[1][q];
-            o2 += s_pc[2][q];
+    long long done = 0;
+    for (int w0 = 0; w0 < nw; w0 += kSortListBlock) {
+        const int wi = w0 + tid;
+        // agent-scope loads: the bits were set by atomics at L2
+        const uint64_t bits =
+            wi < nw ? __hip_atomic_load(bitmap + wi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                    : 0ull;
+        const long long incl = block_incl_scan_i64_n<kSortListBlock>(__popcll(bits), sh);
+        int o = (int)(done + incl - __popcll(bits));
+        for (uint64_t b = bits; b; b &= b - 1, ++o) {
+            const int k = wi * 64 + __ffsll((long long)b) - 1;
+            list[o] = k;
+            if (pos) pos[k] = o;
         }
-        t0 += s_pc[0][q];
-        t2 += s_pc[2][q];
+        done += block_sum_i64_n<kSortListBlock>(__popcll(bits), sh);
     }
-    const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
-    const int i = (int)(word * kWave) + lane;
-    if ((m >> lane) & 1ull) a.spk_list[o0 + __popcll(m & below)] = i;
-    long long st_rows = 0, st_forced = 0, st_syn = 0, st_fsyn = 0;
-    if ((txm >> lane) & 1ull) {
-        RowInfo ri;
-        if (i < a.n_plastic_rows &&
-            make_row_info(ri, i, a.t, true, a.dm1, a.hw, a.row_ptr, a.pend, a.hist, a.t_last, a.xpre,
-                          s_dpow, a.err)) {
-            st_rows = 1;
-            st_syn = ri.len;
-        } else {
-            ri.k = i;
-            ri.rs = a.row_ptr[i];
-            ri.len = 0;
-            ri.age_pre = 0;
-            ri.xp0 = ri.xp_now = 0.f;
-            ri.pad = 0;
-        }
-        a.txinfo[o1 + __popcll(txm & below)] = ri;
-    }
-    if ((fm >> lane) & 1ull) {
-        const int r = o2 + __popcll(fm & below);
-        a.row_list[r] = i;
-        RowInfo ri;
-        if (make_row_info(ri, i, a.t, true, a.dm1, a.hw, a.row_ptr, a.pend, a.hist, a.t_last, a.xpre,
-                          s_dpow, a.err)) {
-            st_rows += 1;
-            st_forced = 1;
-            st_syn += ri.len;
-            st_fsyn = ri.len;
-        }
-        a.info[r] = ri;
-    }
-    if (b == (int)gridDim.x - 1 && tid == 0) {
-        *a.spk_cnt = (int)p0 + t0;
-        *a.row_cnt = (int)p2 + t2;
-        a.gstats[kGSpikes] += (int)p0 + t0;
-    }
-    if (a.info_stats) {
-        st_rows = block_sum_i64(st_rows, sh);
-        st_forced = block_sum_i64(st_forced, sh);
-        st_syn = block_sum_i64(st_syn, sh);
-        st_fsyn = block_sum_i64(st_fsyn, sh);
-        if (tid == 0) {
-            int64_t *slot = a.info_stats + (int64_t)b * kStFields;
-            slot[kStRows] += st_rows;
-            slot[kStForced] += st_forced;
-            slot[kStSyn] += st_syn;
-            slot[kStForcedSyn] += st_fsyn;
-        }
-    }
+}
+
+// Positions of the delay-ring entries: grid (ceil(n / kBlock), d).
+__global__ __launch_bounds__(kBlock) void k_ring_positions(const int32_t *ring,
+                                                           const int32_t *cnt, int32_t *pos,
+                                                           int32_t n)
+{
+    const int q = blockIdx.y;
+    const int r = blockIdx.x * kBlock + threadIdx.x;
+    if (r >= min(max(cnt[q], 0), n)) return;
+    const int k = ring[(int64_t)q * n + r];
+    if (k >= 0 && k < n) pos[(int64_t)q * n + k] = r;
 }
 
 // The fp32 input the next neuron update would compute from the partial sums.
@@ -330,17 +385,27 @@ hipError_t launch_copy_bytes(hipStream_t s, void *dst, const void *src, int64_t 
     return hipMemcpyAsync(dst, src, (size_t)bytes, hipMemcpyDeviceToDevice, s);
 }
 
-hipError_t launch_neuron(hipStream_t s, const NeuronArgs &a, KernelEvents ev)
+hipError_t launch_neuron(hipStream_t s, const NeuronArgs &a, const CompactArgs &c,
+                         KernelEvents ev)
 {
-    hipExtLaunchKernelGGL(k_neuron, dim3(blocks_for(a.n)), dim3(kBlock), 0, s,
-                          ev.start, ev.stop, 0, a);
+    hipExtLaunchKernelGGL(k_neuron, dim3(blocks_for(a.n, kNeuronBlock)), dim3(kNeuronBlock), 0, s,
+                          ev.start, ev.stop, 0, a, c);
     return hipGetLastError();
 }
 
-hipError_t launch_compact(hipStream_t s, const CompactArgs &a, KernelEvents ev)
+hipError_t launch_sort_list(hipStream_t s, int32_t *list, const int32_t *cnt, uint64_t *bitmap,
+                            int32_t *pos, int32_t n)
 {
-    hipExtLaunchKernelGGL(k_compact, dim3(blocks_for(a.n)), dim3(kBlock), 0, s,
-                          ev.start, ev.stop, 0, a);
+    hipLaunchKernelGGL(k_sort_list, dim3(1), dim3(kSortListBlock), 0, s, list, cnt, bitmap, pos, n,
+                       (n + 63) / 64);
+    return hipGetLastError();
+}
+
+hipError_t launch_ring_positions(hipStream_t s, const int32_t *ring, const int32_t *cnt,
+                                 int32_t *pos, int32_t n, int32_t d)
+{
+    hipLaunchKernelGGL(k_ring_positions, dim3(blocks_for(n), d), dim3(kBlock), 0, s, ring, cnt,
+                       pos, n);
     return hipGetLastError();
 }
 

@@ -19,7 +19,7 @@ namespace {
 // potentiates with the pre trace that includes the pre spike at t.
 //
 // Snapshots of every plastic row for a flush (bring all rows to step t, no
-// pre-synaptic spike). During a step the compaction kernel takes them.
+// pre-synaptic spike). During a step the neuron kernel takes them.
 
 __global__ __launch_bounds__(kBlock) void k_row_info(RowInfoArgs a)
 {

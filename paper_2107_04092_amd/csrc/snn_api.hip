@@ -50,10 +50,11 @@ struct snn_ctx {
     long long *apart = nullptr;  // fixed-point partial inputs [C][nacc][n]
     float *ain = nullptr;        // fp32 input [nacc][n] (teacher forcing / views)
     int32_t *ref = nullptr, *t_last = nullptr, *pend = nullptr;
-    uint64_t *hist = nullptr, *mask = nullptr, *txmask = nullptr, *fmask = nullptr;
+    uint64_t *hist = nullptr, *mask = nullptr, *txmask = nullptr;
     uint8_t *code = nullptr;  // per-neuron history codes (k_neuron), n + 16 bytes
     uint64_t *recent = nullptr;
-    int32_t *blk_spk = nullptr, *blk_tx = nullptr, *blk_f = nullptr;
+    unsigned long long *list_acc = nullptr;  // list reservations of the neuron kernel (0 between steps)
+    int32_t *spk_pos = nullptr;  // [D][n] spike-list positions (D > 1 with plasticity), else unused
     int32_t *ring = nullptr, *ring_cnt = nullptr;
     int32_t *rows = nullptr, *row_cnt = nullptr, *err_flag = nullptr, *maxlen = nullptr;
     int64_t *row_ptr = nullptr, *scratch = nullptr, *bsum = nullptr;
@@ -212,7 +213,7 @@ void derive(snn_ctx *c)
     const int64_t work = (int64_t)c->n_slices * c->chunks;
     c->dlv_blocks = (int32_t)((work + 7) / 8 * 8);
     c->dlv_slots = c->dlv_blocks > kGlobalMaxBlocks ? c->dlv_blocks : kGlobalMaxBlocks;
-    c->info_blocks = c->nblk;  // statistics slots of the compaction / flush snapshots
+    c->info_blocks = c->nblk;  // statistics slots of the neuron-kernel / flush snapshots
 }
 
 // Workspace plan: a bump allocator over the caller's buffer.
@@ -244,12 +245,10 @@ void plan_workspace(snn_ctx *c, uint8_t *base)
     c->ain = p.take<float>((int64_t)c->nacc * n);
     c->mask = p.take<uint64_t>(c->nw);
     c->txmask = p.take<uint64_t>(c->nw);
-    c->fmask = p.take<uint64_t>(c->nw);
     c->code = p.take<uint8_t>((int64_t)c->n + 16);
     c->recent = p.take<uint64_t>(c->nw);
-    c->blk_spk = p.take<int32_t>(c->nblk);
-    c->blk_tx = p.take<int32_t>(c->nblk);
-    c->blk_f = p.take<int32_t>(c->nblk);
+    c->list_acc = p.take<unsigned long long>(1);
+    c->spk_pos = p.take<int32_t>(c->delay > 1 ? (int64_t)c->delay * n : 1);
     c->ring = p.take<int32_t>((int64_t)c->delay * n);
     c->ring_cnt = p.take<int32_t>(c->delay);
     c->rows = p.take<int32_t>(n);
@@ -357,13 +356,13 @@ snn_status materialize_input(snn_ctx *c)
     return SNN_OK;
 }
 
-// Events of part `part` (0 neurons, 1 compaction, 2 plasticity, 3 delivery)
+// Events of part `part` (0 neurons and lists, 1 plasticity, 2 delivery)
 // of the current step when timing is on; marks the part as timed.
 KernelEvents part_events(snn_ctx *c, int part)
 {
     KernelEvents ev;
     if (c->t_used < c->t_cap) {
-        const size_t q = (size_t)c->t_used * 4 + part;
+        const size_t q = (size_t)c->t_used * kTimedParts + part;
         ev.start = c->tev[2 * q];
         ev.stop = c->tev[2 * q + 1];
         c->t_rec[q] = 1;
@@ -388,12 +387,8 @@ snn_status launch_step_neurons(snn_ctx *c)
     a.input_forced = c->input_forced;
     a.mask = c->mask;
     a.txmask = c->txmask;
-    a.fmask = c->fmask;
     a.code = c->code;
     a.recent = c->recent;
-    a.blk_spk = c->blk_spk;
-    a.blk_tx = c->blk_tx;
-    a.blk_f = c->blk_f;
     a.t = c->t;
     a.n = c->n;
     a.n_exc = c->cfg.n_exc;
@@ -414,20 +409,14 @@ snn_status launch_step_neurons(snn_ctx *c)
     a.fire_thr = c->fire_thr;
     a.seed = c->cfg.seed;
     for (int q = 0; q < kMaxPoisson; ++q) a.poisson[q] = c->cfg.poisson_cdf[q];
-    snn_status st = check_hip(c, launch_neuron(c->stream, a, part_events(c, 0)), "neuron kernel");
-    if (st) return st;
-    c->input_forced = 0;  // the input has been consumed; the next comes from delivery
     CompactArgs b{};
-    b.mask = c->mask;
-    b.txmask = c->txmask;
-    b.fmask = c->fmask;
-    b.blk_spk = c->blk_spk;
-    b.blk_tx = c->blk_tx;
-    b.blk_f = c->blk_f;
     b.spk_list = c->ring + (int64_t)ring_slot(c, c->t) * c->n;
     b.spk_cnt = c->ring_cnt + ring_slot(c, c->t);
     b.row_list = c->rows;
     b.row_cnt = c->row_cnt;
+    b.acc = c->list_acc;
+    b.spk_pos = c->spk_pos + (c->delay > 1 ? (int64_t)ring_slot(c, c->t) * c->n : 0);
+    b.tx_pos = c->spk_pos + (c->delay > 1 ? (int64_t)ring_slot(c, c->t - (c->delay - 1)) * c->n : 0);
     b.gstats = c->gstats;
     b.n = c->n;
     b.nw = c->nw;
@@ -445,8 +434,10 @@ snn_status launch_step_neurons(snn_ctx *c)
     b.t = c->t;
     b.dm1 = c->delay - 1;
     for (int q = 0; q <= kMaxAge; ++q) b.dpow[q] = c->dpow[q];
-    st = check_hip(c, launch_compact(c->stream, b, part_events(c, 1)), "compaction kernel");
+    snn_status st =
+        check_hip(c, launch_neuron(c->stream, a, b, part_events(c, 0)), "neuron kernel");
     if (st) return st;
+    c->input_forced = 0;  // the input has been consumed; the next comes from delivery
     c->last_neuron_t = c->t;
     return SNN_OK;
 }
@@ -502,7 +493,7 @@ StdpArgs stdp_args(snn_ctx *c, bool flush)
 }
 
 // The plasticity part for rows forced by the 64-step history window (their
-// snapshots were taken by the compaction kernel); rows transmitting at t are
+// snapshots were taken by the neuron kernel); rows transmitting at t are
 // brought up to date by the delivery part. A flush (every plastic row up to
 // step t-1, no pre-synaptic spike) takes its snapshots first. The synapse
 // pass commits t_last and the pre traces.
@@ -558,10 +549,10 @@ snn_status launch_step_plasticity(snn_ctx *c)
         a.mu = c->mu;
         a.stats = c->syn_stats;
         a.syn_count = c->gstats + kGNaiveSyn;
-        return check_hip(c, launch_stdp_naive(c->stream, a, kStdpRowsBlocks, part_events(c, 2)),
+        return check_hip(c, launch_stdp_naive(c->stream, a, kStdpRowsBlocks, part_events(c, 1)),
                          "naive STDP");
     }
-    return launch_plasticity(c, false, c->stream, part_events(c, 2));
+    return launch_plasticity(c, false, c->stream, part_events(c, 1));
 }
 
 
@@ -609,7 +600,7 @@ snn_status launch_step_delivery(snn_ctx *c, int32_t mode)
     if (mode == SNN_DELIVER_LDS_SLICE) {
         // the transmitting rows' plasticity is fused into slice delivery
         st = check_hip(c, launch_deliver_lds(c->stream, a, c->dlv_blocks, dlv_lds_bytes(c),
-                                             part_events(c, 3)),
+                                             part_events(c, 2)),
                        "slice delivery kernel");
         if (st) return st;
         c->n_parts = c->chunks;
@@ -618,7 +609,7 @@ snn_status launch_step_delivery(snn_ctx *c, int32_t mode)
         c->input_forced = c->chunks == 1 ? 1 : 0;
         return SNN_OK;
     }
-    const KernelEvents ev = part_events(c, 3);
+    const KernelEvents ev = part_events(c, 2);
     KernelEvents last{ev.start, ev.stop};
     if (a.plastic) {
         // bring the transmitting rows up to date first (row-wise, L2 gathers)
@@ -749,6 +740,7 @@ snn_status snn_bind_workspace(snn_ctx *c, void *device_ptr, size_t bytes)
     if (e == hipSuccess) e = launch_fill_f32(c->stream, c->ain, (int64_t)c->nacc * c->n, 0.f);
     if (e == hipSuccess) e = launch_fill_i32(c->stream, c->ring_cnt, c->delay, 0);
     if (e == hipSuccess) e = launch_fill_i32(c->stream, c->row_cnt, 1, 0);
+    if (e == hipSuccess) e = launch_fill_i64(c->stream, (int64_t *)c->list_acc, 1, 0);
     if (e == hipSuccess) e = launch_fill_i32(c->stream, c->err_flag, 1, 0);
     if (e == hipSuccess) e = launch_fill_i32(c->stream, c->pend, c->n, 0);
     snn_status st = check_hip(c, e, "workspace initialisation");
@@ -981,8 +973,8 @@ snn_status snn_record_kernel_times(snn_ctx *c, int32_t max_steps)
     snn_status st = check_hip(c, hipStreamSynchronize(c->stream), "kernel timing");
     if (st) return st;
     for (hipEvent_t e : c->tev) (void)hipEventDestroy(e);
-    c->tev.assign((size_t)max_steps * 8, nullptr);
-    c->t_rec.assign((size_t)max_steps * 4, 0);
+    c->tev.assign((size_t)max_steps * kTimedParts * 2, nullptr);
+    c->t_rec.assign((size_t)max_steps * kTimedParts, 0);
     c->t_cap = c->t_used = 0;
     for (hipEvent_t &e : c->tev) {
         if (hipEventCreate(&e) != hipSuccess) {
@@ -1004,11 +996,11 @@ snn_status snn_get_kernel_times(snn_ctx *c, double *mean_ms, int32_t *steps)
     if (!c || !mean_ms || !steps) return SNN_EINVAL;
     snn_status st = check_hip(c, hipStreamSynchronize(c->stream), "kernel timing");
     if (st) return st;
-    for (int part = 0; part < 4; ++part) {
+    for (int part = 0; part < kTimedParts; ++part) {
         double sum = 0;
         int cnt = 0;
         for (int q = 0; q < c->t_used; ++q) {
-            const size_t k = (size_t)q * 4 + part;
+            const size_t k = (size_t)q * kTimedParts + part;
             if (!c->t_rec[k]) continue;
             float ms = 0;
             st = check_hip(c, hipEventElapsedTime(&ms, c->tev[2 * k], c->tev[2 * k + 1]),
@@ -1038,6 +1030,18 @@ snn_status snn_get_state(snn_ctx *c, snn_state_view *out)
     snn_status st = require_ws(c);
     if (st) return st;
     st = materialize_input(c);
+    if (st) return st;
+    for (int q = 0; q < c->delay && !st; ++q)
+        st = check_hip(c,
+                       launch_sort_list(c->stream, c->ring + (int64_t)q * c->n, c->ring_cnt + q,
+                                        (uint64_t *)c->scratch,
+                                        c->delay > 1 ? c->spk_pos + (int64_t)q * c->n : nullptr,
+                                        c->n),
+                       "list sort");
+    if (!st)
+        st = check_hip(c, launch_sort_list(c->stream, c->rows, c->row_cnt, (uint64_t *)c->scratch,
+                                           nullptr, c->n),
+                       "list sort");
     if (st) return st;
     std::memset(out, 0, sizeof *out);
     out->t = c->t;
@@ -1090,6 +1094,13 @@ snn_status snn_set_state(snn_ctx *c, const snn_state_view *in)
     for (const Item &it : items) {
         if (!it.src || !it.dst) continue;
         st = check_hip(c, launch_copy_bytes(c->stream, it.dst, it.src, it.bytes), "state copy");
+        if (st) return st;
+    }
+    if (c->delay > 1 && (in->ring_lists || in->ring_counts)) {
+        st = check_hip(c,
+                       launch_ring_positions(c->stream, c->ring, c->ring_cnt, c->spk_pos, c->n,
+                                             c->delay),
+                       "ring positions");
         if (st) return st;
     }
     c->t = in->t;

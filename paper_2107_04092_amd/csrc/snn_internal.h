@@ -8,6 +8,8 @@
 namespace snn {
 
 constexpr int kBlock = 256;          // threads per workgroup of the element kernels
+constexpr int kNeuronBlock = 1024;   // threads per workgroup of the neuron update (>= kBlock;
+                                     // large: one list reservation per workgroup)
 constexpr int kWave = 64;            // CDNA wavefront width
 constexpr int kMaxPoisson = 32;
 constexpr int kMaxSortRow = 16384;   // longest row the LDS row sort accepts
@@ -36,7 +38,7 @@ enum StdpStat { kStRows = 0, kStForced = 1, kStSyn = 2, kStForcedSyn = 3, kStFie
 enum GlobalStat { kGSpikes = 0, kGNaiveSyn = 1, kGFields = 8 };
 
 // Error bits raised by kernels (device int32, ORed).
-enum DevError { kErrIndex = 1, kErrRowTooLong = 2, kErrWindow = 4 };
+enum DevError { kErrIndex = 1, kErrRowTooLong = 2, kErrWindow = 4, kErrRing = 8 };
 
 struct NeuronArgs {
     float *v;
@@ -51,11 +53,9 @@ struct NeuronArgs {
     int32_t input_forced;
     uint64_t *mask;         // spikes emitted at t
     uint64_t *txmask;       // spikes transmitted at t (emitted at t-D+1)
-    uint64_t *fmask;        // plastic rows forced at t (idle for 64 steps, not transmitting)
     uint8_t *code;          // per neuron: 0 no spike in the last 64 steps, 1 + i one spike
                             // at step t-i, kCodeMulti more than one (see k_neuron)
     uint64_t *recent;       // neurons with a spike in the last 64 steps (hist != 0)
-    int32_t *blk_spk, *blk_tx, *blk_f;
     int64_t t;
     int32_t n, n_exc, model, n_plastic_rows, dm1, ref_steps, poisson_len, n_parts, hw;
     float k_m, v_th, v_reset, v_inf, d_e, d_i, j_ext, d_minus;
@@ -66,16 +66,24 @@ struct NeuronArgs {
 
 struct RowInfo;
 
+// The lists k_neuron builds: spikes of step t (into the delay ring), forced
+// plastic rows, and the snapshots of the rows to update at t. Each workgroup
+// reserves its stretch of every list with one atomic add per list, so a list
+// is ascending within each workgroup's 256 neurons, the stretches in any
+// order; the last workgroup to finish publishes the counts and resets the
+// accumulators for the next step.
 struct CompactArgs {
-    const uint64_t *mask, *txmask, *fmask;
-    const int32_t *blk_spk, *blk_tx, *blk_f;
-    int32_t *spk_list, *spk_cnt;   // ascending spikes of step t (delay-ring slot)
+    int32_t *spk_list, *spk_cnt;   // spikes of step t (delay-ring slot t mod D)
     int32_t *row_list, *row_cnt;   // forced plastic rows
+    unsigned long long *acc;       // packed list reservations (see k_neuron); 0 between steps
+    // position of each neuron in the spike list of the step it last fired
+    // (only D > 1 with plasticity): written for step t, read for step t-D+1
+    int32_t *spk_pos, *tx_pos;
     int64_t *gstats;
     int32_t n, nw, n_plastic_rows, hw;
     // snapshots of the plastic rows to update at step t (see RowInfo): forced
-    // rows in list order, transmitting rows at their position in the
-    // transmitted list (which is the delay-ring list of step t-D+1)
+    // rows aligned with row_list; transmitting rows aligned with the
+    // delay-ring list of step t-D+1 (txinfo[r].k = that list's entry r)
     RowInfo *info;
     RowInfo *txinfo;
     const int64_t *row_ptr;
@@ -203,6 +211,8 @@ struct GraphArgs {
 struct KernelEvents {
     hipEvent_t start = nullptr, stop = nullptr;
 };
+// timed parts of a step: neuron update with its lists, plasticity, delivery
+constexpr int kTimedParts = 3;
 
 // ---- launchers (k_*.hip); all enqueue on `s` and return the launch
 // status of the last kernel they started.
@@ -214,8 +224,16 @@ hipError_t launch_fill_i64(hipStream_t s, int64_t *p, int64_t count, int64_t val
 hipError_t launch_fill_i32(hipStream_t s, int32_t *p, int64_t count, int32_t value);
 hipError_t launch_fill_ll(hipStream_t s, long long *p, int64_t count, long long value);
 hipError_t launch_copy_bytes(hipStream_t s, void *dst, const void *src, int64_t bytes);
-hipError_t launch_neuron(hipStream_t s, const NeuronArgs &a, KernelEvents ev = {});
-hipError_t launch_compact(hipStream_t s, const CompactArgs &a, KernelEvents ev = {});
+hipError_t launch_neuron(hipStream_t s, const NeuronArgs &a, const CompactArgs &b,
+                         KernelEvents ev = {});
+// sorts list[0 .. min(*cnt, n)) (distinct values in [0, n)) in place and,
+// when pos is given, sets pos[list[r]] = r; bitmap: ceil(n/64) words of
+// device scratch
+hipError_t launch_sort_list(hipStream_t s, int32_t *list, const int32_t *cnt, uint64_t *bitmap,
+                            int32_t *pos, int32_t n);
+// pos[q n + ring[q n + r]] = r for every delay-ring slot q < d and r < its count
+hipError_t launch_ring_positions(hipStream_t s, const int32_t *ring, const int32_t *cnt,
+                                 int32_t *pos, int32_t n, int32_t d);
 hipError_t launch_row_info(hipStream_t s, const RowInfoArgs &a, int64_t max_rows);
 hipError_t launch_stdp(hipStream_t s, const StdpArgs &a, int blocks, size_t lds, KernelEvents ev = {});
 hipError_t launch_stdp_rows(hipStream_t s, const StdpArgs &a, int blocks, KernelEvents ev = {});

@@ -230,12 +230,12 @@ def snn_record_kernel_times(ctx, max_steps):
     _check(ctx, load().snn_record_kernel_times(ctx, int(max_steps)))
 
 
-KERNEL_PARTS = ("neuron", "compaction", "plasticity", "delivery")
+KERNEL_PARTS = ("neuron", "plasticity", "delivery")
 
 
 def snn_get_kernel_times(ctx):
     """Mean device milliseconds per step of each part, and the steps recorded."""
-    ms = (ctypes.c_double * 4)()
+    ms = (ctypes.c_double * len(KERNEL_PARTS))()
     steps = _i32()
     _check(ctx, load().snn_get_kernel_times(ctx, ms, ctypes.byref(steps)))
     return dict(zip(KERNEL_PARTS, list(ms))), steps.value

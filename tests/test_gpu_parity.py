@@ -177,6 +177,33 @@ def test_checkpoint_restore_resumes_identically():
     assert_close(to_np(b.graph()["w"]), to_np(a.graph()["w"]), "weights after restore")
 
 
+@pytest.mark.parametrize("mode", [LDS, GLOBAL], ids=["lds", "global"])
+@pytest.mark.parametrize("delay", [1, 3])
+def test_free_run_with_state_reads(mode, delay):
+    """Bernoulli sources run free on both sides. Reading the state mid-run
+    puts the step's lists in ascending order (and re-records the delay-ring
+    positions the transmitting rows' snapshots use); later steps must not
+    notice. Spike lists come back ascending and equal the oracle's."""
+    p = wl.preset("stress", n=3000, p_or_fanout=120, p_fire=0.03, delay=delay)
+    net = gpu_net(p, slice_width=512, spike_chunks=2)
+    o = oracle_net(p)
+    for chunk in (37, 41, 12):
+        net.step(chunk, mode)
+        o.step(chunk)
+        s = net.state()
+        mask, lst = o.spikes()
+        assert np.array_equal(to_np(s["spike_mask"]).view(np.uint64), mask)
+        cnt = int(to_np(s["spike_count"])[0])
+        assert np.array_equal(to_np(s["spike_list"])[:cnt], lst)
+        ring = to_np(s["ring_lists"]).reshape(delay, -1)
+        rc = to_np(s["ring_counts"])
+        for q in range(delay):
+            assert np.all(np.diff(ring[q, :rc[q]]) > 0), "ring slot %d not ascending" % q
+    net.flush_plasticity()
+    compare_all_plastic_weights(net, o)
+    assert net.stats()["device_errors"] == 0
+
+
 ALGO_CASES = [
     ("brunel_plus", dict(n=2500, n_exc=2000), 260, 512, 2),
     ("stress", dict(n=6000, p_or_fanout=200, p_fire=0.02), 200, 1024, 4),
