@@ -200,10 +200,10 @@ __global__ __launch_bounds__(kStdpBlock) void k_stdp(StdpArgs a)
 //
 // Parts start at 64-byte lines of the weight array, and a line that holds a
 // changed weight is stored whole (its unchanged weights included), so the
-// L2 writes no partial line back to HBM. Two parts are in flight per wave:
-// the targets and weights of the next part are loaded while the current one
-// is looked up, updated and stored; the next row's snapshot is fetched one
-// part ahead.
+// L2 writes no partial line back to HBM. Two parts are held per wave: the
+// targets and weights of one are loaded while the other is looked up,
+// updated and stored (both are in flight from the start); the next row's
+// snapshot is fetched one part ahead.
 
 template <int U>
 struct RowPart {
@@ -229,15 +229,6 @@ __device__ __forceinline__ void gather_hist(const uint64_t *hist, int j, uint64_
     }
 }
 
-template <int U>
-__device__ __forceinline__ void row_part_at(RowPart<U> &p, const StdpArgs &a, int i, int nrows)
-{
-    p.i = i;
-    p.ri = RowInfo{};
-    if (i < nrows) p.ri = a.info[i];
-    p.base = -(int)(p.ri.rs & 15);
-}
-
 // Issues the loads of part p. Every lane loads from an address inside the
 // row (clamped) and selects afterwards: a load whose result is used under a
 // lane condition makes the compiler wait for it inside that condition, which
@@ -259,8 +250,10 @@ __device__ __forceinline__ void rows_issue(RowPart<U> &p, const int32_t *col, co
     for (int u = 0; u < U; ++u) {
         const int q = p.base + u * kWave + lane;
         const int qc = min(max(q, 0), len - 1);
-        p.j[u] = col[p.ri.rs + qc];
-        p.w[u] = wgt[p.ri.rs + qc];
+        // streaming (non-temporal) loads: the row is read once, and the
+        // gathered histories stay in L2
+        p.j[u] = __builtin_nontemporal_load(col + p.ri.rs + qc);
+        p.w[u] = __builtin_nontemporal_load(wgt + p.ri.rs + qc);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -287,12 +280,33 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
     const int nrows = a.row_cnt ? *a.row_cnt : a.n_rows_all;
     long long written = 0;
 
-    RowPart<U> A, B;
-    row_part_at(A, a, gw, nrows);
-    rows_issue(A, col, wgt, lane);  // the first loads overlap the staging
-    RowInfo la = RowInfo{};         // lookahead: snapshot of the next row
-    int la_i = gw + nwv;
+    // cursor: the next part to issue (row snapshot, row-list index, base);
+    // la: snapshot of the row after the cursor's
+    RowInfo cur = RowInfo{}, la = RowInfo{};
+    int cur_i = gw, la_i = gw + nwv;
+    if (cur_i < nrows) cur = a.info[cur_i];
     if (la_i < nrows) la = a.info[la_i];
+    int cur_base = -(int)(cur.rs & 15);
+    auto issue = [&](RowPart<U> &p) {
+        p.ri = cur;
+        p.i = cur_i;
+        p.base = cur_base;
+        rows_issue(p, col, wgt, lane);
+        if (cur.age_pre != 0 && cur_base + U * kWave < cur.len) {  // rest of the row
+            cur_base += U * kWave;
+        } else {  // the lookahead row
+            cur = la;
+            cur_i = la_i;
+            cur_base = -(int)(la.rs & 15);
+            la_i += nwv;
+            la = RowInfo{};
+            if (la_i < nrows) la = a.info[la_i];
+        }
+    };
+    // the first two parts are in flight before the staging
+    RowPart<U> A, B;
+    issue(A);
+    issue(B);
     for (int q = tid; q <= kMaxAge; q += NT) s_dpow[q] = a.dpow[q];
     const uint8_t *s_code = s_sum;
     const uint64_t *s_recent = (const uint64_t *)s_sum;
@@ -304,99 +318,138 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
     }
     __syncthreads();
 
-    // look-ups of `p`, then the next part's loads, then p's update and stores
-    auto step = [&](RowPart<U> &p, RowPart<U> &nx) {
+    // Look-ups, update and stores of part p (the other part's loads are in
+    // flight meanwhile); then p takes the next part's loads. The part's
+    // candidate synapses (targets that fired within the summary's reach) are
+    // appended densely to a queue of this wave in LDS (target, weight),
+    // updated 64 per pass with every lane busy (all passes' history gathers
+    // first, then the updates), and each owner lane takes its new weight and
+    // changed flag back for the line stores: the divergent per-synapse loops
+    // run over candidates only, not over every lane of every slot.
+    const int tbytes = a.code ? ((a.n + 15) / 16) * 16 : a.recent ? a.nw * 8 : 0;
+    int32_t *q_j = (int32_t *)(s_sum + tbytes) + (tid / kWave) * (2 * U * kWave);
+    float *q_w = (float *)(q_j + U * kWave);
+    auto step = [&](RowPart<U> &p) {
         const RowInfo ri = p.ri;
         const int age = ri.age_pre & 0xff, pre = ri.age_pre >> 8;
         uint64_t m0, m1;
         window_masks(age, m0, m1);
-        if (HW == 1) m1 = 0ull;  // lets the compiler drop the second word
-        bool live[U];
-        uint64_t h[U], g[U];  // window bits of the target's history words 0 and 1
-        float y[U];
+        if (HW == 1) m1 = 0ull;
+        bool cand[U];
         if (!pre && a.code) {
-            int cd[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) cd[u] = s_code[max(p.j[u], 0)];
+            for (int u = 0; u < U; ++u) cand[u] = p.j[u] >= 0 && s_code[max(p.j[u], 0)] != 0;
+        } else if (!pre && a.recent) {
+            uint64_t rw[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                live[u] = p.j[u] >= 0 && cd[u] != 0;
-                gather_hist<HW>(hist, (live[u] && cd[u] == kCodeMulti) ? p.j[u] : 0, h[u], g[u]);
-            }
+            for (int u = 0; u < U; ++u) rw[u] = s_recent[max(p.j[u], 0) >> 6];
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int pos = (cd[u] - 1) & 127;  // single spike: pos steps ago
-                const uint64_t one = 1ull << (pos & 63);
-                const bool multi = cd[u] == kCodeMulti;
-                h[u] = !live[u] ? 0ull : (multi ? h[u] : (pos < 64 ? one : 0ull)) & m0;
-                g[u] = !live[u] ? 0ull : (multi ? g[u] : (pos >= 64 ? one : 0ull)) & m1;
-                y[u] = 0.f;
-            }
+            for (int u = 0; u < U; ++u)
+                cand[u] = p.j[u] >= 0 && ((rw[u] >> (p.j[u] & 63)) & 1ull);
         } else {
-            if (!pre && a.recent) {
-                uint64_t rw[U];
 #pragma unroll
-                for (int u = 0; u < U; ++u) rw[u] = s_recent[max(p.j[u], 0) >> 6];
+            for (int u = 0; u < U; ++u) cand[u] = p.j[u] >= 0;
+        }
+        // queue offsets: wave-uniform base and ballot per slot (SGPRs); a
+        // lane's entry of slot u is qb[u] + its rank among the slot's lanes
+        uint64_t bl[U];
+        int qb[U];
+        int qn = 0;
 #pragma unroll
-                for (int u = 0; u < U; ++u)
-                    live[u] = p.j[u] >= 0 && ((rw[u] >> (p.j[u] & 63)) & 1ull);
-            } else {
+        for (int u = 0; u < U; ++u) {
+            bl[u] = ballot64(cand[u]);
+            qb[u] = qn;
+            qn += (int)__popcll(bl[u]);
+        }
 #pragma unroll
-                for (int u = 0; u < U; ++u) live[u] = p.j[u] >= 0;
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u) gather_hist<HW>(hist, live[u] ? p.j[u] : 0, h[u], g[u]);
-            if (pre) {
-#pragma unroll
-                for (int u = 0; u < U; ++u) y[u] = ypost[live[u] ? p.j[u] : 0];
-            } else {
-#pragma unroll
-                for (int u = 0; u < U; ++u) y[u] = 0.f;
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                h[u] = live[u] ? (h[u] & m0) : 0ull;
-                g[u] = live[u] ? (g[u] & m1) : 0ull;
+        for (int u = 0; u < U; ++u) {
+            if (cand[u]) {
+                const int e = qb[u] + lane_rank(bl[u]);
+                q_j[e] = p.j[u];
+                q_w[e] = p.w[u];
             }
         }
-        // next part: the rest of this row, else the lookahead row
-        if (ri.age_pre != 0 && p.base + U * kWave < ri.len) {
-            nx.ri = ri;
-            nx.i = p.i;
-            nx.base = p.base + U * kWave;
-        } else {
-            nx.ri = la;
-            nx.i = la_i;
-            nx.base = -(int)(la.rs & 15);
-            la_i += nwv;
-            la = RowInfo{};
-            if (la_i < nrows) la = a.info[la_i];
+        __builtin_amdgcn_wave_barrier();
+        // passes of 64 entries, in two halves of U/2 passes (fewer registers
+        // held); the second half runs only for more than U/2 x 64 entries
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            constexpr int H = U / 2;
+            if (half * H * kWave >= qn) break;  // wave-uniform
+            uint64_t h[H], g[H];
+            float y[H], qw[H];
+            int cd[H];
+#pragma unroll
+            for (int q = 0; q < H; ++q) {
+                const int e0 = (half * H + q) * kWave;
+                h[q] = g[q] = 0ull;
+                y[q] = qw[q] = 0.f;
+                cd[q] = 0;
+                if (e0 < qn) {  // wave-uniform
+                    const int e = e0 + lane;
+                    const int j = e < qn ? q_j[e] : 0;
+                    qw[q] = q_w[e];
+                    if (!pre && a.code) {
+                        cd[q] = s_code[j];
+                        gather_hist<HW>(hist, cd[q] == kCodeMulti ? j : 0, h[q], g[q]);
+                    } else {
+                        gather_hist<HW>(hist, j, h[q], g[q]);
+                    }
+                    if (pre) y[q] = ypost[j];
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < H; ++q) {
+                const int e = (half * H + q) * kWave + lane;
+                if (e < qn) {
+                    uint64_t h0 = h[q], h1 = g[q];
+                    if (!pre && a.code && cd[q] != kCodeMulti) {
+                        const int ps = (cd[q] - 1) & 127;  // single spike: ps steps ago
+                        h0 = ps < 64 ? 1ull << (ps & 63) : 0ull;
+                        h1 = ps >= 64 ? 1ull << (ps & 63) : 0ull;
+                    }
+                    h0 &= m0;
+                    h1 &= m1;
+                    const bool chg = h0 || h1 || pre || !a.event;
+                    float w = qw[q];
+                    if (chg) {
+                        w = a.event ? stdp_synapse(w, h0, h1, age, pre, ri.xp0, ri.xp_now, y[q],
+                                                   s_dpow, c_pot, c_dep, mu)
+                                    : stdp_synapse_steps(w, h0, h1, age, pre, ri.xp0,
+                                                         ri.xp_now, y[q], s_dpow[1], c_pot,
+                                                         c_dep, mu);
+                        ++written;
+                    }
+                    q_w[e] = w;
+                    q_j[e] = chg ? 1 : 0;
+                }
+            }
         }
-        rows_issue(nx, col, wgt, lane);
+        __builtin_amdgcn_wave_barrier();
         if (ri.age_pre != 0 && p.base == -(int)(ri.rs & 15) && lane == 0) {  // first part
             a.t_last[ri.k] = (int32_t)a.t;
             a.xpre[ri.k] = ri.xp_now;
         }
+        const int len = ri.age_pre != 0 ? ri.len : 0;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const bool chg = live[u] && (h[u] || g[u] || pre || !a.event);
-            float w = p.w[u];
-            if (chg) {
-                w = a.event ? stdp_synapse(w, h[u], g[u], age, pre, ri.xp0, ri.xp_now, y[u],
-                                           s_dpow, c_pot, c_dep, mu)
-                            : stdp_synapse_steps(w, h[u], g[u], age, pre, ri.xp0, ri.xp_now,
-                                                 y[u], s_dpow[1], c_pot, c_dep, mu);
-                ++written;
-            }
+            const int e = qb[u] + lane_rank(bl[u]);  // < (u + 1) * 64: inside the queue
+            const int rj = q_j[e];
+            const float rw = q_w[e];
+            const bool c = (bl[u] >> lane) & 1ull;
+            const bool chg = c && rj != 0;
+            const float w = c ? rw : p.w[u];
+            const int qi = p.base + u * kWave + lane;
             const uint64_t m = ballot64(chg);
-            if (((m >> line0) & 0xffffull) && p.j[u] >= 0)
-                wgt[ri.rs + p.base + u * kWave + lane] = w;
+            if (((m >> line0) & 0xffffull) && qi >= 0 && qi < len)
+                __builtin_nontemporal_store(w, wgt + ri.rs + qi);
         }
+        issue(p);
     };
     while (A.i < nrows) {
-        step(A, B);
+        step(A);
         if (B.i >= nrows) break;
-        step(B, A);
+        step(B);
     }
     // one atomic per wave: no workgroup barrier waits for the weight stores
     written = wave_sum_i64(written);
@@ -764,9 +817,10 @@ hipError_t launch_stdp_rows(hipStream_t s, const StdpArgs &a, int blocks, Kernel
 {
     static std::mutex mu;
     static int granted[2] = {64 * 1024, 64 * 1024};
-    const size_t lds = a.code     ? (((size_t)a.n + 15) / 16) * 16
-                       : a.recent ? (size_t)a.nw * sizeof(uint64_t)
-                                  : 0;
+    const size_t table = a.code     ? (((size_t)a.n + 15) / 16) * 16
+                         : a.recent ? (size_t)a.nw * sizeof(uint64_t)
+                                    : 0;
+    const size_t lds = table + stdp_rows_queue_bytes(a.hw);
     const void *kern = a.hw == 2 ? (const void *)k_stdp_rows<2> : (const void *)k_stdp_rows<1>;
     const hipError_t e = allow_dynamic_lds(kern, (int)lds, mu, granted[a.hw == 2]);
     if (e != hipSuccess) return e;

@@ -59,6 +59,13 @@ __device__ __forceinline__ long long wave_sum_i64(long long v)
     return v;
 }
 
+// Number of lanes below this one whose bit is set in a wave-uniform mask.
+__device__ __forceinline__ int lane_rank(uint64_t m)
+{
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                          __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
 // Sum over a kBlock-thread workgroup; every thread gets the total.
 __device__ __forceinline__ long long block_sum_i64(long long v, long long *sh)
 {

@@ -242,8 +242,15 @@ constexpr int kStdpRowsBlock = 1024;   // threads of the row-wise STDP kernel
 constexpr int kStdpRowsUnroll = 8;     // synapses per lane and row part (64-step histories)
 constexpr int kStdpRowsUnroll2 = 4;    // the same with 128-step histories
 constexpr int kStdpRowsBlocks = 256;   // its persistent grid (one workgroup per CU)
-constexpr int kCodeMax = 147456;       // LDS bytes of history codes one row-STDP workgroup stages
-constexpr int kRecentMaxWords = 16384; // LDS-staged spike-recency bitmap: up to 1M neurons
+// LDS of the row-wise STDP workgroup's candidate queues (one per wave: target
+// and weight of up to U x 64 synapses)
+constexpr int stdp_rows_queue_bytes(int hw)
+{
+    return (kStdpRowsBlock / kWave) * (hw == 2 ? kStdpRowsUnroll2 : kStdpRowsUnroll) * kWave * 8;
+}
+// the per-neuron summary it stages beside the queues (160 KB of LDS per workgroup)
+constexpr int kCodeMax = 163840 - stdp_rows_queue_bytes(1) - 1024;  // bytes of history codes
+constexpr int kRecentMaxWords = kCodeMax / 8;  // words of the spike-recency bitmap
 constexpr uint8_t kCodeMulti = 255;    // history code: two or more spikes in the window
 int stdp_static_bytes();  // static LDS of the slice STDP kernel (-1 on error)
 hipError_t launch_deliver_lds(hipStream_t s, const DeliverArgs &a, int blocks, size_t lds, KernelEvents ev = {});
