@@ -97,11 +97,9 @@ __global__ __launch_bounds__(kStdpBlock) void k_stdp(StdpArgs a)
     const int hw = a.hw;
     uint64_t *s_hist = (uint64_t *)stage;
     float *s_y = (float *)(stage + (size_t)a.width * hw * sizeof(uint64_t));
-    const int jn = min(a.width, a.n - j0);
-    for (int x = tid; x < jn; x += kStdpBlock) {
-        for (int q = 0; q < hw; ++q) s_hist[x * hw + q] = a.hist[(int64_t)(j0 + x) * hw + q];
-        s_y[x] = a.ypost[j0 + x];
-    }
+    const int jn = min(a.width, a.n - j0);  // > 0
+    stage_lds<kStdpBlock, 4>(s_hist, a.hist + (int64_t)j0 * hw, jn * hw);
+    stage_lds<kStdpBlock, 4>(s_y, a.ypost + j0, jn);
     for (int x = tid; x <= kMaxAge; x += kStdpBlock) s_dpow[x] = a.dpow[x];
     const int pv_lo = g * a.mult;
     const int pv_hi = min((g + 1) * a.mult, a.n_slices);
@@ -310,12 +308,10 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
     for (int q = tid; q <= kMaxAge; q += NT) s_dpow[q] = a.dpow[q];
     const uint8_t *s_code = s_sum;
     const uint64_t *s_recent = (const uint64_t *)s_sum;
-    if (a.code) {
-        const uint4 *src = (const uint4 *)a.code;
-        for (int q = tid; q < (a.n + 15) / 16; q += NT) ((uint4 *)s_sum)[q] = src[q];
-    } else if (a.recent) {
-        for (int q = tid; q < a.nw; q += NT) ((uint64_t *)s_sum)[q] = a.recent[q];
-    }
+    if (a.code)
+        stage_lds<NT, 4>((uint4 *)s_sum, (const uint4 *)a.code, (a.n + 15) / 16);
+    else if (a.recent)
+        stage_lds<NT, 4>((uint64_t *)s_sum, a.recent, a.nw);
     __syncthreads();
 
     // Look-ups, update and stores of part p (the other part's loads are in
@@ -481,7 +477,7 @@ __global__ __launch_bounds__(kNaiveBlock) void k_stdp_naive(NaiveArgs a)
 {
     extern __shared__ uint64_t s_fire[];
     const int tid = threadIdx.x, lane = tid % kWave;
-    for (int q = tid; q < a.nw; q += kNaiveBlock) s_fire[q] = a.mask[q];
+    stage_lds<kNaiveBlock, 4>(s_fire, a.mask, a.nw);
     __syncthreads();
     const int gw = (blockIdx.x * kNaiveBlock + tid) / kWave;
     const int nwv = gridDim.x * (kNaiveBlock / kWave);
@@ -600,12 +596,9 @@ __global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
     uint64_t *s_hist = (uint64_t *)(acc + span);
     float *s_y = (float *)(s_hist + (size_t)a.width * hw);
     if (a.plastic) {
-        const int jn = min(a.width, a.n - base);
-        for (int x = tid; x < jn; x += kDlvBlock) {
-            for (int q = 0; q < hw; ++q)
-                s_hist[x * hw + q] = a.hist[(int64_t)(base + x) * hw + q];
-            s_y[x] = a.ypost[base + x];
-        }
+        const int jn = min(a.width, a.n - base);  // > 0
+        stage_lds<kDlvBlock, 4>(s_hist, a.hist + (int64_t)base * hw, jn * hw);
+        stage_lds<kDlvBlock, 4>(s_y, a.ypost + base, jn);
         for (int x = tid; x <= kMaxAge; x += kDlvBlock) s_dpow[x] = a.dpow[x];
     }
     const int piv_stride = a.n_slices + 1;

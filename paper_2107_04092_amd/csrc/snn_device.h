@@ -59,6 +59,24 @@ __device__ __forceinline__ long long wave_sum_i64(long long v)
     return v;
 }
 
+// Copies count > 0 elements from global memory into LDS with an NT-thread
+// workgroup, R loads in flight per thread before their stores (a plain
+// strided loop would wait for each load before the next).
+template <int NT, int R, typename T>
+__device__ __forceinline__ void stage_lds(T *dst, const T *__restrict__ src, int count)
+{
+    for (int x0 = 0; x0 < count; x0 += NT * R) {
+        T v[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) v[r] = src[min(x0 + r * NT + (int)threadIdx.x, count - 1)];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int x = x0 + r * NT + (int)threadIdx.x;
+            if (x < count) dst[x] = v[r];
+        }
+    }
+}
+
 // Number of lanes below this one whose bit is set in a wave-uniform mask.
 __device__ __forceinline__ int lane_rank(uint64_t m)
 {
