@@ -42,163 +42,204 @@ __global__ __launch_bounds__(kBlock) void k_fill(T *p, int64_t count, T value)
 }
 
 // ---------------------------------------------------------------------------
-// (1) neuron update, one thread per neuron and one wave64 per mask word, and
-// the lists of the step: spikes (into the delay ring), forced plastic rows
-// and the snapshots of the rows to bring up to date (see CompactArgs).
+// (1) neuron update, one wave64 per mask word and kNeuronRounds neurons per
+// thread, and the lists of the step: spikes (into the delay ring), forced
+// plastic rows and the snapshots of the rows to bring up to date (see
+// CompactArgs).
 //
 // List offsets: each workgroup reserves its stretch of the spike list and of
 // the forced-row list with ONE 64-bit atomic on a packed word (spikes in bits
 // 0-23, forced rows in bits 24-47, a workgroup ticket in bits 48-63; counts
 // stay below n < 2^24). Same-address device-scope atomics serialise, so a
-// workgroup is large (fewer reservations). The workgroup whose ticket comes
+// workgroup covers many neurons (fewer reservations). The workgroup whose ticket comes
 // last holds every other contribution in the returned value: it publishes
 // the counts and clears the word for the next step. Transmitting rows need
 // no reservation: a row transmitting at t spiked at t-D+1, when its position
 // in that step's spike list was recorded (spk_pos); its snapshot goes to the
 // same position, so snapshots line up with the delay-ring list delivery reads.
 
-static_assert((1 << 24) / kNeuronBlock <= 65536, "workgroup ticket must fit in 16 bits");
+// One neuron's update at step t (i < n): its dynamics, its history word(s)
+// and post trace, its history code; returns spiked / transmitting / forced.
+__device__ __forceinline__ void neuron_update(const NeuronArgs &a, int i, int &s, int &tx,
+                                              int &forced, bool &fired_recently)
+{
+    if (a.model == 2) {
+        s = rng32(a.seed, 4, (uint64_t)a.t, (uint64_t)i) < a.fire_thr;
+    } else {
+        float ae, ai = 0.f;
+        if (a.input_forced) {
+            ae = a.ain[i];
+            if (a.model == 1) ai = a.ain[a.n + i];
+        } else {
+            long long se = a.apart[i];
+            for (int c = 1; c < a.n_parts; ++c) se += a.apart[c * a.part_stride + i];
+            ae = from_fix(se);
+            if (a.model == 1) {
+                long long si = a.apart[a.n + i];
+                for (int c = 1; c < a.n_parts; ++c) si += a.apart[c * a.part_stride + a.n + i];
+                ai = from_fix(si);
+            }
+        }
+        float v = a.v[i];
+        int r = a.ref[i];
+        if (a.model == 1) {
+            const float ie = __fadd_rn(__fmul_rn(a.ie[i], a.d_e), ae);
+            const float ii = __fadd_rn(__fmul_rn(a.ii[i], a.d_i), ai);
+            a.ie[i] = ie;
+            a.ii[i] = ii;
+            if (r > 0) {
+                r -= 1;
+                v = a.v_reset;
+            } else {
+                float x = __fsub_rn(a.v_inf, v);
+                x = __fadd_rn(x, ie);
+                x = __fadd_rn(x, ii);
+                v = __fadd_rn(v, __fmul_rn(x, a.k_m));
+                if (v >= a.v_th) {
+                    s = 1;
+                    v = a.v_reset;
+                    r = a.ref_steps;
+                }
+            }
+        } else {
+            if (r > 0) {
+                r -= 1;
+                v = a.v_reset;
+            } else {
+                float x = 0.f;
+                if (a.poisson_len > 0) {
+                    const uint32_t u = rng32(a.seed, 3, (uint64_t)a.t, (uint64_t)i);
+                    int k = 0;
+                    for (int q = 0; q < a.poisson_len; ++q) k += (a.poisson[q] <= u);
+                    x = __fmul_rn(a.j_ext, (float)k);
+                }
+                const float d = __fsub_rn(a.v_inf, v);
+                const float b = __fmul_rn(d, a.k_m);
+                const float c = __fadd_rn(v, b);
+                v = __fadd_rn(c, ae);
+                v = __fadd_rn(v, x);
+                if (v >= a.v_th) {
+                    s = 1;
+                    v = a.v_reset;
+                    r = a.ref_steps;
+                }
+            }
+        }
+        a.v[i] = v;
+        a.ref[i] = r;
+    }
+    uint64_t *hp = a.hist + (int64_t)i * a.hw;
+    uint64_t h = hp[0];
+    uint64_t h1 = a.hw == 2 ? hp[1] : 0ull;
+    if (a.n_plastic_rows > 0) {
+        // post trace seen by a pre spike at step t: posts strictly before t
+        const float y = __fmul_rn(__fadd_rn(a.ypost[i], (float)(h & 1ull)), a.d_minus);
+        a.ypost[i] = y;
+    }
+    h1 = a.hw == 2 ? (h1 << 1) | (h >> 63) : 0ull;
+    h = (h << 1) | (uint64_t)s;
+    hp[0] = h;
+    if (a.hw == 2) hp[1] = h1;
+    // history code for the row-wise STDP of this step: the position + 1 of
+    // the only spike of the last 64 hw steps (bit b = step t-b), 0 for none
+    const int np = __popcll(h) + __popcll(h1);
+    const int pos = h ? __ffsll((long long)h) : 64 + __ffsll((long long)h1);
+    a.code[i] = np == 0 ? (uint8_t)0 : np == 1 ? (uint8_t)pos : kCodeMulti;
+    fired_recently = np != 0;
+    tx = (int)((h >> a.dm1) & 1ull);
+    if (i < a.n_plastic_rows) forced = !tx && (a.t - (int64_t)a.t_last[i] >= 64 * a.hw);
+}
+
+static_assert((1 << 24) / (kNeuronBlock * kNeuronRounds) <= 65536,
+              "workgroup ticket must fit in 16 bits");
 
 __global__ __launch_bounds__(kNeuronBlock) void k_neuron(NeuronArgs a, CompactArgs lst)
 {
     constexpr int NWV = kNeuronBlock / kWave;
-    __shared__ float s_dpow[kMaxAge + 1];
-    __shared__ int s_cnt[2][NWV];
+    constexpr int R = kNeuronRounds;
+    __shared__ int s_cnt[2][R * NWV];
     __shared__ unsigned long long s_st[4];
     __shared__ unsigned long long s_base;
     const int tid = threadIdx.x;
-    const bool plastic = lst.n_plastic_rows > 0;
-    if (plastic)
-        for (int q = tid; q <= kMaxAge; q += kNeuronBlock) s_dpow[q] = lst.dpow[q];
-    if (tid < 4) s_st[tid] = 0ull;
-    const int i = blockIdx.x * kNeuronBlock + tid;
-    int s = 0, tx = 0, forced = 0;
-    bool fired_recently = false;
-    if (i < a.n) {
-        if (a.model == 2) {
-            s = rng32(a.seed, 4, (uint64_t)a.t, (uint64_t)i) < a.fire_thr;
-        } else {
-            float ae, ai = 0.f;
-            if (a.input_forced) {
-                ae = a.ain[i];
-                if (a.model == 1) ai = a.ain[a.n + i];
-            } else {
-                long long se = a.apart[i];
-                for (int c = 1; c < a.n_parts; ++c) se += a.apart[c * a.part_stride + i];
-                ae = from_fix(se);
-                if (a.model == 1) {
-                    long long si = a.apart[a.n + i];
-                    for (int c = 1; c < a.n_parts; ++c) si += a.apart[c * a.part_stride + a.n + i];
-                    ai = from_fix(si);
-                }
-            }
-            float v = a.v[i];
-            int r = a.ref[i];
-            if (a.model == 1) {
-                const float ie = __fadd_rn(__fmul_rn(a.ie[i], a.d_e), ae);
-                const float ii = __fadd_rn(__fmul_rn(a.ii[i], a.d_i), ai);
-                a.ie[i] = ie;
-                a.ii[i] = ii;
-                if (r > 0) {
-                    r -= 1;
-                    v = a.v_reset;
-                } else {
-                    float x = __fsub_rn(a.v_inf, v);
-                    x = __fadd_rn(x, ie);
-                    x = __fadd_rn(x, ii);
-                    v = __fadd_rn(v, __fmul_rn(x, a.k_m));
-                    if (v >= a.v_th) {
-                        s = 1;
-                        v = a.v_reset;
-                        r = a.ref_steps;
-                    }
-                }
-            } else {
-                if (r > 0) {
-                    r -= 1;
-                    v = a.v_reset;
-                } else {
-                    float x = 0.f;
-                    if (a.poisson_len > 0) {
-                        const uint32_t u = rng32(a.seed, 3, (uint64_t)a.t, (uint64_t)i);
-                        int k = 0;
-                        for (int q = 0; q < a.poisson_len; ++q) k += (a.poisson[q] <= u);
-                        x = __fmul_rn(a.j_ext, (float)k);
-                    }
-                    const float d = __fsub_rn(a.v_inf, v);
-                    const float b = __fmul_rn(d, a.k_m);
-                    const float c = __fadd_rn(v, b);
-                    v = __fadd_rn(c, ae);
-                    v = __fadd_rn(v, x);
-                    if (v >= a.v_th) {
-                        s = 1;
-                        v = a.v_reset;
-                        r = a.ref_steps;
-                    }
-                }
-            }
-            a.v[i] = v;
-            a.ref[i] = r;
-        }
-        uint64_t *hp = a.hist + (int64_t)i * a.hw;
-        uint64_t h = hp[0];
-        uint64_t h1 = a.hw == 2 ? hp[1] : 0ull;
-        if (a.n_plastic_rows > 0) {
-            // post trace seen by a pre spike at step t: posts strictly before t
-            const float y = __fmul_rn(__fadd_rn(a.ypost[i], (float)(h & 1ull)), a.d_minus);
-            a.ypost[i] = y;
-        }
-        h1 = a.hw == 2 ? (h1 << 1) | (h >> 63) : 0ull;
-        h = (h << 1) | (uint64_t)s;
-        hp[0] = h;
-        if (a.hw == 2) hp[1] = h1;
-        // history code for the row-wise STDP of this step: the position + 1 of
-        // the only spike of the last 64 hw steps (bit b = step t-b), 0 for none
-        const int np = __popcll(h) + __popcll(h1);
-        const int pos = h ? __ffsll((long long)h) : 64 + __ffsll((long long)h1);
-        a.code[i] = np == 0 ? (uint8_t)0 : np == 1 ? (uint8_t)pos : kCodeMulti;
-        fired_recently = np != 0;
-        tx = (int)((h >> a.dm1) & 1ull);
-        if (i < a.n_plastic_rows) forced = !tx && (a.t - (int64_t)a.t_last[i] >= 64 * a.hw);
-    }
-    const uint64_t m = ballot64(s), txm = ballot64(tx), fm = ballot64(forced);
-    const uint64_t rcm = ballot64(fired_recently);
     const int wave = tid / kWave, lane = tid % kWave;
-    const int64_t word = (int64_t)blockIdx.x * NWV + wave;
-    if (lane == 0) {
-        if (word * kWave < a.n) {
-            a.mask[word] = m;
-            a.txmask[word] = txm;
-            a.recent[word] = rcm;
+    const bool plastic = lst.n_plastic_rows > 0;
+    if (tid < 4) s_st[tid] = 0ull;
+    // The values a row snapshot needs are loaded with the neuron's own state
+    // for every plastic neuron (first edge for every neuron when there is
+    // plasticity), so that the few snapshots taken below cost no second
+    // dependent round trip.
+    int64_t v_rs[R];
+    int v_pend[R], v_tl[R];
+    float v_xp[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int i = (blockIdx.x * R + r) * kNeuronBlock + tid;
+        v_rs[r] = 0;
+        v_pend[r] = v_tl[r] = 0;
+        v_xp[r] = 0.f;
+        if (plastic && i < a.n) {
+            v_rs[r] = lst.row_ptr[i];
+            if (i < lst.n_plastic_rows) {
+                v_pend[r] = lst.pend[i];
+                v_tl[r] = lst.t_last[i];
+                v_xp[r] = lst.xpre[i];
+            }
         }
-        s_cnt[0][wave] = __popcll(m);
-        s_cnt[1][wave] = __popcll(fm);
     }
-    // position of a transmitting row in the spike list of step t-D+1
-    int txpos = -1;
-    if (tx && plastic && lst.dm1 > 0) txpos = lst.tx_pos[i];
-    __syncthreads();  // publishes s_cnt, s_dpow, s_st
-    // snapshots of this thread's row (taken before any kernel commits
-    // t_last / x_pre); their loads overlap the reservation below
-    RowInfo ri{};
-    int ri_ok = 0;
-    if (tx && plastic) {
-        if (i < lst.n_plastic_rows)
-            ri_ok = make_row_info(ri, i, lst.t, true, lst.dm1, lst.hw, lst.row_ptr, lst.pend,
-                                  lst.hist, lst.t_last, lst.xpre, s_dpow, lst.err);
-        if (!ri_ok) {  // nothing to bring up to date: the row is only delivered
-            ri = RowInfo{};
-            ri.k = i;
-            ri.rs = lst.row_ptr[i];
+    // round r covers neurons [(b R + r) B, (b R + r + 1) B) of workgroup b
+    int s[R], tx[R], forced[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int i = (blockIdx.x * R + r) * kNeuronBlock + tid;
+        s[r] = tx[r] = forced[r] = 0;
+        bool fired_recently = false;
+        if (i < a.n) neuron_update(a, i, s[r], tx[r], forced[r], fired_recently);
+        const uint64_t m = ballot64(s[r]), txm = ballot64(tx[r]), fm = ballot64(forced[r]);
+        const uint64_t rcm = ballot64(fired_recently);
+        if (lane == 0) {
+            const int64_t word = (int64_t)(blockIdx.x * R + r) * NWV + wave;
+            if (word * kWave < a.n) {
+                a.mask[word] = m;
+                a.txmask[word] = txm;
+                a.recent[word] = rcm;
+            }
+            s_cnt[0][r * NWV + wave] = __popcll(m);
+            s_cnt[1][r * NWV + wave] = __popcll(fm);
         }
-    } else if (forced) {
-        ri_ok = make_row_info(ri, i, lst.t, true, lst.dm1, lst.hw, lst.row_ptr, lst.pend,
-                              lst.hist, lst.t_last, lst.xpre, s_dpow, lst.err);
     }
+    // snapshots of the rows to bring up to date (taken before any kernel
+    // commits t_last / x_pre), and the position of a transmitting row in the
+    // spike list of step t-D+1; their loads overlap the barrier and the
+    // reservation below
+    RowInfo ri[R];
+    int ri_ok[R], txpos[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int i = (blockIdx.x * R + r) * kNeuronBlock + tid;
+        ri[r] = RowInfo{};
+        ri_ok[r] = 0;
+        txpos[r] = -1;
+        // the row transmits at t exactly when tx (history bit D-1 of step t)
+        if (tx[r] && plastic) {
+            if (lst.dm1 > 0) txpos[r] = lst.tx_pos[i];
+            if (i < lst.n_plastic_rows)
+                ri_ok[r] = make_row_info_v(ri[r], i, lst.t, v_tl[r], v_rs[r], v_pend[r],
+                                           v_xp[r], 1, lst.hw, lst.dpow, lst.err);
+            if (!ri_ok[r]) {  // nothing to bring up to date: the row is only delivered
+                ri[r] = RowInfo{};
+                ri[r].k = i;
+                ri[r].rs = v_rs[r];
+            }
+        } else if (forced[r]) {
+            ri_ok[r] = make_row_info_v(ri[r], i, lst.t, v_tl[r], v_rs[r], v_pend[r], v_xp[r], 0,
+                                       lst.hw, lst.dpow, lst.err);
+        }
+    }
+    __syncthreads();  // publishes s_cnt, s_st
     if (tid == 0) {
         int spk = 0, fr = 0;
 #pragma unroll
-        for (int q = 0; q < NWV; ++q) {
+        for (int q = 0; q < R * NWV; ++q) {
             spk += s_cnt[0][q];
             fr += s_cnt[1][q];
         }
@@ -216,9 +257,19 @@ __global__ __launch_bounds__(kNeuronBlock) void k_neuron(NeuronArgs a, CompactAr
         }
     }
     if (lst.info_stats) {
-        const bool f = forced && ri_ok;
-        const long long v0 = wave_sum_i64(ri_ok ? 1 : 0), v1 = wave_sum_i64(f ? 1 : 0);
-        const long long v2 = wave_sum_i64(ri_ok ? ri.len : 0), v3 = wave_sum_i64(f ? ri.len : 0);
+        long long v0 = 0, v1 = 0, v2 = 0, v3 = 0;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const bool f = forced[r] && ri_ok[r];
+            v0 += ri_ok[r] ? 1 : 0;
+            v1 += f ? 1 : 0;
+            v2 += ri_ok[r] ? ri[r].len : 0;
+            v3 += f ? ri[r].len : 0;
+        }
+        v0 = wave_sum_i64(v0);
+        v1 = wave_sum_i64(v1);
+        v2 = wave_sum_i64(v2);
+        v3 = wave_sum_i64(v3);
         if (lane == 0) {
             if (v0) atomicAdd(s_st + 0, (unsigned long long)v0);
             if (v1) atomicAdd(s_st + 1, (unsigned long long)v1);
@@ -228,40 +279,45 @@ __global__ __launch_bounds__(kNeuronBlock) void k_neuron(NeuronArgs a, CompactAr
     }
     __syncthreads();  // publishes s_base, s_st
     const unsigned long long base = s_base;
+    const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
     int o0 = (int)(base & 0xffffffull), o2 = (int)((base >> 24) & 0xffffffull);
 #pragma unroll
-    for (int q = 0; q < NWV; ++q) {
-        if (q < wave) {
-            o0 += s_cnt[0][q];
-            o2 += s_cnt[1][q];
+    for (int r = 0; r < R; ++r) {
+        const int i = (blockIdx.x * R + r) * kNeuronBlock + tid;
+        // this wave's offsets in round r: every wave of the earlier rounds,
+        // then the earlier waves of this one
+        int p0 = o0, p2 = o2;
+        for (int q = 0; q < r * NWV + wave; ++q) {
+            p0 += s_cnt[0][q];
+            p2 += s_cnt[1][q];
         }
-    }
-    const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
-    // (the bounds checks only catch an accumulator left non-zero by a failed
-    // step; with a cleared one every offset is in range)
-    if (s) {
-        const int pos = o0 + __popcll(m & below);
-        if (pos < a.n) {
-            lst.spk_list[pos] = i;
-            if (plastic && lst.dm1 > 0) lst.spk_pos[i] = pos;
-            if (lst.dm1 == 0) txpos = pos;  // D = 1: transmitted as it fires
-        } else {
-            atomicOr(lst.err, kErrRing);
+        const uint64_t m = ballot64(s[r]), fm = ballot64(forced[r]);
+        // (the bounds checks only catch an accumulator left non-zero by a
+        // failed step; with a cleared one every offset is in range)
+        if (s[r]) {
+            const int pos = p0 + __popcll(m & below);
+            if (pos < a.n) {
+                lst.spk_list[pos] = i;
+                if (plastic && lst.dm1 > 0) lst.spk_pos[i] = pos;
+                if (lst.dm1 == 0) txpos[r] = pos;  // D = 1: transmitted as it fires
+            } else {
+                atomicOr(lst.err, kErrRing);
+            }
         }
-    }
-    if (tx && plastic) {
-        if (txpos >= 0 && txpos < a.n)
-            lst.txinfo[txpos] = ri;
-        else
-            atomicOr(lst.err, kErrRing);
-    }
-    if (forced) {
-        const int r = o2 + __popcll(fm & below);
-        if (r < lst.n_plastic_rows) {
-            lst.row_list[r] = i;
-            lst.info[r] = ri;
-        } else {
-            atomicOr(lst.err, kErrRing);
+        if (tx[r] && plastic) {
+            if (txpos[r] >= 0 && txpos[r] < a.n)
+                lst.txinfo[txpos[r]] = ri[r];
+            else
+                atomicOr(lst.err, kErrRing);
+        }
+        if (forced[r]) {
+            const int q = p2 + __popcll(fm & below);
+            if (q < lst.n_plastic_rows) {
+                lst.row_list[q] = i;
+                lst.info[q] = ri[r];
+            } else {
+                atomicOr(lst.err, kErrRing);
+            }
         }
     }
     if (lst.info_stats && tid == 0) {
@@ -388,8 +444,8 @@ hipError_t launch_copy_bytes(hipStream_t s, void *dst, const void *src, int64_t 
 hipError_t launch_neuron(hipStream_t s, const NeuronArgs &a, const CompactArgs &c,
                          KernelEvents ev)
 {
-    hipExtLaunchKernelGGL(k_neuron, dim3(blocks_for(a.n, kNeuronBlock)), dim3(kNeuronBlock), 0, s,
-                          ev.start, ev.stop, 0, a, c);
+    hipExtLaunchKernelGGL(k_neuron, dim3(blocks_for(a.n, kNeuronBlock * kNeuronRounds)),
+                          dim3(kNeuronBlock), 0, s, ev.start, ev.stop, 0, a, c);
     return hipGetLastError();
 }
 

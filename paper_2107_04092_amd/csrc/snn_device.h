@@ -168,17 +168,17 @@ __device__ __forceinline__ void fill_segment_map(int *mark, int len, int *sh)
 
 // Snapshot of plastic row k for an update at step t (see RowInfo). Returns
 // 1 if the row has something to bring up to date.
-__device__ __forceinline__ int make_row_info(RowInfo &ri, int k, int64_t t, bool pre_allowed,
-                                             int dm1, int hw, const int64_t *row_ptr,
-                                             const int32_t *pend, const uint64_t *hist,
-                                             const int32_t *t_last, const float *xpre,
-                                             const float *dpow, int32_t *err)
+// The same from the row's values: t_last, first edge rs, plastic prefix
+// length, pre trace at t_last, and whether the row transmits at t.
+__device__ __forceinline__ int make_row_info_v(RowInfo &ri, int k, int64_t t, int t_last_k,
+                                               int64_t rs, int pend_k, float xpre_k, int pre,
+                                               int hw, const float *dpow, int32_t *err)
 {
-    int age = (int)(t - (int64_t)t_last[k]);
+    int age = (int)(t - (int64_t)t_last_k);
     ri.k = k;
-    ri.rs = row_ptr[k];
+    ri.rs = rs;
     ri.pad = 0;
-    ri.xp0 = xpre[k];
+    ri.xp0 = xpre_k;
     if (age <= 0) {  // flush: already current
         ri.len = 0;
         ri.age_pre = 0;
@@ -191,11 +191,21 @@ __device__ __forceinline__ int make_row_info(RowInfo &ri, int k, int64_t t, bool
         atomicOr(err, kErrWindow);
         age = 64 * hw;
     }
-    const int pre = pre_allowed ? (int)((hist[(int64_t)k * hw] >> dm1) & 1ull) : 0;
-    ri.len = pend[k];
+    ri.len = pend_k;
     ri.age_pre = age | (pre << 8);
     ri.xp_now = __fadd_rn(__fmul_rn(ri.xp0, dpow[age]), (float)pre);
     return 1;
+}
+
+__device__ __forceinline__ int make_row_info(RowInfo &ri, int k, int64_t t, bool pre_allowed,
+                                             int dm1, int hw, const int64_t *row_ptr,
+                                             const int32_t *pend, const uint64_t *hist,
+                                             const int32_t *t_last, const float *xpre,
+                                             const float *dpow, int32_t *err)
+{
+    const int pre = pre_allowed ? (int)((hist[(int64_t)k * hw] >> dm1) & 1ull) : 0;
+    return make_row_info_v(ri, k, t, t_last[k], row_ptr[k], pend[k], xpre[k], pre, hw, dpow,
+                           err);
 }
 
 // Masks of the window of a row of age `age` (bits age-1 .. 0 of the
