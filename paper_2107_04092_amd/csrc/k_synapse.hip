@@ -582,6 +582,7 @@ __global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
     __shared__ float s_dpow[kMaxAge + 1];
     __shared__ long long sh[kDlvBlock / kWave];
     __shared__ int shi[kDlvBlock / kWave];
+    __shared__ unsigned long long s_written;
     const int tid = threadIdx.x;
     const int nb = gridDim.x;  // multiple of 8
     const int q = (blockIdx.x & 7) * (nb >> 3) + (blockIdx.x >> 3);
@@ -590,7 +591,18 @@ __global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
     const int C = a.chunks;
     const int base = s * a.width;
     const int span = a.nacc * a.width;
+    // the first batch's snapshots (or list entries) go out before the staging
+    // loads, so the two round trips overlap
+    RowInfo ri0 = RowInfo{};
+    int k0 = 0;
+    if (c + C * tid < a.n) {
+        if (a.plastic)
+            ri0 = a.txinfo[c + C * tid];
+        else
+            k0 = a.list[c + C * tid];
+    }
     const int cnt = *a.cnt;  // used only once the first batch's loads are out
+    if (tid == 0) s_written = 0ull;  // published by the batch loop's barriers
     for (int x = tid; x < span; x += kDlvBlock) acc[x] = 0;
     const int hw = a.hw;
     uint64_t *s_hist = (uint64_t *)(acc + span);
@@ -615,7 +627,7 @@ __global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
             int64_t rs;
             float xp0 = 0.f, xpn = 0.f;
             if (a.plastic) {
-                const RowInfo ri = a.txinfo[r];
+                const RowInfo ri = b0 == 0 ? ri0 : a.txinfo[r];
                 k = ri.k;
                 rs = ri.rs;
                 ap = ri.age_pre;
@@ -623,7 +635,7 @@ __global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
                 xp0 = ri.xp0;
                 xpn = ri.xp_now;
             } else {
-                k = a.list[r];
+                k = b0 == 0 ? k0 : a.list[r];
                 rs = 0;
             }
             k = min(max(k, 0), a.n - 1);  // entries past the count are stale
@@ -715,11 +727,13 @@ __global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
         if (c + C * (b0 + kDlvBatch) >= cnt) break;
         __syncthreads();  // staging arrays are rewritten by the next batch
     }
-    ev = block_sum_i64_n<kDlvBlock>(ev, sh);  // ends with the accumulation barrier
-    written = block_sum_i64_n<kDlvBlock>(written, sh);
+    // (ev is thread 0's alone)
+    written = wave_sum_i64(written);
+    if (tid % kWave == 0 && written) atomicAdd(&s_written, (unsigned long long)written);
+    __syncthreads();  // the accumulation barrier: every LDS atomic is done
     if (tid == 0) {
         a.stats[2 * (int64_t)blockIdx.x] += ev;
-        a.stats[2 * (int64_t)blockIdx.x + 1] += written;
+        a.stats[2 * (int64_t)blockIdx.x + 1] += (int64_t)s_written;
     }
     if (a.chunks == 1) {
         for (int x = tid; x < a.width; x += kDlvBlock) {
