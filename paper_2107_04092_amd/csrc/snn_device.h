@@ -36,8 +36,9 @@ __device__ __forceinline__ uint64_t ballot64(bool p) { return __builtin_amdgcn_b
 __device__ __forceinline__ float pow_mu(float w, float mu)
 {
     if (mu == 0.f) return 1.f;
-    if (!(w > 0.f)) return 0.f;
-    return __builtin_amdgcn_exp2f(mu * __builtin_amdgcn_logf(w));
+    // computed unconditionally and selected: no divergent branch per call
+    const float p = __builtin_amdgcn_exp2f(mu * __builtin_amdgcn_logf(w));
+    return w > 0.f ? p : 0.f;
 }
 
 // fp32 -> fixed point (x * 2^32 is exact in fp32; only |x| < 2^-9 loses bits)
@@ -166,10 +167,10 @@ __device__ __forceinline__ void fill_segment_map(int *mark, int len, int *sh)
 }
 
 
-// Snapshot of plastic row k for an update at step t (see RowInfo). Returns
-// 1 if the row has something to bring up to date.
-// The same from the row's values: t_last, first edge rs, plastic prefix
-// length, pre trace at t_last, and whether the row transmits at t.
+// Snapshot of plastic row k for an update at step t (see RowInfo) from the
+// row's values: t_last, first edge rs, plastic prefix length, pre trace at
+// t_last, and whether the row transmits at t. Returns 1 if the row has
+// something to bring up to date.
 __device__ __forceinline__ int make_row_info_v(RowInfo &ri, int k, int64_t t, int t_last_k,
                                                int64_t rs, int pend_k, float xpre_k, int pre,
                                                int hw, const float *dpow, int32_t *err)
@@ -197,6 +198,7 @@ __device__ __forceinline__ int make_row_info_v(RowInfo &ri, int k, int64_t t, in
     return 1;
 }
 
+// The same reading the values from the state arrays.
 __device__ __forceinline__ int make_row_info(RowInfo &ri, int k, int64_t t, bool pre_allowed,
                                              int dm1, int hw, const int64_t *row_ptr,
                                              const int32_t *pend, const uint64_t *hist,
