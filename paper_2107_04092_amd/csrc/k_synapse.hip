@@ -602,18 +602,35 @@ __global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
             k0 = a.list[c + C * tid];
     }
     const int cnt = *a.cnt;  // used only once the first batch's loads are out
+    const int hw = a.hw;
+    const int jn = min(a.width, a.n - base);  // > 0
+    // the slice's histories and post traces: loads out now, stored below
+    StageRegs<4, uint64_t> g_hist;
+    StageRegs<4, float> g_y;
+    if (a.plastic) {
+        stage_issue<kDlvBlock>(g_hist, a.hist + (int64_t)base * hw, jn * hw);
+        stage_issue<kDlvBlock>(g_y, a.ypost + base, jn);
+    }
+    const int piv_stride = a.n_slices + 1;
+    // the first batch's pivots, as soon as its snapshots are in
+    int k0p = 0, p0p = 0, p1p = 0;
+    int64_t rsp = 0;
+    if (c + C * tid < a.n) {
+        k0p = min(max(a.plastic ? ri0.k : k0, 0), a.n - 1);  // entries past the count are stale
+        const int32_t *pv = a.piv + (int64_t)k0p * piv_stride + s;
+        p0p = pv[0];
+        p1p = pv[1];
+        rsp = a.plastic ? ri0.rs : a.row_ptr[k0p];
+    }
     if (tid == 0) s_written = 0ull;  // published by the batch loop's barriers
     for (int x = tid; x < span; x += kDlvBlock) acc[x] = 0;
-    const int hw = a.hw;
     uint64_t *s_hist = (uint64_t *)(acc + span);
     float *s_y = (float *)(s_hist + (size_t)a.width * hw);
     if (a.plastic) {
-        const int jn = min(a.width, a.n - base);  // > 0
-        stage_lds<kDlvBlock, 4>(s_hist, a.hist + (int64_t)base * hw, jn * hw);
-        stage_lds<kDlvBlock, 4>(s_y, a.ypost + base, jn);
+        stage_finish<kDlvBlock>(s_hist, g_hist, a.hist + (int64_t)base * hw, jn * hw);
+        stage_finish<kDlvBlock>(s_y, g_y, a.ypost + base, jn);
         for (int x = tid; x <= kMaxAge; x += kDlvBlock) s_dpow[x] = a.dpow[x];
     }
-    const int piv_stride = a.n_slices + 1;
     const int32_t *__restrict__ col = a.col;
     float *__restrict__ wgt = a.w;
     const float c_pot = a.c_pot, c_dep = a.c_dep, mu = a.mu;
@@ -623,25 +640,24 @@ __global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
         const int r = c + C * (b0 + tid);
         int len = 0;
         if (r < a.n) {
-            int k, plen_row = 0, ap = 0;
+            int k, p0, p1;
             int64_t rs;
-            float xp0 = 0.f, xpn = 0.f;
-            if (a.plastic) {
-                const RowInfo ri = b0 == 0 ? ri0 : a.txinfo[r];
-                k = ri.k;
-                rs = ri.rs;
-                ap = ri.age_pre;
-                plen_row = ri.len;
-                xp0 = ri.xp0;
-                xpn = ri.xp_now;
+            RowInfo ri = RowInfo{};
+            if (a.plastic) ri = b0 == 0 ? ri0 : a.txinfo[r];
+            const int plen_row = ri.len, ap = ri.age_pre;
+            const float xp0 = ri.xp0, xpn = ri.xp_now;
+            if (b0 == 0) {  // prefetched above
+                k = k0p;
+                rs = rsp;
+                p0 = p0p;
+                p1 = p1p;
             } else {
-                k = b0 == 0 ? k0 : a.list[r];
-                rs = 0;
+                k = min(max(a.plastic ? ri.k : a.list[r], 0), a.n - 1);  // past the count: stale
+                const int32_t *pv = a.piv + (int64_t)k * piv_stride + s;
+                p0 = pv[0];
+                p1 = pv[1];
+                rs = a.plastic ? ri.rs : a.row_ptr[k];
             }
-            k = min(max(k, 0), a.n - 1);  // entries past the count are stale
-            const int32_t *pv = a.piv + (int64_t)k * piv_stride + s;
-            const int p0 = pv[0], p1 = pv[1];
-            if (!a.plastic) rs = a.row_ptr[k];
             if (r < cnt) {
                 len = p1 - p0;
                 s_start[tid] = rs + p0;

@@ -64,9 +64,10 @@ __device__ __forceinline__ long long wave_sum_i64(long long v)
 // workgroup, R loads in flight per thread before their stores (a plain
 // strided loop would wait for each load before the next).
 template <int NT, int R, typename T>
-__device__ __forceinline__ void stage_lds(T *dst, const T *__restrict__ src, int count)
+__device__ __forceinline__ void stage_lds(T *dst, const T *__restrict__ src, int count,
+                                          int from = 0)
 {
-    for (int x0 = 0; x0 < count; x0 += NT * R) {
+    for (int x0 = from; x0 < count; x0 += NT * R) {
         T v[R];
 #pragma unroll
         for (int r = 0; r < R; ++r) v[r] = src[min(x0 + r * NT + (int)threadIdx.x, count - 1)];
@@ -76,6 +77,34 @@ __device__ __forceinline__ void stage_lds(T *dst, const T *__restrict__ src, int
             if (x < count) dst[x] = v[r];
         }
     }
+}
+
+// The same in two halves, so that other loads can go out in between: the
+// first R NT elements are loaded into registers by stage_issue, stored by
+// stage_finish, which then copies the rest.
+template <int R, typename T>
+struct StageRegs {
+    T v[R];
+};
+
+template <int NT, int R, typename T>
+__device__ __forceinline__ void stage_issue(StageRegs<R, T> &g, const T *__restrict__ src,
+                                            int count)
+{
+#pragma unroll
+    for (int r = 0; r < R; ++r) g.v[r] = src[min(r * NT + (int)threadIdx.x, count - 1)];
+}
+
+template <int NT, int R, typename T>
+__device__ __forceinline__ void stage_finish(T *dst, const StageRegs<R, T> &g,
+                                             const T *__restrict__ src, int count)
+{
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int x = r * NT + (int)threadIdx.x;
+        if (x < count) dst[x] = g.v[r];
+    }
+    stage_lds<NT, R>(dst, src, count, NT * R);
 }
 
 // Number of lanes below this one whose bit is set in a wave-uniform mask.
