@@ -539,8 +539,11 @@ __global__ __launch_bounds__(kNaiveBlock) void k_stdp_naive(NaiveArgs a)
 // c, c + C, c + 2C, ... The slice accumulator lives in LDS as exact 64-bit
 // fixed point. For a batch of spikes the workgroup first gathers each
 // spike's in-slice segment (row start + piv[k][s], length piv[k][s+1] -
-// piv[k][s]) into LDS and prefix-sums the lengths; then every thread takes
-// flattened elements of the concatenated segments, so lanes stay busy
+// piv[k][s]) into LDS and prefix-sums the lengths; a map from each entry of
+// the concatenated segments to its segment is then filled (by the segments'
+// own threads when all are short, else by marking starts and a max-scan);
+// then every thread takes flattened elements of the concatenated segments,
+// so lanes stay busy
 // whatever the segment lengths and consecutive lanes read consecutive
 // entries of a segment (coalesced loads). Each element adds its weight into
 // acc[target - sW] with an LDS 64-bit integer atomic. With C = 1 the
@@ -566,6 +569,7 @@ constexpr int kDlvBlock = 512;
 constexpr int kDlvBatch = 512;   // spikes whose segments are staged at once
 constexpr int kDlvUnroll = 8;    // flattened elements per thread per window
 constexpr int kDlvWindow = kDlvBlock * kDlvUnroll;
+constexpr int kDlvDirectMax = 32;  // segments up to this long are mapped by their own thread
 static_assert(kDlvBatch == kDlvBlock, "one staged spike per thread");
 
 __global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
@@ -583,6 +587,7 @@ __global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
     __shared__ long long sh[kDlvBlock / kWave];
     __shared__ int shi[kDlvBlock / kWave];
     __shared__ unsigned long long s_written;
+    __shared__ int s_nlong;
     const int tid = threadIdx.x;
     const int nb = gridDim.x;  // multiple of 8
     const int q = (blockIdx.x & 7) * (nb >> 3) + (blockIdx.x >> 3);
@@ -673,22 +678,39 @@ __global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
             }
         }
         const int nbt = min(kDlvBatch, max(0, (cnt - c + C - 1) / C - b0));
-        const long long incl = block_incl_scan_i64_n<kDlvBlock>(len, sh);
+        // one scan gives the offsets and (bits 40+) the number of long segments
+        const long long packed = (long long)len | ((long long)(len > kDlvDirectMax) << 40);
+        const long long incl_p = block_incl_scan_i64_n<kDlvBlock>(packed, sh);
+        const long long incl = incl_p & ((1ll << 40) - 1);
         if (tid < nbt) s_off[tid] = (int)(incl - len);
-        if (tid == kDlvBlock - 1) s_off[nbt] = (int)incl;  // = total (threads >= nbt add 0)
+        if (tid == kDlvBlock - 1) {  // totals (threads >= nbt add 0)
+            s_off[nbt] = (int)incl;
+            s_nlong = (int)(incl_p >> 40);
+        }
         __syncthreads();
         const int total = s_off[nbt];
+        const bool direct = s_nlong == 0;
         ev += tid == 0 ? total : 0;
         for (int e0 = 0; e0 < total; e0 += kDlvWindow) {
             const int we = min(kDlvWindow, total - e0);
-            for (int x = tid; x < we; x += kDlvBlock) s_map[x] = -1;
-            __syncthreads();
-            if (tid < nbt) {
-                const int a0 = max(s_off[tid], e0), a1 = min(s_off[tid + 1], e0 + we);
-                if (a0 < a1) s_map[a0 - e0] = tid;
+            if (direct) {
+                // short segments: each thread writes its own segment's entries
+                if (tid < nbt) {
+                    const int a0 = max(s_off[tid], e0), a1 = min(s_off[tid + 1], e0 + we);
+                    for (int x = a0; x < a1; ++x) s_map[x - e0] = tid;
+                }
+                __syncthreads();
+            } else {
+                // mark each segment's first entry in the window, then max-scan
+                for (int x = tid; x < we; x += kDlvBlock) s_map[x] = -1;
+                __syncthreads();
+                if (tid < nbt) {
+                    const int a0 = max(s_off[tid], e0), a1 = min(s_off[tid + 1], e0 + we);
+                    if (a0 < a1) s_map[a0 - e0] = tid;
+                }
+                __syncthreads();
+                fill_segment_map<kDlvBlock, kDlvUnroll>(s_map, we, shi);
             }
-            __syncthreads();
-            fill_segment_map<kDlvBlock, kDlvUnroll>(s_map, we, shi);
             int tgt[kDlvUnroll], slot[kDlvUnroll], off[kDlvUnroll];
             long long gi[kDlvUnroll];
             float wv[kDlvUnroll];
