@@ -45,6 +45,8 @@ def parse():
     ap.add_argument("--stdp-filter", choices=["auto", "codes", "bitmap", "none"],
                     default="auto")
     ap.add_argument("--history-bits", type=int, choices=[64, 128], default=64)
+    ap.add_argument("--targets", choices=["preset", "32", "16"], default="preset",
+                    help="synapse targets: 32-bit, or 16-bit slice-local (compressed)")
     ap.add_argument("--plasticity", choices=["lazy-event", "lazy", "naive"],
                     default="lazy-event",
                     help="plasticity algorithm (Fig. 2(c), (b), (a))")
@@ -86,19 +88,21 @@ def load_traffic(kernel, workload_key):
         return None
 
 
-def stdp_bytes(st, n, launches):
+def stdp_bytes(st, n, launches, target_bytes=4):
     """Algorithmic bytes of the forced-row STDP kernel (snn_update_plasticity):
-    per synapse update 8 B (target + weight read), per changed weight 4 B
-    (store), per row 40 B (list entry, row pointer, plastic end, source
-    history, t_last and pre trace read and written), per launch 8 B per neuron
-    (the target histories)."""
-    return (8 * st["stdp_forced_synapse_updates"] + 4 * st["stdp_forced_weights_written"] +
-            40 * st["stdp_forced_rows"] + 8 * n * launches)
+    per synapse update the target (4 B, or 2 B compressed) and the weight
+    (4 B) read, per changed weight 4 B (store), per row 40 B (list entry, row
+    pointer, plastic end, source history, t_last and pre trace read and
+    written), per launch 8 B per neuron (the target histories)."""
+    return ((target_bytes + 4) * st["stdp_forced_synapse_updates"] +
+            4 * st["stdp_forced_weights_written"] + 40 * st["stdp_forced_rows"] +
+            8 * n * launches)
 
 
-def delivery_bytes(st, n, n_slices, chunks, nacc, launches, mode):
-    """Algorithmic bytes of delivery with the transmitting rows' STDP: 8 B per
-    event (target + weight) and 4 B per weight STDP changed there. LDS mode
+def delivery_bytes(st, n, n_slices, chunks, nacc, launches, mode, target_bytes=4):
+    """Algorithmic bytes of delivery with the transmitting rows' STDP: per
+    event the target (4 B, or 2 B compressed in LDS mode) and the weight
+    (4 B), and 4 B per weight STDP changed there. LDS mode
     adds per (transmitted spike, slice) 20 B (row snapshot or list entry,
     pivot pair), per launch 12 B per neuron for the targets' histories and
     post traces (plastic networks) and the slice write-back: nacc * n * 4 B of
@@ -110,7 +114,8 @@ def delivery_bytes(st, n, n_slices, chunks, nacc, launches, mode):
     plastic = 12 * n if st["stdp_rows"] > 0 else 0
     if mode == "lds":
         wb = 4 * nacc * n if chunks == 1 else 8 * chunks * nacc * n
-        return 8 * ev + 4 * wtx + 20 * tx * n_slices + (wb + plastic) * launches
+        return ((target_bytes + 4) * ev + 4 * wtx + 20 * tx * n_slices +
+                (wb + plastic) * launches)
     return 16 * ev + 20 * tx + 8 * nacc * n * launches
 
 
@@ -172,7 +177,9 @@ def main():
                                      args.stdp_filter),
                                  history_bits=args.history_bits,
                                  plasticity_algorithm=["lazy-event", "lazy", "naive"].index(
-                                     args.plasticity))
+                                     args.plasticity),
+                                 compressed_targets=(None if args.targets == "preset" else
+                                                     int(args.targets == "16")))
     t0 = time.time()
     net = snn.Network(cfg, stream=stream, device=dev)
     e = net.build_random(p.graph_kind, p.p_or_fanout, p.w_exc, p.w_inh)
@@ -204,8 +211,10 @@ def main():
 
     n_slices = (p.n + width - 1) // width
     nacc = 2 if p.model == snn.SNN_LIF_CUBA else 1
-    b_stdp = stdp_bytes(st, p.n, args.steps) / args.steps
-    b_dlv = delivery_bytes(st, p.n, n_slices, chunks, nacc, args.steps, args.mode) / args.steps
+    tb = 2 if cfg.compressed_targets else 4
+    b_stdp = stdp_bytes(st, p.n, args.steps, tb) / args.steps
+    b_dlv = delivery_bytes(st, p.n, n_slices, chunks, nacc, args.steps, args.mode,
+                           tb) / args.steps
 
     kernels = None
     roofline = None
@@ -221,9 +230,9 @@ def main():
         kt, nrec = net.kernel_times()
         net.record_kernel_times(0)
         st2 = net.stats()
-        b_stdp = stdp_bytes(st2, p.n, args.steps) / args.steps
+        b_stdp = stdp_bytes(st2, p.n, args.steps, tb) / args.steps
         b_dlv = delivery_bytes(st2, p.n, n_slices, chunks, nacc, args.steps,
-                               args.mode) / args.steps
+                               args.mode, tb) / args.steps
         t_neu, t_stdp, t_dlv = kt["neuron"], kt["plasticity"], kt["delivery"]
         kernels = {
             "steps_timed": nrec,
@@ -286,6 +295,7 @@ def main():
             "n": p.n, "synapses": e, "slice_width": width, "spike_chunks": chunks,
             "delivery": args.mode, "stdp_layout": args.stdp_layout,
             "stdp_filter": args.stdp_filter, "history_bits": args.history_bits,
+            "target_bits": 16 if cfg.compressed_targets else 32,
             "plasticity": args.plasticity,
             "stdp_slice_mult": args.stdp_mult, "stdp_chunks": args.stdp_chunks, "seed": p.seed,
         },

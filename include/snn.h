@@ -116,8 +116,8 @@ typedef struct snn_config {
                              looked up as below; 1 = slice-organised, the
                              target group's histories staged in LDS */
     int32_t stdp_filter;  /* row-wise layout, per-neuron summary staged in LDS:
-                             0 = automatic (codes if n + 16 <= 147456, else
-                             the bitmap if n <= 2^20, else none), 1 = history
+                             0 = automatic (codes if n + 16 <= 97280, else
+                             the bitmap if n <= 778240, else none), 1 = history
                              codes (which single step of the window held a
                              spike; more than one: gather), 2 = spike-recency
                              bitmap (gather for targets that fired in the
@@ -135,6 +135,13 @@ typedef struct snn_config {
                              which the graph buffer then holds (8 B more per
                              synapse). All three reach the same weights up to
                              rounding; they differ in work */
+    int32_t compressed_targets; /* 1 = the graph also holds each target's 16-bit
+                             slice-local index, target mod W (Sec. V:
+                             compressed slice-local indices; W is bounded by
+                             the LDS accumulator, so it always fits), which
+                             slice delivery reads instead of the 32-bit target
+                             (half the target bytes). Row-wise kernels read
+                             the 32-bit targets. 0 = off */
     int32_t neuron_model; /* enum snn_neuron_model */
     int32_t plastic;      /* enum snn_plasticity */
     int32_t poisson_len;  /* entries used in poisson_cdf (0 = no external drive) */
@@ -194,6 +201,9 @@ typedef struct snn_graph_view {
     int32_t *pivots;       /* n x (S+1), row-relative: entries pivots[k][s] ..
                               pivots[k][s+1]-1 of row k target [sW, (s+1)W) */
     int32_t *plastic_end;  /* n: row-relative end of the plastic prefix */
+    uint16_t *col16;       /* compressed_targets: n_edges slice-local indices
+                              (col mod W), 1:1 with col; else NULL. Derived
+                              from col by the graph build */
 } snn_graph_view;
 
 typedef struct snn_stats {

@@ -249,21 +249,32 @@ __device__ __forceinline__ int lower_bound_col(const int32_t *p, int len, int64_
 // lanes over slices. Also the plastic prefix end of each row.
 __global__ __launch_bounds__(kBlock) void k_pivots(GraphArgs a)
 {
-    const int64_t k = ((int64_t)blockIdx.x * kBlock + threadIdx.x) / kWave;
     const int lane = threadIdx.x % kWave;
-    if (k >= a.n) return;  // wave-uniform
-    const int64_t rs = a.row_ptr[k];
-    const int len = (int)(a.row_ptr[k + 1] - rs);
-    const int32_t *row = a.col + rs;
-    int32_t *out = a.piv + k * (int64_t)(a.n_slices + 1);
-    for (int s = lane; s <= a.n_slices; s += kWave)
-        out[s] = s == a.n_slices ? len : lower_bound_col(row, len, (int64_t)s * a.width);
-    if (lane == 0) {
-        int pe = 0;
-        if (a.plastic == 2) pe = len;
-        else if (a.plastic == 1 && k < a.n_exc) pe = lower_bound_col(row, len, a.n_exc);
-        a.pend[k] = pe;
+    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
+    for (int64_t k = ((int64_t)blockIdx.x * kBlock + threadIdx.x) / kWave; k < a.n;
+         k += waves) {  // wave-uniform
+        const int64_t rs = a.row_ptr[k];
+        const int len = (int)(a.row_ptr[k + 1] - rs);
+        const int32_t *row = a.col + rs;
+        int32_t *out = a.piv + k * (int64_t)(a.n_slices + 1);
+        for (int s = lane; s <= a.n_slices; s += kWave)
+            out[s] = s == a.n_slices ? len : lower_bound_col(row, len, (int64_t)s * a.width);
+        if (lane == 0) {
+            int pe = 0;
+            if (a.plastic == 2) pe = len;
+            else if (a.plastic == 1 && k < a.n_exc) pe = lower_bound_col(row, len, a.n_exc);
+            a.pend[k] = pe;
+        }
     }
+}
+
+// Compressed targets: each entry's slice-local index, target - sW for the
+// slice s = target / W that holds it (16 bits for W <= 65536).
+__global__ __launch_bounds__(kBlock) void k_encode_targets(GraphArgs a, int64_t n_edges)
+{
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n_edges; e += stride)
+        a.col16[e] = (uint16_t)(a.col[e] % a.width);
 }
 
 }  // namespace
@@ -342,6 +353,14 @@ hipError_t launch_pivots(hipStream_t s, const GraphArgs &a)
 {
     hipLaunchKernelGGL(k_pivots, dim3(blocks_for((int64_t)a.n * kWave)), dim3(kBlock), 0, s,
                        a);
+    return hipGetLastError();
+}
+
+hipError_t launch_encode_targets(hipStream_t s, const GraphArgs &a, int64_t n_edges)
+{
+    if (n_edges <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_encode_targets, dim3(blocks_for(n_edges, kBlock, 1 << 16)), dim3(kBlock),
+                       0, s, a, n_edges);
     return hipGetLastError();
 }
 

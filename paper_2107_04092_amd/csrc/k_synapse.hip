@@ -572,7 +572,9 @@ constexpr int kDlvWindow = kDlvBlock * kDlvUnroll;
 constexpr int kDlvDirectMax = 32;  // segments up to this long are mapped by their own thread
 static_assert(kDlvBatch == kDlvBlock, "one staged spike per thread");
 
-__global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
+// (four waves per SIMD: two workgroups share a CU)
+template <bool CT>
+__global__ __launch_bounds__(kDlvBlock, 4) void k_deliver_lds(DeliverArgs a)
 {
     extern __shared__ long long acc[];  // nacc * W accumulators [, W histories, W traces]
     __shared__ long long s_start[kDlvBatch];
@@ -726,13 +728,17 @@ __global__ __launch_bounds__(kDlvBlock) void k_deliver_lds(DeliverArgs a)
                 slot[u] = l;
                 off[u] = e0 + x - s_off[l];
                 gi[u] = x < we ? s_start[l] + off[u] : 0;  // edge 0 exists when total > 0
-                cv[u] = col[gi[u]];
+                // compressed targets are the slice-local index itself
+                if (CT)
+                    cv[u] = (int)a.col16[gi[u]];
+                else
+                    cv[u] = col[gi[u]] - base;
                 wv[u] = wgt[gi[u]];
             }
 #pragma unroll
             for (int u = 0; u < kDlvUnroll; ++u) {
                 const bool in = u * kDlvBlock + tid < we;
-                tgt[u] = in ? cv[u] - base : -1;
+                tgt[u] = in ? cv[u] : -1;
                 if (!in) wv[u] = 0.f;
             }
             if (a.plastic) {
@@ -893,11 +899,17 @@ hipError_t launch_stdp_naive(hipStream_t s, const NaiveArgs &a, int blocks, Kern
 hipError_t launch_deliver_lds(hipStream_t s, const DeliverArgs &a, int blocks, size_t lds, KernelEvents ev)
 {
     static std::mutex mu;
-    static int granted = 64 * 1024;
-    const hipError_t e = allow_dynamic_lds((const void *)k_deliver_lds, (int)lds, mu, granted);
+    static int granted[2] = {64 * 1024, 64 * 1024};
+    const bool ct = a.col16 != nullptr;
+    const void *kern = ct ? (const void *)k_deliver_lds<true> : (const void *)k_deliver_lds<false>;
+    const hipError_t e = allow_dynamic_lds(kern, (int)lds, mu, granted[ct]);
     if (e != hipSuccess) return e;
-    hipExtLaunchKernelGGL(k_deliver_lds, dim3(blocks), dim3(kDlvBlock), lds, s,
-                          ev.start, ev.stop, 0, a);
+    if (ct)
+        hipExtLaunchKernelGGL(k_deliver_lds<true>, dim3(blocks), dim3(kDlvBlock), lds, s,
+                              ev.start, ev.stop, 0, a);
+    else
+        hipExtLaunchKernelGGL(k_deliver_lds<false>, dim3(blocks), dim3(kDlvBlock), lds, s,
+                              ev.start, ev.stop, 0, a);
     return hipGetLastError();
 }
 
@@ -908,7 +920,11 @@ hipError_t launch_deliver_global(hipStream_t s, const DeliverArgs &a, int blocks
     return hipGetLastError();
 }
 
-int deliver_lds_static_bytes() { return static_lds_bytes((const void *)k_deliver_lds); }
+int deliver_lds_static_bytes()
+{
+    return std::max(static_lds_bytes((const void *)k_deliver_lds<false>),
+                    static_lds_bytes((const void *)k_deliver_lds<true>));
+}
 int stdp_static_bytes() { return static_lds_bytes((const void *)k_stdp); }
 
 }  // namespace snn

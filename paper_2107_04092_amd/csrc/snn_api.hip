@@ -27,6 +27,7 @@ struct snn_ctx {
     int32_t info_blocks = 1, syn_slots = 1;
     int32_t hw = 1;  // 64-bit history words per neuron
     int32_t algo = 0;  // plasticity_algorithm: 0 lazy + event, 1 lazy, 2 naive
+    bool ct = false;  // compressed targets: 16-bit slice-local indices for slice delivery
     float *sx_pre = nullptr, *sx_post = nullptr;  // per-synapse traces (naive)
     // kernel timing: events [step][part][start, stop] for the first t_cap
     // steps run by snn_step after snn_record_kernel_times; t_rec marks parts
@@ -67,6 +68,7 @@ struct snn_ctx {
     size_t g_bytes = 0;
     int64_t n_edges = -1, counted_edges = -1;
     int32_t *col = nullptr;
+    uint16_t *col16 = nullptr;  // compressed targets (ct)
     float *w = nullptr;
     int32_t *piv = nullptr;
     int graph_state = 0;  // 0 none, 1 counted, 2 buffer bound, 3 built
@@ -138,6 +140,8 @@ snn_status validate(snn_ctx *c, const snn_config &k)
         return fail(c, SNN_EINVAL, "plasticity_algorithm must be 0, 1 or 2");
     if (k.stdp_filter < 0 || k.stdp_filter > 3)
         return fail(c, SNN_EINVAL, "stdp_filter must be in [0, 3]");
+    if (k.compressed_targets < 0 || k.compressed_targets > 1)
+        return fail(c, SNN_EINVAL, "compressed_targets must be 0 or 1");
     if (k.stdp_filter == 1 && (int64_t)k.n + 16 > kCodeMax)
         return fail(c, SNN_EINVAL, "stdp_filter 1 needs n + 16 <= %d", kCodeMax);
     if (k.stdp_filter == 2 && (k.n + 63) / 64 > kRecentMaxWords)
@@ -185,6 +189,7 @@ void derive(snn_ctx *c)
     c->nacc = k.neuron_model == SNN_LIF_CUBA ? 2 : 1;
     c->hw = k.history_bits == 128 ? 2 : 1;
     c->algo = k.plasticity_algorithm;
+    c->ct = k.compressed_targets != 0;
     c->n_slices = (k.n + k.slice_width - 1) / k.slice_width;
     c->chunks = k.spike_chunks;
     c->delay = k.delay_steps;
@@ -297,6 +302,7 @@ GraphArgs graph_args(snn_ctx *c)
     a.width = c->cfg.slice_width;
     a.n_slices = c->n_slices;
     a.plastic = c->cfg.plastic;
+    a.col16 = c->col16;
     return a;
 }
 
@@ -323,6 +329,10 @@ snn_status finish_graph(snn_ctx *c)
     GraphArgs a = graph_args(c);
     snn_status st = check_hip(c, launch_pivots(c->stream, a), "pivot kernel");
     if (st) return st;
+    if (c->ct) {
+        st = check_hip(c, launch_encode_targets(c->stream, a, c->n_edges), "target compression");
+        if (st) return st;
+    }
     if (c->algo == 2) {  // per-synapse traces start at 0
         st = check_hip(c, launch_fill_f32(c->stream, c->sx_pre, c->n_edges, 0.f), "traces");
         if (!st) st = check_hip(c, launch_fill_f32(c->stream, c->sx_post, c->n_edges, 0.f),
@@ -577,6 +587,7 @@ DeliverArgs deliver_args(snn_ctx *c)
     a.nacc = c->nacc;
     a.n_work = c->n_slices * c->chunks;
     a.stats = c->dlv_stats;
+    a.col16 = c->col16;
     a.plastic = c->n_plastic_rows > 0 && c->algo != 2;
     a.event = c->algo == 0;
     a.txinfo = c->txinfo;
@@ -799,7 +810,8 @@ snn_status snn_graph_size(const snn_ctx *c, int64_t n_edges, size_t *bytes)
 {
     if (!c || !bytes || n_edges < 0) return SNN_EINVAL;
     *bytes = (c->algo == 2 ? 4 : 2) * align_up((size_t)n_edges * sizeof(int32_t)) +
-             align_up((size_t)c->n * (size_t)(c->n_slices + 1) * 4);
+             align_up((size_t)c->n * (size_t)(c->n_slices + 1) * 4) +
+             (c->ct ? align_up((size_t)n_edges * sizeof(uint16_t)) : 0);
     return SNN_OK;
 }
 
@@ -827,6 +839,7 @@ snn_status snn_bind_graph(snn_ctx *c, void *device_ptr, size_t bytes, int64_t n_
     const size_t pivb = align_up((size_t)c->n * (size_t)(c->n_slices + 1) * 4);
     c->sx_pre = c->algo == 2 ? (float *)(c->g + 2 * arr + pivb) : nullptr;
     c->sx_post = c->algo == 2 ? (float *)(c->g + 3 * arr + pivb) : nullptr;
+    c->col16 = c->ct ? (uint16_t *)(c->g + (c->algo == 2 ? 4 : 2) * arr + pivb) : nullptr;
     if (c->graph_state != 1) c->counted_kind = -1;
     c->graph_state = 2;
     return SNN_OK;
@@ -1120,6 +1133,7 @@ snn_status snn_get_graph(const snn_ctx *c, snn_graph_view *out)
     out->w = c->w;
     out->pivots = c->piv;
     out->plastic_end = c->pend;
+    out->col16 = c->col16;
     return SNN_OK;
 }
 

@@ -21,6 +21,9 @@ constexpr int kStdpUnroll = 4;       // elements per thread with loads in flight
 constexpr int kStdpWindow = kStdpBlock * kStdpUnroll;  // elements per segment map
 constexpr int kGlobalMaxBlocks = 2048;
 constexpr int kLdsBytes = 160 * 1024;
+// slice widths are bounded by the 8-byte accumulators in LDS, so a slice-local
+// index (compressed targets) always fits 16 bits
+static_assert(kLdsBytes / 8 <= 65536, "slice-local index must fit 16 bits");
 // Spike histories: hw 64-bit words per neuron (1 or 2), neuron-major; word 0
 // bit b = step t-b, word 1 bit b = step t-64-b. A plastic row is forced once
 // its last update is 64 hw steps old, so every window fits the history.
@@ -165,6 +168,7 @@ struct DeliverArgs {
     float *ain;              // fp32 input [nacc][n], written directly when C == 1
     int64_t part_stride;
     int32_t n, n_exc, width, n_slices, chunks, nacc, n_work, hw;
+    const uint16_t *col16;   // compressed targets: slice-local indices (nullptr: read `col`)
     int64_t *stats;          // [gridDim.x][2]: events delivered, weights written
     // plasticity of the transmitting rows, fused into slice delivery
     int32_t plastic;         // 0: no plastic rows
@@ -197,6 +201,7 @@ struct NaiveArgs {
 struct GraphArgs {
     int64_t *row_ptr;        // n+1
     int32_t *col;
+    uint16_t *col16;         // compressed targets (encoded from col), or nullptr
     float *w;
     int32_t *piv;
     int32_t *pend;
@@ -244,6 +249,8 @@ constexpr int kStdpRowsBlock = 1024;   // threads of the row-wise STDP kernel
 constexpr int kStdpRowsUnroll = 8;     // synapses per lane and row part (64-step histories)
 constexpr int kStdpRowsUnroll2 = 4;    // the same with 128-step histories
 constexpr int kStdpRowsBlocks = 256;   // its persistent grid (one workgroup per CU)
+
+
 // LDS of the row-wise STDP workgroup's candidate queues (one per wave: target
 // and weight of up to U x 64 synapses)
 constexpr int stdp_rows_queue_bytes(int hw)
@@ -272,5 +279,7 @@ hipError_t launch_edges_scatter(hipStream_t s, const GraphArgs &a, const int32_t
 hipError_t launch_row_maxlen(hipStream_t s, const GraphArgs &a);
 hipError_t launch_row_sort(hipStream_t s, const GraphArgs &a, int pow2len);
 hipError_t launch_pivots(hipStream_t s, const GraphArgs &a);
+// col16 from col (snn_config.compressed_targets): slice-local indices
+hipError_t launch_encode_targets(hipStream_t s, const GraphArgs &a, int64_t n_edges);
 
 }  // namespace snn

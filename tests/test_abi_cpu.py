@@ -72,6 +72,7 @@ def test_struct_layouts_match_header(tmp_path):
     ("stdp_filter", 4, "stdp_filter"),
     ("plasticity_algorithm", 3, "plasticity_algorithm"),
     ("history_bits", 96, "history_bits"),
+    ("compressed_targets", 2, "compressed_targets"),
     ("poisson_len", 33, "poisson_len"),
     ("dt_ms", float("nan"), "NaN"),
     ("tau_m_ms", 0.0, "tau_m_ms"),
@@ -98,6 +99,7 @@ def test_create_rejects_bad_stdp_and_cuba_config():
     cfg.p_fire = 1.5
     with pytest.raises(snn.SnnError, match="p_fire"):
         snn.snn_create(cfg, 0)
+
 
 
 def test_poisson_table_must_be_monotone():

@@ -125,3 +125,27 @@ def test_steps_before_graph_are_rejected():
     with pytest.raises(snn.SnnError) as e:
         snn.snn_build_graph_random(net.ctx, 0.1, 0.1)
     assert e.value.status == snn.SNN_ESTATE
+
+
+def expected_col16(col, width):
+    """The compressed-target format written out: the slice-local index."""
+    return (col % width).astype(np.uint16)
+
+
+@pytest.mark.parametrize("name,kw,width", [
+    ("stress", dict(n=20_000, p_or_fanout=300), 2048),
+    ("tiny", dict(n=1000 + 37), 320),
+    ("brunel_plus", dict(n=3000, n_exc=2400), 1024),
+    ("stress", dict(n=777, p_or_fanout=3000), 64),
+    ("stress", dict(n=100_000, p_or_fanout=2, plastic=PLASTIC_NONE), 12288),
+])
+def test_compressed_targets_encode_the_oracle_graph(name, kw, width):
+    p = wl.preset(name, slice_width=width, **kw)
+    log("compressed targets %s %s W=%d" % (name, kw, width))
+    net = gpu_net(p, compressed_targets=1)
+    o = oracle_net(p)
+    rp_o, col_o, _ = o.graph()
+    g = net.graph()
+    assert np.array_equal(to_np(g["col"]), col_o)
+    got = to_np(g["col16"]).view(np.uint16)
+    assert np.array_equal(got, expected_col16(col_o.astype(np.int64), width))

@@ -204,6 +204,37 @@ def test_free_run_with_state_reads(mode, delay):
     assert net.stats()["device_errors"] == 0
 
 
+CT_CASES = [
+    # name, preset overrides, steps, slice width, chunks
+    ("stress", dict(n=6000, p_or_fanout=200, p_fire=0.02), 200, 1024, 4),
+    ("stress", dict(n=3000, p_or_fanout=150, p_fire=0.03, delay=3), 160, 640, 1),
+    ("brunel_plus", dict(n=2500, n_exc=2000), 300, 512, 2),
+    ("vogels", dict(), 200, 1024, 2),
+    # sparse rows over 18 slices of 4096
+    ("stress", dict(n=70_000, p_or_fanout=3, p_fire=0.05), 150, 4096, 1),
+]
+
+
+@pytest.mark.parametrize("hbits", [64, 128], ids=["h64", "h128"])
+@pytest.mark.parametrize("mode", [LDS, GLOBAL], ids=["lds", "global"])
+@pytest.mark.parametrize("case", CT_CASES, ids=lambda c: "%s-%s" % (c[0], c[1].get("n", "")))
+def test_compressed_targets_parity(case, mode, hbits):
+    """16-bit slice-local targets (read by slice delivery): the same parity
+    bar as the 32-bit targets."""
+    name, kw, steps, width, chunks = case
+    p = wl.preset(name, **kw)
+    log("compressed-target parity %s %s mode=%d history=%d W=%d C=%d" % (
+        name, kw, mode, hbits, width, chunks))
+    net, o, cnt = teacher_forced_run(p, steps, mode, slice_width=width, spike_chunks=chunks,
+                                     history_bits=hbits, compressed_targets=1)
+    assert cnt["spikes"] > 0
+    if p.plastic != PLASTIC_NONE:
+        assert cnt["rows"] > 0
+        net.flush_plasticity()
+        compare_all_plastic_weights(net, o)
+    assert net.stats()["device_errors"] == 0
+
+
 ALGO_CASES = [
     ("brunel_plus", dict(n=2500, n_exc=2000), 260, 512, 2),
     ("stress", dict(n=6000, p_or_fanout=200, p_fire=0.02), 200, 1024, 4),
