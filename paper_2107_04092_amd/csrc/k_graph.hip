@@ -174,9 +174,14 @@ __global__ __launch_bounds__(kBlock) void k_edges_scatter(GraphArgs a, const int
 __global__ __launch_bounds__(kBlock) void k_row_maxlen(GraphArgs a)
 {
     const int k = blockIdx.x * kBlock + threadIdx.x;
-    if (k >= a.n) return;
-    const int64_t len = a.row_ptr[k + 1] - a.row_ptr[k];
-    atomicMax(a.maxlen, (int32_t)(len > 0x7fffffff ? 0x7fffffff : len));
+    int len = 0;
+    if (k < a.n) {
+        const int64_t l = a.row_ptr[k + 1] - a.row_ptr[k];
+        len = (int)(l > 0x7fffffff ? 0x7fffffff : l);
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) len = max(len, __shfl_xor(len, off, kWave));
+    if (threadIdx.x % kWave == 0 && len > 0) atomicMax(a.maxlen, len);  // one per wave
 }
 
 // Order-preserving map of fp32 bits to uint32 (negative floats reversed).

@@ -280,25 +280,32 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
 
     // cursor: the next part to issue (row snapshot, row-list index, base);
     // la: snapshot of the row after the cursor's
+    // Work items are (row, phase) pairs, phase m in [0, P): the wave holding
+    // a pair takes parts m, m + P, m + 2P, ... of the row, so a row of up to
+    // P parts is spread over P waves. The cursor index counts pairs.
+    const int P = a.parts;
+    const int npairs = nrows * P;
+    auto row_of = [&](int i) { return P == 1 ? i : i / P; };
+    auto phase_of = [&](int i) { return P == 1 ? 0 : i % P; };
     RowInfo cur = RowInfo{}, la = RowInfo{};
     int cur_i = gw, la_i = gw + nwv;
-    if (cur_i < nrows) cur = a.info[cur_i];
-    if (la_i < nrows) la = a.info[la_i];
-    int cur_base = -(int)(cur.rs & 15);
+    if (cur_i < npairs) cur = a.info[row_of(cur_i)];
+    if (la_i < npairs) la = a.info[row_of(la_i)];
+    int cur_base = -(int)(cur.rs & 15) + phase_of(cur_i) * (U * kWave);
     auto issue = [&](RowPart<U> &p) {
         p.ri = cur;
         p.i = cur_i;
         p.base = cur_base;
         rows_issue(p, col, wgt, lane);
-        if (cur.age_pre != 0 && cur_base + U * kWave < cur.len) {  // rest of the row
-            cur_base += U * kWave;
-        } else {  // the lookahead row
+        if (cur.age_pre != 0 && cur_base + P * U * kWave < cur.len) {  // the pair's next part
+            cur_base += P * U * kWave;
+        } else {  // the lookahead pair
             cur = la;
+            cur_base = -(int)(la.rs & 15) + phase_of(la_i) * (U * kWave);
             cur_i = la_i;
-            cur_base = -(int)(la.rs & 15);
             la_i += nwv;
             la = RowInfo{};
-            if (la_i < nrows) la = a.info[la_i];
+            if (la_i < npairs) la = a.info[row_of(la_i)];
         }
     };
     // the first two parts are in flight before the staging
@@ -442,9 +449,9 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
         }
         issue(p);
     };
-    while (A.i < nrows) {
+    while (A.i < npairs) {
         step(A);
-        if (B.i >= nrows) break;
+        if (B.i >= npairs) break;
         step(B);
     }
     // one atomic per wave: no workgroup barrier waits for the weight stores

@@ -4,6 +4,7 @@
 #include "snn_internal.h"
 #include "snn.h"
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -28,6 +29,7 @@ struct snn_ctx {
     int32_t hw = 1;  // 64-bit history words per neuron
     int32_t algo = 0;  // plasticity_algorithm: 0 lazy + event, 1 lazy, 2 naive
     bool ct = false;  // compressed targets: 16-bit slice-local indices for slice delivery
+    int32_t max_row = 0;  // longest row of the built graph
     float *sx_pre = nullptr, *sx_post = nullptr;  // per-synapse traces (naive)
     // kernel timing: events [step][part][start, stop] for the first t_cap
     // steps run by snn_step after snn_record_kernel_times; t_rec marks parts
@@ -339,15 +341,22 @@ snn_status finish_graph(snn_ctx *c)
                                 "traces");
         if (st) return st;
     }
-    int32_t err = 0;
+    st = check_hip(c, launch_fill_i32(c->stream, c->maxlen, 1, 0), "row length");
+    if (!st) st = check_hip(c, launch_row_maxlen(c->stream, a), "row length");
+    if (st) return st;
+    int32_t err = 0, maxlen = 0;
     st = check_hip(c, hipMemcpyAsync(&err, c->err_flag, sizeof err, hipMemcpyDeviceToHost,
                                      c->stream), "read error flag");
+    if (!st)
+        st = check_hip(c, hipMemcpyAsync(&maxlen, c->maxlen, sizeof maxlen,
+                                         hipMemcpyDeviceToHost, c->stream), "read row length");
     if (st) return st;
     st = check_hip(c, hipStreamSynchronize(c->stream), "graph build");
     if (st) return st;
     if (err & kErrIndex) return fail(c, SNN_EINVAL, "edge index outside [0, n)");
     if (err & kErrRowTooLong)
         return fail(c, SNN_EINVAL, "a row has more than %d edges", kMaxSortRow);
+    c->max_row = maxlen;
     c->graph_state = 3;
     return SNN_OK;
 }
@@ -498,6 +507,25 @@ StdpArgs stdp_args(snn_ctx *c, bool flush)
     a.recent = filt && (f == 2 || (f == 0 && !fits_code && fits_map)) ? c->recent : nullptr;
     a.event = c->algo == 0;
     a.nw = c->nw;
+    // row-wise layout: a row's parts (counting the row start's offset in its
+    // line) may spread over P waves. P minimises the parts one wave takes in
+    // sequence, ceil(rows P / waves) ceil(parts / P), for the expected number
+    // of rows: all plastic rows in a flush, else the forced rows (staggered:
+    // one in 64 hw per step); ties keep the smaller P (fewer snapshot loads).
+    const int part = (c->hw == 2 ? kStdpRowsUnroll2 : kStdpRowsUnroll) * kWave;
+    const int64_t parts = std::max(1, (c->max_row + 15 + part - 1) / part);
+    const int64_t rows = std::max<int64_t>(1, flush ? c->n_plastic_rows
+                                                    : c->n_plastic_rows / (64 * c->hw));
+    const int64_t waves = (int64_t)kStdpRowsBlocks * (kStdpRowsBlock / kWave);
+    int64_t best = -1;
+    a.parts = 1;
+    for (int pp = 1; pp <= kStdpRowsSplit && pp <= parts; ++pp) {
+        const int64_t chain = ((rows * pp + waves - 1) / waves) * ((parts + pp - 1) / pp);
+        if (best < 0 || chain < best) {
+            best = chain;
+            a.parts = pp;
+        }
+    }
     for (int q = 0; q <= kMaxAge; ++q) a.dpow[q] = c->dpow[q];
     return a;
 }

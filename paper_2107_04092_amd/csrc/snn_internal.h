@@ -154,6 +154,7 @@ struct StdpArgs {
     const uint8_t *code;
     const uint64_t *recent;
     int32_t nw;              // words of `recent`
+    int32_t parts;           // row-wise layout: waves sharing one row (>= 1)
     float dpow[kMaxAge + 1];
 };
 
@@ -249,6 +250,7 @@ constexpr int kStdpRowsBlock = 1024;   // threads of the row-wise STDP kernel
 constexpr int kStdpRowsUnroll = 8;     // synapses per lane and row part (64-step histories)
 constexpr int kStdpRowsUnroll2 = 4;    // the same with 128-step histories
 constexpr int kStdpRowsBlocks = 256;   // its persistent grid (one workgroup per CU)
+constexpr int kStdpRowsSplit = 8;      // most waves that share one row
 
 
 // LDS of the row-wise STDP workgroup's candidate queues (one per wave: target

@@ -100,7 +100,7 @@ PRESETS = {
         graph_kind=GRAPH_BERNOULLI, p_or_fanout=0.1, w_exc=0.1, w_inh=-0.5,
         delay=15, v_th=20.0, v_reset=10.0, v_inf=0.0, tau_ref=2.0,
         v0_lo=0.0, v0_hi=20.0, poisson_mu=2.0, j_ext=0.1,
-        slice_width=4096, steps=10_000),
+        slice_width=1024, spike_chunks=4, compressed_targets=1, steps=10_000),
     # Brunel scaled to 25,000 neurons (20,000/5,000) with power-law STDP on
     # exc->exc synapses.
     "brunel_plus": Preset(
@@ -109,7 +109,7 @@ PRESETS = {
         delay=15, v_th=20.0, v_reset=10.0, v_inf=0.0, tau_ref=2.0,
         v0_lo=0.0, v0_hi=20.0, poisson_mu=2.0, j_ext=0.1,
         plastic=PLASTIC_EXC_EXC, w0=_w0_fixed_point(0.1, 0.11, 0.4),
-        slice_width=4096, steps=100_000),
+        slice_width=1024, spike_chunks=4, compressed_targets=1, steps=100_000),
     # 250,000 Bernoulli(0.005) sources, fan-out 1,000 uniform-random targets
     # (with replacement), STDP on all synapses, D=1.
     "stress": Preset(
