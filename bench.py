@@ -88,15 +88,14 @@ def load_traffic(kernel, workload_key):
         return None
 
 
-def stdp_bytes(st, n, launches, target_bytes=4):
+def stdp_bytes(st, n, launches):
     """Algorithmic bytes of the forced-row STDP kernel (snn_update_plasticity):
-    per synapse update the target (4 B, or 2 B compressed) and the weight
-    (4 B) read, per changed weight 4 B (store), per row 40 B (list entry, row
-    pointer, plastic end, source history, t_last and pre trace read and
-    written), per launch 8 B per neuron (the target histories)."""
-    return ((target_bytes + 4) * st["stdp_forced_synapse_updates"] +
-            4 * st["stdp_forced_weights_written"] + 40 * st["stdp_forced_rows"] +
-            8 * n * launches)
+    per synapse update 8 B (32-bit target and weight read), per changed weight
+    4 B (store), per row 40 B (list entry, row pointer, plastic end, source
+    history, t_last and pre trace read and written), per launch 8 B per neuron
+    (the target histories)."""
+    return (8 * st["stdp_forced_synapse_updates"] + 4 * st["stdp_forced_weights_written"] +
+            40 * st["stdp_forced_rows"] + 8 * n * launches)
 
 
 def delivery_bytes(st, n, n_slices, chunks, nacc, launches, mode, target_bytes=4):
@@ -211,8 +210,9 @@ def main():
 
     n_slices = (p.n + width - 1) // width
     nacc = 2 if p.model == snn.SNN_LIF_CUBA else 1
-    tb = 2 if cfg.compressed_targets else 4
-    b_stdp = stdp_bytes(st, p.n, args.steps, tb) / args.steps
+    # 16-bit targets are read by slice delivery only; row-wise STDP reads 32-bit
+    tb = 2 if cfg.compressed_targets and args.mode == "lds" else 4
+    b_stdp = stdp_bytes(st, p.n, args.steps) / args.steps
     b_dlv = delivery_bytes(st, p.n, n_slices, chunks, nacc, args.steps, args.mode,
                            tb) / args.steps
 
@@ -230,7 +230,7 @@ def main():
         kt, nrec = net.kernel_times()
         net.record_kernel_times(0)
         st2 = net.stats()
-        b_stdp = stdp_bytes(st2, p.n, args.steps, tb) / args.steps
+        b_stdp = stdp_bytes(st2, p.n, args.steps) / args.steps
         b_dlv = delivery_bytes(st2, p.n, n_slices, chunks, nacc, args.steps,
                                args.mode, tb) / args.steps
         t_neu, t_stdp, t_dlv = kt["neuron"], kt["plasticity"], kt["delivery"]
