@@ -58,35 +58,101 @@ __global__ __launch_bounds__(kBlock) void k_fill(T *p, int64_t count, T value)
 // in that step's spike list was recorded (spk_pos); its snapshot goes to the
 // same position, so snapshots line up with the delay-ring list delivery reads.
 
-// One neuron's update at step t (i < n): its dynamics, its history word(s)
-// and post trace, its history code; returns spiked / transmitting / forced.
-__device__ __forceinline__ void neuron_update(const NeuronArgs &a, int i, int &s, int &tx,
-                                              int &forced, bool &fired_recently)
+// A neuron's state as one update reads and writes it: potential,
+// refractory count, CUBA currents, post trace and history words.
+struct NState {
+    float v, ie, ii, y;
+    int r;
+    uint64_t h0, h1;
+};
+
+// M >= 0 fixes the neuron model at compile time for a network without
+// plasticity (the small-network kernel); M < 0 reads both from the arguments.
+// H > 0 fixes the history width in words the same way.
+template <int M>
+__device__ __forceinline__ int nmodel(const NeuronArgs &a) { return M >= 0 ? M : a.model; }
+template <int M>
+__device__ __forceinline__ bool nplastic(const NeuronArgs &a)
 {
-    if (a.model == 2) {
-        s = rng32(a.seed, 4, (uint64_t)a.t, (uint64_t)i) < a.fire_thr;
-    } else {
-        float ae, ai = 0.f;
-        if (a.input_forced) {
-            ae = a.ain[i];
-            if (a.model == 1) ai = a.ain[a.n + i];
-        } else {
-            long long se = a.apart[i];
-            for (int c = 1; c < a.n_parts; ++c) se += a.apart[c * a.part_stride + i];
-            ae = from_fix(se);
-            if (a.model == 1) {
-                long long si = a.apart[a.n + i];
-                for (int c = 1; c < a.n_parts; ++c) si += a.apart[c * a.part_stride + a.n + i];
-                ai = from_fix(si);
-            }
+    return M >= 0 ? false : a.n_plastic_rows > 0;
+}
+template <int H>
+__device__ __forceinline__ int nhw(const NeuronArgs &a) { return H > 0 ? H : a.hw; }
+
+template <int M, int H>
+__device__ __forceinline__ void nstate_load(const NeuronArgs &a, int i, NState &st)
+{
+    st.v = st.ie = st.ii = st.y = 0.f;
+    st.r = 0;
+    if (nmodel<M>(a) != 2) {
+        st.v = a.v[i];
+        st.r = a.ref[i];
+        if (nmodel<M>(a) == 1) {
+            st.ie = a.ie[i];
+            st.ii = a.ii[i];
         }
-        float v = a.v[i];
-        int r = a.ref[i];
+    }
+    const uint64_t *hp = a.hist + (int64_t)i * nhw<H>(a);
+    st.h0 = hp[0];
+    st.h1 = nhw<H>(a) == 2 ? hp[1] : 0ull;
+    if (nplastic<M>(a)) st.y = a.ypost[i];
+}
+
+template <int M, int H>
+__device__ __forceinline__ void nstate_store(const NeuronArgs &a, int i, const NState &st)
+{
+    if (nmodel<M>(a) != 2) {
+        a.v[i] = st.v;
+        a.ref[i] = st.r;
+        if (nmodel<M>(a) == 1) {
+            a.ie[i] = st.ie;
+            a.ii[i] = st.ii;
+        }
+    }
+    uint64_t *hp = a.hist + (int64_t)i * nhw<H>(a);
+    hp[0] = st.h0;
+    if (nhw<H>(a) == 2) hp[1] = st.h1;
+    if (nplastic<M>(a)) a.ypost[i] = st.y;
+}
+
+// The input A(t) of neuron i from the state: the fp32 input, or the sum of
+// the fixed-point partial sums of delivery.
+__device__ __forceinline__ void neuron_input(const NeuronArgs &a, int i, float &ae, float &ai)
+{
+    ai = 0.f;
+    if (a.input_forced) {
+        ae = a.ain[i];
+        if (a.model == 1) ai = a.ain[a.n + i];
+    } else {
+        long long se = a.apart[i];
+        for (int c = 1; c < a.n_parts; ++c) se += a.apart[c * a.part_stride + i];
+        ae = from_fix(se);
         if (a.model == 1) {
-            const float ie = __fadd_rn(__fmul_rn(a.ie[i], a.d_e), ae);
-            const float ii = __fadd_rn(__fmul_rn(a.ii[i], a.d_i), ai);
-            a.ie[i] = ie;
-            a.ii[i] = ii;
+            long long si = a.apart[a.n + i];
+            for (int c = 1; c < a.n_parts; ++c) si += a.apart[c * a.part_stride + a.n + i];
+            ai = from_fix(si);
+        }
+    }
+}
+
+// One neuron's update at step t (i < n) on its state in registers, with
+// input (ae, ai): its dynamics in a fixed fp32 operation order, its post
+// trace and its history words. Returns whether it spiked.
+template <int M, int H>
+__device__ __forceinline__ int neuron_advance(const NeuronArgs &a, int i, int64_t t, float ae,
+                                              float ai, NState &st)
+{
+    int s = 0;
+    if (nmodel<M>(a) == 2) {
+        s = rng32(a.seed, 4, (uint64_t)t, (uint64_t)i) < a.fire_thr;
+    } else {
+        float v = st.v;
+        int r = st.r;
+        if (nmodel<M>(a) == 1) {
+            const float ie = __fadd_rn(__fmul_rn(st.ie, a.d_e), ae);
+            const float ii = __fadd_rn(__fmul_rn(st.ii, a.d_i), ai);
+            st.ie = ie;
+            st.ii = ii;
             if (r > 0) {
                 r -= 1;
                 v = a.v_reset;
@@ -108,7 +174,7 @@ __device__ __forceinline__ void neuron_update(const NeuronArgs &a, int i, int &s
             } else {
                 float x = 0.f;
                 if (a.poisson_len > 0) {
-                    const uint32_t u = rng32(a.seed, 3, (uint64_t)a.t, (uint64_t)i);
+                    const uint32_t u = rng32(a.seed, 3, (uint64_t)t, (uint64_t)i);
                     int k = 0;
                     for (int q = 0; q < a.poisson_len; ++q) k += (a.poisson[q] <= u);
                     x = __fmul_rn(a.j_ext, (float)k);
@@ -125,29 +191,42 @@ __device__ __forceinline__ void neuron_update(const NeuronArgs &a, int i, int &s
                 }
             }
         }
-        a.v[i] = v;
-        a.ref[i] = r;
+        st.v = v;
+        st.r = r;
     }
-    uint64_t *hp = a.hist + (int64_t)i * a.hw;
-    uint64_t h = hp[0];
-    uint64_t h1 = a.hw == 2 ? hp[1] : 0ull;
-    if (a.n_plastic_rows > 0) {
+    if (nplastic<M>(a)) {
         // post trace seen by a pre spike at step t: posts strictly before t
-        const float y = __fmul_rn(__fadd_rn(a.ypost[i], (float)(h & 1ull)), a.d_minus);
-        a.ypost[i] = y;
+        st.y = __fmul_rn(__fadd_rn(st.y, (float)(st.h0 & 1ull)), a.d_minus);
     }
-    h1 = a.hw == 2 ? (h1 << 1) | (h >> 63) : 0ull;
-    h = (h << 1) | (uint64_t)s;
-    hp[0] = h;
-    if (a.hw == 2) hp[1] = h1;
-    // history code for the row-wise STDP of this step: the position + 1 of
-    // the only spike of the last 64 hw steps (bit b = step t-b), 0 for none
-    const int np = __popcll(h) + __popcll(h1);
-    const int pos = h ? __ffsll((long long)h) : 64 + __ffsll((long long)h1);
-    a.code[i] = np == 0 ? (uint8_t)0 : np == 1 ? (uint8_t)pos : kCodeMulti;
-    fired_recently = np != 0;
-    tx = (int)((h >> a.dm1) & 1ull);
-    if (i < a.n_plastic_rows) forced = !tx && (a.t - (int64_t)a.t_last[i] >= 64 * a.hw);
+    st.h1 = nhw<H>(a) == 2 ? (st.h1 << 1) | (st.h0 >> 63) : 0ull;
+    st.h0 = (st.h0 << 1) | (uint64_t)s;
+    return s;
+}
+
+// History code for the row-wise STDP: the position + 1 of the only spike of
+// the last 64 hw steps (bit b = step t-b), 0 for none, kCodeMulti for more.
+__device__ __forceinline__ uint8_t hist_code(uint64_t h0, uint64_t h1)
+{
+    const int np = __popcll(h0) + __popcll(h1);
+    const int pos = h0 ? __ffsll((long long)h0) : 64 + __ffsll((long long)h1);
+    return np == 0 ? (uint8_t)0 : np == 1 ? (uint8_t)pos : kCodeMulti;
+}
+
+// The whole update of neuron i at step t from and to the state arrays;
+// returns spiked / transmitting / forced.
+__device__ __forceinline__ void neuron_update(const NeuronArgs &a, int i, int64_t t, int &s,
+                                              int &tx, int &forced, bool &fired_recently)
+{
+    NState st;
+    nstate_load<-1, 0>(a, i, st);
+    float ae = 0.f, ai = 0.f;
+    if (a.model != 2) neuron_input(a, i, ae, ai);
+    s = neuron_advance<-1, 0>(a, i, t, ae, ai, st);
+    nstate_store<-1, 0>(a, i, st);
+    a.code[i] = hist_code(st.h0, st.h1);
+    fired_recently = (st.h0 | st.h1) != 0ull;
+    tx = (int)((st.h0 >> a.dm1) & 1ull);
+    if (i < a.n_plastic_rows) forced = !tx && (t - (int64_t)a.t_last[i] >= 64 * a.hw);
 }
 
 static_assert((1 << 24) / (kNeuronBlock * kNeuronRounds) <= 65536,
@@ -193,7 +272,7 @@ __global__ __launch_bounds__(kNeuronBlock) void k_neuron(NeuronArgs a, CompactAr
         const int i = (blockIdx.x * R + r) * kNeuronBlock + tid;
         s[r] = tx[r] = forced[r] = 0;
         bool fired_recently = false;
-        if (i < a.n) neuron_update(a, i, s[r], tx[r], forced[r], fired_recently);
+        if (i < a.n) neuron_update(a, i, a.t, s[r], tx[r], forced[r], fired_recently);
         const uint64_t m = ballot64(s[r]), txm = ballot64(tx[r]), fm = ballot64(forced[r]);
         const uint64_t rcm = ballot64(fired_recently);
         if (lane == 0) {
@@ -329,6 +408,126 @@ __global__ __launch_bounds__(kNeuronBlock) void k_neuron(NeuronArgs a, CompactAr
     }
 }
 
+// ---------------------------------------------------------------------------
+// Small networks without plasticity: b.steps whole steps in one workgroup,
+// each thread holding the state of its neurons (one per round of
+// kSmallBlock) in registers from the first step to the last. Each step:
+// (1) the neuron update of every neuron (the same arithmetic as k_neuron;
+// from the second step on the input is the LDS accumulator, exact like the
+// fixed-point partial sums), fire and transmit masks, and the spike list in
+// ascending order into ring slot t mod D; (3) delivery of ring slot
+// (t-D+1) mod D, a wave per transmitted row, lanes over its targets, 64-bit
+// fixed-point LDS atomics. At the end the state goes back to the arrays and
+// the accumulator becomes partial sum 0, where the next neuron update (of
+// either path) reads it.
+
+template <int M, int H>
+__global__ __launch_bounds__(kSmallBlock) void k_small_steps(NeuronArgs a, SmallArgs b)
+{
+    constexpr int NWV = kSmallBlock / kWave;
+    extern __shared__ long long acc[];  // nacc * n
+    __shared__ int s_cnt[kSmallRounds * NWV];
+    __shared__ int s_total;
+    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const int n = a.n;
+    const int rounds = (n + kSmallBlock - 1) / kSmallBlock;  // <= kSmallRounds
+    const int span = b.nacc * n;
+    long long events = 0, spikes = 0;
+    NState st[kSmallRounds];
+#pragma unroll
+    for (int r = 0; r < kSmallRounds; ++r) {
+        const int i = r * kSmallBlock + tid;
+        if (r < rounds && i < n) nstate_load<M, H>(a, i, st[r]);
+    }
+    for (int k = 0; k < b.steps; ++k) {
+        const int64_t t = a.t + k;
+        const int slot = (int)(t % b.delay);
+        int32_t *list = b.ring + (int64_t)slot * n;
+        // (1) neuron update
+        int sp[kSmallRounds];
+#pragma unroll
+        for (int r = 0; r < kSmallRounds; ++r) {
+            sp[r] = 0;
+            if (r >= rounds) continue;  // workgroup-uniform
+            const int i = r * kSmallBlock + tid;
+            uint64_t hw0 = 0ull, hw1 = 0ull;
+            if (i < n) {
+                float ae = 0.f, ai = 0.f;
+                if (M != 2) {
+                    if (k == 0) {
+                        neuron_input(a, i, ae, ai);
+                    } else {
+                        ae = from_fix(acc[i]);
+                        if (M == 1) ai = from_fix(acc[n + i]);
+                    }
+                }
+                sp[r] = neuron_advance<M, H>(a, i, t, ae, ai, st[r]);
+                hw0 = st[r].h0;
+                hw1 = st[r].h1;
+            }
+            const uint64_t m = ballot64(sp[r]);
+            const uint64_t txm = ballot64((hw0 >> a.dm1) & 1ull);
+            const uint64_t rcm = ballot64((hw0 | hw1) != 0ull);
+            if (lane == 0) {
+                const int word = r * NWV + wave;
+                if (word * kWave < n) {
+                    a.mask[word] = m;
+                    a.txmask[word] = txm;
+                    a.recent[word] = rcm;
+                }
+                s_cnt[word] = __popcll(m);
+            }
+        }
+        __syncthreads();  // every input read, every count written
+        for (int x = tid; x < span; x += kSmallBlock) acc[x] = 0;
+        if (tid == 0) {  // exclusive offsets in (round, wave) = ascending order
+            int o = 0;
+            for (int q = 0; q < rounds * NWV; ++q) {
+                const int c = s_cnt[q];
+                s_cnt[q] = o;
+                o += c;
+            }
+            s_total = o;
+            b.ring_cnt[slot] = o;
+        }
+        __syncthreads();
+        const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+#pragma unroll
+        for (int r = 0; r < kSmallRounds; ++r) {
+            if (r >= rounds) continue;
+            const uint64_t m = ballot64(sp[r]);
+            if (sp[r]) list[s_cnt[r * NWV + wave] + __popcll(m & below)] = r * kSmallBlock + tid;
+        }
+        spikes += s_total;
+        __syncthreads();  // the list (global) and the cleared accumulator
+        // (3) delivery of the spikes of step t-D+1 (this step's for D = 1)
+        const int tslot = (int)((t - (b.delay - 1) + (int64_t)b.delay * 64) % b.delay);
+        const int32_t *tlist = b.ring + (int64_t)tslot * n;
+        const int ntx = min(max(b.ring_cnt[tslot], 0), n);
+        for (int q = wave; q < ntx; q += NWV) {  // wave-uniform
+            const int src = min(max(tlist[q], 0), n - 1);
+            const int64_t rs = b.row_ptr[src], re = b.row_ptr[src + 1];
+            const int half = (b.nacc == 2 && src >= b.n_exc) ? n : 0;
+            for (int64_t e = rs + lane; e < re; e += kWave)
+                atomicAdd((unsigned long long *)(acc + b.col[e] + half),
+                          (unsigned long long)to_fix(b.w[e]));
+            if (lane == 0) events += re - rs;
+        }
+        __syncthreads();  // accumulation done before the next step reads it
+    }
+#pragma unroll
+    for (int r = 0; r < kSmallRounds; ++r) {
+        const int i = r * kSmallBlock + tid;
+        if (r < rounds && i < n) {
+            nstate_store<M, H>(a, i, st[r]);
+            a.code[i] = hist_code(st[r].h0, st[r].h1);
+        }
+    }
+    for (int x = tid; x < span; x += kSmallBlock) b.apart[x] = acc[x];
+    if (lane == 0 && events) atomicAdd((unsigned long long *)b.dlv_stats, (unsigned long long)events);
+    if (tid == 0) b.gstats[kGSpikes] += spikes;
+}
+
 // Sorts a list of distinct neuron indices (capacity n entries, values in
 // [0, n)) into ascending order (one workgroup; not on the step's path):
 // scatter into a bitmap of nw = ceil(n/64) words, then read it back in order.
@@ -392,6 +591,20 @@ __global__ __launch_bounds__(kBlock) void k_materialize_input(const long long *a
     ain[i] = from_fix(v);
 }
 
+template <int M, int H>
+hipError_t launch_small(hipStream_t s, const NeuronArgs &a, const SmallArgs &b, size_t lds,
+                        KernelEvents ev)
+{
+    static std::mutex mu;
+    static int granted = 48 * 1024;
+    const hipError_t e =
+        allow_dynamic_lds((const void *)k_small_steps<M, H>, (int)lds, mu, granted);
+    if (e != hipSuccess) return e;
+    hipExtLaunchKernelGGL(k_small_steps<M, H>, dim3(1), dim3(kSmallBlock), lds, s, ev.start,
+                          ev.stop, 0, a, b);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_init_state(hipStream_t s, float *v, int32_t *ref, float *ie, float *ii,
@@ -439,6 +652,21 @@ hipError_t launch_copy_bytes(hipStream_t s, void *dst, const void *src, int64_t 
 {
     if (bytes <= 0) return hipSuccess;
     return hipMemcpyAsync(dst, src, (size_t)bytes, hipMemcpyDeviceToDevice, s);
+}
+
+hipError_t launch_small_steps(hipStream_t s, const NeuronArgs &a, const SmallArgs &b,
+                              KernelEvents ev)
+{
+    const size_t lds = (size_t)b.nacc * a.n * sizeof(long long);
+    const int m = a.model == 1 ? 1 : a.model == 2 ? 2 : 0;
+    switch (m * 2 + (a.hw == 2)) {
+    case 0: return launch_small<0, 1>(s, a, b, lds, ev);
+    case 1: return launch_small<0, 2>(s, a, b, lds, ev);
+    case 2: return launch_small<1, 1>(s, a, b, lds, ev);
+    case 3: return launch_small<1, 2>(s, a, b, lds, ev);
+    case 4: return launch_small<2, 1>(s, a, b, lds, ev);
+    default: return launch_small<2, 2>(s, a, b, lds, ev);
+    }
 }
 
 hipError_t launch_neuron(hipStream_t s, const NeuronArgs &a, const CompactArgs &c,

@@ -389,7 +389,7 @@ KernelEvents part_events(snn_ctx *c, int part)
     return ev;
 }
 
-snn_status launch_step_neurons(snn_ctx *c)
+NeuronArgs neuron_args(snn_ctx *c)
 {
     NeuronArgs a{};
     a.v = c->v;
@@ -428,6 +428,12 @@ snn_status launch_step_neurons(snn_ctx *c)
     a.fire_thr = c->fire_thr;
     a.seed = c->cfg.seed;
     for (int q = 0; q < kMaxPoisson; ++q) a.poisson[q] = c->cfg.poisson_cdf[q];
+    return a;
+}
+
+snn_status launch_step_neurons(snn_ctx *c)
+{
+    NeuronArgs a = neuron_args(c);
     CompactArgs b{};
     b.spk_list = c->ring + (int64_t)ring_slot(c, c->t) * c->n;
     b.spk_cnt = c->ring_cnt + ring_slot(c, c->t);
@@ -995,6 +1001,37 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
     if (n_steps < 0) return fail(c, SNN_EINVAL, "n_steps must be >= 0");
     if (mode != SNN_DELIVER_LDS_SLICE && mode != SNN_DELIVER_GLOBAL_ATOMIC)
         return fail(c, SNN_EINVAL, "unknown delivery mode %d", mode);
+    // a small network without plasticity runs whole steps in one workgroup
+    // (unless kernel times are being recorded per step)
+    const bool small = mode == SNN_DELIVER_LDS_SLICE && c->n_plastic_rows == 0 &&
+                       c->n <= kSmallRounds * kSmallBlock &&
+                       (int64_t)c->nacc * c->n <= kSmallMaxAcc && c->t_used >= c->t_cap;
+    for (int32_t q = 0; small && q < n_steps;) {
+        const int32_t k = std::min<int32_t>(n_steps - q, kSmallChunk);
+        NeuronArgs a = neuron_args(c);
+        SmallArgs b{};
+        b.ring = c->ring;
+        b.ring_cnt = c->ring_cnt;
+        b.delay = c->delay;
+        b.row_ptr = c->row_ptr;
+        b.col = c->col;
+        b.w = c->w;
+        b.apart = c->apart;
+        b.gstats = c->gstats;
+        b.dlv_stats = c->dlv_stats;
+        b.n_exc = c->cfg.n_exc;
+        b.nacc = c->nacc;
+        b.steps = k;
+        if ((st = check_hip(c, launch_small_steps(c->stream, a, b), "small-network steps")))
+            return st;
+        c->t += k;
+        c->steps_done += k;
+        c->last_neuron_t = c->last_deliver_t = c->t - 1;
+        c->n_parts = 1;
+        c->input_forced = 0;
+        q += k;
+    }
+    if (small) return SNN_OK;
     for (int32_t q = 0; q < n_steps; ++q) {
         if ((st = launch_step_neurons(c))) return st;
         if ((st = launch_step_plasticity(c))) return st;

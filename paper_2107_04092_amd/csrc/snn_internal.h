@@ -214,6 +214,26 @@ struct GraphArgs {
     float w_exc, w_inh;
 };
 
+// Several whole steps of a small network without plasticity in one launch of
+// one workgroup (k_small_steps): neuron update, spike list into the delay
+// ring, and delivery into an LDS accumulator that the next step's neuron
+// update reads, so no step waits for a kernel boundary or an HBM round trip.
+struct SmallArgs {
+    int32_t *ring, *ring_cnt;   // delay ring: D lists of n, D counts
+    int32_t delay;
+    const int64_t *row_ptr;
+    const int32_t *col;
+    const float *w;
+    long long *apart;           // after the last step: part 0 = the pending input
+    int64_t *gstats;            // kGSpikes
+    int64_t *dlv_stats;         // slot 0: events delivered
+    int32_t n_exc, nacc, steps;
+};
+constexpr int kSmallBlock = 1024;
+constexpr int kSmallRounds = 4;     // neurons per thread: n <= 4096
+constexpr int kSmallMaxAcc = 8192;  // nacc * n accumulators (64 KiB of LDS)
+constexpr int kSmallChunk = 4096;   // steps per launch
+
 // Optional events placed by a launch itself around the kernel
 // (hipExtLaunchKernelGGL): its device time without marker or dispatch gaps.
 struct KernelEvents {
@@ -232,6 +252,9 @@ hipError_t launch_fill_i64(hipStream_t s, int64_t *p, int64_t count, int64_t val
 hipError_t launch_fill_i32(hipStream_t s, int32_t *p, int64_t count, int32_t value);
 hipError_t launch_fill_ll(hipStream_t s, long long *p, int64_t count, long long value);
 hipError_t launch_copy_bytes(hipStream_t s, void *dst, const void *src, int64_t bytes);
+// k_small_steps: steps a.t .. a.t + b.steps - 1 (a describes step a.t)
+hipError_t launch_small_steps(hipStream_t s, const NeuronArgs &a, const SmallArgs &b,
+                              KernelEvents ev = {});
 hipError_t launch_neuron(hipStream_t s, const NeuronArgs &a, const CompactArgs &b,
                          KernelEvents ev = {});
 // sorts list[0 .. min(*cnt, n)) (distinct values in [0, n)) in place and,

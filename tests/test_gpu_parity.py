@@ -97,6 +97,46 @@ def test_three_part_calls_equal_step():
     assert np.array_equal(to_np(a.graph()["w"]), to_np(b.graph()["w"]))
 
 
+SMALL_CASES = [
+    ("tiny", dict()),
+    ("tiny", dict(n=1037, n_exc=830, delay=3)),
+    ("vogels", dict()),
+    ("stress", dict(n=3000, p_or_fanout=50, p_fire=0.03, plastic=PLASTIC_NONE, delay=2)),
+]
+
+
+@pytest.mark.parametrize("case", SMALL_CASES, ids=lambda c: "%s-%s" % (c[0], c[1].get("n", "")))
+def test_small_network_steps_equal_three_part_calls(case):
+    """Small networks without plasticity run several steps per launch in one
+    workgroup (the input carried in LDS between steps): states, delay ring and
+    statistics equal those of the separate kernels, bit for bit."""
+    name, kw = case
+    p = wl.preset(name, **kw)
+    a = gpu_net(p)
+    b = gpu_net(p)
+    for k in (1, 37, 63):  # several launches, the first of a single step
+        a.step(k, LDS)
+        for _ in range(k):
+            b.update_neurons()
+            b.update_plasticity()
+            b.deliver_spikes(LDS)
+            b.advance()
+    sa, sb = a.state(), b.state()
+    for key in ("v", "refractory", "i_exc", "i_inh", "hist", "input_exc", "input_inh",
+                "spike_mask", "ring_counts"):
+        if sa[key] is None:
+            continue
+        assert np.array_equal(to_np(sa[key]), to_np(sb[key])), key
+    ra, rb = to_np(sa["ring_lists"]).reshape(p.delay, -1), to_np(sb["ring_lists"]).reshape(
+        p.delay, -1)
+    for q, c in enumerate(to_np(sa["ring_counts"])):  # entries past a count are stale
+        assert np.array_equal(ra[q, :c], rb[q, :c]), ("ring slot", q)
+    ta, tb = a.stats(), b.stats()
+    for key in ("steps", "spikes", "delivered_events"):
+        assert ta[key] == tb[key], key
+    assert ta["spikes"] > 0
+
+
 def test_out_of_order_calls_rejected():
     p = wl.preset("stress", n=500, p_or_fanout=10, p_fire=0.03)
     net = gpu_net(p, slice_width=128)

@@ -27,6 +27,7 @@ def _free_run(p, steps, mode, chunk=5000):
 
 
 @pytest.mark.parametrize("name,kw,steps,mode", [
+    ("tiny", dict(), 100_000, snn.SNN_DELIVER_LDS_SLICE),
     ("vogels", dict(), 100_000, snn.SNN_DELIVER_LDS_SLICE),
     ("brunel_plus", dict(n=2500, n_exc=2000, slice_width=512), 10_000,
      snn.SNN_DELIVER_LDS_SLICE),
