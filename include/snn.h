@@ -307,7 +307,14 @@ snn_status snn_deliver_spikes(snn_ctx *ctx, int32_t mode);
 snn_status snn_advance(snn_ctx *ctx);
 
 /* n_steps full steps: parts (1), (2), (3) with delivery mode, then advance.
- * Enqueues only; never synchronises. */
+ * Enqueues only; never synchronises. The result equals that of the separate
+ * part calls in every state and statistic; with SNN_DELIVER_LDS_SLICE and
+ * no kernel times being recorded, networks without plasticity take fewer
+ * launches: up to 4096 neurons run many steps in one workgroup, and with
+ * D >= 2 the inputs of up to D-1 steps (at most 16; 8 for CUBA) come from
+ * spikes already in the delay ring, so one delivery launch computes them
+ * all before one neuron launch runs those steps (Sec. I: the input of step
+ * t depends on the spikes of step t-D only). */
 snn_status snn_step(snn_ctx *ctx, int32_t n_steps, int32_t mode);
 
 /* Kernel timing for profiling. After this call the next max_steps steps run

@@ -135,6 +135,20 @@ __device__ __forceinline__ void neuron_input(const NeuronArgs &a, int i, float &
     }
 }
 
+// The external Poisson count of neuron i at step t: the number of CDF
+// thresholds at or below one 32-bit draw (inversion). Unrolled over the
+// table's capacity, so the thresholds are loaded once, not waited for inside
+// a loop.
+__device__ __forceinline__ int poisson_count(const NeuronArgs &a, int64_t t, int i)
+{
+    const uint32_t u = rng32(a.seed, 3, (uint64_t)t, (uint64_t)i);
+    int k = 0;
+#pragma unroll
+    for (int q = 0; q < kMaxPoisson; ++q)
+        if (q < a.poisson_len) k += (a.poisson[q] <= u);
+    return k;
+}
+
 // One neuron's update at step t (i < n) on its state in registers, with
 // input (ae, ai): its dynamics in a fixed fp32 operation order, its post
 // trace and its history words. Returns whether it spiked.
@@ -174,10 +188,7 @@ __device__ __forceinline__ int neuron_advance(const NeuronArgs &a, int i, int64_
             } else {
                 float x = 0.f;
                 if (a.poisson_len > 0) {
-                    const uint32_t u = rng32(a.seed, 3, (uint64_t)t, (uint64_t)i);
-                    int k = 0;
-                    for (int q = 0; q < a.poisson_len; ++q) k += (a.poisson[q] <= u);
-                    x = __fmul_rn(a.j_ext, (float)k);
+                    x = __fmul_rn(a.j_ext, (float)poisson_count(a, t, i));
                 }
                 const float d = __fsub_rn(a.v_inf, v);
                 const float b = __fmul_rn(d, a.k_m);
@@ -528,6 +539,129 @@ __global__ __launch_bounds__(kSmallBlock) void k_small_steps(NeuronArgs a, Small
     if (tid == 0) b.gstats[kGSpikes] += spikes;
 }
 
+// ---------------------------------------------------------------------------
+// Delay block of a network without plasticity: b.steps (<= D-1) steps of the
+// neuron update, one neuron per thread with its state in registers. Step
+// a.t reads its input like k_neuron (forced input or the partial sums in
+// apart); step a.t + k, k >= 1, reads slot k-1 of abatch, the whole input
+// as one fixed-point sum, written beforehand by the batched delivery. Every
+// slot's load is issued before the first step, so the steps wait for one
+// round trip in all. The spike flags of every step are kept (a bit per step
+// per thread, ballots in LDS), and the spike lists go into the delay ring at
+// the end: one packed reservation per workgroup and step (counts in bits
+// 0-23, a ticket in bits 48-63; the workgroup whose ticket comes last
+// publishes the count and clears the word), the B reservations of a
+// workgroup in flight together. The masks, codes and the state written are
+// those of the last step, and apart part 0 receives slot B-1, the pending
+// input of the next step. Workgroups of 512 threads: the B steps of a
+// thread run one after another, so fewer waves share a SIMD than with 1024,
+// and half as many reservations queue per step as with 256.
+constexpr int kStepsBlock = 512;
+static_assert((1 << 24) / kStepsBlock <= 65536, "workgroup ticket must fit in 16 bits");
+template <int M, int H>
+__global__ __launch_bounds__(kStepsBlock) void k_neuron_steps(NeuronArgs a, BatchArgs b)
+{
+    constexpr int NWV = kStepsBlock / kWave;
+    __shared__ uint64_t s_m[kBatchMax][NWV];
+    __shared__ int s_off[kBatchMax];
+    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const int n = a.n;
+    const int i = blockIdx.x * kStepsBlock + tid;
+    const bool live = i < n;
+    const int ic = live ? i : 0;
+    const int64_t ps = a.part_stride;  // nacc * n
+    // steps per launch: CUBA holds two inputs per step in registers
+    constexpr int KB = batch_steps_max(M);
+    const int B = b.steps;  // 1 .. KB (checked by the launcher)
+    // slot k = input of step a.t + k + 1 (Bernoulli sources read only the
+    // last). Every load is issued unconditionally from a valid slot (past B:
+    // slot B-1 again): a load under a branch would be waited for inside it.
+    long long pe[KB], pi[KB];
+#pragma unroll
+    for (int k = 0; k < KB; ++k) {
+        const int kk = M == 2 ? B - 1 : min(k, B - 1);
+        const long long *p = b.abatch + (int64_t)kk * ps;
+        pe[k] = M == 2 && k > 0 ? 0 : p[ic];
+        pi[k] = M == 1 ? p[n + ic] : 0;
+    }
+    NState st = {};
+    if (live) nstate_load<M, H>(a, i, st);
+    uint32_t fired = 0;
+#pragma unroll
+    for (int k = 0; k < KB; ++k) {
+        if (k >= B) break;
+        float ae = 0.f, ai = 0.f;
+        if (live && M != 2) {
+            if (k == 0) {
+                neuron_input(a, i, ae, ai);
+            } else {
+                ae = from_fix(pe[k - 1]);
+                if (M == 1) ai = from_fix(pi[k - 1]);
+            }
+        }
+        int sp = 0;
+        if (live) sp = neuron_advance<M, H>(a, i, a.t + k, ae, ai, st);
+        fired |= (uint32_t)sp << k;
+        const uint64_t m = ballot64(sp);
+        if (lane == 0) s_m[k][wave] = m;
+    }
+    if (live) {
+        nstate_store<M, H>(a, i, st);
+        a.code[i] = hist_code(st.h0, st.h1);
+        long long le = pe[0], li = pi[0];  // Bernoulli sources: slot B-1 is pe[0]
+        if (M != 2) {
+#pragma unroll
+            for (int k = 1; k < KB; ++k) {
+                if (k == B - 1) {
+                    le = pe[k];
+                    li = pi[k];
+                }
+            }
+        }
+        b.apart[i] = le;
+        if (M == 1) b.apart[n + i] = li;
+    }
+    {
+        const uint64_t m = ballot64(live && ((fired >> (B - 1)) & 1u));
+        const uint64_t txm = ballot64(live && ((st.h0 >> a.dm1) & 1ull));
+        const uint64_t rcm = ballot64(live && (st.h0 | st.h1) != 0ull);
+        const int64_t word = (int64_t)blockIdx.x * NWV + wave;
+        if (lane == 0 && word * kWave < n) {
+            a.mask[word] = m;
+            a.txmask[word] = txm;
+            a.recent[word] = rcm;
+        }
+    }
+    __syncthreads();  // every step's ballots
+    if (tid < B) {
+        const int k = tid;
+        int cnt = 0;
+        for (int w = 0; w < NWV; ++w) cnt += __popcll(s_m[k][w]);
+        const unsigned long long old =
+            atomicAdd(b.acc + k * kAccStride, (unsigned long long)cnt | (1ull << 48));
+        s_off[k] = (int)(old & 0xffffffull);
+        if ((int)(old >> 48) == (int)gridDim.x - 1) {
+            const int total = (int)(old & 0xffffffull) + cnt;
+            (void)atomicExch(b.acc + k * kAccStride, 0ull);
+            const int64_t d = b.delay;
+            b.ring_cnt[(int)((a.t + k) % d)] = total;
+            atomicAdd((unsigned long long *)(b.gstats + kGSpikes), (unsigned long long)total);
+        }
+    }
+    __syncthreads();  // every offset
+    const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+    for (int k = 0; k < B; ++k) {
+        if (!((fired >> k) & 1u)) continue;
+        int pos = s_off[k] + __popcll(s_m[k][wave] & below);
+        for (int w = 0; w < wave; ++w) pos += __popcll(s_m[k][w]);
+        // (only an accumulator left non-zero by a failed launch is out of range)
+        if (pos < n)
+            b.ring[(int64_t)((a.t + k) % b.delay) * n + pos] = i;
+        else
+            atomicOr(b.err, kErrRing);
+    }
+}
+
 // Sorts a list of distinct neuron indices (capacity n entries, values in
 // [0, n)) into ascending order (one workgroup; not on the step's path):
 // scatter into a bitmap of nw = ceil(n/64) words, then read it back in order.
@@ -589,6 +723,14 @@ __global__ __launch_bounds__(kBlock) void k_materialize_input(const long long *a
     long long v = apart[i];
     for (int c = 1; c < parts; ++c) v += apart[c * stride + i];
     ain[i] = from_fix(v);
+}
+
+template <int M, int H>
+hipError_t launch_steps(hipStream_t s, const NeuronArgs &a, const BatchArgs &b)
+{
+    hipLaunchKernelGGL((k_neuron_steps<M, H>), dim3(blocks_for(a.n, kStepsBlock)),
+                       dim3(kStepsBlock), 0, s, a, b);
+    return hipGetLastError();
 }
 
 template <int M, int H>
@@ -666,6 +808,20 @@ hipError_t launch_small_steps(hipStream_t s, const NeuronArgs &a, const SmallArg
     case 3: return launch_small<1, 2>(s, a, b, lds, ev);
     case 4: return launch_small<2, 1>(s, a, b, lds, ev);
     default: return launch_small<2, 2>(s, a, b, lds, ev);
+    }
+}
+
+hipError_t launch_neuron_steps(hipStream_t s, const NeuronArgs &a, const BatchArgs &b)
+{
+    const int m = a.model == 1 ? 1 : a.model == 2 ? 2 : 0;
+    if (b.steps < 1 || b.steps > batch_steps_max(m)) return hipErrorInvalidValue;
+    switch (m * 2 + (a.hw == 2)) {
+    case 0: return launch_steps<0, 1>(s, a, b);
+    case 1: return launch_steps<0, 2>(s, a, b);
+    case 2: return launch_steps<1, 1>(s, a, b);
+    case 3: return launch_steps<1, 2>(s, a, b);
+    case 4: return launch_steps<2, 1>(s, a, b);
+    default: return launch_steps<2, 2>(s, a, b);
     }
 }
 

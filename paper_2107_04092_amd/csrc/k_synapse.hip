@@ -196,12 +196,16 @@ __global__ __launch_bounds__(kStdpBlock) void k_stdp(StdpArgs a)
 // Rows with a pre spike (transmitting rows, in the global-atomic delivery
 // mode) need every target's post trace and gather histories and traces.
 //
-// Parts start at 64-byte lines of the weight array, and a line that holds a
+// Parts start at 128-byte lines of the weight array, and a line that holds a
 // changed weight is stored whole (its unchanged weights included), so the
 // L2 writes no partial line back to HBM. Two parts are held per wave: the
 // targets and weights of one are loaded while the other is looked up,
 // updated and stored (both are in flight from the start); the next row's
 // snapshot is fetched one part ahead.
+
+// Weights per store line: 32 fp32 = one 128-byte L2 line.
+constexpr int kStoreLine = 32;
+constexpr uint64_t kLineMask = (1ull << kStoreLine) - 1;
 
 template <int U>
 struct RowPart {
@@ -272,7 +276,7 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
     const float *__restrict__ ypost = a.ypost;
     const float c_pot = a.c_pot, c_dep = a.c_dep, mu = a.mu;
     const int lane = tid % kWave;
-    const int line0 = lane & ~15;  // first lane of this lane's 16-weight line
+    const int line0 = lane & ~(kStoreLine - 1);  // first lane of this lane's store line
     const int gw = (bid * NT + tid) / kWave;
     const int nwv = nblocks * (NT / kWave);
     const int nrows = a.row_cnt ? *a.row_cnt : a.n_rows_all;
@@ -291,7 +295,7 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
     int cur_i = gw, la_i = gw + nwv;
     if (cur_i < npairs) cur = a.info[row_of(cur_i)];
     if (la_i < npairs) la = a.info[row_of(la_i)];
-    int cur_base = -(int)(cur.rs & 15) + phase_of(cur_i) * (U * kWave);
+    int cur_base = -(int)(cur.rs & (kStoreLine - 1)) + phase_of(cur_i) * (U * kWave);
     auto issue = [&](RowPart<U> &p) {
         p.ri = cur;
         p.i = cur_i;
@@ -301,7 +305,7 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
             cur_base += P * U * kWave;
         } else {  // the lookahead pair
             cur = la;
-            cur_base = -(int)(la.rs & 15) + phase_of(la_i) * (U * kWave);
+            cur_base = -(int)(la.rs & (kStoreLine - 1)) + phase_of(la_i) * (U * kWave);
             cur_i = la_i;
             la_i += nwv;
             la = RowInfo{};
@@ -429,7 +433,7 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
             }
         }
         __builtin_amdgcn_wave_barrier();
-        if (ri.age_pre != 0 && p.base == -(int)(ri.rs & 15) && lane == 0) {  // first part
+        if (ri.age_pre != 0 && p.base == -(int)(ri.rs & (kStoreLine - 1)) && lane == 0) {  // first part
             a.t_last[ri.k] = (int32_t)a.t;
             a.xpre[ri.k] = ri.xp_now;
         }
@@ -444,7 +448,7 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
             const float w = c ? rw : p.w[u];
             const int qi = p.base + u * kWave + lane;
             const uint64_t m = ballot64(chg);
-            if (((m >> line0) & 0xffffull) && qi >= 0 && qi < len)
+            if (((m >> line0) & kLineMask) && qi >= 0 && qi < len)
                 __builtin_nontemporal_store(w, wgt + ri.rs + qi);
         }
         issue(p);
@@ -599,8 +603,24 @@ __global__ __launch_bounds__(kDlvBlock, 4) void k_deliver_lds(DeliverArgs a)
     __shared__ int s_nlong;
     const int tid = threadIdx.x;
     const int nb = gridDim.x;  // multiple of 8
-    const int q = (blockIdx.x & 7) * (nb >> 3) + (blockIdx.x >> 3);
-    if (q >= a.n_work) return;  // whole workgroup, before any barrier
+    const int qa = (blockIdx.x & 7) * (nb >> 3) + (blockIdx.x >> 3);
+    if (qa >= a.n_work) return;  // whole workgroup, before any barrier
+    // a delay block's item (b, slice, chunk) takes step b's ring list and
+    // writes partial sums of step b (b varies slowest: an XCD's range of
+    // items covers neighbouring slices)
+    const int32_t *list = a.list, *cntp = a.cnt;
+    long long *parts = a.apart;
+    int q = qa;
+    if (a.batch > 0) {
+        const int per = a.n_slices * a.chunks;
+        const int bb = qa / per;
+        q = qa - bb * per;
+        const int64_t d = a.delay;
+        const int slot = (int)(((a.t_emit0 + bb) % d + d) % d);
+        list = a.ring + (int64_t)slot * a.n;
+        cntp = a.ring_cnt + slot;
+        parts = a.abatch + (int64_t)bb * a.chunks * a.part_stride;
+    }
     const int s = q / a.chunks, c = q - s * a.chunks;
     const int C = a.chunks;
     const int base = s * a.width;
@@ -613,9 +633,9 @@ __global__ __launch_bounds__(kDlvBlock, 4) void k_deliver_lds(DeliverArgs a)
         if (a.plastic)
             ri0 = a.txinfo[c + C * tid];
         else
-            k0 = a.list[c + C * tid];
+            k0 = list[c + C * tid];
     }
-    const int cnt = *a.cnt;  // used only once the first batch's loads are out
+    const int cnt = *cntp;  // used only once the first batch's loads are out
     const int hw = a.hw;
     const int jn = min(a.width, a.n - base);  // > 0
     // the slice's histories and post traces: loads out now, stored below
@@ -666,7 +686,7 @@ __global__ __launch_bounds__(kDlvBlock, 4) void k_deliver_lds(DeliverArgs a)
                 p0 = p0p;
                 p1 = p1p;
             } else {
-                k = min(max(a.plastic ? ri.k : a.list[r], 0), a.n - 1);  // past the count: stale
+                k = min(max(a.plastic ? ri.k : list[r], 0), a.n - 1);  // past the count: stale
                 const int32_t *pv = a.piv + (int64_t)k * piv_stride + s;
                 p0 = pv[0];
                 p1 = pv[1];
@@ -786,7 +806,7 @@ __global__ __launch_bounds__(kDlvBlock, 4) void k_deliver_lds(DeliverArgs a)
         a.stats[2 * (int64_t)blockIdx.x] += ev;
         a.stats[2 * (int64_t)blockIdx.x + 1] += (int64_t)s_written;
     }
-    if (a.chunks == 1) {
+    if (a.chunks == 1 && a.batch == 0) {
         for (int x = tid; x < a.width; x += kDlvBlock) {
             const int j = base + x;
             if (j < a.n) {
@@ -795,7 +815,7 @@ __global__ __launch_bounds__(kDlvBlock, 4) void k_deliver_lds(DeliverArgs a)
             }
         }
     } else {
-        long long *out = a.apart + (int64_t)c * a.part_stride;
+        long long *out = parts + (int64_t)c * a.part_stride;
         for (int x = tid; x < a.width; x += kDlvBlock) {
             const int j = base + x;
             if (j < a.n) {

@@ -64,6 +64,9 @@ struct snn_ctx {
     int64_t *gstats = nullptr, *info_stats = nullptr, *syn_stats = nullptr, *dlv_stats = nullptr;
     RowInfo *info = nullptr, *txinfo = nullptr;
     int32_t dlv_slots = 0;
+    // delay blocks (no plasticity, D >= 2): steps per block, partial inputs
+    int32_t batch_max = 0;
+    long long *abatch = nullptr;  // [batch_max][C][nacc][n]
 
     // graph
     uint8_t *g = nullptr;
@@ -220,6 +223,19 @@ void derive(snn_ctx *c)
     const int64_t work = (int64_t)c->n_slices * c->chunks;
     c->dlv_blocks = (int32_t)((work + 7) / 8 * 8);
     c->dlv_slots = c->dlv_blocks > kGlobalMaxBlocks ? c->dlv_blocks : kGlobalMaxBlocks;
+    // Delay blocks of up to D-1 steps, their inputs within kBatchBytes of
+    // workspace (none for plastic networks or D = 1). A block's delivery
+    // item is (step, slice) with one chunk: the steps give the parallelism.
+    c->batch_max = 0;
+    if (k.plastic == SNN_PLASTIC_NONE && c->delay >= 2) {
+        const int64_t per_step = (int64_t)c->nacc * c->n * (int64_t)sizeof(long long);
+        int64_t bm = std::min<int64_t>(c->delay - 1, batch_steps_max(k.neuron_model));
+        bm = std::min<int64_t>(bm, kBatchBytes / per_step);
+        if (bm * c->n_slices > (1 << 24)) bm = 0;
+        c->batch_max = (int32_t)std::max<int64_t>(bm, 0);
+        const int64_t bb = (c->batch_max * c->n_slices + 7) / 8 * 8;
+        if (bb > c->dlv_slots) c->dlv_slots = (int32_t)bb;
+    }
     c->info_blocks = c->nblk;  // statistics slots of the neuron-kernel / flush snapshots
 }
 
@@ -254,7 +270,7 @@ void plan_workspace(snn_ctx *c, uint8_t *base)
     c->txmask = p.take<uint64_t>(c->nw);
     c->code = p.take<uint8_t>((int64_t)c->n + 16);
     c->recent = p.take<uint64_t>(c->nw);
-    c->list_acc = p.take<unsigned long long>(1);
+    c->list_acc = p.take<unsigned long long>((int64_t)kBatchMax * kAccStride);
     c->spk_pos = p.take<int32_t>(c->delay > 1 ? (int64_t)c->delay * n : 1);
     c->ring = p.take<int32_t>((int64_t)c->delay * n);
     c->ring_cnt = p.take<int32_t>(c->delay);
@@ -272,6 +288,7 @@ void plan_workspace(snn_ctx *c, uint8_t *base)
     c->info_stats = p.take<int64_t>((int64_t)c->info_blocks * kStFields);
     c->syn_stats = p.take<int64_t>(c->syn_slots);
     c->dlv_stats = p.take<int64_t>(2 * (int64_t)c->dlv_slots);
+    c->abatch = p.take<long long>(c->batch_max > 0 ? (int64_t)c->batch_max * c->nacc * n : 1);
     c->ws_need = p.off;
 }
 
@@ -785,7 +802,8 @@ snn_status snn_bind_workspace(snn_ctx *c, void *device_ptr, size_t bytes)
     if (e == hipSuccess) e = launch_fill_f32(c->stream, c->ain, (int64_t)c->nacc * c->n, 0.f);
     if (e == hipSuccess) e = launch_fill_i32(c->stream, c->ring_cnt, c->delay, 0);
     if (e == hipSuccess) e = launch_fill_i32(c->stream, c->row_cnt, 1, 0);
-    if (e == hipSuccess) e = launch_fill_i64(c->stream, (int64_t *)c->list_acc, 1, 0);
+    if (e == hipSuccess) e = launch_fill_i64(c->stream, (int64_t *)c->list_acc,
+                                                (int64_t)kBatchMax * kAccStride, 0);
     if (e == hipSuccess) e = launch_fill_i32(c->stream, c->err_flag, 1, 0);
     if (e == hipSuccess) e = launch_fill_i32(c->stream, c->pend, c->n, 0);
     snn_status st = check_hip(c, e, "workspace initialisation");
@@ -1032,6 +1050,46 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
         q += k;
     }
     if (small) return SNN_OK;
+    // a network without plasticity and D >= 2 runs in delay blocks (see
+    // BatchArgs): one delivery launch for the inputs of steps t+1 .. t+B,
+    // then one neuron launch for steps t .. t+B-1
+    const bool blocks = mode == SNN_DELIVER_LDS_SLICE && c->batch_max > 0 && c->t_used >= c->t_cap;
+    for (int32_t q = 0; blocks && q < n_steps;) {
+        const int32_t B = std::min<int32_t>(n_steps - q, c->batch_max);
+        DeliverArgs d = deliver_args(c);
+        d.batch = B;
+        d.delay = c->delay;
+        d.t_emit0 = c->t + 1 - c->delay;
+        d.ring = c->ring;
+        d.ring_cnt = c->ring_cnt;
+        d.abatch = c->abatch;
+        d.chunks = 1;
+        d.n_work = B * c->n_slices;
+        const int grid = (d.n_work + 7) / 8 * 8;
+        if ((st = check_hip(c, launch_deliver_lds(c->stream, d, grid, dlv_lds_bytes(c)),
+                            "delay-block delivery")))
+            return st;
+        NeuronArgs a = neuron_args(c);
+        BatchArgs b{};
+        b.ring = c->ring;
+        b.ring_cnt = c->ring_cnt;
+        b.delay = c->delay;
+        b.acc = c->list_acc;
+        b.abatch = c->abatch;
+        b.apart = c->apart;
+        b.gstats = c->gstats;
+        b.err = c->err_flag;
+        b.steps = B;
+        if ((st = check_hip(c, launch_neuron_steps(c->stream, a, b), "delay-block neurons")))
+            return st;
+        c->t += B;
+        c->steps_done += B;
+        c->last_neuron_t = c->last_deliver_t = c->t - 1;
+        c->n_parts = 1;
+        c->input_forced = 0;
+        q += B;
+    }
+    if (blocks) return SNN_OK;
     for (int32_t q = 0; q < n_steps; ++q) {
         if ((st = launch_step_neurons(c))) return st;
         if ((st = launch_step_plasticity(c))) return st;

@@ -74,7 +74,7 @@ struct RowInfo;
 // The lists k_neuron builds: spikes of step t (into the delay ring), forced
 // plastic rows, and the snapshots of the rows to update at t. Each workgroup
 // reserves its stretch of every list with one atomic add per list, so a list
-// is ascending within each workgroup's 256 neurons, the stretches in any
+// is ascending within each workgroup's neurons, the stretches in any
 // order; the last workgroup to finish publishes the counts and resets the
 // accumulators for the next step.
 struct CompactArgs {
@@ -171,6 +171,15 @@ struct DeliverArgs {
     int32_t n, n_exc, width, n_slices, chunks, nacc, n_work, hw;
     const uint16_t *col16;   // compressed targets: slice-local indices (nullptr: read `col`)
     int64_t *stats;          // [gridDim.x][2]: events delivered, weights written
+    // delay block (no plasticity): batch > 0 delivers the spikes of steps
+    // t_emit0 .. t_emit0 + batch - 1 from the delay ring, work item
+    // (b, slice, chunk) writing fixed-point partial c of step b to abatch
+    // (list and cnt unused; the host passes one chunk, so each item writes
+    // the whole sum); n_work counts all batch items
+    int32_t batch, delay;
+    int64_t t_emit0;
+    const int32_t *ring, *ring_cnt;
+    long long *abatch;       // [batch][chunks][nacc][n]
     // plasticity of the transmitting rows, fused into slice delivery
     int32_t plastic;         // 0: no plastic rows
     int32_t event;           // as in StdpArgs
@@ -234,6 +243,33 @@ constexpr int kSmallRounds = 4;     // neurons per thread: n <= 4096
 constexpr int kSmallMaxAcc = 8192;  // nacc * n accumulators (64 KiB of LDS)
 constexpr int kSmallChunk = 4096;   // steps per launch
 
+// Delay-blocked steps of a network without plasticity and delay D >= 2
+// (k_neuron_steps after a batched k_deliver_lds). The input of step t comes
+// from the spikes of step t-D only, so the inputs of steps t0+1 .. t0+B
+// (B <= D-1) depend on spikes already in the delay ring when step t0
+// starts: one delivery launch computes all B of them, then one neuron
+// launch runs steps t0 .. t0+B-1, each thread keeping its neuron's state in
+// registers across the B steps.
+struct BatchArgs {
+    int32_t *ring, *ring_cnt;   // delay ring: D lists of n, D counts
+    int32_t delay;
+    unsigned long long *acc;    // [kBatchMax][kAccStride] packed list reservations (word 0 of
+                                // each row), 0 between launches
+    const long long *abatch;    // [B][nacc][n] fixed-point inputs of steps t0+1 .. t0+B
+    long long *apart;           // partial 0 receives the input of step t0+B
+    int64_t *gstats;            // kGSpikes
+    int32_t *err;
+    int32_t steps;
+};
+constexpr int kBatchMax = 16;  // steps per delay block
+// words between the list reservations of successive block steps: each in a
+// 4 KiB page of its own, so the steps' atomics do not queue on one address
+// range
+constexpr int kAccStride = 512;
+// steps per delay block for neuron model m (CUBA: two inputs per step)
+constexpr int batch_steps_max(int m) { return m == 1 ? kBatchMax / 2 : kBatchMax; }
+constexpr int64_t kBatchBytes = 256ll << 20;  // most workspace for a block's partial inputs
+
 // Optional events placed by a launch itself around the kernel
 // (hipExtLaunchKernelGGL): its device time without marker or dispatch gaps.
 struct KernelEvents {
@@ -257,6 +293,8 @@ hipError_t launch_small_steps(hipStream_t s, const NeuronArgs &a, const SmallArg
                               KernelEvents ev = {});
 hipError_t launch_neuron(hipStream_t s, const NeuronArgs &a, const CompactArgs &b,
                          KernelEvents ev = {});
+// k_neuron_steps: steps a.t .. a.t + b.steps - 1 (a describes step a.t)
+hipError_t launch_neuron_steps(hipStream_t s, const NeuronArgs &a, const BatchArgs &b);
 // sorts list[0 .. min(*cnt, n)) (distinct values in [0, n)) in place and,
 // when pos is given, sets pos[list[r]] = r; bitmap: ceil(n/64) words of
 // device scratch

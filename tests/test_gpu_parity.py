@@ -137,6 +137,73 @@ def test_small_network_steps_equal_three_part_calls(case):
     assert ta["spikes"] > 0
 
 
+DELAY_BLOCK_CASES = [
+    # name, preset overrides, slice width, chunks
+    ("brunel", dict(n=8000, n_exc=6400), 1024, 4),               # D = 15: blocks of 14
+    ("brunel", dict(n=8000, n_exc=6400, delay=2), 512, 1),       # blocks of 1, one chunk
+    ("brunel", dict(n=6000, n_exc=4800, delay=24), 1024, 3),     # blocks of 16 (the cap)
+    ("vogels", dict(n=6000, n_exc=4800, delay=4), 1024, 2),      # CUBA: two accumulators
+    ("vogels", dict(n=5000, n_exc=4000, delay=12), 512, 1),      # CUBA: blocks of 8 (its cap)
+    ("stress", dict(n=9000, p_or_fanout=60, p_fire=0.02, plastic=PLASTIC_NONE, delay=5),
+     2048, 4),
+]
+
+
+@pytest.mark.parametrize("hbits", [64, 128], ids=["h64", "h128"])
+@pytest.mark.parametrize("case", DELAY_BLOCK_CASES,
+                         ids=lambda c: "%s-%s-d%s" % (c[0], c[1].get("n", ""), c[1].get("delay", "")))
+def test_delay_blocks_equal_three_part_calls(case, hbits):
+    """Networks without plasticity and D >= 2 run in delay blocks (one
+    delivery launch for up to D-1 steps' inputs, then one neuron launch for
+    those steps): states, delay ring and statistics equal those of the
+    separate kernels, bit for bit, across blocks cut short by the step count."""
+    name, kw, width, chunks = case
+    p = wl.preset(name, **kw)
+    log("delay blocks %s %s W=%d C=%d history=%d" % (name, kw, width, chunks, hbits))
+    a = gpu_net(p, slice_width=width, spike_chunks=chunks, history_bits=hbits)
+    b = gpu_net(p, slice_width=width, spike_chunks=chunks, history_bits=hbits)
+    for k in (1, 37, 63):
+        a.step(k, LDS)
+        for _ in range(k):
+            b.update_neurons()
+            b.update_plasticity()
+            b.deliver_spikes(LDS)
+            b.advance()
+        sa, sb = a.state(), b.state()
+        for key in ("v", "refractory", "i_exc", "i_inh", "hist", "input_exc", "input_inh",
+                    "spike_mask", "ring_counts"):
+            if sa[key] is None:
+                continue
+            assert np.array_equal(to_np(sa[key]), to_np(sb[key])), (key, k)
+        ra = to_np(sa["ring_lists"]).reshape(p.delay, -1)
+        rb = to_np(sb["ring_lists"]).reshape(p.delay, -1)
+        for q, c in enumerate(to_np(sa["ring_counts"])):
+            assert np.array_equal(ra[q, :c], rb[q, :c]), ("ring slot", q)
+    ta, tb = a.stats(), b.stats()
+    for key in ("steps", "spikes", "delivered_events", "device_errors"):
+        assert ta[key] == tb[key], key
+    assert ta["spikes"] > 0 and ta["delivered_events"] > 0
+    assert ta["device_errors"] == 0
+
+
+def test_delay_blocks_free_run_matches_oracle():
+    """A Brunel network with 15-step delays runs free in delay blocks. Its
+    weights (0.1 and -0.5 in fp32) sum exactly in both the fixed-point and the
+    double accumulation, so the free run stays bit-exact: after every chunk,
+    spikes, histories and potentials equal the oracle's, and the pending input
+    is within the delivery tolerance."""
+    p = wl.preset("brunel", n=5000, n_exc=4000)
+    net = gpu_net(p, slice_width=1024, spike_chunks=2)
+    o = oracle_net(p)
+    t = 0
+    for chunk in (14, 29, 3, 50):
+        net.step(chunk, LDS)
+        o.step(chunk)
+        t += chunk
+        compare_step(net, o, "delay blocks", t, check_rows=False)
+    assert net.stats()["spikes"] > 0
+
+
 def test_out_of_order_calls_rejected():
     p = wl.preset("stress", n=500, p_or_fanout=10, p_fire=0.03)
     net = gpu_net(p, slice_width=128)
