@@ -240,12 +240,17 @@ __device__ __forceinline__ void neuron_update(const NeuronArgs &a, int i, int64_
     if (i < a.n_plastic_rows) forced = !tx && (t - (int64_t)a.t_last[i] >= 64 * a.hw);
 }
 
-static_assert((1 << 24) / (kNeuronBlock * kNeuronRounds) <= 65536,
-              "workgroup ticket must fit in 16 bits");
-
-__global__ __launch_bounds__(kNeuronBlock) void k_neuron(NeuronArgs a, CompactArgs lst)
+// NB threads per workgroup: 1024 on large networks (one list reservation
+// per workgroup; same-address atomics serialise), 256 up to kNeuronSmallN
+// neurons, where 1024 would leave most CUs without a workgroup.
+template <int NB>
+__global__ __launch_bounds__(NB) void k_neuron(NeuronArgs a, CompactArgs lst)
 {
-    constexpr int NWV = kNeuronBlock / kWave;
+    // (n < 2^24 neurons with 1024 threads, at most kNeuronSmallN with fewer)
+    static_assert((NB == kNeuronBlock ? (1 << 24) : kNeuronSmallN) / (NB * kNeuronRounds) <=
+                      65536,
+                  "workgroup ticket must fit in 16 bits");
+    constexpr int NWV = NB / kWave;
     constexpr int R = kNeuronRounds;
     __shared__ int s_cnt[2][R * NWV];
     __shared__ unsigned long long s_st[4];
@@ -263,7 +268,7 @@ __global__ __launch_bounds__(kNeuronBlock) void k_neuron(NeuronArgs a, CompactAr
     float v_xp[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-        const int i = (blockIdx.x * R + r) * kNeuronBlock + tid;
+        const int i = (blockIdx.x * R + r) * NB + tid;
         v_rs[r] = 0;
         v_pend[r] = v_tl[r] = 0;
         v_xp[r] = 0.f;
@@ -280,7 +285,7 @@ __global__ __launch_bounds__(kNeuronBlock) void k_neuron(NeuronArgs a, CompactAr
     int s[R], tx[R], forced[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-        const int i = (blockIdx.x * R + r) * kNeuronBlock + tid;
+        const int i = (blockIdx.x * R + r) * NB + tid;
         s[r] = tx[r] = forced[r] = 0;
         bool fired_recently = false;
         if (i < a.n) neuron_update(a, i, a.t, s[r], tx[r], forced[r], fired_recently);
@@ -305,7 +310,7 @@ __global__ __launch_bounds__(kNeuronBlock) void k_neuron(NeuronArgs a, CompactAr
     int ri_ok[R], txpos[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-        const int i = (blockIdx.x * R + r) * kNeuronBlock + tid;
+        const int i = (blockIdx.x * R + r) * NB + tid;
         ri[r] = RowInfo{};
         ri_ok[r] = 0;
         txpos[r] = -1;
@@ -373,7 +378,7 @@ __global__ __launch_bounds__(kNeuronBlock) void k_neuron(NeuronArgs a, CompactAr
     int o0 = (int)(base & 0xffffffull), o2 = (int)((base >> 24) & 0xffffffull);
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-        const int i = (blockIdx.x * R + r) * kNeuronBlock + tid;
+        const int i = (blockIdx.x * R + r) * NB + tid;
         // this wave's offsets in round r: every wave of the earlier rounds,
         // then the earlier waves of this one
         int p0 = o0, p2 = o2;
@@ -828,8 +833,15 @@ hipError_t launch_neuron_steps(hipStream_t s, const NeuronArgs &a, const BatchAr
 hipError_t launch_neuron(hipStream_t s, const NeuronArgs &a, const CompactArgs &c,
                          KernelEvents ev)
 {
-    hipExtLaunchKernelGGL(k_neuron, dim3(blocks_for(a.n, kNeuronBlock * kNeuronRounds)),
-                          dim3(kNeuronBlock), 0, s, ev.start, ev.stop, 0, a, c);
+    if (a.n <= kNeuronSmallN) {
+        constexpr int NB = kBlock;
+        hipExtLaunchKernelGGL(k_neuron<NB>, dim3(blocks_for(a.n, NB * kNeuronRounds)), dim3(NB),
+                              0, s, ev.start, ev.stop, 0, a, c);
+    } else {
+        constexpr int NB = kNeuronBlock;
+        hipExtLaunchKernelGGL(k_neuron<NB>, dim3(blocks_for(a.n, NB * kNeuronRounds)), dim3(NB),
+                              0, s, ev.start, ev.stop, 0, a, c);
+    }
     return hipGetLastError();
 }
 
