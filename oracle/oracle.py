@@ -15,7 +15,8 @@ Parity status of each oracle function (what pins it, see tests/test_oracle_*.py)
                         hand-computed single-pair weight changes
   delivery (Fig. 3a)    pinned: hand-built graph with known sums, conservation
   graph generators      pinned: edge counts vs binomial expectation, no autapses,
-                        sortedness, fan-out target uniformity
+                        sortedness, fan-out target uniformity; single rows
+                        (fanout_row, bernoulli_row) vs the draw definition
   whole-network rates   parity unpinned (the paper's model definitions and
                         raster data are not available)
 """
@@ -84,6 +85,7 @@ def _load():
         "oracle_build_random": (i64, [P, i32, f64, f32, f32]),
         "oracle_build_edges": (i32, [P, P, P, P, i64]),
         "oracle_fanout_row": (None, [u64, i32, i32, i32, P]),
+        "oracle_bernoulli_row": (i32, [u64, i32, f64, i32, P]),
         "oracle_pivots": (None, [P, i64, i32, i32, P]),
         "oracle_step": (None, [P]),
         "oracle_run": (None, [P, i64]),
@@ -138,6 +140,12 @@ def fanout_row(seed, n, fanout, k):
     out = np.zeros(fanout, dtype=np.int32)
     _load().oracle_fanout_row(seed, n, fanout, k, _ptr(out))
     return out
+
+
+def bernoulli_row(seed, n, p, k):
+    out = np.zeros(n, dtype=np.int32)
+    c = _load().oracle_bernoulli_row(seed, n, p, k, _ptr(out))
+    return out[:c].copy()
 
 
 def threads():

@@ -214,6 +214,18 @@ void oracle_fanout_row(uint64_t seed, int32_t n, int32_t fanout, int32_t k,
     qsort(out, (size_t)fanout, sizeof(int32_t), cmp_i32);
 }
 
+/* Row k of the fixed-probability graph (kind 0 below): the targets j != k
+ * whose stream-0 draw at (k, j) is below floor(p * 2^32), ascending. out
+ * holds n entries; returns the row length. */
+int32_t oracle_bernoulli_row(uint64_t seed, int32_t n, double p, int32_t k, int32_t *out)
+{
+    const uint32_t thr = prob_threshold(p);
+    int32_t c = 0;
+    for (int32_t j = 0; j < n; ++j)
+        if (j != k && rng32(seed, 0, (uint64_t)k, (uint64_t)j) < thr) out[c++] = j;
+    return c;
+}
+
 /* Random graph, weights by source type (w_exc for sources below n_exc).
  * kind 0: each ordered pair (k, j), j != k, is present when the stream-0
  *         draw at (k, j) is below floor(p * 2^32).

@@ -71,3 +71,82 @@ def test_stress_full_size_sampled_parity(hbits):
     net.step(1, snn.SNN_DELIVER_GLOBAL_ATOMIC)
     a_want = o.bernoulli_input(F, w_init, T)
     assert_close(to_np(net.state()["input_exc"]), a_want, "full-size global-atomic input")
+
+
+def test_brunel_full_size_delay_block():
+    """Full-size Brunel network (62,500 LIF neurons with Poisson drive,
+    p = 0.1: 390M synapses, D = 15) in the launch configuration the benchmark
+    times: delay blocks of 14 steps. Teacher forcing over one block: from the
+    state after 100 steps, the oracle (no graph) runs the block's 14 neuron
+    updates, each fed the input the delivered spikes imply; those inputs are
+    summed from the oracle's own rows of every spiking source. Spikes of
+    every step of the block, potentials, refractory counts and histories
+    must be bit-exact (the weights 0.1 and -0.5 sum exactly), and the pending
+    input after the block within the delivery tolerance."""
+    from oracle import oracle
+    p = wl.preset("brunel")
+    D, n = p.delay, p.n
+    log("full-size brunel: n=%d p=%g D=%d W=%d C=%d" % (n, p.p_or_fanout, D, p.slice_width,
+                                                       p.spike_chunks))
+    net = gpu_net(p)
+    T0, B = 100, D - 1
+    net.step(T0, snn.SNN_DELIVER_LDS_SLICE)
+    s0 = net.state()  # views of the device state: copied before the next steps
+    ring0 = to_np(s0["ring_lists"]).reshape(D, -1).copy()
+    cnt0 = to_np(s0["ring_counts"]).copy()
+    v0, ref0, hist0 = to_np(s0["v"]).copy(), to_np(s0["refractory"]).copy(), hist_np(s0["hist"]).copy()
+    a0 = to_np(s0["input_exc"]).copy()
+    ev0 = net.stats()["delivered_events"]
+    net.step(B, snn.SNN_DELIVER_LDS_SLICE)
+    s1 = net.state()
+    ring1 = to_np(s1["ring_lists"]).reshape(D, -1)
+    cnt1 = to_np(s1["ring_counts"])
+    log("  stepped %d + %d" % (T0, B))
+    rows = {}
+
+    def row(k):
+        if k not in rows:
+            rows[k] = oracle.bernoulli_row(p.seed, n, p.p_or_fanout, int(k))
+        return rows[k]
+
+    def input_from(spk):
+        # the input a list of spiking sources delivers, in double from the
+        # oracle's rows, rounded once to fp32
+        acc = np.zeros(n, np.float64)
+        for k in spk:
+            acc[row(k)] += np.float64(np.float32(p.w_exc if k < p.n_exc else p.w_inh))
+        return acc.astype(np.float32)
+
+    o = oracle_net(p, build=False)
+    o.t = T0
+    o.set_neurons(v=v0, refractory=ref0, hist=hist0)
+    events = 0
+    for b in range(B):
+        t = T0 + b
+        if b == 0:
+            a = a0  # pending input at T0: the state
+        else:
+            e = t - D  # emission step of the spikes arriving at t
+            a = input_from(ring0[e % D, :cnt0[e % D]])
+        o.set_input(a_exc=a)
+        o.step(1)
+        mask, lst = o.spikes()
+        slot = t % D
+        assert np.array_equal(ring1[slot, :cnt1[slot]], lst), ("spikes of step", t)
+    # the block delivered the spikes emitted at T0+1-D .. T0+B-D
+    for e in range(T0 + 1 - D, T0 + B + 1 - D):
+        events += sum(len(row(k)) for k in ring0[e % D, :cnt0[e % D]])
+    ost = o.neurons()
+    assert np.array_equal(to_np(s1["v"]).view(np.uint32), ost["v"].view(np.uint32))
+    assert np.array_equal(to_np(s1["refractory"]), ost["refractory"])
+    assert np.array_equal(hist_np(s1["hist"]), ost["hist"])
+    e = T0 + B - D  # pending input of step T0+B
+    assert_close(to_np(s1["input_exc"]), input_from(ring0[e % D, :cnt0[e % D]]),
+                 "pending input after the block")
+    assert net.stats()["delivered_events"] - ev0 == events
+    # the GPU's rows of some of the spiking sources
+    g = net.graph()
+    rp = to_np(g["row_ptr"])
+    for k in list(rows)[:16]:
+        assert np.array_equal(to_np(g["col"][rp[k]:rp[k + 1]]), row(k)), k
+    log("  block checked: %d spiking rows, %d events" % (len(rows), events))

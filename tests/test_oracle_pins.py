@@ -256,6 +256,7 @@ def test_bernoulli_graph_matches_definition(orc):
         js = np.nonzero(u < thr)[0]
         js = js[js != k]
         assert col[rp[k]:rp[k + 1]].tolist() == js.tolist()
+        assert orc.bernoulli_row(p.seed, p.n, 0.1, k).tolist() == js.tolist()
         assert np.all(w[rp[k]:rp[k + 1]] == np.float32(p.w_exc if k < p.n_exc else p.w_inh))
     mean = p.n * (p.n - 1) * 0.1
     assert abs(e - mean) < 5 * math.sqrt(mean * 0.9)
