@@ -571,6 +571,10 @@ __global__ __launch_bounds__(kNaiveBlock) void k_stdp_naive(NaiveArgs a)
 // and then delivered, so the row's targets and weights are read once. The
 // workgroups of slice 0 commit t_last and the pre traces of their spikes.
 //
+// In a delay block (networks without plasticity) the grid also spans the
+// block's steps: item (b, slice) takes ring slot (t_emit0 + b) mod D and
+// writes the fixed-point input of its step to abatch, one chunk per item.
+//
 // The spike count is read in parallel with the first batch's snapshots (the
 // snapshot buffer holds n entries, so reading past the count stays inside
 // it; entries past the count are discarded), and the workgroup's statistics
