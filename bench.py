@@ -19,6 +19,7 @@ Prints one JSON line. `--gpus N` with N > 1 exits: the benchmark runs on one GPU
 
 import argparse
 import hashlib
+import re
 import json
 import os
 import sys
@@ -63,12 +64,18 @@ def parse():
     return ap.parse_args()
 
 
+_COMMENT = re.compile(r"//[^\n]*|/\*.*?\*/", re.S)
+
+
 def kernel_source_digest():
+    """Digest of the library's code with comments and layout removed, so that
+    counters taken on a source stay valid across comment-only edits."""
     h = hashlib.sha256()
     for f in ("k_neuron.hip", "k_synapse.hip", "k_graph.hip", "snn_device.h", "snn_api.hip",
               "snn_internal.h"):
-        with open(os.path.join(ROOT, "paper_2107_04092_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2107_04092_amd", "csrc", f)) as fh:
+            code = _COMMENT.sub(" ", fh.read())
+        h.update(" ".join(code.split()).encode())
     return h.hexdigest()[:16]
 
 
