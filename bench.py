@@ -57,6 +57,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-instrumented", action="store_true",
                     help="no per-kernel event timing (plain timed steps)")
+    ap.add_argument("--no-row-probe", action="store_true",
+                    help="skip the row-stream probe (the forced-row STDP access pattern "
+                         "without its arithmetic, at the same row count)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the timed region, run one device-to-device copy of this many "
                          "MiB: the reference kernel that scales rocprofv3 FETCH_SIZE/WRITE_SIZE "
@@ -266,6 +269,26 @@ def main():
             combined = {"achieved_GBs": round(comb, 1), "frac": round(comb / HBM_PEAK_GBS, 4),
                         "us_per_step": round((t_stdp + t_dlv) * 1e3, 3)}
 
+    ceiling = None
+    if roofline is not None and kname == "k_stdp_rows" and not args.no_row_probe:
+        # the forced-row access pattern without its arithmetic, at the same
+        # row count: targets and weights streamed (8 B per synapse), then
+        # also every weight stored back (12 B per synapse); median of 5
+        rows = max(1, int(round(st2["stdp_forced_rows"] / max(nrec, 1))))
+        meas = {}
+        for write in (False, True):
+            runs = sorted(net.probe_rows(rows, write=write, seed=q + 1) for q in range(5))
+            ms, syn = runs[2]
+            bps = 12 if write else 8
+            meas[write] = (syn * bps / (ms * 1e-3) / 1e9, ms)
+        ceiling = {"kernel": "k_probe_rows", "rows": rows,
+                   "read_GBs": round(meas[False][0], 1),
+                   "read_frac": round(meas[False][0] / HBM_PEAK_GBS, 4),
+                   "read_us": round(meas[False][1] * 1e3, 2),
+                   "read_write_GBs": round(meas[True][0], 1),
+                   "read_write_frac": round(meas[True][0] / HBM_PEAK_GBS, 4),
+                   "read_write_us": round(meas[True][1] * 1e3, 2)}
+
     if args.copy_probe_mib > 0:
         nbytes = args.copy_probe_mib << 20
         src = torch.empty(nbytes, dtype=torch.uint8, device=dev).fill_(1)
@@ -310,6 +333,7 @@ def main():
         "cpu_baseline": cpu,
         "stdp_synapse_updates_per_s": stdp_per_s,
         "delivery_plus_stdp": combined,
+        "row_stream_ceiling": ceiling,
         "kernels": kernels,
         "stats": {k: int(v) for k, v in st.items()},
         "bytes_per_step": {"stdp": int(b_stdp), "delivery": int(b_dlv)},

@@ -332,6 +332,20 @@ snn_status snn_record_kernel_times(snn_ctx *ctx, int32_t max_steps);
  * Synchronises the stream. */
 snn_status snn_get_kernel_times(snn_ctx *ctx, double *mean_ms, int32_t *steps);
 
+/* Measurement only: the access pattern of the forced-row update (Sec.
+ * III-A: a row's targets and weights are read in full, Fig. 2(c)) without
+ * its arithmetic, as the ceiling of what that pattern reaches at a given
+ * row count. Streams the targets and weights of n_rows pseudo-random plastic
+ * rows (row r draws its index from the stream-5 generator at (r, 0), mod
+ * the plastic rows), a wave per part of 512 synapses with non-temporal
+ * loads, on the grid of the row-wise STDP kernel; with write != 0 it also
+ * stores every weight back unchanged. *ms (host) receives the device time
+ * of the one launch, *synapses (host) the synapses covered. Changes no
+ * state. Synchronises the stream. SNN_ESTATE without a built graph or
+ * without plastic rows; SNN_EINVAL for n_rows outside [1, 2^24]. */
+snn_status snn_probe_rows(snn_ctx *ctx, int32_t n_rows, int32_t write, uint64_t seed,
+                          double *ms, int64_t *synapses);
+
 /* Brings every plastic row up to the last completed step t-1 (no pre-
  * synaptic spike), so that all weights equal those of per-step updates. */
 snn_status snn_flush_plasticity(snn_ctx *ctx);

@@ -876,6 +876,51 @@ __global__ __launch_bounds__(kBlock) void k_deliver_global(DeliverArgs a)
     if (tid == 0) a.stats[2 * (int64_t)blockIdx.x] += ev;
 }
 
+// ---------------------------------------------------------------------------
+// Measurement probe, not part of a step: the access pattern of the forced-row
+// STDP without its arithmetic. Each wave streams whole plastic rows, chosen
+// pseudo-randomly (row rng32(seed, 5, r, 0) mod plastic rows for r <
+// n_rows), two parts of 8 synapses per lane in flight, with non-temporal
+// loads of the targets and weights, and with `write` stores every weight
+// back unchanged. `sink` only keeps the loads alive (written with vanishing
+// probability); the synapse count is left to the host, since atomics on one
+// word from every wave would serialise.
+__global__ __launch_bounds__(kStdpRowsBlock) void k_probe_rows(const int64_t *row_ptr,
+                                                               const int32_t *pend,
+                                                               const int32_t *col, float *w,
+                                                               int32_t n_rows, int32_t n_plastic,
+                                                               uint64_t seed, int32_t write,
+                                                               unsigned long long *sink)
+{
+    constexpr int U = 2 * kStdpRowsUnroll;  // two parts in flight, as the STDP kernel holds
+    const int lane = threadIdx.x % kWave;
+    const int gw = (blockIdx.x * kStdpRowsBlock + threadIdx.x) / kWave;
+    const int nwv = gridDim.x * (kStdpRowsBlock / kWave);
+    uint32_t keep = 0;
+    for (int r = gw; r < n_rows; r += nwv) {  // wave-uniform
+        const int k = (int)(rng32(seed, 5, (uint64_t)r, 0) % (uint32_t)n_plastic);
+        const int64_t rs = row_ptr[k];
+        const int len = pend[k];
+        for (int base = 0; base < len; base += U * kWave) {
+            int32_t j[U];
+            float x[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int qc = min(base + u * kWave + lane, len - 1);
+                j[u] = __builtin_nontemporal_load(col + rs + qc);
+                x[u] = __builtin_nontemporal_load(w + rs + qc);
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                keep ^= (uint32_t)j[u] ^ __float_as_uint(x[u]);
+                const int q = base + u * kWave + lane;
+                if (write && q < len) __builtin_nontemporal_store(x[u], w + rs + q);
+            }
+        }
+    }
+    if (keep == 0x9e3779b9u) atomicAdd(sink, 1ull);
+}
+
 }  // namespace
 
 hipError_t launch_row_info(hipStream_t s, const RowInfoArgs &a, int64_t max_rows)
@@ -941,6 +986,18 @@ hipError_t launch_deliver_lds(hipStream_t s, const DeliverArgs &a, int blocks, s
     else
         hipExtLaunchKernelGGL(k_deliver_lds<false>, dim3(blocks), dim3(kDlvBlock), lds, s,
                               ev.start, ev.stop, 0, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_probe_rows(hipStream_t s, const int64_t *row_ptr, const int32_t *pend,
+                             const int32_t *col, float *w, int32_t n_rows, int32_t n_plastic,
+                             uint64_t seed, int32_t write, unsigned long long *sink,
+                             KernelEvents ev)
+{
+    if (n_rows < 1 || n_plastic < 1) return hipErrorInvalidValue;
+    hipExtLaunchKernelGGL(k_probe_rows, dim3(kStdpRowsBlocks), dim3(kStdpRowsBlock), 0, s,
+                          ev.start, ev.stop, 0, row_ptr, pend, col, w, n_rows, n_plastic, seed,
+                          write, sink);
     return hipGetLastError();
 }
 

@@ -1160,6 +1160,47 @@ snn_status snn_flush_plasticity(snn_ctx *c)
     return launch_plasticity(c, true, c->stream);
 }
 
+snn_status snn_probe_rows(snn_ctx *c, int32_t n_rows, int32_t write, uint64_t seed, double *ms,
+                          int64_t *synapses)
+{
+    if (!c || !ms || !synapses) return SNN_EINVAL;
+    snn_status st = require_graph(c);
+    if (st) return st;
+    if (c->n_plastic_rows == 0) return fail(c, SNN_ESTATE, "the network has no plastic rows");
+    if (n_rows < 1 || n_rows > (1 << 24))
+        return fail(c, SNN_EINVAL, "n_rows must be in [1, 2^24]");
+    hipEvent_t ev[2] = {nullptr, nullptr};
+    hipError_t e = hipEventCreate(&ev[0]);
+    if (e == hipSuccess) e = hipEventCreate(&ev[1]);
+    if (e == hipSuccess)
+        e = launch_probe_rows(c->stream, c->row_ptr, c->pend, c->col, c->w, n_rows,
+                              c->n_plastic_rows, seed, write ? 1 : 0,
+                              (unsigned long long *)c->scratch, KernelEvents{ev[0], ev[1]});
+    std::vector<int32_t> pend((size_t)c->n_plastic_rows);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(pend.data(), c->pend, pend.size() * sizeof(int32_t),
+                           hipMemcpyDeviceToHost, c->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+    float t = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&t, ev[0], ev[1]);
+    for (hipEvent_t x : ev)
+        if (x) (void)hipEventDestroy(x);
+    st = check_hip(c, e, "row probe");
+    if (st) return st;
+    // the rows the kernel drew: SplitMix64 of seed ^ (5 << 58 | r << 24), high word
+    int64_t cnt = 0;
+    for (int32_t r = 0; r < n_rows; ++r) {
+        uint64_t z = (seed ^ ((5ull << 58) | ((uint64_t)r << 24))) + 0x9E3779B97F4A7C15ull;
+        z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+        z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+        z ^= z >> 31;
+        cnt += pend[(uint32_t)(z >> 32) % (uint32_t)c->n_plastic_rows];
+    }
+    *ms = t;
+    *synapses = cnt;
+    return SNN_OK;
+}
+
 snn_status snn_get_state(snn_ctx *c, snn_state_view *out)
 {
     if (!c || !out) return SNN_EINVAL;

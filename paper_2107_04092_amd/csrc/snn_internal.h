@@ -309,6 +309,11 @@ hipError_t launch_row_info(hipStream_t s, const RowInfoArgs &a, int64_t max_rows
 hipError_t launch_stdp(hipStream_t s, const StdpArgs &a, int blocks, size_t lds, KernelEvents ev = {});
 hipError_t launch_stdp_rows(hipStream_t s, const StdpArgs &a, int blocks, KernelEvents ev = {});
 hipError_t launch_stdp_naive(hipStream_t s, const NaiveArgs &a, int blocks, KernelEvents ev = {});
+// k_probe_rows: measurement only (sink: one scratch word)
+hipError_t launch_probe_rows(hipStream_t s, const int64_t *row_ptr, const int32_t *pend,
+                             const int32_t *col, float *w, int32_t n_rows, int32_t n_plastic,
+                             uint64_t seed, int32_t write, unsigned long long *sink,
+                             KernelEvents ev);
 constexpr int kStdpRowsBlock = 1024;   // threads of the row-wise STDP kernel
 constexpr int kStdpRowsUnroll = 8;     // synapses per lane and row part (64-step histories)
 constexpr int kStdpRowsUnroll2 = 4;    // the same with 128-step histories

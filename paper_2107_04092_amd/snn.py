@@ -85,6 +85,8 @@ _SIGNATURES = {
     "snn_advance": (_i32, [_P]),
     "snn_step": (_i32, [_P, _i32, _i32]),
     "snn_flush_plasticity": (_i32, [_P]),
+    "snn_probe_rows": (_i32, [_P, _i32, _i32, ctypes.c_uint64, ctypes.POINTER(ctypes.c_double),
+                              ctypes.POINTER(_i64)]),
     "snn_get_state": (_i32, [_P, ctypes.POINTER(snn_state_view)]),
     "snn_set_state": (_i32, [_P, ctypes.POINTER(snn_state_view)]),
     "snn_get_graph": (_i32, [_P, ctypes.POINTER(snn_graph_view)]),
@@ -198,6 +200,15 @@ def snn_step(ctx, n_steps, mode):
 
 def snn_flush_plasticity(ctx):
     _check(ctx, load().snn_flush_plasticity(ctx))
+
+
+def snn_probe_rows(ctx, n_rows, write, seed):
+    """Device milliseconds and synapses of one row-stream probe launch."""
+    ms = ctypes.c_double()
+    syn = _i64()
+    _check(ctx, load().snn_probe_rows(ctx, n_rows, write, seed, ctypes.byref(ms),
+                                      ctypes.byref(syn)))
+    return ms.value, syn.value
 
 
 def snn_get_state(ctx):
@@ -354,6 +365,9 @@ class Network:
 
     def flush_plasticity(self):
         snn_flush_plasticity(self.ctx)
+
+    def probe_rows(self, n_rows, write=False, seed=1):
+        return snn_probe_rows(self.ctx, n_rows, 1 if write else 0, seed)
 
     def stats(self):
         s = snn_get_stats(self.ctx)

@@ -149,3 +149,24 @@ def test_compressed_targets_encode_the_oracle_graph(name, kw, width):
     assert np.array_equal(to_np(g["col"]), col_o)
     got = to_np(g["col16"]).view(np.uint16)
     assert np.array_equal(got, expected_col16(col_o.astype(np.int64), width))
+
+
+def test_row_probe_counts_rows_and_changes_nothing():
+    """The row-stream probe (measurement only) covers n_rows whole plastic
+    rows, stores the weights back bit for bit, and rejects bad calls."""
+    p = wl.preset("stress", n=3000, p_or_fanout=120, p_fire=0.03)
+    net = gpu_net(p, slice_width=512)
+    net.step(20, snn.SNN_DELIVER_LDS_SLICE)
+    w0 = to_np(net.graph()["w"]).copy()
+    for write in (False, True):
+        ms, syn = net.probe_rows(500, write=write, seed=7)
+        assert syn == 500 * 120 and ms > 0
+    assert np.array_equal(to_np(net.graph()["w"]).view(np.uint32), w0.view(np.uint32))
+    with pytest.raises(snn.SnnError) as e:
+        net.probe_rows(0)
+    assert e.value.status == snn.SNN_EINVAL
+    q = gpu_net(wl.preset("stress", n=2000, p_or_fanout=50, plastic=PLASTIC_NONE),
+                slice_width=512)
+    with pytest.raises(snn.SnnError) as e:
+        q.probe_rows(10)
+    assert e.value.status == snn.SNN_ESTATE
