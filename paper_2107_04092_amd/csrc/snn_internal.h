@@ -8,8 +8,8 @@
 namespace snn {
 
 constexpr int kBlock = 256;          // threads per workgroup of the element kernels
-constexpr int kNeuronBlock = 1024;   // threads per workgroup of the neuron update (>= kBlock;
-                                     // large: one list reservation per workgroup)
+constexpr int kNeuronBlock = 1024;   // threads per workgroup of the neuron update on large
+                                     // networks (one list reservation per workgroup)
 constexpr int kNeuronSmallN = 65536; // up to this many neurons the update takes kBlock threads
                                      // per workgroup
 constexpr int kNeuronRounds = 1;     // neurons per thread of the neuron update (more rounds
