@@ -284,6 +284,36 @@ def test_checkpoint_restore_resumes_identically():
     assert_close(to_np(b.graph()["w"]), to_np(a.graph()["w"]), "weights after restore")
 
 
+def test_checkpoint_restore_between_delay_blocks():
+    """A Brunel network (delay blocks of 14) saved after 20 steps and restored
+    into a fresh network, with a forced input for its next step, continues
+    exactly as the original does through the same calls: the ring, the
+    pending input and the neuron state carry every block boundary."""
+    import torch
+    p = wl.preset("brunel", n=6000, n_exc=4800)
+    a = gpu_net(p, slice_width=1024, spike_chunks=2)
+    a.step(20, LDS)
+    s = a.state()
+    keys = ("v", "refractory", "hist", "input_exc", "ring_lists", "ring_counts")
+    snap = {k: s[k].clone() for k in keys}
+    t = int(s["t"])
+    b = gpu_net(p, slice_width=1024, spike_chunks=2)
+    b.set_state(t, **snap)
+    # the same forced input on both: the next step reads it, later ones the blocks
+    bump = snap["input_exc"] + 0.25
+    for net in (a, b):
+        net.set_state(t, input_exc=bump)
+        net.step(47, LDS)
+    sa, sb = a.state(), b.state()
+    for k in ("v", "refractory", "hist", "input_exc", "spike_mask", "ring_counts"):
+        assert np.array_equal(to_np(sa[k]), to_np(sb[k])), k
+    ra = to_np(sa["ring_lists"]).reshape(p.delay, -1)
+    rb = to_np(sb["ring_lists"]).reshape(p.delay, -1)
+    for q, c in enumerate(to_np(sa["ring_counts"])):
+        assert np.array_equal(ra[q, :c], rb[q, :c]), ("ring slot", q)
+    assert a.stats()["spikes"] > 0 and a.stats()["device_errors"] == 0
+
+
 @pytest.mark.parametrize("mode", [LDS, GLOBAL], ids=["lds", "global"])
 @pytest.mark.parametrize("delay", [1, 3])
 def test_free_run_with_state_reads(mode, delay):
