@@ -203,8 +203,6 @@ __global__ __launch_bounds__(kStdpBlock) void k_stdp(StdpArgs a)
 // updated and stored (both are in flight from the start); the next row's
 // snapshot is fetched one part ahead.
 
-// Weights per store line: 32 fp32 = one 128-byte L2 line.
-constexpr int kStoreLine = 32;
 constexpr uint64_t kLineMask = (1ull << kStoreLine) - 1;
 
 template <int U>
@@ -580,18 +578,18 @@ __global__ __launch_bounds__(kNaiveBlock) void k_stdp_naive(NaiveArgs a)
 // it; entries past the count are discarded), and the workgroup's statistics
 // are reduced before its final stores, so no barrier waits for them.
 
-constexpr int kDlvBlock = 512;
 constexpr int kDlvBatch = 512;   // spikes whose segments are staged at once
 constexpr int kDlvUnroll = 8;    // flattened elements per thread per window
 constexpr int kDlvWindow = kDlvBlock * kDlvUnroll;
 constexpr int kDlvDirectMax = 32;  // segments up to this long are mapped by their own thread
 static_assert(kDlvBatch == kDlvBlock, "one staged spike per thread");
 
-// (four waves per SIMD: two workgroups share a CU)
+// The body of one workgroup (bid of nb, nb a multiple of 8); acc is the
+// dynamic LDS: nacc * W accumulators [, W histories, W traces].
 template <bool CT>
-__global__ __launch_bounds__(kDlvBlock, 4) void k_deliver_lds(DeliverArgs a)
+__device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, int nb,
+                                                 long long *acc)
 {
-    extern __shared__ long long acc[];  // nacc * W accumulators [, W histories, W traces]
     __shared__ long long s_start[kDlvBatch];
     __shared__ int s_off[kDlvBatch + 1];
     __shared__ int s_half[kDlvBatch];
@@ -606,8 +604,7 @@ __global__ __launch_bounds__(kDlvBlock, 4) void k_deliver_lds(DeliverArgs a)
     __shared__ unsigned long long s_written;
     __shared__ int s_nlong;
     const int tid = threadIdx.x;
-    const int nb = gridDim.x;  // multiple of 8
-    const int qa = (blockIdx.x & 7) * (nb >> 3) + (blockIdx.x >> 3);
+    const int qa = (bid & 7) * (nb >> 3) + (bid >> 3);
     if (qa >= a.n_work) return;  // whole workgroup, before any barrier
     // a delay block's item (b, slice, chunk) takes step b's ring list and
     // writes partial sums of step b (b varies slowest: an XCD's range of
@@ -807,8 +804,8 @@ __global__ __launch_bounds__(kDlvBlock, 4) void k_deliver_lds(DeliverArgs a)
     if (tid % kWave == 0 && written) atomicAdd(&s_written, (unsigned long long)written);
     __syncthreads();  // the accumulation barrier: every LDS atomic is done
     if (tid == 0) {
-        a.stats[2 * (int64_t)blockIdx.x] += ev;
-        a.stats[2 * (int64_t)blockIdx.x + 1] += (int64_t)s_written;
+        a.stats[2 * (int64_t)bid] += ev;
+        a.stats[2 * (int64_t)bid + 1] += (int64_t)s_written;
     }
     if (a.chunks == 1 && a.batch == 0) {
         for (int x = tid; x < a.width; x += kDlvBlock) {
@@ -828,6 +825,32 @@ __global__ __launch_bounds__(kDlvBlock, 4) void k_deliver_lds(DeliverArgs a)
             }
         }
     }
+}
+
+// (four waves per SIMD: two workgroups share a CU)
+template <bool CT>
+__global__ __launch_bounds__(kDlvBlock, 4) void k_deliver_lds(DeliverArgs a)
+{
+    extern __shared__ long long dyn_acc[];
+    deliver_lds_body<CT>(a, blockIdx.x, gridDim.x, dyn_acc);
+}
+
+// Fused synapse pass of one step: the forced rows' plasticity and slice
+// delivery (with the transmitting rows' plasticity) in one launch. A forced
+// row does not transmit at t, so the two parts touch disjoint rows, and
+// neither reads what the other writes (targets' histories, post traces and
+// history summaries are only read): workgroups [0, nd) deliver, the others
+// take forced-row parts, side by side, in one launch's ramp and drain.
+template <bool CT, int HW>
+__global__ __launch_bounds__(kDlvBlock, 2) void k_synapse_pass(DeliverArgs d, StdpArgs s,
+                                                               int32_t nd)
+{
+    extern __shared__ long long dyn_pass[];
+    if ((int)blockIdx.x < nd)
+        deliver_lds_body<CT>(d, blockIdx.x, nd, dyn_pass);
+    else
+        stdp_rows_body<kDlvBlock, HW == 1 ? kStdpRowsUnroll : kStdpRowsUnroll2, HW>(
+            s, blockIdx.x - nd, gridDim.x - nd, (unsigned char *)dyn_pass);
 }
 
 // Row-wise delivery with global atomics (Fig. 3(a)): a wave per transmitted
@@ -1001,6 +1024,29 @@ hipError_t launch_probe_rows(hipStream_t s, const int64_t *row_ptr, const int32_
     return hipGetLastError();
 }
 
+hipError_t launch_synapse_pass(hipStream_t s, const DeliverArgs &d, const StdpArgs &a, int nd,
+                               int ns, size_t lds, KernelEvents ev)
+{
+    static std::mutex mu;
+    static int granted[4] = {64 * 1024, 64 * 1024, 64 * 1024, 64 * 1024};
+    const int k = (d.col16 != nullptr ? 2 : 0) + (a.hw == 2 ? 1 : 0);
+    const void *kerns[4] = {(const void *)k_synapse_pass<false, 1>,
+                            (const void *)k_synapse_pass<false, 2>,
+                            (const void *)k_synapse_pass<true, 1>,
+                            (const void *)k_synapse_pass<true, 2>};
+    if (nd % 8 != 0 || ns < 1) return hipErrorInvalidValue;
+    const hipError_t e = allow_dynamic_lds(kerns[k], (int)lds, mu, granted[k]);
+    if (e != hipSuccess) return e;
+    const dim3 g(nd + ns), b(kDlvBlock);
+    switch (k) {
+    case 0: hipExtLaunchKernelGGL((k_synapse_pass<false, 1>), g, b, lds, s, ev.start, ev.stop, 0, d, a, nd); break;
+    case 1: hipExtLaunchKernelGGL((k_synapse_pass<false, 2>), g, b, lds, s, ev.start, ev.stop, 0, d, a, nd); break;
+    case 2: hipExtLaunchKernelGGL((k_synapse_pass<true, 1>), g, b, lds, s, ev.start, ev.stop, 0, d, a, nd); break;
+    default: hipExtLaunchKernelGGL((k_synapse_pass<true, 2>), g, b, lds, s, ev.start, ev.stop, 0, d, a, nd); break;
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_deliver_global(hipStream_t s, const DeliverArgs &a, int blocks, KernelEvents ev)
 {
     hipExtLaunchKernelGGL(k_deliver_global, dim3(blocks), dim3(kBlock), 0, s,
@@ -1014,5 +1060,16 @@ int deliver_lds_static_bytes()
                     static_lds_bytes((const void *)k_deliver_lds<true>));
 }
 int stdp_static_bytes() { return static_lds_bytes((const void *)k_stdp); }
+int synapse_pass_static_bytes()
+{
+    int m = -1;
+    for (const void *k : {(const void *)k_synapse_pass<false, 1>, (const void *)k_synapse_pass<false, 2>,
+                          (const void *)k_synapse_pass<true, 1>, (const void *)k_synapse_pass<true, 2>}) {
+        const int b = static_lds_bytes(k);
+        if (b < 0) return -1;
+        m = std::max(m, b);
+    }
+    return m;
+}
 
 }  // namespace snn

@@ -66,6 +66,7 @@ struct snn_ctx {
     int32_t dlv_slots = 0;
     // delay blocks (no plasticity, D >= 2): steps per block, partial inputs
     int32_t batch_max = 0;
+    bool fuse = false;  // plastic, n <= kFusedMaxN: parts (2) and (3) in one launch
     long long *abatch = nullptr;  // [batch_max][C][nacc][n]
 
     // graph
@@ -493,7 +494,8 @@ size_t dlv_lds_bytes(const snn_ctx *c)
 }
 
 // Arguments of the synapse pass over the forced rows (flush: all rows).
-StdpArgs stdp_args(snn_ctx *c, bool flush)
+StdpArgs stdp_args(snn_ctx *c, bool flush,
+                   int64_t waves = (int64_t)kStdpRowsBlocks * (kStdpRowsBlock / kWave))
 {
     StdpArgs a{};
     a.info = c->info;
@@ -536,10 +538,9 @@ StdpArgs stdp_args(snn_ctx *c, bool flush)
     // of rows: all plastic rows in a flush, else the forced rows (staggered:
     // one in 64 hw per step); ties keep the smaller P (fewer snapshot loads).
     const int part = (c->hw == 2 ? kStdpRowsUnroll2 : kStdpRowsUnroll) * kWave;
-    const int64_t parts = std::max(1, (c->max_row + 15 + part - 1) / part);
+    const int64_t parts = std::max(1, (c->max_row + kStoreLine - 1 + part - 1) / part);
     const int64_t rows = std::max<int64_t>(1, flush ? c->n_plastic_rows
                                                     : c->n_plastic_rows / (64 * c->hw));
-    const int64_t waves = (int64_t)kStdpRowsBlocks * (kStdpRowsBlock / kWave);
     int64_t best = -1;
     a.parts = 1;
     for (int pp = 1; pp <= kStdpRowsSplit && pp <= parts; ++pp) {
@@ -653,6 +654,27 @@ DeliverArgs deliver_args(snn_ctx *c)
     a.mu = c->mu;
     for (int q = 0; q <= kMaxAge; ++q) a.dpow[q] = c->dpow[q];
     return a;
+}
+
+// Parts (2) and (3) of a step in one launch (k_synapse_pass): delivery on
+// its usual work items, the forced rows on the CU slots left over.
+snn_status launch_step_synapse_pass(snn_ctx *c)
+{
+    DeliverArgs d = deliver_args(c);
+    const int nd = c->dlv_blocks;
+    const int ns = std::max(8, kFusedSlots - nd);
+    StdpArgs a = stdp_args(c, false, (int64_t)ns * (kDlvBlock / kWave));
+    const size_t table = a.code     ? (((size_t)c->n + 15) / 16) * 16
+                         : a.recent ? (size_t)c->nw * sizeof(uint64_t)
+                                    : 0;
+    const size_t lds = std::max(dlv_lds_bytes(c), table + (size_t)fused_queue_bytes(c->hw));
+    snn_status st =
+        check_hip(c, launch_synapse_pass(c->stream, d, a, nd, ns, lds), "synapse pass kernel");
+    if (st) return st;
+    c->n_parts = c->chunks;
+    c->last_deliver_t = c->t;
+    c->input_forced = c->chunks == 1 ? 1 : 0;
+    return SNN_OK;
 }
 
 snn_status launch_step_delivery(snn_ctx *c, int32_t mode)
@@ -770,6 +792,15 @@ snn_status snn_create(const snn_config *cfg, void *hip_stream, snn_ctx **out)
         if (work > (1 << 20)) return fail(c, SNN_EINVAL, "too many STDP work items");
         c->stdp_grid = (int32_t)((work + 7) / 8 * 8);
         c->syn_slots = c->stdp_grid > kStdpRowsBlocks ? c->stdp_grid : kStdpRowsBlocks;
+    }
+    // the fused synapse pass: its static LDS beside the larger of the two
+    // parts' dynamic LDS (the code table or bitmap is at most kCodeMax bytes)
+    if (c->n_plastic_rows > 0 && c->algo != 2 && cfg->stdp_layout == 0 && c->n <= kFusedMaxN) {
+        const int fstat = synapse_pass_static_bytes();
+        if (fstat < 0) return fail(c, SNN_EDEVICE, "cannot query the kernels");
+        const int64_t table = std::max<int64_t>(((int64_t)c->n + 15) / 16 * 16, (int64_t)c->nw * 8);
+        const int64_t dyn = std::max<int64_t>(need, table + fused_queue_bytes(c->hw));
+        c->fuse = dyn + fstat <= lds_max;
     }
     plan_workspace(c, nullptr);
     return SNN_OK;
@@ -1090,10 +1121,17 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
         q += B;
     }
     if (blocks) return SNN_OK;
+    // plastic networks up to kFusedMaxN neurons: parts (2) and (3) in one
+    // launch (unless kernel times are being recorded per part)
+    const bool fuse = mode == SNN_DELIVER_LDS_SLICE && c->fuse;
     for (int32_t q = 0; q < n_steps; ++q) {
         if ((st = launch_step_neurons(c))) return st;
-        if ((st = launch_step_plasticity(c))) return st;
-        if ((st = launch_step_delivery(c, mode))) return st;
+        if (fuse && c->t_used >= c->t_cap) {
+            if ((st = launch_step_synapse_pass(c))) return st;
+        } else {
+            if ((st = launch_step_plasticity(c))) return st;
+            if ((st = launch_step_delivery(c, mode))) return st;
+        }
         if (c->t_used < c->t_cap) c->t_used += 1;
         c->t += 1;
         c->steps_done += 1;

@@ -318,6 +318,8 @@ constexpr int kStdpRowsBlock = 1024;   // threads of the row-wise STDP kernel
 constexpr int kStdpRowsUnroll = 8;     // synapses per lane and row part (64-step histories)
 constexpr int kStdpRowsUnroll2 = 4;    // the same with 128-step histories
 constexpr int kStdpRowsBlocks = 256;   // its persistent grid (one workgroup per CU)
+constexpr int kDlvBlock = 512;         // threads per workgroup of slice delivery
+constexpr int kStoreLine = 32;         // weights per store line of the row-wise STDP (128 B)
 constexpr int kStdpRowsSplit = 8;      // most waves that share one row
 
 
@@ -329,12 +331,26 @@ constexpr int stdp_rows_queue_bytes(int hw)
 }
 // the per-neuron summary it stages beside the queues (160 KB of LDS per workgroup)
 constexpr int kCodeMax = 163840 - stdp_rows_queue_bytes(1) - 1024;  // bytes of history codes
+// The fused synapse pass (k_synapse_pass) on networks of up to kFusedMaxN
+// neurons, where both parts are short and latency-bound; its workgroups fill
+// kFusedSlots slots (one per CU).
+constexpr int kFusedMaxN = 65536;
+constexpr int kFusedSlots = 256;
+constexpr int fused_queue_bytes(int hw)
+{
+    return (kDlvBlock / kWave) * (hw == 2 ? kStdpRowsUnroll2 : kStdpRowsUnroll) * kWave * 8;
+}
 constexpr int kRecentMaxWords = kCodeMax / 8;  // words of the spike-recency bitmap
 constexpr uint8_t kCodeMulti = 255;    // history code: two or more spikes in the window
 int stdp_static_bytes();  // static LDS of the slice STDP kernel (-1 on error)
 hipError_t launch_deliver_lds(hipStream_t s, const DeliverArgs &a, int blocks, size_t lds, KernelEvents ev = {});
+// k_synapse_pass: slice delivery on workgroups [0, nd) (nd a multiple of 8),
+// forced-row STDP on ns more, kDlvBlock threads each; lds covers both
+hipError_t launch_synapse_pass(hipStream_t s, const DeliverArgs &d, const StdpArgs &a, int nd,
+                               int ns, size_t lds, KernelEvents ev = {});
 hipError_t launch_deliver_global(hipStream_t s, const DeliverArgs &a, int blocks, KernelEvents ev = {});
 int deliver_lds_static_bytes();  // static LDS of the slice kernel (-1 on error)
+int synapse_pass_static_bytes();  // static LDS of the fused synapse pass (-1 on error)
 hipError_t launch_materialize_input(hipStream_t s, const long long *apart, int64_t part_stride,
                                     int32_t n_parts, float *ain, int64_t count);
 hipError_t launch_scan_i64(hipStream_t s, int64_t *data, int64_t count, int64_t *bsum);
