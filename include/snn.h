@@ -314,7 +314,9 @@ snn_status snn_advance(snn_ctx *ctx);
  * D >= 2 the inputs of up to D-1 steps (at most 16; 8 for CUBA) come from
  * spikes already in the delay ring, so one delivery launch computes them
  * all before one neuron launch runs those steps (Sec. I: the input of step
- * t depends on the spikes of step t-D only). */
+ * t depends on the spikes of step t-D only). Plastic networks of up to
+ * 65,536 neurons run parts (2) and (3) in one launch: the forced rows and
+ * the transmitting rows of a step are disjoint. */
 snn_status snn_step(snn_ctx *ctx, int32_t n_steps, int32_t mode);
 
 /* Kernel timing for profiling. After this call the next max_steps steps run
