@@ -249,9 +249,11 @@ def main():
             "neuron_us": round(t_neu * 1e3, 3),
             "plasticity_us": round(t_stdp * 1e3, 3),
             "delivery_us": round(t_dlv * 1e3, 3),
+            "fused_synapse_pass": bool(p.plastic != 0 and t_stdp == 0 and t_dlv > 0),
             "plasticity_bytes_per_launch": int(b_stdp),
             "delivery_bytes_per_launch": int(b_dlv),
-            "delivery_GBs": round(b_dlv / (t_dlv * 1e-3) / 1e9, 1) if t_dlv else None,
+            "delivery_GBs": (round(b_dlv / (t_dlv * 1e-3) / 1e9, 1)
+                             if t_dlv and not (p.plastic != 0 and t_stdp == 0) else None),
         }
         if args.plasticity == "naive":
             kname = "k_stdp_naive"
@@ -259,8 +261,15 @@ def main():
             kname = "k_stdp_rows"
         else:
             kname = "k_stdp"
-        if t_stdp > 0:
+        # a plastic network whose step ran plasticity and delivery in one
+        # launch (the fused synapse pass) records it as the delivery part
+        fused = p.plastic != 0 and t_stdp == 0 and t_dlv > 0 and b_stdp > 0
+        if fused:
+            kname = "k_synapse_pass"
+            ach = (b_stdp + b_dlv) / (t_dlv * 1e-3) / 1e9
+        elif t_stdp > 0:
             ach = b_stdp / (t_stdp * 1e-3) / 1e9
+        if fused or t_stdp > 0:
             traffic = load_traffic(kname, p.name)
             roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
                         "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
@@ -270,7 +279,8 @@ def main():
                         "us_per_step": round((t_stdp + t_dlv) * 1e3, 3)}
 
     ceiling = None
-    if roofline is not None and kname == "k_stdp_rows" and not args.no_row_probe:
+    if roofline is not None and kname in ("k_stdp_rows", "k_synapse_pass") and \
+            not args.no_row_probe:
         # the forced-row access pattern without its arithmetic, at the same
         # row count: targets and weights streamed (8 B per synapse), then
         # also every weight stored back (12 B per synapse); median of 5

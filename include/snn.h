@@ -314,16 +314,18 @@ snn_status snn_advance(snn_ctx *ctx);
  * D >= 2 the inputs of up to D-1 steps (at most 16; 8 for CUBA) come from
  * spikes already in the delay ring, so one delivery launch computes them
  * all before one neuron launch runs those steps (Sec. I: the input of step
- * t depends on the spikes of step t-D only). Plastic networks of up to
- * 65,536 neurons run parts (2) and (3) in one launch: the forced rows and
- * the transmitting rows of a step are disjoint. */
+ * t depends on the spikes of step t-D only). Plastic networks run parts
+ * (2) and (3) in one launch where its LDS leaves the forced rows at least
+ * half a workgroup slot per CU beside the delivery work items: the forced
+ * rows and the transmitting rows of a step are disjoint. */
 snn_status snn_step(snn_ctx *ctx, int32_t n_steps, int32_t mode);
 
 /* Kernel timing for profiling. After this call the next max_steps steps run
  * by snn_step record, per step, the device time of its kernels in three
  * parts: [0] neuron update with its spike / row lists, [1] plasticity,
  * [2] delivery (for the global-atomic mode from the start of the
- * transmitting rows' plasticity to the end of delivery). Each launch places its own events around the kernel
+ * transmitting rows' plasticity to the end of delivery; where snn_step runs
+ * parts (2) and (3) in one launch, that launch, with [1] not recorded). Each launch places its own events around the kernel
  * (no extra stream work). 0 stops recording and frees the events. Calls the
  * stream's synchronisation first. */
 snn_status snn_record_kernel_times(snn_ctx *ctx, int32_t max_steps);

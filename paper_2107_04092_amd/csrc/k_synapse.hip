@@ -578,31 +578,32 @@ __global__ __launch_bounds__(kNaiveBlock) void k_stdp_naive(NaiveArgs a)
 // it; entries past the count are discarded), and the workgroup's statistics
 // are reduced before its final stores, so no barrier waits for them.
 
-constexpr int kDlvBatch = 512;   // spikes whose segments are staged at once
-constexpr int kDlvUnroll = 8;    // flattened elements per thread per window
-constexpr int kDlvWindow = kDlvBlock * kDlvUnroll;
 constexpr int kDlvDirectMax = 32;  // segments up to this long are mapped by their own thread
 static_assert(kDlvBatch == kDlvBlock, "one staged spike per thread");
 
-// The body of one workgroup (bid of nb, nb a multiple of 8); acc is the
-// dynamic LDS: nacc * W accumulators [, W histories, W traces].
+// The body of one workgroup (bid of nb, nb a multiple of 8) in its dynamic
+// LDS: the staging arrays (DlvShared), then nacc * W accumulators [, W
+// histories, W traces]. Keeping the staging arrays in the dynamic region
+// lets a launch that also runs other work reuse the bytes.
 template <bool CT>
 __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, int nb,
-                                                 long long *acc)
+                                                 unsigned char *dyn)
 {
-    __shared__ long long s_start[kDlvBatch];
-    __shared__ int s_off[kDlvBatch + 1];
-    __shared__ int s_half[kDlvBatch];
-    __shared__ int s_plen[kDlvBatch];
-    __shared__ int s_age[kDlvBatch];
-    __shared__ float s_xp0[kDlvBatch];
-    __shared__ float s_xpn[kDlvBatch];
-    __shared__ int s_map[kDlvWindow];
-    __shared__ float s_dpow[kMaxAge + 1];
-    __shared__ long long sh[kDlvBlock / kWave];
-    __shared__ int shi[kDlvBlock / kWave];
-    __shared__ unsigned long long s_written;
-    __shared__ int s_nlong;
+    DlvShared &S = *reinterpret_cast<DlvShared *>(dyn);
+    long long *acc = reinterpret_cast<long long *>(dyn + sizeof(DlvShared));
+    long long *s_start = S.start;
+    int *s_off = S.off;
+    int *s_half = S.half;
+    int *s_plen = S.plen;
+    int *s_age = S.age;
+    float *s_xp0 = S.xp0;
+    float *s_xpn = S.xpn;
+    int *s_map = S.map;
+    float *s_dpow = S.dpow;
+    long long *sh = S.sh;
+    int *shi = S.shi;
+    unsigned long long &s_written = S.written;
+    int &s_nlong = S.nlong;
     const int tid = threadIdx.x;
     const int qa = (bid & 7) * (nb >> 3) + (bid >> 3);
     if (qa >= a.n_work) return;  // whole workgroup, before any barrier
@@ -831,8 +832,8 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
 template <bool CT>
 __global__ __launch_bounds__(kDlvBlock, 4) void k_deliver_lds(DeliverArgs a)
 {
-    extern __shared__ long long dyn_acc[];
-    deliver_lds_body<CT>(a, blockIdx.x, gridDim.x, dyn_acc);
+    extern __shared__ uint4 dyn_dlv[];
+    deliver_lds_body<CT>(a, blockIdx.x, gridDim.x, reinterpret_cast<unsigned char *>(dyn_dlv));
 }
 
 // Fused synapse pass of one step: the forced rows' plasticity and slice
@@ -842,12 +843,12 @@ __global__ __launch_bounds__(kDlvBlock, 4) void k_deliver_lds(DeliverArgs a)
 // history summaries are only read): workgroups [0, nd) deliver, the others
 // take forced-row parts, side by side, in one launch's ramp and drain.
 template <bool CT, int HW>
-__global__ __launch_bounds__(kDlvBlock, 2) void k_synapse_pass(DeliverArgs d, StdpArgs s,
+__global__ __launch_bounds__(kDlvBlock, 4) void k_synapse_pass(DeliverArgs d, StdpArgs s,
                                                                int32_t nd)
 {
-    extern __shared__ long long dyn_pass[];
+    extern __shared__ uint4 dyn_pass[];
     if ((int)blockIdx.x < nd)
-        deliver_lds_body<CT>(d, blockIdx.x, nd, dyn_pass);
+        deliver_lds_body<CT>(d, blockIdx.x, nd, reinterpret_cast<unsigned char *>(dyn_pass));
     else
         stdp_rows_body<kDlvBlock, HW == 1 ? kStdpRowsUnroll : kStdpRowsUnroll2, HW>(
             s, blockIdx.x - nd, gridDim.x - nd, (unsigned char *)dyn_pass);

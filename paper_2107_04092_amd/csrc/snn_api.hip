@@ -66,7 +66,8 @@ struct snn_ctx {
     int32_t dlv_slots = 0;
     // delay blocks (no plasticity, D >= 2): steps per block, partial inputs
     int32_t batch_max = 0;
-    bool fuse = false;  // plastic, n <= kFusedMaxN: parts (2) and (3) in one launch
+    bool fuse = false;  // plastic: parts (2) and (3) of snn_step in one launch
+    int32_t fuse_slots = 0;  // workgroups of the fused pass resident at once
     long long *abatch = nullptr;  // [batch_max][C][nacc][n]
 
     // graph
@@ -487,7 +488,7 @@ snn_status launch_step_neurons(snn_ctx *c)
 
 size_t dlv_lds_bytes(const snn_ctx *c)
 {
-    size_t b = (size_t)c->cfg.slice_width * c->nacc * sizeof(long long);
+    size_t b = sizeof(DlvShared) + (size_t)c->cfg.slice_width * c->nacc * sizeof(long long);
     if (c->n_plastic_rows > 0 && c->algo != 2)
         b += (size_t)c->cfg.slice_width * (c->hw * sizeof(uint64_t) + sizeof(float));
     return b;
@@ -658,18 +659,18 @@ DeliverArgs deliver_args(snn_ctx *c)
 
 // Parts (2) and (3) of a step in one launch (k_synapse_pass): delivery on
 // its usual work items, the forced rows on the CU slots left over.
-snn_status launch_step_synapse_pass(snn_ctx *c)
+snn_status launch_step_synapse_pass(snn_ctx *c, KernelEvents ev)
 {
     DeliverArgs d = deliver_args(c);
     const int nd = c->dlv_blocks;
-    const int ns = std::max(8, kFusedSlots - nd);
+    const int ns = std::max(8, c->fuse_slots - nd);
     StdpArgs a = stdp_args(c, false, (int64_t)ns * (kDlvBlock / kWave));
     const size_t table = a.code     ? (((size_t)c->n + 15) / 16) * 16
                          : a.recent ? (size_t)c->nw * sizeof(uint64_t)
                                     : 0;
     const size_t lds = std::max(dlv_lds_bytes(c), table + (size_t)fused_queue_bytes(c->hw));
     snn_status st =
-        check_hip(c, launch_synapse_pass(c->stream, d, a, nd, ns, lds), "synapse pass kernel");
+        check_hip(c, launch_synapse_pass(c->stream, d, a, nd, ns, lds, ev), "synapse pass kernel");
     if (st) return st;
     c->n_parts = c->chunks;
     c->last_deliver_t = c->t;
@@ -754,13 +755,14 @@ snn_status snn_create(const snn_config *cfg, void *hip_stream, snn_ctx **out)
     const int stat = deliver_lds_static_bytes();
     const int stat_stdp = stdp_static_bytes();
     if (stat < 0 || stat_stdp < 0) return fail(c, SNN_EDEVICE, "cannot query the kernels");
-    int64_t need = (int64_t)cfg->slice_width * 8 * (cfg->neuron_model == SNN_LIF_CUBA ? 2 : 1);
+    int64_t need = (int64_t)sizeof(DlvShared) +
+                   (int64_t)cfg->slice_width * 8 * (cfg->neuron_model == SNN_LIF_CUBA ? 2 : 1);
     const int hw = cfg->history_bits == 128 ? 2 : 1;
     if (cfg->plastic != SNN_PLASTIC_NONE) need += (int64_t)cfg->slice_width * (8 * hw + 4);
     if (need + stat > lds_max)
         return fail(c, SNN_EINVAL,
-                    "slice delivery needs %lld B of LDS (accumulator%s) besides %d B of "
-                    "staging; the device allows %d", (long long)need,
+                    "slice delivery needs %lld B of LDS (staging, accumulator%s) besides %d B "
+                    "of static LDS; the device allows %d", (long long)need,
                     cfg->plastic != SNN_PLASTIC_NONE ? ", histories and post traces" : "", stat,
                     lds_max);
     derive(c);
@@ -793,14 +795,25 @@ snn_status snn_create(const snn_config *cfg, void *hip_stream, snn_ctx **out)
         c->stdp_grid = (int32_t)((work + 7) / 8 * 8);
         c->syn_slots = c->stdp_grid > kStdpRowsBlocks ? c->stdp_grid : kStdpRowsBlocks;
     }
-    // the fused synapse pass: its static LDS beside the larger of the two
-    // parts' dynamic LDS (the code table or bitmap is at most kCodeMax bytes)
-    if (c->n_plastic_rows > 0 && c->algo != 2 && cfg->stdp_layout == 0 && c->n <= kFusedMaxN) {
+    // The fused synapse pass: its static LDS beside the larger of the two
+    // parts' dynamic LDS gives the workgroups a CU holds; it is used when
+    // the delivery items leave at least half a slot per CU to the forced
+    // rows (fewer waves starve them: slower than two launches).
+    if (c->n_plastic_rows > 0 && c->algo != 2 && cfg->stdp_layout == 0) {
         const int fstat = synapse_pass_static_bytes();
         if (fstat < 0) return fail(c, SNN_EDEVICE, "cannot query the kernels");
-        const int64_t table = std::max<int64_t>(((int64_t)c->n + 15) / 16 * 16, (int64_t)c->nw * 8);
+        // the history summary the forced rows stage (as stdp_args chooses it)
+        const int f = cfg->stdp_filter;
+        const bool fits_code = (int64_t)c->n + 16 <= kCodeMax, fits_map = c->nw <= kRecentMaxWords;
+        const int64_t code_b = ((int64_t)c->n + 15) / 16 * 16, map_b = (int64_t)c->nw * 8;
+        const int64_t table = f == 1 ? code_b
+                              : f == 2 ? map_b
+                              : f == 0 ? (fits_code ? code_b : fits_map ? map_b : 0)
+                                       : 0;
         const int64_t dyn = std::max<int64_t>(need, table + fused_queue_bytes(c->hw));
-        c->fuse = dyn + fstat <= lds_max;
+        const int64_t per_cu = std::min<int64_t>(2, lds_max / (dyn + fstat));
+        c->fuse_slots = (int32_t)(kFusedCUs * per_cu);
+        c->fuse = per_cu >= 1 && c->fuse_slots - c->dlv_blocks >= kFusedCUs / 2;
     }
     plan_workspace(c, nullptr);
     return SNN_OK;
@@ -1121,13 +1134,13 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
         q += B;
     }
     if (blocks) return SNN_OK;
-    // plastic networks up to kFusedMaxN neurons: parts (2) and (3) in one
-    // launch (unless kernel times are being recorded per part)
+    // parts (2) and (3) of plastic networks in one launch where it fits
+    // (kernel timing records it as the delivery part)
     const bool fuse = mode == SNN_DELIVER_LDS_SLICE && c->fuse;
     for (int32_t q = 0; q < n_steps; ++q) {
         if ((st = launch_step_neurons(c))) return st;
-        if (fuse && c->t_used >= c->t_cap) {
-            if ((st = launch_step_synapse_pass(c))) return st;
+        if (fuse) {
+            if ((st = launch_step_synapse_pass(c, part_events(c, 2)))) return st;
         } else {
             if ((st = launch_step_plasticity(c))) return st;
             if ((st = launch_step_delivery(c, mode))) return st;

@@ -319,6 +319,26 @@ constexpr int kStdpRowsUnroll = 8;     // synapses per lane and row part (64-ste
 constexpr int kStdpRowsUnroll2 = 4;    // the same with 128-step histories
 constexpr int kStdpRowsBlocks = 256;   // its persistent grid (one workgroup per CU)
 constexpr int kDlvBlock = 512;         // threads per workgroup of slice delivery
+constexpr int kDlvBatch = 512;         // spikes whose segments slice delivery stages at once
+constexpr int kDlvUnroll = 8;          // flattened elements per thread per window
+constexpr int kDlvWindow = kDlvBlock * kDlvUnroll;
+// Slice delivery's staging arrays, at the start of its dynamic LDS.
+struct DlvShared {
+    long long start[kDlvBatch];        // segment starts (edge index)
+    long long sh[kDlvBlock / 64];      // scan scratch
+    unsigned long long written;        // weights written by the workgroup
+    int off[kDlvBatch + 1];            // segment offsets in the batch
+    int half[kDlvBatch];               // accumulator half (CUBA inhibitory sources)
+    int plen[kDlvBatch];               // plastic elements of each segment
+    int age[kDlvBatch];                // row age (window of the replay)
+    float xp0[kDlvBatch], xpn[kDlvBatch];  // pre traces at the last update and now
+    int map[kDlvWindow];               // element -> segment of the window
+    float dpow[kMaxAge + 1];           // decay table
+    int shi[kDlvBlock / 64];           // scan scratch
+    int nlong;                         // segments longer than the direct-map limit
+    int pad_[2];
+};
+static_assert(sizeof(DlvShared) % 16 == 0, "the accumulators follow 16-byte aligned");
 constexpr int kStoreLine = 32;         // weights per store line of the row-wise STDP (128 B)
 constexpr int kStdpRowsSplit = 8;      // most waves that share one row
 
@@ -331,11 +351,9 @@ constexpr int stdp_rows_queue_bytes(int hw)
 }
 // the per-neuron summary it stages beside the queues (160 KB of LDS per workgroup)
 constexpr int kCodeMax = 163840 - stdp_rows_queue_bytes(1) - 1024;  // bytes of history codes
-// The fused synapse pass (k_synapse_pass) on networks of up to kFusedMaxN
-// neurons, where both parts are short and latency-bound; its workgroups fill
-// kFusedSlots slots (one per CU).
-constexpr int kFusedMaxN = 65536;
-constexpr int kFusedSlots = 256;
+// The fused synapse pass (k_synapse_pass): its workgroups fill the slots of
+// every CU (one or two per CU, as the LDS of both parts allows).
+constexpr int kFusedCUs = 256;  // workgroup slots per workgroup that one CU holds
 constexpr int fused_queue_bytes(int hw)
 {
     return (kDlvBlock / kWave) * (hw == 2 ? kStdpRowsUnroll2 : kStdpRowsUnroll) * kWave * 8;
