@@ -353,7 +353,7 @@ constexpr int stdp_rows_queue_bytes(int hw)
 constexpr int kCodeMax = 163840 - stdp_rows_queue_bytes(1) - 1024;  // bytes of history codes
 // The fused synapse pass (k_synapse_pass): its workgroups fill the slots of
 // every CU (one or two per CU, as the LDS of both parts allows).
-constexpr int kFusedCUs = 256;  // workgroup slots per workgroup that one CU holds
+constexpr int kFusedCUs = 256;  // CUs: the pass has kFusedCUs slots per workgroup a CU holds
 constexpr int fused_queue_bytes(int hw)
 {
     return (kDlvBlock / kWave) * (hw == 2 ? kStdpRowsUnroll2 : kStdpRowsUnroll) * kWave * 8;
