@@ -814,6 +814,8 @@ snn_status snn_create(const snn_config *cfg, void *hip_stream, snn_ctx **out)
         const int64_t per_cu = std::min<int64_t>(2, lds_max / (dyn + fstat));
         c->fuse_slots = (int32_t)(kFusedCUs * per_cu);
         c->fuse = per_cu >= 1 && c->fuse_slots - c->dlv_blocks >= kFusedCUs / 2;
+        // the forced-row workgroups of the pass keep a statistics slot each
+        if (c->fuse && c->syn_slots < c->fuse_slots) c->syn_slots = c->fuse_slots;
     }
     plan_workspace(c, nullptr);
     return SNN_OK;

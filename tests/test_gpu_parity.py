@@ -204,6 +204,28 @@ def test_delay_blocks_free_run_matches_oracle():
     assert net.stats()["spikes"] > 0
 
 
+def test_fused_pass_statistics_with_few_stdp_slots():
+    """The fused synapse pass gives each of its forced-row workgroups (here
+    496 of them) a statistics slot, also when the slice-STDP grid (one
+    chunk) would size the slots for fewer: every spike delivers exactly its
+    fan-out, and the weight counts match the separate kernels'."""
+    p = wl.preset("stress", n=3000, p_or_fanout=100, p_fire=0.03)
+    a = gpu_net(p, slice_width=512, spike_chunks=2, stdp_chunks=1)
+    b = gpu_net(p, slice_width=512, spike_chunks=2, stdp_chunks=1)
+    for t in range(70):
+        a.step(1, LDS)
+        b.update_neurons()
+        b.update_plasticity()
+        b.deliver_spikes(LDS)
+        b.advance()
+    sa, sb = a.stats(), b.stats()
+    assert sa["delivered_events"] == sa["spikes"] * 100
+    for key in ("spikes", "delivered_events", "stdp_forced_rows", "stdp_synapse_updates",
+                "stdp_weights_written", "device_errors"):
+        assert sa[key] == sb[key], key
+    assert np.array_equal(to_np(a.graph()["w"]), to_np(b.graph()["w"]))
+
+
 def test_out_of_order_calls_rejected():
     p = wl.preset("stress", n=500, p_or_fanout=10, p_fire=0.03)
     net = gpu_net(p, slice_width=128)
