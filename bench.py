@@ -45,7 +45,8 @@ def parse():
     ap.add_argument("--stdp-layout", choices=["rows", "slice"], default="rows")
     ap.add_argument("--stdp-filter", choices=["auto", "codes", "bitmap", "none"],
                     default="auto")
-    ap.add_argument("--history-bits", type=int, choices=[64, 128], default=64)
+    ap.add_argument("--history-bits", type=int, choices=[64, 128], default=None,
+                    help="spike history per neuron (default: the preset's)")
     ap.add_argument("--targets", choices=["preset", "32", "16"], default="preset",
                     help="synapse targets: 32-bit, or 16-bit slice-local (compressed)")
     ap.add_argument("--plasticity", choices=["lazy-event", "lazy", "naive"],
@@ -98,29 +99,30 @@ def load_traffic(kernel, workload_key):
         return None
 
 
-def stdp_bytes(st, n, launches):
-    """Algorithmic bytes of the forced-row STDP kernel (snn_update_plasticity):
-    per synapse update 8 B (32-bit target and weight read), per changed weight
-    4 B (store), per row 40 B (list entry, row pointer, plastic end, source
-    history, t_last and pre trace read and written), per launch 8 B per neuron
-    (the target histories)."""
+def stdp_bytes(st, n, launches, hw=1):
+    """Algorithmic bytes of the forced-row STDP kernel (snn_update_plasticity)
+    with hw 64-bit history words per neuron: per synapse update 8 B (32-bit
+    target and weight read), per changed weight 4 B (store), per row
+    32 + 8 hw B (list entry, row pointer, plastic end, source history, t_last
+    and pre trace read and written), per launch 8 hw B per neuron (the target
+    histories)."""
     return (8 * st["stdp_forced_synapse_updates"] + 4 * st["stdp_forced_weights_written"] +
-            40 * st["stdp_forced_rows"] + 8 * n * launches)
+            (32 + 8 * hw) * st["stdp_forced_rows"] + 8 * hw * n * launches)
 
 
-def delivery_bytes(st, n, n_slices, chunks, nacc, launches, mode, target_bytes=4):
+def delivery_bytes(st, n, n_slices, chunks, nacc, launches, mode, target_bytes=4, hw=1):
     """Algorithmic bytes of delivery with the transmitting rows' STDP: per
     event the target (4 B, or 2 B compressed in LDS mode) and the weight
     (4 B), and 4 B per weight STDP changed there. LDS mode
     adds per (transmitted spike, slice) 20 B (row snapshot or list entry,
-    pivot pair), per launch 12 B per neuron for the targets' histories and
-    post traces (plastic networks) and the slice write-back: nacc * n * 4 B of
+    pivot pair), per launch 8 hw + 4 B per neuron for the targets' histories
+    and post traces (plastic networks) and the slice write-back: nacc * n * 4 B of
     fp32 inputs with one chunk, else C * nacc * n * 8 B of fixed-point
     partial sums. The global mode adds per spike 20 B, per event the 8 B
     atomic update, and per launch the clear of nacc * n * 8 B."""
     ev, tx = st["delivered_events"], st["spikes"]
     wtx = st["stdp_weights_written"] - st["stdp_forced_weights_written"]
-    plastic = 12 * n if st["stdp_rows"] > 0 else 0
+    plastic = (8 * hw + 4) * n if st["stdp_rows"] > 0 else 0
     if mode == "lds":
         wb = 4 * nacc * n if chunks == 1 else 8 * chunks * nacc * n
         return ((target_bytes + 4) * ev + 4 * wtx + 20 * tx * n_slices +
@@ -171,6 +173,7 @@ def main():
     from paper_2107_04092_amd import snn
 
     p = wl.preset(args.config)
+    hbits = args.history_bits or p.history_bits
     width = args.slice_width or p.slice_width
     chunks = args.chunks or p.spike_chunks
     mode = snn.SNN_DELIVER_LDS_SLICE if args.mode == "lds" else snn.SNN_DELIVER_GLOBAL_ATOMIC
@@ -184,7 +187,7 @@ def main():
                                  stdp_layout=0 if args.stdp_layout == "rows" else 1,
                                  stdp_filter=["auto", "codes", "bitmap", "none"].index(
                                      args.stdp_filter),
-                                 history_bits=args.history_bits,
+                                 history_bits=hbits,
                                  plasticity_algorithm=["lazy-event", "lazy", "naive"].index(
                                      args.plasticity),
                                  compressed_targets=(None if args.targets == "preset" else
@@ -222,9 +225,9 @@ def main():
     nacc = 2 if p.model == snn.SNN_LIF_CUBA else 1
     # 16-bit targets are read by slice delivery only; row-wise STDP reads 32-bit
     tb = 2 if cfg.compressed_targets and args.mode == "lds" else 4
-    b_stdp = stdp_bytes(st, p.n, args.steps) / args.steps
+    b_stdp = stdp_bytes(st, p.n, args.steps, hbits // 64) / args.steps
     b_dlv = delivery_bytes(st, p.n, n_slices, chunks, nacc, args.steps, args.mode,
-                           tb) / args.steps
+                           tb, hbits // 64) / args.steps
 
     kernels = None
     roofline = None
@@ -240,9 +243,9 @@ def main():
         kt, nrec = net.kernel_times()
         net.record_kernel_times(0)
         st2 = net.stats()
-        b_stdp = stdp_bytes(st2, p.n, args.steps) / args.steps
+        b_stdp = stdp_bytes(st2, p.n, args.steps, hbits // 64) / args.steps
         b_dlv = delivery_bytes(st2, p.n, n_slices, chunks, nacc, args.steps,
-                               args.mode, tb) / args.steps
+                               args.mode, tb, hbits // 64) / args.steps
         t_neu, t_stdp, t_dlv = kt["neuron"], kt["plasticity"], kt["delivery"]
         kernels = {
             "steps_timed": nrec,
@@ -334,7 +337,7 @@ def main():
                            ["none", "exc-exc", "all"][p.plastic], args.mode, width, chunks),
             "n": p.n, "synapses": e, "slice_width": width, "spike_chunks": chunks,
             "delivery": args.mode, "stdp_layout": args.stdp_layout,
-            "stdp_filter": args.stdp_filter, "history_bits": args.history_bits,
+            "stdp_filter": args.stdp_filter, "history_bits": hbits,
             "target_bits": 16 if cfg.compressed_targets else 32,
             "plasticity": args.plasticity,
             "stdp_slice_mult": args.stdp_mult, "stdp_chunks": args.stdp_chunks, "seed": p.seed,

@@ -585,20 +585,18 @@ static_assert(kDlvBatch == kDlvBlock, "one staged spike per thread");
 // LDS: the staging arrays (DlvShared), then nacc * W accumulators [, W
 // histories, W traces]. Keeping the staging arrays in the dynamic region
 // lets a launch that also runs other work reuse the bytes.
-template <bool CT>
+template <bool CT, typename MapT>
 __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, int nb,
                                                  unsigned char *dyn)
 {
-    DlvShared &S = *reinterpret_cast<DlvShared *>(dyn);
-    long long *acc = reinterpret_cast<long long *>(dyn + sizeof(DlvShared));
+    DlvSharedT<MapT> &S = *reinterpret_cast<DlvSharedT<MapT> *>(dyn);
+    long long *acc = reinterpret_cast<long long *>(dyn + sizeof(DlvSharedT<MapT>));
     long long *s_start = S.start;
     int *s_off = S.off;
-    int *s_half = S.half;
-    int *s_plen = S.plen;
-    int *s_age = S.age;
+    int *s_info = S.info;
     float *s_xp0 = S.xp0;
     float *s_xpn = S.xpn;
-    int *s_map = S.map;
+    MapT *s_map = S.map;
     float *s_dpow = S.dpow;
     long long *sh = S.sh;
     int *shi = S.shi;
@@ -697,9 +695,9 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
             if (r < cnt) {
                 len = p1 - p0;
                 s_start[tid] = rs + p0;
-                s_half[tid] = (a.nacc == 2 && k >= a.n_exc) ? a.width : 0;
-                s_plen[tid] = ap != 0 ? min(max(plen_row - p0, 0), len) : 0;
-                s_age[tid] = ap & 0xff;
+                const int plen = ap != 0 ? min(max(plen_row - p0, 0), len) : 0;
+                const int inh = (a.nacc == 2 && k >= a.n_exc) ? 1 : 0;
+                s_info[tid] = plen | ((ap & 0xff) << 18) | (inh << 26);
                 s_xp0[tid] = xp0;
                 s_xpn[tid] = xpn;
                 if (a.plastic && s == 0 && ap != 0) {
@@ -728,19 +726,19 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
                 // short segments: each thread writes its own segment's entries
                 if (tid < nbt) {
                     const int a0 = max(s_off[tid], e0), a1 = min(s_off[tid + 1], e0 + we);
-                    for (int x = a0; x < a1; ++x) s_map[x - e0] = tid;
+                    for (int x = a0; x < a1; ++x) s_map[x - e0] = (MapT)(tid + 1);
                 }
                 __syncthreads();
             } else {
                 // mark each segment's first entry in the window, then max-scan
-                for (int x = tid; x < we; x += kDlvBlock) s_map[x] = -1;
+                for (int x = tid; x < we; x += kDlvBlock) s_map[x] = 0;
                 __syncthreads();
                 if (tid < nbt) {
                     const int a0 = max(s_off[tid], e0), a1 = min(s_off[tid + 1], e0 + we);
-                    if (a0 < a1) s_map[a0 - e0] = tid;
+                    if (a0 < a1) s_map[a0 - e0] = (MapT)(tid + 1);
                 }
                 __syncthreads();
-                fill_segment_map<kDlvBlock, kDlvUnroll>(s_map, we, shi);
+                fill_segment_map<kDlvBlock, kDlvUnroll, MapT>(s_map, we, shi, 0);
             }
             int tgt[kDlvUnroll], slot[kDlvUnroll], off[kDlvUnroll];
             long long gi[kDlvUnroll];
@@ -752,7 +750,7 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
 #pragma unroll
             for (int u = 0; u < kDlvUnroll; ++u) {
                 const int x = u * kDlvBlock + tid;  // < kDlvWindow
-                const int lm = s_map[x];
+                const int lm = (int)s_map[x] - 1;  // entries are 1 + segment
                 const int l = x < we ? lm : 0;
                 slot[u] = l;
                 off[u] = e0 + x - s_off[l];
@@ -775,8 +773,9 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
                 for (int u = 0; u < kDlvUnroll; ++u) {
                     if (tgt[u] < 0) continue;
                     const int l = slot[u];
-                    if (off[u] >= s_plen[l]) continue;  // not plastic
-                    const int age = s_age[l];
+                    const int info = s_info[l];
+                    if (off[u] >= (info & 0x3ffff)) continue;  // not plastic
+                    const int age = (info >> 18) & 0xff;
                     uint64_t m0, m1;
                     window_masks(age, m0, m1);
                     const uint64_t h1 = hw == 2 ? s_hist[tgt[u] * 2 + 1] & m1 : 0ull;
@@ -793,7 +792,8 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
 #pragma unroll
             for (int u = 0; u < kDlvUnroll; ++u)
                 if (tgt[u] >= 0)
-                    atomicAdd((unsigned long long *)(acc + tgt[u] + s_half[slot[u]]),
+                    atomicAdd((unsigned long long *)(acc + tgt[u] +
+                                                     (((s_info[slot[u]] >> 26) & 1) ? a.width : 0)),
                               (unsigned long long)to_fix(wv[u]));
             if (e0 + kDlvWindow < total) __syncthreads();  // map rewritten by the next window
         }
@@ -833,7 +833,7 @@ template <bool CT>
 __global__ __launch_bounds__(kDlvBlock, 4) void k_deliver_lds(DeliverArgs a)
 {
     extern __shared__ uint4 dyn_dlv[];
-    deliver_lds_body<CT>(a, blockIdx.x, gridDim.x, reinterpret_cast<unsigned char *>(dyn_dlv));
+    deliver_lds_body<CT, int>(a, blockIdx.x, gridDim.x, reinterpret_cast<unsigned char *>(dyn_dlv));
 }
 
 // Fused synapse pass of one step: the forced rows' plasticity and slice
@@ -848,7 +848,8 @@ __global__ __launch_bounds__(kDlvBlock, 4) void k_synapse_pass(DeliverArgs d, St
 {
     extern __shared__ uint4 dyn_pass[];
     if ((int)blockIdx.x < nd)
-        deliver_lds_body<CT>(d, blockIdx.x, nd, reinterpret_cast<unsigned char *>(dyn_pass));
+        deliver_lds_body<CT, FusedMap<HW>>(d, blockIdx.x, nd,
+                                           reinterpret_cast<unsigned char *>(dyn_pass));
     else
         stdp_rows_body<kDlvBlock, HW == 1 ? kStdpRowsUnroll : kStdpRowsUnroll2, HW>(
             s, blockIdx.x - nd, gridDim.x - nd, (unsigned char *)dyn_pass);

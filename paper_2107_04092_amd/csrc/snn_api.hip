@@ -668,7 +668,8 @@ snn_status launch_step_synapse_pass(snn_ctx *c, KernelEvents ev)
     const size_t table = a.code     ? (((size_t)c->n + 15) / 16) * 16
                          : a.recent ? (size_t)c->nw * sizeof(uint64_t)
                                     : 0;
-    const size_t lds = std::max(dlv_lds_bytes(c), table + (size_t)fused_queue_bytes(c->hw));
+    const size_t dlv = dlv_lds_bytes(c) - sizeof(DlvShared) + fused_dlv_shared_bytes(c->hw);
+    const size_t lds = std::max(dlv, table + (size_t)fused_queue_bytes(c->hw));
     snn_status st =
         check_hip(c, launch_synapse_pass(c->stream, d, a, nd, ns, lds, ev), "synapse pass kernel");
     if (st) return st;
@@ -810,7 +811,8 @@ snn_status snn_create(const snn_config *cfg, void *hip_stream, snn_ctx **out)
                               : f == 2 ? map_b
                               : f == 0 ? (fits_code ? code_b : fits_map ? map_b : 0)
                                        : 0;
-        const int64_t dyn = std::max<int64_t>(need, table + fused_queue_bytes(c->hw));
+        const int64_t dlv = need - (int64_t)sizeof(DlvShared) + (int64_t)fused_dlv_shared_bytes(c->hw);
+        const int64_t dyn = std::max<int64_t>(dlv, table + fused_queue_bytes(c->hw));
         const int64_t per_cu = std::min<int64_t>(2, lds_max / (dyn + fstat));
         c->fuse_slots = (int32_t)(kFusedCUs * per_cu);
         c->fuse = per_cu >= 1 && c->fuse_slots - c->dlv_blocks >= kFusedCUs / 2;

@@ -160,19 +160,20 @@ __device__ __forceinline__ long long block_incl_scan_i64_n(long long v, long lon
 }
 
 // Segment map of a window of flattened elements. On entry mark[x] holds the
-// index of the (non-empty) segment that starts at x, or -1; on exit every
+// index of the (non-empty) segment that starts at x, or `none`; on exit every
 // entry holds the index of the segment containing x (an inclusive max-scan,
-// valid because segment indices grow with their start offsets). NT threads,
-// E consecutive entries each; len <= E NT. Ends with a barrier.
-template <int NT, int E = 4>
-__device__ __forceinline__ void fill_segment_map(int *mark, int len, int *sh)
+// valid because segment indices grow with their start offsets; `none` is
+// below every index). NT threads, E consecutive entries each; len <= E NT.
+// Ends with a barrier.
+template <int NT, int E = 4, typename T = int>
+__device__ __forceinline__ void fill_segment_map(T *mark, int len, int *sh, int none = -1)
 {
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
-    int v[E], m = -1;
+    int v[E], m = none;
 #pragma unroll
     for (int q = 0; q < E; ++q) {
         const int x = E * tid + q;
-        const int u = x < len ? mark[x] : -1;
+        const int u = x < len ? (int)mark[x] : none;
         m = max(m, u);
         v[q] = m;
     }
@@ -185,12 +186,12 @@ __device__ __forceinline__ void fill_segment_map(int *mark, int len, int *sh)
     if (lane == kWave - 1) sh[wave] = inc;
     __syncthreads();
     int excl = __shfl_up(inc, 1, kWave);
-    if (lane == 0) excl = -1;
+    if (lane == 0) excl = none;
     for (int q = 0; q < wave; ++q) excl = max(excl, sh[q]);
 #pragma unroll
     for (int q = 0; q < E; ++q) {
         const int x = E * tid + q;
-        if (x < len) mark[x] = max(excl, v[q]);
+        if (x < len) mark[x] = (T)max(excl, v[q]);
     }
     __syncthreads();
 }

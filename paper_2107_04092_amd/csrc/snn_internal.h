@@ -3,6 +3,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <type_traits>
 #include <stdint.h>
 
 namespace snn {
@@ -322,23 +323,37 @@ constexpr int kDlvBlock = 512;         // threads per workgroup of slice deliver
 constexpr int kDlvBatch = 512;         // spikes whose segments slice delivery stages at once
 constexpr int kDlvUnroll = 8;          // flattened elements per thread per window
 constexpr int kDlvWindow = kDlvBlock * kDlvUnroll;
-// Slice delivery's staging arrays, at the start of its dynamic LDS.
-struct DlvShared {
+// Slice delivery's staging arrays, at the start of its dynamic LDS. MapT is
+// the element type of the segment map: int, or uint16_t where LDS is tight
+// (the fused pass with 128-step histories), at the cost of a few registers.
+template <typename MapT>
+struct DlvSharedT {
     long long start[kDlvBatch];        // segment starts (edge index)
     long long sh[kDlvBlock / 64];      // scan scratch
     unsigned long long written;        // weights written by the workgroup
     int off[kDlvBatch + 1];            // segment offsets in the batch
-    int half[kDlvBatch];               // accumulator half (CUBA inhibitory sources)
-    int plen[kDlvBatch];               // plastic elements of each segment
-    int age[kDlvBatch];                // row age (window of the replay)
+    // per segment: plastic elements (bits 0-17), row age (bits 18-25: the
+    // replay window), inhibitory source of a CUBA network (bit 26)
+    int info[kDlvBatch];
     float xp0[kDlvBatch], xpn[kDlvBatch];  // pre traces at the last update and now
-    int map[kDlvWindow];               // element -> segment of the window
+    MapT map[kDlvWindow];              // element -> 1 + segment of the window (0: none)
     float dpow[kMaxAge + 1];           // decay table
     int shi[kDlvBlock / 64];           // scan scratch
     int nlong;                         // segments longer than the direct-map limit
-    int pad_[2];
+    int pad_[3];
 };
-static_assert(sizeof(DlvShared) % 16 == 0, "the accumulators follow 16-byte aligned");
+using DlvShared = DlvSharedT<int>;
+using DlvShared16 = DlvSharedT<uint16_t>;
+// the fused pass's map type: 16-bit with 128-step histories (two workgroups
+// per CU on the stress network), else int
+template <int HW>
+using FusedMap = typename std::conditional<HW == 2, uint16_t, int>::type;
+inline size_t fused_dlv_shared_bytes(int hw)
+{
+    return hw == 2 ? sizeof(DlvShared16) : sizeof(DlvShared);
+}
+static_assert(sizeof(DlvShared) % 16 == 0 && sizeof(DlvShared16) % 16 == 0,
+              "the accumulators follow 16-byte aligned");
 constexpr int kStoreLine = 32;         // weights per store line of the row-wise STDP (128 B)
 constexpr int kStdpRowsSplit = 8;      // most waves that share one row
 

@@ -68,6 +68,7 @@ class Preset:
     slice_width: int = 1024
     spike_chunks: int = 1
     compressed_targets: int = 0  # 16-bit slice-local targets for slice delivery
+    history_bits: int = 64        # spike history per neuron the benchmark runs with
     steps: int = 1000
     seed: int = SEED
 
@@ -117,7 +118,8 @@ PRESETS = {
         graph_kind=GRAPH_FIXED_FANOUT, p_or_fanout=1000, w_exc=0.1, w_inh=0.1,
         delay=1, p_fire=0.005, plastic=PLASTIC_ALL,
         w0=_w0_fixed_point(0.1, 0.11, 0.4),
-        slice_width=2048, spike_chunks=2, compressed_targets=1, steps=1000),
+        slice_width=2048, spike_chunks=2, compressed_targets=1, history_bits=128,
+        steps=1000),
 }
 
 
