@@ -1,0 +1,73 @@
+"""bench.py without a GPU: the one-GPU guard, the algorithmic byte counts the
+roofline divides, and the source digest that keys the committed traffic
+counters."""
+
+import importlib.util
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def bench_module():
+    spec = importlib.util.spec_from_file_location("bench", os.path.join(ROOT, "bench.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout.strip() == ""
+
+
+STATS = {"stdp_forced_synapse_updates": 1000, "stdp_forced_weights_written": 300,
+         "stdp_forced_rows": 7, "delivered_events": 5000, "spikes": 50,
+         "stdp_weights_written": 900, "stdp_rows": 57}
+
+
+@pytest.mark.parametrize("hw", [1, 2])
+def test_stdp_bytes_by_hand(hw):
+    b = bench_module()
+    n, launches = 100, 3
+    want = 8 * 1000 + 4 * 300 + (32 + 8 * hw) * 7 + 8 * hw * n * launches
+    assert b.stdp_bytes(STATS, n, launches, hw) == want
+
+
+@pytest.mark.parametrize("hw", [1, 2])
+@pytest.mark.parametrize("chunks", [1, 2])
+def test_delivery_bytes_by_hand(hw, chunks):
+    b = bench_module()
+    n, s, nacc, launches = 100, 4, 1, 3
+    wb = 4 * nacc * n if chunks == 1 else 8 * chunks * nacc * n
+    want = (2 + 4) * 5000 + 4 * (900 - 300) + 20 * 50 * s + (wb + (8 * hw + 4) * n) * launches
+    assert b.delivery_bytes(STATS, n, s, chunks, nacc, launches, "lds", 2, hw) == want
+    glob = 16 * 5000 + 20 * 50 + 8 * nacc * n * launches
+    assert b.delivery_bytes(STATS, n, s, chunks, nacc, launches, "global", 4, hw) == glob
+
+
+def test_digest_ignores_comments_and_layout():
+    b = bench_module()
+    a = "int f(int x) { // a comment\n  return x + 1; /* block\n comment */ }\n"
+    c = "int f(int x) {\n\n  return    x + 1;   }"
+    norm = lambda t: " ".join(b._COMMENT.sub(" ", t).split())
+    assert norm(a) == norm(c)
+    assert norm(a) != norm(a.replace("x + 1", "x + 2"))
+    assert len(b.kernel_source_digest()) == 16
+
+
+def test_traffic_is_dropped_for_other_sources(monkeypatch):
+    b = bench_module()
+    d = json.load(open(os.path.join(ROOT, "profiles", "traffic.json")))
+    kernel = next(iter(d["stress"]))
+    monkeypatch.setattr(b, "kernel_source_digest", lambda: d["stress"][kernel]["source_digest"])
+    assert b.load_traffic(kernel, "stress") == float(d["stress"][kernel]["bytes_per_launch"])
+    monkeypatch.setattr(b, "kernel_source_digest", lambda: "0" * 16)
+    assert b.load_traffic(kernel, "stress") is None
