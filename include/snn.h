@@ -101,8 +101,11 @@ typedef struct snn_config {
     int32_t delay_steps;  /* D, 1 .. 64: a spike emitted at step t reaches the
                              neuron update of step t+D */
     int32_t slice_width;  /* W for LDS delivery: multiple of 64, and the
-                             W * 8 B fixed-point accumulator (x2 for CUBA)
-                             must fit in the device's LDS (160 KiB) */
+                             W * 8 B fixed-point accumulator (x2 for CUBA),
+                             with plasticity W * (8 * history words + 4) B
+                             of staged histories and post traces, and about
+                             33 KiB of segment staging must fit in the
+                             device's LDS (160 KiB); SNN_EINVAL otherwise */
     int32_t spike_chunks; /* C in 1..64: workgroups that share one slice, each
                              taking 1/C of the spike list (partial sums are
                              added by the next neuron update) */
