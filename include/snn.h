@@ -104,7 +104,7 @@ typedef struct snn_config {
                              W * 8 B fixed-point accumulator (x2 for CUBA),
                              with plasticity W * (8 * history words + 4) B
                              of staged histories and post traces, and about
-                             33 KiB of segment staging must fit in the
+                             29 KiB of segment staging must fit in the
                              device's LDS (160 KiB); SNN_EINVAL otherwise */
     int32_t spike_chunks; /* C in 1..64: workgroups that share one slice, each
                              taking 1/C of the spike list (partial sums are
