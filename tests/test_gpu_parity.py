@@ -12,8 +12,8 @@ import numpy as np
 import pytest
 
 import workloads as wl
-from workloads.presets import PLASTIC_ALL, PLASTIC_NONE, BERNOULLI_SOURCE, LIF_DELTA, \
-    GRAPH_BERNOULLI
+from workloads.presets import PLASTIC_ALL, PLASTIC_EXC_EXC, PLASTIC_NONE, BERNOULLI_SOURCE, \
+    LIF_DELTA, GRAPH_BERNOULLI
 from paper_2107_04092_amd import snn
 
 from gpu_common import (teacher_forced_run, compare_all_plastic_weights, gpu_net, oracle_net,
@@ -27,6 +27,9 @@ CASES = [
     ("tiny", dict(), 300, 256, 1),
     ("tiny", dict(n=1037, n_exc=830), 300, 320, 3),
     ("vogels", dict(), 300, 1024, 2),
+    # CUBA with STDP on exc->exc: the packed segment word carries the
+    # plastic length, the row age and the inhibitory half together
+    ("vogels", dict(n=3000, n_exc=2400, plastic=PLASTIC_EXC_EXC, w0=0.05), 200, 512, 2),
     ("brunel", dict(n=5000, n_exc=4000), 200, 1024, 1),
     ("brunel_plus", dict(n=2500, n_exc=2000), 300, 512, 2),
     ("stress", dict(n=6000, p_or_fanout=200, p_fire=0.02), 200, 1024, 4),
