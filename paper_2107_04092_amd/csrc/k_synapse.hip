@@ -841,7 +841,11 @@ __global__ __launch_bounds__(kDlvBlock, 4) void k_deliver_lds(DeliverArgs a)
 // row does not transmit at t, so the two parts touch disjoint rows, and
 // neither reads what the other writes (targets' histories, post traces and
 // history summaries are only read): workgroups [0, nd) deliver, the others
-// take forced-row parts, side by side, in one launch's ramp and drain.
+// take forced-row parts, side by side, in one launch's ramp and drain. The
+// dynamic LDS is the larger role's (each role lays its own out from the
+// start), so two workgroups share a CU where it is at most half the CU's;
+// four waves per SIMD bound the registers to match. With 128-step
+// histories the delivery role keeps its segment map in 16 bits.
 template <bool CT, int HW>
 __global__ __launch_bounds__(kDlvBlock, 4) void k_synapse_pass(DeliverArgs d, StdpArgs s,
                                                                int32_t nd)
