@@ -280,10 +280,15 @@ snn_status snn_bind_graph(snn_ctx *ctx, void *device_ptr, size_t bytes, int64_t 
 snn_status snn_build_graph_random(snn_ctx *ctx, float w_exc, float w_inh);
 
 /* Builds the graph from an edge list in device memory (src, dst, w each with
- * the n_edges entries given to snn_bind_graph): groups edges by source,
- * sorts each row by (target, weight), then computes pivots and plastic
- * prefixes. Rows longer than 16384 edges are rejected (SNN_EINVAL), as are
- * indices outside [0, n). Synchronises the stream. */
+ * the n_edges entries given to snn_bind_graph) into the data structures of
+ * Fig. 1: an adjacency list grouped by source with every row sorted by
+ * target (ties by weight), the synapse array aligned with it, and per row
+ * the slice pivots (pivot s = the number of the row's entries whose target
+ * lies below s * W, the leading 0 stored explicitly) plus the plastic prefix
+ * length. Construction runs on the device, as in Sec. IV-B. Edge arrays are
+ * borrowed for the call only. Rows longer than 16384 edges are rejected
+ * (SNN_EINVAL), as are indices outside [0, n); SNN_ESTATE before
+ * snn_bind_graph. Synchronises the stream. */
 snn_status snn_build_graph_edges(snn_ctx *ctx, const int32_t *src, const int32_t *dst,
                                  const float *w);
 
@@ -354,7 +359,14 @@ snn_status snn_probe_rows(snn_ctx *ctx, int32_t n_rows, int32_t write, uint64_t 
                           double *ms, int64_t *synapses);
 
 /* Brings every plastic row up to the last completed step t-1 (no pre-
- * synaptic spike), so that all weights equal those of per-step updates. */
+ * synaptic spike), so that all weights equal those of per-step updates.
+ * Under lazy plasticity (Sec. III-A) a row's weights are brought up to date
+ * only when the row transmits or is forced, so between those updates they
+ * lag behind the naive per-step form (Fig. 2(a)); after this call every
+ * weight equals the naive one up to rounding. Enqueues only (row snapshots,
+ * then the row-wise update); a no-op without plastic rows, at t = 0 or with
+ * naive plasticity, whose weights are always current. SNN_ESTATE before the
+ * graph is built. */
 snn_status snn_flush_plasticity(snn_ctx *ctx);
 
 /* Fills *out with device pointers into the workspace and the step index.

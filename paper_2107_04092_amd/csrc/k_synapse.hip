@@ -1018,13 +1018,13 @@ hipError_t launch_deliver_lds(hipStream_t s, const DeliverArgs &a, int blocks, s
     return hipGetLastError();
 }
 
-hipError_t launch_probe_rows(hipStream_t s, const int64_t *row_ptr, const int32_t *pend,
-                             const int32_t *col, float *w, int32_t n_rows, int32_t n_plastic,
-                             uint64_t seed, int32_t write, unsigned long long *sink,
-                             KernelEvents ev)
+hipError_t launch_probe_rows(hipStream_t s, int blocks, const int64_t *row_ptr,
+                             const int32_t *pend, const int32_t *col, float *w, int32_t n_rows,
+                             int32_t n_plastic, uint64_t seed, int32_t write,
+                             unsigned long long *sink, KernelEvents ev)
 {
-    if (n_rows < 1 || n_plastic < 1) return hipErrorInvalidValue;
-    hipExtLaunchKernelGGL(k_probe_rows, dim3(kStdpRowsBlocks), dim3(kStdpRowsBlock), 0, s,
+    if (n_rows < 1 || n_plastic < 1 || blocks < 1) return hipErrorInvalidValue;
+    hipExtLaunchKernelGGL(k_probe_rows, dim3(blocks), dim3(kStdpRowsBlock), 0, s,
                           ev.start, ev.stop, 0, row_ptr, pend, col, w, n_rows, n_plastic, seed,
                           write, sink);
     return hipGetLastError();

@@ -26,6 +26,7 @@ struct snn_ctx {
     int32_t n_plastic_rows = 0, ref_steps = 0, dlv_blocks = 0;
     int32_t stdp_mult = 1, stdp_width = 0, stdp_groups = 0, stdp_chunks = 1, stdp_grid = 0;
     int32_t info_blocks = 1, syn_slots = 1;
+    int32_t n_cu = 1;  // compute units of the device: one row-STDP workgroup each
     int32_t hw = 1;  // 64-bit history words per neuron
     int32_t algo = 0;  // plasticity_algorithm: 0 lazy + event, 1 lazy, 2 naive
     bool ct = false;  // compressed targets: 16-bit slice-local indices for slice delivery
@@ -495,9 +496,9 @@ size_t dlv_lds_bytes(const snn_ctx *c)
 }
 
 // Arguments of the synapse pass over the forced rows (flush: all rows).
-StdpArgs stdp_args(snn_ctx *c, bool flush,
-                   int64_t waves = (int64_t)kStdpRowsBlocks * (kStdpRowsBlock / kWave))
+StdpArgs stdp_args(snn_ctx *c, bool flush, int64_t waves = 0)
 {
+    if (waves <= 0) waves = (int64_t)c->n_cu * (kStdpRowsBlock / kWave);
     StdpArgs a{};
     a.info = c->info;
     a.row_cnt = flush ? nullptr : c->row_cnt;
@@ -585,7 +586,7 @@ snn_status launch_plasticity(snn_ctx *c, bool flush, hipStream_t s, KernelEvents
     }
     StdpArgs a = stdp_args(c, flush);
     if (c->cfg.stdp_layout == 0)
-        return check_hip(c, launch_stdp_rows(s, a, kStdpRowsBlocks, ev), "STDP kernel");
+        return check_hip(c, launch_stdp_rows(s, a, c->n_cu, ev), "STDP kernel");
     const size_t lds = (size_t)c->stdp_width * (c->hw * sizeof(uint64_t) + sizeof(float));
     return check_hip(c, launch_stdp(s, a, c->stdp_grid, lds, ev), "STDP kernel");
 }
@@ -612,7 +613,7 @@ snn_status launch_step_plasticity(snn_ctx *c)
         a.mu = c->mu;
         a.stats = c->syn_stats;
         a.syn_count = c->gstats + kGNaiveSyn;
-        return check_hip(c, launch_stdp_naive(c->stream, a, kStdpRowsBlocks, part_events(c, 1)),
+        return check_hip(c, launch_stdp_naive(c->stream, a, c->n_cu, part_events(c, 1)),
                          "naive STDP");
     }
     return launch_plasticity(c, false, c->stream, part_events(c, 1));
@@ -702,7 +703,7 @@ snn_status launch_step_delivery(snn_ctx *c, int32_t mode)
         StdpArgs r = stdp_args(c, false);
         r.info = c->txinfo;
         r.row_cnt = a.cnt;
-        st = check_hip(c, launch_stdp_rows(c->stream, r, kStdpRowsBlocks, {ev.start, nullptr}),
+        st = check_hip(c, launch_stdp_rows(c->stream, r, c->n_cu, {ev.start, nullptr}),
                        "STDP of transmitting rows");
         if (st) return st;
         last.start = nullptr;
@@ -753,6 +754,10 @@ snn_status snn_create(const snn_config *cfg, void *hip_stream, snn_ctx **out)
     if (hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, c->device) !=
         hipSuccess)
         return fail(c, SNN_EDEVICE, "cannot query the LDS size");
+    if (hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, c->device) !=
+            hipSuccess ||
+        c->n_cu < 1)
+        return fail(c, SNN_EDEVICE, "cannot query the compute-unit count");
     const int stat = deliver_lds_static_bytes();
     const int stat_stdp = stdp_static_bytes();
     if (stat < 0 || stat_stdp < 0) return fail(c, SNN_EDEVICE, "cannot query the kernels");
@@ -794,7 +799,7 @@ snn_status snn_create(const snn_config *cfg, void *hip_stream, snn_ctx **out)
         const int64_t work = (int64_t)c->stdp_groups * chunks;
         if (work > (1 << 20)) return fail(c, SNN_EINVAL, "too many STDP work items");
         c->stdp_grid = (int32_t)((work + 7) / 8 * 8);
-        c->syn_slots = c->stdp_grid > kStdpRowsBlocks ? c->stdp_grid : kStdpRowsBlocks;
+        c->syn_slots = c->stdp_grid > c->n_cu ? c->stdp_grid : c->n_cu;
     }
     // The fused synapse pass: its static LDS beside the larger of the two
     // parts' dynamic LDS gives the workgroups a CU holds; it is used when
@@ -814,8 +819,8 @@ snn_status snn_create(const snn_config *cfg, void *hip_stream, snn_ctx **out)
         const int64_t dlv = need - (int64_t)sizeof(DlvShared) + (int64_t)fused_dlv_shared_bytes(c->hw);
         const int64_t dyn = std::max<int64_t>(dlv, table + fused_queue_bytes(c->hw));
         const int64_t per_cu = std::min<int64_t>(2, lds_max / (dyn + fstat));
-        c->fuse_slots = (int32_t)(kFusedCUs * per_cu);
-        c->fuse = per_cu >= 1 && c->fuse_slots - c->dlv_blocks >= kFusedCUs / 2;
+        c->fuse_slots = (int32_t)(c->n_cu * per_cu);
+        c->fuse = per_cu >= 1 && c->fuse_slots - c->dlv_blocks >= c->n_cu / 2;
         // the forced-row workgroups of the pass keep a statistics slot each
         if (c->fuse && c->syn_slots < c->fuse_slots) c->syn_slots = c->fuse_slots;
     }
@@ -1228,7 +1233,7 @@ snn_status snn_probe_rows(snn_ctx *c, int32_t n_rows, int32_t write, uint64_t se
     hipError_t e = hipEventCreate(&ev[0]);
     if (e == hipSuccess) e = hipEventCreate(&ev[1]);
     if (e == hipSuccess)
-        e = launch_probe_rows(c->stream, c->row_ptr, c->pend, c->col, c->w, n_rows,
+        e = launch_probe_rows(c->stream, c->n_cu, c->row_ptr, c->pend, c->col, c->w, n_rows,
                               c->n_plastic_rows, seed, write ? 1 : 0,
                               (unsigned long long *)c->scratch, KernelEvents{ev[0], ev[1]});
     std::vector<int32_t> pend((size_t)c->n_plastic_rows);
