@@ -103,6 +103,7 @@ def _load():
         "oracle_get_spikes": (None, [P, P, P]),
         "oracle_get_graph": (None, [P, P, P, P]),
         "oracle_get_traces": (None, [P, P, P]),
+        "oracle_get_weights_at": (None, [P, P, i64, P]),
         "oracle_threads": (i32, []),
         "oracle_set_threads": (None, [i32]),
         "oracle_bernoulli_synapse": (f64, [P, i32, i32, f64, i64]),
@@ -232,6 +233,16 @@ class Oracle:
 
     def weights(self):
         return self.graph()[2]
+
+    def weights_at(self, idx):
+        """Weights of the given edge indices (without copying every weight)."""
+        idx = np.ascontiguousarray(idx, dtype=np.int64)
+        out = np.zeros(len(idx), dtype=np.float64)
+        if len(idx):
+            if idx.min() < 0 or idx.max() >= self.n_edges:
+                raise IndexError("edge index out of range")
+            self._lib.oracle_get_weights_at(self._h, _ptr(idx), len(idx), _ptr(out))
+        return out
 
     def traces(self):
         e = self.n_edges

@@ -546,6 +546,12 @@ void oracle_get_graph(const oracle *o, int64_t *row_ptr, int32_t *col, double *w
     if (w) memcpy(w, o->w, (size_t)o->n_edges * sizeof(double));
 }
 
+/* The weights of the given edges (count indices into the edge arrays). */
+void oracle_get_weights_at(const oracle *o, const int64_t *idx, int64_t count, double *out)
+{
+    for (int64_t q = 0; q < count; ++q) out[q] = o->w[idx[q]];
+}
+
 void oracle_get_traces(const oracle *o, double *x_pre, double *x_post)
 {
     if (!o->x_pre) return;

@@ -145,19 +145,23 @@ def compare_rows(net, o, rows, what, graph_cache):
         return 0
     torch = torch_mod()
     gw = to_np(g["w"][torch.from_numpy(idx).to(g["w"].device)])
-    ow = o.weights()[idx]
+    ow = o.weights_at(idx)
     assert_close(gw, ow, what)
     return len(idx)
 
 
 def teacher_forced_run(p, steps, mode, slice_width=None, spike_chunks=None, check_every=1,
-                       **cfg_kw):
-    """Runs `steps` teacher-forced steps; returns (net, oracle, counters)."""
+                       progress=0, **cfg_kw):
+    """Runs `steps` teacher-forced steps; returns (net, oracle, counters).
+    With progress > 0 a line is logged every `progress` steps."""
     net = gpu_net(p, slice_width, spike_chunks, **cfg_kw)
     o = oracle_net(p)
     cache = {}
     n_rows = n_w = n_spk = 0
     for t in range(steps):
+        if progress and t % progress == 0:
+            log("  teacher-forced step %d/%d (%d rows, %d weights checked)" % (
+                t, steps, n_rows, n_w))
         force_from_oracle(net, o, t)
         o.step()
         net.step(1, mode)

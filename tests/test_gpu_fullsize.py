@@ -1,5 +1,7 @@
-"""Full-size stress network (250,000 Bernoulli sources, fan-out 1,000, 250M
-plastic synapses) in the launch configuration the benchmark times.
+"""Full-size networks in the launch configurations the benchmark times: the
+stress network (250,000 Bernoulli sources, fan-out 1,000, 250M plastic
+synapses), the Brunel network (390M synapses) and Brunel with STDP (25,000
+neurons, 62.5M synapses, 40M of them plastic).
 
 The oracle cannot step a network this size in seconds, but every spike here
 is a counter-based draw, so single outputs are computable one by one: the
@@ -13,7 +15,8 @@ import pytest
 import workloads as wl
 from paper_2107_04092_amd import snn
 
-from gpu_common import gpu_net, oracle_net, to_np, hist_np, assert_close, log
+from gpu_common import (gpu_net, oracle_net, to_np, hist_np, assert_close, log, rate_hz,
+                        teacher_forced_run, compare_all_plastic_weights)
 
 pytestmark = pytest.mark.gpu
 
@@ -150,3 +153,50 @@ def test_brunel_full_size_delay_block():
     for k in list(rows)[:16]:
         assert np.array_equal(to_np(g["col"][rp[k]:rp[k + 1]]), row(k)), k
     log("  block checked: %d spiking rows, %d events" % (len(rows), events))
+
+
+def test_brunel_plus_full_size_teacher_forced():
+    """Brunel with STDP at its stated size (25,000 LIF neurons with Poisson
+    drive, p = 0.1: 62.5M synapses, STDP on the 40M exc->exc ones, D = 15)
+    in the benchmark's launch configuration (W = 1024, four chunks, 16-bit
+    slice-local targets, the fused synapse pass). 150 teacher-forced steps:
+    every step spikes, histories, potentials and refractory counts are
+    bit-exact, the delivered input is within tolerance, and so are the weights
+    of every row made current (forced rows from step 63 on, transmitting rows
+    from step 14 on); after a flush, every plastic weight."""
+    p = wl.preset("brunel_plus")
+    log("full-size brunel_plus: n=%d p=%g D=%d W=%d C=%d" % (
+        p.n, p.p_or_fanout, p.delay, p.slice_width, p.spike_chunks))
+    net, o, cnt = teacher_forced_run(p, 150, snn.SNN_DELIVER_LDS_SLICE, progress=25)
+    log("  %d rows, %d weights, %d spikes checked" % (cnt["rows"], cnt["weights"], cnt["spikes"]))
+    assert cnt["spikes"] > 0 and cnt["rows"] > 0 and cnt["weights"] > 0
+    st = net.stats()
+    assert st["stdp_forced_rows"] > 0
+    assert st["device_errors"] == 0
+    net.flush_plasticity()
+    n_w = compare_all_plastic_weights(net, o)
+    log("  all %d plastic weights equal after the flush" % n_w)
+    assert n_w > 39_000_000
+
+
+def test_brunel_plus_full_size_free_running_rate():
+    """Brunel with STDP at its stated size runs free for 1 s of network time
+    (10,000 steps) on both sides: the mean firing rates agree within 2%. The
+    two runs share every external Poisson draw but drift apart spike by spike
+    as the weights' roundings differ, so only the rate is compared."""
+    p = wl.preset("brunel_plus")
+    steps = 10_000
+    log("full-size brunel_plus free run: %d steps" % steps)
+    net = gpu_net(p)
+    o = oracle_net(p)
+    for done in range(0, steps, 1000):
+        net.step(1000, snn.SNN_DELIVER_LDS_SLICE)
+        o.step(1000)
+        log("  %d/%d steps: gpu %d spikes, oracle %d" % (
+            done + 1000, steps, net.stats()["spikes"], o.spikes_total))
+    g, r = net.stats()["spikes"], o.spikes_total
+    rg, ro = rate_hz(g, p.n, steps), rate_hz(r, p.n, steps)
+    log("  gpu %.3f Hz, oracle %.3f Hz" % (rg, ro))
+    assert net.stats()["device_errors"] == 0
+    assert r >= 100_000
+    assert abs(rg - ro) <= 0.02 * ro
