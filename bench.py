@@ -6,13 +6,26 @@ targets + fp32 weights), power-law STDP on every synapse, delay 1 step.
 
 One step = neuron update (with the spike and row lists), lazy + event-driven STDP
 of the forced rows, and slice (LDS) delivery with the transmitting rows'
-STDP. Timed region: K steps issued by one snn_step call, bracketed by device
-synchronisation. Then K more steps run with the library's kernel timing:
-every kernel launch places HIP events around itself on the library's
-stream, which gives per-kernel device times (the events widen the gaps
-between kernels, so the timed region runs without them). The roofline
-figure of the dominant kernel (forced-row STDP) is its algorithmic bytes
-per launch over its device time.
+STDP. Before the timed region the network runs max(--warmup, 2 x history
+length) untimed steps, so that every history window is full and the forced
+rows have left their staggered start: the timed steps are steady state
+whatever --warmup says. Timed region: K steps issued by one snn_step call,
+bracketed by device synchronisation. Then K more steps run with the
+library's kernel timing: every kernel launch places HIP events around
+itself on the library's stream, which gives per-kernel device times (the
+events widen the gaps between kernels, so the timed region runs without
+them).
+
+The roofline figure of the dominant kernel (the fused synapse pass, or the
+forced-row STDP where the step runs it alone) divides the method's
+algorithmic bytes per step by the kernel's device time. Those bytes follow
+the survey's per-step count (targets and weights read and changed weights
+written per STDP synapse update, row state per triggered row, the gathered
+histories and post traces once per neuron, the age scan, 8 B per delivered
+event, the pivots of each delivered row, the slice write-back), less the
+delivery re-read of the transmitting rows' targets and weights, which a
+fused pass reads once. The bytes this implementation moves by design
+(fixed-point partials, snapshots, staging) are reported beside it.
 
 Prints one JSON line. `--gpus N` with N > 1 exits: the benchmark runs on one GPU.
 """
@@ -55,7 +68,10 @@ def parse():
     ap.add_argument("--stdp-mult", type=int, default=0)
     ap.add_argument("--stdp-chunks", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="time budget of the oracle on all its threads")
+    ap.add_argument("--cpu-seconds-1t", type=float, default=10.0,
+                    help="time budget of the oracle on one thread (0: skip)")
     ap.add_argument("--no-instrumented", action="store_true",
                     help="no per-kernel event timing (plain timed steps)")
     ap.add_argument("--no-row-probe", action="store_true",
@@ -99,20 +115,48 @@ def load_traffic(kernel, workload_key):
         return None
 
 
+def survey_bytes(st, steps, n, n_slices, chunks, nacc, fused):
+    """The method's algorithmic bytes per step, counted as the survey's
+    measurement section writes them (per-step averages of the counters):
+      STDP      12 B per synapse update (target and weight read, weight
+                written), 16 B per triggered row (t_last and pre trace read
+                and written), 12 B per neuron (the gathered history word and
+                post trace, once), 4 B per neuron (the age scan);
+      delivery  8 B per delivered event (target and weight), (S+1) x 4 B of
+                pivots per delivered row, C x nacc x 4 B per neuron of slice
+                write-back;
+      fused     less 8 B per synapse update of a transmitting row: a pass that
+                makes those rows current inside delivery reads their targets
+                and weights once (the survey's fused-pass deduction).
+    Delivered rows are the spikes emitted in the same steps (equal to the
+    transmitted ones in steady state). Returns a dict of floats."""
+    u = st["stdp_synapse_updates"] / steps
+    r = st["stdp_rows"] / steps
+    ev = st["delivered_events"] / steps
+    tx = st["spikes"] / steps
+    u_tx = (st["stdp_synapse_updates"] - st["stdp_forced_synapse_updates"]) / steps
+    plastic = st["stdp_rows"] > 0
+    stdp = (12 * u + 16 * r + 12 * n + 4 * n) if plastic else 0.0
+    dlv = 8 * ev + tx * (n_slices + 1) * 4 + chunks * n * 4 * nacc
+    deduct = 8 * min(ev, u_tx) if (fused and plastic) else 0.0
+    return {"stdp": stdp, "delivery": dlv, "as_written": stdp + dlv,
+            "fused_deduction": deduct, "algorithmic": stdp + dlv - deduct}
+
+
 def stdp_bytes(st, n, launches, hw=1):
-    """Algorithmic bytes of the forced-row STDP kernel (snn_update_plasticity)
-    with hw 64-bit history words per neuron: per synapse update 8 B (32-bit
-    target and weight read), per changed weight 4 B (store), per row
-    32 + 8 hw B (list entry, row pointer, plastic end, source history, t_last
-    and pre trace read and written), per launch 8 hw B per neuron (the target
-    histories)."""
+    """Bytes the forced-row STDP kernel (snn_update_plasticity) of this
+    implementation moves, with hw 64-bit history words per neuron: per
+    synapse update 8 B (32-bit target and weight read), per changed weight
+    4 B (store), per row 32 + 8 hw B (list entry, row pointer, plastic end,
+    source history, t_last and pre trace read and written), per launch
+    8 hw B per neuron (the target histories)."""
     return (8 * st["stdp_forced_synapse_updates"] + 4 * st["stdp_forced_weights_written"] +
             (32 + 8 * hw) * st["stdp_forced_rows"] + 8 * hw * n * launches)
 
 
 def delivery_bytes(st, n, n_slices, chunks, nacc, launches, mode, target_bytes=4, hw=1):
-    """Algorithmic bytes of delivery with the transmitting rows' STDP: per
-    event the target (4 B, or 2 B compressed in LDS mode) and the weight
+    """Bytes this implementation's delivery with the transmitting rows' STDP
+    moves: per event the target (4 B, or 2 B compressed in LDS mode) and the weight
     (4 B), and 4 B per weight STDP changed there. LDS mode
     adds per (transmitted spike, slice) 20 B (row snapshot or list entry,
     pivot pair), per launch 8 hw + 4 B per neuron for the targets' histories
@@ -130,9 +174,25 @@ def delivery_bytes(st, n, n_slices, chunks, nacc, launches, mode, target_bytes=4
     return 16 * ev + 20 * tx + 8 * nacc * n * launches
 
 
-def cpu_baseline(p, seconds):
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo) and its logical CPUs."""
+    name = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    name = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return name, os.cpu_count()
+
+
+def cpu_baseline(p, seconds, seconds_1t):
     """The oracle as it stands on this host's cores: naive dense STDP over all
-    synapses every step plus row-wise delivery, a prefix of the same workload."""
+    synapses every step plus row-wise delivery, a prefix of the same workload
+    with all of the oracle's OpenMP threads, then one more prefix on one
+    thread (each bounded by its time budget)."""
     from oracle import oracle
     import workloads as wl
     o = oracle.Oracle(p, wl.poisson_cdf_table(p.poisson_mu))
@@ -140,25 +200,51 @@ def cpu_baseline(p, seconds):
     o.build_random()
     o.set_neurons(**wl.initial_state(p))
     build_s = time.time() - t0
-    rp = None
-    events = 0
-    steps = 0
-    t0 = time.time()
-    while True:
-        o.step()
-        steps += 1
-        _, lst = o.spikes()
-        if rp is None:
-            rp = o.graph()[0]
-        events += int((rp[lst + 1] - rp[lst]).sum())
-        el = time.time() - t0
-        if el >= seconds or steps >= 200:
-            break
-    return {"value": events / el, "unit": "synaptic events/s", "cores": oracle.threads(),
+    rp = o.graph()[0]
+
+    def run(budget, max_steps):
+        events = steps = 0
+        t0 = time.time()
+        while True:
+            o.step()
+            steps += 1
+            _, lst = o.spikes()
+            events += int((rp[lst + 1] - rp[lst]).sum())
+            el = time.time() - t0
+            if el >= budget or steps >= max_steps:
+                return events, steps, el
+
+    threads = oracle.threads()
+    ev, steps, el = run(seconds, 200)
+    one = None
+    if seconds_1t > 0:
+        oracle.set_threads(1)
+        try:
+            ev1, steps1, el1 = run(seconds_1t, 200)
+        finally:
+            oracle.set_threads(threads)
+        one = {"value": ev1 / el1, "unit": "synaptic events/s", "cores": 1,
+               "steps": steps1, "s_per_step": round(el1 / steps1, 4)}
+    model, ncpu = cpu_model()
+    return {"value": ev / el, "unit": "synaptic events/s", "cores": threads,
             "kind": "oracle",
-            "sample": "%s workload at full size (n=%d, %d synapses), first %d steps after a "
-                      "%.1f s build; dense per-synapse STDP every step + row-wise delivery; "
-                      "%.3f s/step" % (p.name, p.n, o.n_edges, steps, build_s, el / steps)}
+            "sample": "%s workload at full size (n=%d, %d synapses), steps 1-%d after a "
+                      "%.1f s build, %d OpenMP threads; dense per-synapse STDP every step + "
+                      "row-wise delivery; %.3f s/step"
+                      % (p.name, p.n, o.n_edges, steps, build_s, threads, el / steps),
+            "single_thread": one,
+            "cpu_model": model, "host_logical_cpus": ncpu}
+
+
+def check_device_errors(net, where):
+    """Ends the benchmark if a kernel flagged an error condition (a row
+    behind its history window, a ring inconsistency): its numbers would be
+    those of a wrong simulation."""
+    err = net.stats()["device_errors"]
+    if err:
+        print("bench.py: device error flags 0x%x after the %s; no result" % (err, where),
+              file=sys.stderr)
+        sys.exit(1)
 
 
 def main():
@@ -200,9 +286,13 @@ def main():
     torch.cuda.synchronize()
     setup_s = time.time() - t0
 
-    # warm-up (untimed)
-    net.step(args.warmup, mode)
+    # untimed steps: the requested warm-up, and at least two history lengths,
+    # so that every window is full and the forced rows are past their
+    # staggered start (steady state)
+    untimed = max(args.warmup, 2 * hbits)
+    net.step(untimed, mode)
     torch.cuda.synchronize()
+    check_device_errors(net, "untimed steps")
     net.reset_stats()
 
     # timed region: exactly K steps
@@ -217,6 +307,7 @@ def main():
     wall = time.perf_counter() - t_wall
     ms_total = start.elapsed_time(end)
     st = net.stats()
+    check_device_errors(net, "timed steps")
     ms_per_step = ms_total / args.steps
     events_per_s = st["delivered_events"] / (ms_total * 1e-3)
     stdp_per_s = st["stdp_synapse_updates"] / (ms_total * 1e-3)
@@ -267,19 +358,39 @@ def main():
         # a plastic network whose step ran plasticity and delivery in one
         # launch (the fused synapse pass) records it as the delivery part
         fused = p.plastic != 0 and t_stdp == 0 and t_dlv > 0 and b_stdp > 0
+        sb = survey_bytes(st2, args.steps, p.n, n_slices, chunks, nacc,
+                          fused or (args.mode == "lds" and p.plastic != 0))
         if fused:
             kname = "k_synapse_pass"
-            ach = (b_stdp + b_dlv) / (t_dlv * 1e-3) / 1e9
+            t_k = t_dlv
+            alg = sb["algorithmic"]
+            written = sb["as_written"]
+            impl = b_stdp + b_dlv
         elif t_stdp > 0:
-            ach = b_stdp / (t_stdp * 1e-3) / 1e9
+            # the forced rows' share of the STDP count, the kernel's own
+            # (delivery makes the transmitting rows current)
+            f = st2["stdp_forced_synapse_updates"] / args.steps
+            rf = st2["stdp_forced_rows"] / args.steps
+            t_k = t_stdp
+            alg = written = 12 * f + 16 * rf + 16 * p.n
+            impl = b_stdp
         if fused or t_stdp > 0:
+            ach = alg / (t_k * 1e-3) / 1e9
             traffic = load_traffic(kname, p.name)
             roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
                         "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
-                        "traffic": traffic, "kernel": kname}
-            comb = (b_stdp + b_dlv) / ((t_stdp + t_dlv) * 1e-3) / 1e9
+                        "traffic": traffic, "kernel": kname,
+                        "kernel_us": round(t_k * 1e3, 3),
+                        "bytes_per_launch": int(alg),
+                        "bytes_as_written": int(written),
+                        "frac_as_written": round(written / (t_k * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                        "implementation_bytes_per_launch": int(impl),
+                        "traffic_over_algorithmic": (round(traffic / alg, 3)
+                                                     if traffic else None)}
+            comb = sb["algorithmic"] / ((t_stdp + t_dlv) * 1e-3) / 1e9
             combined = {"achieved_GBs": round(comb, 1), "frac": round(comb / HBM_PEAK_GBS, 4),
-                        "us_per_step": round((t_stdp + t_dlv) * 1e3, 3)}
+                        "us_per_step": round((t_stdp + t_dlv) * 1e3, 3),
+                        "survey_bytes_per_step": {k: int(v) for k, v in sb.items()}}
 
     ceiling = None
     if roofline is not None and kname in ("k_stdp_rows", "k_synapse_pass") and \
@@ -313,7 +424,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(p, args.cpu_seconds)
+        cpu = cpu_baseline(p, args.cpu_seconds, args.cpu_seconds_1t)
 
     out = {
         "metric": METRIC,
@@ -322,6 +433,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "untimed_steps": untimed,
         "ms_per_step": ms_per_step,
         "higher_is_better": True,
         "scaling": "weak",
@@ -349,7 +461,7 @@ def main():
         "row_stream_ceiling": ceiling,
         "kernels": kernels,
         "stats": {k: int(v) for k, v in st.items()},
-        "bytes_per_step": {"stdp": int(b_stdp), "delivery": int(b_dlv)},
+        "implementation_bytes_per_step": {"stdp": int(b_stdp), "delivery": int(b_dlv)},
         "setup_s": round(setup_s, 3),
         "host_wall_s": round(wall, 4),
     }

@@ -53,6 +53,37 @@ def test_delivery_bytes_by_hand(hw, chunks):
     assert b.delivery_bytes(STATS, n, s, chunks, nacc, launches, "global", 4, hw) == glob
 
 
+def test_survey_bytes_by_hand():
+    """The survey's per-step count on the stress network in steady state
+    (2,639 rows made current, 1,388 of them forced, 1,251 spikes of 1,000
+    synapses, 123 slices, two chunks): 48.3 MB as the count is written,
+    38.3 MB less the fused pass's single read of the transmitting rows."""
+    b = bench_module()
+    steps, n = 10, 250_000
+    st = {"stdp_synapse_updates": 2_639_000 * steps, "stdp_rows": 2_639 * steps,
+          "stdp_forced_synapse_updates": 1_388_000 * steps, "delivered_events": 1_251_000 * steps,
+          "spikes": 1_251 * steps}
+    sb = b.survey_bytes(st, steps, n, 123, 2, 1, fused=True)
+    stdp = 12 * 2_639_000 + 16 * 2_639 + 16 * n
+    dlv = 8 * 1_251_000 + 1_251 * 124 * 4 + 2 * n * 4
+    assert sb["stdp"] == pytest.approx(stdp) and sb["delivery"] == pytest.approx(dlv)
+    assert sb["as_written"] == pytest.approx(48.34e6, rel=1e-3)
+    assert sb["algorithmic"] == pytest.approx(stdp + dlv - 8 * 1_251_000, rel=1e-12)
+    assert sb["algorithmic"] == pytest.approx(38.33e6, rel=1e-3)
+    # no deduction where delivery re-reads the rows (global atomics), and no
+    # STDP bytes without plastic rows
+    assert b.survey_bytes(st, steps, n, 123, 2, 1, fused=False)["fused_deduction"] == 0
+    st0 = dict(st, stdp_rows=0, stdp_synapse_updates=0, stdp_forced_synapse_updates=0)
+    assert b.survey_bytes(st0, steps, n, 123, 2, 1, fused=True)["stdp"] == 0
+
+
+def test_cpu_model_reads_the_host():
+    b = bench_module()
+    name, ncpu = b.cpu_model()
+    assert ncpu >= 1
+    assert name is None or isinstance(name, str)
+
+
 def test_digest_ignores_comments_and_layout():
     b = bench_module()
     a = "int f(int x) { // a comment\n  return x + 1; /* block\n comment */ }\n"
