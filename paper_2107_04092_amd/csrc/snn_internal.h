@@ -311,14 +311,13 @@ hipError_t launch_stdp(hipStream_t s, const StdpArgs &a, int blocks, size_t lds,
 hipError_t launch_stdp_rows(hipStream_t s, const StdpArgs &a, int blocks, KernelEvents ev = {});
 hipError_t launch_stdp_naive(hipStream_t s, const NaiveArgs &a, int blocks, KernelEvents ev = {});
 // k_probe_rows: measurement only (sink: one scratch word)
-hipError_t launch_probe_rows(hipStream_t s, const int64_t *row_ptr, const int32_t *pend,
-                             const int32_t *col, float *w, int32_t n_rows, int32_t n_plastic,
-                             uint64_t seed, int32_t write, unsigned long long *sink,
-                             KernelEvents ev);
+hipError_t launch_probe_rows(hipStream_t s, int blocks, const int64_t *row_ptr,
+                             const int32_t *pend, const int32_t *col, float *w, int32_t n_rows,
+                             int32_t n_plastic, uint64_t seed, int32_t write,
+                             unsigned long long *sink, KernelEvents ev);
 constexpr int kStdpRowsBlock = 1024;   // threads of the row-wise STDP kernel
 constexpr int kStdpRowsUnroll = 8;     // synapses per lane and row part (64-step histories)
 constexpr int kStdpRowsUnroll2 = 4;    // the same with 128-step histories
-constexpr int kStdpRowsBlocks = 256;   // its persistent grid (one workgroup per CU)
 constexpr int kDlvBlock = 512;         // threads per workgroup of slice delivery
 constexpr int kDlvBatch = 512;         // spikes whose segments slice delivery stages at once
 constexpr int kDlvUnroll = 8;          // flattened elements per thread per window
@@ -366,9 +365,10 @@ constexpr int stdp_rows_queue_bytes(int hw)
 }
 // the per-neuron summary it stages beside the queues (160 KB of LDS per workgroup)
 constexpr int kCodeMax = 163840 - stdp_rows_queue_bytes(1) - 1024;  // bytes of history codes
-// The fused synapse pass (k_synapse_pass): its workgroups fill the slots of
-// every CU (one or two per CU, as the LDS of both parts allows).
-constexpr int kFusedCUs = 256;  // CUs: the pass has kFusedCUs slots per workgroup a CU holds
+// The row-wise STDP kernel runs one workgroup per CU, and the fused synapse
+// pass (k_synapse_pass) fills the slots of every CU (one or two workgroups
+// per CU, as the LDS of both parts allows): both grids come from the CU
+// count of the device (hipDeviceAttributeMultiprocessorCount).
 constexpr int fused_queue_bytes(int hw)
 {
     return (kDlvBlock / kWave) * (hw == 2 ? kStdpRowsUnroll2 : kStdpRowsUnroll) * kWave * 8;
