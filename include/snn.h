@@ -10,10 +10,10 @@
  *   (3) deliver spikes to the neurons' neighbours.
  * Every part runs in hand-written HIP kernels:
  *   - (1) emits a 64-bit firing mask word per 64 neurons (one wave64 ballot),
- *     a spike list (each workgroup appends its spikes at a reserved offset;
- *     snn_get_state puts the lists in ascending order), and shifts each neuron's firing history of
- *     one or two 64-bit words (least significant bit = most recent step,
- *     Fig. 2);
+ *     an ascending spike list (each workgroup learns where its stretch starts
+ *     by a look-back over the counts of the workgroups before it), and shifts
+ *     each neuron's firing history of one or two 64-bit words (least
+ *     significant bit = most recent step, Fig. 2);
  *   - a ring of the last D spike lists implements the network-wide delay;
  *   - (2) is lazy + event-driven STDP (Sec. III-A, Fig. 2(b,c)): only rows
  *     that transmit this step are brought up to date, replaying the missed
@@ -45,6 +45,12 @@
  *     enqueued and snn_last_error(ctx) describes the problem. Asynchronous
  *     kernel faults surface as SNN_EDEVICE at the next synchronising call.
  *   - Threads. A context is bound to one stream and is not thread-safe.
+ *   - Time. The step index and the source of the next input live on the
+ *     device (in the workspace): the neuron update advances the step there,
+ *     and no launch of a step depends on its index, so a step captured into
+ *     a HIP graph (snn_graph_capture) replays correctly. The host's view of
+ *     the step follows the calls made, and is read back from the device by
+ *     the calls that synchronise (snn_get_state).
  */
 #ifndef SNN_H
 #define SNN_H
@@ -162,6 +168,9 @@ typedef struct snn_config {
 
 typedef struct snn_ctx snn_ctx;
 
+/* A captured sequence of steps (snn_graph_capture); opaque, host-side. */
+typedef struct snn_graph snn_graph;
+
 /* Device views of the simulation state, all inside the bound workspace. Each
  * array has n entries unless stated. Returned by snn_get_state (pointers
  * into the workspace, valid until snn_destroy); passed to snn_set_state
@@ -182,14 +191,16 @@ typedef struct snn_state_view {
     uint64_t *spike_mask;   /* last neuron update: ceil(n/64) words, bits >= n zero */
     int32_t *spike_list;    /* last neuron update: ascending indices */
     int32_t *spike_count;   /* device int32 */
-    int32_t *tx_list;       /* spikes transmitted by the last delivery step */
+    int32_t *tx_list;       /* spikes transmitted by the last delivery step
+                               (those of step t-D), ascending */
     int32_t *tx_count;      /* device int32 */
-    int32_t *stdp_rows;     /* plastic rows forced by the 64-step window at the
+    int32_t *stdp_rows;     /* plastic rows forced by the history window at the
                                last neuron update (brought up to date by
-                               snn_update_plasticity); transmitting plastic
-                               rows are brought up to date by delivery */
+                               snn_update_plasticity), ascending; transmitting
+                               plastic rows are brought up to date by delivery */
     int32_t *stdp_row_count;/* device int32 */
-    int32_t *ring_lists;    /* delay ring: D x n spike lists, slot = step mod D */
+    int32_t *ring_lists;    /* delay ring: D x n spike lists (each ascending),
+                               slot = step mod D */
     int32_t *ring_counts;   /* delay ring: D counts */
 } snn_state_view;
 
@@ -228,7 +239,8 @@ typedef struct snn_stats {
                                       skipped), so its weights are no longer exact;
                                       8 = a transmitting neuron had no entry in the
                                       delay ring (a state set whose ring lists
-                                      disagree with the histories) */
+                                      disagree with the histories); 16 = a list scan
+                                      gave up waiting for an earlier workgroup */
 } snn_stats;
 
 /* Human-readable name of a status code (static string). */
@@ -293,9 +305,11 @@ snn_status snn_build_graph_edges(snn_ctx *ctx, const int32_t *src, const int32_t
                                  const float *w);
 
 /* Part (1) of step t (Sec. I): integrates every neuron with its input A(t),
- * writes the firing mask, the spike list into ring slot t mod D, shifts the
- * histories, updates the post-synaptic trace, lists the plastic rows idle
- * for 64 steps (forced), and snapshots the plastic rows to update at t. */
+ * writes the firing mask, the ascending spike list into ring slot t mod D,
+ * shifts the histories, updates the post-synaptic trace, lists the plastic
+ * rows idle for the whole history (forced), snapshots the plastic rows to
+ * update at t, and advances the device's step index. SNN_ESTATE while step t
+ * is in progress (call snn_advance first). */
 snn_status snn_update_neurons(snn_ctx *ctx);
 
 /* Part (2) of step t (Sec. III-A, Fig. 2(c)) for the forced rows: brings
@@ -311,11 +325,13 @@ snn_status snn_update_plasticity(snn_ctx *ctx);
  * is read once. mode is an enum snn_delivery value. */
 snn_status snn_deliver_spikes(snn_ctx *ctx, int32_t mode);
 
-/* Ends step t (t <- t+1). */
+/* Ends step t (t <- t+1 on the host; the device index advanced with part
+ * (1)). SNN_ESTATE if part (1) of step t has not run. */
 snn_status snn_advance(snn_ctx *ctx);
 
 /* n_steps full steps: parts (1), (2), (3) with delivery mode, then advance.
- * Enqueues only; never synchronises. The result equals that of the separate
+ * Enqueues only; never synchronises; its launches can be captured into a
+ * HIP graph (snn_graph_capture). The result equals that of the separate
  * part calls in every state and statistic; with SNN_DELIVER_LDS_SLICE and
  * no kernel times being recorded, networks without plasticity take fewer
  * launches: up to 4096 neurons run many steps in one workgroup, and with
@@ -358,6 +374,31 @@ snn_status snn_get_kernel_times(snn_ctx *ctx, double *mean_ms, int32_t *steps);
 snn_status snn_probe_rows(snn_ctx *ctx, int32_t n_rows, int32_t write, uint64_t seed,
                           double *ms, int64_t *synapses);
 
+/* Captures n_steps steps (snn_step(ctx, n_steps, mode)) into an
+ * instantiated HIP graph on the context's stream, for callers that replay a
+ * fixed step sequence without host launch work (Sec. I: the step loop).
+ * Nothing runs: the capture records the launches only, and the host's view
+ * of time is left as it was. Every launch reads the step index and the input
+ * source from the device (see Time above) and makes no allocation or memset,
+ * so each replay (snn_graph_launch) runs the next n_steps steps and equals
+ * snn_step(ctx, n_steps, mode) there. The path a step takes (small
+ * networks, delay blocks, the fused pass) is fixed at capture. *out (host)
+ * receives the handle, owned by the caller (snn_graph_destroy); it stays
+ * valid while the context and its buffers do. SNN_EINVAL for n_steps < 1 or
+ * a context on the null stream (HIP cannot capture it); SNN_ESTATE while
+ * kernel times are being recorded, a step is in progress or no graph is
+ * built; SNN_EDEVICE if HIP refuses the capture. */
+snn_status snn_graph_capture(snn_ctx *ctx, int32_t n_steps, int32_t mode, snn_graph **out);
+
+/* Enqueues one replay of a captured step sequence on the context's stream
+ * and advances the host's step index by its length. Never synchronises.
+ * SNN_ESTATE while a step is in progress. */
+snn_status snn_graph_launch(snn_ctx *ctx, snn_graph *graph);
+
+/* Releases a captured step sequence (NULL is accepted). Replays already
+ * enqueued are not waited for. */
+void snn_graph_destroy(snn_graph *graph);
+
 /* Brings every plastic row up to the last completed step t-1 (no pre-
  * synaptic spike), so that all weights equal those of per-step updates.
  * Under lazy plasticity (Sec. III-A) a row's weights are brought up to date
@@ -373,14 +414,16 @@ snn_status snn_flush_plasticity(snn_ctx *ctx);
  * Delivery accumulates inputs exactly in 64-bit fixed point (32 fractional
  * bits) over C partial sums; this call first converts them into the fp32
  * input the next neuron update would use, so input_exc/input_inh are
- * readable (and writable) fp32 arrays. It also sorts the D delay-ring
- * lists and the forced-row list into ascending order (a step writes them
- * in workgroup completion order; no part of a step depends on it). */
+ * readable (and writable) fp32 arrays. It reads the step index back from
+ * the device, so it synchronises the stream. Every list is ascending as the
+ * step wrote it. */
 snn_status snn_get_state(snn_ctx *ctx, snn_state_view *out);
 
 /* Copies every non-NULL array of *in (caller device buffers) into the state
- * and sets t = in->t. Used for teacher forcing and checkpoint restore. The
- * output-only fields (spike mask/list/count, tx, stdp rows) are ignored. */
+ * and sets t = in->t, on the host and on the device. Used for teacher
+ * forcing and checkpoint restore. With an input array given, the next
+ * neuron update reads the fp32 input. The output-only fields (spike
+ * mask/list/count, tx, stdp rows) are ignored. */
 snn_status snn_set_state(snn_ctx *ctx, const snn_state_view *in);
 
 /* Device pointers of the graph arrays. */

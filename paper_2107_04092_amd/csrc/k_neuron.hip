@@ -42,21 +42,20 @@ __global__ __launch_bounds__(kBlock) void k_fill(T *p, int64_t count, T value)
 }
 
 // ---------------------------------------------------------------------------
-// (1) neuron update, one wave64 per mask word and kNeuronRounds neurons per
-// thread, and the lists of the step: spikes (into the delay ring), forced
-// plastic rows and the snapshots of the rows to bring up to date (see
-// CompactArgs).
+// (1) neuron update, one wave64 per mask word and one neuron per thread, and
+// the lists of the step: spikes (into the delay ring), forced plastic rows
+// and the snapshots of the rows to bring up to date (see CompactArgs).
 //
-// List offsets: each workgroup reserves its stretch of the spike list and of
-// the forced-row list with ONE 64-bit atomic on a packed word (spikes in bits
-// 0-23, forced rows in bits 24-47, a workgroup ticket in bits 48-63; counts
-// stay below n < 2^24). Same-address device-scope atomics serialise, so a
-// workgroup covers many neurons (fewer reservations). The workgroup whose ticket comes
-// last holds every other contribution in the returned value: it publishes
-// the counts and clears the word for the next step. Transmitting rows need
-// no reservation: a row transmitting at t spiked at t-D+1, when its position
-// in that step's spike list was recorded (spk_pos); its snapshot goes to the
-// same position, so snapshots line up with the delay-ring list delivery reads.
+// List offsets: the lists are ascending, workgroup by workgroup. Each
+// workgroup publishes its spike and forced-row counts in a status word and
+// learns the counts of all earlier workgroups by a decoupled look-back over
+// theirs (lookback), so no workgroup waits on a shared counter: same-address
+// device atomics serialise. Transmitting rows need no list of their own: a
+// row transmitting at t spiked at t-D+1, when its position in that step's
+// spike list was recorded (spk_pos); its snapshot goes to the same position,
+// so snapshots line up with the delay-ring list delivery reads. The step
+// index and the input source come from the device clock (StepClock); the
+// last workgroup publishes the counts and advances the clock.
 
 // A neuron's state as one update reads and writes it: potential,
 // refractory count, CUBA currents, post trace and history words.
@@ -115,24 +114,44 @@ __device__ __forceinline__ void nstate_store(const NeuronArgs &a, int i, const N
     if (nplastic<M>(a)) a.ypost[i] = st.y;
 }
 
-// The input A(t) of neuron i from the state: the fp32 input, or the sum of
-// the fixed-point partial sums of delivery.
-__device__ __forceinline__ void neuron_input(const NeuronArgs &a, int i, float &ae, float &ai)
+// The input A(t) of neuron i from the state: the fp32 input (forced), or the
+// sum of the n_parts fixed-point partial sums of delivery. Which one the
+// clock says is known only when its load returns, so the fp32 input and up
+// to kSpecParts partial sums (a.max_parts of them) are loaded before it is
+// looked at: one round trip instead of two.
+constexpr int kSpecParts = 8;
+__device__ __forceinline__ void neuron_input(const NeuronArgs &a, int forced, int n_parts, int i,
+                                             float &ae, float &ai)
 {
+    const bool cuba = a.model == 1;
+    const float fe = a.ain[i];
+    const float fi = cuba ? a.ain[a.n + i] : 0.f;
+    long long pe[kSpecParts], pi[kSpecParts];
+#pragma unroll
+    for (int c = 0; c < kSpecParts; ++c) {
+        pe[c] = c < a.max_parts ? a.apart[c * a.part_stride + i] : 0;
+        pi[c] = cuba && c < a.max_parts ? a.apart[c * a.part_stride + a.n + i] : 0;
+    }
     ai = 0.f;
-    if (a.input_forced) {
-        ae = a.ain[i];
-        if (a.model == 1) ai = a.ain[a.n + i];
-    } else {
-        long long se = a.apart[i];
-        for (int c = 1; c < a.n_parts; ++c) se += a.apart[c * a.part_stride + i];
-        ae = from_fix(se);
-        if (a.model == 1) {
-            long long si = a.apart[a.n + i];
-            for (int c = 1; c < a.n_parts; ++c) si += a.apart[c * a.part_stride + a.n + i];
-            ai = from_fix(si);
+    if (forced) {
+        ae = fe;
+        ai = fi;
+        return;
+    }
+    long long se = 0, si = 0;
+#pragma unroll
+    for (int c = 0; c < kSpecParts; ++c) {
+        if (c < n_parts) {
+            se += pe[c];
+            si += pi[c];
         }
     }
+    for (int c = kSpecParts; c < n_parts; ++c) {  // beyond the speculative loads
+        se += a.apart[c * a.part_stride + i];
+        if (cuba) si += a.apart[c * a.part_stride + a.n + i];
+    }
+    ae = from_fix(se);
+    if (cuba) ai = from_fix(si);
 }
 
 // The external Poisson count of neuron i at step t: the number of CDF
@@ -223,144 +242,115 @@ __device__ __forceinline__ uint8_t hist_code(uint64_t h0, uint64_t h1)
     return np == 0 ? (uint8_t)0 : np == 1 ? (uint8_t)pos : kCodeMulti;
 }
 
-// The whole update of neuron i at step t from and to the state arrays;
-// returns spiked / transmitting / forced.
-__device__ __forceinline__ void neuron_update(const NeuronArgs &a, int i, int64_t t, int &s,
-                                              int &tx, int &forced, bool &fired_recently)
+// The whole update of neuron i at step t from and to the state arrays, with
+// the input source of the clock; returns spiked / transmitting / forced and,
+// for a plastic row, its t_last.
+__device__ __forceinline__ void neuron_update(const NeuronArgs &a, const StepClock &ck, int i,
+                                              int64_t t, int &s, int &tx, int &forced,
+                                              bool &fired_recently, int &t_last_i)
 {
     NState st;
     nstate_load<-1, 0>(a, i, st);
+    t_last_i = i < a.n_plastic_rows ? a.t_last[i] : 0;
     float ae = 0.f, ai = 0.f;
-    if (a.model != 2) neuron_input(a, i, ae, ai);
+    if (a.model != 2) neuron_input(a, ck.input_forced, ck.n_parts, i, ae, ai);
     s = neuron_advance<-1, 0>(a, i, t, ae, ai, st);
     nstate_store<-1, 0>(a, i, st);
     a.code[i] = hist_code(st.h0, st.h1);
     fired_recently = (st.h0 | st.h1) != 0ull;
     tx = (int)((st.h0 >> a.dm1) & 1ull);
-    if (i < a.n_plastic_rows) forced = !tx && (t - (int64_t)a.t_last[i] >= 64 * a.hw);
+    if (i < a.n_plastic_rows) forced = !tx && (t - (int64_t)t_last_i >= 64 * a.hw);
 }
 
-// NB threads per workgroup: 1024 on large networks (one list reservation
-// per workgroup; same-address atomics serialise), 256 up to kNeuronSmallN
-// neurons, where 1024 would leave most CUs without a workgroup.
+// NB threads per workgroup: 1024 on large networks (fewer workgroups to look
+// back over), 256 up to kNeuronSmallN neurons, where 1024 would leave most
+// CUs without a workgroup.
 template <int NB>
 __global__ __launch_bounds__(NB) void k_neuron(NeuronArgs a, CompactArgs lst)
 {
-    // (n < 2^24 neurons with 1024 threads, at most kNeuronSmallN with fewer)
-    static_assert((NB == kNeuronBlock ? (1 << 24) : kNeuronSmallN) / (NB * kNeuronRounds) <=
-                      65536,
-                  "workgroup ticket must fit in 16 bits");
     constexpr int NWV = NB / kWave;
-    constexpr int R = kNeuronRounds;
-    __shared__ int s_cnt[2][R * NWV];
+    __shared__ int s_cnt[2][NWV];
     __shared__ unsigned long long s_st[4];
-    __shared__ unsigned long long s_base;
+    __shared__ int s_lb[8];
     const int tid = threadIdx.x;
     const int wave = tid / kWave, lane = tid % kWave;
     const bool plastic = lst.n_plastic_rows > 0;
+    const StepClock ck = *a.clk;
+    const int64_t t = ck.t;
+    const int D = lst.delay;
+    const int i = blockIdx.x * NB + tid;
     if (tid < 4) s_st[tid] = 0ull;
-    // The values a row snapshot needs are loaded with the neuron's own state
-    // for every plastic neuron (first edge for every neuron when there is
-    // plasticity), so that the few snapshots taken below cost no second
-    // dependent round trip.
-    int64_t v_rs[R];
-    int v_pend[R], v_tl[R];
-    float v_xp[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        const int i = (blockIdx.x * R + r) * NB + tid;
-        v_rs[r] = 0;
-        v_pend[r] = v_tl[r] = 0;
-        v_xp[r] = 0.f;
-        if (plastic && i < a.n) {
-            v_rs[r] = lst.row_ptr[i];
-            if (i < lst.n_plastic_rows) {
-                v_pend[r] = lst.pend[i];
-                v_tl[r] = lst.t_last[i];
-                v_xp[r] = lst.xpre[i];
-            }
-        }
-    }
-    // round r covers neurons [(b R + r) B, (b R + r + 1) B) of workgroup b
-    int s[R], tx[R], forced[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        const int i = (blockIdx.x * R + r) * NB + tid;
-        s[r] = tx[r] = forced[r] = 0;
-        bool fired_recently = false;
-        if (i < a.n) neuron_update(a, i, a.t, s[r], tx[r], forced[r], fired_recently);
-        const uint64_t m = ballot64(s[r]), txm = ballot64(tx[r]), fm = ballot64(forced[r]);
-        const uint64_t rcm = ballot64(fired_recently);
+    // the count of the transmitted list (D > 1: written D-1 steps ago), at
+    // the fixed address the synapse pass reads
+    if (blockIdx.x == 0 && tid == 0 && a.dm1 > 0) *lst.tx_cnt = lst.ring_cnt[ring_slot(t - a.dm1, D)];
+    int s = 0, tx = 0, forced = 0, tl = 0;
+    bool fired_recently = false;
+    if (i < a.n) neuron_update(a, ck, i, t, s, tx, forced, fired_recently, tl);
+    const uint64_t m = ballot64(s), fm = ballot64(forced);
+    {
+        const uint64_t txm = ballot64(tx), rcm = ballot64(fired_recently);
         if (lane == 0) {
-            const int64_t word = (int64_t)(blockIdx.x * R + r) * NWV + wave;
+            const int64_t word = (int64_t)blockIdx.x * NWV + wave;
             if (word * kWave < a.n) {
                 a.mask[word] = m;
                 a.txmask[word] = txm;
                 a.recent[word] = rcm;
             }
-            s_cnt[0][r * NWV + wave] = __popcll(m);
-            s_cnt[1][r * NWV + wave] = __popcll(fm);
+            s_cnt[0][wave] = __popcll(m);
+            s_cnt[1][wave] = __popcll(fm);
         }
     }
+    // The values a row snapshot needs, loaded for the rows to bring up to
+    // date at t only (transmitting plastic rows, forced rows), and a
+    // transmitting row's position in the spike list of step t-D+1: the loads
+    // are issued now and arrive during the list scan.
+    const bool snap_tx = tx && plastic;
+    int64_t rs = 0;
+    int pend_i = 0, txpos = -1;
+    float xp = 0.f;
+    if (snap_tx || forced) {
+        rs = lst.row_ptr[i];
+        if (i < lst.n_plastic_rows) {
+            pend_i = lst.pend[i];
+            xp = lst.xpre[i];
+        }
+        if (snap_tx && a.dm1 > 0) txpos = lst.spk_pos[(int64_t)ring_slot(t - a.dm1, D) * a.n + i];
+    }
+    __syncthreads();  // s_cnt, s_st
+    int agg_s = 0, agg_f = 0;
+#pragma unroll
+    for (int q = 0; q < NWV; ++q) {
+        agg_s += s_cnt[0][q];
+        agg_f += s_cnt[1][q];
+    }
+    if (tid == 0)
+        publish_status(lst.status + blockIdx.x,
+                       status_word(agg_s, agg_f, t, blockIdx.x == 0 ? kStatusInc : kStatusAgg));
+    lookback<NB, 1>(lst.status, 0, 1, (int)blockIdx.x, t, s_lb, lst.err);
+    const int pre_s = s_lb[6], pre_f = s_lb[7];  // spikes and forced rows of earlier workgroups
+    if (tid == 0 && blockIdx.x > 0)
+        publish_status(lst.status + blockIdx.x,
+                       status_word(pre_s + agg_s, pre_f + agg_f, t, kStatusInc));
     // snapshots of the rows to bring up to date (taken before any kernel
-    // commits t_last / x_pre), and the position of a transmitting row in the
-    // spike list of step t-D+1; their loads overlap the barrier and the
-    // reservation below
-    RowInfo ri[R];
-    int ri_ok[R], txpos[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        const int i = (blockIdx.x * R + r) * NB + tid;
-        ri[r] = RowInfo{};
-        ri_ok[r] = 0;
-        txpos[r] = -1;
+    // commits t_last / x_pre)
+    RowInfo ri = RowInfo{};
+    int ri_ok = 0;
+    if (snap_tx) {
         // the row transmits at t exactly when tx (history bit D-1 of step t)
-        if (tx[r] && plastic) {
-            if (lst.dm1 > 0) txpos[r] = lst.tx_pos[i];
-            if (i < lst.n_plastic_rows)
-                ri_ok[r] = make_row_info_v(ri[r], i, lst.t, v_tl[r], v_rs[r], v_pend[r],
-                                           v_xp[r], 1, lst.hw, lst.dpow, lst.err);
-            if (!ri_ok[r]) {  // nothing to bring up to date: the row is only delivered
-                ri[r] = RowInfo{};
-                ri[r].k = i;
-                ri[r].rs = v_rs[r];
-            }
-        } else if (forced[r]) {
-            ri_ok[r] = make_row_info_v(ri[r], i, lst.t, v_tl[r], v_rs[r], v_pend[r], v_xp[r], 0,
-                                       lst.hw, lst.dpow, lst.err);
+        if (i < lst.n_plastic_rows)
+            ri_ok = make_row_info_v(ri, i, t, tl, rs, pend_i, xp, 1, lst.hw, lst.dpow, lst.err);
+        if (!ri_ok) {  // nothing to bring up to date: the row is only delivered
+            ri = RowInfo{};
+            ri.k = i;
+            ri.rs = rs;
         }
-    }
-    __syncthreads();  // publishes s_cnt, s_st
-    if (tid == 0) {
-        int spk = 0, fr = 0;
-#pragma unroll
-        for (int q = 0; q < R * NWV; ++q) {
-            spk += s_cnt[0][q];
-            fr += s_cnt[1][q];
-        }
-        const unsigned long long mine =
-            (unsigned long long)spk | ((unsigned long long)fr << 24) | (1ull << 48);
-        const unsigned long long old = atomicAdd(lst.acc, mine);
-        s_base = old;
-        if ((int)(old >> 48) == (int)gridDim.x - 1) {
-            const int n_spk = (int)(old & 0xffffffull) + spk;
-            const int n_forced = (int)((old >> 24) & 0xffffffull) + fr;
-            (void)atomicExch(lst.acc, 0ull);
-            *lst.spk_cnt = n_spk;
-            *lst.row_cnt = n_forced;
-            lst.gstats[kGSpikes] += n_spk;
-        }
+    } else if (forced) {
+        ri_ok = make_row_info_v(ri, i, t, tl, rs, pend_i, xp, 0, lst.hw, lst.dpow, lst.err);
     }
     if (lst.info_stats) {
-        long long v0 = 0, v1 = 0, v2 = 0, v3 = 0;
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            const bool f = forced[r] && ri_ok[r];
-            v0 += ri_ok[r] ? 1 : 0;
-            v1 += f ? 1 : 0;
-            v2 += ri_ok[r] ? ri[r].len : 0;
-            v3 += f ? ri[r].len : 0;
-        }
+        const bool f = forced && ri_ok;
+        long long v0 = ri_ok ? 1 : 0, v1 = f ? 1 : 0;
+        long long v2 = ri_ok ? ri.len : 0, v3 = f ? ri.len : 0;
         v0 = wave_sum_i64(v0);
         v1 = wave_sum_i64(v1);
         v2 = wave_sum_i64(v2);
@@ -372,55 +362,60 @@ __global__ __launch_bounds__(NB) void k_neuron(NeuronArgs a, CompactArgs lst)
             if (v3) atomicAdd(s_st + 3, (unsigned long long)v3);
         }
     }
-    __syncthreads();  // publishes s_base, s_st
-    const unsigned long long base = s_base;
+    // this wave's offsets: the earlier workgroups, then the earlier waves
     const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
-    int o0 = (int)(base & 0xffffffull), o2 = (int)((base >> 24) & 0xffffffull);
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        const int i = (blockIdx.x * R + r) * NB + tid;
-        // this wave's offsets in round r: every wave of the earlier rounds,
-        // then the earlier waves of this one
-        int p0 = o0, p2 = o2;
-        for (int q = 0; q < r * NWV + wave; ++q) {
-            p0 += s_cnt[0][q];
-            p2 += s_cnt[1][q];
-        }
-        const uint64_t m = ballot64(s[r]), fm = ballot64(forced[r]);
-        // (the bounds checks only catch an accumulator left non-zero by a
-        // failed step; with a cleared one every offset is in range)
-        if (s[r]) {
-            const int pos = p0 + __popcll(m & below);
-            if (pos < a.n) {
-                lst.spk_list[pos] = i;
-                if (plastic && lst.dm1 > 0) lst.spk_pos[i] = pos;
-                if (lst.dm1 == 0) txpos[r] = pos;  // D = 1: transmitted as it fires
-            } else {
-                atomicOr(lst.err, kErrRing);
-            }
-        }
-        if (tx[r] && plastic) {
-            if (txpos[r] >= 0 && txpos[r] < a.n)
-                lst.txinfo[txpos[r]] = ri[r];
-            else
-                atomicOr(lst.err, kErrRing);
-        }
-        if (forced[r]) {
-            const int q = p2 + __popcll(fm & below);
-            if (q < lst.n_plastic_rows) {
-                lst.row_list[q] = i;
-                lst.info[q] = ri[r];
-            } else {
-                atomicOr(lst.err, kErrRing);
-            }
+    int p0 = pre_s, p2 = pre_f;
+    for (int q = 0; q < wave; ++q) {
+        p0 += s_cnt[0][q];
+        p2 += s_cnt[1][q];
+    }
+    const int slot = ring_slot(t, D);
+    // (the bounds checks only catch a failed scan; otherwise every offset is
+    // in range)
+    if (s) {
+        const int pos = p0 + __popcll(m & below);
+        if (pos < a.n) {
+            lst.ring[(int64_t)slot * a.n + pos] = i;
+            if (plastic && a.dm1 > 0) lst.spk_pos[(int64_t)slot * a.n + i] = pos;
+            if (a.dm1 == 0) txpos = pos;  // D = 1: transmitted as it fires
+        } else {
+            atomicOr(lst.err, kErrRing);
         }
     }
-    if (lst.info_stats && tid == 0) {
-        int64_t *slot = lst.info_stats + (int64_t)blockIdx.x * kStFields;
-        slot[kStRows] += (int64_t)s_st[0];
-        slot[kStForced] += (int64_t)s_st[1];
-        slot[kStSyn] += (int64_t)s_st[2];
-        slot[kStForcedSyn] += (int64_t)s_st[3];
+    if (snap_tx) {
+        if (txpos >= 0 && txpos < a.n)
+            lst.txinfo[txpos] = ri;
+        else
+            atomicOr(lst.err, kErrRing);
+    }
+    if (forced) {
+        const int q = p2 + __popcll(fm & below);
+        if (q < lst.n_plastic_rows) {
+            lst.row_list[q] = i;
+            lst.info[q] = ri;
+        } else {
+            atomicOr(lst.err, kErrRing);
+        }
+    }
+    if (lst.info_stats) {
+        __syncthreads();  // s_st complete
+        if (tid == 0) {
+            int64_t *sl = lst.info_stats + (int64_t)blockIdx.x * kStFields;
+            add_stat(sl + kStRows, (long long)s_st[0]);
+            add_stat(sl + kStForced, (long long)s_st[1]);
+            add_stat(sl + kStSyn, (long long)s_st[2]);
+            add_stat(sl + kStForcedSyn, (long long)s_st[3]);
+        }
+    }
+    if (tid == 0 && blockIdx.x == gridDim.x - 1) {
+        // every workgroup has read the clock: the look-back saw all of them
+        const int n_spk = pre_s + agg_s, n_forced = pre_f + agg_f;
+        lst.ring_cnt[slot] = n_spk;
+        if (a.dm1 == 0) *lst.tx_cnt = n_spk;  // D = 1: this step's spikes transmit
+        *lst.row_cnt = n_forced;
+        add_stat(lst.gstats + kGSpikes, n_spk);
+        add_stat(lst.gstats + kGSteps, 1);
+        a.clk->t = t + 1;
     }
 }
 
@@ -448,6 +443,7 @@ __global__ __launch_bounds__(kSmallBlock) void k_small_steps(NeuronArgs a, Small
     const int n = a.n;
     const int rounds = (n + kSmallBlock - 1) / kSmallBlock;  // <= kSmallRounds
     const int span = b.nacc * n;
+    const StepClock ck = *a.clk;
     long long events = 0, spikes = 0;
     NState st[kSmallRounds];
 #pragma unroll
@@ -456,7 +452,7 @@ __global__ __launch_bounds__(kSmallBlock) void k_small_steps(NeuronArgs a, Small
         if (r < rounds && i < n) nstate_load<M, H>(a, i, st[r]);
     }
     for (int k = 0; k < b.steps; ++k) {
-        const int64_t t = a.t + k;
+        const int64_t t = ck.t + k;
         const int slot = (int)(t % b.delay);
         int32_t *list = b.ring + (int64_t)slot * n;
         // (1) neuron update
@@ -471,7 +467,7 @@ __global__ __launch_bounds__(kSmallBlock) void k_small_steps(NeuronArgs a, Small
                 float ae = 0.f, ai = 0.f;
                 if (M != 2) {
                     if (k == 0) {
-                        neuron_input(a, i, ae, ai);
+                        neuron_input(a, ck.input_forced, ck.n_parts, i, ae, ai);
                     } else {
                         ae = from_fix(acc[i]);
                         if (M == 1) ai = from_fix(acc[n + i]);
@@ -540,45 +536,53 @@ __global__ __launch_bounds__(kSmallBlock) void k_small_steps(NeuronArgs a, Small
         }
     }
     for (int x = tid; x < span; x += kSmallBlock) b.apart[x] = acc[x];
+    // the list scans of the other kernels find no stale step tag after these steps
+    for (int x = tid; x < b.status_words; x += kSmallBlock) b.status[x] = 0ull;
     if (lane == 0 && events) atomicAdd((unsigned long long *)b.dlv_stats, (unsigned long long)events);
-    if (tid == 0) b.gstats[kGSpikes] += spikes;
+    if (tid == 0) {
+        add_stat(b.gstats + kGSpikes, spikes);
+        add_stat(b.gstats + kGSteps, b.steps);
+        a.clk->t = ck.t + b.steps;
+        a.clk->input_forced = 0;  // the next input is partial sum 0
+        a.clk->n_parts = 1;
+    }
 }
 
 // ---------------------------------------------------------------------------
 // Delay block of a network without plasticity: b.steps (<= D-1) steps of the
-// neuron update, one neuron per thread with its state in registers. Step
-// a.t reads its input like k_neuron (forced input or the partial sums in
-// apart); step a.t + k, k >= 1, reads slot k-1 of abatch, the whole input
-// as one fixed-point sum, written beforehand by the batched delivery. Every
+// neuron update, one neuron per thread with its state in registers. Step t0
+// (= clk->t) reads its input like k_neuron (the fp32 input or the partial
+// sums); step t0 + k, k >= 1, reads slot k-1 of abatch, the whole input as
+// one fixed-point sum, written beforehand by the batched delivery. Every
 // slot's load is issued before the first step, so the steps wait for one
 // round trip in all. The spike flags of every step are kept (a bit per step
 // per thread, ballots in LDS), and the spike lists go into the delay ring at
-// the end: one packed reservation per workgroup and step (counts in bits
-// 0-23, a ticket in bits 48-63; the workgroup whose ticket comes last
-// publishes the count and clears the word), the B reservations of a
-// workgroup in flight together. The masks, codes and the state written are
-// those of the last step, and apart part 0 receives slot B-1, the pending
-// input of the next step. Workgroups of 512 threads: the B steps of a
-// thread run one after another, so fewer waves share a SIMD than with 1024,
-// and half as many reservations queue per step as with 256.
+// the end, ascending: one list scan per step (status row k of b.status),
+// the B scans looked back over together. The masks, codes and the state
+// written are those of the last step, and apart part 0 receives slot B-1,
+// the pending input of the next step. Workgroups of 512 threads: the B
+// steps of a thread run one after another, so fewer waves share a SIMD than
+// with 1024.
 constexpr int kStepsBlock = 512;
-static_assert((1 << 24) / kStepsBlock <= 65536, "workgroup ticket must fit in 16 bits");
 template <int M, int H>
 __global__ __launch_bounds__(kStepsBlock) void k_neuron_steps(NeuronArgs a, BatchArgs b)
 {
     constexpr int NWV = kStepsBlock / kWave;
+    static_assert(kStepsBlock / 32 >= kBatchMax, "a half wave per step's list scan");
     __shared__ uint64_t s_m[kBatchMax][NWV];
-    __shared__ int s_off[kBatchMax];
+    __shared__ int s_lb[2 * kBatchMax];
     const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
     const int n = a.n;
     const int i = blockIdx.x * kStepsBlock + tid;
     const bool live = i < n;
     const int ic = live ? i : 0;
     const int64_t ps = a.part_stride;  // nacc * n
+    const StepClock ck = *a.clk;
+    const int64_t t0 = ck.t;
     // steps per launch: CUBA holds two inputs per step in registers
     constexpr int KB = batch_steps_max(M);
     const int B = b.steps;  // 1 .. KB (checked by the launcher)
-    // slot k = input of step a.t + k + 1 (Bernoulli sources read only the
+    // slot k = input of step t0 + k + 1 (Bernoulli sources read only the
     // last). Every load is issued unconditionally from a valid slot (past B:
     // slot B-1 again): a load under a branch would be waited for inside it.
     long long pe[KB], pi[KB];
@@ -598,14 +602,14 @@ __global__ __launch_bounds__(kStepsBlock) void k_neuron_steps(NeuronArgs a, Batc
         float ae = 0.f, ai = 0.f;
         if (live && M != 2) {
             if (k == 0) {
-                neuron_input(a, i, ae, ai);
+                neuron_input(a, ck.input_forced, ck.n_parts, i, ae, ai);
             } else {
                 ae = from_fix(pe[k - 1]);
                 if (M == 1) ai = from_fix(pi[k - 1]);
             }
         }
         int sp = 0;
-        if (live) sp = neuron_advance<M, H>(a, i, a.t + k, ae, ai, st);
+        if (live) sp = neuron_advance<M, H>(a, i, t0 + k, ae, ai, st);
         fired |= (uint32_t)sp << k;
         const uint64_t m = ballot64(sp);
         if (lane == 0) s_m[k][wave] = m;
@@ -638,71 +642,43 @@ __global__ __launch_bounds__(kStepsBlock) void k_neuron_steps(NeuronArgs a, Batc
         }
     }
     __syncthreads();  // every step's ballots
+    // the workgroup's spike count of each step (thread k), published for the scans
+    int own = 0;
     if (tid < B) {
-        const int k = tid;
-        int cnt = 0;
-        for (int w = 0; w < NWV; ++w) cnt += __popcll(s_m[k][w]);
-        const unsigned long long old =
-            atomicAdd(b.acc + k * kAccStride, (unsigned long long)cnt | (1ull << 48));
-        s_off[k] = (int)(old & 0xffffffull);
-        if ((int)(old >> 48) == (int)gridDim.x - 1) {
-            const int total = (int)(old & 0xffffffull) + cnt;
-            (void)atomicExch(b.acc + k * kAccStride, 0ull);
-            const int64_t d = b.delay;
-            b.ring_cnt[(int)((a.t + k) % d)] = total;
-            atomicAdd((unsigned long long *)(b.gstats + kGSpikes), (unsigned long long)total);
-        }
+        for (int w = 0; w < NWV; ++w) own += __popcll(s_m[tid][w]);
+        publish_status(b.status + (int64_t)tid * b.status_stride + blockIdx.x,
+                       status_word(own, 0, t0 + tid, blockIdx.x == 0 ? kStatusInc : kStatusAgg));
     }
-    __syncthreads();  // every offset
+    lookback32<kStepsBlock>(b.status, b.status_stride, B, (int)blockIdx.x, t0, s_lb, b.err);
+    // the spikes of step k before this workgroup: s_lb[2 k]
+    if (tid < B && blockIdx.x > 0)
+        publish_status(b.status + (int64_t)tid * b.status_stride + blockIdx.x,
+                       status_word(s_lb[2 * tid] + own, 0, t0 + tid, kStatusInc));
     const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
-    for (int k = 0; k < B; ++k) {
-        if (!((fired >> k) & 1u)) continue;
-        int pos = s_off[k] + __popcll(s_m[k][wave] & below);
+#pragma unroll
+    for (int k = 0; k < KB; ++k) {
+        if (k >= B || !((fired >> k) & 1u)) continue;
+        int pos = s_lb[2 * k] + __popcll(s_m[k][wave] & below);
         for (int w = 0; w < wave; ++w) pos += __popcll(s_m[k][w]);
-        // (only an accumulator left non-zero by a failed launch is out of range)
+        // (only a failed scan puts an offset out of range)
         if (pos < n)
-            b.ring[(int64_t)((a.t + k) % b.delay) * n + pos] = i;
+            b.ring[(int64_t)ring_slot(t0 + k, b.delay) * n + pos] = i;
         else
             atomicOr(b.err, kErrRing);
     }
-}
-
-// Sorts a list of distinct neuron indices (capacity n entries, values in
-// [0, n)) into ascending order (one workgroup; not on the step's path):
-// scatter into a bitmap of nw = ceil(n/64) words, then read it back in order.
-// Entries past min(*cnt, n) are not read; out-of-range values are dropped.
-// With pos, records each index's new position.
-constexpr int kSortListBlock = 1024;
-__global__ __launch_bounds__(kSortListBlock) void k_sort_list(int32_t *list, const int32_t *cnt,
-                                                              uint64_t *bitmap, int32_t *pos,
-                                                              int32_t n, int32_t nw)
-{
-    __shared__ long long sh[kSortListBlock / kWave];
-    const int tid = threadIdx.x;
-    const int len = min(max(*cnt, 0), n);
-    for (int q = tid; q < nw; q += kSortListBlock) bitmap[q] = 0ull;
-    __syncthreads();
-    for (int q = tid; q < len; q += kSortListBlock) {
-        const int k = list[q];
-        if (k >= 0 && k < n)
-            atomicOr((unsigned long long *)(bitmap + (k >> 6)), 1ull << (k & 63));
-    }
-    __syncthreads();
-    long long done = 0;
-    for (int w0 = 0; w0 < nw; w0 += kSortListBlock) {
-        const int wi = w0 + tid;
-        // agent-scope loads: the bits were set by atomics at L2
-        const uint64_t bits =
-            wi < nw ? __hip_atomic_load(bitmap + wi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                    : 0ull;
-        const long long incl = block_incl_scan_i64_n<kSortListBlock>(__popcll(bits), sh);
-        int o = (int)(done + incl - __popcll(bits));
-        for (uint64_t b = bits; b; b &= b - 1, ++o) {
-            const int k = wi * 64 + __ffsll((long long)b) - 1;
-            list[o] = k;
-            if (pos) pos[k] = o;
+    if (blockIdx.x == gridDim.x - 1) {
+        // every workgroup has read the clock: the scans saw all of them
+        if (tid < B) {
+            const int cnt = s_lb[2 * tid] + own;
+            b.ring_cnt[ring_slot(t0 + tid, b.delay)] = cnt;
+            add_stat(b.gstats + kGSpikes, cnt);
         }
-        done += block_sum_i64_n<kSortListBlock>(__popcll(bits), sh);
+    }
+    if (tid == 0 && blockIdx.x == gridDim.x - 1) {
+        add_stat(b.gstats + kGSteps, B);
+        a.clk->t = t0 + B;
+        a.clk->input_forced = 0;  // the next input is partial sum 0
+        a.clk->n_parts = 1;
     }
 }
 
@@ -718,16 +694,31 @@ __global__ __launch_bounds__(kBlock) void k_ring_positions(const int32_t *ring,
     if (k >= 0 && k < n) pos[(int64_t)q * n + k] = r;
 }
 
-// The fp32 input the next neuron update would compute from the partial sums.
+// The fp32 input the next neuron update would compute from the partial sums
+// (nothing when the clock says it reads the fp32 input already).
 __global__ __launch_bounds__(kBlock) void k_materialize_input(const long long *apart,
-                                                              int64_t stride, int32_t parts,
-                                                              float *ain, int64_t count)
+                                                              int64_t stride,
+                                                              const StepClock *clk, float *ain,
+                                                              int64_t count)
 {
     const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (i >= count) return;
+    const StepClock ck = *clk;
+    if (i >= count || ck.input_forced) return;
     long long v = apart[i];
-    for (int c = 1; c < parts; ++c) v += apart[c * stride + i];
+    for (int c = 1; c < ck.n_parts; ++c) v += apart[c * stride + i];
     ain[i] = from_fix(v);
+}
+
+// Sets the clock: step t unless t < 0, the input source unless
+// input_forced < 0.
+__global__ void k_set_clock(StepClock *clk, int64_t t, int32_t input_forced, int32_t n_parts)
+{
+    if (threadIdx.x != 0) return;
+    if (t >= 0) clk->t = t;
+    if (input_forced >= 0) {
+        clk->input_forced = input_forced;
+        clk->n_parts = n_parts;
+    }
 }
 
 template <int M, int H>
@@ -747,8 +738,7 @@ hipError_t launch_small(hipStream_t s, const NeuronArgs &a, const SmallArgs &b, 
     const hipError_t e =
         allow_dynamic_lds((const void *)k_small_steps<M, H>, (int)lds, mu, granted);
     if (e != hipSuccess) return e;
-    hipExtLaunchKernelGGL(k_small_steps<M, H>, dim3(1), dim3(kSmallBlock), lds, s, ev.start,
-                          ev.stop, 0, a, b);
+    launch_kernel(k_small_steps<M, H>, dim3(1), dim3(kSmallBlock), lds, s, ev, a, b);
     return hipGetLastError();
 }
 
@@ -833,25 +823,17 @@ hipError_t launch_neuron_steps(hipStream_t s, const NeuronArgs &a, const BatchAr
 hipError_t launch_neuron(hipStream_t s, const NeuronArgs &a, const CompactArgs &c,
                          KernelEvents ev)
 {
-    if (a.n <= kNeuronSmallN) {
-        constexpr int NB = kBlock;
-        hipExtLaunchKernelGGL(k_neuron<NB>, dim3(blocks_for(a.n, NB * kNeuronRounds)), dim3(NB),
-                              0, s, ev.start, ev.stop, 0, a, c);
-    } else {
-        constexpr int NB = kNeuronBlock;
-        hipExtLaunchKernelGGL(k_neuron<NB>, dim3(blocks_for(a.n, NB * kNeuronRounds)), dim3(NB),
-                              0, s, ev.start, ev.stop, 0, a, c);
-    }
+    if (a.n <= kNeuronSmallN)
+        launch_kernel(k_neuron<kBlock>, dim3(blocks_for(a.n, kBlock)), dim3(kBlock), 0, s, ev,
+                      a, c);
+    else
+        launch_kernel(k_neuron<kNeuronBlock>, dim3(blocks_for(a.n, kNeuronBlock)),
+                      dim3(kNeuronBlock), 0, s, ev, a, c);
     return hipGetLastError();
 }
 
-hipError_t launch_sort_list(hipStream_t s, int32_t *list, const int32_t *cnt, uint64_t *bitmap,
-                            int32_t *pos, int32_t n)
-{
-    hipLaunchKernelGGL(k_sort_list, dim3(1), dim3(kSortListBlock), 0, s, list, cnt, bitmap, pos, n,
-                       (n + 63) / 64);
-    return hipGetLastError();
-}
+int neuron_grid(int32_t n) { return blocks_for(n, n <= kNeuronSmallN ? kBlock : kNeuronBlock); }
+int neuron_steps_grid(int32_t n) { return blocks_for(n, kStepsBlock); }
 
 hipError_t launch_ring_positions(hipStream_t s, const int32_t *ring, const int32_t *cnt,
                                  int32_t *pos, int32_t n, int32_t d)
@@ -862,11 +844,20 @@ hipError_t launch_ring_positions(hipStream_t s, const int32_t *ring, const int32
 }
 
 hipError_t launch_materialize_input(hipStream_t s, const long long *apart, int64_t part_stride,
-                                    int32_t n_parts, float *ain, int64_t count)
+                                    StepClock *clk, float *ain, int64_t count)
 {
     if (count <= 0) return hipSuccess;
     hipLaunchKernelGGL(k_materialize_input, dim3(blocks_for(count)), dim3(kBlock), 0, s, apart,
-                       part_stride, n_parts, ain, count);
+                       part_stride, clk, ain, count);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_set_clock(s, clk, -1, 1, 1);
+}
+
+hipError_t launch_set_clock(hipStream_t s, StepClock *clk, int64_t t, int32_t input_forced,
+                            int32_t n_parts)
+{
+    hipLaunchKernelGGL(k_set_clock, dim3(1), dim3(kWave), 0, s, clk, t, input_forced, n_parts);
     return hipGetLastError();
 }
 

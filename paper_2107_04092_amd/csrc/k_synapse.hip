@@ -32,7 +32,7 @@ __global__ __launch_bounds__(kBlock) void k_row_info(RowInfoArgs a)
     long long st_rows = 0, st_syn = 0;
     if (r < a.n_rows_all) {
         RowInfo ri;
-        if (make_row_info(ri, r, a.t, false, a.dm1, a.hw, a.row_ptr, a.pend, a.hist, a.t_last, a.xpre,
+        if (make_row_info(ri, r, a.clk->t - 1, false, a.dm1, a.hw, a.row_ptr, a.pend, a.hist, a.t_last, a.xpre,
                           s_dpow, a.err)) {
             st_rows = 1;
             st_syn = ri.len;
@@ -43,8 +43,8 @@ __global__ __launch_bounds__(kBlock) void k_row_info(RowInfoArgs a)
     st_syn = block_sum_i64(st_syn, sh);
     if (tid == 0) {
         int64_t *slot = a.stats + (int64_t)blockIdx.x * kStFields;
-        slot[kStRows] += st_rows;
-        slot[kStSyn] += st_syn;
+        add_stat(slot + kStRows, st_rows);
+        add_stat(slot + kStSyn, st_syn);
     }
 }
 
@@ -80,6 +80,7 @@ __global__ __launch_bounds__(kStdpBlock) void k_stdp(StdpArgs a)
     const int q = (blockIdx.x & 7) * (nb >> 3) + (blockIdx.x >> 3);
     if (q >= a.n_work) return;  // whole workgroup, before any barrier
     const int g = q / a.chunks, cr = q - g * a.chunks;
+    const int64_t t = a.clk->t - 1;
     const int nrows = a.row_cnt ? *a.row_cnt : a.n_rows_all;
     const int lo = (int)((int64_t)nrows * cr / a.chunks);
     const int hi = (int)((int64_t)nrows * (cr + 1) / a.chunks);
@@ -87,7 +88,7 @@ __global__ __launch_bounds__(kStdpBlock) void k_stdp(StdpArgs a)
         for (int r = lo + tid; r < hi; r += kStdpBlock) {
             const RowInfo ri = a.info[r];
             if (ri.age_pre != 0) {
-                a.t_last[ri.k] = (int32_t)a.t;
+                a.t_last[ri.k] = (int32_t)t;
                 a.xpre[ri.k] = ri.xp_now;
             }
         }
@@ -180,7 +181,7 @@ __global__ __launch_bounds__(kStdpBlock) void k_stdp(StdpArgs a)
         __syncthreads();  // staging arrays are rewritten by the next batch
     }
     written = block_sum_i64_n<kStdpBlock>(written, sh);
-    if (tid == 0) a.stats[blockIdx.x] += written;
+    if (tid == 0) add_stat(a.stats + blockIdx.x, written);
 }
 
 // Row-wise layout: waves walk the rows to update in parts of up to U*64
@@ -277,7 +278,8 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
     const int line0 = lane & ~(kStoreLine - 1);  // first lane of this lane's store line
     const int gw = (bid * NT + tid) / kWave;
     const int nwv = nblocks * (NT / kWave);
-    const int nrows = a.row_cnt ? *a.row_cnt : a.n_rows_all;
+    const int64_t t = a.clk->t - 1;
+    const int nrows = a.tx_rows ? *a.tx_cnt : a.row_cnt ? *a.row_cnt : a.n_rows_all;
     long long written = 0;
 
     // cursor: the next part to issue (row snapshot, row-list index, base);
@@ -432,7 +434,7 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
         }
         __builtin_amdgcn_wave_barrier();
         if (ri.age_pre != 0 && p.base == -(int)(ri.rs & (kStoreLine - 1)) && lane == 0) {  // first part
-            a.t_last[ri.k] = (int32_t)a.t;
+            a.t_last[ri.k] = (int32_t)t;
             a.xpre[ri.k] = ri.xp_now;
         }
         const int len = ri.age_pre != 0 ? ri.len : 0;
@@ -608,19 +610,28 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
     // a delay block's item (b, slice, chunk) takes step b's ring list and
     // writes partial sums of step b (b varies slowest: an XCD's range of
     // items covers neighbouring slices)
-    const int32_t *list = a.list, *cntp = a.cnt;
+    // step t = clk->t - 1 delivers the spikes of step t - D + 1; a delay
+    // block starting at step t0 = clk->t delivers those of t0 + 1 - D + b
+    const int64_t t = a.clk->t - 1;
+    int slot = ring_slot(t - (a.delay - 1), a.delay);
     long long *parts = a.apart;
     int q = qa;
     if (a.batch > 0) {
         const int per = a.n_slices * a.chunks;
         const int bb = qa / per;
         q = qa - bb * per;
-        const int64_t d = a.delay;
-        const int slot = (int)(((a.t_emit0 + bb) % d + d) % d);
-        list = a.ring + (int64_t)slot * a.n;
-        cntp = a.ring_cnt + slot;
+        slot = ring_slot(t + 2 - a.delay + bb, a.delay);
         parts = a.abatch + (int64_t)bb * a.chunks * a.part_stride;
+    } else if (qa == 0 && threadIdx.x == 0) {
+        // the next neuron update reads this delivery's output: the fp32
+        // input with one chunk, else the C partial sums
+        a.clk->input_forced = a.chunks == 1 ? 1 : 0;
+        a.clk->n_parts = a.chunks;
     }
+    // (the count of a single step's transmitted list is at a fixed address:
+    // loading it does not wait for the clock)
+    const int32_t *list = a.ring + (int64_t)slot * a.n;
+    const int32_t *cntp = a.batch > 0 ? a.ring_cnt + slot : a.tx_cnt;
     const int s = q / a.chunks, c = q - s * a.chunks;
     const int C = a.chunks;
     const int base = s * a.width;
@@ -701,7 +712,7 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
                 s_xp0[tid] = xp0;
                 s_xpn[tid] = xpn;
                 if (a.plastic && s == 0 && ap != 0) {
-                    a.t_last[k] = (int32_t)a.t;
+                    a.t_last[k] = (int32_t)t;
                     a.xpre[k] = xpn;
                 }
             }
@@ -805,8 +816,8 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
     if (tid % kWave == 0 && written) atomicAdd(&s_written, (unsigned long long)written);
     __syncthreads();  // the accumulation barrier: every LDS atomic is done
     if (tid == 0) {
-        a.stats[2 * (int64_t)bid] += ev;
-        a.stats[2 * (int64_t)bid + 1] += (int64_t)s_written;
+        add_stat(a.stats + 2 * (int64_t)bid, ev);
+        add_stat(a.stats + 2 * (int64_t)bid + 1, (long long)s_written);
     }
     if (a.chunks == 1 && a.batch == 0) {
         for (int x = tid; x < a.width; x += kDlvBlock) {
@@ -871,12 +882,19 @@ __global__ __launch_bounds__(kBlock) void k_deliver_global(DeliverArgs a)
     const int tid = threadIdx.x, lane = tid % kWave;
     const int gw = (blockIdx.x * kBlock + tid) / kWave;
     const int nwv = gridDim.x * (kBlock / kWave);
-    const int cnt = *a.cnt;
+    const int64_t t = a.clk->t - 1;
+    const int slot = ring_slot(t - (a.delay - 1), a.delay);
+    const int32_t *list = a.ring + (int64_t)slot * a.n;
+    const int cnt = a.ring_cnt[slot];
+    if (blockIdx.x == 0 && tid == 0) {  // the next neuron update adds the one sum
+        a.clk->input_forced = 0;
+        a.clk->n_parts = 1;
+    }
     const int32_t *__restrict__ col = a.col;
     const float *__restrict__ wgt = a.w;
     long long ev = 0;
     for (int x = gw; x < cnt; x += nwv) {
-        const int k = a.list[x];
+        const int k = list[x];
         const int64_t rs = a.row_ptr[k], re = a.row_ptr[k + 1];
         long long *dst = (a.nacc == 2 && k >= a.n_exc) ? a.apart + a.n : a.apart;
         for (int64_t e0 = rs; e0 < re; e0 += kWave * kGlobalUnroll) {
@@ -902,7 +920,7 @@ __global__ __launch_bounds__(kBlock) void k_deliver_global(DeliverArgs a)
         if (lane == 0) ev += re - rs;
     }
     ev = block_sum_i64(ev, sh);
-    if (tid == 0) a.stats[2 * (int64_t)blockIdx.x] += ev;
+    if (tid == 0) add_stat(a.stats + 2 * (int64_t)blockIdx.x, ev);
 }
 
 // ---------------------------------------------------------------------------
@@ -964,8 +982,7 @@ hipError_t launch_stdp(hipStream_t s, const StdpArgs &a, int blocks, size_t lds,
     static int granted = 64 * 1024;
     const hipError_t e = allow_dynamic_lds((const void *)k_stdp, (int)lds, mu, granted);
     if (e != hipSuccess) return e;
-    hipExtLaunchKernelGGL(k_stdp, dim3(blocks), dim3(kStdpBlock), lds, s,
-                          ev.start, ev.stop, 0, a);
+    launch_kernel(k_stdp, dim3(blocks), dim3(kStdpBlock), lds, s, ev, a);
     return hipGetLastError();
 }
 
@@ -981,11 +998,9 @@ hipError_t launch_stdp_rows(hipStream_t s, const StdpArgs &a, int blocks, Kernel
     const hipError_t e = allow_dynamic_lds(kern, (int)lds, mu, granted[a.hw == 2]);
     if (e != hipSuccess) return e;
     if (a.hw == 2)
-        hipExtLaunchKernelGGL(k_stdp_rows<2>, dim3(blocks), dim3(kStdpRowsBlock), lds, s,
-                              ev.start, ev.stop, 0, a);
+        launch_kernel(k_stdp_rows<2>, dim3(blocks), dim3(kStdpRowsBlock), lds, s, ev, a);
     else
-        hipExtLaunchKernelGGL(k_stdp_rows<1>, dim3(blocks), dim3(kStdpRowsBlock), lds, s,
-                              ev.start, ev.stop, 0, a);
+        launch_kernel(k_stdp_rows<1>, dim3(blocks), dim3(kStdpRowsBlock), lds, s, ev, a);
     return hipGetLastError();
 }
 
@@ -996,8 +1011,7 @@ hipError_t launch_stdp_naive(hipStream_t s, const NaiveArgs &a, int blocks, Kern
     const size_t lds = (size_t)a.nw * sizeof(uint64_t);
     const hipError_t e = allow_dynamic_lds((const void *)k_stdp_naive, (int)lds, mu, granted);
     if (e != hipSuccess) return e;
-    hipExtLaunchKernelGGL(k_stdp_naive, dim3(blocks), dim3(kNaiveBlock), lds, s,
-                          ev.start, ev.stop, 0, a);
+    launch_kernel(k_stdp_naive, dim3(blocks), dim3(kNaiveBlock), lds, s, ev, a);
     return hipGetLastError();
 }
 
@@ -1010,11 +1024,9 @@ hipError_t launch_deliver_lds(hipStream_t s, const DeliverArgs &a, int blocks, s
     const hipError_t e = allow_dynamic_lds(kern, (int)lds, mu, granted[ct]);
     if (e != hipSuccess) return e;
     if (ct)
-        hipExtLaunchKernelGGL(k_deliver_lds<true>, dim3(blocks), dim3(kDlvBlock), lds, s,
-                              ev.start, ev.stop, 0, a);
+        launch_kernel(k_deliver_lds<true>, dim3(blocks), dim3(kDlvBlock), lds, s, ev, a);
     else
-        hipExtLaunchKernelGGL(k_deliver_lds<false>, dim3(blocks), dim3(kDlvBlock), lds, s,
-                              ev.start, ev.stop, 0, a);
+        launch_kernel(k_deliver_lds<false>, dim3(blocks), dim3(kDlvBlock), lds, s, ev, a);
     return hipGetLastError();
 }
 
@@ -1024,8 +1036,7 @@ hipError_t launch_probe_rows(hipStream_t s, int blocks, const int64_t *row_ptr,
                              unsigned long long *sink, KernelEvents ev)
 {
     if (n_rows < 1 || n_plastic < 1 || blocks < 1) return hipErrorInvalidValue;
-    hipExtLaunchKernelGGL(k_probe_rows, dim3(blocks), dim3(kStdpRowsBlock), 0, s,
-                          ev.start, ev.stop, 0, row_ptr, pend, col, w, n_rows, n_plastic, seed,
+    launch_kernel(k_probe_rows, dim3(blocks), dim3(kStdpRowsBlock), 0, s, ev, row_ptr, pend, col, w, n_rows, n_plastic, seed,
                           write, sink);
     return hipGetLastError();
 }
@@ -1045,18 +1056,17 @@ hipError_t launch_synapse_pass(hipStream_t s, const DeliverArgs &d, const StdpAr
     if (e != hipSuccess) return e;
     const dim3 g(nd + ns), b(kDlvBlock);
     switch (k) {
-    case 0: hipExtLaunchKernelGGL((k_synapse_pass<false, 1>), g, b, lds, s, ev.start, ev.stop, 0, d, a, nd); break;
-    case 1: hipExtLaunchKernelGGL((k_synapse_pass<false, 2>), g, b, lds, s, ev.start, ev.stop, 0, d, a, nd); break;
-    case 2: hipExtLaunchKernelGGL((k_synapse_pass<true, 1>), g, b, lds, s, ev.start, ev.stop, 0, d, a, nd); break;
-    default: hipExtLaunchKernelGGL((k_synapse_pass<true, 2>), g, b, lds, s, ev.start, ev.stop, 0, d, a, nd); break;
+    case 0: launch_kernel((k_synapse_pass<false, 1>), g, b, lds, s, ev, d, a, nd); break;
+    case 1: launch_kernel((k_synapse_pass<false, 2>), g, b, lds, s, ev, d, a, nd); break;
+    case 2: launch_kernel((k_synapse_pass<true, 1>), g, b, lds, s, ev, d, a, nd); break;
+    default: launch_kernel((k_synapse_pass<true, 2>), g, b, lds, s, ev, d, a, nd); break;
     }
     return hipGetLastError();
 }
 
 hipError_t launch_deliver_global(hipStream_t s, const DeliverArgs &a, int blocks, KernelEvents ev)
 {
-    hipExtLaunchKernelGGL(k_deliver_global, dim3(blocks), dim3(kBlock), 0, s,
-                          ev.start, ev.stop, 0, a);
+    launch_kernel(k_deliver_global, dim3(blocks), dim3(kBlock), 0, s, ev, a);
     return hipGetLastError();
 }
 

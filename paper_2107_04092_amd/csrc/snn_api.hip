@@ -57,10 +57,15 @@ struct snn_ctx {
     uint64_t *hist = nullptr, *mask = nullptr, *txmask = nullptr;
     uint8_t *code = nullptr;  // per-neuron history codes (k_neuron), n + 16 bytes
     uint64_t *recent = nullptr;
-    unsigned long long *list_acc = nullptr;  // list reservations of the neuron kernel (0 between steps)
+    StepClock *clk = nullptr;  // per-step scalars on the device (step index, input source)
+    // list-scan status words: k_neuron uses the first neuron_grid(n); a delay
+    // block's step k the row k of status_stride words
+    unsigned long long *status = nullptr;
+    int32_t status_stride = 0, status_words = 0;
     int32_t *spk_pos = nullptr;  // [D][n] spike-list positions (D > 1 with plasticity), else unused
     int32_t *ring = nullptr, *ring_cnt = nullptr;
     int32_t *rows = nullptr, *row_cnt = nullptr, *err_flag = nullptr, *maxlen = nullptr;
+    int32_t *tx_cnt = nullptr;  // transmitted spikes of the step in progress (count)
     int64_t *row_ptr = nullptr, *scratch = nullptr, *bsum = nullptr;
     int64_t *gstats = nullptr, *info_stats = nullptr, *syn_stats = nullptr, *dlv_stats = nullptr;
     RowInfo *info = nullptr, *txinfo = nullptr;
@@ -83,10 +88,16 @@ struct snn_ctx {
     int32_t counted_kind = -1;
     double counted_p = 0.0;
 
-    // time
-    int64_t t = 0, steps_done = 0, last_neuron_t = -1, last_deliver_t = -1;
-    int32_t n_parts = 1;       // partial sums written by the last delivery
-    int32_t input_forced = 1;  // next neuron update reads `ain` instead of partials
+    // time, as the host sees it: t is the step in progress or the next one
+    // (the device clock counts neuron updates: t + 1 while a step is in
+    // progress); a step is in progress when last_neuron_t == t
+    int64_t t = 0, last_neuron_t = -1, last_deliver_t = -1;
+};
+
+// A captured sequence of steps (snn_graph_capture).
+struct snn_graph {
+    hipGraphExec_t exec = nullptr;
+    int32_t steps = 0;
 };
 
 namespace {
@@ -273,12 +284,16 @@ void plan_workspace(snn_ctx *c, uint8_t *base)
     c->txmask = p.take<uint64_t>(c->nw);
     c->code = p.take<uint8_t>((int64_t)c->n + 16);
     c->recent = p.take<uint64_t>(c->nw);
-    c->list_acc = p.take<unsigned long long>((int64_t)kBatchMax * kAccStride);
+    c->clk = p.take<StepClock>(1);
+    c->status_stride = neuron_steps_grid(c->n);
+    c->status_words = std::max<int32_t>(neuron_grid(c->n), kBatchMax * c->status_stride);
+    c->status = p.take<unsigned long long>(c->status_words);
     c->spk_pos = p.take<int32_t>(c->delay > 1 ? (int64_t)c->delay * n : 1);
     c->ring = p.take<int32_t>((int64_t)c->delay * n);
     c->ring_cnt = p.take<int32_t>(c->delay);
     c->rows = p.take<int32_t>(n);
     c->row_cnt = p.take<int32_t>(1);
+    c->tx_cnt = p.take<int32_t>(1);
     c->err_flag = p.take<int32_t>(1);
     c->maxlen = p.take<int32_t>(1);
     c->row_ptr = p.take<int64_t>(n + 1);
@@ -341,7 +356,6 @@ snn_status zero_stats(snn_ctx *c)
         e = launch_fill_i64(c->stream, c->info_stats, (int64_t)c->info_blocks * kStFields, 0);
     if (e == hipSuccess) e = launch_fill_i64(c->stream, c->syn_stats, c->syn_slots, 0);
     if (e == hipSuccess) e = launch_fill_i64(c->stream, c->dlv_stats, 2 * (int64_t)c->dlv_slots, 0);
-    c->steps_done = 0;
     return check_hip(c, e, "reset statistics");
 }
 
@@ -382,16 +396,35 @@ snn_status finish_graph(snn_ctx *c)
 }
 
 // Turns pending fixed-point partial inputs into the fp32 input the next
-// neuron update would compute, so it can be viewed or overwritten.
+// neuron update would compute, so it can be viewed or overwritten (the
+// device clock says which the next update reads; afterwards the fp32 one).
 snn_status materialize_input(snn_ctx *c)
 {
-    if (c->input_forced) return SNN_OK;
-    snn_status st = check_hip(c, launch_materialize_input(c->stream, c->apart,
-                                                         (int64_t)c->nacc * c->n, c->n_parts,
-                                                         c->ain, (int64_t)c->nacc * c->n),
-                              "materialise input");
+    return check_hip(c, launch_materialize_input(c->stream, c->apart, (int64_t)c->nacc * c->n,
+                                                 c->clk, c->ain, (int64_t)c->nacc * c->n),
+                     "materialise input");
+}
+
+// Status words cleared (no stale step tag can match a later scan).
+hipError_t clear_status(snn_ctx *c)
+{
+    return launch_fill_i64(c->stream, (int64_t *)c->status, c->status_words, 0);
+}
+
+// The device clock read back (synchronises the stream); the host's view of
+// t follows it (a replayed capture advances the device only).
+snn_status sync_clock(snn_ctx *c, int64_t *dev_t)
+{
+    StepClock ck{};
+    snn_status st = check_hip(c, hipMemcpyAsync(&ck, c->clk, sizeof ck, hipMemcpyDeviceToHost,
+                                                c->stream), "read the step clock");
+    if (!st) st = check_hip(c, hipStreamSynchronize(c->stream), "read the step clock");
     if (st) return st;
-    c->input_forced = 1;
+    const bool in_step = c->last_neuron_t == c->t;
+    c->t = in_step ? ck.t - 1 : ck.t;
+    c->last_neuron_t = ck.t - 1;
+    if (!in_step) c->last_deliver_t = ck.t - 1;
+    *dev_t = ck.t;
     return SNN_OK;
 }
 
@@ -423,12 +456,12 @@ NeuronArgs neuron_args(snn_ctx *c)
     a.apart = c->apart;
     a.ain = c->ain;
     a.part_stride = (int64_t)c->nacc * c->n;
-    a.input_forced = c->input_forced;
+    a.max_parts = c->chunks;
+    a.clk = c->clk;
     a.mask = c->mask;
     a.txmask = c->txmask;
     a.code = c->code;
     a.recent = c->recent;
-    a.t = c->t;
     a.n = c->n;
     a.n_exc = c->cfg.n_exc;
     a.model = c->cfg.neuron_model;
@@ -436,7 +469,6 @@ NeuronArgs neuron_args(snn_ctx *c)
     a.dm1 = c->delay - 1;
     a.ref_steps = c->ref_steps;
     a.poisson_len = c->cfg.neuron_model == SNN_LIF_DELTA ? c->cfg.poisson_len : 0;
-    a.n_parts = c->n_parts;
     a.k_m = c->k_m;
     a.v_th = c->v_th;
     a.v_reset = c->v_reset;
@@ -455,13 +487,14 @@ snn_status launch_step_neurons(snn_ctx *c)
 {
     NeuronArgs a = neuron_args(c);
     CompactArgs b{};
-    b.spk_list = c->ring + (int64_t)ring_slot(c, c->t) * c->n;
-    b.spk_cnt = c->ring_cnt + ring_slot(c, c->t);
+    b.ring = c->ring;
+    b.ring_cnt = c->ring_cnt;
+    b.tx_cnt = c->tx_cnt;
     b.row_list = c->rows;
     b.row_cnt = c->row_cnt;
-    b.acc = c->list_acc;
-    b.spk_pos = c->spk_pos + (c->delay > 1 ? (int64_t)ring_slot(c, c->t) * c->n : 0);
-    b.tx_pos = c->spk_pos + (c->delay > 1 ? (int64_t)ring_slot(c, c->t - (c->delay - 1)) * c->n : 0);
+    b.status = c->status;
+    b.spk_pos = c->spk_pos;
+    b.delay = c->delay;
     b.gstats = c->gstats;
     b.n = c->n;
     b.nw = c->nw;
@@ -476,13 +509,10 @@ snn_status launch_step_neurons(snn_ctx *c)
     b.xpre = c->xpre;
     b.err = c->err_flag;
     b.info_stats = c->n_plastic_rows > 0 && c->algo != 2 ? c->info_stats : nullptr;
-    b.t = c->t;
-    b.dm1 = c->delay - 1;
     for (int q = 0; q <= kMaxAge; ++q) b.dpow[q] = c->dpow[q];
     snn_status st =
         check_hip(c, launch_neuron(c->stream, a, b, part_events(c, 0)), "neuron kernel");
     if (st) return st;
-    c->input_forced = 0;  // the input has been consumed; the next comes from delivery
     c->last_neuron_t = c->t;
     return SNN_OK;
 }
@@ -505,7 +535,8 @@ StdpArgs stdp_args(snn_ctx *c, bool flush, int64_t waves = 0)
     a.n_rows_all = c->n_plastic_rows;
     a.t_last = c->t_last;
     a.xpre = c->xpre;
-    a.t = flush ? c->t - 1 : c->t;
+    a.clk = c->clk;
+    a.tx_cnt = c->tx_cnt;
     a.col = c->col;
     a.w = c->w;
     a.piv = c->piv;
@@ -569,7 +600,7 @@ snn_status launch_plasticity(snn_ctx *c, bool flush, hipStream_t s, KernelEvents
         r.row_cnt = nullptr;
         r.n_rows_all = c->n_plastic_rows;
         r.dm1 = c->delay - 1;
-        r.t = c->t - 1;
+        r.clk = c->clk;
         r.row_ptr = c->row_ptr;
         r.pend = c->pend;
         r.hist = c->hist;
@@ -627,9 +658,11 @@ DeliverArgs deliver_args(snn_ctx *c)
     a.col = c->col;
     a.w = c->w;
     a.piv = c->piv;
-    const int slot = ring_slot(c, c->t - (c->delay - 1));
-    a.list = c->ring + (int64_t)slot * c->n;
-    a.cnt = c->ring_cnt + slot;
+    a.ring = c->ring;
+    a.ring_cnt = c->ring_cnt;
+    a.tx_cnt = c->tx_cnt;
+    a.clk = c->clk;
+    a.delay = c->delay;
     a.apart = c->apart;
     a.ain = c->ain;
     a.part_stride = (int64_t)c->nacc * c->n;
@@ -650,7 +683,6 @@ DeliverArgs deliver_args(snn_ctx *c)
     a.ypost = c->ypost;
     a.t_last = c->t_last;
     a.xpre = c->xpre;
-    a.t = c->t;
     a.c_pot = c->c_pot;
     a.c_dep = c->c_dep;
     a.mu = c->mu;
@@ -674,9 +706,7 @@ snn_status launch_step_synapse_pass(snn_ctx *c, KernelEvents ev)
     snn_status st =
         check_hip(c, launch_synapse_pass(c->stream, d, a, nd, ns, lds, ev), "synapse pass kernel");
     if (st) return st;
-    c->n_parts = c->chunks;
     c->last_deliver_t = c->t;
-    c->input_forced = c->chunks == 1 ? 1 : 0;
     return SNN_OK;
 }
 
@@ -690,10 +720,7 @@ snn_status launch_step_delivery(snn_ctx *c, int32_t mode)
                                              part_events(c, 2)),
                        "slice delivery kernel");
         if (st) return st;
-        c->n_parts = c->chunks;
         c->last_deliver_t = c->t;
-        // with one chunk each workgroup owns its slice and stores the fp32 input
-        c->input_forced = c->chunks == 1 ? 1 : 0;
         return SNN_OK;
     }
     const KernelEvents ev = part_events(c, 2);
@@ -702,7 +729,7 @@ snn_status launch_step_delivery(snn_ctx *c, int32_t mode)
         // bring the transmitting rows up to date first (row-wise, L2 gathers)
         StdpArgs r = stdp_args(c, false);
         r.info = c->txinfo;
-        r.row_cnt = a.cnt;
+        r.tx_rows = 1;
         st = check_hip(c, launch_stdp_rows(c->stream, r, c->n_cu, {ev.start, nullptr}),
                        "STDP of transmitting rows");
         if (st) return st;
@@ -713,8 +740,6 @@ snn_status launch_step_delivery(snn_ctx *c, int32_t mode)
     st = check_hip(c, launch_deliver_global(c->stream, a, kGlobalMaxBlocks, last),
                    "global delivery kernel");
     if (st) return st;
-    c->n_parts = 1;
-    c->input_forced = 0;
     c->last_deliver_t = c->t;
     return SNN_OK;
 }
@@ -855,15 +880,14 @@ snn_status snn_bind_workspace(snn_ctx *c, void *device_ptr, size_t bytes)
     if (e == hipSuccess) e = launch_fill_f32(c->stream, c->ain, (int64_t)c->nacc * c->n, 0.f);
     if (e == hipSuccess) e = launch_fill_i32(c->stream, c->ring_cnt, c->delay, 0);
     if (e == hipSuccess) e = launch_fill_i32(c->stream, c->row_cnt, 1, 0);
-    if (e == hipSuccess) e = launch_fill_i64(c->stream, (int64_t *)c->list_acc,
-                                                (int64_t)kBatchMax * kAccStride, 0);
+    if (e == hipSuccess) e = launch_fill_i32(c->stream, c->tx_cnt, 1, 0);
+    if (e == hipSuccess) e = clear_status(c);
+    if (e == hipSuccess) e = launch_set_clock(c->stream, c->clk, 0, 1, 1);
     if (e == hipSuccess) e = launch_fill_i32(c->stream, c->err_flag, 1, 0);
     if (e == hipSuccess) e = launch_fill_i32(c->stream, c->pend, c->n, 0);
     snn_status st = check_hip(c, e, "workspace initialisation");
     if (st) return st;
     c->t = 0;
-    c->n_parts = 1;
-    c->input_forced = 1;
     c->last_neuron_t = c->last_deliver_t = -1;
     c->graph_state = 0;
     return zero_stats(c);
@@ -1027,6 +1051,9 @@ snn_status snn_update_neurons(snn_ctx *c)
     if (!c) return SNN_EINVAL;
     snn_status st = require_graph(c);
     if (st) return st;
+    if (c->last_neuron_t == c->t)
+        return fail(c, SNN_ESTATE, "step %lld is in progress: finish it with snn_advance",
+                    (long long)c->t);
     return launch_step_neurons(c);
 }
 
@@ -1059,8 +1086,7 @@ snn_status snn_advance(snn_ctx *c)
     if (st) return st;
     if (c->last_neuron_t != c->t)
         return fail(c, SNN_ESTATE, "step %lld has not run", (long long)c->t);
-    c->t += 1;
-    c->steps_done += 1;
+    c->t += 1;  // the device clock advanced with the neuron update
     return SNN_OK;
 }
 
@@ -1072,6 +1098,9 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
     if (n_steps < 0) return fail(c, SNN_EINVAL, "n_steps must be >= 0");
     if (mode != SNN_DELIVER_LDS_SLICE && mode != SNN_DELIVER_GLOBAL_ATOMIC)
         return fail(c, SNN_EINVAL, "unknown delivery mode %d", mode);
+    if (c->last_neuron_t == c->t)
+        return fail(c, SNN_ESTATE, "step %lld is in progress: finish it with snn_advance",
+                    (long long)c->t);
     // a small network without plasticity runs whole steps in one workgroup
     // (unless kernel times are being recorded per step)
     const bool small = mode == SNN_DELIVER_LDS_SLICE && c->n_plastic_rows == 0 &&
@@ -1090,16 +1119,15 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
         b.apart = c->apart;
         b.gstats = c->gstats;
         b.dlv_stats = c->dlv_stats;
+        b.status = c->status;
+        b.status_words = c->status_words;
         b.n_exc = c->cfg.n_exc;
         b.nacc = c->nacc;
         b.steps = k;
         if ((st = check_hip(c, launch_small_steps(c->stream, a, b), "small-network steps")))
             return st;
         c->t += k;
-        c->steps_done += k;
         c->last_neuron_t = c->last_deliver_t = c->t - 1;
-        c->n_parts = 1;
-        c->input_forced = 0;
         q += k;
     }
     if (small) return SNN_OK;
@@ -1111,10 +1139,6 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
         const int32_t B = std::min<int32_t>(n_steps - q, c->batch_max);
         DeliverArgs d = deliver_args(c);
         d.batch = B;
-        d.delay = c->delay;
-        d.t_emit0 = c->t + 1 - c->delay;
-        d.ring = c->ring;
-        d.ring_cnt = c->ring_cnt;
         d.abatch = c->abatch;
         d.chunks = 1;
         d.n_work = B * c->n_slices;
@@ -1127,7 +1151,8 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
         b.ring = c->ring;
         b.ring_cnt = c->ring_cnt;
         b.delay = c->delay;
-        b.acc = c->list_acc;
+        b.status = c->status;
+        b.status_stride = c->status_stride;
         b.abatch = c->abatch;
         b.apart = c->apart;
         b.gstats = c->gstats;
@@ -1136,10 +1161,7 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
         if ((st = check_hip(c, launch_neuron_steps(c->stream, a, b), "delay-block neurons")))
             return st;
         c->t += B;
-        c->steps_done += B;
         c->last_neuron_t = c->last_deliver_t = c->t - 1;
-        c->n_parts = 1;
-        c->input_forced = 0;
         q += B;
     }
     if (blocks) return SNN_OK;
@@ -1156,7 +1178,6 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
         }
         if (c->t_used < c->t_cap) c->t_used += 1;
         c->t += 1;
-        c->steps_done += 1;
     }
     return SNN_OK;
 }
@@ -1216,6 +1237,9 @@ snn_status snn_flush_plasticity(snn_ctx *c)
     if (!c) return SNN_EINVAL;
     snn_status st = require_graph(c);
     if (st) return st;
+    if (c->last_neuron_t == c->t)
+        return fail(c, SNN_ESTATE, "step %lld is in progress: finish it with snn_advance",
+                    (long long)c->t);
     if (c->n_plastic_rows == 0 || c->t == 0 || c->algo == 2) return SNN_OK;  // naive: current
     return launch_plasticity(c, true, c->stream);
 }
@@ -1268,17 +1292,8 @@ snn_status snn_get_state(snn_ctx *c, snn_state_view *out)
     if (st) return st;
     st = materialize_input(c);
     if (st) return st;
-    for (int q = 0; q < c->delay && !st; ++q)
-        st = check_hip(c,
-                       launch_sort_list(c->stream, c->ring + (int64_t)q * c->n, c->ring_cnt + q,
-                                        (uint64_t *)c->scratch,
-                                        c->delay > 1 ? c->spk_pos + (int64_t)q * c->n : nullptr,
-                                        c->n),
-                       "list sort");
-    if (!st)
-        st = check_hip(c, launch_sort_list(c->stream, c->rows, c->row_cnt, (uint64_t *)c->scratch,
-                                           nullptr, c->n),
-                       "list sort");
+    int64_t dev_t = 0;
+    st = sync_clock(c, &dev_t);
     if (st) return st;
     std::memset(out, 0, sizeof *out);
     out->t = c->t;
@@ -1293,10 +1308,12 @@ snn_status snn_get_state(snn_ctx *c, snn_state_view *out)
     out->input_exc = c->ain;
     out->input_inh = c->nacc == 2 ? c->ain + c->n : nullptr;
     out->spike_mask = c->mask;
-    const int sl = ring_slot(c, c->last_neuron_t < 0 ? 0 : c->last_neuron_t);
+    // the last neuron update ran step dev_t - 1; the last delivery sent the
+    // spikes of step dev_t - D
+    const int sl = ring_slot(c, dev_t > 0 ? dev_t - 1 : 0);
     out->spike_list = c->ring + (int64_t)sl * c->n;
     out->spike_count = c->ring_cnt + sl;
-    const int tl = ring_slot(c, c->last_deliver_t < 0 ? 0 : c->last_deliver_t - (c->delay - 1));
+    const int tl = ring_slot(c, dev_t > 0 ? dev_t - c->delay : 0);
     out->tx_list = c->ring + (int64_t)tl * c->n;
     out->tx_count = c->ring_cnt + tl;
     out->stdp_rows = c->rows;
@@ -1340,6 +1357,13 @@ snn_status snn_set_state(snn_ctx *c, const snn_state_view *in)
                        "ring positions");
         if (st) return st;
     }
+    // the clock: step t, the fp32 input when one was given; the scans' status
+    // words cleared (their step tags refer to the old clock)
+    const bool inp = in->input_exc || in->input_inh;
+    hipError_t e = launch_set_clock(c->stream, c->clk, in->t, inp ? 1 : -1, 1);
+    if (e == hipSuccess) e = clear_status(c);
+    st = check_hip(c, e, "set the step clock");
+    if (st) return st;
     c->t = in->t;
     c->last_neuron_t = c->last_deliver_t = -1;
     return SNN_OK;
@@ -1386,7 +1410,7 @@ snn_status snn_get_stats(snn_ctx *c, snn_stats *out)
     st = check_hip(c, e, "read statistics");
     if (st) return st;
     std::memset(out, 0, sizeof *out);
-    out->steps = c->steps_done;
+    out->steps = g[kGSteps];
     out->spikes = g[kGSpikes];
     out->stdp_synapse_updates = g[kGNaiveSyn];  // naive plasticity (0 otherwise)
     out->device_errors = err;
@@ -1411,6 +1435,76 @@ snn_status snn_reset_stats(snn_ctx *c)
     snn_status st = require_ws(c);
     if (st) return st;
     return zero_stats(c);
+}
+
+snn_status snn_graph_capture(snn_ctx *c, int32_t n_steps, int32_t mode, snn_graph **out)
+{
+    if (!c || !out) return SNN_EINVAL;
+    *out = nullptr;
+    snn_status st = require_graph(c);
+    if (st) return st;
+    if (n_steps < 1) return fail(c, SNN_EINVAL, "n_steps must be >= 1");
+    if (!c->stream) return fail(c, SNN_EINVAL, "the null stream cannot be captured");
+    if (c->t_used < c->t_cap)
+        return fail(c, SNN_ESTATE, "kernel times are being recorded");
+    if (c->last_neuron_t == c->t)
+        return fail(c, SNN_ESTATE, "step %lld is in progress: finish it with snn_advance",
+                    (long long)c->t);
+    // the capture records the launches only: the host's view of time is put back
+    const int64_t t0 = c->t, ln = c->last_neuron_t, ld = c->last_deliver_t;
+    st = check_hip(c, hipStreamBeginCapture(c->stream, hipStreamCaptureModeThreadLocal),
+                   "begin capture");
+    if (st) return st;
+    st = snn_step(c, n_steps, mode);
+    const std::string step_err = c->err;
+    hipGraph_t g = nullptr;
+    const hipError_t e = hipStreamEndCapture(c->stream, &g);
+    c->t = t0;
+    c->last_neuron_t = ln;
+    c->last_deliver_t = ld;
+    if (st) {
+        if (g) (void)hipGraphDestroy(g);
+        c->err = step_err;
+        return st;
+    }
+    st = check_hip(c, e, "end capture");
+    if (st) return st;
+    hipGraphExec_t ex = nullptr;
+    const hipError_t ei = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    st = check_hip(c, ei, "instantiate the captured steps");
+    if (st) return st;
+    snn_graph *h = new (std::nothrow) snn_graph();
+    if (!h) {
+        (void)hipGraphExecDestroy(ex);
+        return fail(c, SNN_ENOMEM, "host allocation failed");
+    }
+    h->exec = ex;
+    h->steps = n_steps;
+    *out = h;
+    return SNN_OK;
+}
+
+snn_status snn_graph_launch(snn_ctx *c, snn_graph *g)
+{
+    if (!c || !g || !g->exec) return SNN_EINVAL;
+    snn_status st = require_graph(c);
+    if (st) return st;
+    if (c->last_neuron_t == c->t)
+        return fail(c, SNN_ESTATE, "step %lld is in progress: finish it with snn_advance",
+                    (long long)c->t);
+    st = check_hip(c, hipGraphLaunch(g->exec, c->stream), "launch the captured steps");
+    if (st) return st;
+    c->t += g->steps;
+    c->last_neuron_t = c->last_deliver_t = c->t - 1;
+    return SNN_OK;
+}
+
+void snn_graph_destroy(snn_graph *g)
+{
+    if (!g) return;
+    if (g->exec) (void)hipGraphExecDestroy(g->exec);
+    delete g;
 }
 
 }  // extern "C"

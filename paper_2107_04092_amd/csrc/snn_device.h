@@ -9,6 +9,7 @@
 #include <hip/hip_ext.h>
 
 #include <mutex>
+#include <utility>
 
 namespace snn {
 namespace {
@@ -45,6 +46,14 @@ __device__ __forceinline__ float pow_mu(float w, float mu)
 __device__ __forceinline__ long long to_fix(float x) { return __float2ll_rn(x * kFixScale); }
 // fixed point -> fp32, one correctly rounded conversion (the scaling is exact)
 __device__ __forceinline__ float from_fix(long long s) { return __ll2float_rn(s) * kFixUnit; }
+
+// Adds v to a 64-bit counter in global memory without waiting for it (an
+// atomic whose result is unused needs no round trip; a read-modify-write
+// would wait for the read).
+__device__ __forceinline__ void add_stat(int64_t *p, long long v)
+{
+    if (v) (void)atomicAdd((unsigned long long *)p, (unsigned long long)v);
+}
 
 __device__ __forceinline__ int wave_sum_i32(int v)
 {
@@ -298,12 +307,206 @@ __device__ __forceinline__ float stdp_synapse_steps(float w, uint64_t h0, uint64
     return w;
 }
 
+// Delay-ring slot of a step (steps before 0 wrap like the ring).
+__device__ __forceinline__ int ring_slot(int64_t step, int d)
+{
+    const int64_t r = step % d;
+    return (int)(r < 0 ? r + d : r);
+}
+
+// A list scan's status word (see kStatusAgg): counts a and b of step t.
+__device__ __forceinline__ unsigned long long status_word(int a, int b, int64_t t,
+                                                          unsigned long long kind)
+{
+    return (unsigned long long)(uint32_t)a | ((unsigned long long)(uint32_t)b << 24) |
+           ((unsigned long long)(t & 0x3fff) << 48) | kind;
+}
+
+__device__ __forceinline__ void publish_status(unsigned long long *p, unsigned long long w)
+{
+    __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Exclusive prefix, over the workgroups before workgroup b, of the two
+// counts of `nscan` (<= R) list scans, by decoupled look-back. Scan r keeps
+// its status words at status + r * stride (one per workgroup) and belongs to
+// step t0 + r. The NT threads read a window of NT predecessors at once
+// (thread i: workgroup base - 1 - i). In each scan the nearest predecessor
+// that has published an inclusive prefix ends the walk; every workgroup
+// between it and b must have published its own counts for that step, else
+// the window is read again. Workgroup 0 publishes an inclusive prefix
+// without waiting, so every walk ends once the workgroups before b have
+// started, which in-order dispatch guarantees. The wait is bounded: after
+// kLookbackSpins rounds the error flag is raised and the counts found so far
+// are used (list writers check their offsets). Called by every thread of
+// the workgroup with workgroup-uniform arguments. The state of each scan
+// lives in LDS (sh: 8 R ints); on return sh[8 r + 6] and sh[8 r + 7] hold
+// scan r's two prefixes.
+template <int NT, int R>
+__device__ void lookback(unsigned long long *status, int64_t stride, int nscan, int b,
+                         int64_t t0, int *sh, int32_t *err)
+{
+    // sh[8 r + ...]: 0 nearest inclusive in the window (NT: none), 1 lanes
+    // not yet published, 2-3 the window's sums, 4 window end, 5 done, 6-7 prefixes
+    const int tid = threadIdx.x, lane = tid % kWave;
+    if (tid < R) {
+        int *q = sh + 8 * tid;
+        q[4] = b;
+        q[5] = b == 0 || tid >= nscan;
+        q[6] = q[7] = 0;
+    }
+    // the earlier workgroups publish at about the same time as this one: a
+    // read issued at once mostly finds their words not yet visible and
+    // costs a second round trip (measured: 0.6 us more per launch)
+    if (b > 0) __builtin_amdgcn_s_sleep(kLookbackDelay);
+    __syncthreads();
+    for (int rounds = 0;; ++rounds) {
+        bool all = true;
+#pragma unroll
+        for (int r = 0; r < R; ++r) all = all && sh[8 * r + 5] != 0;
+        if (all) break;
+        if (rounds >= kLookbackSpins) {
+            if (tid == 0) atomicOr(err, kErrLookback);
+            break;
+        }
+        unsigned long long w[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {  // every read of the round in flight together
+            const int p = sh[8 * r + 4] - 1 - tid;
+            w[r] = 0ull;
+            if (!sh[8 * r + 5] && p >= 0)
+                w[r] = __hip_atomic_load(status + r * stride + p, __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_AGENT);
+        }
+        __syncthreads();  // window ends read before the per-round fields are reset
+        if (tid < R) {
+            sh[8 * tid] = NT;
+            sh[8 * tid + 1] = sh[8 * tid + 2] = sh[8 * tid + 3] = 0;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < R; ++r) {  // the nearest inclusive prefix of the window
+            if (sh[8 * r + 5]) continue;
+            const unsigned tag = (unsigned)((t0 + r) & 0x3fff);
+            const bool inc = sh[8 * r + 4] - 1 - tid >= 0 && (w[r] >> 62) == 2ull &&
+                             (unsigned)((w[r] >> 48) & 0x3fff) == tag;
+            const uint64_t bl = ballot64(inc);
+            if (bl && lane == __ffsll((long long)bl) - 1) atomicMin(&sh[8 * r], tid);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < R; ++r) {  // counts up to it; predecessors not yet published
+            if (sh[8 * r + 5]) continue;
+            const unsigned tag = (unsigned)((t0 + r) & 0x3fff);
+            const bool need = sh[8 * r + 4] - 1 - tid >= 0 && tid <= sh[8 * r];
+            const bool cur = (w[r] >> 62) != 0ull && (unsigned)((w[r] >> 48) & 0x3fff) == tag;
+            const uint64_t bad = ballot64(need && !cur);
+            int va = need && cur ? (int)(w[r] & 0xffffffull) : 0;
+            int vb = need && cur ? (int)((w[r] >> 24) & 0xffffffull) : 0;
+            va = wave_sum_i32(va);
+            vb = wave_sum_i32(vb);
+            if (lane == 0) {
+                if (bad) atomicAdd(&sh[8 * r + 1], (int)__popcll(bad));
+                if (va) atomicAdd(&sh[8 * r + 2], va);
+                if (vb) atomicAdd(&sh[8 * r + 3], vb);
+            }
+        }
+        __syncthreads();
+        if (tid < R && !sh[8 * tid + 5] && sh[8 * tid + 1] == 0) {  // the window is complete
+            int *q = sh + 8 * tid;
+            q[6] += q[2];
+            q[7] += q[3];
+            if (q[0] < NT || q[4] <= NT)
+                q[5] = 1;
+            else
+                q[4] -= NT;
+        }
+        __syncthreads();
+        bool retry = false;
+#pragma unroll
+        for (int r = 0; r < R; ++r) retry = retry || (!sh[8 * r + 5] && sh[8 * r + 1] != 0);
+        if (retry) __builtin_amdgcn_s_sleep(4);
+    }
+}
+
+// The same for up to NT/32 scans, one per half wave: scan r is looked back
+// over by threads 32 r .. 32 r + 31, a window of 32 predecessors at a time,
+// with ballots and shuffles inside the half wave, so the scans need no
+// workgroup barrier until the end. On return out[2 r], out[2 r + 1] (LDS)
+// hold scan r's two prefixes. Bounded as above.
+template <int NT>
+__device__ void lookback32(unsigned long long *status, int64_t stride, int nscan, int b,
+                           int64_t t0, int *out, int32_t *err)
+{
+    static_assert(NT % kWave == 0, "whole waves");
+    const int tid = threadIdx.x, lane = tid % kWave;
+    const int r = tid >> 5, gi = tid & 31, half = lane >> 5;
+    const bool active = r < nscan;
+    const unsigned tag = (unsigned)((t0 + r) & 0x3fff);
+    int base = b, acc_a = 0, acc_b = 0;
+    bool done = !active || b == 0;
+    if (b > 0) __builtin_amdgcn_s_sleep(kLookbackDelay);  // as in lookback
+    for (int rounds = 0;; ++rounds) {
+        if (!ballot64(!done)) break;  // both scans of the wave complete
+        if (rounds >= kLookbackSpins) {
+            if (!done && gi == 0) atomicOr(err, kErrLookback);
+            break;
+        }
+        const int p = base - 1 - gi;
+        unsigned long long w = 0ull;
+        if (!done && p >= 0)
+            w = __hip_atomic_load(status + r * stride + p, __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_AGENT);
+        const bool cur = (w >> 62) != 0ull && (unsigned)((w >> 48) & 0x3fff) == tag;
+        const uint32_t incm =
+            (uint32_t)(ballot64(cur && p >= 0 && (w >> 62) == 2ull) >> (32 * half));
+        const int ip = incm ? __ffs((int)incm) - 1 : 32;  // nearest inclusive prefix
+        const bool need = !done && p >= 0 && gi <= ip;
+        const uint32_t badm = (uint32_t)(ballot64(need && !cur) >> (32 * half));
+        int va = need && cur ? (int)(w & 0xffffffull) : 0;
+        int vb = need && cur ? (int)((w >> 24) & 0xffffffull) : 0;
+#pragma unroll
+        for (int off = 16; off > 0; off >>= 1) {  // sums inside the half wave
+            va += __shfl_xor(va, off, kWave);
+            vb += __shfl_xor(vb, off, kWave);
+        }
+        if (!done && badm == 0) {
+            acc_a += va;
+            acc_b += vb;
+            if (ip < 32 || base <= 32)
+                done = true;
+            else
+                base -= 32;
+        }
+        if (ballot64(!done && badm != 0)) __builtin_amdgcn_s_sleep(4);
+    }
+    if (active && gi == 0) {
+        out[2 * r] = acc_a;
+        out[2 * r + 1] = acc_b;
+    }
+    __syncthreads();
+}
+
 inline int blocks_for(int64_t count, int per = kBlock, int64_t cap = 1 << 20)
 {
     int64_t b = (count + per - 1) / per;
     if (b < 1) b = 1;
     if (b > cap) b = cap;
     return (int)b;
+}
+
+// Launches a kernel; with events, the launch places them around the kernel
+// itself (hipExtLaunchKernelGGL), else it is a plain launch, which a stream
+// capture can record.
+template <typename... KArgs, typename... Args>
+inline void launch_kernel(void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t lds,
+                          hipStream_t s, KernelEvents ev, Args &&...args)
+{
+    if (ev.start || ev.stop)
+        hipExtLaunchKernelGGL(kernel, grid, block, lds, s, ev.start, ev.stop, 0,
+                              std::forward<Args>(args)...);
+    else
+        hipLaunchKernelGGL(kernel, grid, block, lds, s, std::forward<Args>(args)...);
 }
 
 // Raises a kernel's dynamic-LDS limit to `bytes` (once per size increase).

@@ -10,11 +10,9 @@ namespace snn {
 
 constexpr int kBlock = 256;          // threads per workgroup of the element kernels
 constexpr int kNeuronBlock = 1024;   // threads per workgroup of the neuron update on large
-                                     // networks (one list reservation per workgroup)
+                                     // networks (one list-scan status word per workgroup)
 constexpr int kNeuronSmallN = 65536; // up to this many neurons the update takes kBlock threads
                                      // per workgroup
-constexpr int kNeuronRounds = 1;     // neurons per thread of the neuron update (more rounds
-                                     // mean fewer waves: slower on the stress network)
 constexpr int kWave = 64;            // CDNA wavefront width
 constexpr int kMaxPoisson = 32;
 constexpr int kMaxSortRow = 16384;   // longest row the LDS row sort accepts
@@ -43,10 +41,33 @@ constexpr float kFixUnit = 2.3283064365386963e-10f; // 2^-32
 enum StdpStat { kStRows = 0, kStForced = 1, kStSyn = 2, kStForcedSyn = 3, kStFields = 4 };
 
 // Global counters.
-enum GlobalStat { kGSpikes = 0, kGNaiveSyn = 1, kGFields = 8 };
+enum GlobalStat { kGSpikes = 0, kGNaiveSyn = 1, kGSteps = 2, kGFields = 8 };
 
 // Error bits raised by kernels (device int32, ORed).
-enum DevError { kErrIndex = 1, kErrRowTooLong = 2, kErrWindow = 4, kErrRing = 8 };
+enum DevError {
+    kErrIndex = 1, kErrRowTooLong = 2, kErrWindow = 4, kErrRing = 8,
+    kErrLookback = 16  // a list scan waited too long for an earlier workgroup
+};
+
+// Per-step scalars, kept on the device (one struct in the workspace). Every
+// kernel of a step reads them there rather than from its launch arguments,
+// and the neuron update advances the step index, so the launches of a step
+// are the same whatever step they run (a captured step replays correctly).
+struct StepClock {
+    long long t;           // neuron updates run so far: the index of the next step
+    int32_t input_forced;  // 1: the next neuron update reads the fp32 input `ain`
+    int32_t n_parts;       // 0: it adds this many fixed-point partial sums instead
+    long long pad_[2];
+};
+
+// Look-back status words of the list scans, one per workgroup (and step of
+// a multi-step launch): bits 0-23 and 24-47 two counts, bits 48-61 the step
+// they belong to (mod 2^14), bits 62-63 the kind: the workgroup's own counts
+// (aggregate) or those of it and every workgroup before it (inclusive).
+constexpr unsigned long long kStatusAgg = 1ull << 62;
+constexpr unsigned long long kStatusInc = 2ull << 62;
+constexpr int kLookbackSpins = 1 << 16;  // bound of the wait for an earlier workgroup (rounds)
+constexpr int kLookbackDelay = 16;       // s_sleep units (64 clocks) before the first read
 
 struct NeuronArgs {
     float *v;
@@ -56,16 +77,16 @@ struct NeuronArgs {
     float *ypost;
     const int32_t *t_last;
     const long long *apart; // fixed-point partial inputs [n_parts][nacc][n]
-    const float *ain;       // fp32 input [nacc][n], used when input_forced
+    const float *ain;       // fp32 input [nacc][n], used when clk->input_forced
     int64_t part_stride;    // nacc * n
-    int32_t input_forced;
+    int32_t max_parts;      // most partial sums a delivery writes (the chunk count)
+    StepClock *clk;         // step index and input source (advanced by the update)
     uint64_t *mask;         // spikes emitted at t
     uint64_t *txmask;       // spikes transmitted at t (emitted at t-D+1)
     uint8_t *code;          // per neuron: 0 no spike in the last 64 steps, 1 + i one spike
                             // at step t-i, kCodeMulti more than one (see k_neuron)
     uint64_t *recent;       // neurons with a spike in the last 64 steps (hist != 0)
-    int64_t t;
-    int32_t n, n_exc, model, n_plastic_rows, dm1, ref_steps, poisson_len, n_parts, hw;
+    int32_t n, n_exc, model, n_plastic_rows, dm1, ref_steps, poisson_len, hw;
     float k_m, v_th, v_reset, v_inf, d_e, d_i, j_ext, d_minus;
     uint32_t fire_thr;
     uint64_t seed;
@@ -75,20 +96,23 @@ struct NeuronArgs {
 struct RowInfo;
 
 // The lists k_neuron builds: spikes of step t (into the delay ring), forced
-// plastic rows, and the snapshots of the rows to update at t. Each workgroup
-// reserves its stretch of every list with one atomic add per list, so a list
-// is ascending within each workgroup's neurons, the stretches in any
-// order; the last workgroup to finish publishes the counts and resets the
-// accumulators for the next step.
+// plastic rows, and the snapshots of the rows to update at t. The lists are
+// ascending: each workgroup's stretch starts at the counts of all earlier
+// workgroups, which it learns by a decoupled look-back over their status
+// words; the last workgroup publishes the counts and advances the step.
 struct CompactArgs {
-    int32_t *spk_list, *spk_cnt;   // spikes of step t (delay-ring slot t mod D)
+    int32_t *ring, *ring_cnt;      // delay ring: D lists of n and D counts; step t: slot t mod D
+    // the number of rows transmitting at t (the count of ring slot
+    // (t-D+1) mod D) at a fixed address, so that the synapse pass needs no
+    // load that waits for the clock to find it
+    int32_t *tx_cnt;
     int32_t *row_list, *row_cnt;   // forced plastic rows
-    unsigned long long *acc;       // packed list reservations (see k_neuron); 0 between steps
+    unsigned long long *status;    // look-back status words, one per workgroup
     // position of each neuron in the spike list of the step it last fired
-    // (only D > 1 with plasticity): written for step t, read for step t-D+1
-    int32_t *spk_pos, *tx_pos;
+    // (only D > 1 with plasticity): [D][n], slot of the step as in the ring
+    int32_t *spk_pos;
     int64_t *gstats;
-    int32_t n, nw, n_plastic_rows, hw;
+    int32_t n, nw, n_plastic_rows, hw, delay;
     // snapshots of the plastic rows to update at step t (see RowInfo): forced
     // rows aligned with row_list; transmitting rows aligned with the
     // delay-ring list of step t-D+1 (txinfo[r].k = that list's entry r)
@@ -101,8 +125,6 @@ struct CompactArgs {
     const float *xpre;
     int32_t *err;
     int64_t *info_stats;     // [gridDim.x][kStFields]
-    int64_t t;
-    int32_t dm1;
     float dpow[kMaxAge + 1];
 };
 
@@ -124,7 +146,7 @@ struct RowInfoArgs {
     const int32_t *row_cnt;
     int32_t n_rows_all;      // flush mode: rows 0 .. n_rows_all-1
     int32_t dm1, hw;
-    int64_t t;               // list mode: step t; flush mode: last completed step
+    const StepClock *clk;    // flush: rows are brought up to the last completed step
     const int64_t *row_ptr;
     const int32_t *pend;
     const uint64_t *hist;
@@ -139,10 +161,14 @@ struct RowInfoArgs {
 struct StdpArgs {
     const RowInfo *info;
     const int32_t *row_cnt;  // list mode row count (nullptr: flush, n_rows_all)
+    // tx_rows: the rows are the transmitted spikes of step t (info = their
+    // snapshots, tx_cnt their count)
+    int32_t tx_rows;
+    const int32_t *tx_cnt;
     int32_t n_rows_all;
     int32_t *t_last;         // committed here: t_last = t, xpre = xp_now
     float *xpre;
-    int64_t t;
+    const StepClock *clk;    // t = clk->t - 1: the step whose neuron update ran last
     const int32_t *col;      // synapse targets (sorted per row)
     float *w;                // synapse weights
     const int32_t *piv;      // [n][S+1] delivery pivots, used at multiples of `mult`
@@ -166,32 +192,32 @@ struct DeliverArgs {
     const int32_t *col;
     float *w;
     const int32_t *piv;      // [n][S+1]
-    const int32_t *list;
-    const int32_t *cnt;
+    // the transmitted spikes of step t = clk->t - 1: delay-ring slot
+    // (t - D + 1) mod D (a delay block: slots of its steps, below)
+    const int32_t *ring, *ring_cnt;
+    const int32_t *tx_cnt;   // the transmitted spikes' count of the step (see CompactArgs)
+    StepClock *clk;
     long long *apart;        // fixed-point partial inputs [C][nacc][n]
     float *ain;              // fp32 input [nacc][n], written directly when C == 1
     int64_t part_stride;
     int32_t n, n_exc, width, n_slices, chunks, nacc, n_work, hw;
     const uint16_t *col16;   // compressed targets: slice-local indices (nullptr: read `col`)
     int64_t *stats;          // [gridDim.x][2]: events delivered, weights written
-    // delay block (no plasticity): batch > 0 delivers the spikes of steps
-    // t_emit0 .. t_emit0 + batch - 1 from the delay ring, work item
-    // (b, slice, chunk) writing fixed-point partial c of step b to abatch
-    // (list and cnt unused; the host passes one chunk, so each item writes
-    // the whole sum); n_work counts all batch items
+    // delay block (no plasticity): batch > 0 delivers, before the block's
+    // neuron launch, the spikes emitted at steps t0 + 1 - D .. t0 + batch - D
+    // (t0 = clk->t, the block's first step), work item (b, slice, chunk)
+    // writing fixed-point partial c of step b to abatch (the host passes one
+    // chunk, so each item writes the whole sum); n_work counts all batch items
     int32_t batch, delay;
-    int64_t t_emit0;
-    const int32_t *ring, *ring_cnt;
     long long *abatch;       // [batch][chunks][nacc][n]
     // plasticity of the transmitting rows, fused into slice delivery
     int32_t plastic;         // 0: no plastic rows
     int32_t event;           // as in StdpArgs
-    const RowInfo *txinfo;   // aligned with `list`
+    const RowInfo *txinfo;   // aligned with the transmitted list
     const uint64_t *hist;
     const float *ypost;
     int32_t *t_last;
     float *xpre;
-    int64_t t;
     float c_pot, c_dep, mu;
     float dpow[kMaxAge + 1];
 };
@@ -239,6 +265,10 @@ struct SmallArgs {
     long long *apart;           // after the last step: part 0 = the pending input
     int64_t *gstats;            // kGSpikes
     int64_t *dlv_stats;         // slot 0: events delivered
+    // the list scans' status words, cleared at the end (the steps run here
+    // leave stale step tags in them)
+    unsigned long long *status;
+    int32_t status_words;
     int32_t n_exc, nacc, steps;
 };
 constexpr int kSmallBlock = 1024;
@@ -256,8 +286,9 @@ constexpr int kSmallChunk = 4096;   // steps per launch
 struct BatchArgs {
     int32_t *ring, *ring_cnt;   // delay ring: D lists of n, D counts
     int32_t delay;
-    unsigned long long *acc;    // [kBatchMax][kAccStride] packed list reservations (word 0 of
-                                // each row), 0 between launches
+    unsigned long long *status; // [kBatchMax][status_stride] look-back status words (step
+                                // k of the block: row k, one word per workgroup)
+    int32_t status_stride;
     const long long *abatch;    // [B][nacc][n] fixed-point inputs of steps t0+1 .. t0+B
     long long *apart;           // partial 0 receives the input of step t0+B
     int64_t *gstats;            // kGSpikes
@@ -265,10 +296,6 @@ struct BatchArgs {
     int32_t steps;
 };
 constexpr int kBatchMax = 16;  // steps per delay block
-// words between the list reservations of successive block steps: each in a
-// 4 KiB page of its own, so the steps' atomics do not queue on one address
-// range
-constexpr int kAccStride = 512;
 // steps per delay block for neuron model m (CUBA: two inputs per step)
 constexpr int batch_steps_max(int m) { return m == 1 ? kBatchMax / 2 : kBatchMax; }
 constexpr int64_t kBatchBytes = 256ll << 20;  // most workspace for a block's partial inputs
@@ -296,13 +323,11 @@ hipError_t launch_small_steps(hipStream_t s, const NeuronArgs &a, const SmallArg
                               KernelEvents ev = {});
 hipError_t launch_neuron(hipStream_t s, const NeuronArgs &a, const CompactArgs &b,
                          KernelEvents ev = {});
+// workgroups of k_neuron and k_neuron_steps for n neurons (one status word each)
+int neuron_grid(int32_t n);
+int neuron_steps_grid(int32_t n);
 // k_neuron_steps: steps a.t .. a.t + b.steps - 1 (a describes step a.t)
 hipError_t launch_neuron_steps(hipStream_t s, const NeuronArgs &a, const BatchArgs &b);
-// sorts list[0 .. min(*cnt, n)) (distinct values in [0, n)) in place and,
-// when pos is given, sets pos[list[r]] = r; bitmap: ceil(n/64) words of
-// device scratch
-hipError_t launch_sort_list(hipStream_t s, int32_t *list, const int32_t *cnt, uint64_t *bitmap,
-                            int32_t *pos, int32_t n);
 // pos[q n + ring[q n + r]] = r for every delay-ring slot q < d and r < its count
 hipError_t launch_ring_positions(hipStream_t s, const int32_t *ring, const int32_t *cnt,
                                  int32_t *pos, int32_t n, int32_t d);
@@ -384,8 +409,13 @@ hipError_t launch_synapse_pass(hipStream_t s, const DeliverArgs &d, const StdpAr
 hipError_t launch_deliver_global(hipStream_t s, const DeliverArgs &a, int blocks, KernelEvents ev = {});
 int deliver_lds_static_bytes();  // static LDS of the slice kernel (-1 on error)
 int synapse_pass_static_bytes();  // static LDS of the fused synapse pass (-1 on error)
+// the fp32 input from the partial sums when clk->input_forced is 0 (then
+// set to 1 by a second kernel, so that every workgroup reads the flag first)
 hipError_t launch_materialize_input(hipStream_t s, const long long *apart, int64_t part_stride,
-                                    int32_t n_parts, float *ain, int64_t count);
+                                    StepClock *clk, float *ain, int64_t count);
+// clk->t = t unless t < 0, the input flags unless input_forced < 0
+hipError_t launch_set_clock(hipStream_t s, StepClock *clk, int64_t t, int32_t input_forced,
+                            int32_t n_parts);
 hipError_t launch_scan_i64(hipStream_t s, int64_t *data, int64_t count, int64_t *bsum);
 hipError_t launch_graph_count_bernoulli(hipStream_t s, const GraphArgs &a);
 hipError_t launch_graph_fill_bernoulli(hipStream_t s, const GraphArgs &a);

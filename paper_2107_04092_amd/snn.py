@@ -92,6 +92,9 @@ _SIGNATURES = {
     "snn_get_graph": (_i32, [_P, ctypes.POINTER(snn_graph_view)]),
     "snn_get_stats": (_i32, [_P, ctypes.POINTER(snn_stats)]),
     "snn_reset_stats": (_i32, [_P]),
+    "snn_graph_capture": (_i32, [_P, _i32, _i32, ctypes.POINTER(_P)]),
+    "snn_graph_launch": (_i32, [_P, _P]),
+    "snn_graph_destroy": (None, [_P]),
 }
 
 _lib = None
@@ -101,6 +104,9 @@ def load():
     """Loads libsnn.so from the package directory; raises if it is missing."""
     global _lib
     if _lib is None:
+        # torch's HIP runtime first: the library then binds to the same
+        # runtime (same soname) instead of loading a second one
+        import torch  # noqa: F401
         if not os.path.exists(LIB_PATH):
             raise ImportError(
                 "libsnn.so is not built (run python -m paper_2107_04092_amd.build); "
@@ -237,6 +243,20 @@ def snn_reset_stats(ctx):
     _check(ctx, load().snn_reset_stats(ctx))
 
 
+def snn_graph_capture(ctx, n_steps, mode):
+    g = _P()
+    _check(ctx, load().snn_graph_capture(ctx, n_steps, mode, ctypes.byref(g)))
+    return g
+
+
+def snn_graph_launch(ctx, graph):
+    _check(ctx, load().snn_graph_launch(ctx, graph))
+
+
+def snn_graph_destroy(graph):
+    load().snn_graph_destroy(graph)
+
+
 def snn_record_kernel_times(ctx, max_steps):
     _check(ctx, load().snn_record_kernel_times(ctx, int(max_steps)))
 
@@ -365,6 +385,13 @@ class Network:
 
     def flush_plasticity(self):
         snn_flush_plasticity(self.ctx)
+
+    def capture(self, n_steps=1, mode=SNN_DELIVER_LDS_SLICE):
+        """A captured sequence of n_steps steps (replay with replay())."""
+        return snn_graph_capture(self.ctx, n_steps, mode)
+
+    def replay(self, graph):
+        snn_graph_launch(self.ctx, graph)
 
     def probe_rows(self, n_rows, write=False, seed=1):
         return snn_probe_rows(self.ctx, n_rows, 1 if write else 0, seed)

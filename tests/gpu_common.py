@@ -24,12 +24,12 @@ def torch_mod():
     return torch
 
 
-def gpu_net(p, slice_width=None, spike_chunks=None, build=True, **cfg_kw):
+def gpu_net(p, slice_width=None, spike_chunks=None, build=True, stream=None, **cfg_kw):
     torch = torch_mod()
     tab = wl.poisson_cdf_table(p.poisson_mu)
     cfg = snn.config_from_preset(p, tab, slice_width=slice_width, spike_chunks=spike_chunks,
                                  **cfg_kw)
-    net = snn.Network(cfg)
+    net = snn.Network(cfg, stream=stream)
     if build:
         net.build_random(p.graph_kind, p.p_or_fanout, p.w_exc, p.w_inh)
         st = wl.initial_state(p)
