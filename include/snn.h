@@ -344,6 +344,21 @@ snn_status snn_advance(snn_ctx *ctx);
  * rows and the transmitting rows of a step are disjoint. */
 snn_status snn_step(snn_ctx *ctx, int32_t n_steps, int32_t mode);
 
+/* snn_step for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same steps, states and statistics as snn_step(ctx, n_steps, mode), with the
+ * scratch of the steps' list scans (one 64-bit status word per workgroup
+ * and step of a launch) in an array the library holds on each device it runs
+ * on (1 MiB, kept until the process ends) instead of the bound workspace.
+ * The caller still binds the workspace and graph buffers that hold the
+ * state. Allocates nothing (no hipMalloc, hipFree or allocating library
+ * call); enqueues a clear of the words it uses, then the steps. Every call on
+ * one device shares the array: calls that overlap on a device (contexts on
+ * different streams) race and must be ordered by the caller. SNN_EINVAL for
+ * networks above 4,194,304 neurons (more status words than the array holds)
+ * or n_steps < 0; otherwise the errors of snn_step. */
+snn_status snn_step_static(snn_ctx *ctx, int32_t n_steps, int32_t mode);
+
 /* Kernel timing for profiling. After this call the next max_steps steps run
  * by snn_step record, per step, the device time of its kernels in three
  * parts: [0] neuron update with its spike / row lists, [1] plasticity,

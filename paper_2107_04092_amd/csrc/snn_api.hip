@@ -9,11 +9,45 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
 
 using namespace snn;
+
+// Scratch of snn_step_static: the list scans' status words, in device memory
+// the library holds on every device it runs on, so that the call allocates
+// nothing. In host code `scratch` is only a stand-in for the symbol; the
+// kernels get the device address obtained once per device at snn_create.
+constexpr int64_t kScratchWords = 131072;  // 1 MiB of 64-bit status words
+static __device__ __align__(256) unsigned long long scratch[kScratchWords];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+unsigned long long *g_scratch[kMaxDevices] = {};  // device address of `scratch`, per device
+
+// The device address of `scratch` on the current device `dev` (looked up on
+// the first call for that device).
+hipError_t static_scratch(int dev, unsigned long long **out)
+{
+    *out = nullptr;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void *ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            return e;
+        }
+        g_scratch[dev] = (unsigned long long *)ptr;
+    }
+    *out = g_scratch[dev];
+    return hipSuccess;
+}
+}  // namespace
 
 struct snn_ctx {
     snn_config cfg;
@@ -66,6 +100,7 @@ struct snn_ctx {
     int32_t *ring = nullptr, *ring_cnt = nullptr;
     int32_t *rows = nullptr, *row_cnt = nullptr, *err_flag = nullptr, *maxlen = nullptr;
     int32_t *tx_cnt = nullptr;  // transmitted spikes of the step in progress (count)
+    unsigned long long *static_status = nullptr;  // `scratch` on this context's device
     int64_t *row_ptr = nullptr, *scratch = nullptr, *bsum = nullptr;
     int64_t *gstats = nullptr, *info_stats = nullptr, *syn_stats = nullptr, *dlv_stats = nullptr;
     RowInfo *info = nullptr, *txinfo = nullptr;
@@ -775,6 +810,11 @@ snn_status snn_create(const snn_config *cfg, void *hip_stream, snn_ctx **out)
     if (st) return st;
     if (hipGetDevice(&c->device) != hipSuccess)
         return fail(c, SNN_EDEVICE, "no HIP device");
+    {
+        const hipError_t e = static_scratch(c->device, &c->static_status);
+        if (e != hipSuccess)
+            return fail(c, SNN_EDEVICE, "the library's device scratch: %s", hipGetErrorString(e));
+    }
     int lds_max = 0;
     if (hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, c->device) !=
         hipSuccess)
@@ -1180,6 +1220,31 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
         c->t += 1;
     }
     return SNN_OK;
+}
+
+snn_status snn_step_static(snn_ctx *c, int32_t n_steps, int32_t mode)
+{
+    if (!c) return SNN_EINVAL;
+    if (c->status_words > kScratchWords)
+        return fail(c, SNN_EINVAL,
+                    "the list scans need %d status words; the library's scratch holds %lld "
+                    "(networks up to %lld neurons)", c->status_words, (long long)kScratchWords,
+                    (long long)(kScratchWords / kBatchMax) * 512);
+    snn_status st = require_graph(c);
+    if (st) return st;
+    if (!c->static_status) return fail(c, SNN_EDEVICE, "no device scratch on this device");
+    if (n_steps < 0) return fail(c, SNN_EINVAL, "n_steps must be >= 0");
+    if (n_steps == 0) return SNN_OK;
+    // the array keeps the last call's words (any context on this device):
+    // cleared first, with a kernel (no memset node in a captured call)
+    st = check_hip(c, launch_fill_i64(c->stream, (int64_t *)c->static_status, c->status_words, 0),
+                   "clear the scratch");
+    if (st) return st;
+    unsigned long long *own = c->status;
+    c->status = c->static_status;
+    st = snn_step(c, n_steps, mode);
+    c->status = own;
+    return st;
 }
 
 snn_status snn_record_kernel_times(snn_ctx *c, int32_t max_steps)

@@ -84,6 +84,7 @@ _SIGNATURES = {
     "snn_deliver_spikes": (_i32, [_P, _i32]),
     "snn_advance": (_i32, [_P]),
     "snn_step": (_i32, [_P, _i32, _i32]),
+    "snn_step_static": (_i32, [_P, _i32, _i32]),
     "snn_flush_plasticity": (_i32, [_P]),
     "snn_probe_rows": (_i32, [_P, _i32, _i32, ctypes.c_uint64, ctypes.POINTER(ctypes.c_double),
                               ctypes.POINTER(_i64)]),
@@ -202,6 +203,10 @@ def snn_advance(ctx):
 
 def snn_step(ctx, n_steps, mode):
     _check(ctx, load().snn_step(ctx, n_steps, mode))
+
+
+def snn_step_static(ctx, n_steps, mode):
+    _check(ctx, load().snn_step_static(ctx, n_steps, mode))
 
 
 def snn_flush_plasticity(ctx):
@@ -370,6 +375,9 @@ class Network:
     # stepping ------------------------------------------------------------
     def step(self, n=1, mode=SNN_DELIVER_LDS_SLICE):
         snn_step(self.ctx, n, mode)
+
+    def step_static(self, n=1, mode=SNN_DELIVER_LDS_SLICE):
+        snn_step_static(self.ctx, n, mode)
 
     def update_neurons(self):
         snn_update_neurons(self.ctx)
