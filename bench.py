@@ -65,6 +65,8 @@ def parse():
     ap.add_argument("--plasticity", choices=["lazy-event", "lazy", "naive"],
                     default="lazy-event",
                     help="plasticity algorithm (Fig. 2(c), (b), (a))")
+    ap.add_argument("--stdp-xcd", choices=["off", "auto", "2", "4", "8"], default="off",
+                    help="forced rows partitioned over the XCDs by target range")
     ap.add_argument("--stdp-mult", type=int, default=0)
     ap.add_argument("--stdp-chunks", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -277,7 +279,8 @@ def main():
                                  plasticity_algorithm=["lazy-event", "lazy", "naive"].index(
                                      args.plasticity),
                                  compressed_targets=(None if args.targets == "preset" else
-                                                     int(args.targets == "16")))
+                                                     int(args.targets == "16")),
+                                 stdp_xcd={"off": 0, "auto": 1}.get(args.stdp_xcd) or int(args.stdp_xcd))
     t0 = time.time()
     net = snn.Network(cfg, stream=stream, device=dev)
     e = net.build_random(p.graph_kind, p.p_or_fanout, p.w_exc, p.w_inh)
@@ -452,7 +455,8 @@ def main():
             "stdp_filter": args.stdp_filter, "history_bits": hbits,
             "target_bits": 16 if cfg.compressed_targets else 32,
             "plasticity": args.plasticity,
-            "stdp_slice_mult": args.stdp_mult, "stdp_chunks": args.stdp_chunks, "seed": p.seed,
+            "stdp_slice_mult": args.stdp_mult, "stdp_chunks": args.stdp_chunks,
+            "stdp_xcd": args.stdp_xcd, "seed": p.seed,
         },
         "roofline": roofline,
         "cpu_baseline": cpu,

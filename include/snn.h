@@ -151,6 +151,22 @@ typedef struct snn_config {
                              slice delivery reads instead of the 32-bit target
                              (half the target bytes). Row-wise kernels read
                              the 32-bit targets. 0 = off */
+    int32_t stdp_xcd;     /* forced rows partitioned by target range over
+                             the XCDs (row-wise layout, history codes or no
+                             summary: stdp_filter 0 or 1): 0 = off; 2, 4 or 8
+                             = that many ranges; 1 = automatic (the most
+                             ranges whose segments still fill about three
+                             quarters of a 256-entry part, given the edge
+                             count when the graph is bound, and whose codes
+                             fit in LDS). The plastic targets are cut into
+                             ranges of whole slices; range x belongs to the
+                             workgroups on XCDs b mod 8 in [8x/p, 8(x+1)/p),
+                             which update the entries of every forced row
+                             whose targets lie in range x, so the histories
+                             they gather stay in those XCDs' L2. Off where
+                             the plastic targets have fewer slices than
+                             ranges or no range's codes fit. Same weights
+                             either way */
     int32_t neuron_model; /* enum snn_neuron_model */
     int32_t plastic;      /* enum snn_plasticity */
     int32_t poisson_len;  /* entries used in poisson_cdf (0 = no external drive) */
@@ -218,6 +234,9 @@ typedef struct snn_graph_view {
     uint16_t *col16;       /* compressed_targets: n_edges slice-local indices
                               (col mod W), 1:1 with col; else NULL. Derived
                               from col by the graph build */
+    int32_t stdp_ranges;   /* target ranges the forced rows are split into
+                              (stdp_xcd; 0 = whole rows), fixed when the
+                              graph is bound */
 } snn_graph_view;
 
 typedef struct snn_stats {

@@ -120,30 +120,37 @@ __device__ __forceinline__ void nstate_store(const NeuronArgs &a, int i, const N
 // to kSpecParts partial sums (a.max_parts of them) are loaded before it is
 // looked at: one round trip instead of two.
 constexpr int kSpecParts = 8;
-__device__ __forceinline__ void neuron_input(const NeuronArgs &a, int forced, int n_parts, int i,
-                                             float &ae, float &ai)
+struct InputLoads {
+    float fe, fi;
+    long long pe[kSpecParts], pi[kSpecParts];
+};
+__device__ __forceinline__ void input_issue(const NeuronArgs &a, int i, InputLoads &L)
 {
     const bool cuba = a.model == 1;
-    const float fe = a.ain[i];
-    const float fi = cuba ? a.ain[a.n + i] : 0.f;
-    long long pe[kSpecParts], pi[kSpecParts];
+    L.fe = a.ain[i];
+    L.fi = cuba ? a.ain[a.n + i] : 0.f;
 #pragma unroll
     for (int c = 0; c < kSpecParts; ++c) {
-        pe[c] = c < a.max_parts ? a.apart[c * a.part_stride + i] : 0;
-        pi[c] = cuba && c < a.max_parts ? a.apart[c * a.part_stride + a.n + i] : 0;
+        L.pe[c] = c < a.max_parts ? a.apart[c * a.part_stride + i] : 0;
+        L.pi[c] = cuba && c < a.max_parts ? a.apart[c * a.part_stride + a.n + i] : 0;
     }
+}
+__device__ __forceinline__ void input_combine(const NeuronArgs &a, const InputLoads &L, int forced,
+                                              int n_parts, int i, float &ae, float &ai)
+{
+    const bool cuba = a.model == 1;
     ai = 0.f;
     if (forced) {
-        ae = fe;
-        ai = fi;
+        ae = L.fe;
+        ai = L.fi;
         return;
     }
     long long se = 0, si = 0;
 #pragma unroll
     for (int c = 0; c < kSpecParts; ++c) {
         if (c < n_parts) {
-            se += pe[c];
-            si += pi[c];
+            se += L.pe[c];
+            si += L.pi[c];
         }
     }
     for (int c = kSpecParts; c < n_parts; ++c) {  // beyond the speculative loads
@@ -152,6 +159,13 @@ __device__ __forceinline__ void neuron_input(const NeuronArgs &a, int forced, in
     }
     ae = from_fix(se);
     if (cuba) ai = from_fix(si);
+}
+__device__ __forceinline__ void neuron_input(const NeuronArgs &a, int forced, int n_parts, int i,
+                                             float &ae, float &ai)
+{
+    InputLoads L;
+    input_issue(a, i, L);
+    input_combine(a, L, forced, n_parts, i, ae, ai);
 }
 
 // The external Poisson count of neuron i at step t: the number of CDF
@@ -242,24 +256,41 @@ __device__ __forceinline__ uint8_t hist_code(uint64_t h0, uint64_t h1)
     return np == 0 ? (uint8_t)0 : np == 1 ? (uint8_t)pos : kCodeMulti;
 }
 
-// The whole update of neuron i at step t from and to the state arrays, with
-// the input source of the clock; returns spiked / transmitting / forced and,
-// for a plastic row, its t_last.
-__device__ __forceinline__ void neuron_update(const NeuronArgs &a, const StepClock &ck, int i,
-                                              int64_t t, int &s, int &tx, int &forced,
-                                              bool &fired_recently, int &t_last_i)
-{
+// The whole update of neuron i from and to the state arrays, in three parts:
+// the loads, issued before the clock is read (so the state and the clock
+// arrive in one round trip); the update at step t with the input source of
+// the clock, which returns spiked / transmitting / forced and, for a plastic
+// row, its t_last; and the stores (neuron_commit), which the caller issues
+// after its last wait for a load: with stores outstanding, a wait for any
+// load also waits for every earlier store.
+struct NeuronLoads {
     NState st;
-    nstate_load<-1, 0>(a, i, st);
-    t_last_i = i < a.n_plastic_rows ? a.t_last[i] : 0;
+    int t_last;
+    InputLoads in;
+};
+__device__ __forceinline__ void neuron_issue(const NeuronArgs &a, int i, NeuronLoads &L)
+{
+    nstate_load<-1, 0>(a, i, L.st);
+    L.t_last = i < a.n_plastic_rows ? a.t_last[i] : 0;
+    if (a.model != 2) input_issue(a, i, L.in);
+}
+__device__ __forceinline__ void neuron_update(const NeuronArgs &a, const StepClock &ck, int i,
+                                              int64_t t, NeuronLoads &L, int &s, int &tx,
+                                              int &forced, bool &fired_recently, int &t_last_i)
+{
+    NState &st = L.st;
+    t_last_i = L.t_last;
     float ae = 0.f, ai = 0.f;
-    if (a.model != 2) neuron_input(a, ck.input_forced, ck.n_parts, i, ae, ai);
+    if (a.model != 2) input_combine(a, L.in, ck.input_forced, ck.n_parts, i, ae, ai);
     s = neuron_advance<-1, 0>(a, i, t, ae, ai, st);
-    nstate_store<-1, 0>(a, i, st);
-    a.code[i] = hist_code(st.h0, st.h1);
     fired_recently = (st.h0 | st.h1) != 0ull;
     tx = (int)((st.h0 >> a.dm1) & 1ull);
     if (i < a.n_plastic_rows) forced = !tx && (t - (int64_t)t_last_i >= 64 * a.hw);
+}
+__device__ __forceinline__ void neuron_commit(const NeuronArgs &a, int i, const NState &st)
+{
+    nstate_store<-1, 0>(a, i, st);
+    a.code[i] = hist_code(st.h0, st.h1);
 }
 
 // NB threads per workgroup: 1024 on large networks (fewer workgroups to look
@@ -275,30 +306,27 @@ __global__ __launch_bounds__(NB) void k_neuron(NeuronArgs a, CompactArgs lst)
     const int tid = threadIdx.x;
     const int wave = tid / kWave, lane = tid % kWave;
     const bool plastic = lst.n_plastic_rows > 0;
-    const StepClock ck = *a.clk;
-    const int64_t t = ck.t;
     const int D = lst.delay;
     const int i = blockIdx.x * NB + tid;
     if (tid < 4) s_st[tid] = 0ull;
-    // the count of the transmitted list (D > 1: written D-1 steps ago), at
-    // the fixed address the synapse pass reads
-    if (blockIdx.x == 0 && tid == 0 && a.dm1 > 0) *lst.tx_cnt = lst.ring_cnt[ring_slot(t - a.dm1, D)];
+    // the state loads, then the clock (vector loads, which the state loads
+    // do not wait for): one round trip
+    NeuronLoads L;
+    if (i < a.n) neuron_issue(a, i, L);
+    const StepClock ck = load_clock(a.clk);
+    const int64_t t = ck.t;
     int s = 0, tx = 0, forced = 0, tl = 0;
     bool fired_recently = false;
-    if (i < a.n) neuron_update(a, ck, i, t, s, tx, forced, fired_recently, tl);
+    if (i < a.n) neuron_update(a, ck, i, t, L, s, tx, forced, fired_recently, tl);
+    // the count of the transmitted list (D > 1: written D-1 steps ago), for
+    // the fixed address the synapse pass reads: loaded now, stored at the end
+    const bool tx_writer = blockIdx.x == 0 && tid == 0 && a.dm1 > 0;
+    const int tx_count = tx_writer ? lst.ring_cnt[ring_slot(t - a.dm1, D)] : 0;
     const uint64_t m = ballot64(s), fm = ballot64(forced);
-    {
-        const uint64_t txm = ballot64(tx), rcm = ballot64(fired_recently);
-        if (lane == 0) {
-            const int64_t word = (int64_t)blockIdx.x * NWV + wave;
-            if (word * kWave < a.n) {
-                a.mask[word] = m;
-                a.txmask[word] = txm;
-                a.recent[word] = rcm;
-            }
-            s_cnt[0][wave] = __popcll(m);
-            s_cnt[1][wave] = __popcll(fm);
-        }
+    const uint64_t txm = ballot64(tx), rcm = ballot64(fired_recently);
+    if (lane == 0) {
+        s_cnt[0][wave] = __popcll(m);
+        s_cnt[1][wave] = __popcll(fm);
     }
     // The values a row snapshot needs, loaded for the rows to bring up to
     // date at t only (transmitting plastic rows, forced rows), and a
@@ -307,14 +335,26 @@ __global__ __launch_bounds__(NB) void k_neuron(NeuronArgs a, CompactArgs lst)
     const bool snap_tx = tx && plastic;
     int64_t rs = 0;
     int pend_i = 0, txpos = -1;
-    float xp = 0.f;
+    float xp = 0.f, dp = 0.f;
     if (snap_tx || forced) {
         rs = lst.row_ptr[i];
         if (i < lst.n_plastic_rows) {
             pend_i = lst.pend[i];
             xp = lst.xpre[i];
+            dp = lst.dpow[row_age_index(t, tl, lst.hw)];
         }
         if (snap_tx && a.dm1 > 0) txpos = lst.spk_pos[(int64_t)ring_slot(t - a.dm1, D) * a.n + i];
+    }
+    // a forced row's pivots at the range boundaries (forced rows split by
+    // target range): loaded with the snapshot values, read under the same
+    // condition (left unset otherwise, so no merge waits for the loads)
+    int pv[kXcds - 1];
+    if (forced && lst.segb) {
+        // (all seven: the boundaries past the last range repeat its end, so
+        // each index is a pivot of the row; no load waits inside a branch)
+        const int32_t *pr = lst.piv + (int64_t)i * lst.piv_stride;
+#pragma unroll
+        for (int x = 0; x < kXcds - 1; ++x) pv[x] = pr[lst.xcd_piv[x + 1]];
     }
     __syncthreads();  // s_cnt, s_st
     int agg_s = 0, agg_f = 0;
@@ -328,9 +368,14 @@ __global__ __launch_bounds__(NB) void k_neuron(NeuronArgs a, CompactArgs lst)
                        status_word(agg_s, agg_f, t, blockIdx.x == 0 ? kStatusInc : kStatusAgg));
     lookback<NB, 1>(lst.status, 0, 1, (int)blockIdx.x, t, s_lb, lst.err);
     const int pre_s = s_lb[6], pre_f = s_lb[7];  // spikes and forced rows of earlier workgroups
+    // the values loaded before the scan (arrived during it) are taken here,
+    // before thread 0's status store: a later wait for them would also wait
+    // for that store
+    asm volatile("" ::"v"(rs), "v"(pend_i), "v"(xp), "v"(dp), "v"(txpos), "v"(tx_count));
     if (tid == 0 && blockIdx.x > 0)
         publish_status(lst.status + blockIdx.x,
                        status_word(pre_s + agg_s, pre_f + agg_f, t, kStatusInc));
+    if (tx_writer) *lst.tx_cnt = tx_count;
     // snapshots of the rows to bring up to date (taken before any kernel
     // commits t_last / x_pre)
     RowInfo ri = RowInfo{};
@@ -338,23 +383,19 @@ __global__ __launch_bounds__(NB) void k_neuron(NeuronArgs a, CompactArgs lst)
     if (snap_tx) {
         // the row transmits at t exactly when tx (history bit D-1 of step t)
         if (i < lst.n_plastic_rows)
-            ri_ok = make_row_info_v(ri, i, t, tl, rs, pend_i, xp, 1, lst.hw, lst.dpow, lst.err);
+            ri_ok = make_row_info_d(ri, i, t, tl, rs, pend_i, xp, 1, lst.hw, dp, lst.err);
         if (!ri_ok) {  // nothing to bring up to date: the row is only delivered
             ri = RowInfo{};
             ri.k = i;
             ri.rs = rs;
         }
     } else if (forced) {
-        ri_ok = make_row_info_v(ri, i, t, tl, rs, pend_i, xp, 0, lst.hw, lst.dpow, lst.err);
+        ri_ok = make_row_info_d(ri, i, t, tl, rs, pend_i, xp, 0, lst.hw, dp, lst.err);
     }
     if (lst.info_stats) {
         const bool f = forced && ri_ok;
-        long long v0 = ri_ok ? 1 : 0, v1 = f ? 1 : 0;
-        long long v2 = ri_ok ? ri.len : 0, v3 = f ? ri.len : 0;
-        v0 = wave_sum_i64(v0);
-        v1 = wave_sum_i64(v1);
-        v2 = wave_sum_i64(v2);
-        v3 = wave_sum_i64(v3);
+        const long long v0 = __popcll(ballot64(ri_ok)), v1 = __popcll(ballot64(f));
+        const long long v2 = wave_sum_i64(ri_ok ? ri.len : 0), v3 = wave_sum_i64(f ? ri.len : 0);
         if (lane == 0) {
             if (v0) atomicAdd(s_st + 0, (unsigned long long)v0);
             if (v1) atomicAdd(s_st + 1, (unsigned long long)v1);
@@ -393,8 +434,37 @@ __global__ __launch_bounds__(NB) void k_neuron(NeuronArgs a, CompactArgs lst)
         if (q < lst.n_plastic_rows) {
             lst.row_list[q] = i;
             lst.info[q] = ri;
+            if (lst.segb) {
+                // segment ends, moved to the nearest 128-byte line of the
+                // weight array (monotone: the pivots are)
+                int e[kXcds];
+#pragma unroll
+                for (int x = 0; x < kXcds - 1; ++x) {
+                    // (an empty asm pins the pivot here: no conversion of it
+                    // is hoisted to its load, where it would wait for it)
+                    asm volatile("" : "+v"(pv[x]));
+                    const int64_t al = ((rs + pv[x] + kStoreLine / 2) & ~(int64_t)(kStoreLine - 1));
+                    e[x] = x < lst.xparts - 1 ? (int)min(max(al - rs, (int64_t)0), (int64_t)pend_i)
+                                              : pend_i;
+                }
+                e[kXcds - 1] = pend_i;
+                int4 *dst = reinterpret_cast<int4 *>(lst.segb + (int64_t)q * kXcds);
+                dst[0] = make_int4(e[0], e[1], e[2], e[3]);
+                dst[1] = make_int4(e[4], e[5], e[6], e[7]);
+            }
         } else {
             atomicOr(lst.err, kErrRing);
+        }
+    }
+    // the neuron's state and the masks: stored after the last wait for a
+    // load (the snapshot values above)
+    if (i < a.n) neuron_commit(a, i, L.st);
+    if (lane == 0) {
+        const int64_t word = (int64_t)blockIdx.x * NWV + wave;
+        if (word * kWave < a.n) {
+            a.mask[word] = m;
+            a.txmask[word] = txm;
+            a.recent[word] = rcm;
         }
     }
     if (lst.info_stats) {

@@ -464,14 +464,255 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
         atomicAdd((unsigned long long *)(a.stats + bid), (unsigned long long)written);
 }
 
+// Target-range form of the forced-row update (StdpArgs::xcd): workgroup b
+// runs on XCD b mod 8 and belongs to range x = (b mod 8) / (8 / xparts);
+// its waves take, for every forced row, only the entries whose targets lie
+// in range x of the plastic targets (the row's segment x, bounds from the
+// neuron update). The targets' histories a wave gathers then stay in the
+// L2 of its XCDs, and the history codes staged in LDS cover range x only.
+// The host picks xparts so that a segment is about one part (U x 64
+// entries); segment bounds sit on 128-byte lines of the weight array, so
+// no line is stored by two ranges. Otherwise as stdp_rows_body: a
+// candidate queue per wave, two parts in flight, whole lines stored.
+template <int U>
+struct RowPartX {
+    RowInfo ri;
+    int i;       // row-list index (>= nrows: no part)
+    int base;    // element index of lane 0 (line-aligned)
+    int s0, s1;  // the segment's entries
+    int j[U];    // targets (-1: none)
+    float w[U];
+};
+
+template <int NT, int U, int HW>
+__device__ __forceinline__ void stdp_rows_xcd_body(const StdpArgs &a, int bid, int nblocks,
+                                                   unsigned char *s_sum)
+{
+    __shared__ float s_dpow[kMaxAge + 1];
+    constexpr int NWV = NT / kWave;
+    const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+    const int G = kXcds / a.xparts;            // XCDs per range
+    const int x = (bid % kXcds) / G;           // this workgroup's range
+    const int rho0 = x * G;                    // its range's first XCD
+    int grp_wgs = 0;                           // workgroups of the range
+    for (int q = 0; q < G; ++q) grp_wgs += (nblocks - (rho0 + q) + kXcds - 1) / kXcds;
+    const int gw = ((bid / kXcds) * G + (bid % kXcds - rho0)) * NWV + wave;  // wave among the range's
+    const int nwv = grp_wgs * NWV;
+    const int32_t *__restrict__ col = a.col;
+    float *__restrict__ wgt = a.w;
+    const uint64_t *__restrict__ hist = a.hist;
+    const float c_pot = a.c_pot, c_dep = a.c_dep, mu = a.mu;
+    const int line0 = lane & ~(kStoreLine - 1);
+    const int64_t t = a.clk->t - 1;
+    const int nrows = *a.row_cnt;
+    const int lo = a.xlo[x], span = a.xlo[x + 1] - lo;  // this XCD's targets
+    long long written = 0;
+
+    // cursor: the next part to issue; la: the row after the cursor's
+    RowInfo cur = RowInfo{}, la = RowInfo{};
+    int cur_i = gw, la_i = gw + nwv;
+    int cur_s0 = 0, cur_s1 = 0, la_s0 = 0, la_s1 = 0;
+    auto load_row = [&](int r, RowInfo &ri, int &s0, int &s1) {
+        if (r < nrows) {
+            ri = a.info[r];
+            const int32_t *e = a.segb + (int64_t)r * kXcds;
+            s0 = x ? e[x - 1] : 0;
+            s1 = e[x];
+        }
+    };
+    load_row(cur_i, cur, cur_s0, cur_s1);
+    load_row(la_i, la, la_s0, la_s1);
+    auto first_base = [](const RowInfo &ri, int s0) {
+        return s0 - (int)((ri.rs + s0) & (kStoreLine - 1));
+    };
+    int cur_base = first_base(cur, cur_s0);
+    auto issue = [&](RowPartX<U> &p) {
+        p.ri = cur;
+        p.i = cur_i;
+        p.base = cur_base;
+        p.s0 = cur_s0;
+        p.s1 = cur_s1;
+        const bool any = cur_i < nrows && cur_s1 > cur_s0;  // wave-uniform
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            p.j[u] = -1;
+            p.w[u] = 0.f;
+        }
+        if (any) {
+            // clamped loads, selected afterwards (a load used under a lane
+            // condition would be waited for inside it); non-temporal: the
+            // row is read once, the gathered histories stay in L2
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int q = p.base + u * kWave + lane;
+                const int qc = min(max(q, cur_s0), cur_s1 - 1);
+                p.j[u] = __builtin_nontemporal_load(col + cur.rs + qc);
+                p.w[u] = __builtin_nontemporal_load(wgt + cur.rs + qc);
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int q = p.base + u * kWave + lane;
+                if (q < cur_s0 || q >= cur_s1) p.j[u] = -1;
+            }
+        }
+        if (any && cur_base + U * kWave < cur_s1) {  // the segment's next part
+            cur_base += U * kWave;
+        } else {  // the next row
+            cur = la;
+            cur_i = la_i;
+            cur_s0 = la_s0;
+            cur_s1 = la_s1;
+            cur_base = first_base(cur, cur_s0);
+            la_i += nwv;
+            la = RowInfo{};
+            la_s0 = la_s1 = 0;
+            load_row(la_i, la, la_s0, la_s1);
+        }
+    };
+    RowPartX<U> A, B;
+    issue(A);
+    issue(B);
+    for (int q = tid; q <= kMaxAge; q += NT) s_dpow[q] = a.dpow[q];
+    const uint8_t *s_code = s_sum;
+    const int tbytes = a.code ? ((span + 15) / 16) * 16 : 0;
+    if (a.code && span > 0)
+        stage_lds<NT, 4>((uint4 *)s_sum, (const uint4 *)(a.code + lo), (span + 15) / 16);
+    __syncthreads();
+
+    int32_t *q_j = (int32_t *)(s_sum + tbytes) + wave * (2 * U * kWave);
+    float *q_w = (float *)(q_j + U * kWave);
+    // the history code of target j: staged for range x; outside it (a
+    // target next to a range boundary) the history is gathered
+    auto code_of = [&](int j) -> int {
+        const int jj = j - lo;
+        const bool in = (unsigned)jj < (unsigned)span;
+        const int c = s_code[in ? jj : 0];
+        return in ? c : (int)kCodeMulti;
+    };
+    auto step = [&](RowPartX<U> &p) {
+        const RowInfo ri = p.ri;
+        const int age = ri.age_pre & 0xff, pre = ri.age_pre >> 8;
+        uint64_t m0, m1;
+        window_masks(age, m0, m1);
+        if (HW == 1) m1 = 0ull;
+        bool cand[U];
+        if (!pre && a.code) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) cand[u] = p.j[u] >= 0 && code_of(max(p.j[u], 0)) != 0;
+        } else {
+#pragma unroll
+            for (int u = 0; u < U; ++u) cand[u] = p.j[u] >= 0;
+        }
+        uint64_t bl[U];
+        int qb[U];
+        int qn = 0;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            bl[u] = ballot64(cand[u]);
+            qb[u] = qn;
+            qn += (int)__popcll(bl[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (cand[u]) {
+                const int e = qb[u] + lane_rank(bl[u]);
+                q_j[e] = p.j[u];
+                q_w[e] = p.w[u];
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            constexpr int H = U / 2;
+            if (half * H * kWave >= qn) break;  // wave-uniform
+            uint64_t h[H], g[H];
+            float qw[H];
+            int cd[H];
+#pragma unroll
+            for (int q = 0; q < H; ++q) {
+                const int e0 = (half * H + q) * kWave;
+                h[q] = g[q] = 0ull;
+                qw[q] = 0.f;
+                cd[q] = 0;
+                if (e0 < qn) {  // wave-uniform
+                    const int e = e0 + lane;
+                    const int j = e < qn ? q_j[e] : 0;
+                    qw[q] = q_w[e];
+                    cd[q] = (!pre && a.code) ? code_of(j) : (int)kCodeMulti;
+                    gather_hist<HW>(hist, cd[q] == kCodeMulti ? j : 0, h[q], g[q]);
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < H; ++q) {
+                const int e = (half * H + q) * kWave + lane;
+                if (e < qn) {
+                    uint64_t h0 = h[q], h1 = g[q];
+                    if (cd[q] != kCodeMulti) {
+                        const int ps = (cd[q] - 1) & 127;  // single spike: ps steps ago
+                        h0 = ps < 64 ? 1ull << (ps & 63) : 0ull;
+                        h1 = ps >= 64 ? 1ull << (ps & 63) : 0ull;
+                    }
+                    h0 &= m0;
+                    h1 &= m1;
+                    const bool chg = h0 || h1 || !a.event;
+                    float w = qw[q];
+                    if (chg) {
+                        w = a.event ? stdp_synapse(w, h0, h1, age, 0, ri.xp0, ri.xp_now, 0.f,
+                                                   s_dpow, c_pot, c_dep, mu)
+                                    : stdp_synapse_steps(w, h0, h1, age, 0, ri.xp0, ri.xp_now,
+                                                         0.f, s_dpow[1], c_pot, c_dep, mu);
+                        ++written;
+                    }
+                    q_w[e] = w;
+                    q_j[e] = chg ? 1 : 0;
+                }
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+        // the waves of range 0 commit the row's t_last and pre trace (every
+        // row has a first part there, empty or not)
+        if (x == 0 && p.i < nrows && ri.age_pre != 0 && p.base == first_base(ri, 0) &&
+            lane == 0) {
+            a.t_last[ri.k] = (int32_t)t;
+            a.xpre[ri.k] = ri.xp_now;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int e = qb[u] + lane_rank(bl[u]);  // < (u + 1) * 64: inside the queue
+            const int rj = q_j[e];
+            const float rw = q_w[e];
+            const bool c = (bl[u] >> lane) & 1ull;
+            const bool chg = c && rj != 0;
+            const float w = c ? rw : p.w[u];
+            const int qi = p.base + u * kWave + lane;
+            const uint64_t m = ballot64(chg);
+            if (((m >> line0) & kLineMask) && qi >= p.s0 && qi < p.s1)
+                __builtin_nontemporal_store(w, wgt + ri.rs + qi);
+        }
+        issue(p);
+    };
+    while (A.i < nrows) {
+        step(A);
+        if (B.i >= nrows) break;
+        step(B);
+    }
+    written = wave_sum_i64(written);
+    if (lane == 0 && written)
+        atomicAdd((unsigned long long *)(a.stats + bid), (unsigned long long)written);
+}
+
 // One instance per history length: the 128-step one keeps a second word per
 // synapse in registers and takes fewer synapses per lane and part.
 template <int HW>
 __global__ __launch_bounds__(kStdpRowsBlock) void k_stdp_rows(StdpArgs a)
 {
     extern __shared__ uint4 dyn_sum[];
-    stdp_rows_body<kStdpRowsBlock, HW == 1 ? kStdpRowsUnroll : kStdpRowsUnroll2, HW>(
-        a, blockIdx.x, gridDim.x, (unsigned char *)dyn_sum);
+    if (a.xcd)
+        stdp_rows_xcd_body<kStdpRowsBlock, kStdpXcdUnroll, HW>(
+            a, blockIdx.x, gridDim.x, (unsigned char *)dyn_sum);
+    else
+        stdp_rows_body<kStdpRowsBlock, HW == 1 ? kStdpRowsUnroll : kStdpRowsUnroll2, HW>(
+            a, blockIdx.x, gridDim.x, (unsigned char *)dyn_sum);
 }
 
 // Naive plasticity (Fig. 2(a)), the baseline the lazy forms are measured
@@ -575,13 +816,15 @@ __global__ __launch_bounds__(kNaiveBlock) void k_stdp_naive(NaiveArgs a)
 // block's steps: item (b, slice) takes ring slot (t_emit0 + b) mod D and
 // writes the fixed-point input of its step to abatch, one chunk per item.
 //
-// The spike count is read in parallel with the first batch's snapshots (the
-// snapshot buffer holds n entries, so reading past the count stays inside
-// it; entries past the count are discarded), and the workgroup's statistics
-// are reduced before its final stores, so no barrier waits for them.
+// The spike count is read first and only the spikes below it are read
+// (a network with few spikes per step would otherwise read a whole batch of
+// snapshots per workgroup), and the workgroup's statistics are reduced
+// before its final stores, so no barrier waits for them.
 
 constexpr int kDlvDirectMax = 32;  // segments up to this long are mapped by their own thread
-static_assert(kDlvBatch == kDlvBlock, "one staged spike per thread");
+// spikes a thread stages per batch (spike j = r kDlvBlock + tid)
+constexpr int kDlvRounds = (kDlvBatch + kDlvBlock - 1) / kDlvBlock;
+static_assert(kDlvRounds == 2, "two staged spikes per thread");
 
 // The body of one workgroup (bid of nb, nb a multiple of 8) in its dynamic
 // LDS: the staging arrays (DlvShared), then nacc * W accumulators [, W
@@ -597,7 +840,6 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
     int *s_off = S.off;
     int *s_info = S.info;
     float *s_xp0 = S.xp0;
-    float *s_xpn = S.xpn;
     MapT *s_map = S.map;
     float *s_dpow = S.dpow;
     long long *sh = S.sh;
@@ -636,17 +878,24 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
     const int C = a.chunks;
     const int base = s * a.width;
     const int span = a.nacc * a.width;
-    // the first batch's snapshots (or list entries) go out before the staging
-    // loads, so the two round trips overlap
-    RowInfo ri0 = RowInfo{};
-    int k0 = 0;
-    if (c + C * tid < a.n) {
-        if (a.plastic)
-            ri0 = a.txinfo[c + C * tid];
-        else
-            k0 = list[c + C * tid];
+    // the count first (one scalar load), then the first batch's snapshots
+    // (or list entries) below it, before the staging loads, so the two
+    // round trips overlap: spikes j = rr kDlvBlock + tid
+    const int cnt = *cntp;
+    RowInfo ri0[kDlvRounds];
+    int k0[kDlvRounds];
+#pragma unroll
+    for (int rr = 0; rr < kDlvRounds; ++rr) {
+        const int j = rr * kDlvBlock + tid;
+        ri0[rr] = RowInfo{};
+        k0[rr] = 0;
+        if (j < kDlvBatch && c + C * j < cnt) {
+            if (a.plastic)
+                ri0[rr] = a.txinfo[c + C * j];
+            else
+                k0[rr] = list[c + C * j];
+        }
     }
-    const int cnt = *cntp;  // used only once the first batch's loads are out
     const int hw = a.hw;
     const int jn = min(a.width, a.n - base);  // > 0
     // the slice's histories and post traces: loads out now, stored below
@@ -657,15 +906,22 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
         stage_issue<kDlvBlock>(g_y, a.ypost + base, jn);
     }
     const int piv_stride = a.n_slices + 1;
-    // the first batch's pivots, as soon as its snapshots are in
-    int k0p = 0, p0p = 0, p1p = 0;
-    int64_t rsp = 0;
-    if (c + C * tid < a.n) {
-        k0p = min(max(a.plastic ? ri0.k : k0, 0), a.n - 1);  // entries past the count are stale
-        const int32_t *pv = a.piv + (int64_t)k0p * piv_stride + s;
-        p0p = pv[0];
-        p1p = pv[1];
-        rsp = a.plastic ? ri0.rs : a.row_ptr[k0p];
+    // the first batch's pivots, as soon as its snapshots are in (spikes
+    // below the count only)
+    int k0p[kDlvRounds], p0p[kDlvRounds], p1p[kDlvRounds];
+    int64_t rsp[kDlvRounds];
+#pragma unroll
+    for (int rr = 0; rr < kDlvRounds; ++rr) {
+        const int j = rr * kDlvBlock + tid;
+        k0p[rr] = p0p[rr] = p1p[rr] = 0;
+        rsp[rr] = 0;
+        if (j < kDlvBatch && c + C * j < cnt) {
+            k0p[rr] = min(max(a.plastic ? ri0[rr].k : k0[rr], 0), a.n - 1);
+            const int32_t *pv = a.piv + (int64_t)k0p[rr] * piv_stride + s;
+            p0p[rr] = pv[0];
+            p1p[rr] = pv[1];
+            rsp[rr] = a.plastic ? ri0[rr].rs : a.row_ptr[k0p[rr]];
+        }
     }
     if (tid == 0) s_written = 0ull;  // published by the batch loop's barriers
     for (int x = tid; x < span; x += kDlvBlock) acc[x] = 0;
@@ -681,21 +937,25 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
     const float c_pot = a.c_pot, c_dep = a.c_dep, mu = a.mu;
     long long ev = 0, written = 0;
     for (int b0 = 0;; b0 += kDlvBatch) {
-        // stage segment starts and lengths (one spike per thread)
-        const int r = c + C * (b0 + tid);
-        int len = 0;
-        if (r < a.n) {
+        // stage segment starts and lengths (spikes tid and kDlvBlock + tid)
+        int len[kDlvRounds];
+#pragma unroll
+        for (int rr = 0; rr < kDlvRounds; ++rr) {
+            const int j = rr * kDlvBlock + tid;
+            const int r = c + C * (b0 + j);
+            len[rr] = 0;
+            if (j >= kDlvBatch || r >= a.n) continue;
             int k, p0, p1;
             int64_t rs;
             RowInfo ri = RowInfo{};
-            if (a.plastic) ri = b0 == 0 ? ri0 : a.txinfo[r];
+            if (a.plastic) ri = b0 == 0 ? ri0[rr] : a.txinfo[r];
             const int plen_row = ri.len, ap = ri.age_pre;
             const float xp0 = ri.xp0, xpn = ri.xp_now;
             if (b0 == 0) {  // prefetched above
-                k = k0p;
-                rs = rsp;
-                p0 = p0p;
-                p1 = p1p;
+                k = k0p[rr];
+                rs = rsp[rr];
+                p0 = p0p[rr];
+                p1 = p1p[rr];
             } else {
                 k = min(max(a.plastic ? ri.k : list[r], 0), a.n - 1);  // past the count: stale
                 const int32_t *pv = a.piv + (int64_t)k * piv_stride + s;
@@ -704,13 +964,12 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
                 rs = a.plastic ? ri.rs : a.row_ptr[k];
             }
             if (r < cnt) {
-                len = p1 - p0;
-                s_start[tid] = rs + p0;
-                const int plen = ap != 0 ? min(max(plen_row - p0, 0), len) : 0;
+                len[rr] = p1 - p0;
+                s_start[j] = rs + p0;
+                const int plen = ap != 0 ? min(max(plen_row - p0, 0), len[rr]) : 0;
                 const int inh = (a.nacc == 2 && k >= a.n_exc) ? 1 : 0;
-                s_info[tid] = plen | ((ap & 0xff) << 18) | (inh << 26);
-                s_xp0[tid] = xp0;
-                s_xpn[tid] = xpn;
+                s_info[j] = plen | ((ap & 0xff) << 18) | (inh << 26);
+                s_xp0[j] = xp0;
                 if (a.plastic && s == 0 && ap != 0) {
                     a.t_last[k] = (int32_t)t;
                     a.xpre[k] = xpn;
@@ -718,14 +977,24 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
             }
         }
         const int nbt = min(kDlvBatch, max(0, (cnt - c + C - 1) / C - b0));
-        // one scan gives the offsets and (bits 40+) the number of long segments
-        const long long packed = (long long)len | ((long long)(len > kDlvDirectMax) << 40);
-        const long long incl_p = block_incl_scan_i64_n<kDlvBlock>(packed, sh);
-        const long long incl = incl_p & ((1ll << 40) - 1);
-        if (tid < nbt) s_off[tid] = (int)(incl - len);
-        if (tid == kDlvBlock - 1) {  // totals (threads >= nbt add 0)
-            s_off[nbt] = (int)incl;
-            s_nlong = (int)(incl_p >> 40);
+        // segment offsets in spike order, one scan per round that holds
+        // spikes; each packs the number of long segments in bits 40+
+        long long carry = 0;
+#pragma unroll
+        for (int rr = 0; rr < kDlvRounds; ++rr) {
+            if (rr > 0 && nbt <= rr * kDlvBlock) break;  // workgroup-uniform
+            const int j = rr * kDlvBlock + tid;
+            const long long packed =
+                (long long)len[rr] | ((long long)(len[rr] > kDlvDirectMax) << 40);
+            const long long incl_p = block_incl_scan_i64_n<kDlvBlock>(packed, sh) + carry;
+            if (j < nbt) s_off[j] = (int)((incl_p & ((1ll << 40) - 1)) - len[rr]);
+            if (tid == kDlvBlock - 1) S.total = incl_p;
+            __syncthreads();
+            carry = S.total;
+        }
+        if (tid == 0) {  // totals (spikes >= nbt add 0)
+            s_off[nbt] = (int)(carry & ((1ll << 40) - 1));
+            s_nlong = (int)(carry >> 40);
         }
         __syncthreads();
         const int total = s_off[nbt];
@@ -734,19 +1003,27 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
         for (int e0 = 0; e0 < total; e0 += kDlvWindow) {
             const int we = min(kDlvWindow, total - e0);
             if (direct) {
-                // short segments: each thread writes its own segment's entries
-                if (tid < nbt) {
-                    const int a0 = max(s_off[tid], e0), a1 = min(s_off[tid + 1], e0 + we);
-                    for (int x = a0; x < a1; ++x) s_map[x - e0] = (MapT)(tid + 1);
+                // short segments: each thread writes its own segments' entries
+#pragma unroll
+                for (int rr = 0; rr < kDlvRounds; ++rr) {
+                    const int j = rr * kDlvBlock + tid;
+                    if (j < nbt) {
+                        const int a0 = max(s_off[j], e0), a1 = min(s_off[j + 1], e0 + we);
+                        for (int x = a0; x < a1; ++x) s_map[x - e0] = (MapT)(j + 1);
+                    }
                 }
                 __syncthreads();
             } else {
                 // mark each segment's first entry in the window, then max-scan
                 for (int x = tid; x < we; x += kDlvBlock) s_map[x] = 0;
                 __syncthreads();
-                if (tid < nbt) {
-                    const int a0 = max(s_off[tid], e0), a1 = min(s_off[tid + 1], e0 + we);
-                    if (a0 < a1) s_map[a0 - e0] = (MapT)(tid + 1);
+#pragma unroll
+                for (int rr = 0; rr < kDlvRounds; ++rr) {
+                    const int j = rr * kDlvBlock + tid;
+                    if (j < nbt) {
+                        const int a0 = max(s_off[j], e0), a1 = min(s_off[j + 1], e0 + we);
+                        if (a0 < a1) s_map[a0 - e0] = (MapT)(j + 1);
+                    }
                 }
                 __syncthreads();
                 fill_segment_map<kDlvBlock, kDlvUnroll, MapT>(s_map, we, shi, 0);
@@ -791,11 +1068,14 @@ __device__ __forceinline__ void deliver_lds_body(const DeliverArgs &a, int bid, 
                     window_masks(age, m0, m1);
                     const uint64_t h1 = hw == 2 ? s_hist[tgt[u] * 2 + 1] & m1 : 0ull;
                     const uint64_t h0 = s_hist[tgt[u] * hw] & m0;
-                    wv[u] = a.event ? stdp_synapse(wv[u], h0, h1, age, 1, s_xp0[l], s_xpn[l],
+                    // the pre trace after this update, as the snapshot holds it
+                    const float xp0 = s_xp0[l];
+                    const float xpn = __fadd_rn(__fmul_rn(xp0, s_dpow[age]), 1.f);
+                    wv[u] = a.event ? stdp_synapse(wv[u], h0, h1, age, 1, xp0, xpn,
                                                    s_y[tgt[u]], s_dpow, c_pot, c_dep, mu)
-                                    : stdp_synapse_steps(wv[u], h0, h1, age, 1, s_xp0[l],
-                                                         s_xpn[l], s_y[tgt[u]], s_dpow[1], c_pot,
-                                                         c_dep, mu);
+                                    : stdp_synapse_steps(wv[u], h0, h1, age, 1, xp0, xpn,
+                                                         s_y[tgt[u]], s_dpow[1], c_pot, c_dep,
+                                                         mu);
                     wgt[gi[u]] = wv[u];
                     ++written;
                 }
@@ -865,6 +1145,9 @@ __global__ __launch_bounds__(kDlvBlock, 4) void k_synapse_pass(DeliverArgs d, St
     if ((int)blockIdx.x < nd)
         deliver_lds_body<CT, FusedMap<HW>>(d, blockIdx.x, nd,
                                            reinterpret_cast<unsigned char *>(dyn_pass));
+    else if (s.xcd)
+        stdp_rows_xcd_body<kDlvBlock, kStdpXcdUnroll, HW>(
+            s, blockIdx.x - nd, gridDim.x - nd, (unsigned char *)dyn_pass);
     else
         stdp_rows_body<kDlvBlock, HW == 1 ? kStdpRowsUnroll : kStdpRowsUnroll2, HW>(
             s, blockIdx.x - nd, gridDim.x - nd, (unsigned char *)dyn_pass);
@@ -990,10 +1273,15 @@ hipError_t launch_stdp_rows(hipStream_t s, const StdpArgs &a, int blocks, Kernel
 {
     static std::mutex mu;
     static int granted[2] = {64 * 1024, 64 * 1024};
-    const size_t table = a.code     ? (((size_t)a.n + 15) / 16) * 16
+    size_t xspan = 0;  // the largest target range of the XCD form
+    for (int x = 0; x < kXcds; ++x) xspan = std::max(xspan, (size_t)(a.xlo[x + 1] - a.xlo[x]));
+    const size_t table = a.xcd      ? (a.code ? (xspan + 15) / 16 * 16 : 0)
+                         : a.code   ? (((size_t)a.n + 15) / 16) * 16
                          : a.recent ? (size_t)a.nw * sizeof(uint64_t)
                                     : 0;
     const size_t lds = table + stdp_rows_queue_bytes(a.hw);
+    if (a.xcd && (blocks < kXcds || (a.xparts != 2 && a.xparts != 4 && a.xparts != 8)))
+        return hipErrorInvalidValue;
     const void *kern = a.hw == 2 ? (const void *)k_stdp_rows<2> : (const void *)k_stdp_rows<1>;
     const hipError_t e = allow_dynamic_lds(kern, (int)lds, mu, granted[a.hw == 2]);
     if (e != hipSuccess) return e;
@@ -1051,7 +1339,9 @@ hipError_t launch_synapse_pass(hipStream_t s, const DeliverArgs &d, const StdpAr
                             (const void *)k_synapse_pass<false, 2>,
                             (const void *)k_synapse_pass<true, 1>,
                             (const void *)k_synapse_pass<true, 2>};
-    if (nd % 8 != 0 || ns < 1) return hipErrorInvalidValue;
+    // (the XCD form needs a forced-row workgroup on every XCD)
+    if (nd % 8 != 0 || ns < 1 || (a.xcd && ns < kXcds)) return hipErrorInvalidValue;
+    if (a.xcd && a.xparts != 2 && a.xparts != 4 && a.xparts != 8) return hipErrorInvalidValue;
     const hipError_t e = allow_dynamic_lds(kerns[k], (int)lds, mu, granted[k]);
     if (e != hipSuccess) return e;
     const dim3 g(nd + ns), b(kDlvBlock);

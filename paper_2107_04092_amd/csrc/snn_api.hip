@@ -101,6 +101,16 @@ struct snn_ctx {
     int32_t *rows = nullptr, *row_cnt = nullptr, *err_flag = nullptr, *maxlen = nullptr;
     int32_t *tx_cnt = nullptr;  // transmitted spikes of the step in progress (count)
     unsigned long long *static_status = nullptr;  // `scratch` on this context's device
+    // forced rows partitioned by target range over the XCDs (StdpArgs::xcd):
+    // the number of ranges (and the least the LDS reservation allows), the
+    // ranges, their slice boundaries, the largest range's code table bytes,
+    // and the forced rows' segment ends written by the neuron update
+    // ([n_plastic_rows][8])
+    bool xcd = false;
+    int32_t xparts = 0, xparts_min = 0;
+    int32_t xlo[kXcds + 1] = {}, xcd_piv[kXcds + 1] = {};
+    int32_t xcd_table = 0;
+    int32_t *segb = nullptr;
     int64_t *row_ptr = nullptr, *scratch = nullptr, *bsum = nullptr;
     int64_t *gstats = nullptr, *info_stats = nullptr, *syn_stats = nullptr, *dlv_stats = nullptr;
     RowInfo *info = nullptr, *txinfo = nullptr;
@@ -196,6 +206,9 @@ snn_status validate(snn_ctx *c, const snn_config &k)
         return fail(c, SNN_EINVAL, "stdp_filter must be in [0, 3]");
     if (k.compressed_targets < 0 || k.compressed_targets > 1)
         return fail(c, SNN_EINVAL, "compressed_targets must be 0 or 1");
+    if (k.stdp_xcd != 0 && k.stdp_xcd != 1 && k.stdp_xcd != 2 && k.stdp_xcd != 4 &&
+        k.stdp_xcd != 8)
+        return fail(c, SNN_EINVAL, "stdp_xcd must be 0, 1, 2, 4 or 8");
     if (k.stdp_filter == 1 && (int64_t)k.n + 16 > kCodeMax)
         return fail(c, SNN_EINVAL, "stdp_filter 1 needs n + 16 <= %d", kCodeMax);
     if (k.stdp_filter == 2 && (k.n + 63) / 64 > kRecentMaxWords)
@@ -230,6 +243,49 @@ snn_status validate(snn_ctx *c, const snn_config &k)
             return fail(c, SNN_EINVAL, "lambda and alpha must be >= 0");
     }
     return SNN_OK;
+}
+
+// The plastic targets' slices (all targets, or the excitatory ones).
+int32_t xcd_plastic_slices(const snn_ctx *c)
+{
+    const int32_t limit = c->cfg.plastic == SNN_PLASTIC_EXC_EXC ? c->cfg.n_exc : c->n;
+    return (limit + c->cfg.slice_width - 1) / c->cfg.slice_width;
+}
+
+// Cuts the plastic targets' slices into `parts` ranges (entries past the
+// last range repeat its end) and sizes the largest range's code table.
+void set_xcd_ranges(snn_ctx *c, int parts)
+{
+    const int32_t sp = xcd_plastic_slices(c);
+    int32_t span = 0;
+    for (int x = 0; x <= kXcds; ++x) {
+        const int xx = std::min(x, parts);
+        c->xcd_piv[x] = (int32_t)((int64_t)xx * sp / parts);
+        c->xlo[x] = (int32_t)std::min<int64_t>((int64_t)c->xcd_piv[x] * c->cfg.slice_width, c->n);
+        if (x > 0) span = std::max(span, c->xlo[x] - c->xlo[x - 1]);
+    }
+    c->xparts = parts;
+    c->xcd_table = (span + 15) / 16 * 16;
+}
+
+// The automatic range count, once the edge count is known: the most ranges
+// (of 2, 4, 8, at least the count the LDS reservation was made for) whose
+// segments still hold about three quarters of a part, taking a forced row's
+// plastic entries as its share of the edges spread evenly over the targets.
+void choose_xcd_ranges(snn_ctx *c)
+{
+    if (!c->xcd || c->cfg.stdp_xcd != 1) return;
+    const int32_t sp = xcd_plastic_slices(c);
+    const int64_t limit = std::min<int64_t>((int64_t)sp * c->cfg.slice_width, c->n);
+    const double seg = (double)c->n_edges / c->n * (double)limit / c->n;
+    const int part = kStdpXcdUnroll * kWave;
+    int parts = c->xparts_min;
+    for (int p = kXcds; p > c->xparts_min; p /= 2)
+        if (p <= sp && seg / p >= 0.75 * part) {
+            parts = p;
+            break;
+        }
+    set_xcd_ranges(c, parts);
 }
 
 // Constants derived here on the host from the physical parameters (double,
@@ -329,6 +385,7 @@ void plan_workspace(snn_ctx *c, uint8_t *base)
     c->rows = p.take<int32_t>(n);
     c->row_cnt = p.take<int32_t>(1);
     c->tx_cnt = p.take<int32_t>(1);
+    c->segb = p.take<int32_t>(c->xcd ? (int64_t)c->n_plastic_rows * kXcds : 1);
     c->err_flag = p.take<int32_t>(1);
     c->maxlen = p.take<int32_t>(1);
     c->row_ptr = p.take<int64_t>(n + 1);
@@ -544,6 +601,11 @@ snn_status launch_step_neurons(snn_ctx *c)
     b.xpre = c->xpre;
     b.err = c->err_flag;
     b.info_stats = c->n_plastic_rows > 0 && c->algo != 2 ? c->info_stats : nullptr;
+    b.segb = c->xcd ? c->segb : nullptr;
+    b.piv = c->piv;
+    b.piv_stride = c->n_slices + 1;
+    b.xparts = c->xparts;
+    for (int x = 0; x <= kXcds; ++x) b.xcd_piv[x] = c->xcd_piv[x];
     for (int q = 0; q <= kMaxAge; ++q) b.dpow[q] = c->dpow[q];
     snn_status st =
         check_hip(c, launch_neuron(c->stream, a, b, part_events(c, 0)), "neuron kernel");
@@ -599,6 +661,15 @@ StdpArgs stdp_args(snn_ctx *c, bool flush, int64_t waves = 0)
     a.code = filt && (f == 1 || (f == 0 && fits_code)) ? c->code : nullptr;
     a.recent = filt && (f == 2 || (f == 0 && !fits_code && fits_map)) ? c->recent : nullptr;
     a.event = c->algo == 0;
+    // forced rows over the XCDs: each range's codes (none when not event-driven)
+    a.xcd = c->xcd && !flush;
+    a.xparts = c->xparts;
+    a.segb = c->segb;
+    for (int x = 0; x <= kXcds; ++x) a.xlo[x] = c->xlo[x];
+    if (a.xcd) {
+        a.code = filt ? c->code : nullptr;
+        a.recent = nullptr;
+    }
     a.nw = c->nw;
     // row-wise layout: a row's parts (counting the row start's offset in its
     // line) may spread over P waves. P minimises the parts one wave takes in
@@ -733,7 +804,8 @@ snn_status launch_step_synapse_pass(snn_ctx *c, KernelEvents ev)
     const int nd = c->dlv_blocks;
     const int ns = std::max(8, c->fuse_slots - nd);
     StdpArgs a = stdp_args(c, false, (int64_t)ns * (kDlvBlock / kWave));
-    const size_t table = a.code     ? (((size_t)c->n + 15) / 16) * 16
+    const size_t table = a.xcd      ? (a.code ? (size_t)c->xcd_table : 0)
+                         : a.code   ? (((size_t)c->n + 15) / 16) * 16
                          : a.recent ? (size_t)c->nw * sizeof(uint64_t)
                                     : 0;
     const size_t dlv = dlv_lds_bytes(c) - sizeof(DlvShared) + fused_dlv_shared_bytes(c->hw);
@@ -765,6 +837,11 @@ snn_status launch_step_delivery(snn_ctx *c, int32_t mode)
         StdpArgs r = stdp_args(c, false);
         r.info = c->txinfo;
         r.tx_rows = 1;
+        // transmitting rows: the row-wise form, gathering every target's
+        // history and post trace (no summary staged)
+        r.xcd = 0;
+        r.code = nullptr;
+        r.recent = nullptr;
         st = check_hip(c, launch_stdp_rows(c->stream, r, c->n_cu, {ev.start, nullptr}),
                        "STDP of transmitting rows");
         if (st) return st;
@@ -870,6 +947,36 @@ snn_status snn_create(const snn_config *cfg, void *hip_stream, snn_ctx **out)
     // parts' dynamic LDS gives the workgroups a CU holds; it is used when
     // the delivery items leave at least half a slot per CU to the forced
     // rows (fewer waves starve them: slower than two launches).
+    // Forced rows by target range over the XCDs: on where asked for, codes
+    // or no summary are in use, every range has slices and a range's codes
+    // fit in LDS. The LDS reservation is made here for the fewest ranges
+    // allowed (largest table): a fixed count, or (automatic) the fewest
+    // whose codes fit beside the forced rows' queues within the delivery
+    // role's LDS, which the count chosen when the graph is bound does not
+    // undercut.
+    if (c->n_plastic_rows > 0 && c->algo != 2 && cfg->stdp_layout == 0 && cfg->stdp_xcd != 0 &&
+        (cfg->stdp_filter == 0 || cfg->stdp_filter == 1)) {
+        const int32_t sp = xcd_plastic_slices(c);
+        const int64_t dlv = need - (int64_t)sizeof(DlvShared) + (int64_t)fused_dlv_shared_bytes(c->hw);
+        int parts = 0;
+        for (int p = 2; p <= kXcds && !parts; p *= 2) {
+            if (cfg->stdp_xcd > 1 && p != cfg->stdp_xcd) continue;
+            if (p > sp) break;
+            set_xcd_ranges(c, p);
+            const bool fits = c->xcd_table <= kCodeMax &&
+                              (cfg->stdp_xcd > 1 || c->xcd_table + fused_queue_bytes(c->hw) <= dlv);
+            if (fits) parts = p;
+        }
+        if (!parts && cfg->stdp_xcd == 1) {  // else the fewest whose codes fit at all
+            for (int p = 2; p <= kXcds && p <= sp && !parts; p *= 2) {
+                set_xcd_ranges(c, p);
+                if (c->xcd_table <= kCodeMax) parts = p;
+            }
+        }
+        c->xcd = parts > 0;
+        c->xparts_min = parts;
+        if (parts) set_xcd_ranges(c, parts);
+    }
     if (c->n_plastic_rows > 0 && c->algo != 2 && cfg->stdp_layout == 0) {
         const int fstat = synapse_pass_static_bytes();
         if (fstat < 0) return fail(c, SNN_EDEVICE, "cannot query the kernels");
@@ -877,7 +984,8 @@ snn_status snn_create(const snn_config *cfg, void *hip_stream, snn_ctx **out)
         const int f = cfg->stdp_filter;
         const bool fits_code = (int64_t)c->n + 16 <= kCodeMax, fits_map = c->nw <= kRecentMaxWords;
         const int64_t code_b = ((int64_t)c->n + 15) / 16 * 16, map_b = (int64_t)c->nw * 8;
-        const int64_t table = f == 1 ? code_b
+        const int64_t table = c->xcd ? c->xcd_table
+                              : f == 1 ? code_b
                               : f == 2 ? map_b
                               : f == 0 ? (fits_code ? code_b : fits_map ? map_b : 0)
                                        : 0;
@@ -1001,6 +1109,7 @@ snn_status snn_bind_graph(snn_ctx *c, void *device_ptr, size_t bytes, int64_t n_
     c->g = (uint8_t *)device_ptr;
     c->g_bytes = bytes;
     c->n_edges = n_edges;
+    choose_xcd_ranges(c);
     const size_t arr = align_up((size_t)n_edges * sizeof(int32_t));
     c->col = (int32_t *)c->g;
     c->w = (float *)(c->g + arr);
@@ -1447,6 +1556,7 @@ snn_status snn_get_graph(const snn_ctx *c, snn_graph_view *out)
     out->pivots = c->piv;
     out->plastic_end = c->pend;
     out->col16 = c->col16;
+    out->stdp_ranges = c->xcd ? c->xparts : 0;
     return SNN_OK;
 }
 

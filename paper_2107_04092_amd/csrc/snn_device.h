@@ -55,18 +55,67 @@ __device__ __forceinline__ void add_stat(int64_t *p, long long v)
     if (v) (void)atomicAdd((unsigned long long *)p, (unsigned long long)v);
 }
 
+// Wave-wide scans by DPP lane moves (VALU operations: no LDS round trip per
+// step, unlike shuffles). dpp_mov<CTRL, RM> returns, per lane, x of the lane
+// CTRL selects, or id where that lane does not exist or the lane's row is
+// not in the row mask RM.
+template <int CTRL, int RM>
+__device__ __forceinline__ int dpp_mov(int x, int id)
+{
+    return __builtin_amdgcn_update_dpp(id, x, CTRL, RM, 0xf, false);
+}
+template <int CTRL, int RM>
+__device__ __forceinline__ long long dpp_mov(long long x, long long id)
+{
+    const int lo = __builtin_amdgcn_update_dpp((int)id, (int)x, CTRL, RM, 0xf, false);
+    const int hi = __builtin_amdgcn_update_dpp((int)(id >> 32), (int)(x >> 32), CTRL, RM, 0xf,
+                                               false);
+    return (long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo);
+}
+constexpr int kDppRowShr1 = 0x111, kDppRowShr2 = 0x112, kDppRowShr4 = 0x114,
+              kDppRowShr8 = 0x118, kDppRowBcast15 = 0x142, kDppRowBcast31 = 0x143,
+              kDppWaveShr1 = 0x138;
+
+// Inclusive scan over the 64 lanes with the associative op (identity id):
+// shifts by 1, 2, 4, 8 inside each row of 16 lanes, then lane 15 of rows 0
+// and 2 into rows 1 and 3, then lane 31 into rows 2 and 3.
+template <typename T, typename Op>
+__device__ __forceinline__ T wave_incl_scan(T x, T id, Op op)
+{
+    x = op(x, dpp_mov<kDppRowShr1, 0xf>(x, id));
+    x = op(x, dpp_mov<kDppRowShr2, 0xf>(x, id));
+    x = op(x, dpp_mov<kDppRowShr4, 0xf>(x, id));
+    x = op(x, dpp_mov<kDppRowShr8, 0xf>(x, id));
+    x = op(x, dpp_mov<kDppRowBcast15, 0xa>(x, id));
+    x = op(x, dpp_mov<kDppRowBcast31, 0xc>(x, id));
+    return x;
+}
+// The value of the previous lane (lane 0: id).
+template <typename T>
+__device__ __forceinline__ T wave_shr1(T x, T id)
+{
+    return dpp_mov<kDppWaveShr1, 0xf>(x, id);
+}
+struct AddOp {
+    template <typename T>
+    __device__ __forceinline__ T operator()(T a, T b) const { return a + b; }
+};
+struct MaxOp {
+    template <typename T>
+    __device__ __forceinline__ T operator()(T a, T b) const { return a > b ? a : b; }
+};
+
 __device__ __forceinline__ int wave_sum_i32(int v)
 {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
-    return v;
+    return __builtin_amdgcn_readlane(wave_incl_scan(v, 0, AddOp{}), kWave - 1);
 }
 
 __device__ __forceinline__ long long wave_sum_i64(long long v)
 {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
-    return v;
+    const long long s = wave_incl_scan(v, 0ll, AddOp{});
+    const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)s, kWave - 1);
+    const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(s >> 32), kWave - 1);
+    return (long long)(((unsigned long long)hi << 32) | lo);
 }
 
 // Copies count > 0 elements from global memory into LDS with an NT-thread
@@ -156,11 +205,7 @@ template <int NT>
 __device__ __forceinline__ long long block_incl_scan_i64_n(long long v, long long *sh)
 {
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-        const long long u = __shfl_up(v, off, kWave);
-        if (lane >= off) v += u;
-    }
+    v = wave_incl_scan(v, 0ll, AddOp{});
     __syncthreads();
     if (lane == kWave - 1) sh[wave] = v;
     __syncthreads();
@@ -186,16 +231,10 @@ __device__ __forceinline__ void fill_segment_map(T *mark, int len, int *sh, int 
         m = max(m, u);
         v[q] = m;
     }
-    int inc = m;
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-        const int u = __shfl_up(inc, off, kWave);
-        if (lane >= off) inc = max(inc, u);
-    }
+    const int inc = wave_incl_scan(m, none, MaxOp{});
     if (lane == kWave - 1) sh[wave] = inc;
     __syncthreads();
-    int excl = __shfl_up(inc, 1, kWave);
-    if (lane == 0) excl = none;
+    int excl = wave_shr1(inc, none);
     for (int q = 0; q < wave; ++q) excl = max(excl, sh[q]);
 #pragma unroll
     for (int q = 0; q < E; ++q) {
@@ -206,13 +245,21 @@ __device__ __forceinline__ void fill_segment_map(T *mark, int len, int *sh, int 
 }
 
 
+// The decay-table index of a row of t_last t_last_k brought up to step t:
+// its age, at most the history's 64 hw steps (0 for a row already current).
+__device__ __forceinline__ int row_age_index(int64_t t, int t_last_k, int hw)
+{
+    const int age = (int)(t - (int64_t)t_last_k);
+    return age <= 0 ? 0 : min(age, 64 * hw);
+}
+
 // Snapshot of plastic row k for an update at step t (see RowInfo) from the
 // row's values: t_last, first edge rs, plastic prefix length, pre trace at
-// t_last, and whether the row transmits at t. Returns 1 if the row has
-// something to bring up to date.
-__device__ __forceinline__ int make_row_info_v(RowInfo &ri, int k, int64_t t, int t_last_k,
+// t_last, and whether the row transmits at t; dp_age = d_plus^age at
+// row_age_index. Returns 1 if the row has something to bring up to date.
+__device__ __forceinline__ int make_row_info_d(RowInfo &ri, int k, int64_t t, int t_last_k,
                                                int64_t rs, int pend_k, float xpre_k, int pre,
-                                               int hw, const float *dpow, int32_t *err)
+                                               int hw, float dp_age, int32_t *err)
 {
     int age = (int)(t - (int64_t)t_last_k);
     ri.k = k;
@@ -233,8 +280,17 @@ __device__ __forceinline__ int make_row_info_v(RowInfo &ri, int k, int64_t t, in
     }
     ri.len = pend_k;
     ri.age_pre = age | (pre << 8);
-    ri.xp_now = __fadd_rn(__fmul_rn(ri.xp0, dpow[age]), (float)pre);
+    ri.xp_now = __fadd_rn(__fmul_rn(ri.xp0, dp_age), (float)pre);
     return 1;
+}
+
+// The same with the decay table.
+__device__ __forceinline__ int make_row_info_v(RowInfo &ri, int k, int64_t t, int t_last_k,
+                                               int64_t rs, int pend_k, float xpre_k, int pre,
+                                               int hw, const float *dpow, int32_t *err)
+{
+    return make_row_info_d(ri, k, t, t_last_k, rs, pend_k, xpre_k, pre, hw,
+                           dpow[row_age_index(t, t_last_k, hw)], err);
 }
 
 // The same reading the values from the state arrays.
@@ -322,6 +378,19 @@ __device__ __forceinline__ unsigned long long status_word(int a, int b, int64_t 
            ((unsigned long long)(t & 0x3fff) << 48) | kind;
 }
 
+// The step clock read with vector loads (relaxed, device scope): unlike a
+// scalar load, its wait does not join the wait for the kernel arguments.
+__device__ __forceinline__ StepClock load_clock(const StepClock *c)
+{
+    StepClock k{};
+    k.t = __hip_atomic_load(&c->t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const long long f = __hip_atomic_load(reinterpret_cast<const long long *>(&c->input_forced),
+                                          __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    k.input_forced = (int32_t)(uint32_t)f;
+    k.n_parts = (int32_t)(f >> 32);
+    return k;
+}
+
 __device__ __forceinline__ void publish_status(unsigned long long *p, unsigned long long w)
 {
     __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -349,6 +418,11 @@ __device__ void lookback(unsigned long long *status, int64_t stride, int nscan, 
     // sh[8 r + ...]: 0 nearest inclusive in the window (NT: none), 1 lanes
     // not yet published, 2-3 the window's sums, 4 window end, 5 done, 6-7 prefixes
     const int tid = threadIdx.x, lane = tid % kWave;
+    // thread tid reads the predecessor at distance 1 + d in the window: wave
+    // 0, whose thread 0 has just stored this workgroup's status, takes the
+    // farthest distances (none in a grid of at most NT - 63 workgroups), so
+    // the reads the scan waits for are not queued behind that store
+    const int d = (tid + NT - kWave) % NT;
     if (tid < R) {
         int *q = sh + 8 * tid;
         q[4] = b;
@@ -372,7 +446,7 @@ __device__ void lookback(unsigned long long *status, int64_t stride, int nscan, 
         unsigned long long w[R];
 #pragma unroll
         for (int r = 0; r < R; ++r) {  // every read of the round in flight together
-            const int p = sh[8 * r + 4] - 1 - tid;
+            const int p = sh[8 * r + 4] - 1 - d;
             w[r] = 0ull;
             if (!sh[8 * r + 5] && p >= 0)
                 w[r] = __hip_atomic_load(status + r * stride + p, __ATOMIC_RELAXED,
@@ -388,17 +462,17 @@ __device__ void lookback(unsigned long long *status, int64_t stride, int nscan, 
         for (int r = 0; r < R; ++r) {  // the nearest inclusive prefix of the window
             if (sh[8 * r + 5]) continue;
             const unsigned tag = (unsigned)((t0 + r) & 0x3fff);
-            const bool inc = sh[8 * r + 4] - 1 - tid >= 0 && (w[r] >> 62) == 2ull &&
+            const bool inc = sh[8 * r + 4] - 1 - d >= 0 && (w[r] >> 62) == 2ull &&
                              (unsigned)((w[r] >> 48) & 0x3fff) == tag;
-            const uint64_t bl = ballot64(inc);
-            if (bl && lane == __ffsll((long long)bl) - 1) atomicMin(&sh[8 * r], tid);
+            const uint64_t bl = ballot64(inc);  // (d rises with the lane)
+            if (bl && lane == __ffsll((long long)bl) - 1) atomicMin(&sh[8 * r], d);
         }
         __syncthreads();
 #pragma unroll
         for (int r = 0; r < R; ++r) {  // counts up to it; predecessors not yet published
             if (sh[8 * r + 5]) continue;
             const unsigned tag = (unsigned)((t0 + r) & 0x3fff);
-            const bool need = sh[8 * r + 4] - 1 - tid >= 0 && tid <= sh[8 * r];
+            const bool need = sh[8 * r + 4] - 1 - d >= 0 && d <= sh[8 * r];
             const bool cur = (w[r] >> 62) != 0ull && (unsigned)((w[r] >> 48) & 0x3fff) == tag;
             const uint64_t bad = ballot64(need && !cur);
             int va = need && cur ? (int)(w[r] & 0xffffffull) : 0;
@@ -431,7 +505,7 @@ __device__ void lookback(unsigned long long *status, int64_t stride, int nscan, 
 
 // The same for up to NT/32 scans, one per half wave: scan r is looked back
 // over by threads 32 r .. 32 r + 31, a window of 32 predecessors at a time,
-// with ballots and shuffles inside the half wave, so the scans need no
+// with ballots and lane moves inside the wave, so the scans need no
 // workgroup barrier until the end. On return out[2 r], out[2 r + 1] (LDS)
 // hold scan r's two prefixes. Bounded as above.
 template <int NT>
@@ -465,10 +539,12 @@ __device__ void lookback32(unsigned long long *status, int64_t stride, int nscan
         const uint32_t badm = (uint32_t)(ballot64(need && !cur) >> (32 * half));
         int va = need && cur ? (int)(w & 0xffffffull) : 0;
         int vb = need && cur ? (int)((w >> 24) & 0xffffffull) : 0;
-#pragma unroll
-        for (int off = 16; off > 0; off >>= 1) {  // sums inside the half wave
-            va += __shfl_xor(va, off, kWave);
-            vb += __shfl_xor(vb, off, kWave);
+        {  // sums inside the half wave: lanes 31 and 63 of a wave scan
+            const int sa = wave_incl_scan(va, 0, AddOp{}), sb = wave_incl_scan(vb, 0, AddOp{});
+            const int a31 = __builtin_amdgcn_readlane(sa, 31), a63 = __builtin_amdgcn_readlane(sa, 63);
+            const int b31 = __builtin_amdgcn_readlane(sb, 31), b63 = __builtin_amdgcn_readlane(sb, 63);
+            va = half ? a63 - a31 : a31;
+            vb = half ? b63 - b31 : b31;
         }
         if (!done && badm == 0) {
             acc_a += va;

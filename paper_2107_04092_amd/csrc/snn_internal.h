@@ -14,6 +14,7 @@ constexpr int kNeuronBlock = 1024;   // threads per workgroup of the neuron upda
 constexpr int kNeuronSmallN = 65536; // up to this many neurons the update takes kBlock threads
                                      // per workgroup
 constexpr int kWave = 64;            // CDNA wavefront width
+constexpr int kXcds = 8;             // XCDs of the device: workgroup b runs on XCD b mod 8
 constexpr int kMaxPoisson = 32;
 constexpr int kMaxSortRow = 16384;   // longest row the LDS row sort accepts
 constexpr int kStdpBlock = 512;      // threads of the slice STDP kernel
@@ -125,6 +126,13 @@ struct CompactArgs {
     const float *xpre;
     int32_t *err;
     int64_t *info_stats;     // [gridDim.x][kStFields]
+    // target-range segments of the forced rows (see StdpArgs::segb), when
+    // segb is given: segment x < xparts of row k ends at pivot
+    // piv[k][xcd_piv[x + 1]]
+    int32_t *segb;
+    const int32_t *piv;
+    int32_t piv_stride, xparts;
+    int32_t xcd_piv[kXcds + 1];
     float dpow[kMaxAge + 1];
 };
 
@@ -184,6 +192,20 @@ struct StdpArgs {
     const uint64_t *recent;
     int32_t nw;              // words of `recent`
     int32_t parts;           // row-wise layout: waves sharing one row (>= 1)
+    // Forced rows partitioned by target range over the XCDs (xcd != 0): the
+    // plastic targets are cut into xparts (2, 4 or 8) ranges of whole
+    // slices, [xlo[x], xlo[x+1]); range x belongs to the 8 / xparts XCDs
+    // b mod 8 in [x 8 / xparts, (x + 1) 8 / xparts), whose waves bring up
+    // to date the entries of every forced row with targets in range x: the
+    // target histories they gather stay in those XCDs' L2, and they stage
+    // the history codes of range x only. The entries of forced row r (list
+    // position) in range x are segb[8 r + x - 1] (0 for x = 0) ..
+    // segb[8 r + x] - 1, boundaries moved to 128-byte lines of the weight
+    // array so that no line is shared by two ranges (a target next to a
+    // boundary may fall outside the range: it is gathered).
+    int32_t xcd, xparts;
+    const int32_t *segb;
+    int32_t xlo[kXcds + 1];
     float dpow[kMaxAge + 1];
 };
 
@@ -343,8 +365,11 @@ hipError_t launch_probe_rows(hipStream_t s, int blocks, const int64_t *row_ptr,
 constexpr int kStdpRowsBlock = 1024;   // threads of the row-wise STDP kernel
 constexpr int kStdpRowsUnroll = 8;     // synapses per lane and row part (64-step histories)
 constexpr int kStdpRowsUnroll2 = 4;    // the same with 128-step histories
+constexpr int kStdpXcdUnroll = 4;      // the same in the target-range form (both lengths)
 constexpr int kDlvBlock = 512;         // threads per workgroup of slice delivery
-constexpr int kDlvBatch = 512;         // spikes whose segments slice delivery stages at once
+constexpr int kDlvBatch = 704;         // spikes whose segments slice delivery stages at once
+                                       // (two per thread: 1,250 spikes over two chunks fit
+                                       // one batch, 4.5 standard deviations above the mean)
 constexpr int kDlvUnroll = 8;          // flattened elements per thread per window
 constexpr int kDlvWindow = kDlvBlock * kDlvUnroll;
 // Slice delivery's staging arrays, at the start of its dynamic LDS. MapT is
@@ -355,16 +380,19 @@ struct DlvSharedT {
     long long start[kDlvBatch];        // segment starts (edge index)
     long long sh[kDlvBlock / 64];      // scan scratch
     unsigned long long written;        // weights written by the workgroup
+    long long total;                   // the scan's running total between its rounds
     int off[kDlvBatch + 1];            // segment offsets in the batch
     // per segment: plastic elements (bits 0-17), row age (bits 18-25: the
     // replay window), inhibitory source of a CUBA network (bit 26)
     int info[kDlvBatch];
-    float xp0[kDlvBatch], xpn[kDlvBatch];  // pre traces at the last update and now
+    // pre trace at the last update (the trace after this one, x0 d+^age + 1,
+    // is computed where it is needed, as the neuron update computed it)
+    float xp0[kDlvBatch];
     MapT map[kDlvWindow];              // element -> 1 + segment of the window (0: none)
     float dpow[kMaxAge + 1];           // decay table
     int shi[kDlvBlock / 64];           // scan scratch
     int nlong;                         // segments longer than the direct-map limit
-    int pad_[3];
+    int pad_[1];
 };
 using DlvShared = DlvSharedT<int>;
 using DlvShared16 = DlvSharedT<uint16_t>;

@@ -34,7 +34,7 @@ class snn_config(ctypes.Structure):
         ("n", _i32), ("n_exc", _i32), ("delay_steps", _i32), ("slice_width", _i32),
         ("spike_chunks", _i32), ("stdp_slice_mult", _i32), ("stdp_chunks", _i32),
         ("stdp_layout", _i32), ("stdp_filter", _i32), ("history_bits", _i32),
-        ("plasticity_algorithm", _i32), ("compressed_targets", _i32),
+        ("plasticity_algorithm", _i32), ("compressed_targets", _i32), ("stdp_xcd", _i32),
         ("neuron_model", _i32),
         ("plastic", _i32), ("poisson_len", _i32),
         ("dt_ms", _f64), ("tau_m_ms", _f64), ("v_th", _f64), ("v_reset", _f64),
@@ -54,7 +54,8 @@ class snn_state_view(ctypes.Structure):
 
 class snn_graph_view(ctypes.Structure):
     _fields_ = [("n_edges", _i64), ("n_slices", _i32), ("row_ptr", _P),
-                ("col", _P), ("w", _P), ("pivots", _P), ("plastic_end", _P), ("col16", _P)]
+                ("col", _P), ("w", _P), ("pivots", _P), ("plastic_end", _P), ("col16", _P),
+                ("stdp_ranges", _i32)]
 
 
 class snn_stats(ctypes.Structure):
@@ -281,7 +282,8 @@ def snn_get_kernel_times(ctx):
 
 def config_from_preset(p, poisson_table=(), slice_width=None, spike_chunks=None,
                        stdp_slice_mult=0, stdp_chunks=0, stdp_layout=0, stdp_filter=0,
-                       history_bits=64, plasticity_algorithm=0, compressed_targets=None):
+                       history_bits=64, plasticity_algorithm=0, compressed_targets=None,
+                       stdp_xcd=0):
     """snn_config from a preset-like object with the physical parameters."""
     c = snn_config()
     c.n, c.n_exc, c.delay_steps = p.n, p.n_exc, p.delay
@@ -294,6 +296,7 @@ def config_from_preset(p, poisson_table=(), slice_width=None, spike_chunks=None,
     c.plasticity_algorithm = plasticity_algorithm
     c.compressed_targets = (getattr(p, "compressed_targets", 0) if compressed_targets is None
                             else compressed_targets)
+    c.stdp_xcd = stdp_xcd
     c.neuron_model, c.plastic = p.model, p.plastic
     c.dt_ms, c.tau_m_ms, c.v_th, c.v_reset, c.v_inf = p.dt, p.tau_m, p.v_th, p.v_reset, p.v_inf
     c.tau_ref_ms, c.tau_e_ms, c.tau_i_ms = p.tau_ref, p.tau_e, p.tau_i
@@ -485,4 +488,5 @@ class Network:
             "pivots": self._view(self.g, v.pivots, n * (s + 1), torch.int32).view(n, s + 1),
             "plastic_end": self._view(self.ws, v.plastic_end, n, torch.int32),
             "col16": (self._view(self.g, v.col16, e, torch.int16) if v.col16 else None),
+            "stdp_ranges": v.stdp_ranges,
         }

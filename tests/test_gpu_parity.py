@@ -472,3 +472,65 @@ def test_plasticity_algorithms(case, mode, algo, hbits):
         assert st["stdp_synapse_updates"] > 0
     net.flush_plasticity()
     compare_all_plastic_weights(net, o)
+
+
+XCD_CASES = [
+    # name, preset overrides, steps, slice width, chunks, target ranges: the
+    # plastic targets span at least as many slices as ranges
+    ("stress", dict(n=6000, p_or_fanout=200, p_fire=0.02), 200, 256, 2, 8),
+    ("stress", dict(n=3000, p_or_fanout=150, p_fire=0.03, delay=3), 160, 128, 1, 4),
+    ("brunel_plus", dict(n=2500, n_exc=2000), 260, 128, 2, 2),
+    ("vogels", dict(n=3000, n_exc=2400, plastic=PLASTIC_EXC_EXC, w0=0.05), 200, 192, 2, 8),
+]
+
+
+@pytest.mark.parametrize("hbits", [64, 128], ids=["h64", "h128"])
+@pytest.mark.parametrize("filt,algo", [(0, 0), (1, 0), (0, 1)], ids=["auto", "codes", "lazy"])
+@pytest.mark.parametrize("case", XCD_CASES,
+                         ids=lambda c: "%s-%s-x%d" % (c[0], c[1].get("n", ""), c[5]))
+def test_xcd_forced_rows_parity(case, filt, algo, hbits):
+    """Forced rows split by target range over the XCDs (the waves of a
+    range's XCDs take the entries of every forced row whose targets lie in
+    that range, with the range's history codes in LDS): the same
+    teacher-forced bar as the row-wise form."""
+    name, kw, steps, width, chunks, parts = case
+    p = wl.preset(name, **kw)
+    log("xcd parity %s %s filter=%d algo=%d history=%d W=%d C=%d ranges=%d" % (
+        name, kw, filt, algo, hbits, width, chunks, parts))
+    net, o, cnt = teacher_forced_run(p, steps, LDS, slice_width=width, spike_chunks=chunks,
+                                     stdp_filter=filt, plasticity_algorithm=algo,
+                                     history_bits=hbits, stdp_xcd=parts)
+    assert cnt["rows"] > 0 and cnt["weights"] > 0
+    assert net.graph()["stdp_ranges"] == parts
+    st = net.stats()
+    assert st["stdp_forced_rows"] > 0 and st["device_errors"] == 0
+    net.flush_plasticity()
+    compare_all_plastic_weights(net, o)
+
+
+@pytest.mark.parametrize("parts", [1, 2, 4, 8], ids=["auto", "x2", "x4", "x8"])
+@pytest.mark.parametrize("chunks", [2, 32], ids=["fused", "two-launches"])
+@pytest.mark.parametrize("hbits", [64, 128], ids=["h64", "h128"])
+def test_xcd_partition_equals_rowwise(chunks, hbits, parts):
+    """The forced rows split by target range and the row-wise form give the
+    same weights bit for bit (the same arithmetic per synapse, history bits
+    from the same codes or words), inside the fused pass and in the separate
+    forced-row launch (32 chunks leave the pass too few slots), for every
+    range count and the automatic one."""
+    p = wl.preset("stress", n=6000, p_or_fanout=300, p_fire=0.02, delay=2)
+    a = gpu_net(p, 256, chunks, history_bits=hbits, stdp_xcd=parts)  # by target range
+    b = gpu_net(p, 256, chunks, history_bits=hbits)                  # row-wise
+    assert a.graph()["stdp_ranges"] == (parts if parts > 1 else 2)  # 150 entries: 2 ranges
+    assert b.graph()["stdp_ranges"] == 0
+    for k in (1, 70, 150):
+        a.step(k, LDS)
+        b.step(k, LDS)
+    sa, sb = a.state(), b.state()
+    for key in ("hist", "t_last", "trace_pre", "trace_post", "input_exc"):
+        assert np.array_equal(to_np(sa[key]), to_np(sb[key])), key
+    assert np.array_equal(to_np(a.graph()["w"]), to_np(b.graph()["w"]))
+    ta, tb = a.stats(), b.stats()
+    for key in ("stdp_forced_rows", "stdp_synapse_updates", "stdp_weights_written",
+                "device_errors"):
+        assert ta[key] == tb[key], key
+    assert ta["stdp_forced_rows"] > 0 and ta["device_errors"] == 0
