@@ -65,7 +65,7 @@ def parse():
     ap.add_argument("--plasticity", choices=["lazy-event", "lazy", "naive"],
                     default="lazy-event",
                     help="plasticity algorithm (Fig. 2(c), (b), (a))")
-    ap.add_argument("--stdp-xcd", choices=["off", "auto", "2", "4", "8"], default="off",
+    ap.add_argument("--stdp-xcd", choices=sorted(XCD_ARG), default="off",
                     help="forced rows partitioned over the XCDs by target range")
     ap.add_argument("--stdp-mult", type=int, default=0)
     ap.add_argument("--stdp-chunks", type=int, default=0)
@@ -79,12 +79,19 @@ def parse():
     ap.add_argument("--no-row-probe", action="store_true",
                     help="skip the row-stream probe (the forced-row STDP access pattern "
                          "without its arithmetic, at the same row count)")
+    ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_DB", "WRITE_DB"),
+                    help="no run: write profiles/traffic.json for --config from two "
+                         "rocprofv3 --pmc result databases of a run with --copy-probe-mib "
+                         "(FETCH_SIZE, then WRITE_SIZE)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the timed region, run one device-to-device copy of this many "
                          "MiB: the reference kernel that scales rocprofv3 FETCH_SIZE/WRITE_SIZE "
                          "readings to bytes")
     return ap.parse_args()
 
+
+# --stdp-xcd: the config's stdp_xcd (0 off, 1 automatic, else the range count)
+XCD_ARG = {"off": 0, "auto": 1, "2": 2, "4": 4, "8": 8}
 
 _COMMENT = re.compile(r"//[^\n]*|/\*.*?\*/", re.S)
 
@@ -99,6 +106,48 @@ def kernel_source_digest():
             code = _COMMENT.sub(" ", fh.read())
         h.update(" ".join(code.split()).encode())
     return h.hexdigest()[:16]
+
+
+def write_traffic(fetch_db, write_db, workload_key, copy_mib):
+    """HBM bytes per launch of each kernel from two rocprofv3 counter runs
+    (FETCH_SIZE, then WRITE_SIZE, in KiB per dispatch), each scaled by what
+    the same counter reads for the reference copy of copy_mib MiB each way
+    (__amd_rocclr_copyBuffer); averaged over the dispatches after the first
+    quarter. Written to profiles/traffic.json under workload_key with the
+    current source digest."""
+    import sqlite3
+    import collections
+    vals = collections.defaultdict(lambda: collections.defaultdict(list))
+    for db, counter in ((fetch_db, "FETCH_SIZE"), (write_db, "WRITE_SIZE")):
+        con = sqlite3.connect(db)
+        for name, cn, v in con.execute(
+                "select kernel_name, counter_name, value from counters_collection"):
+            if cn != counter:
+                continue
+            k = name.replace("snn::(anonymous namespace)::", "").split("(")[0]
+            k = k.replace("void ", "").split("<")[0].strip()
+            vals[k][cn].append(float(v))
+        con.close()
+    ref = vals["__amd_rocclr_copyBuffer"]
+    kib = copy_mib * 1024.0
+    fs, ws = kib / max(ref["FETCH_SIZE"]), kib / max(ref["WRITE_SIZE"])
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    d = json.load(open(path)) if os.path.exists(path) else {}
+    out = {}
+    for k in ("k_neuron", "k_synapse_pass", "k_deliver_lds", "k_stdp_rows"):
+        f, w = vals[k]["FETCH_SIZE"], vals[k]["WRITE_SIZE"]
+        if not f or not w:
+            continue
+        f, w = f[len(f) // 4:], w[len(w) // 4:]
+        fk, wk = sum(f) / len(f), sum(w) / len(w)
+        out[k] = {"fetch_kib": round(fk, 1), "write_kib": round(wk, 1),
+                  "fetch_scale": round(fs, 4), "write_scale": round(ws, 4),
+                  "bytes_per_launch": round((fk * fs + wk * ws) * 1024),
+                  "dispatches": len(f), "source_digest": kernel_source_digest()}
+    d[workload_key] = out
+    with open(path, "w") as fh:
+        json.dump(d, fh, indent=1)
+    print(json.dumps({workload_key: out}, indent=1))
 
 
 def load_traffic(kernel, workload_key):
@@ -251,6 +300,12 @@ def check_device_errors(net, where):
 
 def main():
     args = parse()
+    if args.write_traffic:
+        if args.copy_probe_mib <= 0:
+            sys.exit("bench.py: --write-traffic needs the --copy-probe-mib of the profiled run")
+        write_traffic(args.write_traffic[0], args.write_traffic[1], args.config,
+                      args.copy_probe_mib)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py: the synapse pass is benchmarked on one GPU only; "
@@ -280,7 +335,7 @@ def main():
                                      args.plasticity),
                                  compressed_targets=(None if args.targets == "preset" else
                                                      int(args.targets == "16")),
-                                 stdp_xcd={"off": 0, "auto": 1}.get(args.stdp_xcd) or int(args.stdp_xcd))
+                                 stdp_xcd=XCD_ARG[args.stdp_xcd])
     t0 = time.time()
     net = snn.Network(cfg, stream=stream, device=dev)
     e = net.build_random(p.graph_kind, p.p_or_fanout, p.w_exc, p.w_inh)

@@ -102,3 +102,43 @@ def test_traffic_is_dropped_for_other_sources(monkeypatch):
     assert b.load_traffic(kernel, "stress") == float(d["stress"][kernel]["bytes_per_launch"])
     monkeypatch.setattr(b, "kernel_source_digest", lambda: "0" * 16)
     assert b.load_traffic(kernel, "stress") is None
+
+
+def test_write_traffic_scales_by_the_reference_copy(tmp_path, monkeypatch):
+    """profiles/traffic.json from two counter databases: each kernel's KiB per
+    dispatch (after the first quarter) scaled by the reference copy's reading
+    for its known size."""
+    import sqlite3
+    b = bench_module()
+    dbs = []
+    for counter, copy_kib, kern in (("FETCH_SIZE", 1024.0, [10.0, 100.0, 100.0, 100.0]),
+                                    ("WRITE_SIZE", 2048.0, [7.0, 50.0, 50.0, 50.0])):
+        path = str(tmp_path / (counter + ".db"))
+        con = sqlite3.connect(path)
+        con.execute("create table counters_collection (kernel_name text, counter_name text, "
+                    "value real)")
+        rows = [("__amd_rocclr_copyBuffer", counter, copy_kib)]
+        rows += [("void snn::(anonymous namespace)::k_synapse_pass<true, 2>(a, b, int)",
+                  counter, v) for v in kern]
+        con.executemany("insert into counters_collection values (?, ?, ?)", rows)
+        con.commit()
+        con.close()
+        dbs.append(path)
+    monkeypatch.setattr(b, "ROOT", str(tmp_path))
+    os.makedirs(tmp_path / "profiles")
+    monkeypatch.setattr(b, "kernel_source_digest", lambda: "abc")
+    b.write_traffic(dbs[0], dbs[1], "stress", 2)  # 2 MiB = 2048 KiB each way
+    d = json.load(open(tmp_path / "profiles" / "traffic.json"))
+    e = d["stress"]["k_synapse_pass"]
+    assert e["fetch_kib"] == 100.0 and e["write_kib"] == 50.0
+    assert e["fetch_scale"] == 2.0 and e["write_scale"] == 1.0
+    assert e["bytes_per_launch"] == round((100.0 * 2.0 + 50.0 * 1.0) * 1024)
+    assert e["source_digest"] == "abc" and e["dispatches"] == 3
+
+
+def test_stdp_xcd_choices_map_to_the_config_field(monkeypatch):
+    b = bench_module()
+    assert b.XCD_ARG == {"off": 0, "auto": 1, "2": 2, "4": 4, "8": 8}
+    for arg, want in (([], 0), (["--stdp-xcd", "auto"], 1), (["--stdp-xcd", "4"], 4)):
+        monkeypatch.setattr(sys, "argv", ["bench.py"] + arg)
+        assert b.XCD_ARG[b.parse().stdp_xcd] == want
