@@ -313,6 +313,7 @@ def main():
         sys.exit(2)
     import torch
     import workloads as wl
+    from workloads.presets import PLASTIC_EXC_EXC
     from paper_2107_04092_amd import snn
 
     p = wl.preset(args.config)
@@ -457,12 +458,17 @@ def main():
         # row count: targets and weights streamed (8 B per synapse), then
         # also every weight stored back (12 B per synapse); median of 5
         rows = max(1, int(round(st2["stdp_forced_rows"] / max(nrec, 1))))
-        meas = {}
-        for write in (False, True):
-            runs = sorted(net.probe_rows(rows, write=write, seed=q + 1) for q in range(5))
-            ms, syn = runs[2]
-            bps = 12 if write else 8
-            meas[write] = (syn * bps / (ms * 1e-3) / 1e9, ms)
+
+        def probe(r):
+            meas = {}
+            for write in (False, True):
+                runs = sorted(net.probe_rows(r, write=write, seed=q + 1) for q in range(5))
+                ms, syn = runs[2]
+                bps = 12 if write else 8
+                meas[write] = (syn * bps / (ms * 1e-3) / 1e9, ms)
+            return meas
+
+        meas = probe(rows)
         ceiling = {"kernel": "k_probe_rows", "rows": rows,
                    "read_GBs": round(meas[False][0], 1),
                    "read_frac": round(meas[False][0] / HBM_PEAK_GBS, 4),
@@ -470,6 +476,16 @@ def main():
                    "read_write_GBs": round(meas[True][0], 1),
                    "read_write_frac": round(meas[True][0] / HBM_PEAK_GBS, 4),
                    "read_write_us": round(meas[True][1] * 1e3, 2)}
+        # the same pattern at 2, 4, 8 and 16 times the rows (within the
+        # plastic rows): how far launch size alone moves the fraction
+        sweep = []
+        for mult in (2, 4, 8, 16):
+            r = min(rows * mult, p.n_exc if p.plastic == PLASTIC_EXC_EXC else p.n)
+            m = probe(r)
+            sweep.append({"rows": r, "read_frac": round(m[False][0] / HBM_PEAK_GBS, 4),
+                          "read_write_frac": round(m[True][0] / HBM_PEAK_GBS, 4),
+                          "read_write_us": round(m[True][1] * 1e3, 2)})
+        ceiling["sweep"] = sweep
 
     if args.copy_probe_mib > 0:
         nbytes = args.copy_probe_mib << 20
