@@ -278,6 +278,16 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
     const int line0 = lane & ~(kStoreLine - 1);  // first lane of this lane's store line
     const int gw = (bid * NT + tid) / kWave;
     const int nwv = nblocks * (NT / kWave);
+    // The prologue costs two round trips: first, together, the summary's
+    // staging loads (one round of eight 8-byte loads per thread holds 32 KB:
+    // the recency bitmap up to 262,144 neurons, the codes up to 32,768), the
+    // row count and the first two rows' snapshots (loaded from indices
+    // clamped to the snapshot array, kept only below the count); then the
+    // first two parts' targets and weights.
+    StageRegs<8, uint64_t> g_sum;
+    const int sum_words = a.code ? (a.n + 7) / 8 : a.recent ? a.nw : 0;
+    const uint64_t *sum_src = a.code ? (const uint64_t *)a.code : a.recent;
+    if (sum_words > 0) stage_issue<NT>(g_sum, sum_src, sum_words);
     const int64_t t = a.clk->t - 1;
     const int nrows = a.tx_rows ? *a.tx_cnt : a.row_cnt ? *a.row_cnt : a.n_rows_all;
     long long written = 0;
@@ -291,10 +301,11 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
     const int npairs = nrows * P;
     auto row_of = [&](int i) { return P == 1 ? i : i / P; };
     auto phase_of = [&](int i) { return P == 1 ? 0 : i % P; };
-    RowInfo cur = RowInfo{}, la = RowInfo{};
+    RowInfo cur = a.info[min(row_of(gw), a.n_info - 1)];
+    RowInfo la = a.info[min(row_of(gw + nwv), a.n_info - 1)];
     int cur_i = gw, la_i = gw + nwv;
-    if (cur_i < npairs) cur = a.info[row_of(cur_i)];
-    if (la_i < npairs) la = a.info[row_of(la_i)];
+    if (cur_i >= npairs) cur = RowInfo{};
+    if (la_i >= npairs) la = RowInfo{};
     int cur_base = -(int)(cur.rs & (kStoreLine - 1)) + phase_of(cur_i) * (U * kWave);
     auto issue = [&](RowPart<U> &p) {
         p.ri = cur;
@@ -312,17 +323,14 @@ __device__ __forceinline__ void stdp_rows_body(const StdpArgs &a, int bid, int n
             if (la_i < npairs) la = a.info[row_of(la_i)];
         }
     };
-    // the first two parts are in flight before the staging
+    // the first two parts go out before the staged words are stored
     RowPart<U> A, B;
     issue(A);
     issue(B);
     for (int q = tid; q <= kMaxAge; q += NT) s_dpow[q] = a.dpow[q];
     const uint8_t *s_code = s_sum;
     const uint64_t *s_recent = (const uint64_t *)s_sum;
-    if (a.code)
-        stage_lds<NT, 4>((uint4 *)s_sum, (const uint4 *)a.code, (a.n + 15) / 16);
-    else if (a.recent)
-        stage_lds<NT, 4>((uint64_t *)s_sum, a.recent, a.nw);
+    if (sum_words > 0) stage_finish<NT>((uint64_t *)s_sum, g_sum, sum_src, sum_words);
     __syncthreads();
 
     // Look-ups, update and stores of part p (the other part's loads are in

@@ -630,6 +630,7 @@ StdpArgs stdp_args(snn_ctx *c, bool flush, int64_t waves = 0)
     a.info = c->info;
     a.row_cnt = flush ? nullptr : c->row_cnt;
     a.n_rows_all = c->n_plastic_rows;
+    a.n_info = std::max<int32_t>(c->n_plastic_rows, 1);
     a.t_last = c->t_last;
     a.xpre = c->xpre;
     a.clk = c->clk;
@@ -836,6 +837,7 @@ snn_status launch_step_delivery(snn_ctx *c, int32_t mode)
         // bring the transmitting rows up to date first (row-wise, L2 gathers)
         StdpArgs r = stdp_args(c, false);
         r.info = c->txinfo;
+        r.n_info = c->n;
         r.tx_rows = 1;
         // transmitting rows: the row-wise form, gathering every target's
         // history and post trace (no summary staged)

@@ -174,6 +174,7 @@ struct StdpArgs {
     int32_t tx_rows;
     const int32_t *tx_cnt;
     int32_t n_rows_all;
+    int32_t n_info;  // entries of info (snapshot loads are clamped to it)
     int32_t *t_last;         // committed here: t_last = t, xpre = xp_now
     float *xpre;
     const StepClock *clk;    // t = clk->t - 1: the step whose neuron update ran last
