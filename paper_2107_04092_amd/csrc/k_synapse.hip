@@ -709,8 +709,8 @@ __device__ __forceinline__ void stdp_rows_xcd_body(const StdpArgs &a, int bid, i
         atomicAdd((unsigned long long *)(a.stats + bid), (unsigned long long)written);
 }
 
-// One instance per history length: the 128-step one keeps a second word per
-// synapse in registers and takes fewer synapses per lane and part.
+// One instance per history length: the 128-step one keeps a second history
+// word per gathered synapse in registers.
 template <int HW>
 __global__ __launch_bounds__(kStdpRowsBlock) void k_stdp_rows(StdpArgs a)
 {
