@@ -67,6 +67,11 @@ def parse():
                     help="plasticity algorithm (Fig. 2(c), (b), (a))")
     ap.add_argument("--stdp-xcd", choices=sorted(XCD_ARG), default="off",
                     help="forced rows partitioned over the XCDs by target range")
+    ap.add_argument("--plastic-blocks", default="on",
+                    help="plastic networks with D >= 2: on (blocks of up to D-1 steps), off "
+                         "(three parts per step) or the most steps per block")
+    ap.add_argument("--block-width", type=int, choices=[0, 64, 128, 256], default=0,
+                    help="targets per group of the plastic blocks (0: automatic)")
     ap.add_argument("--stdp-mult", type=int, default=0)
     ap.add_argument("--stdp-chunks", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -92,6 +97,18 @@ def parse():
 
 # --stdp-xcd: the config's stdp_xcd (0 off, 1 automatic, else the range count)
 XCD_ARG = {"off": 0, "auto": 1, "2": 2, "4": 4, "8": 8}
+
+
+def block_arg(v):
+    """--plastic-blocks: the config's plastic_blocks (0 on, -1 off, k at most k steps)."""
+    if v == "on":
+        return 0
+    if v == "off":
+        return -1
+    k = int(v)
+    if not 1 <= k <= 64:
+        raise ValueError("--plastic-blocks: on, off or 1..64")
+    return k
 
 _COMMENT = re.compile(r"//[^\n]*|/\*.*?\*/", re.S)
 
@@ -336,7 +353,9 @@ def main():
                                      args.plasticity),
                                  compressed_targets=(None if args.targets == "preset" else
                                                      int(args.targets == "16")),
-                                 stdp_xcd=XCD_ARG[args.stdp_xcd])
+                                 stdp_xcd=XCD_ARG[args.stdp_xcd],
+                                 plastic_blocks=block_arg(args.plastic_blocks),
+                                 plastic_block_width=args.block_width)
     t0 = time.time()
     net = snn.Network(cfg, stream=stream, device=dev)
     e = net.build_random(p.graph_kind, p.p_or_fanout, p.w_exc, p.w_inh)
@@ -528,6 +547,8 @@ def main():
             "plasticity": args.plasticity,
             "stdp_slice_mult": args.stdp_mult, "stdp_chunks": args.stdp_chunks,
             "stdp_xcd": args.stdp_xcd, "seed": p.seed,
+            "plastic_blocks": net.graph()["block_steps"],
+            "block_width": net.graph()["block_width"],
         },
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -167,6 +167,16 @@ typedef struct snn_config {
                              the plastic targets have fewer slices than
                              ranges or no range's codes fit. Same weights
                              either way */
+    int32_t plastic_blocks; /* plastic networks (lazy plasticity, slice
+                             delivery) with D >= 2 and n <= 65536: snn_step
+                             runs blocks of up to min(D-1, 16) steps, two
+                             launches per block, each workgroup owning a
+                             group of targets through the whole block (see
+                             snn_step). 0 = on; k > 0 = on, at most k steps
+                             per block; -1 = off (three parts per step).
+                             Same results either way */
+    int32_t plastic_block_width; /* targets per group of those blocks: 64, 128
+                             or 256, dividing slice_width; 0 = automatic */
     int32_t neuron_model; /* enum snn_neuron_model */
     int32_t plastic;      /* enum snn_plasticity */
     int32_t poisson_len;  /* entries used in poisson_cdf (0 = no external drive) */
@@ -237,6 +247,12 @@ typedef struct snn_graph_view {
     int32_t stdp_ranges;   /* target ranges the forced rows are split into
                               (stdp_xcd; 0 = whole rows), fixed when the
                               graph is bound */
+    int32_t block_steps;   /* most steps per plastic block of snn_step
+                              (plastic_blocks; 0 = steps run one by one) */
+    int32_t block_width;   /* targets per group of those blocks (0 = none) */
+    int32_t *block_pivots; /* n x (n / block_width rounded up, + 1),
+                              row-relative like pivots, at the group
+                              boundaries; NULL without blocks */
 } snn_graph_view;
 
 typedef struct snn_stats {
@@ -357,10 +373,20 @@ snn_status snn_advance(snn_ctx *ctx);
  * D >= 2 the inputs of up to D-1 steps (at most 16; 8 for CUBA) come from
  * spikes already in the delay ring, so one delivery launch computes them
  * all before one neuron launch runs those steps (Sec. I: the input of step
- * t depends on the spikes of step t-D only). Plastic networks run parts
- * (2) and (3) in one launch where its LDS leaves the forced rows at least
- * half a workgroup slot per CU beside the delivery work items: the forced
- * rows and the transmitting rows of a step are disjoint. */
+ * t depends on the spikes of step t-D only). Plastic networks with D >= 2
+ * and n <= 65536 (lazy plasticity, snn_config.plastic_blocks) run in blocks
+ * of up to D-1 steps (at most 16): the weight a row delivers at t depends
+ * only on spikes of its targets and on pre spikes that arrived by t (Sec.
+ * III-A: each synapse sees its pre spike D-1 steps after emission), so the
+ * rows to update and deliver at each step of the block are known when it
+ * starts, and one launch lists them, then one launch runs every step of
+ * the block with each workgroup owning a group of targets (their neuron
+ * update, and the plasticity and delivery of every listed row's synapses
+ * onto them); a last launch per call rebuilds the per-step lists. Other
+ * plastic networks run parts (2) and (3) in one launch where its LDS
+ * leaves the forced rows at least half a workgroup slot per CU beside the
+ * delivery work items: the forced rows and the transmitting rows of a step
+ * are disjoint. */
 snn_status snn_step(snn_ctx *ctx, int32_t n_steps, int32_t mode);
 
 /* snn_step for callers that cannot allocate device memory (code under HIP
@@ -416,7 +442,8 @@ snn_status snn_probe_rows(snn_ctx *ctx, int32_t n_rows, int32_t write, uint64_t 
  * source from the device (see Time above) and makes no allocation or memset,
  * so each replay (snn_graph_launch) runs the next n_steps steps and equals
  * snn_step(ctx, n_steps, mode) there. The path a step takes (small
- * networks, delay blocks, the fused pass) is fixed at capture. *out (host)
+ * networks, delay blocks, plastic blocks, the fused pass) is fixed at
+ * capture. *out (host)
  * receives the handle, owned by the caller (snn_graph_destroy); it stays
  * valid while the context and its buffers do. SNN_EINVAL for n_steps < 1 or
  * a context on the null stream (HIP cannot capture it); SNN_ESTATE while

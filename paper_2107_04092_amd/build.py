@@ -13,7 +13,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libsnn.so")
 SOURCES = [os.path.join(CSRC, f) for f in ("k_neuron.hip", "k_synapse.hip", "k_graph.hip",
-                                          "snn_api.hip")]
+                                          "k_block.hip", "snn_api.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

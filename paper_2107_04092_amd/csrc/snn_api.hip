@@ -120,6 +120,14 @@ struct snn_ctx {
     bool fuse = false;  // plastic: parts (2) and (3) of snn_step in one launch
     int32_t fuse_slots = 0;  // workgroups of the fused pass resident at once
     long long *abatch = nullptr;  // [batch_max][C][nacc][n]
+    // plastic blocks (BlockArgs): most steps per block (0: off), targets per
+    // group and groups; the group pivots (graph buffer), the plan's lists
+    // and counts and the block clock (workspace)
+    int32_t pb_max = 0, pb_width = 0, pb_groups = 0;
+    int32_t *gpiv = nullptr;
+    RowInfo *pev = nullptr;
+    int32_t *pev_cnt = nullptr;
+    BlockClock *bclk = nullptr;
 
     // graph
     uint8_t *g = nullptr;
@@ -209,6 +217,14 @@ snn_status validate(snn_ctx *c, const snn_config &k)
     if (k.stdp_xcd != 0 && k.stdp_xcd != 1 && k.stdp_xcd != 2 && k.stdp_xcd != 4 &&
         k.stdp_xcd != 8)
         return fail(c, SNN_EINVAL, "stdp_xcd must be 0, 1, 2, 4 or 8");
+    if (k.plastic_blocks < -1 || k.plastic_blocks > SNN_MAX_DELAY)
+        return fail(c, SNN_EINVAL, "plastic_blocks must be in [-1, 64]");
+    if (k.plastic_block_width != 0 &&
+        ((k.plastic_block_width != 64 && k.plastic_block_width != 128 &&
+          k.plastic_block_width != 256) ||
+         k.slice_width % k.plastic_block_width != 0))
+        return fail(c, SNN_EINVAL,
+                    "plastic_block_width must be 0, or 64, 128 or 256 dividing slice_width");
     if (k.stdp_filter == 1 && (int64_t)k.n + 16 > kCodeMax)
         return fail(c, SNN_EINVAL, "stdp_filter 1 needs n + 16 <= %d", kCodeMax);
     if (k.stdp_filter == 2 && (k.n + 63) / 64 > kRecentMaxWords)
@@ -342,6 +358,30 @@ void derive(snn_ctx *c)
         if (bb > c->dlv_slots) c->dlv_slots = (int32_t)bb;
     }
     c->info_blocks = c->nblk;  // statistics slots of the neuron-kernel / flush snapshots
+    // Plastic blocks (BlockArgs) of up to D-1 steps (at most kBatchMax): lazy
+    // plasticity, D >= 2, up to kPbMaxN neurons. Target groups of 256, 128
+    // or 64 neurons inside slices: the widest that still gives every CU about
+    // one and a half groups, else 64.
+    c->pb_max = c->pb_width = c->pb_groups = 0;
+    if (c->n_plastic_rows > 0 && c->algo != 2 && c->delay >= 2 && k.n <= kPbMaxN &&
+        k.plastic_blocks >= 0) {
+        int32_t bm = std::min<int32_t>(c->delay - 1, kBatchMax);
+        if (k.plastic_blocks > 0) bm = std::min<int32_t>(bm, k.plastic_blocks);
+        int32_t gw = k.plastic_block_width;
+        if (gw == 0) {
+            gw = 64;
+            for (int cand : {256, 128}) {
+                if (k.slice_width % cand == 0 &&
+                    2 * (((int64_t)k.n + cand - 1) / cand) >= 3 * (int64_t)c->n_cu) {
+                    gw = cand;
+                    break;
+                }
+            }
+        }
+        c->pb_max = bm;
+        c->pb_width = gw;
+        c->pb_groups = (k.n + gw - 1) / gw;
+    }
 }
 
 // Workspace plan: a bump allocator over the caller's buffer.
@@ -399,6 +439,9 @@ void plan_workspace(snn_ctx *c, uint8_t *base)
     c->syn_stats = p.take<int64_t>(c->syn_slots);
     c->dlv_stats = p.take<int64_t>(2 * (int64_t)c->dlv_slots);
     c->abatch = p.take<long long>(c->batch_max > 0 ? (int64_t)c->batch_max * c->nacc * n : 1);
+    c->pev = p.take<RowInfo>(c->pb_max > 0 ? (int64_t)c->pb_max * n : 1);
+    c->pev_cnt = p.take<int32_t>(kBatchMax);
+    c->bclk = p.take<BlockClock>(1);
     c->ws_need = p.off;
 }
 
@@ -457,6 +500,14 @@ snn_status finish_graph(snn_ctx *c)
     GraphArgs a = graph_args(c);
     snn_status st = check_hip(c, launch_pivots(c->stream, a), "pivot kernel");
     if (st) return st;
+    if (c->pb_max > 0) {  // pivots at the target groups of the plastic blocks
+        GraphArgs ga = a;
+        ga.piv = c->gpiv;
+        ga.width = c->pb_width;
+        ga.n_slices = c->pb_groups;
+        st = check_hip(c, launch_pivots(c->stream, ga), "group pivot kernel");
+        if (st) return st;
+    }
     if (c->ct) {
         st = check_hip(c, launch_encode_targets(c->stream, a, c->n_edges), "target compression");
         if (st) return st;
@@ -573,6 +624,62 @@ NeuronArgs neuron_args(snn_ctx *c)
     a.seed = c->cfg.seed;
     for (int q = 0; q < kMaxPoisson; ++q) a.poisson[q] = c->cfg.poisson_cdf[q];
     return a;
+}
+
+BlockArgs block_args(snn_ctx *c, int32_t steps)
+{
+    BlockArgs b{};
+    b.row_ptr = c->row_ptr;
+    b.pend = c->pend;
+    b.hist = c->hist;
+    b.t_last = c->t_last;
+    b.xpre = c->xpre;
+    b.status = c->status;
+    b.status_stride = c->status_stride;
+    b.status_words = c->status_words;
+    b.ev = c->pev;
+    b.ev_cnt = c->pev_cnt;
+    b.bclk = c->bclk;
+    b.clk = c->clk;
+    b.info_stats = c->info_stats;
+    b.info_slots = c->info_blocks;
+    b.err = c->err_flag;
+    b.steps = steps;
+    b.n = c->n;
+    b.n_exc = c->cfg.n_exc;
+    b.n_plastic_rows = c->n_plastic_rows;
+    b.hw = c->hw;
+    b.delay = c->delay;
+    b.nacc = c->nacc;
+    b.col = c->col;
+    b.col16 = c->ct ? c->col16 : nullptr;
+    b.w = c->w;
+    b.gpiv = c->gpiv;
+    b.n_edges = c->n_edges;
+    b.gwidth = c->pb_width;
+    b.width = c->cfg.slice_width;
+    b.n_groups = c->pb_groups;
+    b.apart = c->apart;
+    b.part_stride = (int64_t)c->nacc * c->n;
+    b.dlv_stats = c->dlv_stats;
+    b.dlv_slots = c->dlv_slots;
+    b.syn_stats = c->syn_stats;
+    b.syn_slots = c->syn_slots;
+    b.gstats = c->gstats;
+    b.event = c->algo == 0 ? 1 : 0;
+    b.c_pot = c->c_pot;
+    b.c_dep = c->c_dep;
+    b.mu = c->mu;
+    b.ring = c->ring;
+    b.ring_cnt = c->ring_cnt;
+    b.spk_pos = c->spk_pos;
+    b.rows = c->rows;
+    b.row_cnt = c->row_cnt;
+    b.mask = c->mask;
+    b.txmask = c->txmask;
+    b.recent = c->recent;
+    for (int q = 0; q <= kMaxAge; ++q) b.dpow[q] = c->dpow[q];
+    return b;
 }
 
 snn_status launch_step_neurons(snn_ctx *c)
@@ -1090,7 +1197,8 @@ snn_status snn_graph_size(const snn_ctx *c, int64_t n_edges, size_t *bytes)
     if (!c || !bytes || n_edges < 0) return SNN_EINVAL;
     *bytes = (c->algo == 2 ? 4 : 2) * align_up((size_t)n_edges * sizeof(int32_t)) +
              align_up((size_t)c->n * (size_t)(c->n_slices + 1) * 4) +
-             (c->ct ? align_up((size_t)n_edges * sizeof(uint16_t)) : 0);
+             (c->ct ? align_up((size_t)n_edges * sizeof(uint16_t)) : 0) +
+             (c->pb_max > 0 ? align_up((size_t)c->n * (size_t)(c->pb_groups + 1) * 4) : 0);
     return SNN_OK;
 }
 
@@ -1119,7 +1227,10 @@ snn_status snn_bind_graph(snn_ctx *c, void *device_ptr, size_t bytes, int64_t n_
     const size_t pivb = align_up((size_t)c->n * (size_t)(c->n_slices + 1) * 4);
     c->sx_pre = c->algo == 2 ? (float *)(c->g + 2 * arr + pivb) : nullptr;
     c->sx_post = c->algo == 2 ? (float *)(c->g + 3 * arr + pivb) : nullptr;
+    const size_t ctb = c->ct ? align_up((size_t)n_edges * sizeof(uint16_t)) : 0;
     c->col16 = c->ct ? (uint16_t *)(c->g + (c->algo == 2 ? 4 : 2) * arr + pivb) : nullptr;
+    c->gpiv = c->pb_max > 0 ? (int32_t *)(c->g + (c->algo == 2 ? 4 : 2) * arr + pivb + ctb)
+                            : nullptr;
     if (c->graph_state != 1) c->counted_kind = -1;
     c->graph_state = 2;
     return SNN_OK;
@@ -1316,6 +1427,28 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
         q += B;
     }
     if (blocks) return SNN_OK;
+    // a plastic network with D >= 2 runs in blocks of up to D-1 steps (see
+    // BlockArgs): the plan, then the run of the block, and after the last
+    // block the per-step lists
+    const bool pblocks = mode == SNN_DELIVER_LDS_SLICE && c->pb_max > 0 && c->t_used >= c->t_cap;
+    if (pblocks && n_steps > 0) {
+        const NeuronArgs a = neuron_args(c);
+        for (int32_t q = 0; q < n_steps;) {
+            const int32_t B = std::min<int32_t>(n_steps - q, c->pb_max);
+            const BlockArgs b = block_args(c, B);
+            if ((st = check_hip(c, launch_block_plan(c->stream, b), "plastic block plan")))
+                return st;
+            if ((st = check_hip(c, launch_block_run(c->stream, a, b), "plastic block run")))
+                return st;
+            c->t += B;
+            q += B;
+        }
+        if ((st = check_hip(c, launch_block_finish(c->stream, block_args(c, 1)),
+                            "plastic block lists")))
+            return st;
+        c->last_neuron_t = c->last_deliver_t = c->t - 1;
+        return SNN_OK;
+    }
     // parts (2) and (3) of plastic networks in one launch where it fits
     // (kernel timing records it as the delivery part)
     const bool fuse = mode == SNN_DELIVER_LDS_SLICE && c->fuse;
@@ -1559,6 +1692,9 @@ snn_status snn_get_graph(const snn_ctx *c, snn_graph_view *out)
     out->plastic_end = c->pend;
     out->col16 = c->col16;
     out->stdp_ranges = c->xcd ? c->xparts : 0;
+    out->block_steps = c->pb_max;
+    out->block_width = c->pb_width;
+    out->block_pivots = c->gpiv;
     return SNN_OK;
 }
 

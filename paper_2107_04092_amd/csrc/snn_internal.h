@@ -323,6 +323,90 @@ constexpr int kBatchMax = 16;  // steps per delay block
 constexpr int batch_steps_max(int m) { return m == 1 ? kBatchMax / 2 : kBatchMax; }
 constexpr int64_t kBatchBytes = 256ll << 20;  // most workspace for a block's partial inputs
 
+// Blocks of steps of a plastic network with D >= 2 (k_block_plan, then
+// k_block_run). Delivery at step t sends the spikes emitted at t-D+1, and
+// the weight of synapse k->j at t depends only on the pre spikes of k that
+// arrived by t (emitted by t-D+1) and on the post spikes of j. So the rows
+// to bring up to date and to deliver at each of the steps t0 .. t0+B-1
+// (B <= D-1) follow from the histories when t0 starts, and a workgroup that
+// owns a range of targets can run all B steps alone: the neuron update of
+// its targets, then the plasticity and delivery of every listed row's
+// entries that fall in its range, into an accumulator in LDS that its next
+// neuron update reads. No workgroup waits for another within the block.
+//   The plan (one thread per row) walks each row through the block's steps
+// as the neuron update would (transmitting: history bit D-1 of the step;
+// forced: idle for 64 hw steps) and writes each step's list of row
+// snapshots (RowInfo; pad bit 0: transmitting, bit 1: the row was brought
+// up to date at the step before too), ascending, by one
+// decoupled look-back per step; it commits t_last and x_pre after the block.
+// The targets are cut into groups of gwidth neurons inside slices, and each
+// row's entries per group are found from a pivot table at group
+// granularity (gpiv[k][g] = the row-relative first entry of row k with a
+// target >= g gwidth, g = 0..n_groups; the pivot kernel with gwidth for
+// the slice width). After the last block of a call,
+// k_block_finish rebuilds from the histories what the step-by-step path
+// keeps per step: the delay-ring lists of the last D steps with their
+// positions, the masks and forced-row list of the last step; and clears
+// the list scans' status words.
+struct BlockClock {
+    long long t0;          // the block's first step
+    int32_t input_forced;  // the input of step t0, as the step clock said
+    int32_t n_parts;
+    long long pad_[2];
+};
+constexpr int kPbPlanBlock = 512;   // threads of the plan (one row each, a half wave per step's scan)
+constexpr int kPbBlock = 256;       // threads of a target group's workgroup
+constexpr int kPbMaxWidth = 256;    // most targets per group (one neuron per thread)
+constexpr int kPbRounds = 2;        // row snapshots each thread stages per batch
+constexpr int kPbBatch = kPbBlock * kPbRounds;
+constexpr int kPbUnroll = 8;        // flattened entries per thread per window
+constexpr int kPbWindow = kPbBlock * kPbUnroll;
+constexpr int kPbMaxN = 65536;      // largest network the blocks run
+static_assert(kPbPlanBlock / 32 >= kBatchMax, "a half wave per step's list scan");
+static_assert(kPbBatch < 65535, "16-bit segment map");
+struct BlockArgs {
+    // plan
+    const int64_t *row_ptr;
+    const int32_t *pend;
+    const uint64_t *hist;
+    int32_t *t_last;
+    float *xpre;
+    unsigned long long *status;  // [kBatchMax][status_stride] look-back words
+    int32_t status_stride;
+    RowInfo *ev;                 // [kBatchMax][n]: step k's rows at ev + k n
+    int32_t *ev_cnt;             // [kBatchMax]
+    BlockClock *bclk;            // written by the plan, read by the run
+    StepClock *clk;              // read by the plan, advanced by the run
+    int64_t *info_stats;         // plan: rows, forced rows, synapses (kStFields per slot)
+    int32_t info_slots;
+    int32_t *err;
+    int32_t steps, n, n_exc, n_plastic_rows, hw, delay, nacc;
+    // run
+    const int32_t *col;
+    const uint16_t *col16;       // compressed targets (slice-local), or nullptr
+    float *w;
+    const int32_t *gpiv;         // [n][n_groups + 1]
+    int64_t n_edges;             // (entry indices are clamped to the graph)
+    int32_t gwidth, width, n_groups;
+    long long *apart;            // partial 0 receives the input of step t0 + B
+    int64_t part_stride;
+    int64_t *dlv_stats;          // [dlv_slots][2]: events delivered, weights written (transmitting rows)
+    int32_t dlv_slots;
+    int64_t *syn_stats;          // [syn_slots]: weights written (forced rows)
+    int32_t syn_slots;
+    int64_t *gstats;
+    int32_t event;               // 1: replay only the set history bits; 0: every step
+    float c_pot, c_dep, mu;
+    // finish
+    int32_t *ring, *ring_cnt, *spk_pos, *rows, *row_cnt;
+    uint64_t *mask, *txmask, *recent;
+    int32_t status_words;
+    float dpow[kMaxAge + 1];
+};
+hipError_t launch_block_plan(hipStream_t s, const BlockArgs &b);
+hipError_t launch_block_run(hipStream_t s, const NeuronArgs &a, const BlockArgs &b);
+hipError_t launch_block_finish(hipStream_t s, const BlockArgs &b);
+
 // Optional events placed by a launch itself around the kernel
 // (hipExtLaunchKernelGGL): its device time without marker or dispatch gaps.
 struct KernelEvents {

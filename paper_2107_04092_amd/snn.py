@@ -35,7 +35,7 @@ class snn_config(ctypes.Structure):
         ("spike_chunks", _i32), ("stdp_slice_mult", _i32), ("stdp_chunks", _i32),
         ("stdp_layout", _i32), ("stdp_filter", _i32), ("history_bits", _i32),
         ("plasticity_algorithm", _i32), ("compressed_targets", _i32), ("stdp_xcd", _i32),
-        ("neuron_model", _i32),
+        ("plastic_blocks", _i32), ("plastic_block_width", _i32), ("neuron_model", _i32),
         ("plastic", _i32), ("poisson_len", _i32),
         ("dt_ms", _f64), ("tau_m_ms", _f64), ("v_th", _f64), ("v_reset", _f64),
         ("v_inf", _f64), ("tau_ref_ms", _f64), ("tau_e_ms", _f64), ("tau_i_ms", _f64),
@@ -55,7 +55,8 @@ class snn_state_view(ctypes.Structure):
 class snn_graph_view(ctypes.Structure):
     _fields_ = [("n_edges", _i64), ("n_slices", _i32), ("row_ptr", _P),
                 ("col", _P), ("w", _P), ("pivots", _P), ("plastic_end", _P), ("col16", _P),
-                ("stdp_ranges", _i32)]
+                ("stdp_ranges", _i32), ("block_steps", _i32), ("block_width", _i32),
+                ("block_pivots", _P)]
 
 
 class snn_stats(ctypes.Structure):
@@ -283,7 +284,7 @@ def snn_get_kernel_times(ctx):
 def config_from_preset(p, poisson_table=(), slice_width=None, spike_chunks=None,
                        stdp_slice_mult=0, stdp_chunks=0, stdp_layout=0, stdp_filter=0,
                        history_bits=64, plasticity_algorithm=0, compressed_targets=None,
-                       stdp_xcd=0):
+                       stdp_xcd=0, plastic_blocks=0, plastic_block_width=0):
     """snn_config from a preset-like object with the physical parameters."""
     c = snn_config()
     c.n, c.n_exc, c.delay_steps = p.n, p.n_exc, p.delay
@@ -297,6 +298,7 @@ def config_from_preset(p, poisson_table=(), slice_width=None, spike_chunks=None,
     c.compressed_targets = (getattr(p, "compressed_targets", 0) if compressed_targets is None
                             else compressed_targets)
     c.stdp_xcd = stdp_xcd
+    c.plastic_blocks, c.plastic_block_width = plastic_blocks, plastic_block_width
     c.neuron_model, c.plastic = p.model, p.plastic
     c.dt_ms, c.tau_m_ms, c.v_th, c.v_reset, c.v_inf = p.dt, p.tau_m, p.v_th, p.v_reset, p.v_inf
     c.tau_ref_ms, c.tau_e_ms, c.tau_i_ms = p.tau_ref, p.tau_e, p.tau_i
@@ -489,4 +491,8 @@ class Network:
             "plastic_end": self._view(self.ws, v.plastic_end, n, torch.int32),
             "col16": (self._view(self.g, v.col16, e, torch.int16) if v.col16 else None),
             "stdp_ranges": v.stdp_ranges,
+            "block_steps": v.block_steps, "block_width": v.block_width,
+            "block_pivots": (self._view(self.g, v.block_pivots,
+                                        n * ((n + v.block_width - 1) // v.block_width + 1),
+                                        torch.int32) if v.block_pivots else None),
         }

@@ -73,6 +73,10 @@ def test_struct_layouts_match_header(tmp_path):
     ("plasticity_algorithm", 3, "plasticity_algorithm"),
     ("history_bits", 96, "history_bits"),
     ("compressed_targets", 2, "compressed_targets"),
+    ("plastic_blocks", -2, "plastic_blocks"),
+    ("plastic_blocks", 65, "plastic_blocks"),
+    ("plastic_block_width", 96, "plastic_block_width"),
+    ("plastic_block_width", 512, "plastic_block_width"),
     ("poisson_len", 33, "poisson_len"),
     ("dt_ms", float("nan"), "NaN"),
     ("tau_m_ms", 0.0, "tau_m_ms"),
@@ -98,6 +102,10 @@ def test_create_rejects_bad_stdp_and_cuba_config():
     cfg = snn.config_from_preset(wl.preset("stress"))
     cfg.p_fire = 1.5
     with pytest.raises(snn.SnnError, match="p_fire"):
+        snn.snn_create(cfg, 0)
+    cfg = snn.config_from_preset(wl.preset("brunel_plus"), slice_width=320)
+    cfg.plastic_block_width = 128  # target groups must tile the slices
+    with pytest.raises(snn.SnnError, match="plastic_block_width"):
         snn.snn_create(cfg, 0)
 
 

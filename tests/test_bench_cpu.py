@@ -142,3 +142,14 @@ def test_stdp_xcd_choices_map_to_the_config_field(monkeypatch):
     for arg, want in (([], 0), (["--stdp-xcd", "auto"], 1), (["--stdp-xcd", "4"], 4)):
         monkeypatch.setattr(sys, "argv", ["bench.py"] + arg)
         assert b.XCD_ARG[b.parse().stdp_xcd] == want
+
+
+def test_plastic_block_choices_map_to_the_config_field(monkeypatch):
+    b = bench_module()
+    for arg, want in (([], 0), (["--plastic-blocks", "off"], -1),
+                      (["--plastic-blocks", "5"], 5)):
+        monkeypatch.setattr(sys, "argv", ["bench.py"] + arg)
+        assert b.block_arg(b.parse().plastic_blocks) == want
+    for bad in ("0", "65", "x"):
+        with pytest.raises(ValueError):
+            b.block_arg(bad)

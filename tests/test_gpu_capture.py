@@ -23,7 +23,8 @@ LDS, GLOBAL = snn.SNN_DELIVER_LDS_SLICE, snn.SNN_DELIVER_GLOBAL_ATOMIC
 
 CASES = [
     # name, preset overrides, slice width, chunks, mode: one path of snn_step each
-    ("stress", dict(n=3000, p_or_fanout=100, p_fire=0.03, delay=3), 512, 2, LDS),   # fused pass
+    ("stress", dict(n=3000, p_or_fanout=100, p_fire=0.03, delay=3), 512, 2, LDS),   # plastic blocks
+    ("stress", dict(n=3000, p_or_fanout=100, p_fire=0.03, delay=3, blocks=-1), 512, 2, LDS),  # fused pass
     ("stress", dict(n=3000, p_or_fanout=100, p_fire=0.03), 512, 1, GLOBAL),         # global atomics
     ("vogels", dict(n=3000, n_exc=2400, plastic=PLASTIC_EXC_EXC, w0=0.05), 512, 2, LDS),
     ("brunel", dict(n=5000, n_exc=4000), 1024, 2, LDS),                              # delay blocks
@@ -47,17 +48,20 @@ def _same_state(a, b, what):
         assert np.array_equal(ra[q, :c], rb[q, :c]), (what, "ring slot", q)
 
 
-@pytest.mark.parametrize("case", CASES, ids=lambda c: "%s-d%d-m%d" % (
-    c[0], c[1].get("delay", 1 if c[0] != "brunel" else 15), c[4]))
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "%s-d%d-m%d%s" % (
+    c[0], c[1].get("delay", 1 if c[0] != "brunel" else 15), c[4],
+    "-stepwise" if c[1].get("blocks") == -1 else ""))
 def test_captured_step_replays_equal_eager_steps(case):
     import torch
     name, kw, width, chunks, mode = case
+    kw = dict(kw)
+    cfg = dict(plastic_blocks=kw.pop("blocks", 0))
     p = wl.preset(name, **kw)
-    log("capture %s %s W=%d C=%d mode=%d" % (name, kw, width, chunks, mode))
+    log("capture %s %s W=%d C=%d mode=%d %s" % (name, kw, width, chunks, mode, cfg))
     side = torch.cuda.Stream()
-    a = gpu_net(p, width, chunks, stream=side)      # captured step, replayed
-    b = gpu_net(p, width, chunks)                   # eager, one step at a time
-    c = gpu_net(p, width, chunks)                   # eager, one call of 100 steps
+    a = gpu_net(p, width, chunks, stream=side, **cfg)  # captured step, replayed
+    b = gpu_net(p, width, chunks, **cfg)               # eager, one step at a time
+    c = gpu_net(p, width, chunks, **cfg)               # eager, one call of 100 steps
     for net in (a, b, c):
         net.step(3, mode)
     g = a.capture(1, mode)

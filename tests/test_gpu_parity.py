@@ -37,19 +37,26 @@ CASES = [
 ]
 
 
+@pytest.mark.parametrize("blocks", [0, -1], ids=["", "stepwise"])
 @pytest.mark.parametrize("hbits", [64, 128], ids=["h64", "h128"])
 @pytest.mark.parametrize("mode,layout,filt", [(LDS, 0, 1), (LDS, 0, 2), (LDS, 1, 0),
                                               (GLOBAL, 0, 3)],
                          ids=["lds-rowstdp-codes", "lds-rowstdp-bitmap", "lds-slicestdp",
                               "global-rowstdp-gather"])
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "%s-%s" % (c[0], c[1].get("n", "")))
-def test_teacher_forced_parity(case, mode, layout, filt, hbits):
+def test_teacher_forced_parity(case, mode, layout, filt, hbits, blocks):
+    """blocks: plastic networks with D >= 2 run steps of snn_step as blocks
+    (of one step here) unless switched off ("stepwise": three parts per
+    step, which the other networks always take)."""
     name, kw, steps, width, chunks = case
     p = wl.preset(name, **kw)
-    log("parity %s %s mode=%d layout=%d filter=%d history=%d W=%d C=%d steps=%d" % (
-        name, kw, mode, layout, filt, hbits, width, chunks, steps))
+    if blocks == -1 and (p.plastic == PLASTIC_NONE or p.delay < 2 or mode != LDS):
+        pytest.skip("the same steps as without the switch: no blocks here")
+    log("parity %s %s mode=%d layout=%d filter=%d history=%d W=%d C=%d steps=%d blocks=%d" % (
+        name, kw, mode, layout, filt, hbits, width, chunks, steps, blocks))
     net, o, cnt = teacher_forced_run(p, steps, mode, slice_width=width, spike_chunks=chunks,
-                                     stdp_layout=layout, stdp_filter=filt, history_bits=hbits)
+                                     stdp_layout=layout, stdp_filter=filt, history_bits=hbits,
+                                     plastic_blocks=blocks)
     assert cnt["spikes"] > 0
     if p.plastic != PLASTIC_NONE:
         assert cnt["rows"] > 0 and cnt["weights"] > 0
