@@ -155,19 +155,23 @@ def test_brunel_full_size_delay_block():
     log("  block checked: %d spiking rows, %d events" % (len(rows), events))
 
 
-def test_brunel_plus_full_size_teacher_forced():
+@pytest.mark.parametrize("blocks", [0, -1], ids=["blocks", "stepwise"])
+def test_brunel_plus_full_size_teacher_forced(blocks):
     """Brunel with STDP at its stated size (25,000 LIF neurons with Poisson
     drive, p = 0.1: 62.5M synapses, STDP on the 40M exc->exc ones, D = 15)
     in the benchmark's launch configuration (W = 1024, four chunks, 16-bit
-    slice-local targets, the fused synapse pass). 150 teacher-forced steps:
-    every step spikes, histories, potentials and refractory counts are
-    bit-exact, the delivered input is within tolerance, and so are the weights
-    of every row made current (forced rows from step 63 on, transmitting rows
-    from step 14 on); after a flush, every plastic weight."""
+    slice-local targets), each step a block of one step (plan and target
+    groups) or the three parts with the fused synapse pass. 150
+    teacher-forced steps: every step spikes, histories, potentials and
+    refractory counts are bit-exact, the delivered input is within
+    tolerance, and so are the weights of every row made current (forced
+    rows from step 63 on, transmitting rows from step 14 on); after a flush,
+    every plastic weight."""
     p = wl.preset("brunel_plus")
-    log("full-size brunel_plus: n=%d p=%g D=%d W=%d C=%d" % (
-        p.n, p.p_or_fanout, p.delay, p.slice_width, p.spike_chunks))
-    net, o, cnt = teacher_forced_run(p, 150, snn.SNN_DELIVER_LDS_SLICE, progress=25)
+    log("full-size brunel_plus: n=%d p=%g D=%d W=%d C=%d blocks=%d" % (
+        p.n, p.p_or_fanout, p.delay, p.slice_width, p.spike_chunks, blocks))
+    net, o, cnt = teacher_forced_run(p, 150, snn.SNN_DELIVER_LDS_SLICE, progress=25,
+                                     plastic_blocks=blocks)
     log("  %d rows, %d weights, %d spikes checked" % (cnt["rows"], cnt["weights"], cnt["spikes"]))
     assert cnt["spikes"] > 0 and cnt["rows"] > 0 and cnt["weights"] > 0
     st = net.stats()
@@ -200,3 +204,21 @@ def test_brunel_plus_full_size_free_running_rate():
     assert net.stats()["device_errors"] == 0
     assert r >= 100_000
     assert abs(rg - ro) <= 0.02 * ro
+
+
+def test_brunel_plus_full_size_blocks_equal_stepwise():
+    """The benchmark's Brunel+ network (62.5M synapses) run 300 steps in
+    blocks of 14 and step by step: every state array, delay-ring list,
+    weight and statistic bit for bit."""
+    from test_gpu_blocks import same_state
+    p = wl.preset("brunel_plus")
+    a = gpu_net(p)
+    assert a.graph()["block_steps"] == 14
+    a.step(300, snn.SNN_DELIVER_LDS_SLICE)
+    a.synchronize()
+    b = gpu_net(p, plastic_blocks=-1)
+    b.step(300, snn.SNN_DELIVER_LDS_SLICE)
+    log("  300 steps each: %d spikes, %d forced rows" % (a.stats()["spikes"],
+                                                        a.stats()["stdp_forced_rows"]))
+    same_state(a, b, "full-size brunel_plus")
+    assert a.stats()["stdp_forced_rows"] > 0

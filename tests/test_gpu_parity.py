@@ -37,21 +37,31 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("blocks", [0, -1], ids=["", "stepwise"])
+MODES = [((LDS, 0, 1), "lds-rowstdp-codes"), ((LDS, 0, 2), "lds-rowstdp-bitmap"),
+         ((LDS, 1, 0), "lds-slicestdp"), ((GLOBAL, 0, 3), "global-rowstdp-gather")]
+
+
+def _parity_params():
+    """Every case in every mode; plastic networks with D >= 2 in the slice
+    mode run snn_step's steps as blocks (of one step here), so they run once
+    more with the blocks switched off (three parts per step)."""
+    out = []
+    for case in CASES:
+        p = wl.preset(case[0], **case[1])
+        for (mode, layout, filt), mname in MODES:
+            both = p.plastic != PLASTIC_NONE and p.delay >= 2 and mode == LDS
+            for blocks in ([0, -1] if both else [0]):
+                cid = "%s-%s-%s%s" % (case[0], case[1].get("n", ""), mname,
+                                      "-stepwise" if blocks == -1 else "")
+                out.append(pytest.param(case, mode, layout, filt, blocks, id=cid))
+    return out
+
+
 @pytest.mark.parametrize("hbits", [64, 128], ids=["h64", "h128"])
-@pytest.mark.parametrize("mode,layout,filt", [(LDS, 0, 1), (LDS, 0, 2), (LDS, 1, 0),
-                                              (GLOBAL, 0, 3)],
-                         ids=["lds-rowstdp-codes", "lds-rowstdp-bitmap", "lds-slicestdp",
-                              "global-rowstdp-gather"])
-@pytest.mark.parametrize("case", CASES, ids=lambda c: "%s-%s" % (c[0], c[1].get("n", "")))
+@pytest.mark.parametrize("case,mode,layout,filt,blocks", _parity_params())
 def test_teacher_forced_parity(case, mode, layout, filt, hbits, blocks):
-    """blocks: plastic networks with D >= 2 run steps of snn_step as blocks
-    (of one step here) unless switched off ("stepwise": three parts per
-    step, which the other networks always take)."""
     name, kw, steps, width, chunks = case
     p = wl.preset(name, **kw)
-    if blocks == -1 and (p.plastic == PLASTIC_NONE or p.delay < 2 or mode != LDS):
-        pytest.skip("the same steps as without the switch: no blocks here")
     log("parity %s %s mode=%d layout=%d filter=%d history=%d W=%d C=%d steps=%d blocks=%d" % (
         name, kw, mode, layout, filt, hbits, width, chunks, steps, blocks))
     net, o, cnt = teacher_forced_run(p, steps, mode, slice_width=width, spike_chunks=chunks,
