@@ -17,10 +17,10 @@ namespace {
 // plastic row is brought up to date when it transmits, or, idle, once its
 // last update is 64 hw steps old (forced), exactly as the step-by-step
 // neuron update decides; each such event is a snapshot of the row at its
-// step (RowInfo), taken from the t_last and x_pre that the row's earlier
-// events in the block left. The steps are walked twice: once for the event
-// flags (each step's counts, scanned over the workgroups by a decoupled
-// look-back, one scan per step), then for the snapshots, written at their
+// step, taken from the t_last and x_pre that the row's earlier events in the
+// block left. The steps are walked twice: once for the event flags (each
+// step's counts, scanned over the workgroups by a decoupled look-back, one
+// scan per step), then for the snapshots (PbEvent), written at their
 // positions in the step's ascending list.
 
 __global__ __launch_bounds__(kPbPlanBlock) void k_block_plan(BlockArgs b)
@@ -119,17 +119,20 @@ __global__ __launch_bounds__(kPbPlanBlock) void k_block_plan(BlockArgs b)
                 }
             }
         }
-        if (!ok) {  // nothing to bring up to date: the row is only delivered
-            ri = RowInfo{};
-            ri.k = k;
-            ri.rs = rs;
-        }
-        ri.pad = tx;
+        // nothing to bring up to date (ok == 0): the row is only delivered
+        PbEvent pe;
+        pe.rs = (int32_t)rs;
+        pe.lenf = ok ? ((uint32_t)ri.len & 0xffffu) | ((uint32_t)(ri.age_pre & 0xff) << 16) |
+                           ((uint32_t)((ri.age_pre >> 8) & 1) << 24)
+                     : 0u;
+        pe.lenf |= ((uint32_t)tx << 25) | ((uint32_t)(b.nacc == 2 && k >= b.n_exc) << 26);
+        pe.xp0 = ok ? ri.xp0 : 0.f;
+        pe.k = k;
         int pos = s_lb[2 * q] + __popcll(s_m[q][wave] & below);
         for (int w = 0; w < wave; ++w) pos += __popcll(s_m[q][w]);
         // (only a failed scan puts a position out of range)
         if (pos < b.n)
-            b.ev[(int64_t)q * b.n + pos] = ri;
+            b.ev[(int64_t)q * b.n + pos] = pe;
         else
             atomicOr(b.err, kErrRing);
     }
@@ -163,26 +166,28 @@ __global__ __launch_bounds__(kPbPlanBlock) void k_block_plan(BlockArgs b)
 //       input of step t: the state's input at t0, afterwards the LDS
 //       accumulator; the new history words and post traces go to LDS;
 //   (2) the step's rows (the plan's list): for each, its entries with a
-//       target in the group (gpiv), staged as in slice delivery (segment
-//       starts, prefix sums of the lengths, a map from each flattened entry
-//       to its segment), then every entry: the plastic ones brought up to
-//       date from the target's history in LDS (a forced row: only those; its
-//       other entries are not read), and a transmitting row's entries added
-//       to the accumulator (64-bit fixed point, LDS atomics), which step
-//       t+1's neuron update reads.
+//       target in the group, staged as in slice delivery (prefix sums of
+//       the lengths, a map from each flattened entry to its row), then
+//       every entry: the plastic ones brought up to date from the target's
+//       history in LDS (a forced row: only those; its other entries are not
+//       read), and a transmitting row's entries added to the accumulator
+//       (64-bit fixed point, LDS atomics), which step t+1's neuron update
+//       reads.
 // A synapse belongs to the group of its target, so each weight is read and
 // written by one workgroup only, and the steps of a workgroup are ordered by
 // its barriers.
 //
-// The steps are pipelined so that a step waits for no round trip to memory
-// started by itself: once step q's last barrier has ordered its weight
-// stores, the entries of step q+1 (the first window of its first batch,
-// staged and mapped during step q in the other of two staging buffers) are
-// loaded, with the group pivots of step q+3's rows and the snapshots of
-// step q+4; step q+1 consumes only loads started one or more steps before
-// (a wave's loads complete in the order they were issued). Further windows
-// and batches of a step (more entries or rows than one staging holds) are
-// loaded when the step reaches them.
+// The workgroup first loads the records of all its rows of the block (row
+// start plus the group's offset and length, plastic length, age, flags, pre
+// trace) into LDS, so a step stages its rows without a round trip to
+// memory. The steps are pipelined: the next step's rows are staged and
+// mapped while this step's entries are computed, and once the step's last
+// barrier has ordered its weight stores, the next step's entries (its
+// first window) are loaded, one set of loads in flight at a time (a wave's
+// loads complete in the order they were issued, and the loads a step waits
+// for are always the oldest). Further windows and batches of a step are
+// loaded when the step reaches them; a block with more records than LDS
+// holds loads each step's records when it runs.
 //
 // At the end the state goes back, the accumulator becomes partial sum 0 (the
 // input of step t0 + B), and workgroup 0 advances the step clock, which no
@@ -190,57 +195,60 @@ __global__ __launch_bounds__(kPbPlanBlock) void k_block_plan(BlockArgs b)
 
 constexpr int kPbDirect = 32;  // segments up to this long are mapped by their own thread
 constexpr long long kMask40 = (1ll << 40) - 1;
-// per segment of the staging: plastic entries (bits 0-17), age (18-25), pre
-// (26), inhibitory source of a CUBA network (27), delivered (28)
-constexpr int kInfoPlen = 0x3ffff;
-// per loaded entry: segment (bits 0-9), plastic (10), present (11), its
-// offset in the segment (12-31; segments are at most kMaxSortRow long)
+// a record's flags: age (bits 0-7), pre spike (8), delivered (9), inhibitory (10)
+// per loaded entry: record in the batch (bits 0-9), plastic (10), present
+// (11), offset in the segment (12-25), edge index parity (26)
 constexpr int kPkSeg = 0x3ff, kPkPlastic = 1 << 10, kPkIn = 1 << 11, kPkOff = 12;
-static_assert(kPbBatch <= kPkSeg + 1, "segment index fits the entry word");
-static_assert(kMaxSortRow < (1 << (31 - kPkOff)), "segment offset fits the entry word");
-
-struct PbStage {
-    long long start[kPbBatch];  // segment starts (edge index)
-    long long total;            // entries (bits 0-39), segments longer than kPbDirect (40+)
-    int off[kPbBatch + 1];      // segment offsets
-    int info[kPbBatch];
-    float xp0[kPbBatch];
-    float xpn[kPbBatch];
-    uint16_t map[kPbWindow];    // entry -> 1 + segment
-};
+constexpr int kPkOffMask = 0x3fff, kPkOdd = 26;
+static_assert(kPbSegs <= kPkSeg + 1, "record index fits the entry word");
+static_assert(kMaxSortRow <= kPkOffMask + 1, "segment offset fits the entry word");
+// a queued update: record in the batch (bits 0-9), offset (10-23), target in the group (24-31)
+static_assert(kPbMaxWidth <= 256, "target in the group fits the queue word");
+// The graphs of the blocks (at most kPbMaxN rows of at most kMaxSortRow
+// entries) have fewer than 2^31 edges: 32-bit edge indices.
+static_assert((int64_t)kPbMaxN * kMaxSortRow < (1ll << 31), "32-bit edge index");
 
 struct PbEntries {
-    float wv[kPbUnroll];      // weight as loaded
-    int cv[kPbUnroll];        // target as loaded (slice-local with compressed targets)
+    float wv[kPbUnroll];     // weight as loaded
+    uint32_t cv[kPbUnroll];  // target as loaded (compressed: the 32-bit word holding it)
     int pk[kPbUnroll];
 };
 
 template <int HW, bool CT>
 __global__ __launch_bounds__(kPbBlock) void k_block_run(NeuronArgs a, BlockArgs b)
 {
-    __shared__ PbStage S[2];
+    constexpr int NWV = kPbBlock / kWave;
+    constexpr int QH = 4;  // entry slots between queue flushes
+    __shared__ int r_start[kPbRecords];   // first entry of the row in the group (edge index)
+    __shared__ int r_lens[kPbRecords];    // entries (bits 0-15), plastic entries (16-31)
+    __shared__ int r_info[kPbRecords];
+    __shared__ float r_xp0[kPbRecords];
+    __shared__ int s_off[2][kPbSegs + 1];
+    __shared__ uint16_t s_map[2][kPbWindow];  // entry -> 1 + record in the batch
+    __shared__ long long s_tot[2];            // entries (bits 0-39), long segments (40+)
+    __shared__ float q_w[NWV][QH * kWave];
+    __shared__ int q_p[NWV][QH * kWave];
     __shared__ uint64_t s_hist[kPbMaxWidth * HW];
     __shared__ float s_y[kPbMaxWidth];
     __shared__ long long s_acc[2 * kPbMaxWidth];
     __shared__ float s_dpow[kMaxAge + 1];
-    __shared__ long long sh[kPbBlock / kWave];
-    __shared__ int shi[kPbBlock / kWave];
-    __shared__ int s_cnt[kBatchMax];
-    const int tid = threadIdx.x;
+    __shared__ long long sh[NWV];
+    __shared__ int shi[NWV];
+    __shared__ int s_cnt[kBatchMax], s_base[kBatchMax + 1];
+    const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
     // neighbouring groups (which read neighbouring entries of each row) on
     // one XCD: workgroup b runs on XCD b mod 8
     const int nb = gridDim.x;  // multiple of 8
     const int g = (blockIdx.x & 7) * (nb >> 3) + (blockIdx.x >> 3);
     if (g >= b.n_groups) return;  // whole workgroup, before any barrier
-    const int n = a.n;
+    const int n = a.n, G = b.n_groups;
     const int glo = g * b.gwidth;
     const int wn = min(b.gwidth, n - glo);  // > 0
     const int cbase = CT ? glo % b.width : glo;  // subtracted from a loaded target
     const int i = glo + tid;
     const bool live = tid < wn;
     const int B = b.steps;
-    const int G1 = b.n_groups + 1;
-    const long long ne1 = (long long)b.n_edges - 1;  // (same-type min / max)
+    const long long ne = (long long)b.n_edges;
     // the neuron state and the input of the first step (both in flight
     // while the block clock is read)
     NState st = {};
@@ -257,216 +265,246 @@ __global__ __launch_bounds__(kPbBlock) void k_block_run(NeuronArgs a, BlockArgs 
     }
     if (tid < kBatchMax) s_cnt[tid] = tid < B ? min(max(b.ev_cnt[tid], 0), n) : 0;
     for (int q = tid; q <= kMaxAge; q += kPbBlock) s_dpow[q] = b.dpow[q];
+    __syncthreads();  // s_cnt
+    if (tid == 0) {
+        int acc = 0;
+        for (int q = 0; q < kBatchMax; ++q) {
+            s_base[q] = acc;
+            acc += s_cnt[q];
+        }
+        s_base[kBatchMax] = acc;
+    }
     const float c_pot = b.c_pot, c_dep = b.c_dep, mu = b.mu;
     const int32_t *__restrict__ col = b.col;
-    const uint16_t *__restrict__ col16 = b.col16;
+    const uint32_t *__restrict__ col32 = reinterpret_cast<const uint32_t *>(b.col16);
     float *__restrict__ wgt = b.w;
     long long events = 0, w_tx = 0, w_forced = 0, spikes = 0;
-    __syncthreads();  // s_cnt, s_dpow
+    __syncthreads();  // s_base
 
-    auto nbt_of = [&](int q) { return q < B ? min(s_cnt[q], kPbBatch) : 0; };
-    // snapshots e0 + 2 tid, e0 + 2 tid + 1 of step q's list (a valid index
-    // for every lane: the loads go out unconditionally, and lanes past the
-    // count are told apart when staged)
-    auto load_rows = [&](int q, int e0, RowInfo (&R)[kPbRounds]) {
-        const int c = q < B ? s_cnt[q] : 0;
-        const RowInfo *src = b.ev + (int64_t)min(q, B - 1) * n;
+    // LDS records r0 .. r0 + count - 1 from the lists from entry j0 of step
+    // q0 on (across the steps' lists in order): the row's start plus the
+    // group's offset and length (the group pivots of the row, loaded once
+    // the row is known), clamped to the graph (only a failed plan scan,
+    // which leaves list entries unwritten, could point elsewhere)
+    auto load_records = [&](int q0, int j0, int r0, int count) {
+        constexpr int RU = kPbRecords / kPbBlock;  // all records of LDS in one round
+        static_assert(kPbRecords % kPbBlock == 0, "whole rounds of records");
+        for (int x0 = 0; x0 < count; x0 += RU * kPbBlock) {
+            PbEvent pe[RU];
 #pragma unroll
-        for (int r = 0; r < kPbRounds; ++r)
-            R[r] = src[min(e0 + kPbRounds * tid + r, max(c - 1, 0))];
-    };
-    // the group's pivots of those rows
-    auto load_piv = [&](const RowInfo (&R)[kPbRounds], int (&p0)[kPbRounds],
-                        int (&p1)[kPbRounds]) {
+            for (int u = 0; u < RU; ++u) {
+                const int x = min(x0 + u * kPbBlock + tid, max(count - 1, 0));
+                // (the step of flattened entry x: at most kBatchMax lists)
+                int q = q0, j = j0 + x;
+                while (q < B - 1 && j >= s_cnt[q]) {
+                    j -= s_cnt[q];
+                    ++q;
+                }
+                j = min(j, max(s_cnt[q] - 1, 0));
+                pe[u] = b.ev[(int64_t)q * n + j];
+            }
+            int p0[RU], p1[RU];
 #pragma unroll
-        for (int r = 0; r < kPbRounds; ++r) {
-            const int k = min(max(R[r].k, 0), n - 1);
-            const int32_t *gp = b.gpiv + (int64_t)k * G1 + g;
-            p0[r] = gp[0];
-            p1[r] = gp[1];
+            for (int u = 0; u < RU; ++u) {
+                const int32_t *gp = b.gpiv + (int64_t)min(max(pe[u].k, 0), n - 1) * (G + 1) + g;
+                p0[u] = gp[0];
+                p1[u] = gp[1];
+            }
+#pragma unroll
+            for (int u = 0; u < RU; ++u) {
+                const int x = x0 + u * kPbBlock + tid;
+                if (x >= count) continue;
+                int sl = max(p1[u] - p0[u], 0);
+                const uint32_t f = pe[u].lenf;
+                const int plen = min(max((int)(f & 0xffffu) - p0[u], 0), sl);
+                const int deliver = (f >> 25) & 1;
+                if (!deliver) sl = plen;  // a forced row: its plastic entries only
+                const long long st0 = min(max((long long)pe[u].rs + p0[u], 0ll), ne);
+                sl = (int)min((long long)sl, ne - st0);
+                r_start[r0 + x] = (int)st0;
+                r_lens[r0 + x] = sl | (min(plen, sl) << 16);
+                r_info[r0 + x] = (int)((f >> 16) & 0xff) | (int)(((f >> 24) & 1) << 8) |
+                                 (deliver << 9) | (int)(((f >> 26) & 1) << 10);
+                r_xp0[r0 + x] = pe[u].xp0;
+            }
         }
     };
-    // segments of nbt rows into s, offsets scanned; ends with a barrier
-    auto stage = [&](PbStage &s, const RowInfo (&R)[kPbRounds], const int (&p0)[kPbRounds],
-                     const int (&p1)[kPbRounds], int nbt) {
-        int len[kPbRounds];
+    // a batch of nbt records from LDS record rb on, into staging buffer x:
+    // offsets scanned, the map of its first window; ends with a barrier
+    auto build_map = [&](int x, int nbt, int w0, int we, bool direct) {
+        if (direct) {  // short segments: each thread writes its own segments' entries
+#pragma unroll
+            for (int r = 0; r < 2; ++r) {
+                const int j = 2 * tid + r;
+                if (j < nbt) {
+                    const int a0 = max(s_off[x][j], w0), a1 = min(s_off[x][j + 1], w0 + we);
+                    for (int y = a0; y < a1; ++y) s_map[x][y - w0] = (uint16_t)(j + 1);
+                }
+            }
+            __syncthreads();
+        } else {  // mark each segment's first entry in the window, then max-scan
+            for (int y = tid; y < we; y += kPbBlock) s_map[x][y] = 0;
+            __syncthreads();
+#pragma unroll
+            for (int r = 0; r < 2; ++r) {
+                const int j = 2 * tid + r;
+                if (j < nbt) {
+                    const int a0 = max(s_off[x][j], w0), a1 = min(s_off[x][j + 1], w0 + we);
+                    if (a0 < a1) s_map[x][a0 - w0] = (uint16_t)(j + 1);
+                }
+            }
+            __syncthreads();
+            fill_segment_map<kPbBlock, kPbUnroll, uint16_t>(s_map[x], we, shi, 0);
+        }
+    };
+    auto prep = [&](int x, int rb, int nbt) {
+        int len[2];
         long long packed = 0;
 #pragma unroll
-        for (int r = 0; r < kPbRounds; ++r) {
-            const int j = kPbRounds * tid + r;
-            len[r] = 0;
-            if (j < nbt) {
-                const RowInfo &ri = R[r];
-                int sl = max(p1[r] - p0[r], 0);
-                const int deliver = ri.pad & 1;
-                const int plen = ri.age_pre != 0 ? min(max(ri.len - p0[r], 0), sl) : 0;
-                if (!deliver) sl = plen;  // a forced row: its plastic entries only
-                len[r] = sl;
-                const int inh = (b.nacc == 2 && ri.k >= b.n_exc) ? 1 : 0;
-                s.start[j] = ri.rs + p0[r];
-                s.info[j] = plen | ((ri.age_pre & 0xff) << 18) | (((ri.age_pre >> 8) & 1) << 26) |
-                            (inh << 27) | (deliver << 28);
-                s.xp0[j] = ri.xp0;
-                s.xpn[j] = ri.xp_now;
-            }
+        for (int r = 0; r < 2; ++r) {
+            const int j = 2 * tid + r;
+            len[r] = j < nbt ? (r_lens[rb + j] & 0xffff) : 0;
             packed += (long long)len[r] | ((long long)(len[r] > kPbDirect) << 40);
         }
         const long long incl = block_incl_scan_i64_n<kPbBlock>(packed, sh);
         long long ex = (incl - packed) & kMask40;
 #pragma unroll
-        for (int r = 0; r < kPbRounds; ++r) {
-            s.off[kPbRounds * tid + r] = (int)ex;
+        for (int r = 0; r < 2; ++r) {
+            s_off[x][2 * tid + r] = (int)ex;
             ex += len[r];
         }
         if (tid == kPbBlock - 1) {
-            s.off[kPbBatch] = (int)(incl & kMask40);
-            s.total = incl;
+            s_off[x][kPbSegs] = (int)(incl & kMask40);
+            s_tot[x] = incl;
         }
         __syncthreads();
+        const long long tq = s_tot[x];
+        const int total = (int)(tq & kMask40);
+        if (total > 0) build_map(x, nbt, 0, min(total, kPbWindow), (tq >> 40) == 0);
     };
-    // the segment map of window [w0, w0 + we) of s; ends with a barrier
-    auto build_map = [&](PbStage &s, int nbt, int w0, int we, bool direct) {
-        if (direct) {  // short segments: each thread writes its own segments' entries
-#pragma unroll
-            for (int r = 0; r < kPbRounds; ++r) {
-                const int j = kPbRounds * tid + r;
-                if (j < nbt) {
-                    const int a0 = max(s.off[j], w0), a1 = min(s.off[j + 1], w0 + we);
-                    for (int x = a0; x < a1; ++x) s.map[x - w0] = (uint16_t)(j + 1);
-                }
-            }
-            __syncthreads();
-        } else {  // mark each segment's first entry in the window, then max-scan
-            for (int x = tid; x < we; x += kPbBlock) s.map[x] = 0;
-            __syncthreads();
-#pragma unroll
-            for (int r = 0; r < kPbRounds; ++r) {
-                const int j = kPbRounds * tid + r;
-                if (j < nbt) {
-                    const int a0 = max(s.off[j], w0), a1 = min(s.off[j + 1], w0 + we);
-                    if (a0 < a1) s.map[a0 - w0] = (uint16_t)(j + 1);
-                }
-            }
-            __syncthreads();
-            fill_segment_map<kPbBlock, kPbUnroll, uint16_t>(s.map, we, shi, 0);
-        }
-    };
-    // loads of the entries of window [w0, w0 + we) of s: every slot loads
-    // from a valid address (clamped to the graph), the results are looked at
-    // when the entries are computed
-    auto issue = [&](const PbStage &s, int w0, int we, PbEntries &E) {
+    // loads of window [w0, w0 + we) of staging buffer x (records from rb):
+    // every slot loads from a valid address, the results are looked at when
+    // the entries are computed
+    auto issue = [&](int x, int rb, int w0, int we, PbEntries &E) {
 #pragma unroll
         for (int u = 0; u < kPbUnroll; ++u) {
-            const int x = u * kPbBlock + tid;
-            const bool in = x < we;
-            const int l = in ? (int)s.map[x] - 1 : 0;
-            const int off = w0 + x - s.off[l];
-            const long long e = in ? min(max(s.start[l] + off, 0ll), ne1) : 0;
-            E.cv[u] = CT ? (int)col16[e] : col[e];
+            const int y = u * kPbBlock + tid;
+            const bool in = y < we;
+            // a slot no lane of the wave uses loads nothing (wave-uniform)
+            if (u * kPbBlock + wave * kWave >= we) {
+                E.pk[u] = 0;
+                continue;
+            }
+            const int l = in ? (int)s_map[x][y] - 1 : 0;
+            const int off = w0 + y - s_off[x][l];
+            const int r = rb + l;
+            const int e = in ? r_start[r] + off : 0;  // < n_edges
+            E.cv[u] = CT ? col32[e >> 1] : (uint32_t)col[e];
             E.wv[u] = wgt[e];
-            E.pk[u] = in ? l | (off < (s.info[l] & kInfoPlen) ? kPkPlastic : 0) | kPkIn |
-                               (off << kPkOff)
+            E.pk[u] = in ? l | (off < (r_lens[r] >> 16) ? kPkPlastic : 0) | kPkIn |
+                               (off << kPkOff) | ((e & 1) << kPkOdd)
                          : 0;
         }
     };
-    // entries loaded before the step before this one stored its weights:
-    // those of rows brought up to date at both steps are loaded again
-    // an entry's edge index (clamped as when it was loaded)
-    auto edge = [&](const PbStage &s, int pk) {
-        return min(max(s.start[pk & kPkSeg] + (long long)(pk >> kPkOff), 0ll), ne1);
-    };
-    auto compute = [&](const PbStage &s, const PbEntries &E) {
+    // The entries of one window: a transmitting row's entry whose weight
+    // does not change is delivered at once; the entries whose weight
+    // changes (a pre spike, or a post spike of the target within the row's
+    // window) go to the wave's queue, which is then updated 64 at a time
+    // with every lane busy (the replay loops run over those entries only),
+    // stored, and delivered where the row transmits.
+    auto compute = [&](int rb, const PbEntries &E) {
+        float *qw = q_w[wave];
+        int *qp = q_p[wave];
 #pragma unroll
-        for (int u = 0; u < kPbUnroll; ++u) {
-            const int pk = E.pk[u];
-            if (!(pk & kPkIn)) continue;
-            const int l = pk & kPkSeg;
-            const int info = s.info[l];
-            const int j = E.cv[u] - cbase;
-            if ((unsigned)j >= (unsigned)wn) {  // not this group's target
-                atomicOr(b.err, kErrIndex);
-                continue;
+        for (int hf = 0; hf < kPbUnroll / QH; ++hf) {
+            int qn = 0;
+#pragma unroll
+            for (int v = 0; v < QH; ++v) {
+                const int u = hf * QH + v;
+                const int pk = E.pk[u];
+                if (!ballot64(pk & kPkIn)) continue;  // an unused slot of the wave
+                const int l = pk & kPkSeg;
+                const int info = (pk & kPkIn) ? r_info[rb + l] : 0;
+                const uint32_t c = CT ? (((pk >> kPkOdd) & 1) ? E.cv[u] >> 16 : E.cv[u] & 0xffffu)
+                                      : E.cv[u];
+                const int j = (int)c - cbase;
+                const bool ok = (pk & kPkIn) && (unsigned)j < (unsigned)wn;
+                if ((pk & kPkIn) && !ok) atomicOr(b.err, kErrIndex);  // not this group's target
+                bool cand = false;
+                if (ok && (pk & kPkPlastic)) {
+                    uint64_t m0, m1;
+                    window_masks(info & 0xff, m0, m1);
+                    const uint64_t h0 = s_hist[j * HW] & m0;
+                    const uint64_t h1 = HW == 2 ? s_hist[j * 2 + 1] & m1 : 0ull;
+                    cand = h0 || h1 || ((info >> 8) & 1) || !b.event;
+                }
+                if (ok && !cand && ((info >> 9) & 1)) {
+                    atomicAdd((unsigned long long *)(s_acc + j +
+                                                     (((info >> 10) & 1) ? kPbMaxWidth : 0)),
+                              (unsigned long long)to_fix(E.wv[u]));
+                    ++events;
+                }
+                const uint64_t bl = ballot64(cand);
+                if (cand) {
+                    const int e = qn + lane_rank(bl);
+                    qw[e] = E.wv[u];
+                    qp[e] = l | (((pk >> kPkOff) & kPkOffMask) << 10) | (j << 24);
+                }
+                qn += (int)__popcll(bl);
             }
-            float w = E.wv[u];
-            if (pk & kPkPlastic) {
-                const int age = (info >> 18) & 0xff, pre = (info >> 26) & 1;
+            __builtin_amdgcn_wave_barrier();
+            for (int e0 = 0; e0 < qn; e0 += kWave) {  // wave-uniform
+                const int e = e0 + lane;
+                if (e >= qn) continue;
+                float w = qw[e];
+                const unsigned p = (unsigned)qp[e];
+                const int r = rb + (int)(p & kPkSeg);
+                const int off = (int)((p >> 10) & kPkOffMask), j = (int)(p >> 24);
+                const int info = r_info[r];
+                const int age = info & 0xff, pre = (info >> 8) & 1;
                 uint64_t m0, m1;
                 window_masks(age, m0, m1);
                 const uint64_t h0 = s_hist[j * HW] & m0;
                 const uint64_t h1 = HW == 2 ? s_hist[j * 2 + 1] & m1 : 0ull;
-                if (h0 || h1 || pre || !b.event) {
-                    const float y = pre ? s_y[j] : 0.f;
-                    w = b.event ? stdp_synapse(w, h0, h1, age, pre, s.xp0[l], s.xpn[l], y, s_dpow,
-                                               c_pot, c_dep, mu)
-                                : stdp_synapse_steps(w, h0, h1, age, pre, s.xp0[l], s.xpn[l], y,
-                                                     s_dpow[1], c_pot, c_dep, mu);
-                    wgt[edge(s, pk)] = w;
-                    if (pre)
-                        ++w_tx;
-                    else
-                        ++w_forced;
+                const float y = pre ? s_y[j] : 0.f;
+                const float xp0 = r_xp0[r];
+                // the pre trace after this update, as the plan's snapshot has it
+                const float xpn = __fadd_rn(__fmul_rn(xp0, s_dpow[age]), (float)pre);
+                w = b.event ? stdp_synapse(w, h0, h1, age, pre, xp0, xpn, y, s_dpow, c_pot, c_dep, mu)
+                            : stdp_synapse_steps(w, h0, h1, age, pre, xp0, xpn, y, s_dpow[1],
+                                                 c_pot, c_dep, mu);
+                wgt[r_start[r] + off] = w;
+                if (pre)
+                    ++w_tx;
+                else
+                    ++w_forced;
+                if ((info >> 9) & 1) {
+                    atomicAdd((unsigned long long *)(s_acc + j +
+                                                     (((info >> 10) & 1) ? kPbMaxWidth : 0)),
+                              (unsigned long long)to_fix(w));
+                    ++events;
                 }
             }
-            if ((info >> 28) & 1) {
-                atomicAdd((unsigned long long *)(s_acc + j + (((info >> 27) & 1) ? kPbMaxWidth : 0)),
-                          (unsigned long long)to_fix(w));
-                ++events;
-            }
+            __builtin_amdgcn_wave_barrier();  // the queue is rewritten next
         }
     };
-    // everything of the step staged in s beyond its first window, and its
-    // further batches (each loaded, staged and mapped when reached)
-    auto rest_of_step = [&](int q, PbStage &s, PbEntries &E) {
-        const int cnt = s_cnt[q];
-        for (int e0 = 0; e0 < cnt; e0 += kPbBatch) {
-            const int nbt = min(kPbBatch, cnt - e0);
-            if (e0 > 0) {
-                __syncthreads();  // every read of the staging of the batch before
-                RowInfo R[kPbRounds];
-                int p0[kPbRounds], p1[kPbRounds];
-                load_rows(q, e0, R);
-                load_piv(R, p0, p1);
-                stage(s, R, p0, p1, nbt);
-            }
-            const long long tq = s.total;
-            const int total = (int)(tq & kMask40);
-            const bool direct = (tq >> 40) == 0;
-            for (int w0 = e0 > 0 ? 0 : kPbWindow; w0 < total; w0 += kPbWindow) {
-                const int we = min(kPbWindow, total - w0);
-                __syncthreads();  // every read of the map of the window before
-                build_map(s, nbt, w0, we, direct);
-                issue(s, w0, we, E);
-                compute(s, E);
-            }
-        }
-    };
-
-    // prologue: step 0 staged and its first window loaded, the snapshots of
-    // steps 1-3 and the pivots of steps 1-2 loaded
-    PbEntries E;
-    RowInfo R1[kPbRounds], R2[kPbRounds], R3[kPbRounds];
-    int P1a[kPbRounds], P1b[kPbRounds], P2a[kPbRounds], P2b[kPbRounds];
-    {
-        RowInfo R0[kPbRounds];
-        int p0[kPbRounds], p1[kPbRounds];
-        load_rows(0, 0, R0);
-        load_rows(1, 0, R1);
-        load_rows(2, 0, R2);
-        load_rows(3, 0, R3);
-        load_piv(R0, p0, p1);
-        load_piv(R1, P1a, P1b);
-        load_piv(R2, P2a, P2b);
-        stage(S[0], R0, p0, p1, nbt_of(0));
-        const long long tq = S[0].total;
+    // the windows of a staged batch from window w_from on (each mapped,
+    // loaded and computed in turn)
+    auto windows = [&](int x, int rb, int nbt, int w_from, PbEntries &E) {
+        const long long tq = s_tot[x];
         const int total = (int)(tq & kMask40);
-        if (total > 0) build_map(S[0], nbt_of(0), 0, min(total, kPbWindow), (tq >> 40) == 0);
-        issue(S[0], 0, min(total, kPbWindow), E);
-    }
-    for (int q = 0; q < B; ++q) {
-        PbStage &cur = S[q & 1];
-        PbStage &nxt = S[(q + 1) & 1];
+        for (int w0 = w_from; w0 < total; w0 += kPbWindow) {
+            const int we = min(kPbWindow, total - w0);
+            if (w0 > 0) {
+                __syncthreads();  // every read of the map of the window before
+                build_map(x, nbt, w0, we, (tq >> 40) == 0);
+            }
+            issue(x, rb, w0, we, E);
+            compute(rb, E);
+        }
+    };
+    auto neuron_step = [&](int q) {
         const int64_t t = t0 + q;
-        // (1) neuron update; the accumulator it read is cleared
         if (live) {
             float ae = 0.f, ai = 0.f;
             if (a.model != 2) {
@@ -483,36 +521,60 @@ __global__ __launch_bounds__(kPbBlock) void k_block_run(NeuronArgs a, BlockArgs 
             if (HW == 2) s_hist[tid * 2 + 1] = st.h1;
             s_y[tid] = st.y;
         }
-        s_acc[tid] = 0;
-        s_acc[kPbMaxWidth + tid] = 0;
-        // (2a) step q+1 staged and its first window mapped (the staging's
-        // barriers publish the neuron update)
-        if (q + 1 < B) {
-            const int nb1 = nbt_of(q + 1);
-            stage(nxt, R1, P1a, P1b, nb1);
-            const long long tq = nxt.total;
-            const int total = (int)(tq & kMask40);
-            if (total > 0) build_map(nxt, nb1, 0, min(total, kPbWindow), (tq >> 40) == 0);
-        } else {
-            __syncthreads();  // the neuron update's histories and traces
+        if (tid < kPbMaxWidth) {
+            s_acc[tid] = 0;
+            s_acc[kPbMaxWidth + tid] = 0;
         }
-        // (2b) the entries of step q
-        compute(cur, E);
-        rest_of_step(q, cur, E);
-        __syncthreads();  // every atomic and weight store of step q done
-        // (3) the loads for the steps ahead
-        if (q + 1 < B) {
-            const int total = (int)(nxt.total & kMask40);
-            issue(nxt, 0, min(total, kPbWindow), E);
-#pragma unroll
-            for (int r = 0; r < kPbRounds; ++r) {
-                R1[r] = R2[r];
-                R2[r] = R3[r];
-                P1a[r] = P2a[r];
-                P1b[r] = P2b[r];
+    };
+
+    PbEntries E;
+    const int total_rec = s_base[kBatchMax];
+    if (total_rec <= kPbRecords) {
+        // every record of the block in LDS; step 0 staged and its first
+        // window loaded
+        load_records(0, 0, 0, total_rec);
+        __syncthreads();
+        const int nb0 = min(s_cnt[0], kPbSegs);
+        prep(0, s_base[0], nb0);
+        issue(0, s_base[0], 0, min((int)(s_tot[0] & kMask40), kPbWindow), E);
+        for (int q = 0; q < B; ++q) {
+            const int x = q & 1;
+            neuron_step(q);
+            // (2a) the next step's first batch staged and its first window
+            // mapped (the staging's barriers publish the neuron update)
+            if (q + 1 < B)
+                prep(x ^ 1, s_base[q + 1], min(s_cnt[q + 1], kPbSegs));
+            else
+                __syncthreads();  // the neuron update's histories and traces
+            // (2b) this step's entries: the loaded first window, the rest
+            const int nb1 = min(s_cnt[q], kPbSegs);
+            compute(s_base[q], E);
+            windows(x, s_base[q], nb1, kPbWindow, E);
+            for (int e0 = kPbSegs; e0 < s_cnt[q]; e0 += kPbSegs) {  // further batches
+                __syncthreads();  // every read of the staging of the batch before
+                const int nbt = min(kPbSegs, s_cnt[q] - e0);
+                prep(x, s_base[q] + e0, nbt);
+                windows(x, s_base[q] + e0, nbt, 0, E);
             }
-            load_piv(R2, P2a, P2b);
-            load_rows(q + 4, 0, R3);
+            __syncthreads();  // every atomic and weight store of step q done
+            // (3) the next step's first window loaded
+            if (q + 1 < B) issue(x ^ 1, s_base[q + 1], 0,
+                                 min((int)(s_tot[x ^ 1] & kMask40), kPbWindow), E);
+        }
+    } else {
+        // more records than LDS holds: each batch of each step's records is
+        // loaded when the step reaches it
+        for (int q = 0; q < B; ++q) {
+            neuron_step(q);
+            for (int e0 = 0; e0 < s_cnt[q]; e0 += kPbSegs) {
+                __syncthreads();  // every read of the records and staging before
+                const int nbt = min(kPbSegs, s_cnt[q] - e0);
+                load_records(q, e0, 0, nbt);
+                __syncthreads();
+                prep(0, 0, nbt);
+                windows(0, 0, nbt, 0, E);
+            }
+            __syncthreads();  // every atomic of step q done (and the neuron update published)
         }
     }
     if (live) {
@@ -642,7 +704,7 @@ hipError_t launch_block_plan(hipStream_t s, const BlockArgs &b)
 hipError_t launch_block_run(hipStream_t s, const NeuronArgs &a, const BlockArgs &b)
 {
     if (b.steps < 1 || b.steps > kBatchMax || b.gwidth < 1 || b.gwidth > kPbMaxWidth ||
-        b.n_edges < 1 ||
+        b.n_edges < 1 || b.n_edges > INT32_MAX ||
         b.width % b.gwidth != 0 || (int64_t)b.n_groups * b.gwidth < a.n ||
         (int64_t)(b.n_groups - 1) * b.gwidth >= a.n || a.n != b.n || b.nacc < 1 || b.nacc > 2 ||
         b.dlv_slots < 1 || b.syn_slots < 1)

@@ -125,7 +125,7 @@ struct snn_ctx {
     // and counts and the block clock (workspace)
     int32_t pb_max = 0, pb_width = 0, pb_groups = 0;
     int32_t *gpiv = nullptr;
-    RowInfo *pev = nullptr;
+    PbEvent *pev = nullptr;
     int32_t *pev_cnt = nullptr;
     BlockClock *bclk = nullptr;
 
@@ -359,9 +359,9 @@ void derive(snn_ctx *c)
     }
     c->info_blocks = c->nblk;  // statistics slots of the neuron-kernel / flush snapshots
     // Plastic blocks (BlockArgs) of up to D-1 steps (at most kBatchMax): lazy
-    // plasticity, D >= 2, up to kPbMaxN neurons. Target groups of 256, 128
-    // or 64 neurons inside slices: the widest that still gives every CU about
-    // one and a half groups, else 64.
+    // plasticity, D >= 2, up to kPbMaxN neurons. Target groups of 64, 128
+    // or 256 neurons inside slices, one workgroup each: the narrowest that
+    // needs no more workgroups than the device has CUs, else the widest.
     c->pb_max = c->pb_width = c->pb_groups = 0;
     if (c->n_plastic_rows > 0 && c->algo != 2 && c->delay >= 2 && k.n <= kPbMaxN &&
         k.plastic_blocks >= 0) {
@@ -369,13 +369,10 @@ void derive(snn_ctx *c)
         if (k.plastic_blocks > 0) bm = std::min<int32_t>(bm, k.plastic_blocks);
         int32_t gw = k.plastic_block_width;
         if (gw == 0) {
-            gw = 64;
-            for (int cand : {256, 128}) {
-                if (k.slice_width % cand == 0 &&
-                    2 * (((int64_t)k.n + cand - 1) / cand) >= 3 * (int64_t)c->n_cu) {
-                    gw = cand;
-                    break;
-                }
+            for (int cand : {64, 128, 256}) {
+                if (k.slice_width % cand != 0) continue;
+                gw = cand;
+                if (((int64_t)k.n + cand - 1) / cand <= (int64_t)c->n_cu) break;
             }
         }
         c->pb_max = bm;
@@ -439,7 +436,7 @@ void plan_workspace(snn_ctx *c, uint8_t *base)
     c->syn_stats = p.take<int64_t>(c->syn_slots);
     c->dlv_stats = p.take<int64_t>(2 * (int64_t)c->dlv_slots);
     c->abatch = p.take<long long>(c->batch_max > 0 ? (int64_t)c->batch_max * c->nacc * n : 1);
-    c->pev = p.take<RowInfo>(c->pb_max > 0 ? (int64_t)c->pb_max * n : 1);
+    c->pev = p.take<PbEvent>(c->pb_max > 0 ? (int64_t)c->pb_max * n : 1);
     c->pev_cnt = p.take<int32_t>(kBatchMax);
     c->bclk = p.take<BlockClock>(1);
     c->ws_need = p.off;

@@ -335,35 +335,41 @@ constexpr int64_t kBatchBytes = 256ll << 20;  // most workspace for a block's pa
 // neuron update reads. No workgroup waits for another within the block.
 //   The plan (one thread per row) walks each row through the block's steps
 // as the neuron update would (transmitting: history bit D-1 of the step;
-// forced: idle for 64 hw steps) and writes each step's list of row
-// snapshots (RowInfo; pad bit 0: transmitting, bit 1: the row was brought
-// up to date at the step before too), ascending, by one
-// decoupled look-back per step; it commits t_last and x_pre after the block.
-// The targets are cut into groups of gwidth neurons inside slices, and each
-// row's entries per group are found from a pivot table at group
-// granularity (gpiv[k][g] = the row-relative first entry of row k with a
-// target >= g gwidth, g = 0..n_groups; the pivot kernel with gwidth for
-// the slice width). After the last block of a call,
-// k_block_finish rebuilds from the histories what the step-by-step path
-// keeps per step: the delay-ring lists of the last D steps with their
-// positions, the masks and forced-row list of the last step; and clears
-// the list scans' status words.
+// forced: idle for 64 hw steps), and writes each step's list of row updates
+// (PbEvent), ascending, by one decoupled look-back per step, and commits
+// t_last and x_pre after the block. A group finds a row's entries with
+// targets in the group from the pivot table at group granularity
+// (gpiv[k][g] = the row-relative first entry of row k with a target >=
+// g gwidth, g = 0..n_groups; the pivot kernel with gwidth for the slice
+// width). After the last
+// block of a call, k_block_finish rebuilds from the histories what the
+// step-by-step path keeps per step: the delay-ring lists of the last D
+// steps with their positions, the masks and forced-row list of the last
+// step; and clears the list scans' status words.
 struct BlockClock {
     long long t0;          // the block's first step
     int32_t input_forced;  // the input of step t0, as the step clock said
     int32_t n_parts;
     long long pad_[2];
 };
+// One row to bring up to date (and deliver) at a step of a block.
+struct PbEvent {
+    int32_t rs;      // first edge of the row
+    uint32_t lenf;   // plastic prefix length (bits 0-15), age (16-23), pre spike (24),
+                     // transmitting (25), inhibitory source of a CUBA network (26)
+    float xp0;       // pre trace at the row's previous update
+    int32_t k;       // the row
+};
 constexpr int kPbPlanBlock = 512;   // threads of the plan (one row each, a half wave per step's scan)
-constexpr int kPbBlock = 256;       // threads of a target group's workgroup
+constexpr int kPbBlock = 512;       // threads of a target group's workgroup
 constexpr int kPbMaxWidth = 256;    // most targets per group (one neuron per thread)
-constexpr int kPbRounds = 2;        // row snapshots each thread stages per batch
-constexpr int kPbBatch = kPbBlock * kPbRounds;
-constexpr int kPbUnroll = 8;        // flattened entries per thread per window
+constexpr int kPbSegs = 2 * kPbBlock;  // a step's records staged at once (two per thread)
+constexpr int kPbUnroll = 16;       // flattened entries per thread per window
 constexpr int kPbWindow = kPbBlock * kPbUnroll;
+constexpr int kPbRecords = 5120;    // a block's records a workgroup holds in LDS
 constexpr int kPbMaxN = 65536;      // largest network the blocks run
 static_assert(kPbPlanBlock / 32 >= kBatchMax, "a half wave per step's list scan");
-static_assert(kPbBatch < 65535, "16-bit segment map");
+static_assert(kPbSegs < 65535, "16-bit segment map");
 struct BlockArgs {
     // plan
     const int64_t *row_ptr;
@@ -373,7 +379,7 @@ struct BlockArgs {
     float *xpre;
     unsigned long long *status;  // [kBatchMax][status_stride] look-back words
     int32_t status_stride;
-    RowInfo *ev;                 // [kBatchMax][n]: step k's rows at ev + k n
+    PbEvent *ev;                 // [steps][n]: step k's rows at ev + k n
     int32_t *ev_cnt;             // [kBatchMax]
     BlockClock *bclk;            // written by the plan, read by the run
     StepClock *clk;              // read by the plan, advanced by the run
@@ -386,7 +392,7 @@ struct BlockArgs {
     const uint16_t *col16;       // compressed targets (slice-local), or nullptr
     float *w;
     const int32_t *gpiv;         // [n][n_groups + 1]
-    int64_t n_edges;             // (entry indices are clamped to the graph)
+    int64_t n_edges;
     int32_t gwidth, width, n_groups;
     long long *apart;            // partial 0 receives the input of step t0 + B
     int64_t part_stride;
