@@ -87,6 +87,15 @@ CASES = [
     ("stress", dict(n=3000, p_or_fanout=150, p_fire=0.03, delay=3), 640, 1, dict(), 200),
     ("stress", dict(n=4100, p_or_fanout=300, p_fire=0.02, delay=17), 1024, 3,
      dict(history_bits=128), 200),
+    # heavy activity: about 1,200 rows per step (more than one staging batch
+    # of 1,024), over 8,192 entries per group and step (several windows),
+    # and more records per block than a workgroup holds in LDS (each step's
+    # records loaded when it runs)
+    ("stress", dict(n=6000, p_or_fanout=1000, p_fire=0.2, delay=17), 1024, 2,
+     dict(plastic_block_width=64), 60),
+    # the same activity in blocks short enough to keep their records in LDS
+    ("stress", dict(n=6000, p_or_fanout=1000, p_fire=0.2, delay=3), 1024, 2,
+     dict(plastic_block_width=64), 60),
 ]
 
 
