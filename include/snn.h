@@ -169,7 +169,7 @@ typedef struct snn_config {
                              either way */
     int32_t plastic_blocks; /* plastic networks (lazy plasticity, slice
                              delivery) with D >= 2 and n <= 65536: snn_step
-                             runs blocks of up to min(D-1, 16) steps, two
+                             runs blocks of up to min(D-1, 15) steps, two
                              launches per block, each workgroup owning a
                              group of targets through the whole block (see
                              snn_step). 0 = on; k > 0 = on, at most k steps
@@ -375,14 +375,17 @@ snn_status snn_advance(snn_ctx *ctx);
  * all before one neuron launch runs those steps (Sec. I: the input of step
  * t depends on the spikes of step t-D only). Plastic networks with D >= 2
  * and n <= 65536 (lazy plasticity, snn_config.plastic_blocks) run in blocks
- * of up to D-1 steps (at most 16): the weight a row delivers at t depends
+ * of up to D-1 steps (at most 15): the weight a row delivers at t depends
  * only on spikes of its targets and on pre spikes that arrived by t (Sec.
  * III-A: each synapse sees its pre spike D-1 steps after emission), so the
  * rows to update and deliver at each step of the block are known when it
  * starts, and one launch lists them, then one launch runs every step of
  * the block with each workgroup owning a group of targets (their neuron
  * update, and the plasticity and delivery of every listed row's synapses
- * onto them); a last launch per call rebuilds the per-step lists. Other
+ * onto them; a forced update that is its row's last of the block delivers
+ * nothing and is computed after the block's last step, from the targets'
+ * histories at its step); a last launch per call rebuilds the per-step
+ * lists. Other
  * plastic networks run parts (2) and (3) in one launch where its LDS
  * leaves the forced rows at least half a workgroup slot per CU beside the
  * delivery work items: the forced rows and the transmitting rows of a step

@@ -6,6 +6,8 @@
 // operation order.
 #include "snn_neuron.h"
 
+#include <algorithm>
+
 namespace snn {
 namespace {
 
@@ -18,10 +20,13 @@ namespace {
 // last update is 64 hw steps old (forced), exactly as the step-by-step
 // neuron update decides; each such event is a snapshot of the row at its
 // step, taken from the t_last and x_pre that the row's earlier events in the
-// block left. The steps are walked twice: once for the event flags (each
-// step's counts, scanned over the workgroups by a decoupled look-back, one
-// scan per step), then for the snapshots (PbEvent), written at their
-// positions in the step's ascending list.
+// block left. A row is forced at most once per block (64 hw > B steps apart)
+// and only before its first transmission; a forced update that is the row's
+// last event of the block goes to the deferred list (list B) instead of its
+// step's. The steps are walked twice: once for the event flags (each list's
+// counts, scanned over the workgroups by a decoupled look-back, one scan per
+// list), then for the snapshots (PbEvent), written at their positions in
+// their list, ascending.
 
 __global__ __launch_bounds__(kPbPlanBlock) void k_block_plan(BlockArgs b)
 {
@@ -60,8 +65,8 @@ __global__ __launch_bounds__(kPbPlanBlock) void k_block_plan(BlockArgs b)
     }
     for (int q = tid; q <= kMaxAge; q += kPbPlanBlock) s_dpow[q] = b.dpow[q];
     if (tid < kStFields) s_st[tid] = 0ull;
-    // the steps with an event
-    uint32_t evm = 0;
+    // the steps with an event, and the deferred one
+    uint32_t evm = 0, fm = 0;
     {
         int tl = tl0;
         for (int q = 0; q < B; ++q) {  // uniform
@@ -73,24 +78,30 @@ __global__ __launch_bounds__(kPbPlanBlock) void k_block_plan(BlockArgs b)
                     if (t - (int64_t)tl > 0) tl = (int)t;
                 } else if (t - (int64_t)tl >= 64 * hw) {
                     ev = true;
+                    fm |= 1u << q;
                     tl = (int)t;
                 }
             }
             evm |= (uint32_t)ev << q;
-            const uint64_t m = ballot64(ev);
-            if (lane == 0) s_m[q][wave] = m;
         }
     }
+    // (a forced update is the row's last event when no higher bit is set)
+    const uint32_t dfm = fm != 0u && (evm >> (__ffs((int)fm))) == 0u ? fm : 0u;
+    for (int q = 0; q <= B; ++q) {  // uniform
+        const bool ev = q < B ? ((evm & ~dfm) >> q) & 1u : dfm != 0u;
+        const uint64_t m = ballot64(ev);
+        if (lane == 0) s_m[q][wave] = m;
+    }
     __syncthreads();  // s_m, s_dpow, s_st
-    // this workgroup's events of step tid, published for the step's scan
+    // this workgroup's events of list tid, published for the list's scan
     int own = 0;
-    if (tid < B) {
+    if (tid <= B) {
         for (int w = 0; w < NWV; ++w) own += __popcll(s_m[tid][w]);
         publish_status(b.status + (int64_t)tid * b.status_stride + blockIdx.x,
                        status_word(own, 0, t0 + tid, blockIdx.x == 0 ? kStatusInc : kStatusAgg));
     }
-    lookback32<kPbPlanBlock>(b.status, b.status_stride, B, (int)blockIdx.x, t0, s_lb, b.err);
-    if (tid < B && blockIdx.x > 0)
+    lookback32<kPbPlanBlock>(b.status, b.status_stride, B + 1, (int)blockIdx.x, t0, s_lb, b.err);
+    if (tid <= B && blockIdx.x > 0)
         publish_status(b.status + (int64_t)tid * b.status_stride + blockIdx.x,
                        status_word(s_lb[2 * tid] + own, 0, t0 + tid, kStatusInc));
     // the snapshots, at their positions: earlier workgroups, earlier waves,
@@ -125,14 +136,16 @@ __global__ __launch_bounds__(kPbPlanBlock) void k_block_plan(BlockArgs b)
         pe.lenf = ok ? ((uint32_t)ri.len & 0xffffu) | ((uint32_t)(ri.age_pre & 0xff) << 16) |
                            ((uint32_t)((ri.age_pre >> 8) & 1) << 24)
                      : 0u;
-        pe.lenf |= ((uint32_t)tx << 25) | ((uint32_t)(b.nacc == 2 && k >= b.n_exc) << 26);
+        pe.lenf |= ((uint32_t)tx << 25) | ((uint32_t)(b.nacc == 2 && k >= b.n_exc) << 26) |
+                   ((uint32_t)q << 27);
         pe.xp0 = ok ? ri.xp0 : 0.f;
         pe.k = k;
-        int pos = s_lb[2 * q] + __popcll(s_m[q][wave] & below);
-        for (int w = 0; w < wave; ++w) pos += __popcll(s_m[q][w]);
+        const int lq = (dfm >> q) & 1u ? B : q;  // the list
+        int pos = s_lb[2 * lq] + __popcll(s_m[lq][wave] & below);
+        for (int w = 0; w < wave; ++w) pos += __popcll(s_m[lq][w]);
         // (only a failed scan puts a position out of range)
         if (pos < b.n)
-            b.ev[(int64_t)q * b.n + pos] = pe;
+            b.ev[(int64_t)lq * b.n + pos] = pe;
         else
             atomicOr(b.err, kErrRing);
     }
@@ -154,8 +167,8 @@ __global__ __launch_bounds__(kPbPlanBlock) void k_block_plan(BlockArgs b)
     if (tid < kStFields && s_st[tid])
         add_stat(b.info_stats + (int64_t)(blockIdx.x % b.info_slots) * kStFields + tid,
                  (long long)s_st[tid]);
-    // the last workgroup's scans saw every workgroup: the step totals
-    if (blockIdx.x == gridDim.x - 1 && tid < B) b.ev_cnt[tid] = s_lb[2 * tid] + own;
+    // the last workgroup's scans saw every workgroup: the list totals
+    if (blockIdx.x == gridDim.x - 1 && tid <= B) b.ev_cnt[tid] = s_lb[2 * tid] + own;
 }
 
 // ---------------------------------------------------------------------------
@@ -190,8 +203,10 @@ __global__ __launch_bounds__(kPbPlanBlock) void k_block_plan(BlockArgs b)
 // holds loads each step's records when it runs.
 //
 // At the end the state goes back, the accumulator becomes partial sum 0 (the
-// input of step t0 + B), and workgroup 0 advances the step clock, which no
-// workgroup of the run reads (they read the plan's copy).
+// input of step t0 + B), each target's history words at block start and its
+// code for the deferred updates are written (see k_block_deferred), and
+// workgroup 0 advances the step clock, which no workgroup of the run reads
+// (they read the plan's copy).
 
 constexpr int kPbDirect = 32;  // segments up to this long are mapped by their own thread
 constexpr long long kMask40 = (1ll << 40) - 1;
@@ -279,6 +294,7 @@ __global__ __launch_bounds__(kPbBlock) void k_block_run(NeuronArgs a, BlockArgs 
     const uint32_t *__restrict__ col32 = reinterpret_cast<const uint32_t *>(b.col16);
     float *__restrict__ wgt = b.w;
     long long events = 0, w_tx = 0, w_forced = 0, spikes = 0;
+    uint32_t blk = 0u;  // the block's spikes (bit 0: the latest step)
     __syncthreads();  // s_base
 
     // LDS records r0 .. r0 + count - 1 from the lists from entry j0 of step
@@ -516,7 +532,9 @@ __global__ __launch_bounds__(kPbBlock) void k_block_run(NeuronArgs a, BlockArgs 
                     if (b.nacc == 2) ai = from_fix(s_acc[kPbMaxWidth + tid]);
                 }
             }
-            spikes += neuron_advance<-1, HW>(a, i, t, ae, ai, st);
+            const int sp = neuron_advance<-1, HW>(a, i, t, ae, ai, st);
+            spikes += sp;
+            blk = (blk << 1) | (uint32_t)sp;
             s_hist[tid * HW] = st.h0;
             if (HW == 2) s_hist[tid * 2 + 1] = st.h1;
             s_y[tid] = st.y;
@@ -527,6 +545,7 @@ __global__ __launch_bounds__(kPbBlock) void k_block_run(NeuronArgs a, BlockArgs 
         }
     };
 
+    const uint64_t hs0 = st.h0, hs1 = st.h1;  // the history words at block start
     PbEntries E;
     const int total_rec = s_base[kBatchMax];
     if (total_rec <= kPbRecords) {
@@ -582,6 +601,12 @@ __global__ __launch_bounds__(kPbBlock) void k_block_run(NeuronArgs a, BlockArgs 
         a.code[i] = hist_code(st.h0, st.h1);
         b.apart[i] = s_acc[tid];
         if (b.nacc == 2) b.apart[n + i] = s_acc[kPbMaxWidth + tid];
+        b.hstart[(int64_t)i * HW] = hs0;
+        if (HW == 2) b.hstart[(int64_t)i * 2 + 1] = hs1;
+        // the latest spike before the block: its bit in the words at block start
+        const int last = hs0 ? __ffsll((long long)hs0) - 1
+                             : (HW == 2 && hs1) ? 63 + __ffsll((long long)hs1) : 255;
+        b.dcode[i] = blk | ((uint32_t)last << 16);
     }
     events = block_sum_i64_n<kPbBlock>(events, sh);
     w_tx = block_sum_i64_n<kPbBlock>(w_tx, sh);
@@ -600,6 +625,178 @@ __global__ __launch_bounds__(kPbBlock) void k_block_run(NeuronArgs a, BlockArgs 
             b.clk->n_parts = 1;
         }
     }
+}
+
+// ---------------------------------------------------------------------------
+// The deferred forced updates of a block (the plan's list B), after its run,
+// streamed by the whole device: each wave takes whole rows (their plastic
+// entries, from the row's first 8-aligned entry on, kDfPart at a time, each
+// lane 8 consecutive targets and weights in 16-byte loads), the next part
+// loaded while the current one is computed.
+//   An update at step t = t0 + q (age a) changes the synapses whose target
+// spiked in the window (t - a, t] (all of them without event-driven replay).
+// The target's history word at t is its word at block start shifted up by
+// q + 1 steps, under the block's spike bits of steps t0 .. t (Sec. III-A's
+// bit history), so the target's code (the block's spikes, and the bit of its
+// latest spike before the block) decides whether a synapse changes; the
+// synapses that do are queued and brought up to date 64 at a time with the
+// words at block start.
+
+constexpr int kDfBlock = 256;
+constexpr int kDfU = 8;                 // entries per lane per part
+constexpr int kDfPart = kDfU * kWave;   // entries per part of a row
+constexpr int kDfPerCu = 4;             // workgroups per CU (LDS: four queues each)
+
+struct DfPart {
+    int4 c[2];
+    float4 w[2];
+    long long base, lo, hi;  // first entry of the part (8-aligned), the row's plastic entries
+    int age, qs;
+    float xp0;
+    int valid;
+};
+
+template <int HW>
+__global__ __launch_bounds__(kDfBlock) void k_block_deferred(BlockArgs b)
+{
+    constexpr int NWV = kDfBlock / kWave;
+    __shared__ float s_dpow[kMaxAge + 1];
+    __shared__ int q_e[NWV][kDfPart];        // edge index
+    __shared__ int q_j[NWV][kDfPart];        // target
+    __shared__ uint32_t q_c[NWV][kDfPart];   // target's code
+    __shared__ float q_w[NWV][kDfPart];      // weight
+    __shared__ long long sh[NWV];
+    const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+    const int n = b.n, B = b.steps;
+    const int nd = min(max(b.ev_cnt[B], 0), n);
+    const PbEvent *__restrict__ evd = b.ev + (int64_t)B * n;
+    const int32_t *__restrict__ col = b.col;
+    float *__restrict__ wgt = b.w;
+    const uint32_t *__restrict__ dcode = b.dcode;
+    const uint64_t *__restrict__ hst = b.hstart;
+    const long long ne = (long long)b.n_edges;  // < 2^31
+    const float c_pot = b.c_pot, c_dep = b.c_dep, mu = b.mu;
+    for (int x = tid; x <= kMaxAge; x += kDfBlock) s_dpow[x] = b.dpow[x];
+    const int stride = gridDim.x * NWV;
+    // the wave's rows d, d + stride, ...: the current one and the next
+    int d = blockIdx.x * NWV + wave;
+    PbEvent cur_e = PbEvent{}, nxt_e = PbEvent{};
+    if (d < nd) cur_e = evd[d];
+    if (d + stride < nd) nxt_e = evd[d + stride];
+    long long base = 0;
+    bool fresh = true;  // base not yet set for row d
+    auto issue = [&](DfPart &p) {
+        p.valid = 0;
+        if (d >= nd) return;  // wave-uniform
+        const uint32_t f = cur_e.lenf;
+        p.lo = min(max((long long)cur_e.rs, 0ll), ne);
+        p.hi = min(p.lo + (long long)(f & 0xffffu), ne);
+        if (fresh) {
+            base = p.lo & ~7ll;
+            fresh = false;
+        }
+        p.base = base;
+        p.age = min((int)((f >> 16) & 0xff), kMaxAge);
+        p.qs = (int)((f >> 27) & 15);
+        p.xp0 = cur_e.xp0;
+        p.valid = p.base < p.hi;
+        if (p.valid) {
+            // (entries up to 7 past the last edge lie in the next array of
+            // the graph buffer; they are never used)
+            const long long e0 = min(p.base + lane * kDfU, (p.hi - 1) & ~7ll);
+            const int4 *cv = reinterpret_cast<const int4 *>(col + e0);
+            const float4 *wv = reinterpret_cast<const float4 *>(wgt + e0);
+            p.c[0] = cv[0];
+            p.c[1] = cv[1];
+            p.w[0] = wv[0];
+            p.w[1] = wv[1];
+        }
+        base += kDfPart;
+        if (base >= p.hi) {  // the next row
+            d += stride;
+            cur_e = nxt_e;
+            fresh = true;
+            nxt_e = PbEvent{};
+            if (d + stride < nd) nxt_e = evd[d + stride];
+        }
+    };
+    long long written = 0;
+    auto step = [&](DfPart &p) {
+        if (!p.valid) return;  // wave-uniform
+        const int age = p.age, qs = min(p.qs, B - 1);
+        const int sft = B - 1 - qs;
+        const uint32_t bm = age > qs ? 0xffffu : ((1u << age) - 1u);  // block bits in the window
+        const int lth = age - qs - 1;  // a spike before the block: bit last + qs + 1 < age
+        const long long e0 = p.base + lane * kDfU;
+        const int cj[kDfU] = {p.c[0].x, p.c[0].y, p.c[0].z, p.c[0].w,
+                              p.c[1].x, p.c[1].y, p.c[1].z, p.c[1].w};
+        const float wj[kDfU] = {p.w[0].x, p.w[0].y, p.w[0].z, p.w[0].w,
+                                p.w[1].x, p.w[1].y, p.w[1].z, p.w[1].w};
+        uint32_t code[kDfU];
+#pragma unroll
+        for (int v = 0; v < kDfU; ++v) code[v] = dcode[min(max(cj[v], 0), n - 1)];
+        bool cand[kDfU];
+#pragma unroll
+        for (int v = 0; v < kDfU; ++v) {
+            const long long e = e0 + v;
+            const bool in = e >= p.lo && e < p.hi;
+            if (in && (unsigned)cj[v] >= (unsigned)n) atomicOr(b.err, kErrIndex);
+            const uint32_t c = code[v];
+            cand[v] = in && (unsigned)cj[v] < (unsigned)n &&
+                      (!b.event || (((c & 0xffffu) >> sft) & bm) != 0u ||
+                       (int)((c >> 16) & 0xff) < lth);
+        }
+        int *qe = q_e[wave], *qj = q_j[wave];
+        uint32_t *qc = q_c[wave];
+        float *qw = q_w[wave];
+        int qn = 0;
+#pragma unroll
+        for (int v = 0; v < kDfU; ++v) {
+            const uint64_t bl = ballot64(cand[v]);
+            if (cand[v]) {
+                const int x = qn + lane_rank(bl);
+                qe[x] = (int)(e0 + v);
+                qj[x] = cj[v];
+                qc[x] = code[v];
+                qw[x] = wj[v];
+            }
+            qn += (int)__popcll(bl);
+        }
+        __builtin_amdgcn_wave_barrier();
+        uint64_t m0, m1;
+        window_masks(age, m0, m1);
+        const float xp0 = p.xp0;
+        const float xpn = __fadd_rn(__fmul_rn(xp0, s_dpow[age]), 0.f);  // no pre spike
+        for (int x0 = 0; x0 < qn; x0 += kWave) {  // wave-uniform
+            const int x = x0 + lane;
+            if (x >= qn) continue;
+            const int j = qj[x];
+            const uint32_t c = qc[x];
+            const uint64_t s0 = hst[(int64_t)j * HW];
+            const uint64_t s1 = HW == 2 ? hst[(int64_t)j * 2 + 1] : 0ull;
+            const uint64_t h0 = ((s0 << (qs + 1)) | (uint64_t)((c & 0xffffu) >> sft)) & m0;
+            const uint64_t h1 = HW == 2 ? ((s1 << (qs + 1)) | (s0 >> (63 - qs))) & m1 : 0ull;
+            float w = qw[x];
+            w = b.event ? stdp_synapse(w, h0, h1, age, 0, xp0, xpn, 0.f, s_dpow, c_pot, c_dep, mu)
+                        : stdp_synapse_steps(w, h0, h1, age, 0, xp0, xpn, 0.f, s_dpow[1], c_pot,
+                                             c_dep, mu);
+            wgt[qe[x]] = w;
+            ++written;
+        }
+        __builtin_amdgcn_wave_barrier();  // the queue is rewritten next
+    };
+    __syncthreads();  // s_dpow
+    DfPart P0, P1;
+    issue(P0);
+    issue(P1);
+    while (P0.valid || P1.valid || d < nd) {  // wave-uniform
+        step(P0);
+        issue(P0);
+        step(P1);
+        issue(P1);
+    }
+    written = block_sum_i64_n<kDfBlock>(written, sh);
+    if (tid == 0 && written) add_stat(b.syn_stats + (blockIdx.x % b.syn_slots), written);
 }
 
 // ---------------------------------------------------------------------------
@@ -692,7 +889,7 @@ hipError_t launch_run(hipStream_t s, const NeuronArgs &a, const BlockArgs &b)
 
 hipError_t launch_block_plan(hipStream_t s, const BlockArgs &b)
 {
-    if (b.steps < 1 || b.steps > kBatchMax || b.steps > b.delay - 1 || b.n < 1 ||
+    if (b.steps < 1 || b.steps > kPbMaxSteps || b.steps > b.delay - 1 || b.n < 1 ||
         b.n > kPbMaxN || b.status_stride < blocks_for(b.n, kPbPlanBlock) ||
         (int64_t)b.status_stride * kBatchMax > b.status_words)
         return hipErrorInvalidValue;
@@ -703,7 +900,7 @@ hipError_t launch_block_plan(hipStream_t s, const BlockArgs &b)
 
 hipError_t launch_block_run(hipStream_t s, const NeuronArgs &a, const BlockArgs &b)
 {
-    if (b.steps < 1 || b.steps > kBatchMax || b.gwidth < 1 || b.gwidth > kPbMaxWidth ||
+    if (b.steps < 1 || b.steps > kPbMaxSteps || b.gwidth < 1 || b.gwidth > kPbMaxWidth ||
         b.n_edges < 1 || b.n_edges > INT32_MAX ||
         b.width % b.gwidth != 0 || (int64_t)b.n_groups * b.gwidth < a.n ||
         (int64_t)(b.n_groups - 1) * b.gwidth >= a.n || a.n != b.n || b.nacc < 1 || b.nacc > 2 ||
@@ -712,6 +909,21 @@ hipError_t launch_block_run(hipStream_t s, const NeuronArgs &a, const BlockArgs 
     const bool ct = b.col16 != nullptr;
     if (a.hw == 2) return ct ? launch_run<2, true>(s, a, b) : launch_run<2, false>(s, a, b);
     return ct ? launch_run<1, true>(s, a, b) : launch_run<1, false>(s, a, b);
+}
+
+hipError_t launch_block_deferred(hipStream_t s, const BlockArgs &b)
+{
+    if (b.steps < 1 || b.steps > kPbMaxSteps || b.n < 1 || b.n_edges < 1 ||
+        b.n_edges > INT32_MAX || b.n_cu < 1 || b.syn_slots < 1 || (b.hw != 1 && b.hw != 2))
+        return hipErrorInvalidValue;
+    const int grid = (int)std::min<int64_t>((int64_t)b.n_cu * kDfPerCu,
+                                            ((int64_t)b.n + kDfBlock / kWave - 1) /
+                                                (kDfBlock / kWave));
+    if (b.hw == 2)
+        hipLaunchKernelGGL(k_block_deferred<2>, dim3(grid), dim3(kDfBlock), 0, s, b);
+    else
+        hipLaunchKernelGGL(k_block_deferred<1>, dim3(grid), dim3(kDfBlock), 0, s, b);
+    return hipGetLastError();
 }
 
 hipError_t launch_block_finish(hipStream_t s, const BlockArgs &b)

@@ -127,6 +127,8 @@ struct snn_ctx {
     int32_t *gpiv = nullptr;
     PbEvent *pev = nullptr;
     int32_t *pev_cnt = nullptr;
+    uint32_t *pdcode = nullptr;
+    uint64_t *phstart = nullptr;
     BlockClock *bclk = nullptr;
 
     // graph
@@ -358,14 +360,14 @@ void derive(snn_ctx *c)
         if (bb > c->dlv_slots) c->dlv_slots = (int32_t)bb;
     }
     c->info_blocks = c->nblk;  // statistics slots of the neuron-kernel / flush snapshots
-    // Plastic blocks (BlockArgs) of up to D-1 steps (at most kBatchMax): lazy
+    // Plastic blocks (BlockArgs) of up to D-1 steps (at most kPbMaxSteps): lazy
     // plasticity, D >= 2, up to kPbMaxN neurons. Target groups of 64, 128
     // or 256 neurons inside slices, one workgroup each: the narrowest that
     // needs no more workgroups than the device has CUs, else the widest.
     c->pb_max = c->pb_width = c->pb_groups = 0;
     if (c->n_plastic_rows > 0 && c->algo != 2 && c->delay >= 2 && k.n <= kPbMaxN &&
         k.plastic_blocks >= 0) {
-        int32_t bm = std::min<int32_t>(c->delay - 1, kBatchMax);
+        int32_t bm = std::min<int32_t>(c->delay - 1, kPbMaxSteps);
         if (k.plastic_blocks > 0) bm = std::min<int32_t>(bm, k.plastic_blocks);
         int32_t gw = k.plastic_block_width;
         if (gw == 0) {
@@ -436,8 +438,10 @@ void plan_workspace(snn_ctx *c, uint8_t *base)
     c->syn_stats = p.take<int64_t>(c->syn_slots);
     c->dlv_stats = p.take<int64_t>(2 * (int64_t)c->dlv_slots);
     c->abatch = p.take<long long>(c->batch_max > 0 ? (int64_t)c->batch_max * c->nacc * n : 1);
-    c->pev = p.take<PbEvent>(c->pb_max > 0 ? (int64_t)c->pb_max * n : 1);
+    c->pev = p.take<PbEvent>(c->pb_max > 0 ? (int64_t)(c->pb_max + 1) * n : 1);
     c->pev_cnt = p.take<int32_t>(kBatchMax);
+    c->pdcode = p.take<uint32_t>(c->pb_max > 0 ? n : 1);
+    c->phstart = p.take<uint64_t>(c->pb_max > 0 ? n * c->hw : 1);
     c->bclk = p.take<BlockClock>(1);
     c->ws_need = p.off;
 }
@@ -636,6 +640,9 @@ BlockArgs block_args(snn_ctx *c, int32_t steps)
     b.status_words = c->status_words;
     b.ev = c->pev;
     b.ev_cnt = c->pev_cnt;
+    b.dcode = c->pdcode;
+    b.hstart = c->phstart;
+    b.n_cu = c->n_cu;
     b.bclk = c->bclk;
     b.clk = c->clk;
     b.info_stats = c->info_stats;
@@ -1436,6 +1443,8 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
             if ((st = check_hip(c, launch_block_plan(c->stream, b), "plastic block plan")))
                 return st;
             if ((st = check_hip(c, launch_block_run(c->stream, a, b), "plastic block run")))
+                return st;
+            if ((st = check_hip(c, launch_block_deferred(c->stream, b), "plastic block deferred")))
                 return st;
             c->t += B;
             q += B;

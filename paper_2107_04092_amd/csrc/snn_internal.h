@@ -337,7 +337,11 @@ constexpr int64_t kBatchBytes = 256ll << 20;  // most workspace for a block's pa
 // as the neuron update would (transmitting: history bit D-1 of the step;
 // forced: idle for 64 hw steps), and writes each step's list of row updates
 // (PbEvent), ascending, by one decoupled look-back per step, and commits
-// t_last and x_pre after the block. A group finds a row's entries with
+// t_last and x_pre after the block. A forced update that is its row's last
+// event of the block delivers nothing and no later event of the block reads
+// its weights: it goes to one more list, the deferred updates, which the run
+// computes after the block's last step from the targets' histories at the
+// update's step (the history at block start and the block's spike bits). A group finds a row's entries with
 // targets in the group from the pivot table at group granularity
 // (gpiv[k][g] = the row-relative first entry of row k with a target >=
 // g gwidth, g = 0..n_groups; the pivot kernel with gwidth for the slice
@@ -356,7 +360,8 @@ struct BlockClock {
 struct PbEvent {
     int32_t rs;      // first edge of the row
     uint32_t lenf;   // plastic prefix length (bits 0-15), age (16-23), pre spike (24),
-                     // transmitting (25), inhibitory source of a CUBA network (26)
+                     // transmitting (25), inhibitory source of a CUBA network (26),
+                     // step in the block (27-30)
     float xp0;       // pre trace at the row's previous update
     int32_t k;       // the row
 };
@@ -368,7 +373,9 @@ constexpr int kPbUnroll = 16;       // flattened entries per thread per window
 constexpr int kPbWindow = kPbBlock * kPbUnroll;
 constexpr int kPbRecords = 5120;    // a block's records a workgroup holds in LDS
 constexpr int kPbMaxN = 65536;      // largest network the blocks run
-static_assert(kPbPlanBlock / 32 >= kBatchMax, "a half wave per step's list scan");
+constexpr int kPbMaxSteps = kBatchMax - 1;  // steps per block: lists 0 .. B-1, deferred list B
+static_assert(kPbPlanBlock / 32 >= kPbMaxSteps + 1, "a half wave per list scan");
+static_assert(kPbMaxSteps < 16, "step in the block fits PbEvent::lenf");
 static_assert(kPbSegs < 65535, "16-bit segment map");
 struct BlockArgs {
     // plan
@@ -379,8 +386,13 @@ struct BlockArgs {
     float *xpre;
     unsigned long long *status;  // [kBatchMax][status_stride] look-back words
     int32_t status_stride;
-    PbEvent *ev;                 // [steps][n]: step k's rows at ev + k n
-    int32_t *ev_cnt;             // [kBatchMax]
+    PbEvent *ev;                 // [steps + 1][n]: step k's rows at ev + k n, the deferred
+                                 // forced updates at ev + steps n
+    int32_t *ev_cnt;             // [kBatchMax]: the lists' lengths
+    uint32_t *dcode;             // [n] run -> deferred: the block's spikes (bits 0-15, bit 0 =
+                                 // its last step), bit of the latest spike before it (16-23)
+    uint64_t *hstart;            // [n][hw] run -> deferred: history words at block start
+    int32_t n_cu;
     BlockClock *bclk;            // written by the plan, read by the run
     StepClock *clk;              // read by the plan, advanced by the run
     int64_t *info_stats;         // plan: rows, forced rows, synapses (kStFields per slot)
@@ -411,6 +423,7 @@ struct BlockArgs {
 };
 hipError_t launch_block_plan(hipStream_t s, const BlockArgs &b);
 hipError_t launch_block_run(hipStream_t s, const NeuronArgs &a, const BlockArgs &b);
+hipError_t launch_block_deferred(hipStream_t s, const BlockArgs &b);
 hipError_t launch_block_finish(hipStream_t s, const BlockArgs &b);
 
 // Optional events placed by a launch itself around the kernel

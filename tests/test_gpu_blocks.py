@@ -114,7 +114,7 @@ def test_blocks_equal_stepwise(case):
     a = gpu_net(p, width, chunks, **extra)
     b = gpu_net(p, width, chunks, **dict(extra, plastic_blocks=-1))
     ga = a.graph()
-    assert ga["block_steps"] == min(p.delay - 1, 16, extra.get("plastic_blocks", 0) or 16)
+    assert ga["block_steps"] == min(p.delay - 1, 15, extra.get("plastic_blocks", 0) or 15)
     assert ga["block_width"] == extra.get("plastic_block_width", ga["block_width"])
     assert b.graph()["block_steps"] == 0
     # uneven calls: a block cut short at the end of each call
