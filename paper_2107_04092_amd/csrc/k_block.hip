@@ -601,12 +601,19 @@ __global__ __launch_bounds__(kPbBlock) void k_block_run(NeuronArgs a, BlockArgs 
         a.code[i] = hist_code(st.h0, st.h1);
         b.apart[i] = s_acc[tid];
         if (b.nacc == 2) b.apart[n + i] = s_acc[kPbMaxWidth + tid];
-        b.hstart[(int64_t)i * HW] = hs0;
-        if (HW == 2) b.hstart[(int64_t)i * 2 + 1] = hs1;
-        // the latest spike before the block: its bit in the words at block start
+        uint64_t *hqi = b.hq + (int64_t)i * (2 * HW);
+        hqi[0] = hs0;
+        if (HW == 2) hqi[1] = hs1;
+        hqi[HW] = blk;
+        // the code of the deferred updates: the first step of the block with
+        // a spike (15: none), and the bit L of the latest spike before it
+        // against the window of a forced update at step q (L + q + 1 < 64 hw,
+        // q < 15): 0 if always inside, 15 if never, else L - (64 hw - 16)
+        const int first = blk ? B - 1 - (31 - __clz((int)blk)) : 15;
         const int last = hs0 ? __ffsll((long long)hs0) - 1
-                             : (HW == 2 && hs1) ? 63 + __ffsll((long long)hs1) : 255;
-        b.dcode[i] = blk | ((uint32_t)last << 16);
+                             : (HW == 2 && hs1) ? 63 + __ffsll((long long)hs1) : 1 << 20;
+        const int lc = last <= 64 * HW - 16 ? 0 : last >= 64 * HW - 1 ? 15 : last - (64 * HW - 16);
+        b.dcode[i] = (uint8_t)(first | (lc << 4));
     }
     events = block_sum_i64_n<kPbBlock>(events, sh);
     w_tx = block_sum_i64_n<kPbBlock>(w_tx, sh);
@@ -629,23 +636,28 @@ __global__ __launch_bounds__(kPbBlock) void k_block_run(NeuronArgs a, BlockArgs 
 
 // ---------------------------------------------------------------------------
 // The deferred forced updates of a block (the plan's list B), after its run,
-// streamed by the whole device: each wave takes whole rows (their plastic
-// entries, from the row's first 8-aligned entry on, kDfPart at a time, each
-// lane 8 consecutive targets and weights in 16-byte loads), the next part
-// loaded while the current one is computed.
-//   An update at step t = t0 + q (age a) changes the synapses whose target
-// spiked in the window (t - a, t] (all of them without event-driven replay).
-// The target's history word at t is its word at block start shifted up by
-// q + 1 steps, under the block's spike bits of steps t0 .. t (Sec. III-A's
-// bit history), so the target's code (the block's spikes, and the bit of its
-// latest spike before the block) decides whether a synapse changes; the
-// synapses that do are queued and brought up to date 64 at a time with the
-// words at block start.
+// streamed by the whole device: one workgroup per CU, the rows' plastic
+// entries (from each row's first 8-aligned entry on) cut into parts of
+// kDfPart, spread over the waves (each lane 8 consecutive targets and
+// weights in 16-byte loads), the next part loaded while the current one is
+// computed.
+//   An update at step t = t0 + q changes the synapses whose target spiked in
+// the window (t - a, t] (every one without event-driven replay). The
+// target's history word at t is its word at block start shifted up by q + 1
+// steps, under the block's spike bits of steps t0 .. t (Sec. III-A's bit
+// history). A forced update has the longest age, a = 64 hw (> q), so a
+// synapse changes iff its target spiked in the block at a step <= q, or
+// before the block at bit L of the start words with L + q + 1 < a: one byte
+// per target holds both (the first spike step in the block; L against the
+// last 15 bits of the window), staged in LDS. The synapses that pass are
+// queued and brought up to date 64 at a time from the full words (hq), which
+// decide exactly (an update of another age queues every entry).
 
-constexpr int kDfBlock = 256;
-constexpr int kDfU = 8;                 // entries per lane per part
-constexpr int kDfPart = kDfU * kWave;   // entries per part of a row
-constexpr int kDfPerCu = 4;             // workgroups per CU (LDS: four queues each)
+constexpr int kDfBlock = 1024;
+constexpr int kDfPart = kPbDfPart;      // entries per part of a row
+constexpr int kDfU = kDfPart / kWave;   // entries per lane per part
+static_assert(kDfU == 8, "two 16-byte loads of targets and of weights per lane");
+static_assert(kPbMaxN <= 65536, "target in 16 bits of the queue word");
 
 struct DfPart {
     int4 c[2];
@@ -660,11 +672,11 @@ template <int HW>
 __global__ __launch_bounds__(kDfBlock) void k_block_deferred(BlockArgs b)
 {
     constexpr int NWV = kDfBlock / kWave;
+    constexpr int A = 64 * HW;  // the age of a forced update
+    __shared__ uint8_t s_code[kPbMaxN];
+    __shared__ int q_p[NWV][kDfPart];    // target (bits 0-15), entry in the part (16-24)
+    __shared__ float q_w[NWV][kDfPart];  // weight
     __shared__ float s_dpow[kMaxAge + 1];
-    __shared__ int q_e[NWV][kDfPart];        // edge index
-    __shared__ int q_j[NWV][kDfPart];        // target
-    __shared__ uint32_t q_c[NWV][kDfPart];   // target's code
-    __shared__ float q_w[NWV][kDfPart];      // weight
     __shared__ long long sh[NWV];
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
     const int n = b.n, B = b.steps;
@@ -672,82 +684,121 @@ __global__ __launch_bounds__(kDfBlock) void k_block_deferred(BlockArgs b)
     const PbEvent *__restrict__ evd = b.ev + (int64_t)B * n;
     const int32_t *__restrict__ col = b.col;
     float *__restrict__ wgt = b.w;
-    const uint32_t *__restrict__ dcode = b.dcode;
-    const uint64_t *__restrict__ hst = b.hstart;
+    const uint64_t *__restrict__ hq = b.hq;
     const long long ne = (long long)b.n_edges;  // < 2^31
     const float c_pot = b.c_pot, c_dep = b.c_dep, mu = b.mu;
-    for (int x = tid; x <= kMaxAge; x += kDfBlock) s_dpow[x] = b.dpow[x];
+    // the targets' codes (padded to 16 bytes), loaded first: every later
+    // load of the wave completes after them
+    constexpr int kCodeLoads = kPbMaxN / 16 / kDfBlock;
+    uint4 cl[kCodeLoads];
+    const int ncv = (n + 15) / 16;
+#pragma unroll
+    for (int u = 0; u < kCodeLoads; ++u)
+        cl[u] = reinterpret_cast<const uint4 *>(b.dcode)[min(u * kDfBlock + tid, ncv - 1)];
+    // Items: part p of row r is item r P + p (P = parts of the longest
+    // row); the wave takes items w0 + j stride, j = 0 .. nit - 1. Lane l
+    // holds the record of the row of item (j & ~63) + l, read out for the
+    // current item j (no load inside the part stream waits on a record).
+    const int P = b.df_parts;
     const int stride = gridDim.x * NWV;
-    // the wave's rows d, d + stride, ...: the current one and the next
-    int d = blockIdx.x * NWV + wave;
-    PbEvent cur_e = PbEvent{}, nxt_e = PbEvent{};
-    if (d < nd) cur_e = evd[d];
-    if (d + stride < nd) nxt_e = evd[d + stride];
-    long long base = 0;
-    bool fresh = true;  // base not yet set for row d
-    auto issue = [&](DfPart &p) {
-        p.valid = 0;
-        if (d >= nd) return;  // wave-uniform
-        const uint32_t f = cur_e.lenf;
-        p.lo = min(max((long long)cur_e.rs, 0ll), ne);
-        p.hi = min(p.lo + (long long)(f & 0xffffu), ne);
-        if (fresh) {
-            base = p.lo & ~7ll;
-            fresh = false;
+    const int w0 = blockIdx.x * NWV + wave;
+    const long long nitems = (long long)nd * P;
+    const int nit = w0 < nitems ? (int)((nitems - 1 - w0) / stride + 1) : 0;
+    PbEvent le = PbEvent{};
+    int j = 0;
+    long long base = 0, r_lo = 0, r_hi = 0;  // the current item's part, its row's entries
+    int r_age = 0, r_qs = 0;
+    float r_xp0 = 0.f;
+    auto set_item = [&]() {  // j < nit
+        if ((j & 63) == 0) {
+            const long long it = w0 + (long long)(j + lane) * stride;
+            le = j + lane < nit ? evd[it / P] : PbEvent{};
         }
-        p.base = base;
-        p.age = min((int)((f >> 16) & 0xff), kMaxAge);
-        p.qs = (int)((f >> 27) & 15);
-        p.xp0 = cur_e.xp0;
-        p.valid = p.base < p.hi;
-        if (p.valid) {
-            // (entries up to 7 past the last edge lie in the next array of
-            // the graph buffer; they are never used)
-            const long long e0 = min(p.base + lane * kDfU, (p.hi - 1) & ~7ll);
-            const int4 *cv = reinterpret_cast<const int4 *>(col + e0);
-            const float4 *wv = reinterpret_cast<const float4 *>(wgt + e0);
-            p.c[0] = cv[0];
-            p.c[1] = cv[1];
-            p.w[0] = wv[0];
-            p.w[1] = wv[1];
-        }
-        base += kDfPart;
-        if (base >= p.hi) {  // the next row
-            d += stride;
-            cur_e = nxt_e;
-            fresh = true;
-            nxt_e = PbEvent{};
-            if (d + stride < nd) nxt_e = evd[d + stride];
-        }
+        const int src = j & 63;
+        const long long rs = __builtin_amdgcn_readlane(le.rs, src);
+        const uint32_t f = (uint32_t)__builtin_amdgcn_readlane((int)le.lenf, src);
+        r_xp0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(le.xp0), src));
+        r_lo = min(max(rs, 0ll), ne);
+        r_hi = min(r_lo + (long long)(f & 0xffffu), ne);
+        base = (r_lo & ~7ll) + (long long)((w0 + (long long)j * stride) % P) * kDfPart;
+        r_age = min((int)((f >> 16) & 0xff), kMaxAge);
+        r_qs = (int)((f >> 27) & 15);
     };
+    if (nit > 0) set_item();
+    // the next part's loads, from a valid address whether or not the part
+    // exists, so that every part issues the same loads
+    auto issue = [&](DfPart &p) {
+        p.valid = j < nit && base < r_hi;
+        p.base = base;
+        p.lo = r_lo;
+        p.hi = r_hi;
+        p.age = r_age;
+        p.qs = r_qs;
+        p.xp0 = r_xp0;
+        // (entries up to 7 past the last edge lie in the next array of the
+        // graph buffer; they are never used)
+        const long long e0 = p.valid ? min(base + lane * kDfU, (r_hi - 1) & ~7ll) : 0ll;
+        const int4 *cv = reinterpret_cast<const int4 *>(col + e0);
+        const float4 *wv = reinterpret_cast<const float4 *>(wgt + e0);
+        p.c[0] = cv[0];
+        p.c[1] = cv[1];
+        p.w[0] = wv[0];
+        p.w[1] = wv[1];
+        if (j < nit && ++j < nit) set_item();  // wave-uniform
+    };
+    DfPart P0, P1;
+    issue(P0);
+    issue(P1);
+#pragma unroll
+    for (int u = 0; u < kCodeLoads; ++u)
+        if (u * kDfBlock + tid < ncv) reinterpret_cast<uint4 *>(s_code)[u * kDfBlock + tid] = cl[u];
+    for (int x = tid; x <= kMaxAge; x += kDfBlock) s_dpow[x] = b.dpow[x];
+    __syncthreads();
     long long written = 0;
+    // The history words of the first kDfRounds rounds of the queue are
+    // gathered before the next part's loads are issued (a wave's loads
+    // complete in order: waiting for a later gather waits for every earlier
+    // load), so that part loads while this one is brought up to date.
+    constexpr int kDfRounds = 2;
+    auto words_of = [&](int j, uint64_t &s0, uint64_t &s1, uint64_t &blk) {
+        const uint4 *hj = reinterpret_cast<const uint4 *>(hq + (int64_t)j * (2 * HW));
+        const uint4 v0 = hj[0];
+        if (HW == 2) {
+            const uint4 v1 = hj[1];
+            s1 = (uint64_t)v0.z | ((uint64_t)v0.w << 32);
+            blk = (uint64_t)v1.x | ((uint64_t)v1.y << 32);
+        } else {
+            s1 = 0ull;
+            blk = (uint64_t)v0.z | ((uint64_t)v0.w << 32);
+        }
+        s0 = (uint64_t)v0.x | ((uint64_t)v0.y << 32);
+    };
+    // a part, then the next part's loads into p
     auto step = [&](DfPart &p) {
-        if (!p.valid) return;  // wave-uniform
+        if (!p.valid) {  // wave-uniform
+            issue(p);
+            return;
+        }
         const int age = p.age, qs = min(p.qs, B - 1);
-        const int sft = B - 1 - qs;
-        const uint32_t bm = age > qs ? 0xffffu : ((1u << age) - 1u);  // block bits in the window
-        const int lth = age - qs - 1;  // a spike before the block: bit last + qs + 1 < age
-        const long long e0 = p.base + lane * kDfU;
+        const long long pbase = p.base;
+        const float xp0 = p.xp0;
+        const bool filt = b.event && age == A;  // the codes decide
         const int cj[kDfU] = {p.c[0].x, p.c[0].y, p.c[0].z, p.c[0].w,
                               p.c[1].x, p.c[1].y, p.c[1].z, p.c[1].w};
         const float wj[kDfU] = {p.w[0].x, p.w[0].y, p.w[0].z, p.w[0].w,
                                 p.w[1].x, p.w[1].y, p.w[1].z, p.w[1].w};
-        uint32_t code[kDfU];
-#pragma unroll
-        for (int v = 0; v < kDfU; ++v) code[v] = dcode[min(max(cj[v], 0), n - 1)];
+        const long long e0 = pbase + lane * kDfU;
         bool cand[kDfU];
 #pragma unroll
         for (int v = 0; v < kDfU; ++v) {
             const long long e = e0 + v;
             const bool in = e >= p.lo && e < p.hi;
-            if (in && (unsigned)cj[v] >= (unsigned)n) atomicOr(b.err, kErrIndex);
-            const uint32_t c = code[v];
-            cand[v] = in && (unsigned)cj[v] < (unsigned)n &&
-                      (!b.event || (((c & 0xffffu) >> sft) & bm) != 0u ||
-                       (int)((c >> 16) & 0xff) < lth);
+            const bool okj = (unsigned)cj[v] < (unsigned)n;
+            if (in && !okj) atomicOr(b.err, kErrIndex);
+            const int c = s_code[okj ? cj[v] : 0];
+            cand[v] = in && okj && (!filt || (c & 15) <= qs || (c >> 4) + qs < 15);
         }
-        int *qe = q_e[wave], *qj = q_j[wave];
-        uint32_t *qc = q_c[wave];
+        int *qp = q_p[wave];
         float *qw = q_w[wave];
         int qn = 0;
 #pragma unroll
@@ -755,45 +806,54 @@ __global__ __launch_bounds__(kDfBlock) void k_block_deferred(BlockArgs b)
             const uint64_t bl = ballot64(cand[v]);
             if (cand[v]) {
                 const int x = qn + lane_rank(bl);
-                qe[x] = (int)(e0 + v);
-                qj[x] = cj[v];
-                qc[x] = code[v];
+                qp[x] = cj[v] | ((lane * kDfU + v) << 16);
                 qw[x] = wj[v];
             }
             qn += (int)__popcll(bl);
         }
         __builtin_amdgcn_wave_barrier();
+        uint64_t g0[kDfRounds], g1[kDfRounds], gb[kDfRounds];
+        int gp[kDfRounds];
+#pragma unroll
+        for (int r = 0; r < kDfRounds; ++r) {  // every lane, clamped into the queue
+            const int x = min(r * kWave + lane, max(qn - 1, 0));
+            gp[r] = qn > 0 ? qp[x] : 0;
+            words_of(gp[r] & 0xffff, g0[r], g1[r], gb[r]);
+        }
+        issue(p);
         uint64_t m0, m1;
         window_masks(age, m0, m1);
-        const float xp0 = p.xp0;
+        const int sft = B - 1 - qs;
         const float xpn = __fadd_rn(__fmul_rn(xp0, s_dpow[age]), 0.f);  // no pre spike
-        for (int x0 = 0; x0 < qn; x0 += kWave) {  // wave-uniform
-            const int x = x0 + lane;
-            if (x >= qn) continue;
-            const int j = qj[x];
-            const uint32_t c = qc[x];
-            const uint64_t s0 = hst[(int64_t)j * HW];
-            const uint64_t s1 = HW == 2 ? hst[(int64_t)j * 2 + 1] : 0ull;
-            const uint64_t h0 = ((s0 << (qs + 1)) | (uint64_t)((c & 0xffffu) >> sft)) & m0;
+        auto update = [&](int x, int pk, uint64_t s0, uint64_t s1, uint64_t blk) {
+            const uint64_t h0 = ((s0 << (qs + 1)) | (blk >> sft)) & m0;
             const uint64_t h1 = HW == 2 ? ((s1 << (qs + 1)) | (s0 >> (63 - qs))) & m1 : 0ull;
+            if (b.event && !(h0 | h1)) return;  // unchanged
             float w = qw[x];
             w = b.event ? stdp_synapse(w, h0, h1, age, 0, xp0, xpn, 0.f, s_dpow, c_pot, c_dep, mu)
                         : stdp_synapse_steps(w, h0, h1, age, 0, xp0, xpn, 0.f, s_dpow[1], c_pot,
                                              c_dep, mu);
-            wgt[qe[x]] = w;
+            wgt[pbase + (pk >> 16)] = w;
             ++written;
+        };
+#pragma unroll
+        for (int r = 0; r < kDfRounds; ++r) {
+            const int x = r * kWave + lane;
+            if (x < qn) update(x, gp[r], g0[r], g1[r], gb[r]);
+        }
+        for (int x0 = kDfRounds * kWave; x0 < qn; x0 += kWave) {  // wave-uniform; rare
+            const int x = x0 + lane;
+            if (x >= qn) continue;
+            const int pk = qp[x];
+            uint64_t s0, s1, blk;
+            words_of(pk & 0xffff, s0, s1, blk);
+            update(x, pk, s0, s1, blk);
         }
         __builtin_amdgcn_wave_barrier();  // the queue is rewritten next
     };
-    __syncthreads();  // s_dpow
-    DfPart P0, P1;
-    issue(P0);
-    issue(P1);
-    while (P0.valid || P1.valid || d < nd) {  // wave-uniform
+    while (P0.valid || P1.valid || j < nit) {  // wave-uniform
         step(P0);
-        issue(P0);
         step(P1);
-        issue(P1);
     }
     written = block_sum_i64_n<kDfBlock>(written, sh);
     if (tid == 0 && written) add_stat(b.syn_stats + (blockIdx.x % b.syn_slots), written);
@@ -913,12 +973,12 @@ hipError_t launch_block_run(hipStream_t s, const NeuronArgs &a, const BlockArgs 
 
 hipError_t launch_block_deferred(hipStream_t s, const BlockArgs &b)
 {
-    if (b.steps < 1 || b.steps > kPbMaxSteps || b.n < 1 || b.n_edges < 1 ||
-        b.n_edges > INT32_MAX || b.n_cu < 1 || b.syn_slots < 1 || (b.hw != 1 && b.hw != 2))
+    if (b.steps < 1 || b.steps > kPbMaxSteps || b.n < 1 || b.n > kPbMaxN || b.n_edges < 1 ||
+        b.n_edges > INT32_MAX || b.n_cu < 1 || b.syn_slots < 1 || (b.hw != 1 && b.hw != 2) ||
+        b.df_parts < 1 || b.df_parts > (kMaxSortRow + 7 + kDfPart - 1) / kDfPart)
         return hipErrorInvalidValue;
-    const int grid = (int)std::min<int64_t>((int64_t)b.n_cu * kDfPerCu,
-                                            ((int64_t)b.n + kDfBlock / kWave - 1) /
-                                                (kDfBlock / kWave));
+    const int grid = (int)std::min<int64_t>(
+        (int64_t)b.n_cu, ((int64_t)b.n * b.df_parts + kDfBlock / kWave - 1) / (kDfBlock / kWave));
     if (b.hw == 2)
         hipLaunchKernelGGL(k_block_deferred<2>, dim3(grid), dim3(kDfBlock), 0, s, b);
     else

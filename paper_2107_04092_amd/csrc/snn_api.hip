@@ -127,8 +127,8 @@ struct snn_ctx {
     int32_t *gpiv = nullptr;
     PbEvent *pev = nullptr;
     int32_t *pev_cnt = nullptr;
-    uint32_t *pdcode = nullptr;
-    uint64_t *phstart = nullptr;
+    uint8_t *pdcode = nullptr;
+    uint64_t *phq = nullptr;
     BlockClock *bclk = nullptr;
 
     // graph
@@ -440,8 +440,8 @@ void plan_workspace(snn_ctx *c, uint8_t *base)
     c->abatch = p.take<long long>(c->batch_max > 0 ? (int64_t)c->batch_max * c->nacc * n : 1);
     c->pev = p.take<PbEvent>(c->pb_max > 0 ? (int64_t)(c->pb_max + 1) * n : 1);
     c->pev_cnt = p.take<int32_t>(kBatchMax);
-    c->pdcode = p.take<uint32_t>(c->pb_max > 0 ? n : 1);
-    c->phstart = p.take<uint64_t>(c->pb_max > 0 ? n * c->hw : 1);
+    c->pdcode = p.take<uint8_t>(c->pb_max > 0 ? (n + 15) / 16 * 16 : 1);
+    c->phq = p.take<uint64_t>(c->pb_max > 0 ? 2 * n * c->hw : 1);
     c->bclk = p.take<BlockClock>(1);
     c->ws_need = p.off;
 }
@@ -641,8 +641,10 @@ BlockArgs block_args(snn_ctx *c, int32_t steps)
     b.ev = c->pev;
     b.ev_cnt = c->pev_cnt;
     b.dcode = c->pdcode;
-    b.hstart = c->phstart;
+    b.hq = c->phq;
     b.n_cu = c->n_cu;
+    b.df_parts = (int32_t)std::max<int64_t>(1, ((int64_t)c->max_row + 7 + kPbDfPart - 1) /
+                                                   kPbDfPart);
     b.bclk = c->bclk;
     b.clk = c->clk;
     b.info_stats = c->info_stats;

@@ -374,6 +374,7 @@ constexpr int kPbWindow = kPbBlock * kPbUnroll;
 constexpr int kPbRecords = 5120;    // a block's records a workgroup holds in LDS
 constexpr int kPbMaxN = 65536;      // largest network the blocks run
 constexpr int kPbMaxSteps = kBatchMax - 1;  // steps per block: lists 0 .. B-1, deferred list B
+constexpr int kPbDfPart = 8 * 64;   // entries per part of a deferred row (8 per lane)
 static_assert(kPbPlanBlock / 32 >= kPbMaxSteps + 1, "a half wave per list scan");
 static_assert(kPbMaxSteps < 16, "step in the block fits PbEvent::lenf");
 static_assert(kPbSegs < 65535, "16-bit segment map");
@@ -389,10 +390,13 @@ struct BlockArgs {
     PbEvent *ev;                 // [steps + 1][n]: step k's rows at ev + k n, the deferred
                                  // forced updates at ev + steps n
     int32_t *ev_cnt;             // [kBatchMax]: the lists' lengths
-    uint32_t *dcode;             // [n] run -> deferred: the block's spikes (bits 0-15, bit 0 =
-                                 // its last step), bit of the latest spike before it (16-23)
-    uint64_t *hstart;            // [n][hw] run -> deferred: history words at block start
+    uint8_t *dcode;              // [n, padded to 16] run -> deferred: per target, the first
+                                 // spike step of the block (bits 0-3), the latest spike before
+                                 // it against a forced window (4-7)
+    uint64_t *hq;                // [n][2 hw] run -> deferred: history words at block start,
+                                 // then the block's spikes (bit 0: its last step)
     int32_t n_cu;
+    int32_t df_parts;            // parts of kDfPart entries of the longest row (deferred)
     BlockClock *bclk;            // written by the plan, read by the run
     StepClock *clk;              // read by the plan, advanced by the run
     int64_t *info_stats;         // plan: rows, forced rows, synapses (kStFields per slot)
