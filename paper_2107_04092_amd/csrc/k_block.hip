@@ -24,15 +24,20 @@ namespace {
 // and only before its first transmission; a forced update that is the row's
 // last event of the block goes to the deferred list (list B) instead of its
 // step's. The steps are walked twice: once for the event flags (each list's
-// counts, scanned over the workgroups by a decoupled look-back, one scan per
-// list), then for the snapshots (PbEvent), written at their positions in
-// their list, ascending.
+// count in the workgroup, which one atomic add per list turns into the
+// workgroup's place in the list), then for the snapshots (PbEvent), written
+// at their positions. A list is ascending inside each workgroup's share; the
+// shares come in the order the workgroups arrive, and no result depends on
+// the order (the run accumulates in exact fixed point and every synapse's
+// update is its own).
 
 __global__ __launch_bounds__(kPbPlanBlock) void k_block_plan(BlockArgs b)
 {
     constexpr int NWV = kPbPlanBlock / kWave;
     __shared__ uint64_t s_m[kBatchMax][NWV];
-    __shared__ int s_lb[2 * kBatchMax];
+    __shared__ int s_lb[kBatchMax];
+    __shared__ int s_wp[kBatchMax][NWV];  // events of list q in the waves before
+    __shared__ int s_rq[NWV][kWave];      // a wave's lanes with an event
     __shared__ float s_dpow[kMaxAge + 1];
     __shared__ unsigned long long s_st[kStFields];
     const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
@@ -93,31 +98,47 @@ __global__ __launch_bounds__(kPbPlanBlock) void k_block_plan(BlockArgs b)
         if (lane == 0) s_m[q][wave] = m;
     }
     __syncthreads();  // s_m, s_dpow, s_st
-    // this workgroup's events of list tid, published for the list's scan
-    int own = 0;
+    // this workgroup's place in list tid; the other block's counts cleared
+    // for the next plan (the launches that read them have ended)
     if (tid <= B) {
-        for (int w = 0; w < NWV; ++w) own += __popcll(s_m[tid][w]);
-        publish_status(b.status + (int64_t)tid * b.status_stride + blockIdx.x,
-                       status_word(own, 0, t0 + tid, blockIdx.x == 0 ? kStatusInc : kStatusAgg));
+        int own = 0;
+        for (int w = 0; w < NWV; ++w) {
+            s_wp[tid][w] = own;
+            own += __popcll(s_m[tid][w]);
+        }
+        s_lb[tid] = own ? atomicAdd(b.ev_cnt + tid, own) : 0;
     }
-    lookback32<kPbPlanBlock>(b.status, b.status_stride, B + 1, (int)blockIdx.x, t0, s_lb, b.err);
-    if (tid <= B && blockIdx.x > 0)
-        publish_status(b.status + (int64_t)tid * b.status_stride + blockIdx.x,
-                       status_word(s_lb[2 * tid] + own, 0, t0 + tid, kStatusInc));
-    // the snapshots, at their positions: earlier workgroups, earlier waves,
-    // earlier lanes
-    const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
-    int tl = tl0;
-    float xp = xp0;
+    if (blockIdx.x == 0 && tid < kBatchMax) b.ev_cnt_next[tid] = 0;
+    __syncthreads();  // s_lb
+    // the snapshots, at their positions (the workgroup's place in the list,
+    // then earlier waves, then earlier lanes). A wave's rows with an event
+    // are compacted first: a lane walks one such row's events in order (each
+    // snapshot starts from the one before), with the wave's lanes busy.
+    const uint64_t hm = ballot64(evm != 0u);
+    if (evm != 0u) s_rq[wave][lane_rank(hm)] = lane;
+    __builtin_amdgcn_wave_barrier();
+    const int nq = (int)__popcll(hm);  // wave-uniform
+    const int src = lane < nq ? s_rq[wave][lane] : lane;
+    const int kr = blockIdx.x * kPbPlanBlock + wave * kWave + src;  // the lane's row
+    const uint32_t r_evm = (uint32_t)__shfl((int)evm, src);
+    const uint32_t r_dfm = (uint32_t)__shfl((int)dfm, src);
+    const uint64_t r_h0 = (uint64_t)__shfl((long long)h0, src);
+    const int64_t r_rs = (int64_t)__shfl((long long)rs, src);
+    const int r_tl0 = __shfl(tl0, src), r_pend = __shfl(pend_k, src);
+    const float r_xp0 = __shfl(xp0, src);
+    const bool r_plastic = kr < b.n_plastic_rows;
+    const uint64_t below = src == 0 ? 0ull : (~0ull >> (64 - src));
+    int tl = r_tl0;
+    float xp = r_xp0;
     long long n_rows = 0, n_forced = 0, n_syn = 0, n_fsyn = 0;
-    for (int q = 0; q < B; ++q) {
-        if (!((evm >> q) & 1u)) continue;
+    for (uint32_t m = lane < nq ? r_evm : 0u; m; m &= m - 1u) {
+        const int q = __ffs((int)m) - 1;
         const int64_t t = t0 + q;
-        const int tx = (int)((h0 >> (D - 2 - q)) & 1ull);
+        const int tx = (int)((r_h0 >> (D - 2 - q)) & 1ull);
         RowInfo ri = RowInfo{};
         int ok = 0;
-        if (plastic) {
-            ok = make_row_info_d(ri, k, t, tl, rs, pend_k, xp, tx, hw,
+        if (r_plastic) {
+            ok = make_row_info_d(ri, kr, t, tl, r_rs, r_pend, xp, tx, hw,
                                  s_dpow[row_age_index(t, tl, hw)], b.err);
             if (ok) {
                 tl = (int)t;
@@ -132,26 +153,25 @@ __global__ __launch_bounds__(kPbPlanBlock) void k_block_plan(BlockArgs b)
         }
         // nothing to bring up to date (ok == 0): the row is only delivered
         PbEvent pe;
-        pe.rs = (int32_t)rs;
+        pe.rs = (int32_t)r_rs;
         pe.lenf = ok ? ((uint32_t)ri.len & 0xffffu) | ((uint32_t)(ri.age_pre & 0xff) << 16) |
                            ((uint32_t)((ri.age_pre >> 8) & 1) << 24)
                      : 0u;
-        pe.lenf |= ((uint32_t)tx << 25) | ((uint32_t)(b.nacc == 2 && k >= b.n_exc) << 26) |
+        pe.lenf |= ((uint32_t)tx << 25) | ((uint32_t)(b.nacc == 2 && kr >= b.n_exc) << 26) |
                    ((uint32_t)q << 27);
         pe.xp0 = ok ? ri.xp0 : 0.f;
-        pe.k = k;
-        const int lq = (dfm >> q) & 1u ? B : q;  // the list
-        int pos = s_lb[2 * lq] + __popcll(s_m[lq][wave] & below);
-        for (int w = 0; w < wave; ++w) pos += __popcll(s_m[lq][w]);
-        // (only a failed scan puts a position out of range)
+        pe.k = kr;
+        const int lq = (r_dfm >> q) & 1u ? B : q;  // the list
+        const int pos = s_lb[lq] + s_wp[lq][wave] + (int)__popcll(s_m[lq][wave] & below);
+        // (the counts of a list never exceed n unless they did not start at 0)
         if (pos < b.n)
             b.ev[(int64_t)lq * b.n + pos] = pe;
         else
             atomicOr(b.err, kErrRing);
     }
-    if (plastic && tl != tl0) {  // the row as its last event in the block left it
-        b.t_last[k] = tl;
-        b.xpre[k] = xp;
+    if (lane < nq && r_plastic && tl != r_tl0) {  // the row as its last event left it
+        b.t_last[kr] = tl;
+        b.xpre[kr] = xp;
     }
     n_rows = wave_sum_i64(n_rows);
     n_forced = wave_sum_i64(n_forced);
@@ -167,8 +187,6 @@ __global__ __launch_bounds__(kPbPlanBlock) void k_block_plan(BlockArgs b)
     if (tid < kStFields && s_st[tid])
         add_stat(b.info_stats + (int64_t)(blockIdx.x % b.info_slots) * kStFields + tid,
                  (long long)s_st[tid]);
-    // the last workgroup's scans saw every workgroup: the list totals
-    if (blockIdx.x == gridDim.x - 1 && tid <= B) b.ev_cnt[tid] = s_lb[2 * tid] + own;
 }
 
 // ---------------------------------------------------------------------------
@@ -883,6 +901,10 @@ __global__ __launch_bounds__(kPbFinishBlock) void k_block_finish(BlockArgs b)
     for (int64_t x = (int64_t)q * kPbFinishBlock + tid; x < b.status_words;
          x += (int64_t)gridDim.x * kPbFinishBlock)
         b.status[x] = 0ull;
+    if (q == 0 && tid < kBatchMax) {  // both blocks' list counts, for the next call's plans
+        b.ev_cnt[tid] = 0;
+        b.ev_cnt_next[tid] = 0;
+    }
     if (tid == 0) s_base = 0;
     const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
     const bool lists = q < D;
@@ -950,8 +972,7 @@ hipError_t launch_run(hipStream_t s, const NeuronArgs &a, const BlockArgs &b)
 hipError_t launch_block_plan(hipStream_t s, const BlockArgs &b)
 {
     if (b.steps < 1 || b.steps > kPbMaxSteps || b.steps > b.delay - 1 || b.n < 1 ||
-        b.n > kPbMaxN || b.status_stride < blocks_for(b.n, kPbPlanBlock) ||
-        (int64_t)b.status_stride * kBatchMax > b.status_words)
+        b.n > kPbMaxN || b.ev_cnt == b.ev_cnt_next)
         return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_block_plan, dim3(blocks_for(b.n, kPbPlanBlock)), dim3(kPbPlanBlock), 0,
                        s, b);

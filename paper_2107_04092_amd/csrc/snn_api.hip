@@ -439,7 +439,7 @@ void plan_workspace(snn_ctx *c, uint8_t *base)
     c->dlv_stats = p.take<int64_t>(2 * (int64_t)c->dlv_slots);
     c->abatch = p.take<long long>(c->batch_max > 0 ? (int64_t)c->batch_max * c->nacc * n : 1);
     c->pev = p.take<PbEvent>(c->pb_max > 0 ? (int64_t)(c->pb_max + 1) * n : 1);
-    c->pev_cnt = p.take<int32_t>(kBatchMax);
+    c->pev_cnt = p.take<int32_t>(2 * kBatchMax);  // consecutive blocks alternate halves
     c->pdcode = p.take<uint8_t>(c->pb_max > 0 ? (n + 15) / 16 * 16 : 1);
     c->phq = p.take<uint64_t>(c->pb_max > 0 ? 2 * n * c->hw : 1);
     c->bclk = p.take<BlockClock>(1);
@@ -627,7 +627,9 @@ NeuronArgs neuron_args(snn_ctx *c)
     return a;
 }
 
-BlockArgs block_args(snn_ctx *c, int32_t steps)
+// parity: the block's place in the call (consecutive blocks use the two
+// halves of the list counts in turn)
+BlockArgs block_args(snn_ctx *c, int32_t steps, int32_t parity)
 {
     BlockArgs b{};
     b.row_ptr = c->row_ptr;
@@ -639,7 +641,8 @@ BlockArgs block_args(snn_ctx *c, int32_t steps)
     b.status_stride = c->status_stride;
     b.status_words = c->status_words;
     b.ev = c->pev;
-    b.ev_cnt = c->pev_cnt;
+    b.ev_cnt = c->pev_cnt + (parity & 1) * kBatchMax;
+    b.ev_cnt_next = c->pev_cnt + (~parity & 1) * kBatchMax;
     b.dcode = c->pdcode;
     b.hq = c->phq;
     b.n_cu = c->n_cu;
@@ -1148,6 +1151,7 @@ snn_status snn_bind_workspace(snn_ctx *c, void *device_ptr, size_t bytes)
     if (e == hipSuccess) e = launch_set_clock(c->stream, c->clk, 0, 1, 1);
     if (e == hipSuccess) e = launch_fill_i32(c->stream, c->err_flag, 1, 0);
     if (e == hipSuccess) e = launch_fill_i32(c->stream, c->pend, c->n, 0);
+    if (e == hipSuccess) e = launch_fill_i32(c->stream, c->pev_cnt, 2 * kBatchMax, 0);
     snn_status st = check_hip(c, e, "workspace initialisation");
     if (st) return st;
     c->t = 0;
@@ -1439,9 +1443,9 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
     const bool pblocks = mode == SNN_DELIVER_LDS_SLICE && c->pb_max > 0 && c->t_used >= c->t_cap;
     if (pblocks && n_steps > 0) {
         const NeuronArgs a = neuron_args(c);
-        for (int32_t q = 0; q < n_steps;) {
+        for (int32_t q = 0, k = 0; q < n_steps; ++k) {
             const int32_t B = std::min<int32_t>(n_steps - q, c->pb_max);
-            const BlockArgs b = block_args(c, B);
+            const BlockArgs b = block_args(c, B, k);
             if ((st = check_hip(c, launch_block_plan(c->stream, b), "plastic block plan")))
                 return st;
             if ((st = check_hip(c, launch_block_run(c->stream, a, b), "plastic block run")))
@@ -1451,7 +1455,7 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
             c->t += B;
             q += B;
         }
-        if ((st = check_hip(c, launch_block_finish(c->stream, block_args(c, 1)),
+        if ((st = check_hip(c, launch_block_finish(c->stream, block_args(c, 1, 0)),
                             "plastic block lists")))
             return st;
         c->last_neuron_t = c->last_deliver_t = c->t - 1;

@@ -336,8 +336,8 @@ constexpr int64_t kBatchBytes = 256ll << 20;  // most workspace for a block's pa
 //   The plan (one thread per row) walks each row through the block's steps
 // as the neuron update would (transmitting: history bit D-1 of the step;
 // forced: idle for 64 hw steps), and writes each step's list of row updates
-// (PbEvent), ascending, by one decoupled look-back per step, and commits
-// t_last and x_pre after the block. A forced update that is its row's last
+// (PbEvent), each workgroup's share placed by one atomic add per list, and
+// commits t_last and x_pre after the block. A forced update that is its row's last
 // event of the block delivers nothing and no later event of the block reads
 // its weights: it goes to one more list, the deferred updates, which the run
 // computes after the block's last step from the targets' histories at the
@@ -385,11 +385,12 @@ struct BlockArgs {
     const uint64_t *hist;
     int32_t *t_last;
     float *xpre;
-    unsigned long long *status;  // [kBatchMax][status_stride] look-back words
-    int32_t status_stride;
+    unsigned long long *status;  // look-back words of the step-by-step kernels (the finish
+    int32_t status_stride;       // clears them)
     PbEvent *ev;                 // [steps + 1][n]: step k's rows at ev + k n, the deferred
                                  // forced updates at ev + steps n
-    int32_t *ev_cnt;             // [kBatchMax]: the lists' lengths
+    int32_t *ev_cnt;             // [kBatchMax]: the lists' lengths (0 when the plan starts)
+    int32_t *ev_cnt_next;        // [kBatchMax]: the other block's, cleared by the plan
     uint8_t *dcode;              // [n, padded to 16] run -> deferred: per target, the first
                                  // spike step of the block (bits 0-3), the latest spike before
                                  // it against a forced window (4-7)
