@@ -553,6 +553,195 @@ __global__ __launch_bounds__(kStepsBlock) void k_neuron_steps(NeuronArgs a, Batc
     }
 }
 
+// Steps t0 .. t0+B-1 of a plastic network of Bernoulli sources with D = 1
+// (see SourceArgs), one neuron per thread, kStepsBlock threads per
+// workgroup (a half wave per step's list scan). A row transmits at the step
+// its neuron fires; a plastic row is forced at a step where it neither
+// transmits nor was updated in the last 64 hw steps, as in k_neuron. The
+// walk through the steps records the spike and forced bits and the state of
+// each step; after the scans a second walk over the row's updates makes
+// their snapshots, each starting from the t_last and pre trace the one
+// before left (what the passes commit in between, step by step).
+template <int H>
+__global__ __launch_bounds__(kStepsBlock) void k_source_steps(NeuronArgs a, CompactArgs lst,
+                                                              SourceArgs b)
+{
+    constexpr int NWV = kStepsBlock / kWave;
+    static_assert(kStepsBlock / 32 >= kSrcMaxSteps, "a half wave per step's list scan");
+    __shared__ uint64_t s_m[kSrcMaxSteps][NWV];  // transmitted rows of step k, per wave
+    __shared__ uint64_t s_f[kSrcMaxSteps][NWV];  // forced rows
+    __shared__ int s_lb[2 * kBatchMax];
+    __shared__ unsigned long long s_st[4];
+    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const int n = a.n, npl = lst.n_plastic_rows;  // npl > 0
+    const int i = blockIdx.x * kStepsBlock + tid;
+    const bool live = i < n, prow = i < npl;
+    const int ic = live ? i : 0, ip = prow ? i : 0;
+    const int B = b.steps;  // 1 .. kSrcMaxSteps (checked by the launcher)
+    if (tid < 4) s_st[tid] = 0ull;
+    // the state and the row's values, then the clock: one round trip (every
+    // load unconditional, from a valid index)
+    NState st;
+    nstate_load<-1, H>(a, ic, st);
+    const int tl0 = a.t_last[ip];
+    const int64_t rs = lst.row_ptr[ic];
+    const int pend_k = lst.pend[ip];
+    const float xp0 = lst.xpre[ip];
+    const StepClock ck = load_clock(a.clk);
+    const int64_t t0 = ck.t;
+    const int64_t nh = (int64_t)n * H;
+    uint32_t fired = 0, forced = 0;
+    int tl = tl0;
+    for (int k = 0; k < B; ++k) {
+        const int64_t t = t0 + k;
+        const int s = live ? neuron_advance<-1, H>(a, ic, t, 0.f, 0.f, st) : 0;
+        const int f = live && prow && !s && t - (int64_t)tl >= 64 * H;
+        if (live && prow && (s || f) && t > (int64_t)tl) tl = (int)t;
+        fired |= (uint32_t)s << k;
+        forced |= (uint32_t)f << k;
+        const uint64_t m = ballot64(s), fm = ballot64(f);
+        const uint64_t rcm = ballot64(live && (st.h0 | st.h1) != 0ull);
+        if (lane == 0) {
+            s_m[k][wave] = m;
+            s_f[k][wave] = fm;
+        }
+        if (k < B - 1) {  // the step's versions (the last step's go to the state arrays)
+            if (live) {
+                uint64_t *hp = b.hist + k * nh + (int64_t)i * H;
+                hp[0] = st.h0;
+                if (H == 2) hp[1] = st.h1;
+                b.ypost[(int64_t)k * n + i] = st.y;
+                b.code[(int64_t)k * b.code_stride + i] = hist_code(st.h0, st.h1);
+            }
+            const int64_t word = (int64_t)blockIdx.x * NWV + wave;
+            if (lane == 0 && word * kWave < n) b.recent[(int64_t)k * lst.nw + word] = rcm;
+        } else {
+            const int64_t word = (int64_t)blockIdx.x * NWV + wave;
+            if (lane == 0 && word * kWave < n) {
+                a.mask[word] = m;
+                a.txmask[word] = m;  // D = 1: the spikes of the step transmit
+                a.recent[word] = rcm;
+            }
+        }
+    }
+    if (live) neuron_commit(a, i, st);
+    __syncthreads();  // every step's ballots, s_st
+    // the workgroup's transmitted and forced counts of step `tid`, published
+    // for the scans
+    int own_s = 0, own_f = 0;
+    if (tid < B) {
+        for (int w = 0; w < NWV; ++w) {
+            own_s += __popcll(s_m[tid][w]);
+            own_f += __popcll(s_f[tid][w]);
+        }
+        publish_status(b.status + (int64_t)tid * b.status_stride + blockIdx.x,
+                       status_word(own_s, own_f, t0 + tid,
+                                   blockIdx.x == 0 ? kStatusInc : kStatusAgg));
+    }
+    lookback32<kStepsBlock>(b.status, b.status_stride, B, (int)blockIdx.x, t0, s_lb, lst.err);
+    if (tid < B && blockIdx.x > 0)
+        publish_status(b.status + (int64_t)tid * b.status_stride + blockIdx.x,
+                       status_word(s_lb[2 * tid] + own_s, s_lb[2 * tid + 1] + own_f, t0 + tid,
+                                   kStatusInc));
+    // the row's updates in step order, each at its place in its step's list:
+    // the earlier workgroups, then the earlier waves, then the earlier lanes
+    const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+    int tlw = tl0;
+    float xp = xp0;
+    long long n_rows = 0, n_forced = 0, n_syn = 0, n_fsyn = 0;
+    for (uint32_t ev = fired | forced; ev; ev &= ev - 1u) {
+        const int k = __ffs((int)ev) - 1;
+        const int64_t t = t0 + k;
+        const int tx = (int)((fired >> k) & 1u);
+        const bool last = k == B - 1;
+        RowInfo ri = RowInfo{};
+        int ok = 0;
+        if (prow) {
+            ok = make_row_info_d(ri, i, t, tlw, rs, pend_k, xp, tx, H,
+                                 lst.dpow[row_age_index(t, tlw, H)], lst.err);
+            if (ok) {
+                tlw = (int)t;
+                xp = ri.xp_now;
+                n_rows += 1;
+                n_syn += ri.len;
+                if (!tx) {
+                    n_forced += 1;
+                    n_fsyn += ri.len;
+                }
+            }
+        }
+        if (tx) {
+            if (!ok) {  // nothing to bring up to date: the row is only delivered
+                ri = RowInfo{};
+                ri.k = i;
+                ri.rs = rs;
+            }
+            int pos = s_lb[2 * k] + __popcll(s_m[k][wave] & below);
+            for (int w = 0; w < wave; ++w) pos += __popcll(s_m[k][w]);
+            // (only a failed scan puts a position out of range)
+            if (pos < n) {
+                (last ? lst.ring : b.tx + (int64_t)k * n)[pos] = i;
+                (last ? lst.txinfo : b.txinfo + (int64_t)k * n)[pos] = ri;
+            } else {
+                atomicOr(lst.err, kErrRing);
+            }
+        } else {
+            int pos = s_lb[2 * k + 1] + __popcll(s_f[k][wave] & below);
+            for (int w = 0; w < wave; ++w) pos += __popcll(s_f[k][w]);
+            if (pos < npl) {
+                (last ? lst.row_list : b.rows + (int64_t)k * npl)[pos] = i;
+                (last ? lst.info : b.info + (int64_t)k * npl)[pos] = ri;
+            } else {
+                atomicOr(lst.err, kErrRing);
+            }
+        }
+    }
+    if (lst.info_stats) {
+        n_rows = wave_sum_i64(n_rows);
+        n_forced = wave_sum_i64(n_forced);
+        n_syn = wave_sum_i64(n_syn);
+        n_fsyn = wave_sum_i64(n_fsyn);
+        if (lane == 0) {
+            if (n_rows) atomicAdd(s_st + 0, (unsigned long long)n_rows);
+            if (n_forced) atomicAdd(s_st + 1, (unsigned long long)n_forced);
+            if (n_syn) atomicAdd(s_st + 2, (unsigned long long)n_syn);
+            if (n_fsyn) atomicAdd(s_st + 3, (unsigned long long)n_fsyn);
+        }
+        __syncthreads();  // s_st complete
+        if (tid < 4 && s_st[tid]) {
+            int64_t *sl = lst.info_stats + (int64_t)(blockIdx.x % b.info_slots) * kStFields;
+            const int f = tid == 0 ? kStRows : tid == 1 ? kStForced : tid == 2 ? kStSyn
+                                                                                : kStForcedSyn;
+            add_stat(sl + f, (long long)s_st[tid]);
+        }
+    }
+    // copies of the clock as the passes before the last expect it
+    if (blockIdx.x == 0 && tid < B - 1) {
+        StepClock c = ck;
+        c.t = t0 + tid + 1;
+        b.clk[tid] = c;
+    }
+    if (blockIdx.x == gridDim.x - 1) {
+        // every workgroup has read the clock: the scans saw all of them
+        if (tid < B) {
+            const int cs = s_lb[2 * tid] + own_s, cf = s_lb[2 * tid + 1] + own_f;
+            if (tid == B - 1) {
+                lst.ring_cnt[0] = cs;
+                *lst.tx_cnt = cs;
+                *lst.row_cnt = cf;
+            } else {
+                b.cnt[2 * tid] = cs;
+                b.cnt[2 * tid + 1] = cf;
+            }
+            add_stat(lst.gstats + kGSpikes, cs);
+        }
+        if (tid == 0) {
+            add_stat(lst.gstats + kGSteps, B);
+            a.clk->t = t0 + B;
+        }
+    }
+}
+
 // Positions of the delay-ring entries: grid (ceil(n / kBlock), d).
 __global__ __launch_bounds__(kBlock) void k_ring_positions(const int32_t *ring,
                                                            const int32_t *cnt, int32_t *pos,
@@ -702,6 +891,24 @@ hipError_t launch_neuron(hipStream_t s, const NeuronArgs &a, const CompactArgs &
                       dim3(kNeuronBlock), 0, s, ev, a, c);
     return hipGetLastError();
 }
+
+hipError_t launch_source_steps(hipStream_t s, const NeuronArgs &a, const CompactArgs &c,
+                               const SourceArgs &b)
+{
+    if (b.steps < 1 || b.steps > kSrcMaxSteps || a.model != 2 || c.delay != 1 ||
+        c.n_plastic_rows < 1 || c.n_plastic_rows > a.n || (a.hw != 1 && a.hw != 2) ||
+        b.info_slots < 1 || b.status_stride < source_steps_grid(a.n) || c.segb)
+        return hipErrorInvalidValue;
+    if (a.hw == 2)
+        hipLaunchKernelGGL(k_source_steps<2>, dim3(source_steps_grid(a.n)), dim3(kStepsBlock), 0,
+                           s, a, c, b);
+    else
+        hipLaunchKernelGGL(k_source_steps<1>, dim3(source_steps_grid(a.n)), dim3(kStepsBlock), 0,
+                           s, a, c, b);
+    return hipGetLastError();
+}
+
+int source_steps_grid(int32_t n) { return blocks_for(n, kStepsBlock); }
 
 int neuron_grid(int32_t n) { return blocks_for(n, n <= kNeuronSmallN ? kBlock : kNeuronBlock); }
 int neuron_steps_grid(int32_t n) { return blocks_for(n, kStepsBlock); }

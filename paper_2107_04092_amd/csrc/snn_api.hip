@@ -130,6 +130,16 @@ struct snn_ctx {
     uint8_t *pdcode = nullptr;
     uint64_t *phq = nullptr;
     BlockClock *bclk = nullptr;
+    // source blocks (SourceArgs: Bernoulli sources, D = 1, plastic): most
+    // steps per block (0: off) and the per-step versions of the arrays the
+    // synapse pass reads, for the steps before a block's last
+    int32_t sb_max = 0, sv_code_stride = 0;
+    uint64_t *sv_hist = nullptr, *sv_recent = nullptr;
+    float *sv_ypost = nullptr;
+    uint8_t *sv_code = nullptr;
+    int32_t *sv_tx = nullptr, *sv_rows = nullptr, *sv_cnt = nullptr;
+    RowInfo *sv_txinfo = nullptr, *sv_info = nullptr;
+    StepClock *sv_clk = nullptr;
 
     // graph
     uint8_t *g = nullptr;
@@ -443,6 +453,21 @@ void plan_workspace(snn_ctx *c, uint8_t *base)
     c->pdcode = p.take<uint8_t>(c->pb_max > 0 ? (n + 15) / 16 * 16 : 1);
     c->phq = p.take<uint64_t>(c->pb_max > 0 ? 2 * n * c->hw : 1);
     c->bclk = p.take<BlockClock>(1);
+    {
+        const int64_t v = c->sb_max > 1 ? c->sb_max - 1 : 0;  // versions
+        const int64_t npl = std::max<int32_t>(c->n_plastic_rows, 1);
+        c->sv_code_stride = (int32_t)((n + 16 + 15) / 16 * 16);
+        c->sv_hist = p.take<uint64_t>(v ? v * n * c->hw : 1);
+        c->sv_ypost = p.take<float>(v ? v * n : 1);
+        c->sv_code = p.take<uint8_t>(v ? v * c->sv_code_stride : 1);
+        c->sv_recent = p.take<uint64_t>(v ? v * c->nw : 1);
+        c->sv_tx = p.take<int32_t>(v ? v * n : 1);
+        c->sv_txinfo = p.take<RowInfo>(v ? v * n : 1);
+        c->sv_rows = p.take<int32_t>(v ? v * npl : 1);
+        c->sv_info = p.take<RowInfo>(v ? v * npl : 1);
+        c->sv_cnt = p.take<int32_t>(v ? 2 * v : 1);
+        c->sv_clk = p.take<StepClock>(v ? v : 1);
+    }
     c->ws_need = p.off;
 }
 
@@ -691,9 +716,8 @@ BlockArgs block_args(snn_ctx *c, int32_t steps, int32_t parity)
     return b;
 }
 
-snn_status launch_step_neurons(snn_ctx *c)
+CompactArgs compact_args(snn_ctx *c)
 {
-    NeuronArgs a = neuron_args(c);
     CompactArgs b{};
     b.ring = c->ring;
     b.ring_cnt = c->ring_cnt;
@@ -723,6 +747,13 @@ snn_status launch_step_neurons(snn_ctx *c)
     b.xparts = c->xparts;
     for (int x = 0; x <= kXcds; ++x) b.xcd_piv[x] = c->xcd_piv[x];
     for (int q = 0; q <= kMaxAge; ++q) b.dpow[q] = c->dpow[q];
+    return b;
+}
+
+snn_status launch_step_neurons(snn_ctx *c)
+{
+    NeuronArgs a = neuron_args(c);
+    CompactArgs b = compact_args(c);
     snn_status st =
         check_hip(c, launch_neuron(c->stream, a, b, part_events(c, 0)), "neuron kernel");
     if (st) return st;
@@ -914,13 +945,32 @@ DeliverArgs deliver_args(snn_ctx *c)
 }
 
 // Parts (2) and (3) of a step in one launch (k_synapse_pass): delivery on
-// its usual work items, the forced rows on the CU slots left over.
-snn_status launch_step_synapse_pass(snn_ctx *c, KernelEvents ev)
+// its usual work items, the forced rows on the CU slots left over. ver >= 0:
+// the step of a source block whose lists, histories, post traces, history
+// summaries, counts and clock are the block's version ver (SourceArgs).
+snn_status launch_step_synapse_pass(snn_ctx *c, KernelEvents ev, int ver = -1)
 {
     DeliverArgs d = deliver_args(c);
     const int nd = c->dlv_blocks;
     const int ns = std::max(8, c->fuse_slots - nd);
     StdpArgs a = stdp_args(c, false, (int64_t)ns * (kDlvBlock / kWave));
+    if (ver >= 0) {
+        const int64_t n = c->n, npl = c->n_plastic_rows;
+        d.ring = c->sv_tx + ver * n;
+        d.ring_cnt = d.tx_cnt = c->sv_cnt + 2 * ver;
+        d.clk = c->sv_clk + ver;
+        d.txinfo = c->sv_txinfo + ver * n;
+        d.hist = c->sv_hist + ver * n * c->hw;
+        d.ypost = c->sv_ypost + ver * n;
+        a.info = c->sv_info + ver * npl;
+        a.row_cnt = c->sv_cnt + 2 * ver + 1;
+        a.tx_cnt = c->sv_cnt + 2 * ver;
+        a.clk = c->sv_clk + ver;
+        a.hist = d.hist;
+        a.ypost = d.ypost;
+        if (a.code) a.code = c->sv_code + ver * (int64_t)c->sv_code_stride;
+        if (a.recent) a.recent = c->sv_recent + ver * (int64_t)c->nw;
+    }
     const size_t table = a.xcd      ? (a.code ? (size_t)c->xcd_table : 0)
                          : a.code   ? (((size_t)c->n + 15) / 16) * 16
                          : a.recent ? (size_t)c->nw * sizeof(uint64_t)
@@ -1115,6 +1165,15 @@ snn_status snn_create(const snn_config *cfg, void *hip_stream, snn_ctx **out)
         // the forced-row workgroups of the pass keep a statistics slot each
         if (c->fuse && c->syn_slots < c->fuse_slots) c->syn_slots = c->fuse_slots;
     }
+    // Source blocks (SourceArgs): plastic networks of Bernoulli sources with
+    // D = 1, lazy plasticity, whose step runs the fused synapse pass on whole
+    // forced rows; at most kSrcMaxSteps steps (or plastic_blocks) per block.
+    c->sb_max = 0;
+    if (c->n_plastic_rows > 0 && c->algo != 2 && c->delay == 1 &&
+        cfg->neuron_model == SNN_BERNOULLI_SOURCE && c->fuse && !c->xcd &&
+        cfg->plastic_blocks >= 0)
+        c->sb_max = cfg->plastic_blocks > 0 ? std::min<int32_t>(cfg->plastic_blocks, kSrcMaxSteps)
+                                            : kSrcMaxSteps;
     plan_workspace(c, nullptr);
     return SNN_OK;
 }
@@ -1437,6 +1496,48 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
         q += B;
     }
     if (blocks) return SNN_OK;
+    // a plastic network of Bernoulli sources with D = 1 runs in source
+    // blocks (see SourceArgs): one launch for the neuron updates and lists
+    // of up to sb_max steps, then the synapse pass of each step on its
+    // versions (the last step's are the state arrays). The scans' status
+    // words are cleared before and after, so that no word a different launch
+    // shape left can match a step tag.
+    const bool sblocks = mode == SNN_DELIVER_LDS_SLICE && c->sb_max > 0 && c->t_used >= c->t_cap;
+    if (sblocks && n_steps > 0) {
+        if ((st = check_hip(c, clear_status(c), "clear the list scans"))) return st;
+        NeuronArgs a = neuron_args(c);
+        CompactArgs l = compact_args(c);
+        for (int32_t q = 0; q < n_steps;) {
+            const int32_t B = std::min<int32_t>(n_steps - q, c->sb_max);
+            SourceArgs b{};
+            b.status = c->status;
+            b.status_stride = c->status_stride;
+            b.steps = B;
+            b.info_slots = c->info_blocks;
+            b.code_stride = c->sv_code_stride;
+            b.hist = c->sv_hist;
+            b.ypost = c->sv_ypost;
+            b.code = c->sv_code;
+            b.recent = c->sv_recent;
+            b.tx = c->sv_tx;
+            b.txinfo = c->sv_txinfo;
+            b.rows = c->sv_rows;
+            b.info = c->sv_info;
+            b.cnt = c->sv_cnt;
+            b.clk = c->sv_clk;
+            if ((st = check_hip(c, launch_source_steps(c->stream, a, l, b), "source block")))
+                return st;
+            c->last_neuron_t = c->t;  // the history summaries are current
+            for (int32_t k = 0; k < B; ++k) {
+                if ((st = launch_step_synapse_pass(c, {}, k < B - 1 ? k : -1))) return st;
+                c->t += 1;
+            }
+            q += B;
+        }
+        if ((st = check_hip(c, clear_status(c), "clear the list scans"))) return st;
+        c->last_neuron_t = c->last_deliver_t = c->t - 1;
+        return SNN_OK;
+    }
     // a plastic network with D >= 2 runs in blocks of up to D-1 steps (see
     // BlockArgs): the plan, then the run of the block, and after the last
     // block the per-step lists
@@ -1704,7 +1805,7 @@ snn_status snn_get_graph(const snn_ctx *c, snn_graph_view *out)
     out->plastic_end = c->pend;
     out->col16 = c->col16;
     out->stdp_ranges = c->xcd ? c->xparts : 0;
-    out->block_steps = c->pb_max;
+    out->block_steps = c->pb_max > 0 ? c->pb_max : c->sb_max;
     out->block_width = c->pb_width;
     out->block_pivots = c->gpiv;
     return SNN_OK;

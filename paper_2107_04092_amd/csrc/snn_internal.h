@@ -426,6 +426,45 @@ struct BlockArgs {
     int32_t status_words;
     float dpow[kMaxAge + 1];
 };
+// Blocks of steps of a plastic network of Bernoulli sources with D = 1
+// (k_source_steps, then one synapse pass per step). A source fires on a
+// counter-based draw that no input changes, so one launch runs the neuron
+// update of B steps: each thread walks its neuron through them (spike,
+// history, post trace) and its row through the updates of each step
+// (transmitting, or forced by the history window), with t_last and x_pre
+// carried in registers from one update to the next exactly as the synapse
+// passes will commit them. For every step it writes what that step's pass
+// reads: the histories, post traces and history summaries after the step,
+// its transmitted and forced lists, ascending (one decoupled look-back per
+// step, the B scans together), their snapshots, their counts and a copy of
+// the clock. The last step of the block writes to the state arrays
+// themselves (ring slot, lists, counts, masks, clock), so after the block
+// the state is that of the step-by-step path; the steps before it write to
+// versions of those arrays in the workspace (step k at k times the stride
+// of each). The passes then run one per step, in order.
+struct SourceArgs {
+    unsigned long long *status;  // [kBatchMax][status_stride]: step k's scan in row k
+    int32_t status_stride;
+    int32_t steps;               // B: 1 .. kSrcMaxSteps
+    int32_t info_slots;          // statistics slots of CompactArgs::info_stats
+    int32_t code_stride;         // bytes per version of `code`
+    uint64_t *hist;              // versions: [B-1][n][hw]
+    float *ypost;                // [B-1][n]
+    uint8_t *code;               // [B-1][code_stride]
+    uint64_t *recent;            // [B-1][nw]
+    int32_t *tx;                 // [B-1][n]: the transmitted (= spike) list of the step
+    RowInfo *txinfo;             // [B-1][n]
+    int32_t *rows;               // [B-1][n_plastic_rows]: the forced rows
+    RowInfo *info;               // [B-1][n_plastic_rows]
+    int32_t *cnt;                // [B-1][2]: transmitted and forced counts
+    StepClock *clk;              // [B-1]: t = t0 + k + 1, as after the step's neuron update
+};
+constexpr int kSrcMaxSteps = kBatchMax;  // steps per source block (one scan per half wave)
+hipError_t launch_source_steps(hipStream_t s, const NeuronArgs &a, const CompactArgs &c,
+                               const SourceArgs &b);
+// workgroups of k_source_steps
+int source_steps_grid(int32_t n);
+
 hipError_t launch_block_plan(hipStream_t s, const BlockArgs &b);
 hipError_t launch_block_run(hipStream_t s, const NeuronArgs &a, const BlockArgs &b);
 hipError_t launch_block_deferred(hipStream_t s, const BlockArgs &b);

@@ -195,3 +195,36 @@ def rate_hz(spikes, n, steps, dt_ms=0.1):
 
 def poisson_sigma(count):
     return math.sqrt(max(count, 1))
+
+
+KEYS = ("v", "refractory", "i_exc", "i_inh", "hist", "trace_post", "t_last", "trace_pre",
+        "input_exc", "input_inh", "spike_mask", "ring_counts", "spike_count", "tx_count",
+        "stdp_row_count")
+STAT_KEYS = ("steps", "spikes", "delivered_events", "stdp_rows", "stdp_forced_rows",
+             "stdp_synapse_updates", "stdp_weights_written", "stdp_forced_synapse_updates",
+             "stdp_forced_weights_written", "device_errors")
+
+
+def same_state(a, b, what, weights=True):
+    sa, sb = a.state(), b.state()
+    assert sa["t"] == sb["t"], (what, "t", sa["t"], sb["t"])
+    for k in KEYS:
+        ga, gb = to_np(sa[k]), to_np(sb[k])
+        assert np.array_equal(ga.view(np.uint8), gb.view(np.uint8)), (what, k)
+    for lst, cnt in (("spike_list", "spike_count"), ("tx_list", "tx_count"),
+                     ("stdp_rows", "stdp_row_count")):
+        c = int(to_np(sa[cnt])[0])
+        assert np.array_equal(to_np(sa[lst])[:c], to_np(sb[lst])[:c]), (what, lst)
+    d = a.cfg.delay_steps
+    ra = to_np(sa["ring_lists"]).reshape(d, -1)
+    rb = to_np(sb["ring_lists"]).reshape(d, -1)
+    for q, c in enumerate(to_np(sa["ring_counts"])):
+        assert np.array_equal(ra[q, :c], rb[q, :c]), (what, "ring slot", q)
+        assert np.all(np.diff(ra[q, :c]) > 0), (what, "ring slot ascending", q)
+    if weights:
+        wa, wb = to_np(a.graph()["w"]), to_np(b.graph()["w"])
+        assert np.array_equal(wa.view(np.uint32), wb.view(np.uint32)), (what, "weights")
+    ta, tb = a.stats(), b.stats()
+    for k in STAT_KEYS:
+        assert ta[k] == tb[k], (what, k, ta[k], tb[k])
+    assert ta["device_errors"] == 0, what

@@ -16,7 +16,7 @@ import workloads as wl
 from paper_2107_04092_amd import snn
 
 from gpu_common import (gpu_net, oracle_net, to_np, hist_np, assert_close, log, rate_hz,
-                        teacher_forced_run, compare_all_plastic_weights)
+                        teacher_forced_run, compare_all_plastic_weights, same_state)
 
 pytestmark = pytest.mark.gpu
 
@@ -74,6 +74,26 @@ def test_stress_full_size_sampled_parity(hbits):
     net.step(1, snn.SNN_DELIVER_GLOBAL_ATOMIC)
     a_want = o.bernoulli_input(F, w_init, T)
     assert_close(to_np(net.state()["input_exc"]), a_want, "full-size global-atomic input")
+
+
+def test_stress_full_size_source_blocks_equal_stepwise():
+    """The full-size stress network in the benchmark's launch configuration
+    (source blocks of 16 steps: one neuron launch, then a fused synapse pass
+    per step) against the same network stepped one neuron launch and one
+    pass at a time, over 300 steps in uneven calls: every state array, every
+    list and all 250M weights bit for bit."""
+    p = wl.preset("stress")
+    log("full-size stress: source blocks vs stepwise")
+    a = gpu_net(p)
+    b = gpu_net(p, plastic_blocks=-1)
+    assert a.graph()["block_steps"] == 16 and b.graph()["block_steps"] == 0
+    done = 0
+    for n_steps in (150, 1, 149):
+        a.step(n_steps, snn.SNN_DELIVER_LDS_SLICE)
+        b.step(n_steps, snn.SNN_DELIVER_LDS_SLICE)
+        done += n_steps
+        same_state(a, b, "after %d steps" % done)
+        log("  %d steps equal" % done)
 
 
 def test_brunel_full_size_delay_block():

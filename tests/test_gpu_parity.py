@@ -43,13 +43,16 @@ MODES = [((LDS, 0, 1), "lds-rowstdp-codes"), ((LDS, 0, 2), "lds-rowstdp-bitmap")
 
 def _parity_params():
     """Every case in every mode; plastic networks with D >= 2 in the slice
-    mode run snn_step's steps as blocks (of one step here), so they run once
-    more with the blocks switched off (three parts per step)."""
+    mode run snn_step's steps as blocks (of one step here), and so do
+    plastic networks of Bernoulli sources with D = 1 whose step fuses the
+    synapse pass (row-wise layout), so they run once more with the blocks
+    switched off (parts one by one)."""
     out = []
     for case in CASES:
         p = wl.preset(case[0], **case[1])
         for (mode, layout, filt), mname in MODES:
-            both = p.plastic != PLASTIC_NONE and p.delay >= 2 and mode == LDS
+            both = p.plastic != PLASTIC_NONE and mode == LDS and (
+                p.delay >= 2 or (p.model == BERNOULLI_SOURCE and layout == 0))
             for blocks in ([0, -1] if both else [0]):
                 cid = "%s-%s-%s%s" % (case[0], case[1].get("n", ""), mname,
                                       "-stepwise" if blocks == -1 else "")
