@@ -416,9 +416,16 @@ def main():
         b_dlv = delivery_bytes(st2, p.n, n_slices, chunks, nacc, args.steps,
                                args.mode, tb, hbits // 64) / args.steps
         t_neu, t_stdp, t_dlv = kt["neuron"], kt["plasticity"], kt["delivery"]
+        # a plastic network of Bernoulli sources with D = 1 runs its neuron
+        # updates in source blocks: one launch per block of steps
+        nsteps = (net.graph()["block_steps"] or 1) if (
+            p.model == snn.SNN_BERNOULLI_SOURCE and p.delay == 1 and p.plastic != 0
+            and args.mode == "lds") else 1
         kernels = {
             "steps_timed": nrec,
             "neuron_us": round(t_neu * 1e3, 3),
+            "neuron_steps_per_launch": nsteps,
+            "neuron_us_per_step": round(t_neu * 1e3 / nsteps, 3),
             "plasticity_us": round(t_stdp * 1e3, 3),
             "delivery_us": round(t_dlv * 1e3, 3),
             "fused_synapse_pass": bool(p.plastic != 0 and t_stdp == 0 and t_dlv > 0),

@@ -893,18 +893,18 @@ hipError_t launch_neuron(hipStream_t s, const NeuronArgs &a, const CompactArgs &
 }
 
 hipError_t launch_source_steps(hipStream_t s, const NeuronArgs &a, const CompactArgs &c,
-                               const SourceArgs &b)
+                               const SourceArgs &b, KernelEvents ev)
 {
     if (b.steps < 1 || b.steps > kSrcMaxSteps || a.model != 2 || c.delay != 1 ||
         c.n_plastic_rows < 1 || c.n_plastic_rows > a.n || (a.hw != 1 && a.hw != 2) ||
         b.info_slots < 1 || b.status_stride < source_steps_grid(a.n) || c.segb)
         return hipErrorInvalidValue;
     if (a.hw == 2)
-        hipLaunchKernelGGL(k_source_steps<2>, dim3(source_steps_grid(a.n)), dim3(kStepsBlock), 0,
-                           s, a, c, b);
+        launch_kernel(k_source_steps<2>, dim3(source_steps_grid(a.n)), dim3(kStepsBlock), 0, s,
+                      ev, a, c, b);
     else
-        hipLaunchKernelGGL(k_source_steps<1>, dim3(source_steps_grid(a.n)), dim3(kStepsBlock), 0,
-                           s, a, c, b);
+        launch_kernel(k_source_steps<1>, dim3(source_steps_grid(a.n)), dim3(kStepsBlock), 0, s,
+                      ev, a, c, b);
     return hipGetLastError();
 }
 

@@ -1501,8 +1501,10 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
     // of up to sb_max steps, then the synapse pass of each step on its
     // versions (the last step's are the state arrays). The scans' status
     // words are cleared before and after, so that no word a different launch
-    // shape left can match a step tag.
-    const bool sblocks = mode == SNN_DELIVER_LDS_SLICE && c->sb_max > 0 && c->t_used >= c->t_cap;
+    // shape left can match a step tag. With kernel timing on, the block's
+    // launch is timed as the neuron part of its first step and each pass as
+    // the delivery part of its step.
+    const bool sblocks = mode == SNN_DELIVER_LDS_SLICE && c->sb_max > 0;
     if (sblocks && n_steps > 0) {
         if ((st = check_hip(c, clear_status(c), "clear the list scans"))) return st;
         NeuronArgs a = neuron_args(c);
@@ -1525,11 +1527,14 @@ snn_status snn_step(snn_ctx *c, int32_t n_steps, int32_t mode)
             b.info = c->sv_info;
             b.cnt = c->sv_cnt;
             b.clk = c->sv_clk;
-            if ((st = check_hip(c, launch_source_steps(c->stream, a, l, b), "source block")))
+            if ((st = check_hip(c, launch_source_steps(c->stream, a, l, b, part_events(c, 0)),
+                                "source block")))
                 return st;
             c->last_neuron_t = c->t;  // the history summaries are current
             for (int32_t k = 0; k < B; ++k) {
-                if ((st = launch_step_synapse_pass(c, {}, k < B - 1 ? k : -1))) return st;
+                if ((st = launch_step_synapse_pass(c, part_events(c, 2), k < B - 1 ? k : -1)))
+                    return st;
+                if (c->t_used < c->t_cap) c->t_used += 1;
                 c->t += 1;
             }
             q += B;

@@ -460,10 +460,6 @@ struct SourceArgs {
     StepClock *clk;              // [B-1]: t = t0 + k + 1, as after the step's neuron update
 };
 constexpr int kSrcMaxSteps = kBatchMax;  // steps per source block (one scan per half wave)
-hipError_t launch_source_steps(hipStream_t s, const NeuronArgs &a, const CompactArgs &c,
-                               const SourceArgs &b);
-// workgroups of k_source_steps
-int source_steps_grid(int32_t n);
 
 hipError_t launch_block_plan(hipStream_t s, const BlockArgs &b);
 hipError_t launch_block_run(hipStream_t s, const NeuronArgs &a, const BlockArgs &b);
@@ -477,6 +473,10 @@ struct KernelEvents {
 };
 // timed parts of a step: neuron update with its lists, plasticity, delivery
 constexpr int kTimedParts = 3;
+// k_source_steps (see SourceArgs) and its workgroups for n neurons
+hipError_t launch_source_steps(hipStream_t s, const NeuronArgs &a, const CompactArgs &c,
+                               const SourceArgs &b, KernelEvents ev = {});
+int source_steps_grid(int32_t n);
 
 // ---- launchers (k_*.hip); all enqueue on `s` and return the launch
 // status of the last kernel they started.
