@@ -151,7 +151,7 @@ def write_traffic(fetch_db, write_db, workload_key, copy_mib):
     path = os.path.join(ROOT, "profiles", "traffic.json")
     d = json.load(open(path)) if os.path.exists(path) else {}
     out = {}
-    for k in ("k_neuron", "k_synapse_pass", "k_deliver_lds", "k_stdp_rows"):
+    for k in ("k_neuron", "k_source_steps", "k_synapse_pass", "k_deliver_lds", "k_stdp_rows"):
         f, w = vals[k]["FETCH_SIZE"], vals[k]["WRITE_SIZE"]
         if not f or not w:
             continue

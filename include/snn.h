@@ -169,12 +169,16 @@ typedef struct snn_config {
                              either way */
     int32_t plastic_blocks; /* plastic networks (lazy plasticity, slice
                              delivery) with D >= 2 and n <= 65536: snn_step
-                             runs blocks of up to min(D-1, 15) steps, two
-                             launches per block, each workgroup owning a
-                             group of targets through the whole block (see
-                             snn_step). 0 = on; k > 0 = on, at most k steps
-                             per block; -1 = off (three parts per step).
-                             Same results either way */
+                             runs blocks of up to min(D-1, 15) steps, each
+                             workgroup owning a group of targets through
+                             the whole block; plastic networks of
+                             Bernoulli sources with D = 1 whose step fuses
+                             parts (2) and (3): snn_step runs the neuron
+                             updates of up to 16 steps in one launch, then
+                             each step's synapse pass (see snn_step). 0 =
+                             on; k > 0 = on, at most k steps per block; -1
+                             = off (the parts step by step). Same results
+                             either way */
     int32_t plastic_block_width; /* targets per group of those blocks: 64, 128
                              or 256, dividing slice_width; 0 = automatic */
     int32_t neuron_model; /* enum snn_neuron_model */
@@ -247,8 +251,9 @@ typedef struct snn_graph_view {
     int32_t stdp_ranges;   /* target ranges the forced rows are split into
                               (stdp_xcd; 0 = whole rows), fixed when the
                               graph is bound */
-    int32_t block_steps;   /* most steps per plastic block of snn_step
-                              (plastic_blocks; 0 = steps run one by one) */
+    int32_t block_steps;   /* most steps per plastic block or source block
+                              of snn_step (plastic_blocks; 0 = steps run one
+                              by one) */
     int32_t block_width;   /* targets per group of those blocks (0 = none) */
     int32_t *block_pivots; /* n x (n / block_width rounded up, + 1),
                               row-relative like pivots, at the group
@@ -385,7 +390,15 @@ snn_status snn_advance(snn_ctx *ctx);
  * onto them; a forced update that is its row's last of the block delivers
  * nothing and is computed after the block's last step, from the targets'
  * histories at its step); a last launch per call rebuilds the per-step
- * lists. Other
+ * lists. Plastic networks of Bernoulli sources with D = 1 (lazy plasticity,
+ * snn_config.plastic_blocks, the fused pass below on whole forced rows) run
+ * the neuron part of up to 16 steps in one launch: a source fires on a
+ * counter-based draw that no input changes, so the spikes, histories and
+ * the rows each step brings up to date (with the t_last and pre trace each
+ * update leaves for the next) are known before any of those steps' synapse
+ * passes; the launch writes, for each step, the lists, snapshots and
+ * histories its pass reads, and the passes then run one per step, in order.
+ * Other
  * plastic networks run parts (2) and (3) in one launch where its LDS
  * leaves the forced rows at least half a workgroup slot per CU beside the
  * delivery work items: the forced rows and the transmitting rows of a step
