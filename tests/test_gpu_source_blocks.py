@@ -20,6 +20,11 @@ Checked here:
     exc->exc plasticity (rows without plasticity transmit only), 16- and
     32-bit targets, one to four chunks, ragged sizes, block lengths capped,
     heavy activity;
+  - free runs against the oracle (both sides draw the same spikes): after
+    calls of 1 to 132 steps (blocks cut at every call's end), spikes,
+    lists, histories and the last step's delivered input, and the weights
+    of the rows the last step made current; every plastic weight after a
+    flush;
   - sequences that mix blocks with the separate part calls;
   - captured blocks replayed against eager steps.
 Teacher-forced oracle parity of the same path (blocks of one step) runs in
@@ -34,7 +39,8 @@ import workloads as wl
 from workloads.presets import PLASTIC_EXC_EXC
 from paper_2107_04092_amd import snn
 
-from gpu_common import gpu_net, to_np, log, same_state
+from gpu_common import (gpu_net, oracle_net, to_np, log, same_state, compare_step, compare_rows,
+                        compare_all_plastic_weights)
 
 pytestmark = pytest.mark.gpu
 LDS = snn.SNN_DELIVER_LDS_SLICE
@@ -124,3 +130,32 @@ def test_captured_source_blocks_replay_equal_eager_steps():
             same_state(a, c, "replay %d" % k)
     finally:
         snn.snn_graph_destroy(g)
+
+
+@pytest.mark.parametrize("hbits", [64, 128], ids=["h64", "h128"])
+@pytest.mark.parametrize("kw", [dict(n=3000, p_or_fanout=150, p_fire=0.03),
+                                # several updates of a row in one block: rows
+                                # that transmit twice, forced rows that
+                                # transmit later in the block
+                                dict(n=2000, p_or_fanout=200, p_fire=0.1)],
+                         ids=["p0.03", "p0.1"])
+def test_source_blocks_free_run_matches_oracle(kw, hbits):
+    p = wl.preset("stress", **kw)
+    log("source blocks free run %s history=%d" % (kw, hbits))
+    net = gpu_net(p, 640, 2, history_bits=hbits)
+    assert net.graph()["block_steps"] == 16
+    o = oracle_net(p)
+    cache = {}
+    t = n_w = 0
+    for chunk in (16, 37, 1, 64, 50, 132):
+        net.step(chunk, LDS)
+        o.step(chunk)
+        t += chunk
+        rows = compare_step(net, o, "source blocks", t)
+        n_w += compare_rows(net, o, rows, "rows made current at t=%d" % t, cache)
+    assert n_w > 0
+    net.flush_plasticity()
+    compare_all_plastic_weights(net, o)
+    st = net.stats()
+    assert st["spikes"] == o.spikes_total > 0
+    assert st["stdp_forced_rows"] > 0 and st["device_errors"] == 0
