@@ -300,7 +300,10 @@ void snn_destroy(snn_ctx *ctx);
 const char *snn_last_error(const snn_ctx *ctx);
 
 /* Bytes of device workspace for neuron state, spike lists, the delay ring,
- * row pointers and statistics. Depends only on the configuration. */
+ * row pointers and statistics, and the per-step lists, snapshots and
+ * histories of the blocks snn_step runs (plastic_blocks; for source blocks
+ * about 93 bytes per neuron and step of a block besides its last: 350 MB
+ * for 250,000 neurons). Depends only on the configuration. */
 snn_status snn_workspace_size(const snn_ctx *ctx, size_t *bytes);
 
 /* Binds a device buffer of at least snn_workspace_size bytes (256-byte
