@@ -18,7 +18,8 @@ Checked here:
     all weights and all statistics; 64- and 128-step histories, history
     codes and the recency bitmap, lazy and lazy + event-driven plasticity,
     exc->exc plasticity (rows without plasticity transmit only), 16- and
-    32-bit targets, one to four chunks, ragged sizes, block lengths capped,
+    32-bit targets, one to four chunks, ragged sizes, networks of one
+    workgroup and of one wave, block lengths capped (down to one step),
     heavy activity;
   - free runs against the oracle (both sides draw the same spikes): after
     calls of 1 to 132 steps (blocks cut at every call's end), spikes,
@@ -58,6 +59,10 @@ CASES = [
      dict(), 250),
     # heavy activity: about 1,200 spikes and forced rows per step
     (dict(n=6000, p_or_fanout=1000, p_fire=0.2), 1024, 2, dict(history_bits=128), 60),
+    # one workgroup (one wave, and a ragged wave); blocks of one step
+    (dict(n=64, p_or_fanout=20, p_fire=0.05), 64, 1, dict(), 200),
+    (dict(n=300, p_or_fanout=30, p_fire=0.05), 128, 2, dict(history_bits=128), 200),
+    (dict(n=2000, p_or_fanout=100, p_fire=0.05), 512, 2, dict(plastic_blocks=1), 150),
 ]
 
 SHORT = dict(plastic_blocks="B", history_bits="h", compressed_targets="ct",

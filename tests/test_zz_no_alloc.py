@@ -45,7 +45,10 @@ def _same(a, b, d, what):
      ("stress", dict(n=3000, p_or_fanout=60, p_fire=0.03, delay=3), 512, 1, 50)],
     [("brunel", dict(n=6000, n_exc=4800), 1024, 2, 45),
      ("tiny", dict(), 256, 1, 30)],
-], ids=["plastic", "delay-blocks"])
+    # Bernoulli sources with D = 1: source blocks (16 status rows per block)
+    [("stress", dict(n=6000, p_or_fanout=120, p_fire=0.03), 1024, 2, 77),
+     ("stress", dict(n=3000, p_or_fanout=60, p_fire=0.03), 512, 1, 50)],
+], ids=["plastic", "delay-blocks", "source-blocks"])
 def test_static_step_equals_step(case):
     for name, kw, width, chunks, steps in case:
         p = wl.preset(name, **kw)
